@@ -1,0 +1,453 @@
+"""Plain float64 CPU oracle of NAMOH routed mixture-of-head attention.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring): slow, obviously
+correct, shares no code with the GPU library.
+
+Paper passages followed (NAMOH, "Native Sparse Attention from
+Mixture-of-Head"):
+
+* Sec. 3.1, Eq. (namoh-gates): TopK head selection, mask m, gates g.
+* Sec. 3.1, the paragraph on sparse projection: ordered index sets I_i and
+  lengths n_i; routing before projection.
+* Sec. 3.1, Eq. (namoh-attention): causal scaled dot-product attention of a
+  routed query over keys/values of earlier-or-equal tokens routed to the same
+  head; output o_t = sum over selected heads of g_{t,i} h_{t,i} W_O^(i).
+* Sec. 3.2, Eq. (namoh-head-rope): head-relative rank rho_i(t) = (number of
+  tokens s <= t routed to head i) - 1, RoPE at that rank; global RoPE
+  replaces rho_i(t) by t.
+* Sec. 3.2, "Efficient execution": each (batch, head) subsequence is an
+  independent packed sequence; decoding touches only the selected heads.
+* App. D.3 (NAMOH complexity), Eqs. (app-assignment-count),
+  (app-routed-kv), (app-routed-interactions): sum_i n_i = TK, M_KV = TK,
+  A_KV = sum over the next token's heads of n_i, C_attn = 1/2 sum n_i(n_i+1).
+
+Readings where the paper is silent (each also listed in the design notes):
+
+* R1 selection ranks the raw float32 router logits (softmax is monotone, so
+  the set equals TopK of the affinities); equal logits go to the lower head
+  index; -0.0 equals +0.0.  ``topk_idx[t, :]`` lists the heads in that order.
+* R2 gates: ``GATE_SOFTMAX_SELECTED`` (softmax over the K selected logits,
+  the workloads' wording) or ``GATE_SOFTMAX_ALL`` (g = softmax over all H
+  logits, not renormalised: Eq. namoh-gates as printed).
+* R3 W_O^(i) is the identity, so o_t lives in the head width d.
+* R4 RoPE uses the rotate-half pairing (element j with j + d/2),
+  theta_j = base^(-2j/d), x'_j = x_j cos - x_{j+d/2} sin,
+  x'_{j+d/2} = x_{j+d/2} cos + x_j sin.  V is not rotated.
+* R5 softmax scale 1/sqrt(d) unless given.
+* R6 decode caches hold keys after rotation, in rank order; the new token
+  takes rank n (its head's current length) and attends to itself.
+* R7 sequences of a batch are independent (ranks restart per sequence).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+__all__ = [
+    "GATE_SOFTMAX_SELECTED", "GATE_SOFTMAX_ALL",
+    "ROPE_HEAD_RELATIVE", "ROPE_GLOBAL", "ROPE_NONE",
+    "select_heads", "route_gates", "membership", "head_ranks", "permutation",
+    "rope_rotate", "visibility_mask", "attention_definition",
+    "attention_gathered", "combine_packed", "combine_dense", "prefill",
+    "prefill_rows", "decode_step", "brute_force_layer", "interaction_count",
+    "shared_head_counts",
+]
+
+GATE_SOFTMAX_SELECTED = 0
+GATE_SOFTMAX_ALL = 1
+ROPE_HEAD_RELATIVE = 0
+ROPE_GLOBAL = 1
+ROPE_NONE = 2
+
+
+# ----------------------------------------------------------------------------
+# Routing: Sec. 3.1 Eq. (namoh-gates)
+
+def select_heads(logits: np.ndarray, K: int) -> np.ndarray:
+    """S_K(t): the K highest-scoring heads of every token.
+
+    ``logits`` [..., H] (float32 values, compared exactly in float64).  Heads
+    are ordered by logit descending, then head index ascending (reading R1);
+    the first K are returned as int32 [..., K] in that order.
+    """
+    l = np.asarray(logits, dtype=np.float64)
+    if np.isnan(l).any():
+        raise ValueError("router logits must not be NaN")
+    H = l.shape[-1]
+    if not 1 <= K <= H:
+        raise ValueError("need 1 <= K <= H")
+    # np.lexsort: last key is primary.  Primary: -logit ascending; secondary:
+    # head index ascending.  Float comparison makes -0.0 == +0.0.
+    idx = np.broadcast_to(np.arange(H), l.shape)
+    order = np.lexsort((idx, -l), axis=-1)
+    return order[..., :K].astype(np.int32)
+
+
+def route_gates(logits: np.ndarray, topk_idx: np.ndarray, mode: int) -> np.ndarray:
+    """Gates g_{t,i} of the selected heads, float64 [..., K] (reading R2)."""
+    l = np.asarray(logits, dtype=np.float64)
+    if mode == GATE_SOFTMAX_SELECTED:
+        sel = np.take_along_axis(l, topk_idx.astype(np.int64), axis=-1)
+        e = np.exp(sel - sel.max(axis=-1, keepdims=True))
+        return e / e.sum(axis=-1, keepdims=True)
+    if mode == GATE_SOFTMAX_ALL:
+        e = np.exp(l - l.max(axis=-1, keepdims=True))
+        a = e / e.sum(axis=-1, keepdims=True)          # affinities a_t
+        return np.take_along_axis(a, topk_idx.astype(np.int64), axis=-1)  # g = m * a
+    raise ValueError("unknown gate mode")
+
+
+def membership(topk_idx: np.ndarray, H: int) -> np.ndarray:
+    """m_{t,i} = 1{i in S_K(t)}: bool [B, T, H]."""
+    B, T, K = topk_idx.shape
+    m = np.zeros((B, T, H), dtype=bool)
+    for k in range(K):
+        np.put_along_axis(m, topk_idx[..., k:k + 1].astype(np.int64), True, axis=-1)
+    return m
+
+
+def head_ranks(m: np.ndarray) -> np.ndarray:
+    """rho_i(t) = sum_{s<=t} m_{s,i} - 1 (Eq. namoh-head-rope), int64 [B,T,H].
+
+    Meaningful only where m is set."""
+    return np.cumsum(m.astype(np.int64), axis=1) - 1
+
+
+def permutation(topk_idx: np.ndarray, H: int):
+    """Packed varlen layout of the ordered index sets I_i (Sec. 3.1, 3.2).
+
+    Returns ``head_len`` int32 [B,H] (n_i per sequence), ``seg_offsets``
+    int32 [B*H+1] (segment b*H+h starts there; exclusive running sum of the
+    lengths in segment order), ``perm_token`` int32 [B*T*K] (packed position
+    -> token t, tokens ascending inside a segment) and ``slot_pos`` int32
+    [B,T,K] (packed position of the pair (t, topk_idx[b,t,k])).
+    """
+    B, T, K = topk_idx.shape
+    m = membership(topk_idx, H)
+    n = m.sum(axis=1)                                     # [B, H]
+    flat = n.reshape(-1)
+    seg_offsets = np.concatenate([[0], np.cumsum(flat)]).astype(np.int64)
+    perm = np.empty(int(seg_offsets[-1]), dtype=np.int64)
+    for b in range(B):
+        for h in range(H):
+            s = b * H + h
+            perm[seg_offsets[s]:seg_offsets[s + 1]] = np.nonzero(m[b, :, h])[0]
+    rho = head_ranks(m)
+    slot = np.empty((B, T, K), dtype=np.int64)
+    for b in range(B):
+        for k in range(K):
+            hk = topk_idx[b, :, k].astype(np.int64)
+            slot[b, :, k] = seg_offsets[b * H + hk] + rho[b, np.arange(T), hk]
+    return (n.astype(np.int32), seg_offsets.astype(np.int32),
+            perm.astype(np.int32), slot.astype(np.int32))
+
+
+# ----------------------------------------------------------------------------
+# Positional encoding: Sec. 3.2 Eq. (namoh-head-rope), reading R4
+
+def rope_rotate(x: np.ndarray, positions: np.ndarray, base: float) -> np.ndarray:
+    """x R(p) for rows x [..., n, d] at positions p [..., n] (float64)."""
+    x = np.asarray(x, dtype=np.float64)
+    d = x.shape[-1]
+    half = d // 2
+    j = np.arange(half, dtype=np.float64)
+    theta = np.power(float(base), -2.0 * j / d)
+    ang = np.asarray(positions, dtype=np.float64)[..., None] * theta
+    c, s = np.cos(ang), np.sin(ang)
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def _positions(rank: np.ndarray, t: np.ndarray, rope_mode: int):
+    if rope_mode == ROPE_HEAD_RELATIVE:
+        return rank
+    if rope_mode == ROPE_GLOBAL:
+        return t
+    return None
+
+
+def _rotate(x, pos, base):
+    return x if pos is None else rope_rotate(x, pos, base)
+
+
+# ----------------------------------------------------------------------------
+# Attention, definition form (O1): explicit visibility mask
+
+def visibility_mask(m_bh: np.ndarray, rows: np.ndarray) -> np.ndarray:
+    """Vis_i[t, s] = m_{t,i} and m_{s,i} and s <= t over global indices
+    (Eq. namoh-attention), for the query tokens ``rows``: bool [len(rows), T]."""
+    T = m_bh.shape[0]
+    s = np.arange(T)
+    return m_bh[rows][:, None] & m_bh[None, :] & (s[None, :] <= rows[:, None])
+
+
+def attention_definition(q, k, v, topk_idx, H, rope_base, rope_mode=ROPE_HEAD_RELATIVE,
+                         scale=None, block=512):
+    """h_{t,i} for every routed pair from the definition, float64 [B,H,T,d]
+    (zero where m_{t,i} = 0).  q, k, v: float64 [B,H,T,d]."""
+    B, _, T, d = q.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    m = membership(topk_idx, H)
+    rho = head_ranks(m)
+    out = np.zeros((B, H, T, d))
+    t_all = np.arange(T)
+    for b in range(B):
+        for h in range(H):
+            mb = m[b, :, h]
+            tok = np.nonzero(mb)[0]
+            if tok.size == 0:
+                continue
+            pos = _positions(rho[b, :, h], t_all, rope_mode)
+            # rotate every token's key at its own rank; non-routed keys are
+            # never visible, so their (meaningless) rotation is never used.
+            kt = _rotate(k[b, h], pos, rope_base)
+            qt = _rotate(q[b, h], pos, rope_base)
+            for i0 in range(0, tok.size, block):
+                rows = tok[i0:i0 + block]
+                vis = visibility_mask(mb, rows)
+                sc = (qt[rows] @ kt.T) * scale
+                sc = np.where(vis, sc, -np.inf)
+                sc = sc - sc.max(axis=1, keepdims=True)
+                p = np.where(vis, np.exp(sc), 0.0)
+                p /= p.sum(axis=1, keepdims=True)
+                out[b, h, rows] = p @ v[b, h]
+    return out
+
+
+def combine_dense(h_dense, topk_idx, gates):
+    """o_t = sum_{i in S_K(t)} g_{t,i} h_{t,i} (Eq. namoh-attention, R3)."""
+    B, H, T, d = h_dense.shape
+    o = np.zeros((B, T, d))
+    for kk in range(topk_idx.shape[-1]):
+        hk = topk_idx[:, :, kk].astype(np.int64)
+        sel = h_dense[np.arange(B)[:, None], hk, np.arange(T)[None, :]]
+        o += gates[:, :, kk, None] * sel
+    return o
+
+
+# ----------------------------------------------------------------------------
+# Attention, gathered form (O2): per packed segment
+
+def attention_gathered(q, k, v, head_len, seg_offsets, perm_token, H, rope_base,
+                       rope_mode=ROPE_HEAD_RELATIVE, scale=None, block=1024,
+                       segments=None):
+    """Packed ungated head outputs float64 [B*T*K, d].
+
+    Each (batch, head) segment is an independent causal sequence of its
+    routed tokens in order (Sec. 3.2, efficient execution).  ``segments``
+    limits the work to a subset of segment ids (rows of other segments stay
+    zero)."""
+    B, _, T, d = q.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    N = int(seg_offsets[-1])
+    out = np.zeros((N, d))
+    segs = range(B * H) if segments is None else segments
+    for sid in segs:
+        b, h = divmod(int(sid), H)
+        a, e = int(seg_offsets[sid]), int(seg_offsets[sid + 1])
+        n = e - a
+        if n == 0:
+            continue
+        tok = perm_token[a:e].astype(np.int64)
+        pos = _positions(np.arange(n), tok, rope_mode)
+        qt = _rotate(q[b, h, tok], pos, rope_base)
+        kt = _rotate(k[b, h, tok], pos, rope_base)
+        vv = v[b, h, tok]
+        for r0 in range(0, n, block):
+            r1 = min(n, r0 + block)
+            sc = (qt[r0:r1] @ kt[:r1].T) * scale
+            causal = np.arange(r1)[None, :] <= np.arange(r0, r1)[:, None]
+            sc = np.where(causal, sc, -np.inf)
+            sc -= sc.max(axis=1, keepdims=True)
+            p = np.exp(sc)
+            p /= p.sum(axis=1, keepdims=True)
+            out[a + r0:a + r1] = p @ vv[:r1]
+    return out
+
+
+def combine_packed(h_packed, slot_pos, gates):
+    """o_t = sum_k g_{t,k} h[slot_pos[t,k]] in k order."""
+    B, T, K = slot_pos.shape
+    o = np.zeros((B, T, h_packed.shape[-1]))
+    for kk in range(K):
+        o += gates[:, :, kk, None] * h_packed[slot_pos[:, :, kk].astype(np.int64)]
+    return o
+
+
+def prefill(logits, q, k, v, K, rope_base, rope_mode=ROPE_HEAD_RELATIVE,
+            gate_mode=GATE_SOFTMAX_SELECTED, scale=None, form="gathered"):
+    """Whole layer: routing, permutation, attention, combine.
+
+    q, k, v float64 [B,H,T,d].  ``form`` = 'gathered' (O2) or 'definition'
+    (O1).  Returns a dict of every intermediate the GPU library exposes."""
+    H = logits.shape[-1]
+    topk = select_heads(logits, K)
+    g = route_gates(logits, topk, gate_mode)
+    head_len, seg_offsets, perm, slot = permutation(topk, H)
+    if form == "definition":
+        hd = attention_definition(q, k, v, topk, H, rope_base, rope_mode, scale)
+        o = combine_dense(hd, topk, g)
+        # pack the dense per-head outputs at the permutation's positions
+        B, _, T, d = q.shape
+        hp = np.zeros((int(seg_offsets[-1]), d))
+        for b in range(B):
+            for kk in range(K):
+                hp[slot[b, :, kk]] = hd[b, topk[b, :, kk], np.arange(T)]
+    else:
+        hp = attention_gathered(q, k, v, head_len, seg_offsets, perm, H, rope_base,
+                                rope_mode, scale)
+        o = combine_packed(hp, slot, g)
+    return {"topk_idx": topk, "gates": g, "head_len": head_len,
+            "seg_offsets": seg_offsets, "perm_token": perm, "slot_pos": slot,
+            "head_out": hp, "out": o}
+
+
+def prefill_rows(q, k, v, topk_idx, gates, H, rope_base, b, tokens,
+                 rope_mode=ROPE_HEAD_RELATIVE, scale=None):
+    """Layer output o_t for a few tokens of sequence b, each computed on its
+    own from the definition (used to sample outputs at full size).
+
+    q, k, v are indexable [B,H,T,d] arrays in any float dtype (converted
+    row by row); returns float64 [len(tokens), d] and the per-head outputs
+    float64 [len(tokens), K, d]."""
+    topk_b = topk_idx[b]
+    T, K = topk_b.shape
+    d = q.shape[-1]
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    m = membership(topk_idx[b:b + 1], H)[0]
+    o = np.zeros((len(tokens), d))
+    hs = np.zeros((len(tokens), K, d))
+    for r, t in enumerate(tokens):
+        for kk in range(K):
+            h = int(topk_b[t, kk])
+            src = np.nonzero(m[:t + 1, h])[0]       # s in I_h, s <= t
+            ranks = np.arange(src.size)             # rho_h(s)
+            pos = _positions(ranks, src, rope_mode)
+            kt = _rotate(np.asarray(k[b, h][src], dtype=np.float64), pos, rope_base)
+            qpos = None if pos is None else pos[-1:]
+            qt = _rotate(np.asarray(q[b, h][t:t + 1], dtype=np.float64), qpos, rope_base)
+            sc = (kt @ qt[0]) * scale
+            p = np.exp(sc - sc.max())
+            p /= p.sum()
+            hs[r, kk] = p @ np.asarray(v[b, h][src], dtype=np.float64)
+            o[r] += gates[b, t, kk] * hs[r, kk]
+    return o, hs
+
+
+# ----------------------------------------------------------------------------
+# Decode: Sec. 3.1 (prefill and incremental decoding compute the same thing),
+# Sec. 3.2 (decoding reads/updates only the selected caches), reading R6
+
+def decode_step(logits, q, k, v, cache_k, cache_v, cache_len, K, rope_base,
+                rope_mode=ROPE_HEAD_RELATIVE, gate_mode=GATE_SOFTMAX_SELECTED,
+                seq_pos=None, scale=None):
+    """One decoding step for B sequences.
+
+    logits [B,H]; q,k,v float64 [B,H,d]; ``cache_k(b, h, n)`` and
+    ``cache_v(b, h, n)`` return rows [0, n) of the post-RoPE key / value
+    cache of head h (float64 [n, d]); cache_len int [B,H].
+
+    Returns topk_idx [B,K], gates [B,K], out [B,d], the appended rotated
+    keys [B,K,d] and the updated lengths.  Only the selected heads' caches
+    are read."""
+    B, H, d = q.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    topk = select_heads(logits, K)
+    g = route_gates(logits, topk, gate_mode)
+    out = np.zeros((B, d))
+    new_k = np.zeros((B, K, d))
+    new_len = np.array(cache_len, dtype=np.int64, copy=True)
+    for b in range(B):
+        for kk in range(K):
+            h = int(topk[b, kk])
+            n = int(cache_len[b, h])
+            p = n if rope_mode == ROPE_HEAD_RELATIVE else (
+                None if rope_mode == ROPE_NONE else int(seq_pos[b]))
+            pos = None if p is None else np.array([p])
+            qt = _rotate(q[b, h][None], pos, rope_base)[0]
+            kt = _rotate(k[b, h][None], pos, rope_base)[0]
+            Kc = np.concatenate([np.asarray(cache_k(b, h, n), dtype=np.float64).reshape(n, d), kt[None]])
+            Vc = np.concatenate([np.asarray(cache_v(b, h, n), dtype=np.float64).reshape(n, d), v[b, h][None]])
+            sc = (Kc @ qt) * scale
+            w = np.exp(sc - sc.max())
+            w /= w.sum()
+            out[b] += g[b, kk] * (w @ Vc)
+            new_k[b, kk] = kt
+            new_len[b, h] = n + 1
+    return {"topk_idx": topk, "gates": g, "out": out, "new_k": new_k,
+            "cache_len": new_len}
+
+
+# ----------------------------------------------------------------------------
+# O0: brute force with scalar loops (tiny inputs only)
+
+def brute_force_layer(logits, q, k, v, K, rope_base, rope_mode=ROPE_HEAD_RELATIVE,
+                      gate_mode=GATE_SOFTMAX_SELECTED, scale=None):
+    """Scalar-loop evaluation of Eqs. (namoh-gates), (namoh-head-rope),
+    (namoh-attention) for one sequence: logits [T,H], q/k/v [H,T,d] (nested
+    lists or arrays).  Returns (selected heads per token, gates, o [T][d])."""
+    T, H = len(logits), len(logits[0])
+    d = len(q[0][0])
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    sel, gat = [], []
+    for t in range(T):
+        row = [float(x) for x in logits[t]]
+        heads = sorted(range(H), key=lambda i: (-row[i], i))[:K]
+        if gate_mode == GATE_SOFTMAX_SELECTED:
+            mx = max(row[i] for i in heads)
+            ex = [math.exp(row[i] - mx) for i in heads]
+            gat.append([e / sum(ex) for e in ex])
+        else:
+            mx = max(row)
+            z = sum(math.exp(x - mx) for x in row)
+            gat.append([math.exp(row[i] - mx) / z for i in heads])
+        sel.append(heads)
+
+    def rot(vec, p):
+        if rope_mode == ROPE_NONE:
+            return list(vec)
+        half = d // 2
+        outv = [0.0] * d
+        for j in range(half):
+            ang = p * float(rope_base) ** (-2.0 * j / d)
+            c, s = math.cos(ang), math.sin(ang)
+            outv[j] = vec[j] * c - vec[j + half] * s
+            outv[j + half] = vec[j + half] * c + vec[j] * s
+        return outv
+
+    o = [[0.0] * d for _ in range(T)]
+    for t in range(T):
+        for kk, i in enumerate(sel[t]):
+            hist = [s for s in range(t + 1) if i in sel[s]]     # I_i, s <= t
+            def pos_of(s):
+                rank = sum(1 for u in range(s + 1) if i in sel[u]) - 1
+                return rank if rope_mode == ROPE_HEAD_RELATIVE else s
+            qt = rot([float(x) for x in q[i][t]], pos_of(t))
+            scores = []
+            for s in hist:
+                ks = rot([float(x) for x in k[i][s]], pos_of(s))
+                scores.append(sum(a * b for a, b in zip(qt, ks)) * scale)
+            mx = max(scores)
+            w = [math.exp(x - mx) for x in scores]
+            z = sum(w)
+            for j in range(d):
+                acc = sum(w[u] / z * float(v[i][s][j]) for u, s in enumerate(hist))
+                o[t][j] += gat[t][kk] * acc
+    return sel, gat, o
+
+
+# ----------------------------------------------------------------------------
+# Cost accounting: App. D.3
+
+def interaction_count(head_len) -> int:
+    """C_attn = 1/2 sum_i n_i (n_i + 1) (Eq. app-routed-interactions)."""
+    n = np.asarray(head_len, dtype=np.int64)
+    return int((n * (n + 1)).sum() // 2)
+
+
+def shared_head_counts(m_b: np.ndarray) -> np.ndarray:
+    """R = tril(M M^T) for one sequence's mask M [T,H] (Sec. 4.3): the number
+    of active heads shared by token t and an earlier-or-equal token s."""
+    M = m_b.astype(np.int64)
+    return np.tril(M @ M.T)

@@ -1,0 +1,394 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Each test checks the oracle against something other than itself: values the
+paper prints for its worked example, closed forms of App. D.3, library
+routines (numpy stable sort, scipy softmax, torch scaled-dot-product
+attention), an independent complex-number form of RoPE, brute force with
+scalar loops, and invariants.  No GPU is touched.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+
+import oracle as O
+from paper_2609_38832_amd import workloads as W
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+rng = np.random.default_rng(1234)
+
+
+def _rand_logits(B, T, H, seed=0):
+    return np.random.default_rng(seed).standard_normal((B, T, H)).astype(np.float32)
+
+
+# ----------------------------------------------------------------------------
+# selection (Eq. namoh-gates TopK; ties -> lower head index)
+
+def test_select_matches_scalar_sort():
+    l = _rand_logits(2, 50, 7, seed=1)
+    got = O.select_heads(l, 3)
+    for b in range(2):
+        for t in range(50):
+            row = [float(x) for x in l[b, t]]
+            want = sorted(range(7), key=lambda i: (-row[i], i))[:3]
+            assert list(got[b, t]) == want
+
+
+def test_select_matches_numpy_stable_argsort_with_ties():
+    # integer-valued logits: many exact ties
+    l = np.random.default_rng(2).integers(-3, 4, size=(3, 200, 16)).astype(np.float32)
+    got = O.select_heads(l, 5)
+    want = np.argsort(-l.astype(np.float64), axis=-1, kind="stable")[..., :5]
+    np.testing.assert_array_equal(got, want)
+
+
+def test_select_forced_ties_and_specials():
+    assert list(O.select_heads(np.zeros((1, 6), np.float32), 3)[0]) == [0, 1, 2]
+    # -0.0 equals +0.0: lower index wins
+    z = np.array([[0.0, -0.0, 0.0, -0.0]], np.float32)
+    assert list(O.select_heads(z, 2)[0]) == [0, 1]
+    z2 = np.array([[-0.0, 0.0, -1.0]], np.float32)
+    assert list(O.select_heads(z2, 2)[0]) == [0, 1]
+    inf = np.array([[-np.inf, np.inf, np.inf, 1.0, -np.inf]], np.float32)
+    assert list(O.select_heads(inf, 4)[0]) == [1, 2, 3, 0]
+    with pytest.raises(ValueError):
+        O.select_heads(np.array([[np.nan, 0.0]], np.float32), 1)
+
+
+def test_each_token_has_exactly_K_distinct_heads():
+    l = _rand_logits(2, 300, 12, seed=3)
+    topk = O.select_heads(l, 4)
+    m = O.membership(topk, 12)
+    assert (m.sum(-1) == 4).all()
+    assert all(len(set(r)) == 4 for r in topk.reshape(-1, 4).tolist())
+
+
+# ----------------------------------------------------------------------------
+# gates
+
+def test_gates_softmax_selected_and_all():
+    l = _rand_logits(1, 40, 10, seed=4)
+    topk = O.select_heads(l, 3)
+    g = O.route_gates(l, topk, O.GATE_SOFTMAX_SELECTED)
+    sel = np.take_along_axis(l.astype(np.float64), topk.astype(np.int64), -1)
+    np.testing.assert_allclose(g, scipy.special.softmax(sel, axis=-1), rtol=1e-13)
+    np.testing.assert_allclose(g.sum(-1), 1.0, rtol=1e-13)
+    assert (np.diff(g, axis=-1) <= 1e-15).all()         # ordered by logit
+    ga = O.route_gates(l, topk, O.GATE_SOFTMAX_ALL)
+    a = scipy.special.softmax(l.astype(np.float64), axis=-1)
+    np.testing.assert_allclose(ga, np.take_along_axis(a, topk.astype(np.int64), -1), rtol=1e-13)
+    assert (ga.sum(-1) < 1.0).all()
+
+
+def test_gates_K_equals_H_modes_agree():
+    l = _rand_logits(1, 20, 6, seed=5)
+    topk = O.select_heads(l, 6)
+    np.testing.assert_allclose(O.route_gates(l, topk, 0), O.route_gates(l, topk, 1), rtol=1e-13)
+
+
+# ----------------------------------------------------------------------------
+# membership, ranks, permutation: worked example of Fig. 2 and App. D.3
+
+def test_worked_example_fig2():
+    fx = json.load(open(os.path.join(HERE, "golden", "worked_example_fig2.json")))
+    pr = fx["printed"]
+    H, K = pr["H"], pr["K"]
+    asg = fx["assignment"]
+    T = len(asg)
+    logits = np.zeros((1, T, H), np.float32)
+    for t, heads in enumerate(asg):
+        logits[0, t, heads] = 1.0
+    topk = O.select_heads(logits, K)
+    m = O.membership(topk, H)
+    rho = O.head_ranks(m)
+    head0 = np.nonzero(m[0, :8, 0])[0]
+    assert list(head0) == pr["head0_global_positions_prefill"]
+    assert list(rho[0, head0, 0]) == pr["head0_local_indices"]
+    assert sorted(topk[0, 8]) == pr["token8_heads"]
+    assert rho[0, 8, 0] == pr["token8_head0_index"]
+    assert sorted(topk[0, 9]) == pr["token9_heads"]
+    # the permutation places head 0's tokens first, at their local indices
+    n, off, perm, slot = O.permutation(topk[:, :8], H)
+    assert list(perm[off[0]:off[1]]) == pr["head0_global_positions_prefill"]
+
+
+def test_permutation_invariants():
+    B, T, H, K = 3, 257, 10, 3
+    topk = O.select_heads(_rand_logits(B, T, H, seed=6), K)
+    n, off, perm, slot = O.permutation(topk, H)
+    assert n.sum() == B * T * K                                 # sum n_i = TK
+    assert (n.sum(1) == T * K).all()
+    assert off[0] == 0 and off[-1] == B * T * K
+    np.testing.assert_array_equal(np.diff(off), n.reshape(-1))
+    for s in range(B * H):
+        seg = perm[off[s]:off[s + 1]]
+        assert (np.diff(seg) > 0).all()                         # ascending t
+    for b in range(B):
+        for t in range(T):
+            for kk in range(K):
+                p = slot[b, t, kk]
+                assert perm[p] == t
+                sid = np.searchsorted(off, p, side="right") - 1
+                assert sid == b * H + topk[b, t, kk]
+    assert len(set(slot.reshape(-1).tolist())) == B * T * K       # bijection
+
+
+def test_rank_is_running_count():
+    topk = O.select_heads(_rand_logits(1, 64, 5, seed=7), 2)
+    m = O.membership(topk, 5)
+    rho = O.head_ranks(m)
+    for h in range(5):
+        toks = np.nonzero(m[0, :, h])[0]
+        assert list(rho[0, toks, h]) == list(range(len(toks)))
+
+
+@pytest.mark.parametrize("H", [8, 16, 32, 64])
+def test_kv_storage_unchanged_as_H_grows(H):
+    T, K = 1000, 8
+    topk = O.select_heads(_rand_logits(1, T, H, seed=H), K)
+    n, *_ = O.permutation(topk, H)
+    assert n.sum() == T * K                                     # M_KV = TK
+
+
+# ----------------------------------------------------------------------------
+# visibility mask and interaction counts (Sec. 4.3, App. D.3)
+
+def _all_vis(m_b):
+    T, H = m_b.shape
+    return [O.visibility_mask(m_b[:, h], np.arange(T)) for h in range(H)]
+
+
+def test_mask_sum_equals_tril_MMt_and_interactions():
+    T, H, K = 90, 6, 2
+    topk = O.select_heads(_rand_logits(1, T, H, seed=8), K)
+    m = O.membership(topk, H)[0]
+    vis = _all_vis(m)
+    R = sum(v.astype(np.int64) for v in vis)
+    np.testing.assert_array_equal(R, O.shared_head_counts(m))
+    n = m.sum(0)
+    pop = sum(int(v.sum()) for v in vis)
+    assert pop == O.interaction_count(n)
+    # second-moment form, Eq. (app-load-second-moment) / (namoh-attention-work)
+    nbar = T * K / H
+    cv2 = ((n - nbar) ** 2).mean() / nbar ** 2
+    assert math.isclose(pop, T * T * K * K / (2 * H) * (1 + cv2) + T * K / 2, rel_tol=1e-12)
+
+
+def test_interaction_bounds_attained():
+    T, H, K = 48, 8, 2
+    # exactly balanced: token t takes heads (tK + j) mod H
+    bal = np.array([[(t * K + j) % H for j in range(K)] for t in range(T)])[None]
+    n, *_ = O.permutation(bal.astype(np.int32), H)
+    assert O.interaction_count(n) == T * T * K * K // (2 * H) + T * K // 2
+    # every token picks the same heads: upper bound K T (T+1) / 2
+    same = np.tile(np.array([[3, 5]]), (T, 1))[None].astype(np.int32)
+    n2, *_ = O.permutation(same, H)
+    assert O.interaction_count(n2) == K * T * (T + 1) // 2
+    m = O.membership(same, H)[0]
+    pop = sum(int(v.sum()) for v in _all_vis(m))
+    assert pop == K * T * (T + 1) // 2
+
+
+# ----------------------------------------------------------------------------
+# RoPE (Eq. namoh-head-rope, reading R4)
+
+def test_rope_matches_complex_rotation():
+    d, base = 16, 500.0
+    x = rng.standard_normal((7, d))
+    p = np.array([0, 1, 2, 5, 77, 1000, 123456])
+    got = O.rope_rotate(x, p, base)
+    half = d // 2
+    z = x[:, :half] + 1j * x[:, half:]
+    freqs = np.array([base ** (-(2 * j) / d) for j in range(half)])
+    zr = z * np.exp(1j * np.outer(p, freqs))
+    np.testing.assert_allclose(got, np.concatenate([zr.real, zr.imag], -1), atol=1e-12)
+
+
+def test_rope_hand_values_and_properties():
+    # d = 4, base 100: theta = (1, 0.1).  Element 1 pairs with element 3.
+    e1 = np.array([[0.0, 1.0, 0.0, 0.0]])
+    r = O.rope_rotate(e1, np.array([1]), 100.0)[0]
+    np.testing.assert_allclose(r, [0.0, math.cos(0.1), 0.0, math.sin(0.1)], atol=1e-15)
+    e0 = np.array([[1.0, 0.0]])
+    np.testing.assert_allclose(O.rope_rotate(e0, np.array([math.pi / 2]), 7.0)[0], [0, 1], atol=1e-15)
+    x = rng.standard_normal((5, 32))
+    np.testing.assert_allclose(O.rope_rotate(x, np.zeros(5), 1e4), x)   # identity at 0
+    np.testing.assert_allclose(np.linalg.norm(O.rope_rotate(x, np.arange(5) * 37, 1e4), axis=1),
+                               np.linalg.norm(x, axis=1), rtol=1e-13)
+    # scores depend on the position difference only
+    q, k = rng.standard_normal(32), rng.standard_normal(32)
+    for a, b in [(3, 10), (100, 107), (1000, 1007)]:
+        s = O.rope_rotate(q[None], np.array([b]), 1e4)[0] @ O.rope_rotate(k[None], np.array([a]), 1e4)[0]
+        s0 = O.rope_rotate(q[None], np.array([b - a]), 1e4)[0] @ k
+        assert math.isclose(s, s0, rel_tol=1e-10, abs_tol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# attention: K = H reduces to dense causal MHA with standard RoPE
+
+def test_K_equals_H_is_dense_causal_mha_torch_sdpa():
+    torch = pytest.importorskip("torch")
+    import torch.nn.functional as F
+    B, T, H, d, base = 2, 37, 4, 8, 1e4
+    g = np.random.default_rng(9)
+    q, k, v = (g.standard_normal((B, H, T, d)) for _ in range(3))
+    logits = g.standard_normal((B, T, H)).astype(np.float32)
+    for form in ("definition", "gathered"):
+        res = O.prefill(logits, q, k, v, H, base, O.ROPE_HEAD_RELATIVE, O.GATE_SOFTMAX_ALL, form=form)
+        pos = np.arange(T)
+        qr = O.rope_rotate(q, np.broadcast_to(pos, (B, H, T)), base)
+        kr = O.rope_rotate(k, np.broadcast_to(pos, (B, H, T)), base)
+        ref = F.scaled_dot_product_attention(torch.from_numpy(qr), torch.from_numpy(kr),
+                                             torch.from_numpy(v), is_causal=True).numpy()
+        a = scipy.special.softmax(logits.astype(np.float64), -1)           # [B,T,H]
+        o_ref = np.einsum("bth,bhtd->btd", a, ref)
+        np.testing.assert_allclose(res["out"], o_ref, atol=1e-12)
+        # head-relative and global RoPE coincide when K = H
+        res_g = O.prefill(logits, q, k, v, H, base, O.ROPE_GLOBAL, O.GATE_SOFTMAX_ALL, form=form)
+        np.testing.assert_allclose(res_g["out"], res["out"], atol=1e-12)
+
+
+def test_attention_special_cases():
+    B, T, H, K, d = 1, 30, 5, 2, 6
+    g = np.random.default_rng(10)
+    logits = g.standard_normal((B, T, H)).astype(np.float32)
+    # head 4 selected by token 7 only: that head's output there is v itself
+    logits[..., 4] = -10.0
+    logits[0, 7, 4] = 10.0
+    q, k, v = (g.standard_normal((B, H, T, d)) for _ in range(3))
+    res = O.prefill(logits, q, k, v, K, 1e4, form="definition")
+    slot = res["slot_pos"][0, 7, 0]
+    assert res["topk_idx"][0, 7, 0] == 4
+    np.testing.assert_allclose(res["head_out"][slot], v[0, 4, 7], atol=1e-14)
+    # q = 0: uniform weights -> prefix mean of the head's routed values
+    res0 = O.prefill(logits, np.zeros_like(q), k, v, K, 1e4, form="gathered")
+    n, off, perm = res0["head_len"], res0["seg_offsets"], res0["perm_token"]
+    for h in range(H):
+        toks = perm[off[h]:off[h + 1]]
+        for r in range(len(toks)):
+            np.testing.assert_allclose(res0["head_out"][off[h] + r],
+                                       v[0, h, toks[:r + 1]].mean(0), atol=1e-13)
+    # constant V -> constant output (gates sum to one)
+    vc = np.full_like(v, 0.375)
+    resc = O.prefill(logits, q, k, vc, K, 1e4, form="gathered")
+    np.testing.assert_allclose(resc["out"], 0.375, atol=1e-13)
+
+
+@pytest.mark.parametrize("rope_mode", [O.ROPE_HEAD_RELATIVE, O.ROPE_GLOBAL, O.ROPE_NONE])
+@pytest.mark.parametrize("gate_mode", [O.GATE_SOFTMAX_SELECTED, O.GATE_SOFTMAX_ALL])
+def test_brute_force_equals_definition_equals_gathered(rope_mode, gate_mode):
+    T, H, K, d, base = 24, 5, 2, 6, 100.0
+    g = np.random.default_rng(11 + rope_mode + 3 * gate_mode)
+    logits = g.integers(-2, 3, size=(1, T, H)).astype(np.float32)   # ties included
+    q, k, v = (g.standard_normal((1, H, T, d)) for _ in range(3))
+    sel, gat, o0 = O.brute_force_layer(logits[0], q[0], k[0], v[0], K, base, rope_mode, gate_mode)
+    r1 = O.prefill(logits, q, k, v, K, base, rope_mode, gate_mode, form="definition")
+    r2 = O.prefill(logits, q, k, v, K, base, rope_mode, gate_mode, form="gathered")
+    assert r1["topk_idx"][0].tolist() == sel
+    np.testing.assert_allclose(r1["gates"][0], np.array(gat), atol=1e-15)
+    np.testing.assert_allclose(r1["out"][0], np.array(o0), atol=1e-12)
+    np.testing.assert_allclose(r2["out"], r1["out"], atol=1e-12)
+    np.testing.assert_allclose(r2["head_out"], r1["head_out"], atol=1e-12)
+
+
+def test_definition_equals_gathered_medium():
+    B, T, H, K, d = 2, 300, 6, 3, 16
+    g = np.random.default_rng(12)
+    logits = g.standard_normal((B, T, H)).astype(np.float32)
+    q, k, v = (g.standard_normal((B, H, T, d)) for _ in range(3))
+    r1 = O.prefill(logits, q, k, v, K, 1e4, form="definition")
+    r2 = O.prefill(logits, q, k, v, K, 1e4, form="gathered")
+    np.testing.assert_allclose(r2["out"], r1["out"], atol=1e-12)
+    # sampled rows computed one by one agree too
+    toks = [0, 1, 150, 299]
+    o, hs = O.prefill_rows(q, k, v, r1["topk_idx"], r1["gates"], H, 1e4, 1, toks)
+    np.testing.assert_allclose(o, r1["out"][1, toks], atol=1e-12)
+    for i, t in enumerate(toks):
+        np.testing.assert_allclose(hs[i], r1["head_out"][r1["slot_pos"][1, t]], atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# decode (Sec. 3.1: prefill and incremental decoding are the same computation)
+
+def _cache_from_prefill(q, k, logits, K, base, Tp):
+    """Post-RoPE key cache of each head after Tp tokens, in rank order."""
+    B, H, T, d = q.shape
+    topk = O.select_heads(logits[:, :Tp], K)
+    m = O.membership(topk, H)
+    rho = O.head_ranks(m)
+    caches = {}
+    for b in range(B):
+        for h in range(H):
+            toks = np.nonzero(m[b, :, h])[0]
+            caches[(b, h)] = toks, O.rope_rotate(k[b, h, toks], rho[b, toks, h], base)
+    return caches
+
+
+@pytest.mark.parametrize("gate_mode", [O.GATE_SOFTMAX_SELECTED, O.GATE_SOFTMAX_ALL])
+def test_prefill_equals_incremental_decode(gate_mode):
+    B, T, H, K, d, base = 2, 41, 6, 3, 8, 1e4
+    g = np.random.default_rng(13)
+    logits = g.standard_normal((B, T, H)).astype(np.float32)
+    q, k, v = (g.standard_normal((B, H, T, d)) for _ in range(3))
+    full = O.prefill(logits, q, k, v, K, base, gate_mode=gate_mode, form="definition")
+    for Tp in (0, 1, 20, T - 1):
+        caches = _cache_from_prefill(q, k, logits, K, base, Tp)
+        lens = np.array([[len(caches[(b, h)][0]) for h in range(H)] for b in range(B)])
+        res = O.decode_step(logits[:, Tp], q[:, :, Tp], k[:, :, Tp], v[:, :, Tp],
+                            lambda b, h, n: caches[(b, h)][1][:n],
+                            lambda b, h, n: v[b, h, caches[(b, h)][0][:n]],
+                            lens, K, base, gate_mode=gate_mode)
+        np.testing.assert_allclose(res["out"], full["out"][:, Tp], atol=1e-12)
+        np.testing.assert_array_equal(res["topk_idx"], full["topk_idx"][:, Tp])
+        for b in range(B):
+            for kk in range(K):
+                assert res["cache_len"][b, res["topk_idx"][b, kk]] == lens[b, res["topk_idx"][b, kk]] + 1
+
+
+def test_decode_reads_only_selected_caches_and_counts():
+    B, H, K, d = 3, 8, 2, 4
+    g = np.random.default_rng(14)
+    logits = g.standard_normal((B, H)).astype(np.float32)
+    q, k, v = (g.standard_normal((B, H, d)) for _ in range(3))
+    lens = g.integers(0, 9, size=(B, H))
+    store_k = g.standard_normal((B, H, 10, d))
+    store_v = g.standard_normal((B, H, 10, d))
+    reads = []
+
+    def ck(b, h, n):
+        reads.append((b, h, n))
+        return store_k[b, h, :n]
+    r1 = O.decode_step(logits, q, k, v, ck, lambda b, h, n: store_v[b, h, :n], lens, K, 1e4)
+    topk = r1["topk_idx"]
+    assert sorted((b, h) for b, h, _ in reads) == sorted((b, int(h)) for b in range(B) for h in topk[b])
+    # A_KV = sum of the selected heads' lengths (Eq. namoh-kv-cost)
+    assert sum(n for *_, n in reads) == sum(int(lens[b, h]) for b in range(B) for h in topk[b])
+    # perturb every non-selected cache: output unchanged
+    sk2, sv2 = store_k.copy(), store_v.copy()
+    for b in range(B):
+        for h in range(H):
+            if h not in topk[b]:
+                sk2[b, h] += 100.0
+                sv2[b, h] -= 50.0
+    r2 = O.decode_step(logits, q, k, v, lambda b, h, n: sk2[b, h, :n],
+                       lambda b, h, n: sv2[b, h, :n], lens, K, 1e4)
+    np.testing.assert_array_equal(r2["out"], r1["out"])
+
+
+# ----------------------------------------------------------------------------
+# input generator: determinism and format (no layer arithmetic)
+
+def test_workload_generator_is_deterministic_and_rounds_bf16():
+    w = W.WORKLOADS[1].with_(T=64)
+    a, b = W.prefill_inputs(w), W.prefill_inputs(w)
+    for key in a:
+        np.testing.assert_array_equal(a[key], b[key])
+    x = np.array([1.0, 1.00390625, 1.01171875, -2.5e-3, 3.0e5], np.float32)
+    bits = W.f32_to_bf16_bits(x)
+    # 1 + 2^-8 is a tie -> even (1.0); 1 + 3*2^-8 is a tie -> even (1 + 2^-6)
+    np.testing.assert_array_equal(W.bf16_bits_to_f32(bits)[:3], [1.0, 1.0, 1.015625])
+    assert abs(W.bf16_bits_to_f32(bits)[3] / x[3] - 1) < 2 ** -8
