@@ -1,0 +1,332 @@
+#!/usr/bin/env python3
+"""Throughput of the routed mixture-of-head attention layer on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload N]
+
+A step is one pass of the whole layer over one batch of seeded synthetic
+input already resident in HBM: for prefill workloads route (top-K, gates,
+permutation) + attention (packing with RoPE, MFMA attention, gated combine);
+for the decode workload one decode step (route, append, history attention,
+combine).  Prints one JSON line.  The default workload is the balanced bf16
+prefill (B=4, T=4096, H=32, K=8, d=64).
+
+The roofline entry is for the dominant kernel (routed attention for prefill,
+history attention for decode): algorithmic FLOPs (4*d*sum n(n+1)/2) or bytes
+(sum over active heads of (n+1)*2*d*2) per launch divided by its average
+duration, timed with HIP events recorded by the library on the launch stream.
+The cpu_baseline entry times the CPU oracle (float64 numpy) on a bounded
+sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2609_38832_amd import workloads as W  # noqa: E402
+
+METRIC = "routed-attn prefill tokens/s + decode KV GB/s, % of MFMA/HBM peak (1 GPU)"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3       # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def source_digest(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_entry(kernel, workload_name, per_launch_units):
+    """HBM traffic from committed rocprofv3 counter runs, if they were taken
+    on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload_name}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("source_digest") != source_digest(rec["sources"]):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_info():
+    cores = len(os.sched_getaffinity(0))
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        info = threadpool_info()
+        if info:
+            threads = max(i.get("num_threads", 1) for i in info)
+    except Exception:
+        pass
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return cores, threads, model
+
+
+# ----------------------------------------------------------------------------
+def bench_prefill(w, args, torch, L, DI):
+    dev = torch.device("cuda:0")
+    log(f"generating inputs for {w.name}")
+    inp = W.prefill_inputs(w)
+    logits = torch.from_numpy(inp["logits"]).to(dev)
+    q, k, v = (DI.to_device(inp[n], w.dtype, dev) for n in ("q", "k", "v"))
+    B, T, H, K, d = w.B, w.T, w.H, w.K, w.d
+    i32 = dict(dtype=torch.int32, device=dev)
+    routing = {
+        "topk_idx": torch.empty(B, T, K, **i32),
+        "gates": torch.empty(B, T, K, dtype=torch.float32, device=dev),
+        "head_len": torch.empty(B, H, **i32),
+        "seg_offsets": torch.empty(B * H + 1, **i32),
+        "perm_token": torch.empty(B * T * K, **i32),
+        "slot_pos": torch.empty(B, T, K, **i32),
+    }
+    rws = L.workspace(L.route_workspace_size(B, T, H, K), dev)
+    dt = L.dtype_code(q.dtype)
+    aws = L.workspace(L.attn_workspace_size(B, T, H, K, d, dt), dev)
+    out = torch.empty(B, T, d, dtype=q.dtype, device=dev)
+
+    def step():
+        L.route(logits, K, L.GATE_SOFTMAX_SELECTED, out=routing, ws=rws)
+        L.attn_fwd(q, k, v, routing, K, w.rope_base, L.ROPE_HEAD_RELATIVE, out=out, ws=aws)
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    n = routing["head_len"].cpu().numpy().astype(np.int64)
+    c_attn = int((n * (n + 1) // 2).sum())
+    flops = 4.0 * d * c_attn
+
+    L.profile_enable(args.steps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_total = e0.elapsed_time(e1)
+    kern = {}
+    for sec in ("attn", "pack", "combine"):
+        r = L.profile_read(sec)
+        if r is not None and r[1] > 0:
+            kern[sec] = r[0] / r[1]
+    L.profile_enable(0)
+    ms_step = ms_total / args.steps
+    tokens_s = B * T / (ms_step * 1e-3)
+    attn_ms = kern.get("attn", float("nan"))
+    mfma = w.dtype == "bf16" and d in (64, 128)
+    peak = PEAK_BF16_TFLOPS if mfma else PEAK_FP32_TFLOPS
+    achieved = flops / (attn_ms * 1e-3) / 1e12
+    roof = {"kernel": "k_attn_mfma" if mfma else "k_attn_generic",
+            "bound": "mfma" if mfma else "alu", "achieved": round(achieved, 2), "peak": peak,
+            "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+            "traffic": traffic_entry("k_attn_mfma", w.name, None),
+            "algorithmic_per_launch": {"flops": flops, "C_attn": c_attn},
+            "kernel_ms": round(attn_ms, 4)}
+    res = {"metric": METRIC, "value": round(tokens_s, 1), "unit": "tokens/s",
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+           "config": {"workload": w.name, "B": B, "T": T, "H": H, "K": K, "d_head": d,
+                      "rope": "head-relative", "rope_base": w.rope_base,
+                      "gates": "softmax over selected"},
+           "roofline": roof,
+           "kernels_ms": {k2: round(v2, 4) for k2, v2 in kern.items()}}
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_prefill(w, inp, n, args.cpu_budget)
+    return res
+
+
+def cpu_baseline_prefill(w, inp, head_len, budget_s):
+    import oracle as O
+    cores, threads, model = cpu_info()
+    log(f"cpu baseline: oracle on up to ~{budget_s:.0f} s of segments")
+    t0 = time.perf_counter()
+    topk = O.select_heads(inp["logits"], w.K)
+    g = O.route_gates(inp["logits"], topk, O.GATE_SOFTMAX_SELECTED)
+    n, off, perm, slot = O.permutation(topk, w.H)
+    t_route = time.perf_counter() - t0
+    # attention over whole segments, in order, until the budget is spent
+    f64 = {}
+    done_work, segs = 0, 0
+    t1 = time.perf_counter()
+    total_work = float((head_len * (head_len + 1) // 2).sum())
+    for sid in range(w.B * w.H):
+        b, h = divmod(sid, w.H)
+        if (b, h) not in f64:
+            f64[(b, h)] = True
+        sub = {key: W.as_float64(inp[key][b:b + 1, h:h + 1], w.dtype) for key in ("q", "k", "v")}
+        a, e = int(off[sid]), int(off[sid + 1])
+        off_local = np.array([0, e - a], dtype=np.int64)
+        O.attention_gathered(sub["q"], sub["k"], sub["v"], None, off_local, perm[a:e], 1,
+                             w.rope_base)
+        nn = e - a
+        done_work += nn * (nn + 1) / 2
+        segs += 1
+        if time.perf_counter() - t1 > budget_s:
+            break
+    t_attn = time.perf_counter() - t1
+    t_est = t_route + t_attn * (total_work / max(done_work, 1.0))
+    return {"value": round(w.B * w.T / t_est, 2), "unit": "tokens/s", "cores": threads or cores,
+            "kind": "oracle",
+            "sample": (f"routing+permutation of the whole batch ({t_route:.2f} s) plus float64 "
+                       f"gathered causal attention of {segs}/{w.B * w.H} (batch, head) segments "
+                       f"({t_attn:.2f} s), extrapolated by causal work sum n(n+1)/2"),
+            "host_cpu": model, "host_cores": cores}
+
+
+# ----------------------------------------------------------------------------
+def bench_decode(w, args, torch, L, DI):
+    dev = torch.device("cuda:0")
+    log(f"prior head lengths for {w.name}")
+    lengths = W.decode_prior_lengths(w)
+    cap = W.decode_cache_capacity(lengths, steps=args.warmup + args.steps + 1)
+    log(f"filling caches on the device: 2 x [{w.B},{w.H},{cap},{w.d}] {w.dtype}")
+    kc, vc = DI.decode_caches(w.B, w.H, cap, w.d, w.dtype, w.seed, w.qkv_scale, dev)
+    step_in = W.decode_step_inputs(w)
+    logits = torch.from_numpy(step_in["logits"]).to(dev)
+    q, k, v = (DI.to_device(step_in[n], w.dtype, dev) for n in ("q", "k", "v"))
+    cache_len = torch.from_numpy(lengths).to(dev)
+    B, H, K, d = w.B, w.H, w.K, w.d
+    outd = {"topk_idx": torch.empty(B, K, dtype=torch.int32, device=dev),
+            "gates": torch.empty(B, K, dtype=torch.float32, device=dev),
+            "out": torch.empty(B, d, dtype=q.dtype, device=dev)}
+    ws = L.workspace(L.decode_workspace_size(B, H, K, d, cap), dev)
+
+    def step():
+        L.decode_step(logits, q, k, v, kc, vc, cache_len, K, w.rope_base, out=outd, ws=ws)
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    len0 = cache_len.cpu().numpy().astype(np.int64)
+    topk = outd["topk_idx"].cpu().numpy()
+    esz = 2 if w.dtype == "bf16" else 4
+    # the same token is decoded each step, so the same heads grow by one row
+    rows = [sum(int(len0[b, h]) + 1 + s for b in range(B) for h in topk[b]) for s in range(args.steps)]
+    kv_bytes = [r * 2 * d * esz for r in rows]
+    L.profile_enable(args.steps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_total = e0.elapsed_time(e1)
+    r = L.profile_read("decode_attn")
+    L.profile_enable(0)
+    kern_ms = r[0] / r[1]
+    ms_step = ms_total / args.steps
+    mean_bytes = float(np.mean(kv_bytes))
+    gbs_step = mean_bytes / (ms_step * 1e-3) / 1e9
+    gbs_kern = mean_bytes / (kern_ms * 1e-3) / 1e9
+    res = {"metric": METRIC, "value": round(gbs_step, 1), "unit": "GB/s",
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+           "config": {"workload": w.name, "B": B, "prior_tokens": w.prior, "H": H, "K": K,
+                      "d_head": d, "cap": cap, "rope": "head-relative", "rope_base": w.rope_base},
+           "roofline": {"kernel": "k_decode_attn", "bound": "hbm", "achieved": round(gbs_kern, 1),
+                        "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(gbs_kern / PEAK_HBM_GBS, 4),
+                        "traffic": traffic_entry("k_decode_attn", w.name, None),
+                        "algorithmic_per_launch": {"kv_bytes": mean_bytes,
+                                                   "rows": float(np.mean(rows))},
+                        "kernel_ms": round(kern_ms, 4)},
+           "tokens_per_s": round(B / (ms_step * 1e-3), 1)}
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_decode(w, step_in, kc, vc, len0, topk, args.cpu_budget, torch)
+    del kc, vc
+    return res
+
+
+def cpu_baseline_decode(w, step_in, kc, vc, lengths, topk, budget_s, torch):
+    import oracle as O
+    cores, threads, model = cpu_info()
+    log("cpu baseline: oracle decode on a sample of sequences")
+    d = w.d
+
+    def host(t):
+        return W.as_float64(t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16), w.dtype) \
+            if w.dtype == "bf16" else t.cpu().numpy().astype(np.float64)
+
+    sf = {k: W.as_float64(step_in[k], w.dtype) for k in ("q", "k", "v")}
+    done_bytes, t_sum, nseq = 0.0, 0.0, 0
+    for b in range(w.B):
+        hist = {int(h): (host(kc[b, h, :lengths[b, h]]), host(vc[b, h, :lengths[b, h]]))
+                for h in topk[b]}
+        t0 = time.perf_counter()
+        O.decode_step(step_in["logits"][b:b + 1], sf["q"][b:b + 1], sf["k"][b:b + 1],
+                      sf["v"][b:b + 1], lambda _b, h, n: hist[h][0], lambda _b, h, n: hist[h][1],
+                      lengths[b:b + 1], w.K, w.rope_base)
+        t_sum += time.perf_counter() - t0
+        done_bytes += sum((int(lengths[b, h]) + 1) * 2 * d * 2 for h in topk[b])
+        nseq += 1
+        if t_sum > budget_s:
+            break
+    return {"value": round(done_bytes / t_sum / 1e9, 3), "unit": "GB/s",
+            "cores": threads or cores, "kind": "oracle",
+            "sample": (f"float64 decode step of {nseq}/{w.B} sequences "
+                       f"({t_sum:.2f} s, history rows copied to the host beforehand, not timed); "
+                       f"value = algorithmic bf16 KV bytes of those sequences / time"),
+            "host_cpu": model, "host_cores": cores}
+
+
+# ----------------------------------------------------------------------------
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--workload", type=int, default=2, choices=sorted(W.WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle work for the CPU baseline sample")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; the path is sharded by "
+                          "batch or head across GPUs in design only", "n_gpus": args.gpus}))
+        sys.exit(2)
+    w = W.WORKLOADS[args.workload]
+    if args.steps is None:
+        args.steps = 20 if w.decode else 50
+    if args.warmup is None:
+        args.warmup = 5 if w.decode else 10
+    import torch
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    from paper_2609_38832_amd import _lib as L
+    from paper_2609_38832_amd import device_inputs as DI
+    L.lib()
+    res = (bench_decode if w.decode else bench_prefill)(w, args, torch, L, DI)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,186 @@
+/*
+ * namoh.h — C ABI of the MI355X (gfx950) routed mixture-of-head attention
+ * library (libnamoh.so).
+ *
+ * The layer follows NAMOH ("Native Sparse Attention from Mixture-of-Head"):
+ * every token picks K of H heads from its router logits (Sec. 3.1,
+ * Eq. namoh-gates), each head runs causal scaled dot-product attention only
+ * over the tokens routed to it (Sec. 3.1, Eq. namoh-attention), with RoPE at
+ * the token's rank inside that head's subsequence (Sec. 3.2,
+ * Eq. namoh-head-rope), and the gated per-head outputs are summed per token.
+ * The per-head output projection W_O^(i) is taken as the identity, so the
+ * layer output has the head width d.
+ *
+ * Conventions shared by every call
+ *  - Every pointer argument is a DEVICE pointer to contiguous memory owned by
+ *    the caller.  The library allocates nothing, frees nothing, never
+ *    synchronises, and enqueues all its work on `stream` (a hipStream_t;
+ *    NULL = the default stream), in order.
+ *  - Arguments are validated on the host before anything is enqueued; a call
+ *    that returns an error has launched nothing.  namoh_last_error() then
+ *    gives a thread-local message.
+ *  - Floating-point tensors are 16-byte aligned; int32 / float32 index and
+ *    gate arrays are 4-byte aligned.
+ *  - Limits: 1 <= K <= H <= 64; d_head in {32, 64, 128}; B, T >= 1;
+ *    B*T*K < 2^31.
+ *  - No floating-point atomics are used: results are bit-identical from run
+ *    to run for the same inputs.
+ *  - Workspace: query its size with the matching *_workspace_size() call;
+ *    pass at least that many bytes, 256-byte aligned (NULL allowed when the
+ *    size is 0).  Its contents need not be initialised and are garbage after.
+ */
+#ifndef NAMOH_H_
+#define NAMOH_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum namoh_status {
+  NAMOH_OK = 0,
+  NAMOH_ERR_INVALID_ARG = 1,  /* NULL pointer, bad size, bad enum, misalignment */
+  NAMOH_ERR_UNSUPPORTED = 2,  /* valid request outside the supported set      */
+  NAMOH_ERR_WORKSPACE = 3,    /* workspace smaller than the size query        */
+  NAMOH_ERR_HIP = 4           /* a HIP runtime/launch error (e.g. no device)  */
+} namoh_status;
+
+typedef enum namoh_dtype { NAMOH_F32 = 0, NAMOH_BF16 = 1 } namoh_dtype;
+
+/* Gate definition.  SOFTMAX_SELECTED: g = softmax over the K selected logits
+ * (gates sum to one).  SOFTMAX_ALL: g_i = softmax over all H logits at the
+ * selected heads, not renormalised (Eq. namoh-gates as printed). */
+typedef enum namoh_gate_mode {
+  NAMOH_GATE_SOFTMAX_SELECTED = 0,
+  NAMOH_GATE_SOFTMAX_ALL = 1
+} namoh_gate_mode;
+
+/* Position used by RoPE.  HEAD_RELATIVE: the token's zero-based rank inside
+ * the head's routed subsequence (Eq. namoh-head-rope).  GLOBAL: the token's
+ * index t (Sec. 3.2, last sentence of the head-relative paragraph).  NONE:
+ * no rotation.  Rotation pairs element j with j + d/2, angle
+ * p * base^(-2j/d), V is never rotated. */
+typedef enum namoh_rope_mode {
+  NAMOH_ROPE_HEAD_RELATIVE = 0,
+  NAMOH_ROPE_GLOBAL = 1,
+  NAMOH_ROPE_NONE = 2
+} namoh_rope_mode;
+
+/* ------------------------------------------------------------------------
+ * Routing and dispatch (Sec. 3.1, Eq. namoh-gates and the definition of the
+ * ordered index sets I_i; Sec. 3.2 "Efficient execution": packing of each
+ * (batch, head) subsequence).
+ *
+ * In:  logits    float32 [B, T, H]   router logits (finite; NaN is outside
+ *                                    the contract).
+ * Out: topk_idx  int32 [B, T, K]     selected heads ordered by logit
+ *                                    descending, equal logits by head index
+ *                                    ascending (-0.0 equals +0.0).
+ *      gates     float32 [B, T, K]   gate of topk_idx[b,t,k] (gate_mode).
+ *      head_len  int32 [B, H]        n_i of every (b, h).
+ *      seg_offsets int32 [B*H + 1]   segment s = b*H + h occupies packed
+ *                                    positions [seg_offsets[s], seg_offsets[s+1]).
+ *      perm_token int32 [B*T*K]      packed position -> token t; tokens are
+ *                                    ascending inside a segment, so the rank
+ *                                    rho_h(t) = position - seg_offsets[s].
+ *      slot_pos  int32 [B, T, K]     packed position of (b, t, topk_idx[b,t,k]).
+ * All outputs are exact integers / deterministic floats.
+ * ---------------------------------------------------------------------- */
+size_t namoh_route_workspace_size(int B, int T, int H, int K);
+
+namoh_status namoh_route(const float* logits, int B, int T, int H, int K,
+                         int gate_mode, int32_t* topk_idx, float* gates,
+                         int32_t* head_len, int32_t* seg_offsets,
+                         int32_t* perm_token, int32_t* slot_pos,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Routed causal attention and gated combine (Sec. 3.1 Eq. namoh-attention,
+ * Sec. 3.2 Eq. namoh-head-rope).  Consumes namoh_route's outputs.
+ *
+ * In:  q, k, v     [B, H, T, d] of `dtype` (dense per head; only the rows of
+ *                  routed (t, h) pairs are read).
+ *      rope_base   > 0 unless rope_mode == NONE.
+ *      softmax_scale  <= 0 selects 1/sqrt(d).
+ *      gates, seg_offsets, perm_token, slot_pos: as produced by namoh_route.
+ * Out: out         [B, T, d] of `out_dtype`:
+ *                  o_t = sum_k gates[b,t,k] * h(t, topk_idx[b,t,k]).
+ *      head_out    optional float32 [B*T*K, d]: ungated head outputs h at
+ *                  their packed positions; NULL to skip.
+ * bf16 with d in {64, 128} runs on bf16 MFMA (float32 accumulation and
+ * softmax; rotated q/k and the probabilities are rounded to bf16 before
+ * their products); every other combination runs in float32 arithmetic.
+ * ---------------------------------------------------------------------- */
+size_t namoh_attn_fwd_workspace_size(int B, int T, int H, int K, int d_head,
+                                     int dtype);
+
+namoh_status namoh_attn_fwd(const void* q, const void* k, const void* v,
+                            int dtype, int B, int T, int H, int K, int d_head,
+                            float rope_base, int rope_mode, float softmax_scale,
+                            const float* gates, const int32_t* seg_offsets,
+                            const int32_t* perm_token, const int32_t* slot_pos,
+                            void* out, int out_dtype, float* head_out,
+                            void* workspace, size_t workspace_bytes,
+                            void* stream);
+
+/* ------------------------------------------------------------------------
+ * One decoding step for B sequences (Sec. 3.1: prefill and incremental
+ * decoding compute the same thing; Sec. 3.2: decoding launches only the
+ * active heads and reads/updates only their caches; Eq. namoh-kv-cost).
+ *
+ * In:  logits     float32 [B, H]     the new token's router logits.
+ *      q, k, v    [B, H, d] `dtype`  the new token's projections; only the
+ *                                    K selected heads are read.
+ *      k_cache, v_cache [B, H, cap, d] `dtype`: rows [0, cache_len[b,h]) hold
+ *                 head h's rotated keys / values in rank order.
+ *      cache_len  int32 [B, H]       in/out.
+ *      seq_pos    int32 [B]          the new token's global index; read only
+ *                                    when rope_mode == GLOBAL (else NULL ok).
+ * Out: topk_idx int32 [B, K], gates float32 [B, K], out [B, d] `out_dtype`.
+ *      For each selected head h with n = cache_len[b,h] < cap, the rotated
+ *      key (rank n) and the value are written to row n, cache_len becomes
+ *      n + 1, and the token attends to rows [0, n] (itself included).
+ *      If n == cap the append is skipped, *dev_status (if non-NULL) is set
+ *      to 1 and that head contributes nothing to out.  *dev_status is never
+ *      cleared by the library.
+ * ---------------------------------------------------------------------- */
+size_t namoh_decode_workspace_size(int B, int H, int K, int d_head, int cap);
+
+namoh_status namoh_decode_step(const float* logits, const void* q,
+                               const void* k, const void* v, int dtype,
+                               void* k_cache, void* v_cache, int32_t* cache_len,
+                               const int32_t* seq_pos, int B, int H, int K,
+                               int d_head, int cap, float rope_base,
+                               int rope_mode, int gate_mode,
+                               float softmax_scale, int32_t* topk_idx,
+                               float* gates, void* out, int out_dtype,
+                               int32_t* dev_status, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Diagnostics (not part of the layer's computation).  Opt-in timing of the
+ * dominant kernels with HIP events recorded on the call's stream: sections
+ * "attn" (routed attention kernel), "pack" (key/value packing), "combine",
+ * "decode_attn" (decode history attention).  namoh_profile_enable(n) keeps
+ * up to n launches per section (n = 0 stops and clears); it creates HIP
+ * events, so it allocates.  namoh_profile_read waits for the recorded events
+ * and returns the summed milliseconds and the launch count; it returns -1 for
+ * a section that was never timed.  Not for concurrent use from several host
+ * threads.
+ * ---------------------------------------------------------------------- */
+int namoh_profile_enable(int capacity);
+int namoh_profile_read(const char* section, double* total_ms, int* count);
+
+/* Static description of a status code. */
+const char* namoh_status_string(int status);
+/* Thread-local detail of the last non-OK return on this thread ("" if none). */
+const char* namoh_last_error(void);
+/* Library version string. */
+const char* namoh_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NAMOH_H_ */

@@ -348,14 +348,15 @@ def decode_step(logits, q, k, v, cache_k, cache_v, cache_len, K, rope_base,
     ``cache_v(b, h, n)`` return rows [0, n) of the post-RoPE key / value
     cache of head h (float64 [n, d]); cache_len int [B,H].
 
-    Returns topk_idx [B,K], gates [B,K], out [B,d], the appended rotated
-    keys [B,K,d] and the updated lengths.  Only the selected heads' caches
-    are read."""
+    Returns topk_idx [B,K], gates [B,K], out [B,d], the ungated head outputs
+    [B,K,d], the appended rotated keys [B,K,d] and the updated lengths.  Only
+    the selected heads' caches are read."""
     B, H, d = q.shape
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     topk = select_heads(logits, K)
     g = route_gates(logits, topk, gate_mode)
     out = np.zeros((B, d))
+    heads = np.zeros((B, K, d))
     new_k = np.zeros((B, K, d))
     new_len = np.array(cache_len, dtype=np.int64, copy=True)
     for b in range(B):
@@ -372,11 +373,12 @@ def decode_step(logits, q, k, v, cache_k, cache_v, cache_len, K, rope_base,
             sc = (Kc @ qt) * scale
             w = np.exp(sc - sc.max())
             w /= w.sum()
-            out[b] += g[b, kk] * (w @ Vc)
+            heads[b, kk] = w @ Vc
+            out[b] += g[b, kk] * heads[b, kk]
             new_k[b, kk] = kt
             new_len[b, h] = n + 1
-    return {"topk_idx": topk, "gates": g, "out": out, "new_k": new_k,
-            "cache_len": new_len}
+    return {"topk_idx": topk, "gates": g, "out": out, "head_out": heads,
+            "new_k": new_k, "cache_len": new_len}
 
 
 # ----------------------------------------------------------------------------

@@ -1,0 +1,243 @@
+"""ctypes binding of libnamoh.so (C ABI declared in include/namoh.h).
+
+Only argument marshalling happens here: torch supplies device memory (outputs
+and workspace are ``torch.empty`` on the inputs' device) and the current
+stream; every step of the layer runs in the library's HIP kernels.  There is
+no fallback: if the library is missing or a call fails, an exception is
+raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libnamoh.so")
+
+NAMOH_OK = 0
+NAMOH_ERR_INVALID_ARG = 1
+NAMOH_ERR_UNSUPPORTED = 2
+NAMOH_ERR_WORKSPACE = 3
+NAMOH_ERR_HIP = 4
+
+F32, BF16 = 0, 1
+GATE_SOFTMAX_SELECTED, GATE_SOFTMAX_ALL = 0, 1
+ROPE_HEAD_RELATIVE, ROPE_GLOBAL, ROPE_NONE = 0, 1, 2
+
+EXPORTED = (
+    "namoh_route_workspace_size", "namoh_route",
+    "namoh_attn_fwd_workspace_size", "namoh_attn_fwd",
+    "namoh_decode_workspace_size", "namoh_decode_step",
+    "namoh_status_string", "namoh_last_error", "namoh_version",
+    "namoh_profile_enable", "namoh_profile_read",
+)
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_F = ctypes.c_float
+_S = ctypes.c_size_t
+
+_SIGS = {
+    "namoh_route_workspace_size": (_S, [_I, _I, _I, _I]),
+    "namoh_route": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+    "namoh_attn_fwd_workspace_size": (_S, [_I, _I, _I, _I, _I, _I]),
+    "namoh_attn_fwd": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F,
+                            _P, _P, _P, _P, _P, _I, _P, _P, _S, _P]),
+    "namoh_decode_workspace_size": (_S, [_I, _I, _I, _I, _I]),
+    "namoh_decode_step": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I,
+                               _F, _I, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
+    "namoh_status_string": (ctypes.c_char_p, [_I]),
+    "namoh_last_error": (ctypes.c_char_p, []),
+    "namoh_version": (ctypes.c_char_p, []),
+    "namoh_profile_enable": (_I, [_I]),
+    "namoh_profile_read": (_I, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                ctypes.POINTER(ctypes.c_int)]),
+}
+
+_lib = None
+
+
+class NamohError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} [{status_string(status)}]")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load the HIP library (built in-tree by ``build()``); raise if absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                              "(python -m paper_2609_38832_amd.build)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def status_string(s: int) -> str:
+    return lib().namoh_status_string(int(s)).decode()
+
+
+def last_error() -> str:
+    return lib().namoh_last_error().decode()
+
+
+def check(status: int) -> None:
+    if status != NAMOH_OK:
+        raise NamohError(status, last_error())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.float32:
+        return F32
+    if dt == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {dt}")
+
+
+def torch_dtype(code: int) -> torch.dtype:
+    return torch.float32 if code == F32 else torch.bfloat16
+
+
+def workspace(nbytes: int, device) -> torch.Tensor:
+    """A device byte buffer whose data pointer is 256-byte aligned.  The
+    returned tensor is a view starting at the aligned address."""
+    raw = torch.empty(max(int(nbytes), 1) + 256, dtype=torch.uint8, device=device)
+    off = (-raw.data_ptr()) % 256
+    return raw[off:off + max(int(nbytes), 1)]
+
+
+def _need_cuda(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("tensors must live on the GPU")
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+
+
+# ----------------------------------------------------------------------------
+def route_workspace_size(B, T, H, K) -> int:
+    return int(lib().namoh_route_workspace_size(B, T, H, K))
+
+
+def route(logits: torch.Tensor, K: int, gate_mode: int = GATE_SOFTMAX_SELECTED,
+          out: Optional[dict] = None, ws: Optional[torch.Tensor] = None) -> dict:
+    """namoh_route on float32 logits [B, T, H]."""
+    _need_cuda(logits)
+    if logits.dtype != torch.float32 or logits.dim() != 3:
+        raise ValueError("logits must be float32 [B, T, H]")
+    B, T, H = logits.shape
+    dev = logits.device
+    if out is None:
+        i32 = dict(dtype=torch.int32, device=dev)
+        out = {
+            "topk_idx": torch.empty(B, T, K, **i32),
+            "gates": torch.empty(B, T, K, dtype=torch.float32, device=dev),
+            "head_len": torch.empty(B, H, **i32),
+            "seg_offsets": torch.empty(B * H + 1, **i32),
+            "perm_token": torch.empty(B * T * K, **i32),
+            "slot_pos": torch.empty(B, T, K, **i32),
+        }
+    nbytes = route_workspace_size(B, T, H, K)
+    if ws is None:
+        ws = workspace(nbytes, dev)
+    check(lib().namoh_route(_ptr(logits), B, T, H, K, gate_mode,
+                            _ptr(out["topk_idx"]), _ptr(out["gates"]), _ptr(out["head_len"]),
+                            _ptr(out["seg_offsets"]), _ptr(out["perm_token"]),
+                            _ptr(out["slot_pos"]), _ptr(ws), ws.numel(), _stream(dev)))
+    return out
+
+
+def attn_workspace_size(B, T, H, K, d, dtype_c) -> int:
+    return int(lib().namoh_attn_fwd_workspace_size(B, T, H, K, d, dtype_c))
+
+
+def attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K: int,
+             rope_base: float, rope_mode: int = ROPE_HEAD_RELATIVE,
+             softmax_scale: float = 0.0, out_dtype: Optional[torch.dtype] = None,
+             head_out: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+             ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """namoh_attn_fwd on dense q/k/v [B, H, T, d]; returns out [B, T, d]."""
+    _need_cuda(q, k, v, head_out, out)
+    B, H, T, d = q.shape
+    if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
+        raise ValueError("q, k, v must share shape and dtype")
+    dt = dtype_code(q.dtype)
+    odt = q.dtype if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty(B, T, d, dtype=odt, device=q.device)
+    if ws is None:
+        ws = workspace(attn_workspace_size(B, T, H, K, d, dt), q.device)
+    check(lib().namoh_attn_fwd(_ptr(q), _ptr(k), _ptr(v), dt, B, T, H, K, d,
+                               float(rope_base), rope_mode, float(softmax_scale),
+                               _ptr(routing["gates"]), _ptr(routing["seg_offsets"]),
+                               _ptr(routing["perm_token"]), _ptr(routing["slot_pos"]),
+                               _ptr(out), dtype_code(out.dtype), _ptr(head_out),
+                               _ptr(ws), ws.numel(), _stream(q.device)))
+    return out
+
+
+def decode_workspace_size(B, H, K, d, cap) -> int:
+    return int(lib().namoh_decode_workspace_size(B, H, K, d, cap))
+
+
+def decode_step(logits: torch.Tensor, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                k_cache: torch.Tensor, v_cache: torch.Tensor, cache_len: torch.Tensor,
+                K: int, rope_base: float, rope_mode: int = ROPE_HEAD_RELATIVE,
+                gate_mode: int = GATE_SOFTMAX_SELECTED, softmax_scale: float = 0.0,
+                seq_pos: Optional[torch.Tensor] = None,
+                out_dtype: Optional[torch.dtype] = None,
+                dev_status: Optional[torch.Tensor] = None,
+                out: Optional[dict] = None, ws: Optional[torch.Tensor] = None) -> dict:
+    """namoh_decode_step; caches [B, H, cap, d] are updated in place."""
+    _need_cuda(logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, dev_status)
+    B, H, d = q.shape
+    cap = k_cache.shape[2]
+    dt = dtype_code(q.dtype)
+    dev = q.device
+    if out is None:
+        out = {
+            "topk_idx": torch.empty(B, K, dtype=torch.int32, device=dev),
+            "gates": torch.empty(B, K, dtype=torch.float32, device=dev),
+            "out": torch.empty(B, d, dtype=q.dtype if out_dtype is None else out_dtype, device=dev),
+        }
+    if ws is None:
+        ws = workspace(decode_workspace_size(B, H, K, d, cap), dev)
+    check(lib().namoh_decode_step(_ptr(logits), _ptr(q), _ptr(k), _ptr(v), dt,
+                                  _ptr(k_cache), _ptr(v_cache), _ptr(cache_len), _ptr(seq_pos),
+                                  B, H, K, d, cap, float(rope_base), rope_mode, gate_mode,
+                                  float(softmax_scale), _ptr(out["topk_idx"]), _ptr(out["gates"]),
+                                  _ptr(out["out"]), dtype_code(out["out"].dtype),
+                                  _ptr(dev_status), _ptr(ws), ws.numel(), _stream(dev)))
+    return out
+
+
+# ----------------------------------------------------------------------------
+def profile_enable(capacity: int) -> None:
+    """Start (capacity > 0) or stop (0) event timing of the main kernels."""
+    lib().namoh_profile_enable(int(capacity))
+
+
+def profile_read(section: str):
+    """(total milliseconds, launch count) of a timed section, or None."""
+    ms = ctypes.c_double()
+    n = ctypes.c_int()
+    if lib().namoh_profile_read(section.encode(), ctypes.byref(ms), ctypes.byref(n)) != 0:
+        return None
+    return ms.value, n.value

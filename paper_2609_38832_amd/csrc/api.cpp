@@ -1,0 +1,228 @@
+// C ABI of libnamoh: host-side validation, workspace checks, dispatch.
+// Every argument is checked before anything is enqueued, so a call that
+// returns an error has launched nothing.  The semantics of each call are
+// documented in include/namoh.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/namoh.h"
+#include "internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+namoh_status fail(namoh_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+namoh_status ok() {
+  g_err[0] = '\0';
+  return NAMOH_OK;
+}
+
+bool aligned(const void* p, size_t a) {
+  return (reinterpret_cast<uintptr_t>(p) % a) == 0;
+}
+
+#define REQUIRE(cond, ...)                                   \
+  do {                                                       \
+    if (!(cond)) return fail(NAMOH_ERR_INVALID_ARG, __VA_ARGS__); \
+  } while (0)
+
+#define REQUIRE_PTR(p, a)                                                      \
+  do {                                                                         \
+    if ((p) == nullptr) return fail(NAMOH_ERR_INVALID_ARG, #p " is NULL");     \
+    if (!aligned((p), (a)))                                                    \
+      return fail(NAMOH_ERR_INVALID_ARG, #p " is not %d-byte aligned", (int)(a)); \
+  } while (0)
+
+namoh_status check_sizes(int B, int T, int H, int K) {
+  REQUIRE(B >= 1, "B must be >= 1 (got %d)", B);
+  REQUIRE(T >= 1, "T must be >= 1 (got %d)", T);
+  REQUIRE(H >= 1 && H <= 64, "H must be in [1, 64] (got %d)", H);
+  REQUIRE(K >= 1 && K <= H, "K must be in [1, H] (got K=%d, H=%d)", K, H);
+  const long long nr = static_cast<long long>(B) * T * K;
+  REQUIRE(nr < (1ll << 31), "B*T*K must be < 2^31 (got %lld)", nr);
+  return NAMOH_OK;
+}
+
+namoh_status check_head_width(int d) {
+  if (d != 32 && d != 64 && d != 128)
+    return fail(NAMOH_ERR_UNSUPPORTED, "d_head must be 32, 64 or 128 (got %d)", d);
+  return NAMOH_OK;
+}
+
+namoh_status check_workspace(void* ws, size_t have, size_t need) {
+  if (need == 0) return NAMOH_OK;
+  if (ws == nullptr) return fail(NAMOH_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
+  if (!aligned(ws, 256)) return fail(NAMOH_ERR_INVALID_ARG, "workspace is not 256-byte aligned");
+  if (have < need)
+    return fail(NAMOH_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", have, need);
+  return NAMOH_OK;
+}
+
+namoh_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return ok();
+  return fail(NAMOH_ERR_HIP, "HIP error %d: %s", static_cast<int>(e), hipGetErrorString(e));
+}
+
+// Clears a sticky error left by an earlier unrelated call so that the
+// launches below report their own status.
+void clear_hip_error() { (void)hipGetLastError(); }
+
+}  // namespace
+
+extern "C" {
+
+const char* namoh_status_string(int s) {
+  switch (s) {
+    case NAMOH_OK: return "NAMOH_OK";
+    case NAMOH_ERR_INVALID_ARG: return "NAMOH_ERR_INVALID_ARG";
+    case NAMOH_ERR_UNSUPPORTED: return "NAMOH_ERR_UNSUPPORTED";
+    case NAMOH_ERR_WORKSPACE: return "NAMOH_ERR_WORKSPACE";
+    case NAMOH_ERR_HIP: return "NAMOH_ERR_HIP";
+    default: return "NAMOH_UNKNOWN_STATUS";
+  }
+}
+
+const char* namoh_last_error(void) { return g_err; }
+
+const char* namoh_version(void) { return "namoh-gfx950 0.1"; }
+
+size_t namoh_route_workspace_size(int B, int T, int H, int K) {
+  if (check_sizes(B, T, H, K) != NAMOH_OK) return 0;
+  return namoh::route_workspace_bytes(B, T, H, K);
+}
+
+namoh_status namoh_route(const float* logits, int B, int T, int H, int K,
+                         int gate_mode, int32_t* topk_idx, float* gates,
+                         int32_t* head_len, int32_t* seg_offsets,
+                         int32_t* perm_token, int32_t* slot_pos,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  namoh_status s;
+  if ((s = check_sizes(B, T, H, K)) != NAMOH_OK) return s;
+  REQUIRE(gate_mode == NAMOH_GATE_SOFTMAX_SELECTED || gate_mode == NAMOH_GATE_SOFTMAX_ALL,
+          "unknown gate_mode %d", gate_mode);
+  REQUIRE_PTR(logits, 4);
+  REQUIRE_PTR(topk_idx, 4);
+  REQUIRE_PTR(gates, 4);
+  REQUIRE_PTR(head_len, 4);
+  REQUIRE_PTR(seg_offsets, 4);
+  REQUIRE_PTR(perm_token, 4);
+  REQUIRE_PTR(slot_pos, 4);
+  if ((s = check_workspace(workspace, workspace_bytes,
+                           namoh::route_workspace_bytes(B, T, H, K))) != NAMOH_OK)
+    return s;
+  clear_hip_error();
+  return hip_status(namoh::launch_route(logits, B, T, H, K, gate_mode, topk_idx, gates,
+                                        head_len, seg_offsets, perm_token, slot_pos,
+                                        workspace, static_cast<hipStream_t>(stream)));
+}
+
+size_t namoh_attn_fwd_workspace_size(int B, int T, int H, int K, int d_head, int dtype) {
+  if (check_sizes(B, T, H, K) != NAMOH_OK || check_head_width(d_head) != NAMOH_OK) return 0;
+  if (dtype != NAMOH_F32 && dtype != NAMOH_BF16) return 0;
+  return namoh::attn_workspace_bytes(B, T, H, K, d_head, dtype);
+}
+
+namoh_status namoh_attn_fwd(const void* q, const void* k, const void* v, int dtype,
+                            int B, int T, int H, int K, int d_head, float rope_base,
+                            int rope_mode, float softmax_scale, const float* gates,
+                            const int32_t* seg_offsets, const int32_t* perm_token,
+                            const int32_t* slot_pos, void* out, int out_dtype,
+                            float* head_out, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  namoh_status s;
+  if ((s = check_sizes(B, T, H, K)) != NAMOH_OK) return s;
+  if ((s = check_head_width(d_head)) != NAMOH_OK) return s;
+  REQUIRE(dtype == NAMOH_F32 || dtype == NAMOH_BF16, "unknown dtype %d", dtype);
+  REQUIRE(out_dtype == NAMOH_F32 || out_dtype == NAMOH_BF16, "unknown out_dtype %d", out_dtype);
+  REQUIRE(rope_mode == NAMOH_ROPE_HEAD_RELATIVE || rope_mode == NAMOH_ROPE_GLOBAL ||
+              rope_mode == NAMOH_ROPE_NONE,
+          "unknown rope_mode %d", rope_mode);
+  REQUIRE(rope_mode == NAMOH_ROPE_NONE || (std::isfinite(rope_base) && rope_base > 0.f),
+          "rope_base must be finite and > 0 (got %g)", static_cast<double>(rope_base));
+  REQUIRE(!std::isnan(softmax_scale) && !std::isinf(softmax_scale), "softmax_scale must be finite");
+  const long long dense = static_cast<long long>(B) * H * T * d_head;
+  REQUIRE(dense < (1ll << 40), "q/k/v too large");
+  REQUIRE_PTR(q, 16);
+  REQUIRE_PTR(k, 16);
+  REQUIRE_PTR(v, 16);
+  REQUIRE_PTR(gates, 4);
+  REQUIRE_PTR(seg_offsets, 4);
+  REQUIRE_PTR(perm_token, 4);
+  REQUIRE_PTR(slot_pos, 4);
+  REQUIRE_PTR(out, 16);
+  if (head_out != nullptr) REQUIRE_PTR(head_out, 16);
+  if ((s = check_workspace(workspace, workspace_bytes,
+                           namoh::attn_workspace_bytes(B, T, H, K, d_head, dtype))) != NAMOH_OK)
+    return s;
+  const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
+  clear_hip_error();
+  return hip_status(namoh::launch_attn(q, k, v, dtype, B, T, H, K, d_head, rope_base, rope_mode,
+                                       scale, gates, seg_offsets, perm_token, slot_pos, out,
+                                       out_dtype, head_out, workspace,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+size_t namoh_decode_workspace_size(int B, int H, int K, int d_head, int cap) {
+  if (check_sizes(B, 1, H, K) != NAMOH_OK || check_head_width(d_head) != NAMOH_OK || cap < 1)
+    return 0;
+  return namoh::decode_workspace_bytes(B, H, K, d_head, cap);
+}
+
+namoh_status namoh_decode_step(const float* logits, const void* q, const void* k,
+                               const void* v, int dtype, void* k_cache, void* v_cache,
+                               int32_t* cache_len, const int32_t* seq_pos, int B, int H,
+                               int K, int d_head, int cap, float rope_base, int rope_mode,
+                               int gate_mode, float softmax_scale, int32_t* topk_idx,
+                               float* gates, void* out, int out_dtype, int32_t* dev_status,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  namoh_status s;
+  if ((s = check_sizes(B, 1, H, K)) != NAMOH_OK) return s;
+  if ((s = check_head_width(d_head)) != NAMOH_OK) return s;
+  REQUIRE(cap >= 1, "cap must be >= 1 (got %d)", cap);
+  REQUIRE(dtype == NAMOH_F32 || dtype == NAMOH_BF16, "unknown dtype %d", dtype);
+  REQUIRE(out_dtype == NAMOH_F32 || out_dtype == NAMOH_BF16, "unknown out_dtype %d", out_dtype);
+  REQUIRE(gate_mode == NAMOH_GATE_SOFTMAX_SELECTED || gate_mode == NAMOH_GATE_SOFTMAX_ALL,
+          "unknown gate_mode %d", gate_mode);
+  REQUIRE(rope_mode == NAMOH_ROPE_HEAD_RELATIVE || rope_mode == NAMOH_ROPE_GLOBAL ||
+              rope_mode == NAMOH_ROPE_NONE,
+          "unknown rope_mode %d", rope_mode);
+  REQUIRE(rope_mode == NAMOH_ROPE_NONE || (std::isfinite(rope_base) && rope_base > 0.f),
+          "rope_base must be finite and > 0 (got %g)", static_cast<double>(rope_base));
+  REQUIRE(!std::isnan(softmax_scale) && !std::isinf(softmax_scale), "softmax_scale must be finite");
+  REQUIRE_PTR(logits, 4);
+  REQUIRE_PTR(q, 16);
+  REQUIRE_PTR(k, 16);
+  REQUIRE_PTR(v, 16);
+  REQUIRE_PTR(k_cache, 16);
+  REQUIRE_PTR(v_cache, 16);
+  REQUIRE_PTR(cache_len, 4);
+  if (rope_mode == NAMOH_ROPE_GLOBAL) REQUIRE_PTR(seq_pos, 4);
+  REQUIRE_PTR(topk_idx, 4);
+  REQUIRE_PTR(gates, 4);
+  REQUIRE_PTR(out, 16);
+  if (dev_status != nullptr) REQUIRE_PTR(dev_status, 4);
+  if ((s = check_workspace(workspace, workspace_bytes,
+                           namoh::decode_workspace_bytes(B, H, K, d_head, cap))) != NAMOH_OK)
+    return s;
+  const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
+  clear_hip_error();
+  return hip_status(namoh::launch_decode(logits, q, k, v, dtype, k_cache, v_cache, cache_len,
+                                         seq_pos, B, H, K, d_head, cap, rope_base, rope_mode,
+                                         gate_mode, scale, topk_idx, gates, out, out_dtype,
+                                         dev_status, workspace, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

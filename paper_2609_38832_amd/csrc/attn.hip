@@ -1,0 +1,758 @@
+// Routed causal attention over the packed per-head subsequences, and the gated
+// combine back to token order.
+//
+// Sec. 3.1 Eq. namoh-attention: the routed query (t, i) attends to the keys and
+// values of tokens s <= t routed to the same head i.  Sec. 3.2
+// Eq. namoh-head-rope: RoPE at the rank inside the head's subsequence.
+// Sec. 3.2 "Efficient execution": every (batch, head) subsequence is an
+// independent causal sequence; query tiles with large and small causal work
+// are interleaved across compute units.
+//
+// Launch sequence for one call:
+//   k_attn_prep   one workgroup: per segment key-tile counts and their
+//                 running sum (tile_off), the work list of (segment, query
+//                 block) items sorted by causal work, heaviest first (counting
+//                 sort by key-tile count), the RoPE table length.
+//   k_rope_table  cos/sin of p * base^(-2j/d), angles in double, stored f32.
+//   bf16, d in {64, 128}:
+//     k_pack_kv   gathers each 64-row key tile of a segment by perm_token,
+//                 applies RoPE at the key's rank while loading it, rounds to
+//                 bf16 (packed row-major), and writes the values as a
+//                 transposed d x 64 tile (the operand layout of the P.V
+//                 product).  The packed rotated keys / values are what a
+//                 prefill hands to the per-head decode caches.
+//     k_attn_mfma one workgroup per work item: the query block is gathered
+//                 and rotated into registers once; key/value tiles are
+//                 double-buffered through LDS; S^T = K Q^T and O^T += V^T P^T
+//                 run on v_mfma_f32_32x32x16_bf16 with fp32 accumulation and
+//                 an fp32 online softmax (exp2).
+//   other dtype / width:
+//     k_attn_generic  fp32 arithmetic, one lane per query, keys gathered and
+//                 rotated while staging each tile.
+//   k_combine     o_t = sum_k gate(t,k) * h[slot_pos(t,k)] in k order.
+#include <cmath>
+
+#include "common.h"
+#include "internal.h"
+
+namespace namoh {
+
+constexpr int kBN = 64;            // keys per tile
+constexpr int kPrepThreads = 1024;
+constexpr int kSortBins = 4096;    // work keys are clamped to this many bins
+
+// mfma kernel shape: waves per workgroup and 32-query sub-tiles per wave
+template <int D> struct MfmaShape;
+template <> struct MfmaShape<64> { static constexpr int NW = 4, NQT = 2; };
+template <> struct MfmaShape<128> { static constexpr int NW = 4, NQT = 2; };
+constexpr int kGenericBM = 64;
+
+enum Meta { kMetaItems = 0, kMetaTiles = 1, kMetaTablePos = 2, kMetaBad = 3, kMetaCount = 4 };
+
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kPrepThreads) void k_attn_prep(
+    const int32_t* __restrict__ seg_offsets, int BH, int T, int BM,
+    int rope_mode, int Nr, int max_items, int32_t* __restrict__ tile_off,
+    int2* __restrict__ items, int32_t* __restrict__ meta) {
+  __shared__ int s_hist[kSortBins];
+  __shared__ int s_wave[kPrepThreads / kWave + 1];
+  __shared__ int s_maxn;
+  __shared__ int s_bad;
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kSortBins; i += kPrepThreads) s_hist[i] = 0;
+  if (tid == 0) {
+    s_maxn = 0;
+    s_bad = seg_offsets[0] != 0 || seg_offsets[BH] != Nr;
+  }
+  __syncthreads();
+  // offsets that are not a valid packing of Nr rows disable the call: every
+  // later kernel then sees zero items and zero tiles.
+  for (int s = tid; s < BH; s += kPrepThreads)
+    if (seg_offsets[s + 1] < seg_offsets[s] || seg_offsets[s + 1] - seg_offsets[s] > T) s_bad = 1;
+  __syncthreads();
+  if (s_bad) {
+    if (tid == 0) {
+      meta[kMetaItems] = 0;
+      meta[kMetaTiles] = 0;
+      meta[kMetaTablePos] = 0;
+      meta[kMetaBad] = 1;
+    }
+    return;
+  }
+
+  // key-tile running sum, longest segment, histogram of item work
+  int carry = 0;
+  for (int start = 0; start < BH; start += kPrepThreads) {
+    const int s = start + tid;
+    const int n = s < BH ? seg_offsets[s + 1] - seg_offsets[s] : 0;
+    const int tiles = (n + kBN - 1) / kBN;
+    if (n > 0) atomicMax(&s_maxn, n);
+    const int nqb = (n + BM - 1) / BM;
+    for (int qb = 0; qb < nqb; ++qb) {
+      const int w = min(tiles, (qb + 1) * BM / kBN);
+      atomicAdd(&s_hist[kSortBins - 1 - min(w, kSortBins - 1)], 1);
+    }
+    int total;
+    const int ex = block_exclusive_scan<kPrepThreads>(tiles, s_wave, total);
+    if (s < BH) tile_off[s] = carry + ex;
+    carry += total;
+  }
+  if (tid == 0) {
+    tile_off[BH] = carry;
+    meta[kMetaBad] = 0;
+    meta[kMetaTiles] = carry;
+    meta[kMetaTablePos] = rope_mode == 0 ? s_maxn : (rope_mode == 1 ? T : 0);
+  }
+  // exclusive scan of the histogram -> insertion cursors (heaviest first)
+  constexpr int PER = kSortBins / kPrepThreads;
+  int h[PER];
+  int sum = 0;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    h[i] = s_hist[tid * PER + i];
+    sum += h[i];
+  }
+  int total;
+  int run = block_exclusive_scan<kPrepThreads>(sum, s_wave, total);
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    s_hist[tid * PER + i] = run;
+    run += h[i];
+  }
+  if (tid == 0) meta[kMetaItems] = min(total, max_items);
+  __syncthreads();
+  for (int s = tid; s < BH; s += kPrepThreads) {
+    const int n = seg_offsets[s + 1] - seg_offsets[s];
+    const int tiles = (n + kBN - 1) / kBN;
+    const int nqb = (n + BM - 1) / BM;
+    for (int qb = 0; qb < nqb; ++qb) {
+      const int w = min(tiles, (qb + 1) * BM / kBN);
+      const int pos = atomicAdd(&s_hist[kSortBins - 1 - min(w, kSortBins - 1)], 1);
+      if (pos < max_items) items[pos] = make_int2(s, qb);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// table[p * (d/2) + j] = (cos, sin)(p * base^(-2j/d)), p < meta[kMetaTablePos]
+__global__ __launch_bounds__(256) void k_rope_table(
+    const int32_t* __restrict__ meta, int d, double log_base,
+    float2* __restrict__ table) {
+  const int half = d / 2;
+  const size_t total = static_cast<size_t>(meta[kMetaTablePos]) * half;
+  for (size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+       i < total; i += static_cast<size_t>(gridDim.x) * blockDim.x) {
+    const int p = static_cast<int>(i / half);
+    const int j = static_cast<int>(i - static_cast<size_t>(p) * half);
+    const double theta = exp(-(2.0 * j / d) * log_base);
+    double sn, cs;
+    sincos(static_cast<double>(p) * theta, &sn, &cs);
+    table[i] = make_float2(static_cast<float>(cs), static_cast<float>(sn));
+  }
+}
+
+// ---------------------------------------------------------------------------
+NAMOH_DEV int find_segment(const int32_t* __restrict__ tile_off, int BH, int gt) {
+  int lo = 0, hi = BH;  // tile_off[lo] <= gt < tile_off[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (tile_off[mid] <= gt) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+NAMOH_DEV void unpack8(const uint4 x, float* f) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    f[2 * e] = lo_bf16(w[e]);
+    f[2 * e + 1] = hi_bf16(w[e]);
+  }
+}
+
+NAMOH_DEV uint4 pack8(const float* f) {
+  return make_uint4(pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]),
+                    pack_bf16x2(f[4], f[5]), pack_bf16x2(f[6], f[7]));
+}
+
+// Rotate the pair (x1[e], x2[e]) = (elements j, j + d/2) for 8 consecutive j
+// starting at j0, with cs = table row of the position.
+NAMOH_DEV void rope8(float* x1, float* x2, const float2* __restrict__ cs) {
+  const float4* c4 = reinterpret_cast<const float4*>(cs);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float4 w = c4[e];  // (cos, sin) of j0+2e, then of j0+2e+1
+    const float a0 = x1[2 * e], b0 = x2[2 * e];
+    const float a1 = x1[2 * e + 1], b1 = x2[2 * e + 1];
+    x1[2 * e] = a0 * w.x - b0 * w.y;
+    x2[2 * e] = b0 * w.x + a0 * w.y;
+    x1[2 * e + 1] = a1 * w.z - b1 * w.w;
+    x2[2 * e + 1] = b1 * w.z + a1 * w.w;
+  }
+}
+
+// Position of key `p16` within a 16-key group of the transposed value tile:
+// bits 2 and 3 swapped (see k_attn_mfma, P.V operand order).
+NAMOH_DEV int vt_key_of_pos(int p) {
+  return (p & ~12) | ((p & 4) << 1) | ((p & 8) >> 1);
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void k_pack_kv(
+    const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    const float2* __restrict__ table, const int32_t* __restrict__ seg_offsets,
+    const int32_t* __restrict__ tile_off, const int32_t* __restrict__ perm_token,
+    const int32_t* __restrict__ meta, int BH, int T, int H, int rope_mode,
+    uint16_t* __restrict__ Kp, uint16_t* __restrict__ Vt) {
+  __shared__ __attribute__((aligned(16))) uint16_t sv[kBN][D + 8];
+  const int gt = blockIdx.x;
+  if (gt >= meta[kMetaTiles]) return;
+  const int s = find_segment(tile_off, BH, gt);
+  const int r0 = (gt - tile_off[s]) * kBN;
+  const int b = s / H, h = s - (s / H) * H;
+  const int seg0 = seg_offsets[s];
+  const int n = seg_offsets[s + 1] - seg0;
+  const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
+  const int tid = threadIdx.x;
+
+  constexpr int HP = D / 16;  // 8-element granule pairs (j, j + d/2) per row
+  for (int u = tid; u < kBN * HP; u += 256) {
+    const int row = u / HP, c = u - (u / HP) * HP;
+    const int r = r0 + row;
+    float x1[8], x2[8];
+    uint4 o1 = make_uint4(0, 0, 0, 0), o2 = o1;
+    if (r < n) {
+      const int t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
+      const uint16_t* src = k + (head_base + t) * D;
+      const uint4 a = *reinterpret_cast<const uint4*>(src + 8 * c);
+      const uint4 bb = *reinterpret_cast<const uint4*>(src + D / 2 + 8 * c);
+      if (rope_mode != 2) {
+        unpack8(a, x1);
+        unpack8(bb, x2);
+        const int pos = rope_mode == 0 ? r : t;
+        rope8(x1, x2, table + static_cast<size_t>(pos) * (D / 2) + 8 * c);
+        o1 = pack8(x1);
+        o2 = pack8(x2);
+      } else {
+        o1 = a;
+        o2 = bb;
+      }
+    }
+    uint16_t* dst = Kp + (static_cast<size_t>(gt) * kBN + row) * D;
+    *reinterpret_cast<uint4*>(dst + 8 * c) = o1;
+    *reinterpret_cast<uint4*>(dst + D / 2 + 8 * c) = o2;
+  }
+  constexpr int RG = D / 8;  // granules per value row
+  for (int u = tid; u < kBN * RG; u += 256) {
+    const int row = u / RG, gr = u - (u / RG) * RG;
+    const int r = r0 + row;
+    uint4 x = make_uint4(0, 0, 0, 0);
+    if (r < n) {
+      const int t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
+      x = *reinterpret_cast<const uint4*>(v + (head_base + t) * D + 8 * gr);
+    }
+    *reinterpret_cast<uint4*>(&sv[row][8 * gr]) = x;
+  }
+  __syncthreads();
+  for (int u = tid; u < D * (kBN / 8); u += 256) {
+    const int m = u / (kBN / 8), pg = u - (u / (kBN / 8)) * (kBN / 8);
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t lo = sv[vt_key_of_pos(8 * pg + 2 * e)][m];
+      const uint32_t hi = sv[vt_key_of_pos(8 * pg + 2 * e + 1)][m];
+      w[e] = lo | (hi << 16);
+    }
+    *reinterpret_cast<uint4*>(Vt + (static_cast<size_t>(gt) * D + m) * kBN + 8 * pg) =
+        make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+// Loads one packed key tile and one transposed value tile (KPT 16-byte
+// granules each per thread) into registers.
+template <int D, int KPT, int NT>
+NAMOH_DEV void tile_gload(const uint16_t* __restrict__ Kp, const uint16_t* __restrict__ Vt,
+                          int tile, int tid, u32x4 (&kreg)[KPT], u32x4 (&vreg)[KPT]) {
+  const u32x4* kp = reinterpret_cast<const u32x4*>(Kp + static_cast<size_t>(tile) * kBN * D);
+  const u32x4* vp = reinterpret_cast<const u32x4*>(Vt + static_cast<size_t>(tile) * D * kBN);
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    kreg[i] = kp[tid + i * NT];
+    vreg[i] = vp[tid + i * NT];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 MFMA flash attention over one (segment, query block) work item.
+//
+// v_mfma_f32_32x32x16_bf16 operand order used here (wave64, lane = 32*g + c):
+// A (32 x 16): lane holds row c, reduction slots 8g..8g+7; B (16 x 32): lane
+// holds column c, the same reduction slots; C (32 x 32): lane holds column c,
+// rows 8j + 4g + i in accumulator 4j + i.  The kernel computes the transposed
+// scores S^T = K Q^T (keys are rows), so every lane owns one query and 16 of
+// its keys per 32-key sub-tile: the softmax row reduction is in-lane plus one
+// exchange with lane c ^ 32.  The probabilities of a 16-key reduction step
+// are accumulators 8s..8s+7, i.e. keys 8a + 4g + i (a = 0, 1); the
+// transposed value tile stores, inside each 16-key group, key 8a + 4g + i at
+// position 8g + 4a + i, so one 16-byte LDS read gives the matching A operand.
+template <int D, int NQT, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void k_attn_mfma(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kp,
+    const uint16_t* __restrict__ Vt, const float2* __restrict__ table,
+    const int32_t* __restrict__ seg_offsets, const int32_t* __restrict__ tile_off,
+    const int32_t* __restrict__ perm_token, const int2* __restrict__ items,
+    const int32_t* __restrict__ meta, int T, int H, int rope_mode,
+    float scale_log2, float* __restrict__ hout) {
+  constexpr int BM = 32 * NQT * NW;
+  constexpr int KS = D / 16;  // reduction steps of S^T = K Q^T
+  constexpr int MT = D / 32;  // 32-row tiles of O^T
+  constexpr int NT = NW * 64;
+  constexpr int KPT = kBN * D / 8 / NT;  // 16-byte granules per thread per tile
+  static_assert(kBN * D / 8 % NT == 0, "tile/thread mismatch");
+
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[2][D * kBN];
+
+  if (static_cast<int>(blockIdx.x) >= meta[kMetaItems]) return;
+  const int2 it = items[blockIdx.x];
+  const int s = it.x;
+  const int q0 = it.y * BM;
+  const int b = s / H, h = s - (s / H) * H;
+  const int seg0 = seg_offsets[s];
+  const int n = seg_offsets[s + 1] - seg0;
+  const int tile0 = tile_off[s];
+  const int ntiles = (n + kBN - 1) / kBN;
+  const int kt_end = min(ntiles, (q0 + BM + kBN - 1) / kBN);
+  const int tid = threadIdx.x;
+  const int wave = tid / 64, lane = tid % 64;
+  const int c = lane & 31, g = lane >> 5;
+  const int wq_first = q0 + 32 * wave;
+  const int wq_last = q0 + 32 * ((NQT - 1) * NW + wave) + 31;
+  const int wave_tiles = min(ntiles, wq_last / kBN + 1);
+  const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
+
+  // ---- query block: gather, rotate, round to bf16 B operands -------------
+  bf16x8 qB[NQT][KS];
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt) {
+    const int r = q0 + 32 * (qt * NW + wave) + c;
+    const int rr = r < n ? r : n - 1;
+    const int t = min(static_cast<unsigned>(perm_token[seg0 + rr]), static_cast<unsigned>(T - 1));
+    const uint16_t* qrow = q + (head_base + t) * D;
+    const int pos = rope_mode == 0 ? rr : t;
+#pragma unroll
+    for (int s2 = 0; s2 < KS / 2; ++s2) {
+      float x1[8], x2[8];
+      unpack8(*reinterpret_cast<const uint4*>(qrow + 16 * s2 + 8 * g), x1);
+      unpack8(*reinterpret_cast<const uint4*>(qrow + D / 2 + 16 * s2 + 8 * g), x2);
+      if (rope_mode != 2)
+        rope8(x1, x2, table + static_cast<size_t>(pos) * (D / 2) + 16 * s2 + 8 * g);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        qB[qt][s2][e] = static_cast<__bf16>(r < n ? x1[e] : 0.f);
+        qB[qt][s2 + KS / 2][e] = static_cast<__bf16>(r < n ? x2[e] : 0.f);
+      }
+    }
+  }
+
+  f32x16 O[MT][NQT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) O[mt][qt][e] = 0.f;
+  float m_run[NQT], l_run[NQT];
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt) {
+    m_run[qt] = -1e30f;
+    l_run[qt] = 0.f;
+  }
+
+  u32x4 kreg[KPT], vreg[KPT];
+  if (kt_end > 0) tile_gload<D, KPT, NT>(Kp, Vt, tile0, tid, kreg, vreg);
+  for (int kt = 0; kt < kt_end; ++kt) {
+    const int buf = kt & 1;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int u = tid + i * NT;
+      const int row = u / (D / 8), gr = u % (D / 8);
+      *reinterpret_cast<u32x4*>(&sK[buf][row * D + ((gr ^ (row & 7)) * 8)]) = kreg[i];
+      const int m = u / (kBN / 8), gv = u % (kBN / 8);
+      *reinterpret_cast<u32x4*>(&sV[buf][m * kBN + ((gv ^ (m & 7)) * 8)]) = vreg[i];
+    }
+    __syncthreads();
+    if (kt + 1 < kt_end) tile_gload<D, KPT, NT>(Kp, Vt, tile0 + kt + 1, tid, kreg, vreg);
+    if (kt < wave_tiles) {
+      // ---- S^T = K Q^T --------------------------------------------------
+      f32x16 S[2][NQT];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) S[kk][qt][e] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          const int row = 32 * kk + c;
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+              &sK[buf][row * D + (((2 * ks + g) ^ (row & 7)) * 8)]);
+#pragma unroll
+          for (int qt = 0; qt < NQT; ++qt)
+            S[kk][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qB[qt][ks], S[kk][qt], 0, 0, 0);
+        }
+      }
+      // ---- causal / length mask ----------------------------------------
+      const int key0 = kt * kBN;
+      if (key0 + kBN - 1 > wq_first || key0 + kBN > n) {
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int qt = 0; qt < NQT; ++qt) {
+            const int qr = q0 + 32 * (qt * NW + wave) + c;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const int key = key0 + 32 * kk + 8 * j + 4 * g + i;
+                if (key > qr || key >= n) S[kk][qt][4 * j + i] = -INFINITY;
+              }
+          }
+      }
+      // ---- online softmax ----------------------------------------------
+      bf16x8 pB[NQT][4];
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) mx = fmaxf(mx, S[kk][qt][e]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mnew = fmaxf(m_run[qt], mx);
+        const float alpha = __builtin_amdgcn_exp2f((m_run[qt] - mnew) * scale_log2);
+        const float mc = mnew * scale_log2;
+        float ls = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const float p = __builtin_amdgcn_exp2f(fmaf(S[kk][qt][e], scale_log2, -mc));
+            S[kk][qt][e] = p;
+            ls += p;
+          }
+        l_run[qt] = l_run[qt] * alpha + ls;
+        m_run[qt] = mnew;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) O[mt][qt][e] *= alpha;
+#pragma unroll
+        for (int k2 = 0; k2 < 4; ++k2)
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            pB[qt][k2][e] = static_cast<__bf16>(S[k2 >> 1][qt][8 * (k2 & 1) + e]);
+      }
+      // ---- O^T += V^T P^T ------------------------------------------------
+#pragma unroll
+      for (int k2 = 0; k2 < 4; ++k2) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const int row = 32 * mt + c;
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+              &sV[buf][row * kBN + (((2 * k2 + g) ^ (row & 7)) * 8)]);
+#pragma unroll
+          for (int qt = 0; qt < NQT; ++qt)
+            O[mt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pB[qt][k2], O[mt][qt], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  // ---- epilogue: normalise and store the packed head outputs -----------
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt) {
+    const float lt = l_run[qt] + __shfl_xor(l_run[qt], 32);
+    const float inv = 1.f / lt;
+    const int r = q0 + 32 * (qt * NW + wave) + c;
+    if (r < n) {
+      float* orow = hout + static_cast<size_t>(seg0 + r) * D;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int d0 = 32 * mt + 8 * j + 4 * g;
+          *reinterpret_cast<float4*>(orow + d0) =
+              make_float4(O[mt][qt][4 * j] * inv, O[mt][qt][4 * j + 1] * inv,
+                          O[mt][qt][4 * j + 2] * inv, O[mt][qt][4 * j + 3] * inv);
+        }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32-arithmetic attention for every other dtype / head width: one lane per
+// query, keys gathered by perm_token and rotated while each tile is staged.
+template <int D, bool BF16>
+NAMOH_DEV void load_row(const void* base, size_t row, float* out) {
+  if constexpr (BF16) {
+    const uint4* p = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + row * D);
+#pragma unroll
+    for (int i = 0; i < D / 8; ++i) unpack8(p[i], out + 8 * i);
+  } else {
+    const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(base) + row * D);
+#pragma unroll
+    for (int i = 0; i < D / 4; ++i) {
+      const float4 x = p[i];
+      out[4 * i] = x.x; out[4 * i + 1] = x.y; out[4 * i + 2] = x.z; out[4 * i + 3] = x.w;
+    }
+  }
+}
+
+template <int D>
+NAMOH_DEV void rope_row(float* x, const float2* __restrict__ cs) {
+#pragma unroll
+  for (int j = 0; j < D / 2; ++j) {
+    const float2 w = cs[j];
+    const float a = x[j], bb = x[j + D / 2];
+    x[j] = a * w.x - bb * w.y;
+    x[j + D / 2] = bb * w.x + a * w.y;
+  }
+}
+
+template <int D, bool BF16>
+__global__ __launch_bounds__(64) void k_attn_generic(
+    const void* __restrict__ q, const void* __restrict__ k,
+    const void* __restrict__ v, const float2* __restrict__ table,
+    const int32_t* __restrict__ seg_offsets, const int32_t* __restrict__ perm_token,
+    const int2* __restrict__ items, const int32_t* __restrict__ meta, int T,
+    int H, int rope_mode, float scale, float* __restrict__ hout) {
+  __shared__ float sK[kBN][D + 1];
+  __shared__ float sV[kBN][D + 1];
+  if (static_cast<int>(blockIdx.x) >= meta[kMetaItems]) return;
+  const int2 it = items[blockIdx.x];
+  const int s = it.x;
+  const int q0 = it.y * kGenericBM;
+  const int b = s / H, h = s - (s / H) * H;
+  const int seg0 = seg_offsets[s];
+  const int n = seg_offsets[s + 1] - seg0;
+  const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
+  const int lane = threadIdx.x;
+  const int r = q0 + lane;
+
+  float qv[D], acc[D], row[D];
+  {
+    const int rr = r < n ? r : n - 1;
+    const int t = min(static_cast<unsigned>(perm_token[seg0 + rr]), static_cast<unsigned>(T - 1));
+    load_row<D, BF16>(q, head_base + t, qv);
+    if (rope_mode != 2)
+      rope_row<D>(qv, table + static_cast<size_t>(rope_mode == 0 ? rr : t) * (D / 2));
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      qv[d] *= scale;
+      acc[d] = 0.f;
+    }
+  }
+  float m = -INFINITY, l = 0.f;
+  const int ntiles = (n + kBN - 1) / kBN;
+  const int kt_end = min(ntiles, (q0 + kGenericBM - 1) / kBN + 1);
+  for (int kt = 0; kt < kt_end; ++kt) {
+    const int key = kt * kBN + lane;
+    if (key < n) {
+      const int t = min(static_cast<unsigned>(perm_token[seg0 + key]), static_cast<unsigned>(T - 1));
+      load_row<D, BF16>(k, head_base + t, row);
+      if (rope_mode != 2)
+        rope_row<D>(row, table + static_cast<size_t>(rope_mode == 0 ? key : t) * (D / 2));
+#pragma unroll
+      for (int d = 0; d < D; ++d) sK[lane][d] = row[d];
+      load_row<D, BF16>(v, head_base + t, row);
+#pragma unroll
+      for (int d = 0; d < D; ++d) sV[lane][d] = row[d];
+    }
+    __syncthreads();
+    const int jmax = min(min(kBN, n - kt * kBN), r - kt * kBN + 1);
+    for (int j = 0; j < kBN; ++j) {
+      float sc = 0.f;
+#pragma unroll
+      for (int d = 0; d < D; ++d) sc = fmaf(qv[d], sK[j][d], sc);
+      if (j < jmax) {
+        const float mn = fmaxf(m, sc);
+        const float corr = expf(m - mn);
+        const float p = expf(sc - mn);
+        l = l * corr + p;
+#pragma unroll
+        for (int d = 0; d < D; ++d) acc[d] = fmaf(p, sV[j][d], acc[d] * corr);
+        m = mn;
+      }
+    }
+    __syncthreads();
+  }
+  if (r < n) {
+    const float inv = 1.f / l;
+    float* orow = hout + static_cast<size_t>(seg0 + r) * D;
+#pragma unroll
+    for (int d = 0; d < D; d += 4)
+      *reinterpret_cast<float4*>(orow + d) =
+          make_float4(acc[d] * inv, acc[d + 1] * inv, acc[d + 2] * inv, acc[d + 3] * inv);
+  }
+}
+
+// ---------------------------------------------------------------------------
+template <bool OUT_BF16>
+__global__ __launch_bounds__(256) void k_combine(
+    const float* __restrict__ hout, const float* __restrict__ gates,
+    const int32_t* __restrict__ slot_pos, long BT, int K, int D, int Nr,
+    void* __restrict__ out) {
+  const int C = D / 4;
+  const long idx = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const long tok = idx / C;
+  const int cc = static_cast<int>(idx - tok * C);
+  if (tok >= BT) return;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int k = 0; k < K; ++k) {
+    const int p = slot_pos[tok * K + k];
+    if (static_cast<unsigned>(p) >= static_cast<unsigned>(Nr)) continue;
+    const float gk = gates[tok * K + k];
+    const float4 x = reinterpret_cast<const float4*>(hout)[static_cast<size_t>(p) * C + cc];
+    acc.x = fmaf(gk, x.x, acc.x);
+    acc.y = fmaf(gk, x.y, acc.y);
+    acc.z = fmaf(gk, x.z, acc.z);
+    acc.w = fmaf(gk, x.w, acc.w);
+  }
+  if constexpr (OUT_BF16) {
+    reinterpret_cast<uint2*>(out)[idx] =
+        make_uint2(pack_bf16x2(acc.x, acc.y), pack_bf16x2(acc.z, acc.w));
+  } else {
+    reinterpret_cast<float4*>(out)[idx] = acc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+static bool use_mfma(int d, int dtype) { return dtype == 1 && (d == 64 || d == 128); }
+
+static int block_queries(int d, int dtype) {
+  if (!use_mfma(d, dtype)) return kGenericBM;
+  return d == 64 ? 32 * MfmaShape<64>::NQT * MfmaShape<64>::NW
+                 : 32 * MfmaShape<128>::NQT * MfmaShape<128>::NW;
+}
+
+struct AttnWs {
+  int32_t* meta;
+  int32_t* tile_off;
+  int2* items;
+  float2* table;
+  uint16_t* Kp;
+  uint16_t* Vt;
+  float* hpack;
+  size_t bytes;
+  size_t max_items, max_tiles;
+};
+
+static AttnWs carve_attn(void* ws, int B, int T, int H, int K, int d, int dtype) {
+  const size_t BH = static_cast<size_t>(B) * H;
+  const size_t Nr = static_cast<size_t>(B) * T * K;
+  const int BM = block_queries(d, dtype);
+  AttnWs w;
+  w.max_items = Nr / BM + BH + 1;
+  w.max_tiles = Nr / kBN + BH + 1;
+  Carver cv(ws);
+  w.meta = cv.take<int32_t>(kMetaCount);
+  w.tile_off = cv.take<int32_t>(BH + 1);
+  w.items = cv.take<int2>(w.max_items);
+  w.table = cv.take<float2>(static_cast<size_t>(T) * (d / 2));
+  if (use_mfma(d, dtype)) {
+    w.Kp = cv.take<uint16_t>(w.max_tiles * kBN * d);
+    w.Vt = cv.take<uint16_t>(w.max_tiles * kBN * d);
+  } else {
+    w.Kp = w.Vt = nullptr;
+  }
+  w.hpack = cv.take<float>(Nr * d);
+  w.bytes = cv.off;
+  return w;
+}
+
+size_t attn_workspace_bytes(int B, int T, int H, int K, int d, int dtype) {
+  return carve_attn(nullptr, B, T, H, K, d, dtype).bytes;
+}
+
+template <int D>
+static void launch_mfma(const AttnWs& w, const void* q, const void* k, const void* v,
+                        int B, int T, int H, int rope_mode, float scale_log2,
+                        const int32_t* seg_offsets, const int32_t* perm_token,
+                        float* hout, hipStream_t st) {
+  constexpr int NW = MfmaShape<D>::NW, NQT = MfmaShape<D>::NQT;
+  prof_mark("pack", true, st);
+  k_pack_kv<D><<<static_cast<unsigned>(w.max_tiles), 256, 0, st>>>(
+      static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), w.table,
+      seg_offsets, w.tile_off, perm_token, w.meta, B * H, T, H, rope_mode, w.Kp, w.Vt);
+  prof_mark("pack", false, st);
+  prof_mark("attn", true, st);
+  k_attn_mfma<D, NQT, NW><<<static_cast<unsigned>(w.max_items), NW * 64, 0, st>>>(
+      static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.table, seg_offsets, w.tile_off,
+      perm_token, w.items, w.meta, T, H, rope_mode, scale_log2, hout);
+  prof_mark("attn", false, st);
+}
+
+template <int D, bool BF16>
+static void launch_generic(const AttnWs& w, const void* q, const void* k, const void* v,
+                           int T, int H, int rope_mode, float scale,
+                           const int32_t* seg_offsets, const int32_t* perm_token,
+                           float* hout, hipStream_t st) {
+  prof_mark("attn", true, st);
+  k_attn_generic<D, BF16><<<static_cast<unsigned>(w.max_items), 64, 0, st>>>(
+      q, k, v, w.table, seg_offsets, perm_token, w.items, w.meta, T, H, rope_mode,
+      scale, hout);
+  prof_mark("attn", false, st);
+}
+
+hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
+                       int B, int T, int H, int K, int d, float rope_base,
+                       int rope_mode, float scale, const float* gates,
+                       const int32_t* seg_offsets, const int32_t* perm_token,
+                       const int32_t* slot_pos, void* out, int out_dtype,
+                       float* head_out, void* ws, hipStream_t st) {
+  const AttnWs w = carve_attn(ws, B, T, H, K, d, dtype);
+  float* hout = head_out ? head_out : w.hpack;
+  const int BM = block_queries(d, dtype);
+  const int Nr = B * T * K;
+  k_attn_prep<<<1, kPrepThreads, 0, st>>>(seg_offsets, B * H, T, BM, rope_mode, Nr,
+                                          static_cast<int>(w.max_items), w.tile_off,
+                                          w.items, w.meta);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (rope_mode != 2) {
+    k_rope_table<<<512, 256, 0, st>>>(w.meta, d, std::log(static_cast<double>(rope_base)), w.table);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if (use_mfma(d, dtype)) {
+    const float sl2 = scale * 1.4426950408889634f;
+    if (d == 64)
+      launch_mfma<64>(w, q, k, v, B, T, H, rope_mode, sl2, seg_offsets, perm_token, hout, st);
+    else
+      launch_mfma<128>(w, q, k, v, B, T, H, rope_mode, sl2, seg_offsets, perm_token, hout, st);
+  } else {
+    const bool bf = dtype == 1;
+#define NAMOH_GEN(DD)                                                                        \
+  (bf ? launch_generic<DD, true>(w, q, k, v, T, H, rope_mode, scale, seg_offsets, perm_token, hout, st) \
+      : launch_generic<DD, false>(w, q, k, v, T, H, rope_mode, scale, seg_offsets, perm_token, hout, st))
+    if (d == 32) NAMOH_GEN(32);
+    else if (d == 64) NAMOH_GEN(64);
+    else NAMOH_GEN(128);
+#undef NAMOH_GEN
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const long BT = static_cast<long>(B) * T;
+  const long threads = BT * (d / 4);
+  const unsigned grid = static_cast<unsigned>((threads + 255) / 256);
+  prof_mark("combine", true, st);
+  if (out_dtype == 1)
+    k_combine<true><<<grid, 256, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+  else
+    k_combine<false><<<grid, 256, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+  prof_mark("combine", false, st);
+  return hipGetLastError();
+}
+
+}  // namespace namoh

@@ -1,0 +1,83 @@
+// Shared device helpers for the gfx950 kernels: bf16 conversion, wave-level
+// primitives, launch plumbing.  Internal to libnamoh.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define NAMOH_DEV __device__ __forceinline__
+
+namespace namoh {
+
+constexpr int kWave = 64;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// bf16 stored as raw 16-bit patterns in memory.
+NAMOH_DEV float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// Round to nearest even; inputs here are finite.
+NAMOH_DEV uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// Two floats -> packed bf16 pair (lo in the low half).
+NAMOH_DEV uint32_t pack_bf16x2(float lo, float hi) {
+  return static_cast<uint32_t>(f32_to_bf16(lo)) |
+         (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+}
+
+NAMOH_DEV float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
+NAMOH_DEV float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Lanes below the calling lane in a 64-wide wave.
+NAMOH_DEV uint64_t lanemask_lt() {
+  const int lane = __lane_id();
+  return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+}
+
+NAMOH_DEV int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Inclusive scan across a 64-lane wave.
+NAMOH_DEV int wave_inclusive_scan(int x) {
+  const int lane = __lane_id();
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(x, o, kWave);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+// Exclusive scan of one int per thread across a workgroup of NT threads.
+// `s_wave` must hold NT/64 ints; returns the exclusive prefix and sets
+// `total`.  Contains barriers: every thread of the block must call it.
+template <int NT>
+NAMOH_DEV int block_exclusive_scan(int x, int* s_wave, int& total) {
+  static_assert(NT % kWave == 0 && NT / kWave <= kWave, "block size");
+  const int lane = __lane_id();
+  const int wave = threadIdx.x / kWave;
+  const int incl = wave_inclusive_scan(x);
+  if (lane == kWave - 1) s_wave[wave] = incl;
+  __syncthreads();
+  if (wave == 0) {
+    const int wv = lane < NT / kWave ? s_wave[lane] : 0;
+    const int wi = wave_inclusive_scan(wv);
+    if (lane < NT / kWave) s_wave[lane] = wi - wv;
+    if (lane == NT / kWave - 1) s_wave[NT / kWave] = wi;  // block total
+  }
+  __syncthreads();
+  const int r = s_wave[wave] + incl - x;
+  total = s_wave[NT / kWave];
+  __syncthreads();
+  return r;
+}
+
+}  // namespace namoh

@@ -1,0 +1,370 @@
+// One decoding step: route the new token, append it to its selected heads'
+// caches, attend over each selected head's history, gate and combine.
+//
+// Sec. 3.1: routing uses only the current token, so incremental decoding is
+// the same causal computation as prefill; the new token's rank in head h is
+// that head's current length n (Eq. namoh-head-rope) and it attends to itself.
+// Sec. 3.2: only the active heads' queries run, and only their caches are read
+// or written.  Eq. namoh-kv-cost: the step reads sum over the selected heads
+// of (n + 1) cached rows, which makes it HBM-bound.
+//
+//   k_decode_route_append  one wave per sequence: lane = head; the rank of
+//                          each head under (logit desc, index asc) by H
+//                          comparisons, gates, then for each selected head the
+//                          rotation of q and k at rank n (angles in double),
+//                          the cache append and the length update.
+//   k_decode_attn          split over 512-row chunks of every selected head's
+//                          history: 16-byte coalesced loads of K and V rows
+//                          (a row spans d*esize/16 lanes), several rows in
+//                          flight per lane, online softmax in exp2 domain,
+//                          one (max, sum, acc[d]) partial per chunk.
+//   k_decode_combine       merges the chunk partials of each head by
+//                          log-sum-exp and sums the gated head outputs.
+#include <cmath>
+
+#include "common.h"
+#include "internal.h"
+
+namespace namoh {
+
+constexpr int kDecChunk = 512;   // cached rows per attention workgroup
+constexpr int kDecUnroll = 8;    // rows per lane in flight
+
+template <bool BF16>
+NAMOH_DEV float ld_elem(const void* p, size_t i) {
+  if constexpr (BF16) return bf16_to_f32(static_cast<const uint16_t*>(p)[i]);
+  else return static_cast<const float*>(p)[i];
+}
+
+template <bool BF16>
+NAMOH_DEV void st_elem(void* p, size_t i, float x) {
+  if constexpr (BF16) static_cast<uint16_t*>(p)[i] = f32_to_bf16(x);
+  else static_cast<float*>(p)[i] = x;
+}
+
+template <int D, bool BF16>
+__global__ __launch_bounds__(64) void k_decode_route_append(
+    const float* __restrict__ logits, const void* __restrict__ q,
+    const void* __restrict__ k, const void* __restrict__ v,
+    void* __restrict__ k_cache, void* __restrict__ v_cache,
+    int32_t* __restrict__ cache_len, const int32_t* __restrict__ seq_pos,
+    int H, int K, long cap, double log_base, int rope_mode, int gate_mode,
+    float qscale, int32_t* __restrict__ topk_idx, float* __restrict__ gates,
+    int32_t* __restrict__ dev_status, float* __restrict__ qrot,
+    int32_t* __restrict__ rows) {
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x;
+  const bool real = lane < H;
+  const float l = real ? logits[static_cast<size_t>(b) * H + lane] : 0.f;
+  int rank = 0;
+  for (int j = 0; j < H; ++j) {
+    const float lj = __shfl(l, j);
+    rank += (lj > l) || (lj == l && j < lane);
+  }
+  const bool sel = real && rank < K;
+  const uint64_t first = __ballot(real && rank == 0);
+  const float lmax = __shfl(l, __ffsll(static_cast<long long>(first)) - 1);
+  const float e_sel = sel ? expf(l - lmax) : 0.f;
+  float e_den = gate_mode == 1 ? (real ? expf(l - lmax) : 0.f) : e_sel;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) e_den += __shfl_xor(e_den, o);
+  if (sel) {
+    topk_idx[static_cast<size_t>(b) * K + rank] = lane;
+    gates[static_cast<size_t>(b) * K + rank] = e_sel / e_den;
+  }
+
+  for (int kk = 0; kk < K; ++kk) {
+    const uint64_t mk = __ballot(sel && rank == kk);
+    const size_t bk = static_cast<size_t>(b) * K + kk;
+    if (mk == 0) {  // only reachable with NaN logits (outside the contract)
+      if (lane == 0) {
+        rows[bk] = 0;
+        topk_idx[bk] = -1;
+        if (dev_status) dev_status[0] = 2;
+      }
+      continue;
+    }
+    const int h = __ffsll(static_cast<long long>(mk)) - 1;
+    const size_t bh = static_cast<size_t>(b) * H + h;
+    const int n = cache_len[bh];
+    if (n < 0 || n >= cap) {
+      if (lane == 0) {
+        rows[bk] = 0;
+        if (dev_status) dev_status[0] = 1;
+      }
+      continue;
+    }
+    const long pos = rope_mode == 0 ? n : (rope_mode == 1 ? seq_pos[b] : 0);
+    const size_t src = bh * D;
+    const size_t dst = (bh * cap + n) * D;
+    for (int j = lane; j < D / 2; j += 64) {
+      float cs = 1.f, sn = 0.f;
+      if (rope_mode != 2) {
+        const double theta = exp(-(2.0 * j / D) * log_base);
+        double s, c;
+        sincos(static_cast<double>(pos) * theta, &s, &c);
+        cs = static_cast<float>(c);
+        sn = static_cast<float>(s);
+      }
+      const float k1 = ld_elem<BF16>(k, src + j), k2 = ld_elem<BF16>(k, src + j + D / 2);
+      const float q1 = ld_elem<BF16>(q, src + j), q2 = ld_elem<BF16>(q, src + j + D / 2);
+      st_elem<BF16>(k_cache, dst + j, k1 * cs - k2 * sn);
+      st_elem<BF16>(k_cache, dst + j + D / 2, k2 * cs + k1 * sn);
+      st_elem<BF16>(v_cache, dst + j, ld_elem<BF16>(v, src + j));
+      st_elem<BF16>(v_cache, dst + j + D / 2, ld_elem<BF16>(v, src + j + D / 2));
+      qrot[bk * D + j] = (q1 * cs - q2 * sn) * qscale;
+      qrot[bk * D + j + D / 2] = (q2 * cs + q1 * sn) * qscale;
+    }
+    if (lane == 0) {
+      cache_len[bh] = n + 1;
+      rows[bk] = n + 1;
+    }
+  }
+}
+
+template <int D, bool BF16>
+__global__ __launch_bounds__(256) void k_decode_attn(
+    const void* __restrict__ k_cache, const void* __restrict__ v_cache,
+    const int32_t* __restrict__ topk_idx, const int32_t* __restrict__ rows,
+    const float* __restrict__ qrot, int H, int K, long cap, int nchunk,
+    float* __restrict__ part_acc, float* __restrict__ part_ml) {
+  constexpr int EPG = BF16 ? 8 : 4;   // elements per 16-byte granule
+  constexpr int G = D / EPG;          // lanes per row
+  constexpr int RPW = 64 / G;         // rows per wave per step
+  constexpr int RPB = 4 * RPW;        // rows per workgroup per step
+  constexpr int U = kDecUnroll;
+  __shared__ float s_ml[RPB][2];
+  __shared__ float s_acc[RPB][D];
+
+  const int bk = blockIdx.x / nchunk;
+  const int chunk = blockIdx.x - bk * nchunk;
+  const int L = rows[bk];
+  const int r0 = chunk * kDecChunk;
+  if (r0 >= L) return;
+  const int r1 = min(L, r0 + kDecChunk);
+  const int b = bk / K;
+  const int h = topk_idx[bk];
+  const size_t rowbase = (static_cast<size_t>(b) * H + h) * cap;
+  const int tid = threadIdx.x;
+  const int lane = tid % 64, wave = tid / 64;
+  const int sub = lane % G;
+  const int grp = wave * RPW + lane / G;
+
+  float qv[EPG];
+#pragma unroll
+  for (int e = 0; e < EPG; ++e) qv[e] = qrot[static_cast<size_t>(bk) * D + sub * EPG + e];
+  float m = -1e30f, lsum = 0.f, acc[EPG];
+#pragma unroll
+  for (int e = 0; e < EPG; ++e) acc[e] = 0.f;
+
+  const u32x4* kc = reinterpret_cast<const u32x4*>(k_cache);
+  const u32x4* vc = reinterpret_cast<const u32x4*>(v_cache);
+  for (int rb = r0; rb < r1; rb += RPB * U) {
+    u32x4 kx[U], vx[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int r = rb + u * RPB + grp;
+      if (r < r1) {
+        const size_t gi = (rowbase + r) * G + sub;
+        kx[u] = kc[gi];
+        vx[u] = vc[gi];
+      } else {
+        kx[u] = u32x4{0u, 0u, 0u, 0u};
+        vx[u] = kx[u];
+      }
+    }
+    float sc[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float f[EPG];
+      if constexpr (BF16) {
+        const uint32_t w[4] = {kx[u].x, kx[u].y, kx[u].z, kx[u].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          f[2 * e] = lo_bf16(w[e]);
+          f[2 * e + 1] = hi_bf16(w[e]);
+        }
+      } else {
+        f[0] = __uint_as_float(kx[u].x); f[1] = __uint_as_float(kx[u].y);
+        f[2] = __uint_as_float(kx[u].z); f[3] = __uint_as_float(kx[u].w);
+      }
+      float dsum = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPG; ++e) dsum = fmaf(qv[e], f[e], dsum);
+#pragma unroll
+      for (int o = G / 2; o > 0; o >>= 1) dsum += __shfl_xor(dsum, o);
+      sc[u] = (rb + u * RPB + grp < r1) ? dsum : -INFINITY;
+    }
+    float mx = sc[0];
+#pragma unroll
+    for (int u = 1; u < U; ++u) mx = fmaxf(mx, sc[u]);
+    const float mnew = fmaxf(m, mx);
+    const float corr = __builtin_amdgcn_exp2f(m - mnew);
+    lsum *= corr;
+#pragma unroll
+    for (int e = 0; e < EPG; ++e) acc[e] *= corr;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float p = __builtin_amdgcn_exp2f(sc[u] - mnew);
+      lsum += p;
+      float f[EPG];
+      if constexpr (BF16) {
+        const uint32_t w[4] = {vx[u].x, vx[u].y, vx[u].z, vx[u].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          f[2 * e] = lo_bf16(w[e]);
+          f[2 * e + 1] = hi_bf16(w[e]);
+        }
+      } else {
+        f[0] = __uint_as_float(vx[u].x); f[1] = __uint_as_float(vx[u].y);
+        f[2] = __uint_as_float(vx[u].z); f[3] = __uint_as_float(vx[u].w);
+      }
+#pragma unroll
+      for (int e = 0; e < EPG; ++e) acc[e] = fmaf(p, f[e], acc[e]);
+    }
+    m = mnew;
+  }
+  if (sub == 0) {
+    s_ml[grp][0] = m;
+    s_ml[grp][1] = lsum;
+  }
+#pragma unroll
+  for (int e = 0; e < EPG; ++e) s_acc[grp][sub * EPG + e] = acc[e];
+  __syncthreads();
+  if (tid < D) {
+    float M = -1e30f;
+    for (int gi = 0; gi < RPB; ++gi) M = fmaxf(M, s_ml[gi][0]);
+    float Ls = 0.f, A = 0.f;
+    for (int gi = 0; gi < RPB; ++gi) {
+      const float w = __builtin_amdgcn_exp2f(s_ml[gi][0] - M);
+      Ls = fmaf(s_ml[gi][1], w, Ls);
+      A = fmaf(s_acc[gi][tid], w, A);
+    }
+    const size_t pi = static_cast<size_t>(bk) * nchunk + chunk;
+    part_acc[pi * D + tid] = A;
+    if (tid == 0) {
+      part_ml[2 * pi] = M;
+      part_ml[2 * pi + 1] = Ls;
+    }
+  }
+}
+
+template <int D, bool OUT_BF16>
+__global__ __launch_bounds__(256) void k_decode_combine(
+    const float* __restrict__ gates, const int32_t* __restrict__ rows,
+    const float* __restrict__ part_acc, const float* __restrict__ part_ml,
+    int K, int nchunk, void* __restrict__ out) {
+  constexpr int NP = 256 / D;
+  __shared__ float s_o[NP][D];
+  const int b = blockIdx.x;
+  const int d = threadIdx.x % D, part = threadIdx.x / D;
+  float o = 0.f;
+  for (int kk = part; kk < K; kk += NP) {
+    const size_t bk = static_cast<size_t>(b) * K + kk;
+    const int L = rows[bk];
+    if (L == 0) continue;
+    const int nc = (L + kDecChunk - 1) / kDecChunk;
+    const float* ml = part_ml + bk * nchunk * 2;
+    float M = -1e30f;
+    for (int c = 0; c < nc; ++c) M = fmaxf(M, ml[2 * c]);
+    float Ls = 0.f, A = 0.f;
+    for (int c = 0; c < nc; ++c) {
+      const float w = __builtin_amdgcn_exp2f(ml[2 * c] - M);
+      Ls = fmaf(ml[2 * c + 1], w, Ls);
+      A = fmaf(part_acc[(bk * nchunk + c) * D + d], w, A);
+    }
+    o = fmaf(gates[bk], A / Ls, o);
+  }
+  s_o[part][d] = o;
+  __syncthreads();
+  if (threadIdx.x < D) {
+    float r = 0.f;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) r += s_o[p][d];
+    if constexpr (OUT_BF16) static_cast<uint16_t*>(out)[static_cast<size_t>(b) * D + d] = f32_to_bf16(r);
+    else static_cast<float*>(out)[static_cast<size_t>(b) * D + d] = r;
+  }
+}
+
+static int dec_nchunk(int cap) { return (cap + kDecChunk - 1) / kDecChunk; }
+
+struct DecWs {
+  float* qrot;
+  int32_t* rows;
+  float* part_acc;
+  float* part_ml;
+  size_t bytes;
+};
+
+static DecWs carve_dec(void* ws, int B, int K, int d, int cap) {
+  const size_t BK = static_cast<size_t>(B) * K;
+  const size_t nc = dec_nchunk(cap);
+  Carver cv(ws);
+  DecWs w;
+  w.qrot = cv.take<float>(BK * d);
+  w.rows = cv.take<int32_t>(BK);
+  w.part_acc = cv.take<float>(BK * nc * d);
+  w.part_ml = cv.take<float>(BK * nc * 2);
+  w.bytes = cv.off;
+  return w;
+}
+
+size_t decode_workspace_bytes(int B, int /*H*/, int K, int d, int cap) {
+  return carve_dec(nullptr, B, K, d, cap).bytes;
+}
+
+template <int D, bool BF16>
+static hipError_t run_decode(const float* logits, const void* q, const void* k,
+                             const void* v, void* k_cache, void* v_cache,
+                             int32_t* cache_len, const int32_t* seq_pos, int B,
+                             int H, int K, int cap, float rope_base,
+                             int rope_mode, int gate_mode, float scale,
+                             int32_t* topk_idx, float* gates, void* out,
+                             int out_dtype, int32_t* dev_status, void* ws,
+                             hipStream_t st) {
+  const DecWs w = carve_dec(ws, B, K, D, cap);
+  const int nc = dec_nchunk(cap);
+  const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
+  k_decode_route_append<D, BF16><<<B, 64, 0, st>>>(
+      logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, H, K, cap, log_base,
+      rope_mode, gate_mode, scale * 1.4426950408889634f, topk_idx, gates,
+      dev_status, w.qrot, w.rows);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t grid = static_cast<size_t>(B) * K * nc;
+  prof_mark("decode_attn", true, st);
+  k_decode_attn<D, BF16><<<static_cast<unsigned>(grid), 256, 0, st>>>(
+      k_cache, v_cache, topk_idx, w.rows, w.qrot, H, K, cap, nc, w.part_acc, w.part_ml);
+  prof_mark("decode_attn", false, st);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (out_dtype == 1)
+    k_decode_combine<D, true><<<B, 256, 0, st>>>(gates, w.rows, w.part_acc, w.part_ml, K, nc, out);
+  else
+    k_decode_combine<D, false><<<B, 256, 0, st>>>(gates, w.rows, w.part_acc, w.part_ml, K, nc, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode(const float* logits, const void* q, const void* k,
+                         const void* v, int dtype, void* k_cache,
+                         void* v_cache, int32_t* cache_len,
+                         const int32_t* seq_pos, int B, int H, int K, int d,
+                         int cap, float rope_base, int rope_mode,
+                         int gate_mode, float scale, int32_t* topk_idx,
+                         float* gates, void* out, int out_dtype,
+                         int32_t* dev_status, void* ws, hipStream_t st) {
+#define NAMOH_DEC(DD, BF)                                                               \
+  return run_decode<DD, BF>(logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, B, H, \
+                            K, cap, rope_base, rope_mode, gate_mode, scale, topk_idx,    \
+                            gates, out, out_dtype, dev_status, ws, st)
+  if (dtype == 1) {
+    if (d == 32) NAMOH_DEC(32, true);
+    if (d == 64) NAMOH_DEC(64, true);
+    NAMOH_DEC(128, true);
+  }
+  if (d == 32) NAMOH_DEC(32, false);
+  if (d == 64) NAMOH_DEC(64, false);
+  NAMOH_DEC(128, false);
+#undef NAMOH_DEC
+}
+
+}  // namespace namoh

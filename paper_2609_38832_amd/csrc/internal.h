@@ -1,0 +1,59 @@
+// Internal launch interface between the C ABI (api.cpp) and the kernels.
+// Every launcher enqueues on `st` and returns the first HIP error it sees.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace namoh {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
+
+// Carves consecutive aligned regions out of one workspace block.
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* p) : base(static_cast<char*>(p)) {}
+  template <class T>
+  T* take(size_t count) {
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += align_up(count * sizeof(T));
+    return p;
+  }
+};
+
+// ---- opt-in event timing (profile.cpp) ------------------------------------
+void prof_mark(const char* section, bool begin, hipStream_t st);
+
+// ---- routing (route.hip) -------------------------------------------------
+constexpr int kRouteChunk = 256;  // tokens per routing block
+size_t route_workspace_bytes(int B, int T, int H, int K);
+hipError_t launch_route(const float* logits, int B, int T, int H, int K,
+                        int gate_mode, int32_t* topk_idx, float* gates,
+                        int32_t* head_len, int32_t* seg_offsets,
+                        int32_t* perm_token, int32_t* slot_pos, void* ws,
+                        hipStream_t st);
+
+// ---- prefill attention (attn.hip) ----------------------------------------
+size_t attn_workspace_bytes(int B, int T, int H, int K, int d, int dtype);
+hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
+                       int B, int T, int H, int K, int d, float rope_base,
+                       int rope_mode, float scale, const float* gates,
+                       const int32_t* seg_offsets, const int32_t* perm_token,
+                       const int32_t* slot_pos, void* out, int out_dtype,
+                       float* head_out, void* ws, hipStream_t st);
+
+// ---- decode (decode.hip) --------------------------------------------------
+size_t decode_workspace_bytes(int B, int H, int K, int d, int cap);
+hipError_t launch_decode(const float* logits, const void* q, const void* k,
+                         const void* v, int dtype, void* k_cache,
+                         void* v_cache, int32_t* cache_len,
+                         const int32_t* seq_pos, int B, int H, int K, int d,
+                         int cap, float rope_base, int rope_mode,
+                         int gate_mode, float scale, int32_t* topk_idx,
+                         float* gates, void* out, int out_dtype,
+                         int32_t* dev_status, void* ws, hipStream_t st);
+
+}  // namespace namoh

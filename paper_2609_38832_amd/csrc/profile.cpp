@@ -1,0 +1,103 @@
+// Opt-in kernel timing with HIP events (diagnostics; off by default).
+//
+// When enabled, the launchers bracket their dominant kernel of each call
+// with a pair of events on the call's stream.  Reading the results
+// synchronises on the recorded events.  Not safe for concurrent use from
+// several host threads; enabling allocates events, so it is meant for
+// benchmarks, not for code that must not allocate.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace namoh {
+namespace {
+
+struct Section {
+  std::string name;
+  std::vector<hipEvent_t> start, stop;
+  int used = 0;
+};
+
+struct Profiler {
+  bool on = false;
+  int capacity = 0;
+  std::vector<Section> sections;
+
+  Section* find(const char* name, bool create) {
+    for (auto& s : sections)
+      if (s.name == name) return &s;
+    if (!create) return nullptr;
+    sections.emplace_back();
+    Section& s = sections.back();
+    s.name = name;
+    s.start.resize(capacity, nullptr);
+    s.stop.resize(capacity, nullptr);
+    return &s;
+  }
+
+  void clear() {
+    for (auto& s : sections) {
+      for (auto e : s.start) if (e) (void)hipEventDestroy(e);
+      for (auto e : s.stop) if (e) (void)hipEventDestroy(e);
+    }
+    sections.clear();
+  }
+};
+
+Profiler g_prof;
+
+}  // namespace
+
+void prof_mark(const char* section, bool begin, hipStream_t st) {
+  if (!g_prof.on) return;
+  Section* s = g_prof.find(section, true);
+  if (begin) {
+    if (s->used >= g_prof.capacity) return;
+    hipEvent_t& e = s->start[s->used];
+    if (!e && hipEventCreate(&e) != hipSuccess) { e = nullptr; return; }
+    (void)hipEventRecord(e, st);
+  } else {
+    if (s->used >= g_prof.capacity || !s->start[s->used]) return;
+    hipEvent_t& e = s->stop[s->used];
+    if (!e && hipEventCreate(&e) != hipSuccess) { e = nullptr; return; }
+    (void)hipEventRecord(e, st);
+    ++s->used;
+  }
+}
+
+}  // namespace namoh
+
+extern "C" {
+
+// Starts (capacity > 0) or stops (capacity == 0) timing; clears old records.
+int namoh_profile_enable(int capacity) {
+  namoh::g_prof.clear();
+  namoh::g_prof.on = capacity > 0;
+  namoh::g_prof.capacity = capacity > 0 ? capacity : 0;
+  return 0;
+}
+
+// Total milliseconds and number of timed launches of one section
+// ("attn", "pack", "decode_attn", ...).  Returns 0, or -1 if unknown.
+int namoh_profile_read(const char* section, double* total_ms, int* count) {
+  *total_ms = 0.0;
+  *count = 0;
+  for (auto& s : namoh::g_prof.sections) {
+    if (s.name != section) continue;
+    for (int i = 0; i < s.used; ++i) {
+      if (hipEventSynchronize(s.stop[i]) != hipSuccess) return -1;
+      float ms = 0.f;
+      if (hipEventElapsedTime(&ms, s.start[i], s.stop[i]) != hipSuccess) return -1;
+      *total_ms += ms;
+    }
+    *count = s.used;
+    return 0;
+  }
+  return -1;
+}
+
+}  // extern "C"

@@ -25,8 +25,10 @@ them.
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import math
-from dataclasses import dataclass, field, replace
+import os
+from dataclasses import dataclass, replace
 from typing import Optional
 
 import numpy as np
@@ -142,16 +144,26 @@ def prefill_logits(w: Workload) -> np.ndarray:
     return out
 
 
+def _workers() -> int:
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
 def prefill_qkv(w: Workload, which: str) -> np.ndarray:
     """Dense per-head tensor [B, H, T, d] for which in {'q','k','v'}.
 
-    bf16 tensors are returned as uint16 bit patterns, f32 as float32.
+    bf16 tensors are returned as uint16 bit patterns, f32 as float32.  Blocks
+    are drawn in parallel threads (each block has its own seeded generator,
+    so the result does not depend on the thread count).
     """
     tid = {"q": TID_Q, "k": TID_K, "v": TID_V}[which]
     out = np.empty((w.B, w.H, w.T, w.d), dtype=storage_dtype(w.dtype))
-    for b in range(w.B):
-        for h in range(w.H):
-            out[b, h] = normal_block(w.seed, tid, b, h, (w.T, w.d), w.qkv_scale, w.dtype)
+
+    def fill(bh):
+        b, h = divmod(bh, w.H)
+        out[b, h] = normal_block(w.seed, tid, b, h, (w.T, w.d), w.qkv_scale, w.dtype)
+
+    with cf.ThreadPoolExecutor(_workers()) as ex:
+        list(ex.map(fill, range(w.B * w.H)))
     return out
 
 
@@ -173,7 +185,8 @@ def decode_prior_lengths(w: Workload) -> np.ndarray:
     """
     out = np.zeros((w.B, w.H), dtype=np.int64)
     chunk = 1 << 15
-    for b in range(w.B):
+
+    def count(b):
         g = _rng(w.seed, TID_PRIOR, b, 0)
         left = w.prior
         while left > 0:
@@ -182,6 +195,9 @@ def decode_prior_lengths(w: Workload) -> np.ndarray:
             pick = np.argpartition(u, w.K - 1, axis=1)[:, :w.K]
             out[b] += np.bincount(pick.ravel(), minlength=w.H)
             left -= m
+
+    with cf.ThreadPoolExecutor(_workers()) as ex:
+        list(ex.map(count, range(w.B)))
     return out.astype(np.int32)
 
 
