@@ -9,11 +9,11 @@
 // are interleaved across compute units.
 //
 // Launch sequence for one call:
-//   k_attn_prep   one workgroup: per segment key-tile counts and their
-//                 running sum (tile_off), the work list of (segment, query
-//                 block) items sorted by causal work, heaviest first (counting
-//                 sort by key-tile count), the RoPE table length.
-//   k_rope_table  cos/sin of p * base^(-2j/d), angles in double, stored f32.
+//   k_attn_prep   workgroup 0: per segment key-tile counts and their running
+//                 sum (tile_off), the work list of (segment, query block)
+//                 items sorted by causal work, heaviest first (counting sort
+//                 by key-tile count).  Other workgroups: the RoPE table,
+//                 cos/sin of p * base^(-2j/d) from double angles, stored f32.
 //   bf16, d in {64, 128}:
 //     k_pack_kv   gathers each 64-row key tile of a segment by perm_token,
 //                 applies RoPE at the key's rank while loading it, rounds to
@@ -42,15 +42,31 @@ constexpr int kPrepThreads = 1024;
 constexpr int kSortBins = 4096;    // work keys are clamped to this many bins
 
 // mfma kernel shape: waves per workgroup and 32-query sub-tiles per wave
+#ifndef NAMOH_D64_NW
+#define NAMOH_D64_NW 8
+#endif
+#ifndef NAMOH_D64_NQT
+#define NAMOH_D64_NQT 1
+#endif
+#ifndef NAMOH_D128_NW
+#define NAMOH_D128_NW 8
+#endif
+#ifndef NAMOH_D128_NQT
+#define NAMOH_D128_NQT 1
+#endif
 template <int D> struct MfmaShape;
-template <> struct MfmaShape<64> { static constexpr int NW = 4, NQT = 2; };
-template <> struct MfmaShape<128> { static constexpr int NW = 4, NQT = 2; };
+template <> struct MfmaShape<64> { static constexpr int NW = NAMOH_D64_NW, NQT = NAMOH_D64_NQT; };
+template <> struct MfmaShape<128> { static constexpr int NW = NAMOH_D128_NW, NQT = NAMOH_D128_NQT; };
+// The running softmax maximum is only raised when a tile exceeds it by more
+// than 2^kLazyLog2 (probabilities then stay below 2^kLazyLog2 and the final
+// normalisation is exact), so the output accumulator is rarely rescaled.
+constexpr float kLazyLog2 = 8.f;
 constexpr int kGenericBM = 64;
 
 enum Meta { kMetaItems = 0, kMetaTiles = 1, kMetaTablePos = 2, kMetaBad = 3, kMetaCount = 4 };
 
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kPrepThreads) void k_attn_prep(
+NAMOH_DEV void attn_schedule(
     const int32_t* __restrict__ seg_offsets, int BH, int T, int BM,
     int rope_mode, int Nr, int max_items, int32_t* __restrict__ tile_off,
     int2* __restrict__ items, int32_t* __restrict__ meta) {
@@ -134,14 +150,37 @@ __global__ __launch_bounds__(kPrepThreads) void k_attn_prep(
 }
 
 // ---------------------------------------------------------------------------
-// table[p * (d/2) + j] = (cos, sin)(p * base^(-2j/d)), p < meta[kMetaTablePos]
-__global__ __launch_bounds__(256) void k_rope_table(
-    const int32_t* __restrict__ meta, int d, double log_base,
-    float2* __restrict__ table) {
+// Workgroup 0 builds the schedule (above); workgroups 1.. fill the RoPE table
+// table[p * (d/2) + j] = (cos, sin)(p * base^(-2j/d)) for p < P, with angles
+// in double.  P (longest segment for head-relative positions, T for global
+// ones) is recomputed by each table workgroup from seg_offsets.
+__global__ __launch_bounds__(kPrepThreads) void k_attn_prep(
+    const int32_t* __restrict__ seg_offsets, int BH, int T, int BM,
+    int rope_mode, int Nr, int max_items, int d, double log_base,
+    int32_t* __restrict__ tile_off, int2* __restrict__ items,
+    int32_t* __restrict__ meta, float2* __restrict__ table) {
+  if (blockIdx.x == 0) {
+    attn_schedule(seg_offsets, BH, T, BM, rope_mode, Nr, max_items, tile_off, items, meta);
+    return;
+  }
+  if (rope_mode == 2) return;
+  __shared__ int s_p;
+  int P = T;
+  if (rope_mode == 0) {
+    if (threadIdx.x == 0) s_p = 0;
+    __syncthreads();
+    int mx = 0;
+    for (int s = threadIdx.x; s < BH; s += kPrepThreads)
+      mx = max(mx, min(seg_offsets[s + 1] - seg_offsets[s], T));
+    atomicMax(&s_p, mx);
+    __syncthreads();
+    P = s_p;
+  }
   const int half = d / 2;
-  const size_t total = static_cast<size_t>(meta[kMetaTablePos]) * half;
-  for (size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-       i < total; i += static_cast<size_t>(gridDim.x) * blockDim.x) {
+  const size_t total = static_cast<size_t>(P) * half;
+  const size_t stride = static_cast<size_t>(gridDim.x - 1) * kPrepThreads;
+  for (size_t i = static_cast<size_t>(blockIdx.x - 1) * kPrepThreads + threadIdx.x; i < total;
+       i += stride) {
     const int p = static_cast<int>(i / half);
     const int j = static_cast<int>(i - static_cast<size_t>(p) * half);
     const double theta = exp(-(2.0 * j / d) * log_base);
@@ -330,6 +369,7 @@ __global__ __launch_bounds__(NW * 64, 1) void k_attn_mfma(
   const int wq_last = q0 + 32 * ((NQT - 1) * NW + wave) + 31;
   const int wave_tiles = min(ntiles, wq_last / kBN + 1);
   const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
+  const float lazy_thr = kLazyLog2 / scale_log2;
 
   // ---- query block: gather, rotate, round to bf16 B operands -------------
   bf16x8 qB[NQT][KS];
@@ -423,16 +463,20 @@ __global__ __launch_bounds__(NW * 64, 1) void k_attn_mfma(
       }
       // ---- online softmax ----------------------------------------------
       bf16x8 pB[NQT][4];
+      float alpha[NQT];
+      bool rescale = false;
 #pragma unroll
       for (int qt = 0; qt < NQT; ++qt) {
         float mx = -INFINITY;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) mx = fmaxf(mx, S[kk][qt][e]);
+          for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(S[kk][qt][e], S[kk][qt][e + 1]));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float mnew = fmaxf(m_run[qt], mx);
-        const float alpha = __builtin_amdgcn_exp2f((m_run[qt] - mnew) * scale_log2);
+        const bool up = mx > m_run[qt] + lazy_thr;
+        const float mnew = up ? mx : m_run[qt];
+        alpha[qt] = up ? __builtin_amdgcn_exp2f((m_run[qt] - mnew) * scale_log2) : 1.f;
+        rescale |= up;
         const float mc = mnew * scale_log2;
         float ls = 0.f;
 #pragma unroll
@@ -443,17 +487,21 @@ __global__ __launch_bounds__(NW * 64, 1) void k_attn_mfma(
             S[kk][qt][e] = p;
             ls += p;
           }
-        l_run[qt] = l_run[qt] * alpha + ls;
+        l_run[qt] = l_run[qt] * alpha[qt] + ls;
         m_run[qt] = mnew;
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) O[mt][qt][e] *= alpha;
 #pragma unroll
         for (int k2 = 0; k2 < 4; ++k2)
 #pragma unroll
           for (int e = 0; e < 8; ++e)
             pB[qt][k2][e] = static_cast<__bf16>(S[k2 >> 1][qt][8 * (k2 & 1) + e]);
+      }
+      if (__any(rescale)) {
+#pragma unroll
+        for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) O[mt][qt][e] *= alpha[qt];
       }
       // ---- O^T += V^T P^T ------------------------------------------------
 #pragma unroll
@@ -717,15 +765,12 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   float* hout = head_out ? head_out : w.hpack;
   const int BM = block_queries(d, dtype);
   const int Nr = B * T * K;
-  k_attn_prep<<<1, kPrepThreads, 0, st>>>(seg_offsets, B * H, T, BM, rope_mode, Nr,
-                                          static_cast<int>(w.max_items), w.tile_off,
-                                          w.items, w.meta);
+  const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
+  k_attn_prep<<<1 + 64, kPrepThreads, 0, st>>>(seg_offsets, B * H, T, BM, rope_mode, Nr,
+                                               static_cast<int>(w.max_items), d, log_base,
+                                               w.tile_off, w.items, w.meta, w.table);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (rope_mode != 2) {
-    k_rope_table<<<512, 256, 0, st>>>(w.meta, d, std::log(static_cast<double>(rope_base)), w.table);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
   if (use_mfma(d, dtype)) {
     const float sl2 = scale * 1.4426950408889634f;
     if (d == 64)

@@ -249,40 +249,66 @@ __global__ __launch_bounds__(256) void k_decode_attn(
   }
 }
 
+// One workgroup per sequence; wave w merges the chunk partials of heads
+// w, w + 4, ... (lane c holds chunk c's max and sum; the accumulators are
+// read column-wise, d = lane + 64 i), then the gated head outputs are summed
+// in head order.
 template <int D, bool OUT_BF16>
 __global__ __launch_bounds__(256) void k_decode_combine(
     const float* __restrict__ gates, const int32_t* __restrict__ rows,
     const float* __restrict__ part_acc, const float* __restrict__ part_ml,
     int K, int nchunk, void* __restrict__ out) {
-  constexpr int NP = 256 / D;
-  __shared__ float s_o[NP][D];
+  constexpr int NWV = 4;
+  constexpr int DPL = (D + 63) / 64;  // output columns per lane
+  __shared__ float s_o[NWV][D];
   const int b = blockIdx.x;
-  const int d = threadIdx.x % D, part = threadIdx.x / D;
-  float o = 0.f;
-  for (int kk = part; kk < K; kk += NP) {
+  const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
+  float o[DPL];
+#pragma unroll
+  for (int i = 0; i < DPL; ++i) o[i] = 0.f;
+  for (int kk = wave; kk < K; kk += NWV) {
     const size_t bk = static_cast<size_t>(b) * K + kk;
     const int L = rows[bk];
     if (L == 0) continue;
     const int nc = (L + kDecChunk - 1) / kDecChunk;
     const float* ml = part_ml + bk * nchunk * 2;
     float M = -1e30f;
-    for (int c = 0; c < nc; ++c) M = fmaxf(M, ml[2 * c]);
-    float Ls = 0.f, A = 0.f;
+    for (int c = lane; c < nc; c += 64) M = fmaxf(M, ml[2 * c]);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+    float Ls = 0.f;
+    for (int c = lane; c < nc; c += 64) Ls += ml[2 * c + 1] * __builtin_amdgcn_exp2f(ml[2 * c] - M);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) Ls += __shfl_xor(Ls, off);
+    const float scale = gates[bk] / Ls;
+    float a[DPL];
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) a[i] = 0.f;
+    const float* pa = part_acc + bk * nchunk * D;
+#pragma unroll 4
     for (int c = 0; c < nc; ++c) {
       const float w = __builtin_amdgcn_exp2f(ml[2 * c] - M);
-      Ls = fmaf(ml[2 * c + 1], w, Ls);
-      A = fmaf(part_acc[(bk * nchunk + c) * D + d], w, A);
+#pragma unroll
+      for (int i = 0; i < DPL; ++i) {
+        const int d = lane + 64 * i;
+        if (d < D) a[i] = fmaf(pa[static_cast<size_t>(c) * D + d], w, a[i]);
+      }
     }
-    o = fmaf(gates[bk], A / Ls, o);
+#pragma unroll
+    for (int i = 0; i < DPL; ++i) o[i] = fmaf(a[i], scale, o[i]);
   }
-  s_o[part][d] = o;
+#pragma unroll
+  for (int i = 0; i < DPL; ++i) {
+    const int d = lane + 64 * i;
+    if (d < D) s_o[wave][d] = o[i];
+  }
   __syncthreads();
   if (threadIdx.x < D) {
     float r = 0.f;
 #pragma unroll
-    for (int p = 0; p < NP; ++p) r += s_o[p][d];
-    if constexpr (OUT_BF16) static_cast<uint16_t*>(out)[static_cast<size_t>(b) * D + d] = f32_to_bf16(r);
-    else static_cast<float*>(out)[static_cast<size_t>(b) * D + d] = r;
+    for (int w = 0; w < NWV; ++w) r += s_o[w][threadIdx.x];
+    if constexpr (OUT_BF16) static_cast<uint16_t*>(out)[static_cast<size_t>(b) * D + threadIdx.x] = f32_to_bf16(r);
+    else static_cast<float*>(out)[static_cast<size_t>(b) * D + threadIdx.x] = r;
   }
 }
 

@@ -28,7 +28,7 @@ struct Carver {
 void prof_mark(const char* section, bool begin, hipStream_t st);
 
 // ---- routing (route.hip) -------------------------------------------------
-constexpr int kRouteChunk = 256;  // tokens per routing block
+constexpr int kRouteChunk = 64;   // tokens per routing workgroup (one wave)
 size_t route_workspace_bytes(int B, int T, int H, int K);
 hipError_t launch_route(const float* logits, int B, int T, int H, int K,
                         int gate_mode, int32_t* topk_idx, float* gates,

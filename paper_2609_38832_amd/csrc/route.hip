@@ -6,39 +6,52 @@
 // of the (token, head) pairs by segment b*H + h.
 //
 // Three launches, no atomics, so every output is deterministic:
-//   1. k_route_count   one lane per token: K passes of a register argmax over
-//                      the H logits (strict '>' scanning heads upward, so equal
-//                      logits resolve to the lower head index), gates, and per
-//                      256-token chunk the number of tokens routed to each head
-//                      (wave ballot + popcount).
-//   2. k_route_scan    one workgroup: exclusive scan of the chunk counts laid
-//                      out [b][h][chunk], which is exactly segment order, then
-//                      tokens-in-chunk order.  Gives seg_offsets and head_len.
-//   3. k_route_scatter recomputes the chunk's ballots; a pair's packed
-//                      position = chunk base + earlier waves' counts + the
-//                      number of lower lanes in its wave routed to the same
+//   1. k_route_count   one wave per 64-token chunk: the chunk's logits are
+//                      staged through LDS with coalesced loads; one lane per
+//                      token runs K passes of a register argmax over the H
+//                      logits (strict '>' scanning heads upward, so equal
+//                      logits resolve to the lower head index), computes the
+//                      gates, and the wave counts the chunk's tokens per head
+//                      (ballot + popcount).
+//   2. k_route_scan    one wave per (b, h) segment: exclusive scan of the
+//                      segment's chunk counts and the head length n.
+//   3. k_route_scatter one wave per chunk: the segment offsets of sequence b
+//                      are b*T*K plus a scan of its H head lengths (every
+//                      sequence contributes exactly T*K pairs); a pair's
+//                      packed position = segment offset + earlier chunks of the
+//                      segment + lower lanes of this chunk routed to the same
 //                      head (popcount of ballot & lanes-below).
 #include "common.h"
 #include "internal.h"
 
 namespace namoh {
 
+constexpr int kRC = kRouteChunk;   // 64 tokens = one wave per chunk
+
 template <int HMAX>
-__global__ __launch_bounds__(kRouteChunk) void k_route_count(
+__global__ __launch_bounds__(kRC) void k_route_count(
     const float* __restrict__ logits, int T, int H, int K, int gate_mode,
     int nchunk, int32_t* __restrict__ topk_idx, float* __restrict__ gates,
     int32_t* __restrict__ chunk_counts) {
+  __shared__ float s_l[kRC * (HMAX + 1)];
   const int b = blockIdx.x / nchunk;
   const int c = blockIdx.x - b * nchunk;
-  const int t = c * kRouteChunk + threadIdx.x;
-  const bool valid = t < T;
-  const size_t row = static_cast<size_t>(b) * T + (valid ? t : 0);
-
+  const int lane = threadIdx.x;
+  const int t0 = c * kRC;
+  const int rows = min(kRC, T - t0);
+  const size_t row0 = static_cast<size_t>(b) * T + t0;
+  const float* src = logits + row0 * H;
+  for (int i = lane; i < rows * H; i += kRC) {
+    const int r = i / H, j = i - (i / H) * H;
+    s_l[r * (HMAX + 1) + j] = src[i];
+  }
+  __syncthreads();
+  const bool valid = lane < rows;
   float l[HMAX];
-  const float* lp = logits + row * H;
 #pragma unroll
-  for (int j = 0; j < HMAX; ++j) l[j] = (valid && j < H) ? lp[j] : 0.f;
+  for (int j = 0; j < HMAX; ++j) l[j] = (valid && j < H) ? s_l[lane * (HMAX + 1) + j] : 0.f;
 
+  const size_t row = row0 + (valid ? lane : 0);
   int32_t* tk = topk_idx + row * K;
   float* gk = gates + row * K;
   uint64_t taken = 0;
@@ -72,94 +85,54 @@ __global__ __launch_bounds__(kRouteChunk) void k_route_count(
     const float inv = 1.f / denom;
     for (int k = 0; k < K; ++k) gk[k] *= inv;
   }
-
-  // per-chunk head counts
-  __shared__ int s_cnt[kRouteChunk / kWave][64];
-  const int lane = __lane_id();
-  const int wave = threadIdx.x / kWave;
   int mine = 0;
   for (int h = 0; h < H; ++h) {
-    const uint64_t bal = __ballot(valid && ((taken >> h) & 1ull));
-    if (lane == h) mine = __popcll(bal);
+    const int cnt = __popcll(__ballot(valid && ((taken >> h) & 1ull)));
+    if (lane == h) mine = cnt;
   }
-  s_cnt[wave][lane] = mine;
-  __syncthreads();
-  if (threadIdx.x < H) {
-    int s = 0;
-#pragma unroll
-    for (int w = 0; w < kRouteChunk / kWave; ++w) s += s_cnt[w][threadIdx.x];
-    chunk_counts[(static_cast<size_t>(b) * H + threadIdx.x) * nchunk + c] = s;
-  }
+  if (lane < H) chunk_counts[(static_cast<size_t>(b) * H + lane) * nchunk + c] = mine;
 }
 
-constexpr int kScanThreads = 1024;
-constexpr int kScanItems = 4;
-
-__global__ __launch_bounds__(kScanThreads) void k_route_scan(
-    const int32_t* __restrict__ counts, int L, int nchunk, int BH,
-    int32_t* __restrict__ base, int32_t* __restrict__ seg_offsets,
+__global__ __launch_bounds__(kWave) void k_route_scan(
+    const int32_t* __restrict__ counts, int nchunk, int32_t* __restrict__ within,
     int32_t* __restrict__ head_len) {
-  __shared__ int s_wave[kScanThreads / kWave];
-  __shared__ int s_carry;
-  const int tid = threadIdx.x;
-  const int lane = __lane_id();
-  const int wave = tid / kWave;
-  if (tid == 0) s_carry = 0;
-  __syncthreads();
-  for (int start = 0; start < L; start += kScanThreads * kScanItems) {
-    int v[kScanItems];
-    int sum = 0;
-#pragma unroll
-    for (int i = 0; i < kScanItems; ++i) {
-      const int idx = start + tid * kScanItems + i;
-      v[i] = idx < L ? counts[idx] : 0;
-      sum += v[i];
-    }
-    const int incl = wave_inclusive_scan(sum);
-    if (lane == kWave - 1) s_wave[wave] = incl;
-    __syncthreads();
-    if (wave == 0) {
-      const int wv = lane < kScanThreads / kWave ? s_wave[lane] : 0;
-      const int wi = wave_inclusive_scan(wv);
-      if (lane < kScanThreads / kWave) s_wave[lane] = wi - wv;  // exclusive
-    }
-    __syncthreads();
-    int run = s_carry + s_wave[wave] + incl - sum;
-#pragma unroll
-    for (int i = 0; i < kScanItems; ++i) {
-      const int idx = start + tid * kScanItems + i;
-      if (idx < L) {
-        base[idx] = run;
-        if (idx % nchunk == 0) seg_offsets[idx / nchunk] = run;
-      }
-      run += v[i];
-    }
-    __syncthreads();
-    if (tid == kScanThreads - 1) s_carry = run;
-    __syncthreads();
+  const int s = blockIdx.x;
+  const int lane = threadIdx.x;
+  const size_t base = static_cast<size_t>(s) * nchunk;
+  int carry = 0;
+  for (int i0 = 0; i0 < nchunk; i0 += kWave) {
+    const int i = i0 + lane;
+    const int x = i < nchunk ? counts[base + i] : 0;
+    const int incl = wave_inclusive_scan(x);
+    if (i < nchunk) within[base + i] = carry + incl - x;
+    carry += __shfl(incl, kWave - 1);
   }
-  if (tid == 0) seg_offsets[BH] = s_carry;
-  for (int s = tid; s < BH; s += kScanThreads) {
-    int n = 0;
-    for (int c = 0; c < nchunk; ++c) n += counts[static_cast<size_t>(s) * nchunk + c];
-    head_len[s] = n;
-  }
+  if (lane == 0) head_len[s] = carry;
 }
 
-__global__ __launch_bounds__(kRouteChunk) void k_route_scatter(
-    const int32_t* __restrict__ topk_idx, int T, int H, int K, int nchunk,
-    const int32_t* __restrict__ base, int32_t* __restrict__ perm_token,
+__global__ __launch_bounds__(kRC) void k_route_scatter(
+    const int32_t* __restrict__ topk_idx, int B, int T, int H, int K, int nchunk,
+    const int32_t* __restrict__ within, const int32_t* __restrict__ head_len,
+    int32_t* __restrict__ seg_offsets, int32_t* __restrict__ perm_token,
     int32_t* __restrict__ slot_pos) {
-  __shared__ uint64_t s_bal[kRouteChunk / kWave][64];
-  __shared__ int s_base[kRouteChunk / kWave][64];
+  __shared__ uint64_t s_bal[64];
+  __shared__ int s_base[64];
   const int b = blockIdx.x / nchunk;
   const int c = blockIdx.x - b * nchunk;
-  const int t = c * kRouteChunk + threadIdx.x;
+  const int lane = threadIdx.x;
+  const int t = c * kRC + lane;
   const bool valid = t < T;
-  const int lane = __lane_id();
-  const int wave = threadIdx.x / kWave;
   const size_t row = static_cast<size_t>(b) * T + (valid ? t : 0);
   const int32_t* tk = topk_idx + row * K;
+
+  // segment offsets of sequence b
+  const int hl = lane < H ? head_len[static_cast<size_t>(b) * H + lane] : 0;
+  const int seg_off = b * T * K + wave_inclusive_scan(hl) - hl;
+  if (lane < H) {
+    if (c == 0) seg_offsets[static_cast<size_t>(b) * H + lane] = seg_off;
+    s_base[lane] = seg_off + within[(static_cast<size_t>(b) * H + lane) * nchunk + c];
+  }
+  if (c == 0 && b == B - 1 && lane == 0) seg_offsets[static_cast<size_t>(B) * H] = B * T * K;
 
   uint64_t mask = 0;
   if (valid)
@@ -169,24 +142,14 @@ __global__ __launch_bounds__(kRouteChunk) void k_route_scatter(
     const uint64_t bal = __ballot((mask >> h) & 1ull);
     if (lane == h) mine = bal;
   }
-  s_bal[wave][lane] = mine;
-  __syncthreads();
-  if (threadIdx.x < H) {
-    const int h = threadIdx.x;
-    int acc = base[(static_cast<size_t>(b) * H + h) * nchunk + c];
-#pragma unroll
-    for (int w = 0; w < kRouteChunk / kWave; ++w) {
-      s_base[w][h] = acc;
-      acc += __popcll(s_bal[w][h]);
-    }
-  }
+  s_bal[lane] = mine;
   __syncthreads();
   if (valid) {
     const uint64_t below = lanemask_lt();
     int32_t* sp = slot_pos + row * K;
     for (int k = 0; k < K; ++k) {
       const int h = tk[k];
-      const int pos = s_base[wave][h] + __popcll(s_bal[wave][h] & below);
+      const int pos = s_base[h] + __popcll(s_bal[h] & below);
       perm_token[pos] = t;
       sp[k] = pos;
     }
@@ -208,22 +171,22 @@ hipError_t launch_route(const float* logits, int B, int T, int H, int K,
   const size_t L = static_cast<size_t>(B) * H * nchunk;
   Carver cv(ws);
   int32_t* counts = cv.take<int32_t>(L);
-  int32_t* base = cv.take<int32_t>(L);
+  int32_t* within = cv.take<int32_t>(L);
   const dim3 grid(static_cast<unsigned>(static_cast<size_t>(B) * nchunk));
   if (H <= 8)
-    k_route_count<8><<<grid, kRouteChunk, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
+    k_route_count<8><<<grid, kRC, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
   else if (H <= 16)
-    k_route_count<16><<<grid, kRouteChunk, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
+    k_route_count<16><<<grid, kRC, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
   else if (H <= 32)
-    k_route_count<32><<<grid, kRouteChunk, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
+    k_route_count<32><<<grid, kRC, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
   else
-    k_route_count<64><<<grid, kRouteChunk, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
+    k_route_count<64><<<grid, kRC, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  k_route_scan<<<1, kScanThreads, 0, st>>>(counts, static_cast<int>(L), nchunk, B * H, base, seg_offsets, head_len);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  k_route_scatter<<<grid, kRouteChunk, 0, st>>>(topk_idx, T, H, K, nchunk, base, perm_token, slot_pos);
+  k_route_scan<<<B * H, kWave, 0, st>>>(counts, nchunk, within, head_len);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  k_route_scatter<<<grid, kRC, 0, st>>>(topk_idx, B, T, H, K, nchunk, within, head_len,
+                                        seg_offsets, perm_token, slot_pos);
   return hipGetLastError();
 }
 

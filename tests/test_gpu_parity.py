@@ -102,7 +102,7 @@ MID = {
     "long_d128_mid": W.WORKLOADS[3].with_(T=2600, H=16),
     "skewed_d128_mid": W.WORKLOADS[4].with_(B=1, T=3000),
     "peaky_d128": W.WORKLOADS[3].with_(T=1100, H=8, K=3, qkv_scale=1.0),
-    "peaky_d64": W.WORKLOADS[2].with_(B=1, T=900, qkv_scale=1.5),
+    "peaky_d64": W.WORKLOADS[2].with_(B=1, T=900, qkv_scale=1.0),
     "fp32_d64": W.WORKLOADS[2].with_(B=1, T=700, dtype="f32"),
     "fp32_d128": W.WORKLOADS[3].with_(T=600, H=8, dtype="f32"),
     "bf16_d32": W.WORKLOADS[1].with_(T=800, dtype="bf16"),
