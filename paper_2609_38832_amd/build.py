@@ -38,9 +38,15 @@ def hipcc() -> str:
     return p
 
 
+# Per-source flags.  The attention kernels never produce NaN (masked scores are
+# -inf and are only ever compared or exponentiated), so max/min need no NaN
+# quieting.
+EXTRA = {"attn.hip": ["-fno-honor-nans", "-mno-amdgpu-ieee"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *COMMON, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *COMMON, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".hip"):
         cmd[1:1] = ["-x", "hip"]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -54,9 +54,24 @@ constexpr int kSortBins = 4096;    // work keys are clamped to this many bins
 #ifndef NAMOH_D128_NQT
 #define NAMOH_D128_NQT 1
 #endif
+#ifndef NAMOH_D64_MINB
+#define NAMOH_D64_MINB 1
+#endif
+#ifndef NAMOH_D128_MINB
+#define NAMOH_D128_MINB 1
+#endif
+// NW waves per workgroup, NQT 32-query sub-tiles per wave, MINB workgroups
+// per compute unit the register allocation must allow.
 template <int D> struct MfmaShape;
-template <> struct MfmaShape<64> { static constexpr int NW = NAMOH_D64_NW, NQT = NAMOH_D64_NQT; };
-template <> struct MfmaShape<128> { static constexpr int NW = NAMOH_D128_NW, NQT = NAMOH_D128_NQT; };
+template <> struct MfmaShape<64> {
+  static constexpr int NW = NAMOH_D64_NW, NQT = NAMOH_D64_NQT, MINB = NAMOH_D64_MINB;
+};
+template <> struct MfmaShape<128> {
+  static constexpr int NW = NAMOH_D128_NW, NQT = NAMOH_D128_NQT, MINB = NAMOH_D128_MINB;
+};
+#ifndef NAMOH_ATTN_PIPE
+#define NAMOH_ATTN_PIPE 0
+#endif
 // The running softmax maximum is only raised when a tile exceeds it by more
 // than 2^kLazyLog2 (probabilities then stay below 2^kLazyLog2 and the final
 // normalisation is exact), so the output accumulator is rarely rescaled.
@@ -209,6 +224,17 @@ NAMOH_DEV void unpack8(const uint4 x, float* f) {
   }
 }
 
+// Combine x of lanes l and l ^ 32 (v_permlane32_swap hands every lane both
+// values; max and sum are symmetric, so the order of the pair is irrelevant).
+NAMOH_DEV float pair_max32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+NAMOH_DEV float pair_sum32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 NAMOH_DEV uint4 pack8(const float* f) {
   return make_uint4(pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]),
                     pack_bf16x2(f[4], f[5]), pack_bf16x2(f[6], f[7]));
@@ -307,18 +333,269 @@ __global__ __launch_bounds__(256) void k_pack_kv(
   }
 }
 
-// Loads one packed key tile and one transposed value tile (KPT 16-byte
-// granules each per thread) into registers.
+// LDS granule swizzle.  gfx950 LDS serves 256 bytes (64 banks) per clock,
+// i.e. 16 lanes of a 16-byte read at once; the operand reads below have 16
+// consecutive lanes read the same logical 16-byte granule of 16 consecutive
+// rows.  XOR-ing the granule index with row bits makes those 16 reads cover
+// all 64 banks: rows of 16 granules (256 B) use row & 15; rows of 8 granules
+// (128 B, two rows per bank sweep) use (row >> 1) & 7.
+template <int GPR>
+NAMOH_DEV int swz(int row, int gr) {
+  static_assert(GPR == 8 || GPR == 16, "granules per row");
+  return GPR == 16 ? (gr ^ (row & 15)) : (gr ^ ((row >> 1) & 7));
+}
+
+// Tile staging: KPT 16-byte granules per thread of one packed key tile or
+// one transposed value tile (contiguous in HBM) into registers, then into
+// swizzled LDS.
+template <int KPT, int NT>
+NAMOH_DEV void tile_gload(const uint16_t* __restrict__ tile, int tid, u32x4 (&reg)[KPT]) {
+  const u32x4* p = reinterpret_cast<const u32x4*>(tile);
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) reg[i] = p[tid + i * NT];
+}
+
+// key tile: kBN rows of D elements
 template <int D, int KPT, int NT>
-NAMOH_DEV void tile_gload(const uint16_t* __restrict__ Kp, const uint16_t* __restrict__ Vt,
-                          int tile, int tid, u32x4 (&kreg)[KPT], u32x4 (&vreg)[KPT]) {
-  const u32x4* kp = reinterpret_cast<const u32x4*>(Kp + static_cast<size_t>(tile) * kBN * D);
-  const u32x4* vp = reinterpret_cast<const u32x4*>(Vt + static_cast<size_t>(tile) * D * kBN);
+NAMOH_DEV void tile_lstore_k(uint16_t* sKb, int tid, const u32x4 (&reg)[KPT]) {
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
-    kreg[i] = kp[tid + i * NT];
-    vreg[i] = vp[tid + i * NT];
+    const int u = tid + i * NT;
+    const int row = u / (D / 8), gr = u % (D / 8);
+    *reinterpret_cast<u32x4*>(&sKb[row * D + swz<D / 8>(row, gr) * 8]) = reg[i];
   }
+}
+
+// transposed value tile: D rows of kBN keys
+template <int D, int KPT, int NT>
+NAMOH_DEV void tile_lstore_v(uint16_t* sVb, int tid, const u32x4 (&reg)[KPT]) {
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    const int u = tid + i * NT;
+    const int m = u / (kBN / 8), gv = u % (kBN / 8);
+    *reinterpret_cast<u32x4*>(&sVb[m * kBN + swz<kBN / 8>(m, gv) * 8]) = reg[i];
+  }
+}
+
+// S^T = K Q^T for one 64-key tile: 2 key sub-tiles x NQT query sub-tiles.
+// All LDS operand reads of the tile are issued before the first MFMA (the
+// scheduling barrier keeps them there), so LDS latency is paid once per tile
+// instead of once per MFMA.
+template <int D, int NQT>
+NAMOH_DEV void qk_tile(f32x16 (&S)[2][NQT], const uint16_t* __restrict__ sKb,
+                       const bf16x8 (&qB)[NQT][D / 16], int c, int g) {
+  constexpr int KS = D / 16;
+  bf16x8 a[KS][2];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int row = 32 * kk + c;
+      a[ks][kk] = *reinterpret_cast<const bf16x8*>(&sKb[row * D + swz<D / 8>(row, 2 * ks + g) * 8]);
+    }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) S[kk][qt][e] = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt)
+        S[kk][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][kk], qB[qt][ks], S[kk][qt], 0, 0, 0);
+}
+
+// Pieces of one tile's work for the software-pipelined loop.
+template <int D>
+NAMOH_DEV void qk_reads(bf16x8 (&a)[D / 16][2], const uint16_t* __restrict__ sKb, int c, int g) {
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int row = 32 * kk + c;
+      a[ks][kk] = *reinterpret_cast<const bf16x8*>(&sKb[row * D + swz<D / 8>(row, 2 * ks + g) * 8]);
+    }
+}
+
+template <int D, int NQT>
+NAMOH_DEV void qk_mfma(f32x16 (&S)[2][NQT], const bf16x8 (&a)[D / 16][2],
+                       const bf16x8 (&qB)[NQT][D / 16]) {
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) S[kk][qt][e] = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt)
+        S[kk][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][kk], qB[qt][ks], S[kk][qt], 0, 0, 0);
+}
+
+template <int D>
+NAMOH_DEV void v_reads(bf16x8 (&va)[4][D / 32], const uint16_t* __restrict__ sVb, int c, int g) {
+#pragma unroll
+  for (int k2 = 0; k2 < 4; ++k2)
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt) {
+      const int row = 32 * mt + c;
+      va[k2][mt] = *reinterpret_cast<const bf16x8*>(&sVb[row * kBN + swz<kBN / 8>(row, 2 * k2 + g) * 8]);
+    }
+}
+
+// Probabilities of one unmasked tile (branch-free VALU work).
+template <int NQT>
+NAMOH_DEV void softmax_probs(f32x16 (&S)[2][NQT], bf16x8 (&pB)[NQT][4], float (&alpha)[NQT],
+                             bool& rescale, float (&m_run)[NQT], float (&l_run)[NQT],
+                             float scale_log2, float lazy_thr) {
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(S[kk][qt][e], S[kk][qt][e + 1]));
+    mx = pair_max32(mx);
+    const bool up = mx > m_run[qt] + lazy_thr;
+    const float mnew = up ? mx : m_run[qt];
+    alpha[qt] = up ? __builtin_amdgcn_exp2f((m_run[qt] - mnew) * scale_log2) : 1.f;
+    rescale |= up;
+    const float mc = mnew * scale_log2;
+    float ls = 0.f;
+#pragma unroll
+    for (int k2 = 0; k2 < 4; ++k2) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        pB[qt][k2][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(
+            fmaf(S[k2 >> 1][qt][8 * (k2 & 1) + e], scale_log2, -mc)));
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const bf16x2 pr = {pB[qt][k2][e], pB[qt][k2][e + 1]};
+        ls = __builtin_amdgcn_fdot2_f32_bf16(pr, kOnes2, ls, false);
+      }
+    }
+    l_run[qt] = l_run[qt] * alpha[qt] + ls;
+    m_run[qt] = mnew;
+  }
+}
+
+template <int D, int NQT>
+NAMOH_DEV void rescale_o(f32x16 (&O)[D / 32][NQT], const float (&alpha)[NQT]) {
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) O[mt][qt][e] *= alpha[qt];
+}
+
+template <int D, int NQT>
+NAMOH_DEV void pv_mfma(f32x16 (&O)[D / 32][NQT], const bf16x8 (&va)[4][D / 32],
+                       const bf16x8 (&pB)[NQT][4]) {
+#pragma unroll
+  for (int k2 = 0; k2 < 4; ++k2)
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt)
+        O[mt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[k2][mt], pB[qt][k2], O[mt][qt], 0, 0, 0);
+}
+
+// Mask, online softmax and O^T += V^T P^T for one 64-key tile.
+template <int D, int NQT, int NW>
+NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
+                          float (&m_run)[NQT], float (&l_run)[NQT],
+                          const uint16_t* __restrict__ sVb, int key0, int q0,
+                          int wave, int n, int c, int g, float scale_log2,
+                          float lazy_thr) {
+  // value operands: the first VPRE 16-key steps are read while the softmax
+  // runs (all of them for d = 64; half for d = 128, to stay within 256
+  // registers), the rest while the first P.V products execute
+  constexpr int VPRE = D == 128 ? 2 : 4;
+  bf16x8 va[4][D / 32];
+  auto vread = [&](int k2) {
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt) {
+      const int row = 32 * mt + c;
+      va[k2][mt] = *reinterpret_cast<const bf16x8*>(&sVb[row * kBN + swz<kBN / 8>(row, 2 * k2 + g) * 8]);
+    }
+  };
+#pragma unroll
+  for (int k2 = 0; k2 < VPRE; ++k2) vread(k2);
+  // key 32kk + 8j + 4g + i of the tile is visible to query qr iff it is
+  // <= min(qr, n - 1); with lim = min(qr, n - 1) - key0 - 4g the test is a
+  // comparison of a constant with one per-lane value.
+  if (key0 + kBN - 1 > q0 + 32 * wave || key0 + kBN > n) {
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+      const int qr = q0 + 32 * (qt * NW + wave) + c;
+      const int lim = min(qr, n - 1) - key0 - 4 * g;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (32 * kk + 8 * j + i > lim) S[kk][qt][4 * j + i] = -INFINITY;
+    }
+  }
+  bf16x8 pB[NQT][4];
+  float alpha[NQT];
+  bool rescale = false;
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(S[kk][qt][e], S[kk][qt][e + 1]));
+    mx = pair_max32(mx);
+    const bool up = mx > m_run[qt] + lazy_thr;
+    const float mnew = up ? mx : m_run[qt];
+    alpha[qt] = up ? __builtin_amdgcn_exp2f((m_run[qt] - mnew) * scale_log2) : 1.f;
+    rescale |= up;
+    const float mc = mnew * scale_log2;
+    float ls = 0.f;
+#pragma unroll
+    for (int k2 = 0; k2 < 4; ++k2) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        pB[qt][k2][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(
+            fmaf(S[k2 >> 1][qt][8 * (k2 & 1) + e], scale_log2, -mc)));
+      // row sum of the rounded probabilities: pairs times (1, 1)
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const bf16x2 pr = {pB[qt][k2][e], pB[qt][k2][e + 1]};
+        ls = __builtin_amdgcn_fdot2_f32_bf16(pr, kOnes2, ls, false);
+      }
+    }
+    l_run[qt] = l_run[qt] * alpha[qt] + ls;
+    m_run[qt] = mnew;
+  }
+  if (__any(rescale)) {
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+      for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) O[mt][qt][e] *= alpha[qt];
+  }
+#pragma unroll
+  for (int k2 = VPRE; k2 < 4; ++k2) vread(k2);
+#pragma unroll
+  for (int k2 = 0; k2 < 4; ++k2)
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt)
+        O[mt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[k2][mt], pB[qt][k2], O[mt][qt], 0, 0, 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -335,7 +612,7 @@ NAMOH_DEV void tile_gload(const uint16_t* __restrict__ Kp, const uint16_t* __res
 // transposed value tile stores, inside each 16-key group, key 8a + 4g + i at
 // position 8g + 4a + i, so one 16-byte LDS read gives the matching A operand.
 template <int D, int NQT, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void k_attn_mfma(
+__global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kp,
     const uint16_t* __restrict__ Vt, const float2* __restrict__ table,
     const int32_t* __restrict__ seg_offsets, const int32_t* __restrict__ tile_off,
@@ -365,7 +642,6 @@ __global__ __launch_bounds__(NW * 64, 1) void k_attn_mfma(
   const int tid = threadIdx.x;
   const int wave = tid / 64, lane = tid % 64;
   const int c = lane & 31, g = lane >> 5;
-  const int wq_first = q0 + 32 * wave;
   const int wq_last = q0 + 32 * ((NQT - 1) * NW + wave) + 31;
   const int wave_tiles = min(ntiles, wq_last / kBN + 1);
   const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
@@ -409,120 +685,102 @@ __global__ __launch_bounds__(NW * 64, 1) void k_attn_mfma(
     l_run[qt] = 0.f;
   }
 
+#if NAMOH_ATTN_PIPE
+  // ---- software-pipelined tile loop -------------------------------------
+  // Iteration j issues the score MFMAs of tile j + 1 interleaved with the
+  // softmax VALU work of tile j (only the wave's last, diagonal tile needs a
+  // mask, so every other iteration is one branch-free block that the
+  // scheduling barriers below interleave), then the P.V MFMAs of tile j.
+  // LDS holds K_{j+1} and V_j during iteration j; after the barrier that
+  // opens iteration j the wave stores K_{j+2} into the key buffer K_j used
+  // and V_{j+1} into the value buffer V_{j-1} used (both idle: every wave has
+  // left iteration j - 1), and starts the global loads of K_{j+3}, V_{j+2}.
+  constexpr size_t TS = static_cast<size_t>(kBN) * D;
+  const uint16_t* Kbase = Kp + static_cast<size_t>(tile0) * TS;
+  const uint16_t* Vbase = Vt + static_cast<size_t>(tile0) * TS;
   u32x4 kreg[KPT], vreg[KPT];
-  if (kt_end > 0) tile_gload<D, KPT, NT>(Kp, Vt, tile0, tid, kreg, vreg);
-  for (int kt = 0; kt < kt_end; ++kt) {
-    const int buf = kt & 1;
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int u = tid + i * NT;
-      const int row = u / (D / 8), gr = u % (D / 8);
-      *reinterpret_cast<u32x4*>(&sK[buf][row * D + ((gr ^ (row & 7)) * 8)]) = kreg[i];
-      const int m = u / (kBN / 8), gv = u % (kBN / 8);
-      *reinterpret_cast<u32x4*>(&sV[buf][m * kBN + ((gv ^ (m & 7)) * 8)]) = vreg[i];
-    }
+  if (kt_end > 0) {
+    tile_gload<KPT, NT>(Kbase, tid, kreg);
+    tile_gload<KPT, NT>(Vbase, tid, vreg);
+    tile_lstore_k<D, KPT, NT>(sK[0], tid, kreg);
+    tile_lstore_v<D, KPT, NT>(sV[0], tid, vreg);
+  }
+  if (kt_end > 1) {
+    tile_gload<KPT, NT>(Kbase + TS, tid, kreg);
+    tile_lstore_k<D, KPT, NT>(sK[1], tid, kreg);
+  }
+  __syncthreads();
+  if (kt_end > 2) tile_gload<KPT, NT>(Kbase + 2 * TS, tid, kreg);
+  if (kt_end > 1) tile_gload<KPT, NT>(Vbase + TS, tid, vreg);
+  f32x16 SA[2][NQT], SB[2][NQT];
+  if (wave_tiles > 0) qk_tile<D, NQT>(SA, sK[0], qB, c, g);
+
+  auto step = [&](int j, f32x16 (&Scur)[2][NQT], f32x16 (&Snext)[2][NQT]) {
     __syncthreads();
-    if (kt + 1 < kt_end) tile_gload<D, KPT, NT>(Kp, Vt, tile0 + kt + 1, tid, kreg, vreg);
-    if (kt < wave_tiles) {
-      // ---- S^T = K Q^T --------------------------------------------------
-      f32x16 S[2][NQT];
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int qt = 0; qt < NQT; ++qt)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) S[kk][qt][e] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-          const int row = 32 * kk + c;
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-              &sK[buf][row * D + (((2 * ks + g) ^ (row & 7)) * 8)]);
-#pragma unroll
-          for (int qt = 0; qt < NQT; ++qt)
-            S[kk][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qB[qt][ks], S[kk][qt], 0, 0, 0);
-        }
-      }
-      // ---- causal / length mask ----------------------------------------
-      const int key0 = kt * kBN;
-      if (key0 + kBN - 1 > wq_first || key0 + kBN > n) {
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-          for (int qt = 0; qt < NQT; ++qt) {
-            const int qr = q0 + 32 * (qt * NW + wave) + c;
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                const int key = key0 + 32 * kk + 8 * j + 4 * g + i;
-                if (key > qr || key >= n) S[kk][qt][4 * j + i] = -INFINITY;
-              }
-          }
-      }
-      // ---- online softmax ----------------------------------------------
+    if (j + 2 < kt_end) tile_lstore_k<D, KPT, NT>(sK[j & 1], tid, kreg);
+    if (j + 1 < kt_end) tile_lstore_v<D, KPT, NT>(sV[(j + 1) & 1], tid, vreg);
+    if (j + 3 < kt_end) tile_gload<KPT, NT>(Kbase + (j + 3) * TS, tid, kreg);
+    if (j + 2 < kt_end) tile_gload<KPT, NT>(Vbase + (j + 2) * TS, tid, vreg);
+    if (j + 1 < wave_tiles) {
+      bf16x8 ka[D / 16][2];
+      qk_reads<D>(ka, sK[(j + 1) & 1], c, g);
       bf16x8 pB[NQT][4];
       float alpha[NQT];
       bool rescale = false;
+      softmax_probs<NQT>(Scur, pB, alpha, rescale, m_run, l_run, scale_log2, lazy_thr);
+      qk_mfma<D, NQT>(Snext, ka, qB);
+      // interleave: all LDS reads first, then one MFMA per VALU group
 #pragma unroll
-      for (int qt = 0; qt < NQT; ++qt) {
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-          for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(S[kk][qt][e], S[kk][qt][e + 1]));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const bool up = mx > m_run[qt] + lazy_thr;
-        const float mnew = up ? mx : m_run[qt];
-        alpha[qt] = up ? __builtin_amdgcn_exp2f((m_run[qt] - mnew) * scale_log2) : 1.f;
-        rescale |= up;
-        const float mc = mnew * scale_log2;
-        float ls = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const float p = __builtin_amdgcn_exp2f(fmaf(S[kk][qt][e], scale_log2, -mc));
-            S[kk][qt][e] = p;
-            ls += p;
-          }
-        l_run[qt] = l_run[qt] * alpha[qt] + ls;
-        m_run[qt] = mnew;
-#pragma unroll
-        for (int k2 = 0; k2 < 4; ++k2)
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            pB[qt][k2][e] = static_cast<__bf16>(S[k2 >> 1][qt][8 * (k2 & 1) + e]);
+      for (int i = 0; i < 2 * (D / 16) * NQT; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
       }
-      if (__any(rescale)) {
-#pragma unroll
-        for (int qt = 0; qt < NQT; ++qt)
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) O[mt][qt][e] *= alpha[qt];
-      }
-      // ---- O^T += V^T P^T ------------------------------------------------
-#pragma unroll
-      for (int k2 = 0; k2 < 4; ++k2) {
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const int row = 32 * mt + c;
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-              &sV[buf][row * kBN + (((2 * k2 + g) ^ (row & 7)) * 8)]);
-#pragma unroll
-          for (int qt = 0; qt < NQT; ++qt)
-            O[mt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pB[qt][k2], O[mt][qt], 0, 0, 0);
-        }
-      }
+      bf16x8 va[4][D / 32];
+      v_reads<D>(va, sV[j & 1], c, g);
+      if (__any(rescale)) rescale_o<D, NQT>(O, alpha);
+      pv_mfma<D, NQT>(O, va, pB);
+    } else if (j < wave_tiles) {
+      softmax_pv<D, NQT, NW>(Scur, O, m_run, l_run, sV[j & 1], j * kBN, q0, wave, n, c, g,
+                             scale_log2, lazy_thr);
+    }
+  };
+  for (int j = 0; j < kt_end; j += 2) {
+    step(j, SA, SB);
+    if (j + 1 < kt_end) step(j + 1, SB, SA);
+  }
+
+#else
+  // ---- tile loop: double-buffered K/V tiles, one barrier per tile --------
+  constexpr size_t TS = static_cast<size_t>(kBN) * D;
+  const uint16_t* Kbase = Kp + static_cast<size_t>(tile0) * TS;
+  const uint16_t* Vbase = Vt + static_cast<size_t>(tile0) * TS;
+  u32x4 kreg[KPT], vreg[KPT];
+  if (kt_end > 0) {
+    tile_gload<KPT, NT>(Kbase, tid, kreg);
+    tile_gload<KPT, NT>(Vbase, tid, vreg);
+  }
+  for (int kt = 0; kt < kt_end; ++kt) {
+    const int buf = kt & 1;
+    tile_lstore_k<D, KPT, NT>(sK[buf], tid, kreg);
+    tile_lstore_v<D, KPT, NT>(sV[buf], tid, vreg);
+    __syncthreads();
+    if (kt + 1 < kt_end) {
+      tile_gload<KPT, NT>(Kbase + (kt + 1) * TS, tid, kreg);
+      tile_gload<KPT, NT>(Vbase + (kt + 1) * TS, tid, vreg);
+    }
+    if (kt < wave_tiles) {
+      f32x16 S[2][NQT];
+      qk_tile<D, NQT>(S, sK[buf], qB, c, g);
+      softmax_pv<D, NQT, NW>(S, O, m_run, l_run, sV[buf], kt * kBN, q0, wave, n, c, g,
+                             scale_log2, lazy_thr);
     }
   }
 
+#endif
   // ---- epilogue: normalise and store the packed head outputs -----------
 #pragma unroll
   for (int qt = 0; qt < NQT; ++qt) {
-    const float lt = l_run[qt] + __shfl_xor(l_run[qt], 32);
+    const float lt = pair_sum32(l_run[qt]);
     const float inv = 1.f / lt;
     const int r = q0 + 32 * (qt * NW + wave) + c;
     if (r < n) {
