@@ -611,14 +611,14 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
 // are accumulators 8s..8s+7, i.e. keys 8a + 4g + i (a = 0, 1); the
 // transposed value tile stores, inside each 16-key group, key 8a + 4g + i at
 // position 8g + 4a + i, so one 16-byte LDS read gives the matching A operand.
-template <int D, int NQT, int NW>
+template <int D, int NQT, int NW, bool HB>
 __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kp,
     const uint16_t* __restrict__ Vt, const float2* __restrict__ table,
     const int32_t* __restrict__ seg_offsets, const int32_t* __restrict__ tile_off,
     const int32_t* __restrict__ perm_token, const int2* __restrict__ items,
     const int32_t* __restrict__ meta, int T, int H, int rope_mode,
-    float scale_log2, float* __restrict__ hout) {
+    float scale_log2, void* __restrict__ hout) {
   constexpr int BM = 32 * NQT * NW;
   constexpr int KS = D / 16;  // reduction steps of S^T = K Q^T
   constexpr int MT = D / 32;  // 32-row tiles of O^T
@@ -784,15 +784,19 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     const float inv = 1.f / lt;
     const int r = q0 + 32 * (qt * NW + wave) + c;
     if (r < n) {
-      float* orow = hout + static_cast<size_t>(seg0 + r) * D;
+      const size_t orow = static_cast<size_t>(seg0 + r) * D;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int d0 = 32 * mt + 8 * j + 4 * g;
-          *reinterpret_cast<float4*>(orow + d0) =
-              make_float4(O[mt][qt][4 * j] * inv, O[mt][qt][4 * j + 1] * inv,
-                          O[mt][qt][4 * j + 2] * inv, O[mt][qt][4 * j + 3] * inv);
+          const float4 o4 = make_float4(O[mt][qt][4 * j] * inv, O[mt][qt][4 * j + 1] * inv,
+                                        O[mt][qt][4 * j + 2] * inv, O[mt][qt][4 * j + 3] * inv);
+          if constexpr (HB)
+            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(hout) + orow + d0) =
+                make_uint2(pack_bf16x2(o4.x, o4.y), pack_bf16x2(o4.z, o4.w));
+          else
+            *reinterpret_cast<float4*>(static_cast<float*>(hout) + orow + d0) = o4;
         }
     }
   }
@@ -906,9 +910,9 @@ __global__ __launch_bounds__(64) void k_attn_generic(
 }
 
 // ---------------------------------------------------------------------------
-template <bool OUT_BF16>
+template <bool IN_BF16, bool OUT_BF16>
 __global__ __launch_bounds__(256) void k_combine(
-    const float* __restrict__ hout, const float* __restrict__ gates,
+    const void* __restrict__ hout, const float* __restrict__ gates,
     const int32_t* __restrict__ slot_pos, long BT, int K, int D, int Nr,
     void* __restrict__ out) {
   const int C = D / 4;
@@ -921,7 +925,13 @@ __global__ __launch_bounds__(256) void k_combine(
     const int p = slot_pos[tok * K + k];
     if (static_cast<unsigned>(p) >= static_cast<unsigned>(Nr)) continue;
     const float gk = gates[tok * K + k];
-    const float4 x = reinterpret_cast<const float4*>(hout)[static_cast<size_t>(p) * C + cc];
+    float4 x;
+    if constexpr (IN_BF16) {
+      const uint2 u = reinterpret_cast<const uint2*>(hout)[static_cast<size_t>(p) * C + cc];
+      x = make_float4(lo_bf16(u.x), hi_bf16(u.x), lo_bf16(u.y), hi_bf16(u.y));
+    } else {
+      x = reinterpret_cast<const float4*>(hout)[static_cast<size_t>(p) * C + cc];
+    }
     acc.x = fmaf(gk, x.x, acc.x);
     acc.y = fmaf(gk, x.y, acc.y);
     acc.z = fmaf(gk, x.z, acc.z);
@@ -987,7 +997,7 @@ template <int D>
 static void launch_mfma(const AttnWs& w, const void* q, const void* k, const void* v,
                         int B, int T, int H, int rope_mode, float scale_log2,
                         const int32_t* seg_offsets, const int32_t* perm_token,
-                        float* hout, hipStream_t st) {
+                        void* hout, bool hout_bf16, hipStream_t st) {
   constexpr int NW = MfmaShape<D>::NW, NQT = MfmaShape<D>::NQT;
   prof_mark("pack", true, st);
   k_pack_kv<D><<<static_cast<unsigned>(w.max_tiles), 256, 0, st>>>(
@@ -995,9 +1005,14 @@ static void launch_mfma(const AttnWs& w, const void* q, const void* k, const voi
       seg_offsets, w.tile_off, perm_token, w.meta, B * H, T, H, rope_mode, w.Kp, w.Vt);
   prof_mark("pack", false, st);
   prof_mark("attn", true, st);
-  k_attn_mfma<D, NQT, NW><<<static_cast<unsigned>(w.max_items), NW * 64, 0, st>>>(
-      static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.table, seg_offsets, w.tile_off,
-      perm_token, w.items, w.meta, T, H, rope_mode, scale_log2, hout);
+  if (hout_bf16)
+    k_attn_mfma<D, NQT, NW, true><<<static_cast<unsigned>(w.max_items), NW * 64, 0, st>>>(
+        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.table, seg_offsets, w.tile_off,
+        perm_token, w.items, w.meta, T, H, rope_mode, scale_log2, hout);
+  else
+    k_attn_mfma<D, NQT, NW, false><<<static_cast<unsigned>(w.max_items), NW * 64, 0, st>>>(
+        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.table, seg_offsets, w.tile_off,
+        perm_token, w.items, w.meta, T, H, rope_mode, scale_log2, hout);
   prof_mark("attn", false, st);
 }
 
@@ -1020,7 +1035,11 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
                        const int32_t* slot_pos, void* out, int out_dtype,
                        float* head_out, void* ws, hipStream_t st) {
   const AttnWs w = carve_attn(ws, B, T, H, K, d, dtype);
-  float* hout = head_out ? head_out : w.hpack;
+  // Without a caller-supplied head_out, the MFMA path keeps the packed head
+  // outputs in bf16 (half the traffic of the attention epilogue and of the
+  // combine); the combine accumulates in fp32 either way.
+  const bool hb = head_out == nullptr && use_mfma(d, dtype);
+  void* hout = head_out ? static_cast<void*>(head_out) : static_cast<void*>(w.hpack);
   const int BM = block_queries(d, dtype);
   const int Nr = B * T * K;
   const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
@@ -1032,14 +1051,14 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   if (use_mfma(d, dtype)) {
     const float sl2 = scale * 1.4426950408889634f;
     if (d == 64)
-      launch_mfma<64>(w, q, k, v, B, T, H, rope_mode, sl2, seg_offsets, perm_token, hout, st);
+      launch_mfma<64>(w, q, k, v, B, T, H, rope_mode, sl2, seg_offsets, perm_token, hout, hb, st);
     else
-      launch_mfma<128>(w, q, k, v, B, T, H, rope_mode, sl2, seg_offsets, perm_token, hout, st);
+      launch_mfma<128>(w, q, k, v, B, T, H, rope_mode, sl2, seg_offsets, perm_token, hout, hb, st);
   } else {
     const bool bf = dtype == 1;
 #define NAMOH_GEN(DD)                                                                        \
-  (bf ? launch_generic<DD, true>(w, q, k, v, T, H, rope_mode, scale, seg_offsets, perm_token, hout, st) \
-      : launch_generic<DD, false>(w, q, k, v, T, H, rope_mode, scale, seg_offsets, perm_token, hout, st))
+  (bf ? launch_generic<DD, true>(w, q, k, v, T, H, rope_mode, scale, seg_offsets, perm_token, static_cast<float*>(hout), st) \
+      : launch_generic<DD, false>(w, q, k, v, T, H, rope_mode, scale, seg_offsets, perm_token, static_cast<float*>(hout), st))
     if (d == 32) NAMOH_GEN(32);
     else if (d == 64) NAMOH_GEN(64);
     else NAMOH_GEN(128);
@@ -1050,10 +1069,14 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   const long threads = BT * (d / 4);
   const unsigned grid = static_cast<unsigned>((threads + 255) / 256);
   prof_mark("combine", true, st);
-  if (out_dtype == 1)
-    k_combine<true><<<grid, 256, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+  if (hb && out_dtype == 1)
+    k_combine<true, true><<<grid, 256, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+  else if (hb)
+    k_combine<true, false><<<grid, 256, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+  else if (out_dtype == 1)
+    k_combine<false, true><<<grid, 256, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
   else
-    k_combine<false><<<grid, 256, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+    k_combine<false, false><<<grid, 256, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
   prof_mark("combine", false, st);
   return hipGetLastError();
 }

@@ -5,14 +5,13 @@
 // every (batch, head) subsequence): the permutation is a stable counting sort
 // of the (token, head) pairs by segment b*H + h.
 //
-// Three launches, no atomics, so every output is deterministic:
-//   1. k_route_count   one wave per 64-token chunk: the chunk's logits are
-//                      staged through LDS with coalesced loads; one lane per
-//                      token runs K passes of a register argmax over the H
-//                      logits (strict '>' scanning heads upward, so equal
-//                      logits resolve to the lower head index), computes the
-//                      gates, and the wave counts the chunk's tokens per head
-//                      (ballot + popcount).
+// Three launches; the only atomics are integer adds of counts, so every
+// output is deterministic:
+//   1. k_route_count   eight lanes per token, 64 tokens per workgroup: K
+//                      rounds of a cooperative argmax under the total order
+//                      (logit desc, head asc) on order-preserving integer
+//                      keys, the gates, and per 64-token chunk the number of
+//                      tokens routed to each head (LDS integer adds, exact).
 //   2. k_route_scan    one wave per (b, h) segment: exclusive scan of the
 //                      segment's chunk counts and the head length n.
 //   3. k_route_scatter one wave per chunk: the segment offsets of sequence b
@@ -21,76 +20,110 @@
 //                      packed position = segment offset + earlier chunks of the
 //                      segment + lower lanes of this chunk routed to the same
 //                      head (popcount of ballot & lanes-below).
+#include <climits>
+
 #include "common.h"
 #include "internal.h"
 
 namespace namoh {
 
-constexpr int kRC = kRouteChunk;   // 64 tokens = one wave per chunk
+constexpr int kRC = kRouteChunk;   // tokens per chunk
+constexpr int kLPT = 8;            // lanes per token in k_route_count
+constexpr int kCountThreads = kRC * kLPT;
 
+// Order-preserving integer key of a float logit (-0.0 first made +0.0); the
+// map is its own inverse.
+NAMOH_DEV int logit_key(float f) {
+  const int bits = __float_as_int(f == 0.f ? 0.f : f);
+  return bits ^ ((bits >> 31) & 0x7FFFFFFF);
+}
+NAMOH_DEV float key_logit(int k) { return __int_as_float(k ^ ((k >> 31) & 0x7FFFFFFF)); }
+
+// 8 lanes per token, each holding HMAX/8 heads.  Round k picks the largest
+// (key, -head) pair below the previous round's winner: every lane scans its
+// heads, then three xor-shuffles inside the 8-lane group reduce to the
+// winner (larger key, then lower head index).  Real logits have keys above
+// INT_MIN, so the INT_MIN padding of heads >= H never wins while K <= H.
 template <int HMAX>
-__global__ __launch_bounds__(kRC) void k_route_count(
+__global__ __launch_bounds__(kCountThreads) void k_route_count(
     const float* __restrict__ logits, int T, int H, int K, int gate_mode,
     int nchunk, int32_t* __restrict__ topk_idx, float* __restrict__ gates,
     int32_t* __restrict__ chunk_counts) {
-  __shared__ float s_l[kRC * (HMAX + 1)];
+  constexpr int HL = HMAX / kLPT;
+  __shared__ int s_cnt[64];
   const int b = blockIdx.x / nchunk;
   const int c = blockIdx.x - b * nchunk;
-  const int lane = threadIdx.x;
-  const int t0 = c * kRC;
-  const int rows = min(kRC, T - t0);
-  const size_t row0 = static_cast<size_t>(b) * T + t0;
-  const float* src = logits + row0 * H;
-  for (int i = lane; i < rows * H; i += kRC) {
-    const int r = i / H, j = i - (i / H) * H;
-    s_l[r * (HMAX + 1) + j] = src[i];
-  }
-  __syncthreads();
-  const bool valid = lane < rows;
-  float l[HMAX];
-#pragma unroll
-  for (int j = 0; j < HMAX; ++j) l[j] = (valid && j < H) ? s_l[lane * (HMAX + 1) + j] : 0.f;
+  const int tid = threadIdx.x;
+  const int sub = tid % kLPT;
+  const int t = c * kRC + tid / kLPT;
+  const bool valid = t < T;
+  const size_t row = static_cast<size_t>(b) * T + (valid ? t : 0);
+  if (tid < 64) s_cnt[tid] = 0;
 
-  const size_t row = row0 + (valid ? lane : 0);
+  int key[HL];
+  float val[HL];
+  const float* lp = logits + row * H;
+#pragma unroll
+  for (int e = 0; e < HL; ++e) {
+    const int j = sub * HL + e;
+    val[e] = (valid && j < H) ? lp[j] : -INFINITY;
+    key[e] = (valid && j < H) ? logit_key(val[e]) : INT_MIN;
+  }
   int32_t* tk = topk_idx + row * K;
   float* gk = gates + row * K;
-  uint64_t taken = 0;
+  int pk = INT_MAX, pj = -1;     // previous winner
+  unsigned own = 0;              // selected heads owned by this lane
   float lmax = 0.f, denom = 0.f;
   for (int k = 0; k < K; ++k) {
-    int best = -1;
-    float bv = 0.f;
+    int bk = INT_MIN, bj = INT_MAX;
 #pragma unroll
-    for (int j = 0; j < HMAX; ++j) {
-      const bool avail = (j < H) && !((taken >> j) & 1ull);
-      const bool better = avail && (best < 0 || l[j] > bv);
-      best = better ? j : best;
-      bv = better ? l[j] : bv;
+    for (int e = 0; e < HL; ++e) {
+      const int j = sub * HL + e;
+      const bool cand = key[e] < pk || (key[e] == pk && j > pj);
+      const bool better = cand && (key[e] > bk || (key[e] == bk && j < bj));
+      bk = better ? key[e] : bk;
+      bj = better ? j : bj;
     }
-    taken |= 1ull << best;
-    if (k == 0) lmax = bv;
-    const float e = expf(bv - lmax);
+#pragma unroll
+    for (int o = 1; o < kLPT; o <<= 1) {
+      const int ok = __shfl_xor(bk, o, kLPT);
+      const int oj = __shfl_xor(bj, o, kLPT);
+      const bool better = ok > bk || (ok == bk && oj < bj);
+      bk = better ? ok : bk;
+      bj = better ? oj : bj;
+    }
+    pk = bk;
+    pj = bj;
+    if (bj / HL == sub) own |= 1u << (bj - sub * HL);
+    const float v = key_logit(bk);
+    if (k == 0) lmax = v;
+    const float e = expf(v - lmax);
     denom += e;
-    if (valid) {
-      tk[k] = best;
+    if (valid && sub == 0) {
+      tk[k] = bj;
       gk[k] = e;  // unnormalised; scaled below
     }
   }
   if (gate_mode == 1) {  // softmax over all H logits, no renormalisation
-    denom = 0.f;
+    float part = 0.f;
 #pragma unroll
-    for (int j = 0; j < HMAX; ++j)
-      if (j < H) denom += expf(l[j] - lmax);
+    for (int e = 0; e < HL; ++e)
+      if (sub * HL + e < H) part += expf(val[e] - lmax);
+#pragma unroll
+    for (int o = 1; o < kLPT; o <<= 1) part += __shfl_xor(part, o, kLPT);
+    denom = part;
   }
-  if (valid) {
+  if (valid && sub == 0) {
     const float inv = 1.f / denom;
     for (int k = 0; k < K; ++k) gk[k] *= inv;
   }
-  int mine = 0;
-  for (int h = 0; h < H; ++h) {
-    const int cnt = __popcll(__ballot(valid && ((taken >> h) & 1ull)));
-    if (lane == h) mine = cnt;
-  }
-  if (lane < H) chunk_counts[(static_cast<size_t>(b) * H + lane) * nchunk + c] = mine;
+  __syncthreads();
+  if (valid)
+#pragma unroll
+    for (int e = 0; e < HL; ++e)
+      if ((own >> e) & 1u) atomicAdd(&s_cnt[sub * HL + e], 1);
+  __syncthreads();
+  if (tid < H) chunk_counts[(static_cast<size_t>(b) * H + tid) * nchunk + c] = s_cnt[tid];
 }
 
 __global__ __launch_bounds__(kWave) void k_route_scan(
@@ -174,13 +207,13 @@ hipError_t launch_route(const float* logits, int B, int T, int H, int K,
   int32_t* within = cv.take<int32_t>(L);
   const dim3 grid(static_cast<unsigned>(static_cast<size_t>(B) * nchunk));
   if (H <= 8)
-    k_route_count<8><<<grid, kRC, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
+    k_route_count<8><<<grid, kCountThreads, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
   else if (H <= 16)
-    k_route_count<16><<<grid, kRC, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
+    k_route_count<16><<<grid, kCountThreads, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
   else if (H <= 32)
-    k_route_count<32><<<grid, kRC, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
+    k_route_count<32><<<grid, kCountThreads, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
   else
-    k_route_count<64><<<grid, kRC, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
+    k_route_count<64><<<grid, kCountThreads, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   k_route_scan<<<B * H, kWave, 0, st>>>(counts, nchunk, within, head_len);
