@@ -8,11 +8,12 @@
 // or written.  Eq. namoh-kv-cost: the step reads sum over the selected heads
 // of (n + 1) cached rows, which makes it HBM-bound.
 //
-//   k_decode_route_append  one wave per sequence: lane = head; the rank of
-//                          each head under (logit desc, index asc) by H
-//                          comparisons, gates, then for each selected head the
-//                          rotation of q and k at rank n (angles in double),
-//                          the cache append and the length update.
+//   k_decode_route_append  one workgroup per sequence: in every wave lane =
+//                          head, the rank of each head under (logit desc,
+//                          index asc) by H comparisons, gates; then wave w
+//                          handles the selected heads w, w + 4, ...: rotation
+//                          of q and k at rank n (angles in double), the cache
+//                          append and the length update.
 //   k_decode_attn          split over 512-row chunks of every selected head's
 //                          history: 16-byte coalesced loads of K and V rows
 //                          (a row spans d*esize/16 lanes), several rows in
@@ -42,8 +43,10 @@ NAMOH_DEV void st_elem(void* p, size_t i, float x) {
   else static_cast<float*>(p)[i] = x;
 }
 
+constexpr int kAppendWaves = 4;
+
 template <int D, bool BF16>
-__global__ __launch_bounds__(64) void k_decode_route_append(
+__global__ __launch_bounds__(64 * kAppendWaves) void k_decode_route_append(
     const float* __restrict__ logits, const void* __restrict__ q,
     const void* __restrict__ k, const void* __restrict__ v,
     void* __restrict__ k_cache, void* __restrict__ v_cache,
@@ -53,7 +56,8 @@ __global__ __launch_bounds__(64) void k_decode_route_append(
     int32_t* __restrict__ dev_status, float* __restrict__ qrot,
     int32_t* __restrict__ rows) {
   const int b = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x % 64;
+  const int wave = threadIdx.x / 64;
   const bool real = lane < H;
   const float l = real ? logits[static_cast<size_t>(b) * H + lane] : 0.f;
   int rank = 0;
@@ -68,12 +72,13 @@ __global__ __launch_bounds__(64) void k_decode_route_append(
   float e_den = gate_mode == 1 ? (real ? expf(l - lmax) : 0.f) : e_sel;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) e_den += __shfl_xor(e_den, o);
-  if (sel) {
+  if (sel && wave == 0) {
     topk_idx[static_cast<size_t>(b) * K + rank] = lane;
     gates[static_cast<size_t>(b) * K + rank] = e_sel / e_den;
   }
 
-  for (int kk = 0; kk < K; ++kk) {
+  // every wave routed the token; wave w appends heads w, w + 4, ...
+  for (int kk = wave; kk < K; kk += kAppendWaves) {
     const uint64_t mk = __ballot(sel && rank == kk);
     const size_t bk = static_cast<size_t>(b) * K + kk;
     if (mk == 0) {  // only reachable with NaN logits (outside the contract)
@@ -351,7 +356,7 @@ static hipError_t run_decode(const float* logits, const void* q, const void* k,
   const DecWs w = carve_dec(ws, B, K, D, cap);
   const int nc = dec_nchunk(cap);
   const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
-  k_decode_route_append<D, BF16><<<B, 64, 0, st>>>(
+  k_decode_route_append<D, BF16><<<B, 64 * kAppendWaves, 0, st>>>(
       logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, H, K, cap, log_base,
       rope_mode, gate_mode, scale * 1.4426950408889634f, topk_idx, gates,
       dev_status, w.qrot, w.rows);

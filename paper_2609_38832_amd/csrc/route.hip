@@ -44,7 +44,7 @@ NAMOH_DEV float key_logit(int k) { return __int_as_float(k ^ ((k >> 31) & 0x7FFF
 // heads, then three xor-shuffles inside the 8-lane group reduce to the
 // winner (larger key, then lower head index).  Real logits have keys above
 // INT_MIN, so the INT_MIN padding of heads >= H never wins while K <= H.
-template <int HMAX>
+template <int HMAX, int KMAX>
 __global__ __launch_bounds__(kCountThreads) void k_route_count(
     const float* __restrict__ logits, int T, int H, int K, int gate_mode,
     int nchunk, int32_t* __restrict__ topk_idx, float* __restrict__ gates,
@@ -74,7 +74,18 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
   int pk = INT_MAX, pj = -1;     // previous winner
   unsigned own = 0;              // selected heads owned by this lane
   float lmax = 0.f, denom = 0.f;
-  for (int k = 0; k < K; ++k) {
+  // with K <= KMAX (<= 8) the winners stay in registers and lane k of the
+  // group stores round k; otherwise lane 0 stores and rescales in place
+  int wj[KMAX];
+  float we[KMAX];
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    wj[k] = 0;
+    we[k] = 0.f;
+  }
+#pragma unroll (KMAX <= 8 ? KMAX : 1)
+  for (int k = 0; k < (KMAX <= 8 ? KMAX : K); ++k) {
+    if (KMAX <= 8 && k >= K) break;
     int bk = INT_MIN, bj = INT_MAX;
 #pragma unroll
     for (int e = 0; e < HL; ++e) {
@@ -99,7 +110,10 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
     if (k == 0) lmax = v;
     const float e = expf(v - lmax);
     denom += e;
-    if (valid && sub == 0) {
+    if constexpr (KMAX <= 8) {
+      wj[k] = bj;
+      we[k] = e;
+    } else if (valid && sub == 0) {
       tk[k] = bj;
       gk[k] = e;  // unnormalised; scaled below
     }
@@ -113,8 +127,21 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
     for (int o = 1; o < kLPT; o <<= 1) part += __shfl_xor(part, o, kLPT);
     denom = part;
   }
-  if (valid && sub == 0) {
-    const float inv = 1.f / denom;
+  const float inv = 1.f / denom;
+  if constexpr (KMAX <= 8) {
+    int mj = 0;
+    float me = 0.f;
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k)
+      if (sub == k) {
+        mj = wj[k];
+        me = we[k];
+      }
+    if (valid && sub < K) {
+      tk[sub] = mj;
+      gk[sub] = me * inv;
+    }
+  } else if (valid && sub == 0) {
     for (int k = 0; k < K; ++k) gk[k] *= inv;
   }
   __syncthreads();
@@ -206,14 +233,14 @@ hipError_t launch_route(const float* logits, int B, int T, int H, int K,
   int32_t* counts = cv.take<int32_t>(L);
   int32_t* within = cv.take<int32_t>(L);
   const dim3 grid(static_cast<unsigned>(static_cast<size_t>(B) * nchunk));
-  if (H <= 8)
-    k_route_count<8><<<grid, kCountThreads, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
-  else if (H <= 16)
-    k_route_count<16><<<grid, kCountThreads, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
-  else if (H <= 32)
-    k_route_count<32><<<grid, kCountThreads, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
-  else
-    k_route_count<64><<<grid, kCountThreads, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts);
+#define NAMOH_RC(HM, KM) \
+  k_route_count<HM, KM><<<grid, kCountThreads, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts)
+  const bool small_k = K <= 8;
+  if (H <= 8) NAMOH_RC(8, 8);
+  else if (H <= 16) { if (small_k) NAMOH_RC(16, 8); else NAMOH_RC(16, 64); }
+  else if (H <= 32) { if (small_k) NAMOH_RC(32, 8); else NAMOH_RC(32, 64); }
+  else { if (small_k) NAMOH_RC(64, 8); else NAMOH_RC(64, 64); }
+#undef NAMOH_RC
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   k_route_scan<<<B * H, kWave, 0, st>>>(counts, nchunk, within, head_len);
