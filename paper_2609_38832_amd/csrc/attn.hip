@@ -10,9 +10,10 @@
 //
 // Launch sequence for one call:
 //   k_attn_prep   workgroup 0: per segment key-tile counts and their running
-//                 sum (tile_off), the work list of (segment, query block)
-//                 items sorted by causal work, heaviest first (counting sort
-//                 by key-tile count).  Other workgroups: the RoPE table,
+//                 sum (tile_off), and the work list of (segment, query block)
+//                 items: split over the 8 XCDs in segment order by causal
+//                 work, heaviest first inside each XCD (counting sort by
+//                 key-tile count).  Other workgroups: the RoPE table,
 //                 cos/sin of p * base^(-2j/d) from double angles, stored f32.
 //   bf16, d in {64, 128}:
 //     k_pack_kv   gathers each 64-row key tile of a segment by perm_token,
@@ -39,26 +40,25 @@ namespace namoh {
 
 constexpr int kBN = 64;            // keys per tile
 constexpr int kPrepThreads = 1024;
-constexpr int kSortBins = 4096;    // work keys are clamped to this many bins
 
 // mfma kernel shape: waves per workgroup and 32-query sub-tiles per wave
 #ifndef NAMOH_D64_NW
-#define NAMOH_D64_NW 8
+#define NAMOH_D64_NW 4
 #endif
 #ifndef NAMOH_D64_NQT
 #define NAMOH_D64_NQT 1
 #endif
 #ifndef NAMOH_D128_NW
-#define NAMOH_D128_NW 8
+#define NAMOH_D128_NW 4
 #endif
 #ifndef NAMOH_D128_NQT
 #define NAMOH_D128_NQT 1
 #endif
 #ifndef NAMOH_D64_MINB
-#define NAMOH_D64_MINB 1
+#define NAMOH_D64_MINB 2
 #endif
 #ifndef NAMOH_D128_MINB
-#define NAMOH_D128_MINB 1
+#define NAMOH_D128_MINB 2
 #endif
 // NW waves per workgroup, NQT 32-query sub-tiles per wave, MINB workgroups
 // per compute unit the register allocation must allow.
@@ -78,19 +78,36 @@ template <> struct MfmaShape<128> {
 constexpr float kLazyLog2 = 8.f;
 constexpr int kGenericBM = 64;
 
-enum Meta { kMetaItems = 0, kMetaTiles = 1, kMetaTablePos = 2, kMetaBad = 3, kMetaCount = 4 };
+// Work items are (segment, query block).  They are split over the 8 XCDs
+// (each with its own L2): items are laid out in segment order, and an item
+// goes to XCD floor(8 * work before it / total work), so every XCD gets an
+// eighth of the causal work and a segment's key/value tiles stay in one L2
+// (a segment spans two XCDs only at a split point).  Inside an XCD the items
+// run heaviest first (longest-processing-time order).  Workgroup i runs item
+// rank i / 8 of XCD i % 8, matching the round-robin order in which the
+// hardware hands workgroups to XCDs.
+constexpr int kXcd = 8;
+constexpr int kXcdBins = 1024;     // work keys per XCD, clamped to this many
+enum Meta {
+  kMetaItems = 0, kMetaTiles = 1, kMetaTablePos = 2, kMetaBad = 3, kMetaStride = 4,
+  kMetaXcd = 8, kMetaCount = 16
+};
 
 // ---------------------------------------------------------------------------
 NAMOH_DEV void attn_schedule(
     const int32_t* __restrict__ seg_offsets, int BH, int T, int BM,
     int rope_mode, int Nr, int max_items, int32_t* __restrict__ tile_off,
-    int2* __restrict__ items, int32_t* __restrict__ meta) {
-  __shared__ int s_hist[kSortBins];
+    long long* __restrict__ work_off, int2* __restrict__ items,
+    int32_t* __restrict__ meta) {
+  __shared__ int s_hist[kXcd * kXcdBins];
   __shared__ int s_wave[kPrepThreads / kWave + 1];
+  __shared__ int s_xbase[kXcd + 1];
   __shared__ int s_maxn;
   __shared__ int s_bad;
+  __shared__ long long s_lwave[kPrepThreads / kWave + 1];
   const int tid = threadIdx.x;
-  for (int i = tid; i < kSortBins; i += kPrepThreads) s_hist[i] = 0;
+  const int per_qb = BM / kBN;           // key tiles added per query block
+  for (int i = tid; i < kXcd * kXcdBins; i += kPrepThreads) s_hist[i] = 0;
   if (tid == 0) {
     s_maxn = 0;
     s_bad = seg_offsets[0] != 0 || seg_offsets[BH] != Nr;
@@ -107,35 +124,80 @@ NAMOH_DEV void attn_schedule(
       meta[kMetaTiles] = 0;
       meta[kMetaTablePos] = 0;
       meta[kMetaBad] = 1;
+      meta[kMetaStride] = max_items;
+      for (int x = 0; x < kXcd; ++x) meta[kMetaXcd + x] = 0;
     }
     return;
   }
 
-  // key-tile running sum, longest segment, histogram of item work
+  // pass 1: key-tile running sum (tile_off), longest segment, work running
+  // sum over segments (work_off)
   int carry = 0;
+  long long wcarry = 0;
   for (int start = 0; start < BH; start += kPrepThreads) {
     const int s = start + tid;
     const int n = s < BH ? seg_offsets[s + 1] - seg_offsets[s] : 0;
     const int tiles = (n + kBN - 1) / kBN;
     if (n > 0) atomicMax(&s_maxn, n);
     const int nqb = (n + BM - 1) / BM;
-    for (int qb = 0; qb < nqb; ++qb) {
-      const int w = min(tiles, (qb + 1) * BM / kBN);
-      atomicAdd(&s_hist[kSortBins - 1 - min(w, kSortBins - 1)], 1);
-    }
+    long long wsum = 0;
+    for (int qb = 0; qb < nqb; ++qb) wsum += min(tiles, (qb + 1) * per_qb);
     int total;
     const int ex = block_exclusive_scan<kPrepThreads>(tiles, s_wave, total);
-    if (s < BH) tile_off[s] = carry + ex;
+    // 64-bit exclusive scan of the segment work (wave scans + one wave)
+    long long incl = wsum;
+    const int lane = tid % kWave, wave = tid / kWave;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const long long y = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += y;
+    }
+    if (lane == kWave - 1) s_lwave[wave] = incl;
+    __syncthreads();
+    if (tid == 0) {
+      long long acc = 0;
+      for (int w = 0; w < kPrepThreads / kWave; ++w) {
+        const long long v = s_lwave[w];
+        s_lwave[w] = acc;
+        acc += v;
+      }
+      s_lwave[kPrepThreads / kWave] = acc;
+    }
+    __syncthreads();
+    if (s < BH) {
+      tile_off[s] = carry + ex;
+      work_off[s] = wcarry + s_lwave[wave] + incl - wsum;
+    }
     carry += total;
+    wcarry += s_lwave[kPrepThreads / kWave];
+    __syncthreads();
   }
+  const long long wtotal = wcarry > 0 ? wcarry : 1;
   if (tid == 0) {
     tile_off[BH] = carry;
     meta[kMetaBad] = 0;
     meta[kMetaTiles] = carry;
     meta[kMetaTablePos] = rope_mode == 0 ? s_maxn : (rope_mode == 1 ? T : 0);
+    meta[kMetaStride] = max_items;
   }
-  // exclusive scan of the histogram -> insertion cursors (heaviest first)
-  constexpr int PER = kSortBins / kPrepThreads;
+  __syncthreads();
+  // pass 2: histogram of item work per XCD
+  for (int s = tid; s < BH; s += kPrepThreads) {
+    const int n = seg_offsets[s + 1] - seg_offsets[s];
+    const int tiles = (n + kBN - 1) / kBN;
+    const int nqb = (n + BM - 1) / BM;
+    long long before = work_off[s];
+    for (int qb = 0; qb < nqb; ++qb) {
+      const int w = min(tiles, (qb + 1) * per_qb);
+      const int x = static_cast<int>(min(static_cast<long long>(kXcd - 1), before * kXcd / wtotal));
+      atomicAdd(&s_hist[x * kXcdBins + kXcdBins - 1 - min(w, kXcdBins - 1)], 1);
+      before += w;
+    }
+  }
+  __syncthreads();
+  // per-XCD exclusive scans of the histograms (heaviest bin first)
+  constexpr int PER = kXcd * kXcdBins / kPrepThreads;
+  constexpr int TPX = kPrepThreads / kXcd;   // threads per XCD
   int h[PER];
   int sum = 0;
 #pragma unroll
@@ -145,23 +207,42 @@ NAMOH_DEV void attn_schedule(
   }
   int total;
   int run = block_exclusive_scan<kPrepThreads>(sum, s_wave, total);
+  if (tid % TPX == 0) s_xbase[tid / TPX] = run;
+  if (tid == 0) s_xbase[kXcd] = total;
+  __syncthreads();
+  run -= s_xbase[tid / TPX];
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     s_hist[tid * PER + i] = run;
     run += h[i];
   }
-  if (tid == 0) meta[kMetaItems] = min(total, max_items);
+  if (tid < kXcd) meta[kMetaXcd + tid] = min(s_xbase[tid + 1] - s_xbase[tid], max_items);
+  if (tid == 0) meta[kMetaItems] = total;
   __syncthreads();
+  // pass 3: place the items
   for (int s = tid; s < BH; s += kPrepThreads) {
     const int n = seg_offsets[s + 1] - seg_offsets[s];
     const int tiles = (n + kBN - 1) / kBN;
     const int nqb = (n + BM - 1) / BM;
+    long long before = work_off[s];
     for (int qb = 0; qb < nqb; ++qb) {
-      const int w = min(tiles, (qb + 1) * BM / kBN);
-      const int pos = atomicAdd(&s_hist[kSortBins - 1 - min(w, kSortBins - 1)], 1);
-      if (pos < max_items) items[pos] = make_int2(s, qb);
+      const int w = min(tiles, (qb + 1) * per_qb);
+      const int x = static_cast<int>(min(static_cast<long long>(kXcd - 1), before * kXcd / wtotal));
+      const int pos = atomicAdd(&s_hist[x * kXcdBins + kXcdBins - 1 - min(w, kXcdBins - 1)], 1);
+      if (pos < max_items) items[static_cast<size_t>(x) * max_items + pos] = make_int2(s, qb);
+      before += w;
     }
   }
+}
+
+// Work item of this workgroup, or false if it has none.
+NAMOH_DEV bool my_item(const int2* __restrict__ items, const int32_t* __restrict__ meta,
+                       int2& it) {
+  const int x = blockIdx.x % kXcd;
+  const int rank = blockIdx.x / kXcd;
+  if (rank >= meta[kMetaXcd + x]) return false;
+  it = items[static_cast<size_t>(x) * meta[kMetaStride] + rank];
+  return true;
 }
 
 // ---------------------------------------------------------------------------
@@ -172,10 +253,11 @@ NAMOH_DEV void attn_schedule(
 __global__ __launch_bounds__(kPrepThreads) void k_attn_prep(
     const int32_t* __restrict__ seg_offsets, int BH, int T, int BM,
     int rope_mode, int Nr, int max_items, int d, double log_base,
-    int32_t* __restrict__ tile_off, int2* __restrict__ items,
-    int32_t* __restrict__ meta, float2* __restrict__ table) {
+    int32_t* __restrict__ tile_off, long long* __restrict__ work_off,
+    int2* __restrict__ items, int32_t* __restrict__ meta, float2* __restrict__ table) {
   if (blockIdx.x == 0) {
-    attn_schedule(seg_offsets, BH, T, BM, rope_mode, Nr, max_items, tile_off, items, meta);
+    attn_schedule(seg_offsets, BH, T, BM, rope_mode, Nr, max_items, tile_off, work_off, items,
+                  meta);
     return;
   }
   if (rope_mode == 2) return;
@@ -377,6 +459,30 @@ NAMOH_DEV void tile_lstore_v(uint16_t* sVb, int tid, const u32x4 (&reg)[KPT]) {
   }
 }
 
+// Direct global -> LDS staging (global_load_lds_dwordx4): lane l of a wave
+// instruction writes LDS granule base + l, so the swizzle is applied on the
+// global side: the lane that fills physical granule P = row * GPR + phys
+// fetches logical granule swz(row, phys) of that row (the XOR is its own
+// inverse).  Completion is tracked by vmcnt: wait_tile_dma() before the
+// barrier that publishes the tile.
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+template <int GPR, int KPT, int NT>
+NAMOH_DEV void tile_dma(const uint16_t* __restrict__ tile, uint16_t* lds_tile, int tid) {
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    const int P = tid + i * NT;                 // physical granule of this lane
+    const int row = P / GPR, phys = P % GPR;
+    const int gr = swz<GPR>(row, phys);
+    const uint16_t* src = tile + (row * GPR + gr) * 8;
+    uint16_t* dst = lds_tile + (P - (tid & 63)) * 8;   // wave-uniform base
+    __builtin_amdgcn_global_load_lds((glb_void_t*)(src), (lds_void_t*)(dst), 16, 0, 0);
+  }
+}
+
+NAMOH_DEV void wait_tile_dma() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+
 // S^T = K Q^T for one 64-key tile: 2 key sub-tiles x NQT query sub-tiles.
 // All LDS operand reads of the tile are issued before the first MFMA (the
 // scheduling barrier keeps them there), so LDS latency is paid once per tile
@@ -508,6 +614,68 @@ NAMOH_DEV void pv_mfma(f32x16 (&O)[D / 32][NQT], const bf16x8 (&va)[4][D / 32],
         O[mt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[k2][mt], pB[qt][k2], O[mt][qt], 0, 0, 0);
 }
 
+// Single 32-query sub-tile versions (the two-sub-tile ping-pong loop).
+template <int D>
+NAMOH_DEV void qk_mfma1(f32x16 (&S)[2], const bf16x8 (&a)[D / 16][2], const bf16x8 (&qB)[D / 16]) {
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) S[kk][e] = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+      S[kk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][kk], qB[ks], S[kk], 0, 0, 0);
+}
+
+NAMOH_DEV void softmax_probs1(f32x16 (&S)[2], bf16x8 (&pB)[4], float& alpha, bool& rescale,
+                              float& m_run, float& l_run, float scale_log2, float lazy_thr) {
+  float mx = -INFINITY;
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+    for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(S[kk][e], S[kk][e + 1]));
+  mx = pair_max32(mx);
+  const bool up = mx > m_run + lazy_thr;
+  const float mnew = up ? mx : m_run;
+  alpha = up ? __builtin_amdgcn_exp2f((m_run - mnew) * scale_log2) : 1.f;
+  rescale = up;
+  const float mc = mnew * scale_log2;
+  float ls = 0.f;
+#pragma unroll
+  for (int k2 = 0; k2 < 4; ++k2) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      pB[k2][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(
+          fmaf(S[k2 >> 1][8 * (k2 & 1) + e], scale_log2, -mc)));
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const bf16x2 pr = {pB[k2][e], pB[k2][e + 1]};
+      ls = __builtin_amdgcn_fdot2_f32_bf16(pr, kOnes2, ls, false);
+    }
+  }
+  l_run = l_run * alpha + ls;
+  m_run = mnew;
+}
+
+template <int D, int NQT, int QT>
+NAMOH_DEV void pv_mfma_q(f32x16 (&O)[D / 32][NQT], const bf16x8 (&va)[4][D / 32],
+                         const bf16x8 (&pB)[4]) {
+#pragma unroll
+  for (int k2 = 0; k2 < 4; ++k2)
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt)
+      O[mt][QT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[k2][mt], pB[k2], O[mt][QT], 0, 0, 0);
+}
+
+template <int D, int NQT, int QT>
+NAMOH_DEV void rescale_q(f32x16 (&O)[D / 32][NQT], float alpha) {
+#pragma unroll
+  for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) O[mt][QT][e] *= alpha;
+}
+
 // Mask, online softmax and O^T += V^T P^T for one 64-key tile.
 template <int D, int NQT, int NW>
 NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
@@ -629,8 +797,8 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   __shared__ __attribute__((aligned(16))) uint16_t sK[2][kBN * D];
   __shared__ __attribute__((aligned(16))) uint16_t sV[2][D * kBN];
 
-  if (static_cast<int>(blockIdx.x) >= meta[kMetaItems]) return;
-  const int2 it = items[blockIdx.x];
+  int2 it;
+  if (!my_item(items, meta, it)) return;
   const int s = it.x;
   const int q0 = it.y * BM;
   const int b = s / H, h = s - (s / H) * H;
@@ -685,7 +853,66 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     l_run[qt] = 0.f;
   }
 
-#if NAMOH_ATTN_PIPE
+#if NAMOH_ATTN_PIPE == 2
+  // ---- two-sub-tile ping-pong -------------------------------------------
+  // Each wave owns two 32-query sub-tiles.  On tiles that need no mask, the
+  // score MFMAs of sub-tile 1 are interleaved with the softmax of sub-tile 0,
+  // and the P.V MFMAs of sub-tile 0 with the softmax of sub-tile 1, so the
+  // wave keeps its matrix and vector pipes busy at the same time.
+  static_assert(NQT == 2, "ping-pong loop needs two query sub-tiles per wave");
+  constexpr size_t TS = static_cast<size_t>(kBN) * D;
+  const uint16_t* Kbase = Kp + static_cast<size_t>(tile0) * TS;
+  const uint16_t* Vbase = Vt + static_cast<size_t>(tile0) * TS;
+  if (kt_end > 0) {
+    tile_dma<D / 8, KPT, NT>(Kbase, sK[0], tid);
+    tile_dma<kBN / 8, KPT, NT>(Vbase, sV[0], tid);
+  }
+  for (int kt = 0; kt < kt_end; ++kt) {
+    const int buf = kt & 1;
+    wait_tile_dma();
+    __syncthreads();
+    if (kt + 1 < kt_end) {
+      tile_dma<D / 8, KPT, NT>(Kbase + (kt + 1) * TS, sK[buf ^ 1], tid);
+      tile_dma<kBN / 8, KPT, NT>(Vbase + (kt + 1) * TS, sV[buf ^ 1], tid);
+    }
+    if (kt >= wave_tiles) continue;
+    const int key0 = kt * kBN;
+    if (key0 + kBN - 1 > q0 + 32 * wave || key0 + kBN > n) {
+      f32x16 S[2][NQT];
+      qk_tile<D, NQT>(S, sK[buf], qB, c, g);
+      softmax_pv<D, NQT, NW>(S, O, m_run, l_run, sV[buf], key0, q0, wave, n, c, g,
+                             scale_log2, lazy_thr);
+      continue;
+    }
+    bf16x8 ka[KS][2];
+    qk_reads<D>(ka, sK[buf], c, g);
+    f32x16 S0[2], S1[2];
+    qk_mfma1<D>(S0, ka, qB[0]);
+    qk_mfma1<D>(S1, ka, qB[1]);
+    bf16x8 p0[4], p1[4];
+    float a0, a1;
+    bool r0, r1;
+    softmax_probs1(S0, p0, a0, r0, m_run[0], l_run[0], scale_log2, lazy_thr);
+#pragma unroll
+    for (int i = 0; i < 2 * KS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 1);
+    }
+    bf16x8 va[4][MT];
+    v_reads<D>(va, sV[buf], c, g);
+    if (__any(r0)) rescale_q<D, NQT, 0>(O, a0);
+    pv_mfma_q<D, NQT, 0>(O, va, p0);
+    softmax_probs1(S1, p1, a1, r1, m_run[1], l_run[1], scale_log2, lazy_thr);
+#pragma unroll
+    for (int i = 0; i < 4 * MT; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 2);
+    }
+    if (__any(r1)) rescale_q<D, NQT, 1>(O, a1);
+    pv_mfma_q<D, NQT, 1>(O, va, p1);
+  }
+
+#elif NAMOH_ATTN_PIPE
   // ---- software-pipelined tile loop -------------------------------------
   // Iteration j issues the score MFMAs of tile j + 1 interleaved with the
   // softmax VALU work of tile j (only the wave's last, diagonal tile needs a
@@ -751,22 +978,23 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
 
 #else
   // ---- tile loop: double-buffered K/V tiles, one barrier per tile --------
+  // Tile kt + 1 is copied straight into the idle LDS buffer (global -> LDS)
+  // while tile kt is computed; the barrier at the top of the next iteration
+  // publishes it.
   constexpr size_t TS = static_cast<size_t>(kBN) * D;
   const uint16_t* Kbase = Kp + static_cast<size_t>(tile0) * TS;
   const uint16_t* Vbase = Vt + static_cast<size_t>(tile0) * TS;
-  u32x4 kreg[KPT], vreg[KPT];
   if (kt_end > 0) {
-    tile_gload<KPT, NT>(Kbase, tid, kreg);
-    tile_gload<KPT, NT>(Vbase, tid, vreg);
+    tile_dma<D / 8, KPT, NT>(Kbase, sK[0], tid);
+    tile_dma<kBN / 8, KPT, NT>(Vbase, sV[0], tid);
   }
   for (int kt = 0; kt < kt_end; ++kt) {
     const int buf = kt & 1;
-    tile_lstore_k<D, KPT, NT>(sK[buf], tid, kreg);
-    tile_lstore_v<D, KPT, NT>(sV[buf], tid, vreg);
+    wait_tile_dma();
     __syncthreads();
     if (kt + 1 < kt_end) {
-      tile_gload<KPT, NT>(Kbase + (kt + 1) * TS, tid, kreg);
-      tile_gload<KPT, NT>(Vbase + (kt + 1) * TS, tid, vreg);
+      tile_dma<D / 8, KPT, NT>(Kbase + (kt + 1) * TS, sK[buf ^ 1], tid);
+      tile_dma<kBN / 8, KPT, NT>(Vbase + (kt + 1) * TS, sV[buf ^ 1], tid);
     }
     if (kt < wave_tiles) {
       f32x16 S[2][NQT];
@@ -841,8 +1069,8 @@ __global__ __launch_bounds__(64) void k_attn_generic(
     int H, int rope_mode, float scale, float* __restrict__ hout) {
   __shared__ float sK[kBN][D + 1];
   __shared__ float sV[kBN][D + 1];
-  if (static_cast<int>(blockIdx.x) >= meta[kMetaItems]) return;
-  const int2 it = items[blockIdx.x];
+  int2 it;
+  if (!my_item(items, meta, it)) return;
   const int s = it.x;
   const int q0 = it.y * kGenericBM;
   const int b = s / H, h = s - (s / H) * H;
@@ -957,6 +1185,7 @@ static int block_queries(int d, int dtype) {
 struct AttnWs {
   int32_t* meta;
   int32_t* tile_off;
+  long long* work_off;
   int2* items;
   float2* table;
   uint16_t* Kp;
@@ -976,7 +1205,8 @@ static AttnWs carve_attn(void* ws, int B, int T, int H, int K, int d, int dtype)
   Carver cv(ws);
   w.meta = cv.take<int32_t>(kMetaCount);
   w.tile_off = cv.take<int32_t>(BH + 1);
-  w.items = cv.take<int2>(w.max_items);
+  w.work_off = cv.take<long long>(BH + 1);
+  w.items = cv.take<int2>(kXcd * w.max_items);
   w.table = cv.take<float2>(static_cast<size_t>(T) * (d / 2));
   if (use_mfma(d, dtype)) {
     w.Kp = cv.take<uint16_t>(w.max_tiles * kBN * d);
@@ -1006,11 +1236,11 @@ static void launch_mfma(const AttnWs& w, const void* q, const void* k, const voi
   prof_mark("pack", false, st);
   prof_mark("attn", true, st);
   if (hout_bf16)
-    k_attn_mfma<D, NQT, NW, true><<<static_cast<unsigned>(w.max_items), NW * 64, 0, st>>>(
+    k_attn_mfma<D, NQT, NW, true><<<static_cast<unsigned>(kXcd * w.max_items), NW * 64, 0, st>>>(
         static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.table, seg_offsets, w.tile_off,
         perm_token, w.items, w.meta, T, H, rope_mode, scale_log2, hout);
   else
-    k_attn_mfma<D, NQT, NW, false><<<static_cast<unsigned>(w.max_items), NW * 64, 0, st>>>(
+    k_attn_mfma<D, NQT, NW, false><<<static_cast<unsigned>(kXcd * w.max_items), NW * 64, 0, st>>>(
         static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.table, seg_offsets, w.tile_off,
         perm_token, w.items, w.meta, T, H, rope_mode, scale_log2, hout);
   prof_mark("attn", false, st);
@@ -1022,7 +1252,7 @@ static void launch_generic(const AttnWs& w, const void* q, const void* k, const 
                            const int32_t* seg_offsets, const int32_t* perm_token,
                            float* hout, hipStream_t st) {
   prof_mark("attn", true, st);
-  k_attn_generic<D, BF16><<<static_cast<unsigned>(w.max_items), 64, 0, st>>>(
+  k_attn_generic<D, BF16><<<static_cast<unsigned>(kXcd * w.max_items), 64, 0, st>>>(
       q, k, v, w.table, seg_offsets, perm_token, w.items, w.meta, T, H, rope_mode,
       scale, hout);
   prof_mark("attn", false, st);
@@ -1045,7 +1275,7 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
   k_attn_prep<<<1 + 64, kPrepThreads, 0, st>>>(seg_offsets, B * H, T, BM, rope_mode, Nr,
                                                static_cast<int>(w.max_items), d, log_base,
-                                               w.tile_off, w.items, w.meta, w.table);
+                                               w.tile_off, w.work_off, w.items, w.meta, w.table);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (use_mfma(d, dtype)) {
