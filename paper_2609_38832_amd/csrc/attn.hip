@@ -9,25 +9,25 @@
 // are interleaved across compute units.
 //
 // Launch sequence for one call:
-//   k_attn_prep   workgroup 0: per segment key-tile counts and their running
-//                 sum (tile_off), and the work list of (segment, query block)
-//                 items: split over the 8 XCDs in segment order by causal
-//                 work, heaviest first inside each XCD (counting sort by
-//                 key-tile count).  Other workgroups: the RoPE table,
-//                 cos/sin of p * base^(-2j/d) from double angles, stored f32.
+//   k_rope_table  cos/sin of p * base^(-2j/d), angles formed and reduced in
+//                 double, stored f32 (skipped without RoPE).
 //   bf16, d in {64, 128}:
-//     k_pack_kv   gathers each 64-row key tile of a segment by perm_token,
-//                 applies RoPE at the key's rank while loading it, rounds to
-//                 bf16 (packed row-major), and writes the values as a
-//                 transposed d x 64 tile (the operand layout of the P.V
-//                 product).  The packed rotated keys / values are what a
-//                 prefill hands to the per-head decode caches.
+//     k_pack_kv   workgroup 0 builds the work list of (segment, query block)
+//                 items sorted by causal work, heaviest first (counting sort
+//                 by key-tile count).  Every other workgroup gathers one
+//                 64-row key tile of a segment by perm_token, applies RoPE at
+//                 the key's rank while loading it, rounds to bf16 (packed
+//                 row-major), and writes the values as a transposed d x 64
+//                 tile (the operand layout of the P.V product).  The packed
+//                 rotated keys / values are what a prefill hands to the
+//                 per-head decode caches.
 //     k_attn_mfma one workgroup per work item: the query block is gathered
-//                 and rotated into registers once; key/value tiles are
-//                 double-buffered through LDS; S^T = K Q^T and O^T += V^T P^T
+//                 and rotated into registers once; key/value tiles stream
+//                 through a ring of LDS stages; S^T = K Q^T and O^T += V^T P^T
 //                 run on v_mfma_f32_32x32x16_bf16 with fp32 accumulation and
 //                 an fp32 online softmax (exp2).
 //   other dtype / width:
+//     k_attn_schedule  the work list alone.
 //     k_attn_generic  fp32 arithmetic, one lane per query, keys gathered and
 //                 rotated while staging each tile.
 //   k_combine     o_t = sum_k gate(t,k) * h[slot_pos(t,k)] in k order.
@@ -39,7 +39,6 @@
 namespace namoh {
 
 constexpr int kBN = 64;            // keys per tile
-constexpr int kPrepThreads = 1024;
 
 // mfma kernel shape: waves per workgroup and 32-query sub-tiles per wave
 #ifndef NAMOH_D64_NW
@@ -62,240 +61,250 @@ constexpr int kPrepThreads = 1024;
 #endif
 // NW waves per workgroup, NQT 32-query sub-tiles per wave, MINB workgroups
 // per compute unit the register allocation must allow.
+#ifndef NAMOH_D64_NS
+#define NAMOH_D64_NS 2
+#endif
+#ifndef NAMOH_D128_NS
+#define NAMOH_D128_NS 2
+#endif
+// NS key/value tile stages in LDS (NS - 1 tiles in flight while one is used).
 template <int D> struct MfmaShape;
 template <> struct MfmaShape<64> {
-  static constexpr int NW = NAMOH_D64_NW, NQT = NAMOH_D64_NQT, MINB = NAMOH_D64_MINB;
+  static constexpr int NW = NAMOH_D64_NW, NQT = NAMOH_D64_NQT, MINB = NAMOH_D64_MINB,
+                       NS = NAMOH_D64_NS;
 };
 template <> struct MfmaShape<128> {
-  static constexpr int NW = NAMOH_D128_NW, NQT = NAMOH_D128_NQT, MINB = NAMOH_D128_MINB;
+  static constexpr int NW = NAMOH_D128_NW, NQT = NAMOH_D128_NQT, MINB = NAMOH_D128_MINB,
+                       NS = NAMOH_D128_NS;
 };
-#ifndef NAMOH_ATTN_PIPE
-#define NAMOH_ATTN_PIPE 0
-#endif
 // The running softmax maximum is only raised when a tile exceeds it by more
 // than 2^kLazyLog2 (probabilities then stay below 2^kLazyLog2 and the final
 // normalisation is exact), so the output accumulator is rarely rescaled.
 constexpr float kLazyLog2 = 8.f;
 constexpr int kGenericBM = 64;
 
-// Work items are (segment, query block).  They are split over the 8 XCDs
-// (each with its own L2): items are laid out in segment order, and an item
-// goes to XCD floor(8 * work before it / total work), so every XCD gets an
-// eighth of the causal work and a segment's key/value tiles stay in one L2
-// (a segment spans two XCDs only at a split point).  Inside an XCD the items
-// run heaviest first (longest-processing-time order).  Workgroup i runs item
-// rank i / 8 of XCD i % 8, matching the round-robin order in which the
-// hardware hands workgroups to XCDs.
-constexpr int kXcd = 8;
-constexpr int kXcdBins = 1024;     // work keys per XCD, clamped to this many
-enum Meta {
-  kMetaItems = 0, kMetaTiles = 1, kMetaTablePos = 2, kMetaBad = 3, kMetaStride = 4,
-  kMetaXcd = 8, kMetaCount = 16
+constexpr int kSortBins = 2048;    // work keys (key tiles) are clamped to this many bins
+constexpr int kSegLds = 1024;      // segment offsets staged in LDS up to this many segments
+constexpr int kPackThreads = 256;
+enum Meta { kMetaItems = 0, kMetaBad = 1, kMetaCount = 4 };
+
+// Packed key tiles of segment s (first packed row seg0, length n) are
+// numbered from seg_tile0 = floor(seg0 / 64) + s.  The ranges of successive
+// segments are disjoint and increasing, because
+// floor((seg0 + n) / 64) - floor(seg0 / 64) + 1 >= ceil(n / 64), and every
+// index stays below Nr / 64 + BH + 1, so no running sum is needed.
+NAMOH_DEV int seg_tile0(int seg0, int s) { return seg0 / kBN + s; }
+
+// One work item, a (segment, query block) pair with everything the attention
+// workgroup needs before its first load, so an item costs one dependent
+// global read.
+struct __attribute__((aligned(32))) WorkItem {
+  int s, qb, seg0, n;            // segment b*H + h, query block, first packed row, length
+  int tile0, pad0, pad1, pad2;   // first packed key tile of the segment
 };
 
 // ---------------------------------------------------------------------------
-NAMOH_DEV void attn_schedule(
-    const int32_t* __restrict__ seg_offsets, int BH, int T, int BM,
-    int rope_mode, int Nr, int max_items, int32_t* __restrict__ tile_off,
-    long long* __restrict__ work_off, int2* __restrict__ items,
-    int32_t* __restrict__ meta) {
-  __shared__ int s_hist[kXcd * kXcdBins];
-  __shared__ int s_wave[kPrepThreads / kWave + 1];
-  __shared__ int s_xbase[kXcd + 1];
-  __shared__ int s_maxn;
-  __shared__ int s_bad;
-  __shared__ long long s_lwave[kPrepThreads / kWave + 1];
+// LDS atomic add of `add` to bins[key] for the active lanes of a wave, one
+// atomic per distinct key (lanes with equal keys are served by the lowest of
+// them); returns, for each active lane, the bin's old value plus the number
+// of lower lanes of the wave with the same key.
+NAMOH_DEV int wave_bin_add(int* bins, int key, bool active) {
+  const int lane = __lane_id();
+  uint64_t todo = __ballot(active);
+  int result = 0;
+  while (todo) {
+    const int leader = __ffsll(static_cast<unsigned long long>(todo)) - 1;
+    const int k = __shfl(key, leader);
+    const uint64_t m = __ballot(active && key == k);
+    int base = 0;
+    if (lane == leader) base = atomicAdd(&bins[k], __popcll(m));
+    base = __shfl(base, leader);
+    if (active && key == k) result = base + __popcll(m & lanemask_lt());
+    todo &= ~m;
+  }
+  return result;
+}
+
+// ---------------------------------------------------------------------------
+// The work list: items sorted by causal work (key tiles), heaviest first,
+// by a counting sort; workgroup i runs item i, and the hardware dispatches
+// workgroups in index order, which makes the assignment to compute units
+// longest-processing-time first.  (Placing items by XCD so that a segment's
+// key/value tiles stay in one L2 measured no faster: the tiles are re-read
+// from the shared last-level cache at a rate the kernel does not saturate.)
+// The sort visits the items as a (query block, segment) grid, one item per
+// thread per round, so every round is a few wave-aggregated LDS atomics.
+// Offsets that are not a valid packing of Nr rows (out of order, a segment
+// longer than T, or not ending at Nr) produce an empty list.  The global
+// stores come last: a barrier after a store would wait for it.
+struct SchedLds {
+  int hist[kSortBins];
+  int off[kSegLds + 1];
+  int wmax[16], wbad[16];
+  int wave[17];
+};
+
+template <int NT>
+NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, int T, int BM,
+                             int Nr, int max_items, WorkItem* __restrict__ items,
+                             int32_t* __restrict__ meta, SchedLds& L) {
+  static_assert(NT % kWave == 0 && NT / kWave <= 16 && kSortBins % NT == 0, "block size");
   const int tid = threadIdx.x;
+  const int lane = tid % kWave, wave = tid / kWave;
   const int per_qb = BM / kBN;           // key tiles added per query block
-  for (int i = tid; i < kXcd * kXcdBins; i += kPrepThreads) s_hist[i] = 0;
-  if (tid == 0) {
-    s_maxn = 0;
-    s_bad = seg_offsets[0] != 0 || seg_offsets[BH] != Nr;
+  const bool in_lds = BH <= kSegLds;
+  if (in_lds)
+    for (int i = tid; i <= BH; i += NT) L.off[i] = seg_offsets_g[i];
+  for (int i = tid; i < kSortBins; i += NT) L.hist[i] = 0;
+  __syncthreads();
+  const int32_t* off = in_lds ? L.off : seg_offsets_g;
+  // validity and the longest segment
+  int mx = 0, bad = 0;
+  for (int s = tid; s < BH; s += NT) {
+    const int n = off[s + 1] - off[s];
+    mx = max(mx, n);
+    bad |= n < 0 || n > T;
+  }
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    mx = max(mx, __shfl_xor(mx, o));
+    bad |= __shfl_xor(bad, o);
+  }
+  if (lane == 0) {
+    L.wmax[wave] = mx;
+    L.wbad[wave] = bad;
   }
   __syncthreads();
-  // offsets that are not a valid packing of Nr rows disable the call: every
-  // later kernel then sees zero items and zero tiles.
-  for (int s = tid; s < BH; s += kPrepThreads)
-    if (seg_offsets[s + 1] < seg_offsets[s] || seg_offsets[s + 1] - seg_offsets[s] > T) s_bad = 1;
-  __syncthreads();
-  if (s_bad) {
+  int maxn = 0;
+  bad = off[0] != 0 || off[BH] != Nr;
+#pragma unroll
+  for (int w = 0; w < NT / kWave; ++w) {
+    maxn = max(maxn, L.wmax[w]);
+    bad |= L.wbad[w];
+  }
+  if (bad) {
     if (tid == 0) {
       meta[kMetaItems] = 0;
-      meta[kMetaTiles] = 0;
-      meta[kMetaTablePos] = 0;
       meta[kMetaBad] = 1;
-      meta[kMetaStride] = max_items;
-      for (int x = 0; x < kXcd; ++x) meta[kMetaXcd + x] = 0;
     }
     return;
   }
-
-  // pass 1: key-tile running sum (tile_off), longest segment, work running
-  // sum over segments (work_off)
-  int carry = 0;
-  long long wcarry = 0;
-  for (int start = 0; start < BH; start += kPrepThreads) {
-    const int s = start + tid;
-    const int n = s < BH ? seg_offsets[s + 1] - seg_offsets[s] : 0;
-    const int tiles = (n + kBN - 1) / kBN;
-    if (n > 0) atomicMax(&s_maxn, n);
-    const int nqb = (n + BM - 1) / BM;
-    long long wsum = 0;
-    for (int qb = 0; qb < nqb; ++qb) wsum += min(tiles, (qb + 1) * per_qb);
-    int total;
-    const int ex = block_exclusive_scan<kPrepThreads>(tiles, s_wave, total);
-    // 64-bit exclusive scan of the segment work (wave scans + one wave)
-    long long incl = wsum;
-    const int lane = tid % kWave, wave = tid / kWave;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const long long y = __shfl_up(incl, o, kWave);
-      if (lane >= o) incl += y;
-    }
-    if (lane == kWave - 1) s_lwave[wave] = incl;
-    __syncthreads();
-    if (tid == 0) {
-      long long acc = 0;
-      for (int w = 0; w < kPrepThreads / kWave; ++w) {
-        const long long v = s_lwave[w];
-        s_lwave[w] = acc;
-        acc += v;
-      }
-      s_lwave[kPrepThreads / kWave] = acc;
-    }
-    __syncthreads();
-    if (s < BH) {
-      tile_off[s] = carry + ex;
-      work_off[s] = wcarry + s_lwave[wave] + incl - wsum;
-    }
-    carry += total;
-    wcarry += s_lwave[kPrepThreads / kWave];
-    __syncthreads();
-  }
-  const long long wtotal = wcarry > 0 ? wcarry : 1;
-  if (tid == 0) {
-    tile_off[BH] = carry;
-    meta[kMetaBad] = 0;
-    meta[kMetaTiles] = carry;
-    meta[kMetaTablePos] = rope_mode == 0 ? s_maxn : (rope_mode == 1 ? T : 0);
-    meta[kMetaStride] = max_items;
+  const int max_nqb = (maxn + BM - 1) / BM;
+  const long grid_items = static_cast<long>(max_nqb) * BH;
+  // grid cell g = qb * BH + s; the work key is the bin index (heaviest first)
+  auto cell = [&](long g, int& s, int& qb, int& seg0, int& n, int& key) {
+    qb = static_cast<int>(g / BH);
+    s = static_cast<int>(g - static_cast<long>(qb) * BH);
+    seg0 = off[s];
+    n = off[s + 1] - seg0;
+    const int w = min((n + kBN - 1) / kBN, (qb + 1) * per_qb);
+    key = kSortBins - 1 - min(w, kSortBins - 1);
+    return qb * BM < n;
+  };
+  for (long g0 = 0; g0 < grid_items; g0 += NT) {
+    const long g = g0 + tid;
+    int sg = 0, qb = 0, seg0 = 0, n = 0, key = 0;
+    const bool act = g < grid_items && cell(g, sg, qb, seg0, n, key);
+    wave_bin_add(L.hist, key, act);
   }
   __syncthreads();
-  // pass 2: histogram of item work per XCD
-  for (int s = tid; s < BH; s += kPrepThreads) {
-    const int n = seg_offsets[s + 1] - seg_offsets[s];
-    const int tiles = (n + kBN - 1) / kBN;
-    const int nqb = (n + BM - 1) / BM;
-    long long before = work_off[s];
-    for (int qb = 0; qb < nqb; ++qb) {
-      const int w = min(tiles, (qb + 1) * per_qb);
-      const int x = static_cast<int>(min(static_cast<long long>(kXcd - 1), before * kXcd / wtotal));
-      atomicAdd(&s_hist[x * kXcdBins + kXcdBins - 1 - min(w, kXcdBins - 1)], 1);
-      before += w;
-    }
-  }
-  __syncthreads();
-  // per-XCD exclusive scans of the histograms (heaviest bin first)
-  constexpr int PER = kXcd * kXcdBins / kPrepThreads;
-  constexpr int TPX = kPrepThreads / kXcd;   // threads per XCD
+  // exclusive scan of the histogram -> insertion cursors (heaviest first)
+  constexpr int PER = kSortBins / NT;
   int h[PER];
   int sum = 0;
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
-    h[i] = s_hist[tid * PER + i];
+    h[i] = L.hist[tid * PER + i];
     sum += h[i];
   }
   int total;
-  int run = block_exclusive_scan<kPrepThreads>(sum, s_wave, total);
-  if (tid % TPX == 0) s_xbase[tid / TPX] = run;
-  if (tid == 0) s_xbase[kXcd] = total;
-  __syncthreads();
-  run -= s_xbase[tid / TPX];
+  int run = block_exclusive_scan<NT>(sum, L.wave, total);
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
-    s_hist[tid * PER + i] = run;
+    L.hist[tid * PER + i] = run;
     run += h[i];
   }
-  if (tid < kXcd) meta[kMetaXcd + tid] = min(s_xbase[tid + 1] - s_xbase[tid], max_items);
-  if (tid == 0) meta[kMetaItems] = total;
   __syncthreads();
-  // pass 3: place the items
-  for (int s = tid; s < BH; s += kPrepThreads) {
-    const int n = seg_offsets[s + 1] - seg_offsets[s];
-    const int tiles = (n + kBN - 1) / kBN;
-    const int nqb = (n + BM - 1) / BM;
-    long long before = work_off[s];
-    for (int qb = 0; qb < nqb; ++qb) {
-      const int w = min(tiles, (qb + 1) * per_qb);
-      const int x = static_cast<int>(min(static_cast<long long>(kXcd - 1), before * kXcd / wtotal));
-      const int pos = atomicAdd(&s_hist[x * kXcdBins + kXcdBins - 1 - min(w, kXcdBins - 1)], 1);
-      if (pos < max_items) items[static_cast<size_t>(x) * max_items + pos] = make_int2(s, qb);
-      before += w;
+  for (long g0 = 0; g0 < grid_items; g0 += NT) {
+    const long g = g0 + tid;
+    int sg = 0, qb = 0, seg0 = 0, n = 0, key = 0;
+    const bool act = g < grid_items && cell(g, sg, qb, seg0, n, key);
+    const int pos = wave_bin_add(L.hist, key, act);
+    if (act && pos < max_items) {
+      WorkItem wi;
+      wi.s = sg;
+      wi.qb = qb;
+      wi.seg0 = seg0;
+      wi.n = n;
+      wi.tile0 = seg_tile0(seg0, sg);
+      wi.pad0 = wi.pad1 = wi.pad2 = 0;
+      items[pos] = wi;
     }
   }
+  if (tid == 0) {
+    meta[kMetaItems] = min(total, max_items);
+    meta[kMetaBad] = 0;
+  }
 }
 
-// Work item of this workgroup, or false if it has none.
-NAMOH_DEV bool my_item(const int2* __restrict__ items, const int32_t* __restrict__ meta,
-                       int2& it) {
-  const int x = blockIdx.x % kXcd;
-  const int rank = blockIdx.x / kXcd;
-  if (rank >= meta[kMetaXcd + x]) return false;
-  it = items[static_cast<size_t>(x) * meta[kMetaStride] + rank];
-  return true;
+// Work item of this workgroup, or false if it has none.  The record is read
+// together with the item count (the grid has max_items workgroups, so the
+// read is in bounds either way).
+NAMOH_DEV bool my_item(const WorkItem* __restrict__ items, const int32_t* __restrict__ meta,
+                       WorkItem& it) {
+  const int cnt = meta[kMetaItems];
+  it = items[blockIdx.x];
+  return static_cast<int>(blockIdx.x) < cnt;
 }
 
 // ---------------------------------------------------------------------------
-// Workgroup 0 builds the schedule (above); workgroups 1.. fill the RoPE table
-// table[p * (d/2) + j] = (cos, sin)(p * base^(-2j/d)) for p < P, with angles
-// in double.  P (longest segment for head-relative positions, T for global
-// ones) is recomputed by each table workgroup from seg_offsets.
-__global__ __launch_bounds__(kPrepThreads) void k_attn_prep(
-    const int32_t* __restrict__ seg_offsets, int BH, int T, int BM,
-    int rope_mode, int Nr, int max_items, int d, double log_base,
-    int32_t* __restrict__ tile_off, long long* __restrict__ work_off,
-    int2* __restrict__ items, int32_t* __restrict__ meta, float2* __restrict__ table) {
-  if (blockIdx.x == 0) {
-    attn_schedule(seg_offsets, BH, T, BM, rope_mode, Nr, max_items, tile_off, work_off, items,
-                  meta);
-    return;
-  }
-  if (rope_mode == 2) return;
-  __shared__ int s_p;
+// RoPE table table[p * (d/2) + j] = (cos, sin)(p * base^(-2j/d)) for p < P,
+// the angles formed and reduced in double.  P (longest segment for
+// head-relative positions, T for global ones) is recomputed by every
+// workgroup from seg_offsets.
+constexpr int kTableThreads = 256;
+__global__ __launch_bounds__(kTableThreads) void k_rope_table(
+    const int32_t* __restrict__ seg_offsets, int BH, int T, int rope_mode, int d,
+    double log_base, float2* __restrict__ table) {
+  __shared__ int s_p[kTableThreads / kWave];
+  __shared__ double s_theta[64];
+  const int half = d / 2;
+  const int tid = threadIdx.x;
+  if (tid < half) s_theta[tid] = exp(-(2.0 * tid / d) * log_base);
   int P = T;
   if (rope_mode == 0) {
-    if (threadIdx.x == 0) s_p = 0;
-    __syncthreads();
     int mx = 0;
-    for (int s = threadIdx.x; s < BH; s += kPrepThreads)
+    for (int s = tid; s < BH; s += kTableThreads)
       mx = max(mx, min(seg_offsets[s + 1] - seg_offsets[s], T));
-    atomicMax(&s_p, mx);
-    __syncthreads();
-    P = s_p;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) mx = max(mx, __shfl_xor(mx, o));
+    if (tid % kWave == 0) s_p[tid / kWave] = mx;
   }
-  const int half = d / 2;
+  __syncthreads();
+  if (rope_mode == 0) {
+    P = 0;
+#pragma unroll
+    for (int w = 0; w < kTableThreads / kWave; ++w) P = max(P, s_p[w]);
+  }
   const size_t total = static_cast<size_t>(P) * half;
-  const size_t stride = static_cast<size_t>(gridDim.x - 1) * kPrepThreads;
-  for (size_t i = static_cast<size_t>(blockIdx.x - 1) * kPrepThreads + threadIdx.x; i < total;
-       i += stride) {
+  const size_t stride = static_cast<size_t>(gridDim.x) * kTableThreads;
+  for (size_t i = static_cast<size_t>(blockIdx.x) * kTableThreads + tid; i < total; i += stride) {
     const int p = static_cast<int>(i / half);
     const int j = static_cast<int>(i - static_cast<size_t>(p) * half);
-    const double theta = exp(-(2.0 * j / d) * log_base);
-    double sn, cs;
-    sincos(static_cast<double>(p) * theta, &sn, &cs);
-    table[i] = make_float2(static_cast<float>(cs), static_cast<float>(sn));
+    table[i] = rope_cos_sin(static_cast<double>(p) * s_theta[j]);
   }
 }
 
-// ---------------------------------------------------------------------------
-NAMOH_DEV int find_segment(const int32_t* __restrict__ tile_off, int BH, int gt) {
-  int lo = 0, hi = BH;  // tile_off[lo] <= gt < tile_off[hi]
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (tile_off[mid] <= gt) lo = mid; else hi = mid;
-  }
-  return lo;
+// The schedule on its own (paths without the packing kernel, which otherwise
+// builds it in its workgroup 0).
+__global__ __launch_bounds__(kPackThreads) void k_attn_schedule(
+    const int32_t* __restrict__ seg_offsets, int BH, int T, int BM, int Nr, int max_items,
+    WorkItem* __restrict__ items, int32_t* __restrict__ meta) {
+  __shared__ SchedLds L;
+  attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, items, meta, L);
 }
+
+// ---------------------------------------------------------------------------
 
 NAMOH_DEV void unpack8(const uint4 x, float* f) {
   const uint32_t w[4] = {x.x, x.y, x.z, x.w};
@@ -324,8 +333,13 @@ NAMOH_DEV uint4 pack8(const float* f) {
 
 // Rotate the pair (x1[e], x2[e]) = (elements j, j + d/2) for 8 consecutive j
 // starting at j0, with cs = table row of the position.
-NAMOH_DEV void rope8(float* x1, float* x2, const float2* __restrict__ cs) {
-  const float4* c4 = reinterpret_cast<const float4*>(cs);
+NAMOH_DEV void load_rope8(float4 (&c4)[4], const float2* __restrict__ cs) {
+  const float4* p = reinterpret_cast<const float4*>(cs);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) c4[e] = p[e];
+}
+
+NAMOH_DEV void rope8(float* x1, float* x2, const float4 (&c4)[4]) {
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const float4 w = c4[e];  // (cos, sin) of j0+2e, then of j0+2e+1
@@ -344,26 +358,56 @@ NAMOH_DEV int vt_key_of_pos(int p) {
   return (p & ~12) | ((p & 4) << 1) | ((p & 8) >> 1);
 }
 
+// Workgroup 0 builds the attention schedule (it only needs seg_offsets and
+// runs alongside the packing); workgroup 1 + gt packs key tile gt.
 template <int D>
-__global__ __launch_bounds__(256) void k_pack_kv(
+struct PackLds {
+  uint16_t sv[kBN][D + 8];
+  int off[kSegLds + 1];
+};
+
+template <int D>
+__global__ __launch_bounds__(kPackThreads) void k_pack_kv(
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const float2* __restrict__ table, const int32_t* __restrict__ seg_offsets,
-    const int32_t* __restrict__ tile_off, const int32_t* __restrict__ perm_token,
-    const int32_t* __restrict__ meta, int BH, int T, int H, int rope_mode,
+    const int32_t* __restrict__ perm_token, int BH, int T, int H, int Nr, int rope_mode,
+    int BM, int max_items, WorkItem* __restrict__ items, int32_t* __restrict__ meta,
     uint16_t* __restrict__ Kp, uint16_t* __restrict__ Vt) {
-  __shared__ __attribute__((aligned(16))) uint16_t sv[kBN][D + 8];
-  const int gt = blockIdx.x;
-  if (gt >= meta[kMetaTiles]) return;
-  const int s = find_segment(tile_off, BH, gt);
-  const int r0 = (gt - tile_off[s]) * kBN;
-  const int b = s / H, h = s - (s / H) * H;
-  const int seg0 = seg_offsets[s];
-  const int n = seg_offsets[s + 1] - seg0;
-  const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
+  __shared__ __attribute__((aligned(16))) union {
+    SchedLds sched;
+    PackLds<D> pack;
+  } L;
+  if (blockIdx.x == 0) {
+    attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, items, meta, L.sched);
+    return;
+  }
+  const int gt = blockIdx.x - 1;
   const int tid = threadIdx.x;
+  // segment of tile gt: the last s with seg_tile0(off[s], s) <= gt
+  const bool in_lds = BH <= kSegLds;
+  if (in_lds) {
+    for (int i = tid; i <= BH; i += kPackThreads) L.pack.off[i] = seg_offsets[i];
+    __syncthreads();
+  }
+  const int32_t* off = in_lds ? L.pack.off : seg_offsets;
+  int lo = 0, hi = BH;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (seg_tile0(off[mid], mid) <= gt) lo = mid; else hi = mid;
+  }
+  const int s = lo;
+  const int seg0 = off[s];
+  const int n = off[s + 1] - seg0;
+  const int r0 = (gt - seg_tile0(seg0, s)) * kBN;
+  // a tile index in a gap between segments, or offsets that are not a
+  // packing of [0, Nr) (the schedule is then empty): nothing to pack
+  if (r0 < 0 || r0 >= n || seg0 < 0 || n > T || seg0 + n > Nr) return;
+  auto& sv = L.pack.sv;
+  const int b = s / H, h = s - (s / H) * H;
+  const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
 
   constexpr int HP = D / 16;  // 8-element granule pairs (j, j + d/2) per row
-  for (int u = tid; u < kBN * HP; u += 256) {
+  for (int u = tid; u < kBN * HP; u += kPackThreads) {
     const int row = u / HP, c = u - (u / HP) * HP;
     const int r = r0 + row;
     float x1[8], x2[8];
@@ -377,7 +421,9 @@ __global__ __launch_bounds__(256) void k_pack_kv(
         unpack8(a, x1);
         unpack8(bb, x2);
         const int pos = rope_mode == 0 ? r : t;
-        rope8(x1, x2, table + static_cast<size_t>(pos) * (D / 2) + 8 * c);
+        float4 cs[4];
+        load_rope8(cs, table + static_cast<size_t>(pos) * (D / 2) + 8 * c);
+        rope8(x1, x2, cs);
         o1 = pack8(x1);
         o2 = pack8(x2);
       } else {
@@ -390,7 +436,7 @@ __global__ __launch_bounds__(256) void k_pack_kv(
     *reinterpret_cast<uint4*>(dst + D / 2 + 8 * c) = o2;
   }
   constexpr int RG = D / 8;  // granules per value row
-  for (int u = tid; u < kBN * RG; u += 256) {
+  for (int u = tid; u < kBN * RG; u += kPackThreads) {
     const int row = u / RG, gr = u - (u / RG) * RG;
     const int r = r0 + row;
     uint4 x = make_uint4(0, 0, 0, 0);
@@ -401,7 +447,7 @@ __global__ __launch_bounds__(256) void k_pack_kv(
     *reinterpret_cast<uint4*>(&sv[row][8 * gr]) = x;
   }
   __syncthreads();
-  for (int u = tid; u < D * (kBN / 8); u += 256) {
+  for (int u = tid; u < D * (kBN / 8); u += kPackThreads) {
     const int m = u / (kBN / 8), pg = u - (u / (kBN / 8)) * (kBN / 8);
     uint32_t w[4];
 #pragma unroll
@@ -427,47 +473,16 @@ NAMOH_DEV int swz(int row, int gr) {
   return GPR == 16 ? (gr ^ (row & 15)) : (gr ^ ((row >> 1) & 7));
 }
 
-// Tile staging: KPT 16-byte granules per thread of one packed key tile or
-// one transposed value tile (contiguous in HBM) into registers, then into
-// swizzled LDS.
-template <int KPT, int NT>
-NAMOH_DEV void tile_gload(const uint16_t* __restrict__ tile, int tid, u32x4 (&reg)[KPT]) {
-  const u32x4* p = reinterpret_cast<const u32x4*>(tile);
-#pragma unroll
-  for (int i = 0; i < KPT; ++i) reg[i] = p[tid + i * NT];
-}
-
-// key tile: kBN rows of D elements
-template <int D, int KPT, int NT>
-NAMOH_DEV void tile_lstore_k(uint16_t* sKb, int tid, const u32x4 (&reg)[KPT]) {
-#pragma unroll
-  for (int i = 0; i < KPT; ++i) {
-    const int u = tid + i * NT;
-    const int row = u / (D / 8), gr = u % (D / 8);
-    *reinterpret_cast<u32x4*>(&sKb[row * D + swz<D / 8>(row, gr) * 8]) = reg[i];
-  }
-}
-
-// transposed value tile: D rows of kBN keys
-template <int D, int KPT, int NT>
-NAMOH_DEV void tile_lstore_v(uint16_t* sVb, int tid, const u32x4 (&reg)[KPT]) {
-#pragma unroll
-  for (int i = 0; i < KPT; ++i) {
-    const int u = tid + i * NT;
-    const int m = u / (kBN / 8), gv = u % (kBN / 8);
-    *reinterpret_cast<u32x4*>(&sVb[m * kBN + swz<kBN / 8>(m, gv) * 8]) = reg[i];
-  }
-}
-
-// Direct global -> LDS staging (global_load_lds_dwordx4): lane l of a wave
-// instruction writes LDS granule base + l, so the swizzle is applied on the
-// global side: the lane that fills physical granule P = row * GPR + phys
-// fetches logical granule swz(row, phys) of that row (the XOR is its own
-// inverse).  Completion is tracked by vmcnt: wait_tile_dma() before the
-// barrier that publishes the tile.
+// Tile staging, direct global -> LDS (global_load_lds_dwordx4): KPT 16-byte
+// granules per thread of one packed key tile or one transposed value tile
+// (contiguous in HBM).  Lane l of a wave instruction writes LDS granule
+// base + l, so the swizzle is applied on the global side: the lane that
+// fills physical granule P = row * GPR + phys fetches logical granule
+// swz(row, phys) of that row (the XOR is its own inverse).  Completion is
+// tracked by vmcnt: wait_vmcnt<N>() before the barrier that publishes a tile
+// leaves only the N most recent loads of the wave in flight.
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
-
 template <int GPR, int KPT, int NT>
 NAMOH_DEV void tile_dma(const uint16_t* __restrict__ tile, uint16_t* lds_tile, int tid) {
 #pragma unroll
@@ -481,7 +496,13 @@ NAMOH_DEV void tile_dma(const uint16_t* __restrict__ tile, uint16_t* lds_tile, i
   }
 }
 
-NAMOH_DEV void wait_tile_dma() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+// s_waitcnt vmcnt(N) (expcnt and lgkmcnt left at their "no wait" values);
+// the 6-bit count is split over bits 3:0 and 15:14 of the immediate.
+template <int N>
+NAMOH_DEV void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
 
 // S^T = K Q^T for one 64-key tile: 2 key sub-tiles x NQT query sub-tiles.
 // All LDS operand reads of the tile are issued before the first MFMA (the
@@ -513,167 +534,6 @@ NAMOH_DEV void qk_tile(f32x16 (&S)[2][NQT], const uint16_t* __restrict__ sKb,
 #pragma unroll
       for (int qt = 0; qt < NQT; ++qt)
         S[kk][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][kk], qB[qt][ks], S[kk][qt], 0, 0, 0);
-}
-
-// Pieces of one tile's work for the software-pipelined loop.
-template <int D>
-NAMOH_DEV void qk_reads(bf16x8 (&a)[D / 16][2], const uint16_t* __restrict__ sKb, int c, int g) {
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks)
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int row = 32 * kk + c;
-      a[ks][kk] = *reinterpret_cast<const bf16x8*>(&sKb[row * D + swz<D / 8>(row, 2 * ks + g) * 8]);
-    }
-}
-
-template <int D, int NQT>
-NAMOH_DEV void qk_mfma(f32x16 (&S)[2][NQT], const bf16x8 (&a)[D / 16][2],
-                       const bf16x8 (&qB)[NQT][D / 16]) {
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-    for (int qt = 0; qt < NQT; ++qt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) S[kk][qt][e] = 0.f;
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks)
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int qt = 0; qt < NQT; ++qt)
-        S[kk][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][kk], qB[qt][ks], S[kk][qt], 0, 0, 0);
-}
-
-template <int D>
-NAMOH_DEV void v_reads(bf16x8 (&va)[4][D / 32], const uint16_t* __restrict__ sVb, int c, int g) {
-#pragma unroll
-  for (int k2 = 0; k2 < 4; ++k2)
-#pragma unroll
-    for (int mt = 0; mt < D / 32; ++mt) {
-      const int row = 32 * mt + c;
-      va[k2][mt] = *reinterpret_cast<const bf16x8*>(&sVb[row * kBN + swz<kBN / 8>(row, 2 * k2 + g) * 8]);
-    }
-}
-
-// Probabilities of one unmasked tile (branch-free VALU work).
-template <int NQT>
-NAMOH_DEV void softmax_probs(f32x16 (&S)[2][NQT], bf16x8 (&pB)[NQT][4], float (&alpha)[NQT],
-                             bool& rescale, float (&m_run)[NQT], float (&l_run)[NQT],
-                             float scale_log2, float lazy_thr) {
-#pragma unroll
-  for (int qt = 0; qt < NQT; ++qt) {
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(S[kk][qt][e], S[kk][qt][e + 1]));
-    mx = pair_max32(mx);
-    const bool up = mx > m_run[qt] + lazy_thr;
-    const float mnew = up ? mx : m_run[qt];
-    alpha[qt] = up ? __builtin_amdgcn_exp2f((m_run[qt] - mnew) * scale_log2) : 1.f;
-    rescale |= up;
-    const float mc = mnew * scale_log2;
-    float ls = 0.f;
-#pragma unroll
-    for (int k2 = 0; k2 < 4; ++k2) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        pB[qt][k2][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(
-            fmaf(S[k2 >> 1][qt][8 * (k2 & 1) + e], scale_log2, -mc)));
-#pragma unroll
-      for (int e = 0; e < 8; e += 2) {
-        const bf16x2 pr = {pB[qt][k2][e], pB[qt][k2][e + 1]};
-        ls = __builtin_amdgcn_fdot2_f32_bf16(pr, kOnes2, ls, false);
-      }
-    }
-    l_run[qt] = l_run[qt] * alpha[qt] + ls;
-    m_run[qt] = mnew;
-  }
-}
-
-template <int D, int NQT>
-NAMOH_DEV void rescale_o(f32x16 (&O)[D / 32][NQT], const float (&alpha)[NQT]) {
-#pragma unroll
-  for (int qt = 0; qt < NQT; ++qt)
-#pragma unroll
-    for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) O[mt][qt][e] *= alpha[qt];
-}
-
-template <int D, int NQT>
-NAMOH_DEV void pv_mfma(f32x16 (&O)[D / 32][NQT], const bf16x8 (&va)[4][D / 32],
-                       const bf16x8 (&pB)[NQT][4]) {
-#pragma unroll
-  for (int k2 = 0; k2 < 4; ++k2)
-#pragma unroll
-    for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-      for (int qt = 0; qt < NQT; ++qt)
-        O[mt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[k2][mt], pB[qt][k2], O[mt][qt], 0, 0, 0);
-}
-
-// Single 32-query sub-tile versions (the two-sub-tile ping-pong loop).
-template <int D>
-NAMOH_DEV void qk_mfma1(f32x16 (&S)[2], const bf16x8 (&a)[D / 16][2], const bf16x8 (&qB)[D / 16]) {
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) S[kk][e] = 0.f;
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks)
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-      S[kk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][kk], qB[ks], S[kk], 0, 0, 0);
-}
-
-NAMOH_DEV void softmax_probs1(f32x16 (&S)[2], bf16x8 (&pB)[4], float& alpha, bool& rescale,
-                              float& m_run, float& l_run, float scale_log2, float lazy_thr) {
-  float mx = -INFINITY;
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-    for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(S[kk][e], S[kk][e + 1]));
-  mx = pair_max32(mx);
-  const bool up = mx > m_run + lazy_thr;
-  const float mnew = up ? mx : m_run;
-  alpha = up ? __builtin_amdgcn_exp2f((m_run - mnew) * scale_log2) : 1.f;
-  rescale = up;
-  const float mc = mnew * scale_log2;
-  float ls = 0.f;
-#pragma unroll
-  for (int k2 = 0; k2 < 4; ++k2) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      pB[k2][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(
-          fmaf(S[k2 >> 1][8 * (k2 & 1) + e], scale_log2, -mc)));
-#pragma unroll
-    for (int e = 0; e < 8; e += 2) {
-      const bf16x2 pr = {pB[k2][e], pB[k2][e + 1]};
-      ls = __builtin_amdgcn_fdot2_f32_bf16(pr, kOnes2, ls, false);
-    }
-  }
-  l_run = l_run * alpha + ls;
-  m_run = mnew;
-}
-
-template <int D, int NQT, int QT>
-NAMOH_DEV void pv_mfma_q(f32x16 (&O)[D / 32][NQT], const bf16x8 (&va)[4][D / 32],
-                         const bf16x8 (&pB)[4]) {
-#pragma unroll
-  for (int k2 = 0; k2 < 4; ++k2)
-#pragma unroll
-    for (int mt = 0; mt < D / 32; ++mt)
-      O[mt][QT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[k2][mt], pB[k2], O[mt][QT], 0, 0, 0);
-}
-
-template <int D, int NQT, int QT>
-NAMOH_DEV void rescale_q(f32x16 (&O)[D / 32][NQT], float alpha) {
-#pragma unroll
-  for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) O[mt][QT][e] *= alpha;
 }
 
 // Mask, online softmax and O^T += V^T P^T for one 64-key tile.
@@ -783,10 +643,9 @@ template <int D, int NQT, int NW, bool HB>
 __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kp,
     const uint16_t* __restrict__ Vt, const float2* __restrict__ table,
-    const int32_t* __restrict__ seg_offsets, const int32_t* __restrict__ tile_off,
-    const int32_t* __restrict__ perm_token, const int2* __restrict__ items,
-    const int32_t* __restrict__ meta, int T, int H, int rope_mode,
-    float scale_log2, void* __restrict__ hout) {
+    const int32_t* __restrict__ perm_token, const WorkItem* __restrict__ items,
+    const int32_t* __restrict__ meta, int T, int H, int rope_mode, float scale_log2,
+    void* __restrict__ hout) {
   constexpr int BM = 32 * NQT * NW;
   constexpr int KS = D / 16;  // reduction steps of S^T = K Q^T
   constexpr int MT = D / 32;  // 32-row tiles of O^T
@@ -794,17 +653,18 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   constexpr int KPT = kBN * D / 8 / NT;  // 16-byte granules per thread per tile
   static_assert(kBN * D / 8 % NT == 0, "tile/thread mismatch");
 
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kBN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2][D * kBN];
-
-  int2 it;
+  constexpr int NS = MfmaShape<D>::NS;
+  static_assert(NS >= 2 && 2 * KPT * (NS - 2) < 64, "tile stages");
+  __shared__ __attribute__((aligned(16))) uint16_t sK[NS][kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[NS][D * kBN];
+  WorkItem it;
   if (!my_item(items, meta, it)) return;
-  const int s = it.x;
-  const int q0 = it.y * BM;
+  const int s = it.s;
+  const int q0 = it.qb * BM;
   const int b = s / H, h = s - (s / H) * H;
-  const int seg0 = seg_offsets[s];
-  const int n = seg_offsets[s + 1] - seg0;
-  const int tile0 = tile_off[s];
+  const int seg0 = it.seg0;
+  const int n = it.n;
+  const int tile0 = it.tile0;
   const int ntiles = (n + kBN - 1) / kBN;
   const int kt_end = min(ntiles, (q0 + BM + kBN - 1) / kBN);
   const int tid = threadIdx.x;
@@ -815,22 +675,60 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
   const float lazy_thr = kLazyLog2 / scale_log2;
 
+  // token of each query row (issued before the tile loads, so waiting for it
+  // does not wait for them)
+  int qtok[NQT];
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt) {
+    const int r = q0 + 32 * (qt * NW + wave) + c;
+    qtok[qt] = perm_token[seg0 + (r < n ? r : n - 1)];
+  }
+
+  // ---- first NS - 1 key/value tiles: in flight during the query gather ---
+  // (always NS - 1 loads, repeating the last tile when the item has fewer,
+  // so the number of loads in flight is the same on every path; the
+  // repeats land in stages the loop never reads and are complete before the
+  // loop's last iteration)
+  constexpr size_t TS = static_cast<size_t>(kBN) * D;
+  const uint16_t* Kbase = Kp + static_cast<size_t>(tile0) * TS;
+  const uint16_t* Vbase = Vt + static_cast<size_t>(tile0) * TS;
+#pragma unroll
+  for (int i = 0; i < NS - 1; ++i) {
+    const int ti = min(i, kt_end - 1);
+    tile_dma<D / 8, KPT, NT>(Kbase + ti * TS, sK[i], tid);
+    tile_dma<kBN / 8, KPT, NT>(Vbase + ti * TS, sV[i], tid);
+  }
+
   // ---- query block: gather, rotate, round to bf16 B operands -------------
+  // (the query rows and their RoPE factors are loaded together; the table
+  // has T rows, so the read in the no-RoPE mode, replaced by the identity
+  // rotation, is in bounds)
   bf16x8 qB[NQT][KS];
 #pragma unroll
   for (int qt = 0; qt < NQT; ++qt) {
     const int r = q0 + 32 * (qt * NW + wave) + c;
     const int rr = r < n ? r : n - 1;
-    const int t = min(static_cast<unsigned>(perm_token[seg0 + rr]), static_cast<unsigned>(T - 1));
+    const int t = min(static_cast<unsigned>(qtok[qt]), static_cast<unsigned>(T - 1));
     const uint16_t* qrow = q + (head_base + t) * D;
-    const int pos = rope_mode == 0 ? rr : t;
+    const int pos = rope_mode == 0 ? rr : (rope_mode == 1 ? t : 0);
+    u32x4 qa[KS / 2], qb2[KS / 2];
+    float4 cs[KS / 2][4];
+#pragma unroll
+    for (int s2 = 0; s2 < KS / 2; ++s2) {
+      qa[s2] = *reinterpret_cast<const u32x4*>(qrow + 16 * s2 + 8 * g);
+      qb2[s2] = *reinterpret_cast<const u32x4*>(qrow + D / 2 + 16 * s2 + 8 * g);
+      load_rope8(cs[s2], table + static_cast<size_t>(pos) * (D / 2) + 16 * s2 + 8 * g);
+    }
 #pragma unroll
     for (int s2 = 0; s2 < KS / 2; ++s2) {
       float x1[8], x2[8];
-      unpack8(*reinterpret_cast<const uint4*>(qrow + 16 * s2 + 8 * g), x1);
-      unpack8(*reinterpret_cast<const uint4*>(qrow + D / 2 + 16 * s2 + 8 * g), x2);
-      if (rope_mode != 2)
-        rope8(x1, x2, table + static_cast<size_t>(pos) * (D / 2) + 16 * s2 + 8 * g);
+      unpack8(make_uint4(qa[s2][0], qa[s2][1], qa[s2][2], qa[s2][3]), x1);
+      unpack8(make_uint4(qb2[s2][0], qb2[s2][1], qb2[s2][2], qb2[s2][3]), x2);
+      if (rope_mode == 2) {   // identity rotation
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cs[s2][e] = make_float4(1.f, 0.f, 1.f, 0.f);
+      }
+      rope8(x1, x2, cs[s2]);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         qB[qt][s2][e] = static_cast<__bf16>(r < n ? x1[e] : 0.f);
@@ -853,158 +751,32 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     l_run[qt] = 0.f;
   }
 
-#if NAMOH_ATTN_PIPE == 2
-  // ---- two-sub-tile ping-pong -------------------------------------------
-  // Each wave owns two 32-query sub-tiles.  On tiles that need no mask, the
-  // score MFMAs of sub-tile 1 are interleaved with the softmax of sub-tile 0,
-  // and the P.V MFMAs of sub-tile 0 with the softmax of sub-tile 1, so the
-  // wave keeps its matrix and vector pipes busy at the same time.
-  static_assert(NQT == 2, "ping-pong loop needs two query sub-tiles per wave");
-  constexpr size_t TS = static_cast<size_t>(kBN) * D;
-  const uint16_t* Kbase = Kp + static_cast<size_t>(tile0) * TS;
-  const uint16_t* Vbase = Vt + static_cast<size_t>(tile0) * TS;
-  if (kt_end > 0) {
-    tile_dma<D / 8, KPT, NT>(Kbase, sK[0], tid);
-    tile_dma<kBN / 8, KPT, NT>(Vbase, sV[0], tid);
-  }
+  // ---- tile loop: NS-stage ring of K/V tiles, one barrier per tile -------
+  // At the top of iteration kt the wave has tiles kt .. kt + NS - 2 in
+  // flight; waiting until at most NS - 2 tiles' loads remain completes tile
+  // kt (near the end fewer tiles are in flight and the wait is for all).
+  // After the barrier every wave has finished tile kt - 1, so its stage
+  // receives tile kt + NS - 1.
   for (int kt = 0; kt < kt_end; ++kt) {
-    const int buf = kt & 1;
-    wait_tile_dma();
+    const int st = kt % NS;
+    if (kt + NS - 2 < kt_end)
+      wait_vmcnt<2 * KPT * (NS - 2)>();
+    else
+      wait_vmcnt<0>();
     __syncthreads();
-    if (kt + 1 < kt_end) {
-      tile_dma<D / 8, KPT, NT>(Kbase + (kt + 1) * TS, sK[buf ^ 1], tid);
-      tile_dma<kBN / 8, KPT, NT>(Vbase + (kt + 1) * TS, sV[buf ^ 1], tid);
-    }
-    if (kt >= wave_tiles) continue;
-    const int key0 = kt * kBN;
-    if (key0 + kBN - 1 > q0 + 32 * wave || key0 + kBN > n) {
-      f32x16 S[2][NQT];
-      qk_tile<D, NQT>(S, sK[buf], qB, c, g);
-      softmax_pv<D, NQT, NW>(S, O, m_run, l_run, sV[buf], key0, q0, wave, n, c, g,
-                             scale_log2, lazy_thr);
-      continue;
-    }
-    bf16x8 ka[KS][2];
-    qk_reads<D>(ka, sK[buf], c, g);
-    f32x16 S0[2], S1[2];
-    qk_mfma1<D>(S0, ka, qB[0]);
-    qk_mfma1<D>(S1, ka, qB[1]);
-    bf16x8 p0[4], p1[4];
-    float a0, a1;
-    bool r0, r1;
-    softmax_probs1(S0, p0, a0, r0, m_run[0], l_run[0], scale_log2, lazy_thr);
-#pragma unroll
-    for (int i = 0; i < 2 * KS; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
-      __builtin_amdgcn_sched_group_barrier(0x002, 5, 1);
-    }
-    bf16x8 va[4][MT];
-    v_reads<D>(va, sV[buf], c, g);
-    if (__any(r0)) rescale_q<D, NQT, 0>(O, a0);
-    pv_mfma_q<D, NQT, 0>(O, va, p0);
-    softmax_probs1(S1, p1, a1, r1, m_run[1], l_run[1], scale_log2, lazy_thr);
-#pragma unroll
-    for (int i = 0; i < 4 * MT; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
-      __builtin_amdgcn_sched_group_barrier(0x002, 5, 2);
-    }
-    if (__any(r1)) rescale_q<D, NQT, 1>(O, a1);
-    pv_mfma_q<D, NQT, 1>(O, va, p1);
-  }
-
-#elif NAMOH_ATTN_PIPE
-  // ---- software-pipelined tile loop -------------------------------------
-  // Iteration j issues the score MFMAs of tile j + 1 interleaved with the
-  // softmax VALU work of tile j (only the wave's last, diagonal tile needs a
-  // mask, so every other iteration is one branch-free block that the
-  // scheduling barriers below interleave), then the P.V MFMAs of tile j.
-  // LDS holds K_{j+1} and V_j during iteration j; after the barrier that
-  // opens iteration j the wave stores K_{j+2} into the key buffer K_j used
-  // and V_{j+1} into the value buffer V_{j-1} used (both idle: every wave has
-  // left iteration j - 1), and starts the global loads of K_{j+3}, V_{j+2}.
-  constexpr size_t TS = static_cast<size_t>(kBN) * D;
-  const uint16_t* Kbase = Kp + static_cast<size_t>(tile0) * TS;
-  const uint16_t* Vbase = Vt + static_cast<size_t>(tile0) * TS;
-  u32x4 kreg[KPT], vreg[KPT];
-  if (kt_end > 0) {
-    tile_gload<KPT, NT>(Kbase, tid, kreg);
-    tile_gload<KPT, NT>(Vbase, tid, vreg);
-    tile_lstore_k<D, KPT, NT>(sK[0], tid, kreg);
-    tile_lstore_v<D, KPT, NT>(sV[0], tid, vreg);
-  }
-  if (kt_end > 1) {
-    tile_gload<KPT, NT>(Kbase + TS, tid, kreg);
-    tile_lstore_k<D, KPT, NT>(sK[1], tid, kreg);
-  }
-  __syncthreads();
-  if (kt_end > 2) tile_gload<KPT, NT>(Kbase + 2 * TS, tid, kreg);
-  if (kt_end > 1) tile_gload<KPT, NT>(Vbase + TS, tid, vreg);
-  f32x16 SA[2][NQT], SB[2][NQT];
-  if (wave_tiles > 0) qk_tile<D, NQT>(SA, sK[0], qB, c, g);
-
-  auto step = [&](int j, f32x16 (&Scur)[2][NQT], f32x16 (&Snext)[2][NQT]) {
-    __syncthreads();
-    if (j + 2 < kt_end) tile_lstore_k<D, KPT, NT>(sK[j & 1], tid, kreg);
-    if (j + 1 < kt_end) tile_lstore_v<D, KPT, NT>(sV[(j + 1) & 1], tid, vreg);
-    if (j + 3 < kt_end) tile_gload<KPT, NT>(Kbase + (j + 3) * TS, tid, kreg);
-    if (j + 2 < kt_end) tile_gload<KPT, NT>(Vbase + (j + 2) * TS, tid, vreg);
-    if (j + 1 < wave_tiles) {
-      bf16x8 ka[D / 16][2];
-      qk_reads<D>(ka, sK[(j + 1) & 1], c, g);
-      bf16x8 pB[NQT][4];
-      float alpha[NQT];
-      bool rescale = false;
-      softmax_probs<NQT>(Scur, pB, alpha, rescale, m_run, l_run, scale_log2, lazy_thr);
-      qk_mfma<D, NQT>(Snext, ka, qB);
-      // interleave: all LDS reads first, then one MFMA per VALU group
-#pragma unroll
-      for (int i = 0; i < 2 * (D / 16) * NQT; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
-      }
-      bf16x8 va[4][D / 32];
-      v_reads<D>(va, sV[j & 1], c, g);
-      if (__any(rescale)) rescale_o<D, NQT>(O, alpha);
-      pv_mfma<D, NQT>(O, va, pB);
-    } else if (j < wave_tiles) {
-      softmax_pv<D, NQT, NW>(Scur, O, m_run, l_run, sV[j & 1], j * kBN, q0, wave, n, c, g,
-                             scale_log2, lazy_thr);
-    }
-  };
-  for (int j = 0; j < kt_end; j += 2) {
-    step(j, SA, SB);
-    if (j + 1 < kt_end) step(j + 1, SB, SA);
-  }
-
-#else
-  // ---- tile loop: double-buffered K/V tiles, one barrier per tile --------
-  // Tile kt + 1 is copied straight into the idle LDS buffer (global -> LDS)
-  // while tile kt is computed; the barrier at the top of the next iteration
-  // publishes it.
-  constexpr size_t TS = static_cast<size_t>(kBN) * D;
-  const uint16_t* Kbase = Kp + static_cast<size_t>(tile0) * TS;
-  const uint16_t* Vbase = Vt + static_cast<size_t>(tile0) * TS;
-  if (kt_end > 0) {
-    tile_dma<D / 8, KPT, NT>(Kbase, sK[0], tid);
-    tile_dma<kBN / 8, KPT, NT>(Vbase, sV[0], tid);
-  }
-  for (int kt = 0; kt < kt_end; ++kt) {
-    const int buf = kt & 1;
-    wait_tile_dma();
-    __syncthreads();
-    if (kt + 1 < kt_end) {
-      tile_dma<D / 8, KPT, NT>(Kbase + (kt + 1) * TS, sK[buf ^ 1], tid);
-      tile_dma<kBN / 8, KPT, NT>(Vbase + (kt + 1) * TS, sV[buf ^ 1], tid);
+    if (kt + NS - 1 < kt_end) {
+      const int nst = (kt + NS - 1) % NS;
+      tile_dma<D / 8, KPT, NT>(Kbase + (kt + NS - 1) * TS, sK[nst], tid);
+      tile_dma<kBN / 8, KPT, NT>(Vbase + (kt + NS - 1) * TS, sV[nst], tid);
     }
     if (kt < wave_tiles) {
       f32x16 S[2][NQT];
-      qk_tile<D, NQT>(S, sK[buf], qB, c, g);
-      softmax_pv<D, NQT, NW>(S, O, m_run, l_run, sV[buf], kt * kBN, q0, wave, n, c, g,
+      qk_tile<D, NQT>(S, sK[st], qB, c, g);
+      softmax_pv<D, NQT, NW>(S, O, m_run, l_run, sV[st], kt * kBN, q0, wave, n, c, g,
                              scale_log2, lazy_thr);
     }
   }
 
-#endif
   // ---- epilogue: normalise and store the packed head outputs -----------
 #pragma unroll
   for (int qt = 0; qt < NQT; ++qt) {
@@ -1064,18 +836,18 @@ template <int D, bool BF16>
 __global__ __launch_bounds__(64) void k_attn_generic(
     const void* __restrict__ q, const void* __restrict__ k,
     const void* __restrict__ v, const float2* __restrict__ table,
-    const int32_t* __restrict__ seg_offsets, const int32_t* __restrict__ perm_token,
-    const int2* __restrict__ items, const int32_t* __restrict__ meta, int T,
-    int H, int rope_mode, float scale, float* __restrict__ hout) {
+    const int32_t* __restrict__ perm_token, const WorkItem* __restrict__ items,
+    const int32_t* __restrict__ meta, int T, int H, int rope_mode, float scale,
+    float* __restrict__ hout) {
   __shared__ float sK[kBN][D + 1];
   __shared__ float sV[kBN][D + 1];
-  int2 it;
+  WorkItem it;
   if (!my_item(items, meta, it)) return;
-  const int s = it.x;
-  const int q0 = it.y * kGenericBM;
+  const int s = it.s;
+  const int q0 = it.qb * kGenericBM;
   const int b = s / H, h = s - (s / H) * H;
-  const int seg0 = seg_offsets[s];
-  const int n = seg_offsets[s + 1] - seg0;
+  const int seg0 = it.seg0;
+  const int n = it.n;
   const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
   const int lane = threadIdx.x;
   const int r = q0 + lane;
@@ -1138,38 +910,66 @@ __global__ __launch_bounds__(64) void k_attn_generic(
 }
 
 // ---------------------------------------------------------------------------
+// One thread per (token, 8 output elements).  The K slots are gathered four
+// at a time (all loads of a batch issued before their products) and summed
+// in k order.
 template <bool IN_BF16, bool OUT_BF16>
 __global__ __launch_bounds__(256) void k_combine(
     const void* __restrict__ hout, const float* __restrict__ gates,
     const int32_t* __restrict__ slot_pos, long BT, int K, int D, int Nr,
     void* __restrict__ out) {
-  const int C = D / 4;
+  const int C = D / 8;
   const long idx = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
   const long tok = idx / C;
   const int cc = static_cast<int>(idx - tok * C);
   if (tok >= BT) return;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int k = 0; k < K; ++k) {
-    const int p = slot_pos[tok * K + k];
-    if (static_cast<unsigned>(p) >= static_cast<unsigned>(Nr)) continue;
-    const float gk = gates[tok * K + k];
-    float4 x;
-    if constexpr (IN_BF16) {
-      const uint2 u = reinterpret_cast<const uint2*>(hout)[static_cast<size_t>(p) * C + cc];
-      x = make_float4(lo_bf16(u.x), hi_bf16(u.x), lo_bf16(u.y), hi_bf16(u.y));
-    } else {
-      x = reinterpret_cast<const float4*>(hout)[static_cast<size_t>(p) * C + cc];
+  float acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  const int32_t* sp = slot_pos + tok * K;
+  const float* gp = gates + tok * K;
+  for (int k0 = 0; k0 < K; k0 += 4) {
+    int p[4];
+    float gk[4];
+    float x[4][8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool in = k0 + i < K;
+      p[i] = in ? sp[k0 + i] : -1;
+      gk[i] = in ? gp[k0 + i] : 0.f;
     }
-    acc.x = fmaf(gk, x.x, acc.x);
-    acc.y = fmaf(gk, x.y, acc.y);
-    acc.z = fmaf(gk, x.z, acc.z);
-    acc.w = fmaf(gk, x.w, acc.w);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (static_cast<unsigned>(p[i]) < static_cast<unsigned>(Nr)) {
+        if constexpr (IN_BF16) {
+          const uint4 u =
+              reinterpret_cast<const uint4*>(hout)[static_cast<size_t>(p[i]) * C + cc];
+          unpack8(u, x[i]);
+        } else {
+          const float4* src =
+              reinterpret_cast<const float4*>(hout) + (static_cast<size_t>(p[i]) * C + cc) * 2;
+          const float4 a = src[0], bb = src[1];
+          x[i][0] = a.x; x[i][1] = a.y; x[i][2] = a.z; x[i][3] = a.w;
+          x[i][4] = bb.x; x[i][5] = bb.y; x[i][6] = bb.z; x[i][7] = bb.w;
+        }
+      } else {
+        gk[i] = 0.f;   // slot outside the packed rows contributes nothing
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[i][e] = 0.f;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (k0 + i < K)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = fmaf(gk[i], x[i][e], acc[e]);
   }
   if constexpr (OUT_BF16) {
-    reinterpret_cast<uint2*>(out)[idx] =
-        make_uint2(pack_bf16x2(acc.x, acc.y), pack_bf16x2(acc.z, acc.w));
+    reinterpret_cast<uint4*>(out)[idx] = pack8(acc);
   } else {
-    reinterpret_cast<float4*>(out)[idx] = acc;
+    float4* dst = reinterpret_cast<float4*>(out) + idx * 2;
+    dst[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    dst[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
   }
 }
 
@@ -1184,9 +984,7 @@ static int block_queries(int d, int dtype) {
 
 struct AttnWs {
   int32_t* meta;
-  int32_t* tile_off;
-  long long* work_off;
-  int2* items;
+  WorkItem* items;
   float2* table;
   uint16_t* Kp;
   uint16_t* Vt;
@@ -1204,9 +1002,7 @@ static AttnWs carve_attn(void* ws, int B, int T, int H, int K, int d, int dtype)
   w.max_tiles = Nr / kBN + BH + 1;
   Carver cv(ws);
   w.meta = cv.take<int32_t>(kMetaCount);
-  w.tile_off = cv.take<int32_t>(BH + 1);
-  w.work_off = cv.take<long long>(BH + 1);
-  w.items = cv.take<int2>(kXcd * w.max_items);
+  w.items = cv.take<WorkItem>(w.max_items);
   w.table = cv.take<float2>(static_cast<size_t>(T) * (d / 2));
   if (use_mfma(d, dtype)) {
     w.Kp = cv.take<uint16_t>(w.max_tiles * kBN * d);
@@ -1225,24 +1021,26 @@ size_t attn_workspace_bytes(int B, int T, int H, int K, int d, int dtype) {
 
 template <int D>
 static void launch_mfma(const AttnWs& w, const void* q, const void* k, const void* v,
-                        int B, int T, int H, int rope_mode, float scale_log2,
+                        int B, int T, int H, int Nr, int rope_mode, float scale_log2,
                         const int32_t* seg_offsets, const int32_t* perm_token,
                         void* hout, bool hout_bf16, hipStream_t st) {
   constexpr int NW = MfmaShape<D>::NW, NQT = MfmaShape<D>::NQT;
   prof_mark("pack", true, st);
-  k_pack_kv<D><<<static_cast<unsigned>(w.max_tiles), 256, 0, st>>>(
-      static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), w.table,
-      seg_offsets, w.tile_off, perm_token, w.meta, B * H, T, H, rope_mode, w.Kp, w.Vt);
+  k_pack_kv<D><<<static_cast<unsigned>(1 + w.max_tiles), kPackThreads, 0, st>>>(
+      static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), w.table, seg_offsets,
+      perm_token, B * H, T, H, Nr, rope_mode, 32 * NQT * NW, static_cast<int>(w.max_items),
+      w.items, w.meta, w.Kp, w.Vt);
   prof_mark("pack", false, st);
   prof_mark("attn", true, st);
+  const unsigned grid = static_cast<unsigned>(w.max_items);
   if (hout_bf16)
-    k_attn_mfma<D, NQT, NW, true><<<static_cast<unsigned>(kXcd * w.max_items), NW * 64, 0, st>>>(
-        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.table, seg_offsets, w.tile_off,
-        perm_token, w.items, w.meta, T, H, rope_mode, scale_log2, hout);
+    k_attn_mfma<D, NQT, NW, true><<<grid, NW * 64, 0, st>>>(
+        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.table, perm_token, w.items, w.meta, T,
+        H, rope_mode, scale_log2, hout);
   else
-    k_attn_mfma<D, NQT, NW, false><<<static_cast<unsigned>(kXcd * w.max_items), NW * 64, 0, st>>>(
-        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.table, seg_offsets, w.tile_off,
-        perm_token, w.items, w.meta, T, H, rope_mode, scale_log2, hout);
+    k_attn_mfma<D, NQT, NW, false><<<grid, NW * 64, 0, st>>>(
+        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.table, perm_token, w.items, w.meta, T,
+        H, rope_mode, scale_log2, hout);
   prof_mark("attn", false, st);
 }
 
@@ -1252,9 +1050,8 @@ static void launch_generic(const AttnWs& w, const void* q, const void* k, const 
                            const int32_t* seg_offsets, const int32_t* perm_token,
                            float* hout, hipStream_t st) {
   prof_mark("attn", true, st);
-  k_attn_generic<D, BF16><<<static_cast<unsigned>(kXcd * w.max_items), 64, 0, st>>>(
-      q, k, v, w.table, seg_offsets, perm_token, w.items, w.meta, T, H, rope_mode,
-      scale, hout);
+  k_attn_generic<D, BF16><<<static_cast<unsigned>(w.max_items), 64, 0, st>>>(
+      q, k, v, w.table, perm_token, w.items, w.meta, T, H, rope_mode, scale, hout);
   prof_mark("attn", false, st);
 }
 
@@ -1273,18 +1070,23 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   const int BM = block_queries(d, dtype);
   const int Nr = B * T * K;
   const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
-  k_attn_prep<<<1 + 64, kPrepThreads, 0, st>>>(seg_offsets, B * H, T, BM, rope_mode, Nr,
-                                               static_cast<int>(w.max_items), d, log_base,
-                                               w.tile_off, w.work_off, w.items, w.meta, w.table);
+  if (rope_mode != 2)
+    k_rope_table<<<64, kTableThreads, 0, st>>>(seg_offsets, B * H, T, rope_mode, d, log_base,
+                                               w.table);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (use_mfma(d, dtype)) {
     const float sl2 = scale * 1.4426950408889634f;
     if (d == 64)
-      launch_mfma<64>(w, q, k, v, B, T, H, rope_mode, sl2, seg_offsets, perm_token, hout, hb, st);
+      launch_mfma<64>(w, q, k, v, B, T, H, Nr, rope_mode, sl2, seg_offsets, perm_token, hout, hb,
+                      st);
     else
-      launch_mfma<128>(w, q, k, v, B, T, H, rope_mode, sl2, seg_offsets, perm_token, hout, hb, st);
+      launch_mfma<128>(w, q, k, v, B, T, H, Nr, rope_mode, sl2, seg_offsets, perm_token, hout, hb,
+                       st);
   } else {
+    k_attn_schedule<<<1, kPackThreads, 0, st>>>(seg_offsets, B * H, T, BM, Nr,
+                                                static_cast<int>(w.max_items), w.items, w.meta);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     const bool bf = dtype == 1;
 #define NAMOH_GEN(DD)                                                                        \
   (bf ? launch_generic<DD, true>(w, q, k, v, T, H, rope_mode, scale, seg_offsets, perm_token, static_cast<float*>(hout), st) \
@@ -1296,7 +1098,7 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const long BT = static_cast<long>(B) * T;
-  const long threads = BT * (d / 4);
+  const long threads = BT * (d / 8);
   const unsigned grid = static_cast<unsigned>((threads + 255) / 256);
   prof_mark("combine", true, st);
   if (hb && out_dtype == 1)

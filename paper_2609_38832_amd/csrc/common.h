@@ -47,6 +47,31 @@ NAMOH_DEV uint64_t lanemask_lt() {
 
 NAMOH_DEV int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+// (cos, sin) of a RoPE angle given in double, in double arithmetic without
+// library calls: Cody-Waite reduction by pi/2 (two-part constant, fused
+// multiply-adds) to |r| <= pi/4, Taylor polynomials of degree 11 (sin) and
+// 12 (cos) there (truncation below 1e-11), and the quadrant's sign/swap.
+// Accurate to the final float rounding for angles below 2^30.
+NAMOH_DEV float2 rope_cos_sin(double angle) {
+  constexpr double kTwoOverPi = 0.6366197723675814;
+  constexpr double kPiHalfHi = 1.5707963267948966;
+  constexpr double kPiHalfLo = 6.123233995736766e-17;
+  const double n = rint(angle * kTwoOverPi);
+  double r = fma(-n, kPiHalfHi, angle);
+  r = fma(-n, kPiHalfLo, r);
+  const double r2 = r * r;
+  const double sn =
+      r * (1.0 + r2 * (-1.0 / 6 + r2 * (1.0 / 120 + r2 * (-1.0 / 5040 +
+           r2 * (1.0 / 362880 + r2 * (-1.0 / 39916800))))));
+  const double cs =
+      1.0 + r2 * (-1.0 / 2 + r2 * (1.0 / 24 + r2 * (-1.0 / 720 + r2 * (1.0 / 40320 +
+            r2 * (-1.0 / 3628800 + r2 * (1.0 / 479001600))))));
+  const int q = static_cast<int>(static_cast<long long>(n) & 3);
+  const double c = q == 0 ? cs : (q == 1 ? -sn : (q == 2 ? -cs : sn));
+  const double s = q == 0 ? sn : (q == 1 ? cs : (q == 2 ? -sn : -cs));
+  return make_float2(static_cast<float>(c), static_cast<float>(s));
+}
+
 // Inclusive scan across a 64-lane wave.
 NAMOH_DEV int wave_inclusive_scan(int x) {
   const int lane = __lane_id();

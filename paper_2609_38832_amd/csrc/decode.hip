@@ -105,11 +105,9 @@ __global__ __launch_bounds__(64 * kAppendWaves) void k_decode_route_append(
     for (int j = lane; j < D / 2; j += 64) {
       float cs = 1.f, sn = 0.f;
       if (rope_mode != 2) {
-        const double theta = exp(-(2.0 * j / D) * log_base);
-        double s, c;
-        sincos(static_cast<double>(pos) * theta, &s, &c);
-        cs = static_cast<float>(c);
-        sn = static_cast<float>(s);
+        const float2 w = rope_cos_sin(static_cast<double>(pos) * exp(-(2.0 * j / D) * log_base));
+        cs = w.x;
+        sn = w.y;
       }
       const float k1 = ld_elem<BF16>(k, src + j), k2 = ld_elem<BF16>(k, src + j + D / 2);
       const float q1 = ld_elem<BF16>(q, src + j), q2 = ld_elem<BF16>(q, src + j + D / 2);

@@ -5,21 +5,20 @@
 // every (batch, head) subsequence): the permutation is a stable counting sort
 // of the (token, head) pairs by segment b*H + h.
 //
-// Three launches; the only atomics are integer adds of counts, so every
-// output is deterministic:
+// Three launches; no global atomics, so every output is deterministic:
 //   1. k_route_count   eight lanes per token, 64 tokens per workgroup: K
 //                      rounds of a cooperative argmax under the total order
-//                      (logit desc, head asc) on order-preserving integer
-//                      keys, the gates, and per 64-token chunk the number of
-//                      tokens routed to each head (LDS integer adds, exact).
+//                      (logit desc, head asc), the gates, and for every
+//                      selected (token, head) its rank among the chunk's
+//                      tokens routed to that head (stored in slot_pos for
+//                      now), plus the chunk's per-head counts.
 //   2. k_route_scan    one wave per (b, h) segment: exclusive scan of the
 //                      segment's chunk counts and the head length n.
-//   3. k_route_scatter one wave per chunk: the segment offsets of sequence b
-//                      are b*T*K plus a scan of its H head lengths (every
-//                      sequence contributes exactly T*K pairs); a pair's
-//                      packed position = segment offset + earlier chunks of the
-//                      segment + lower lanes of this chunk routed to the same
-//                      head (popcount of ballot & lanes-below).
+//   3. k_route_scatter one workgroup per chunk: the segment offsets of
+//                      sequence b are b*T*K plus a scan of its H head
+//                      lengths (every sequence contributes exactly T*K
+//                      pairs); a pair's packed position = segment offset +
+//                      earlier chunks of the segment + its rank in the chunk.
 #include <climits>
 
 #include "common.h"
@@ -30,6 +29,8 @@ namespace namoh {
 constexpr int kRC = kRouteChunk;   // tokens per chunk
 constexpr int kLPT = 8;            // lanes per token in k_route_count
 constexpr int kCountThreads = kRC * kLPT;
+constexpr int kCountWaves = kCountThreads / kWave;
+constexpr int kScatterThreads = 512;
 
 // Order-preserving integer key of a float logit (-0.0 first made +0.0); the
 // map is its own inverse.
@@ -39,80 +40,128 @@ NAMOH_DEV int logit_key(float f) {
 }
 NAMOH_DEV float key_logit(int k) { return __int_as_float(k ^ ((k >> 31) & 0x7FFFFFFF)); }
 
-// 8 lanes per token, each holding HMAX/8 heads.  Round k picks the largest
-// (key, -head) pair below the previous round's winner: every lane scans its
-// heads, then three xor-shuffles inside the 8-lane group reduce to the
-// winner (larger key, then lower head index).  Real logits have keys above
-// INT_MIN, so the INT_MIN padding of heads >= H never wins while K <= H.
+// Candidate (logit, head) as one unsigned 64-bit value whose order is the
+// selection order: the logit key (sign flipped to unsigned order) above,
+// 255 - head below (equal logits: the lower head index is larger).  0 is
+// below every real candidate and marks padding and removed heads.
+NAMOH_DEV uint64_t cand(int key, int j) {
+  return (static_cast<uint64_t>(static_cast<uint32_t>(key) ^ 0x80000000u) << 32) |
+         static_cast<uint32_t>(255 - j);
+}
+NAMOH_DEV int cand_head(uint64_t c) { return 255 - static_cast<int>(c & 0xFFu); }
+NAMOH_DEV int cand_key(uint64_t c) {
+  return static_cast<int>(static_cast<uint32_t>(c >> 32) ^ 0x80000000u);
+}
+
+// 64-bit max with the value of another lane of the 8-lane group, moved by a
+// DPP lane pattern (quad_perm [1,0,3,2] = xor 1, [2,3,0,1] = xor 2,
+// row_half_mirror = lane 7 - i inside each 8-lane group).
+template <int CTRL>
+NAMOH_DEV uint64_t max_dpp(uint64_t x) {
+  const int lo = __builtin_amdgcn_mov_dpp(static_cast<int>(static_cast<uint32_t>(x)), CTRL, 0xF,
+                                          0xF, true);
+  const int hi = __builtin_amdgcn_mov_dpp(static_cast<int>(static_cast<uint32_t>(x >> 32)), CTRL,
+                                          0xF, 0xF, true);
+  const uint64_t y = (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) |
+                     static_cast<uint32_t>(lo);
+  return y > x ? y : x;
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141;
+
+// 8 lanes per token, lane `sub` holding heads sub*HL .. sub*HL + HL - 1.
+// Round k: every lane takes the largest of its remaining candidates, three
+// DPP steps reduce the group to the winner (after the first two the four
+// lanes of each quad agree, so the mirror exchange pairs the two quads), and
+// the owning lane removes it.  K <= KMAX <= 8 keeps the winners in
+// registers and lane k of the group stores round k; otherwise lane 0 stores
+// and rescales in place.
 template <int HMAX, int KMAX>
 __global__ __launch_bounds__(kCountThreads) void k_route_count(
     const float* __restrict__ logits, int T, int H, int K, int gate_mode,
     int nchunk, int32_t* __restrict__ topk_idx, float* __restrict__ gates,
-    int32_t* __restrict__ chunk_counts) {
+    int32_t* __restrict__ slot_rank, int32_t* __restrict__ chunk_counts) {
   constexpr int HL = HMAX / kLPT;
-  __shared__ int s_cnt[64];
+  __shared__ int s_wcnt[kCountWaves][HMAX];
   const int b = blockIdx.x / nchunk;
   const int c = blockIdx.x - b * nchunk;
   const int tid = threadIdx.x;
   const int sub = tid % kLPT;
+  const int wave = tid / kWave, lane = tid % kWave;
   const int t = c * kRC + tid / kLPT;
   const bool valid = t < T;
   const size_t row = static_cast<size_t>(b) * T + (valid ? t : 0);
-  if (tid < 64) s_cnt[tid] = 0;
 
-  int key[HL];
   float val[HL];
-  const float* lp = logits + row * H;
+  const float* lp = logits + row * H + sub * HL;
+  const bool vec = H == HMAX && (reinterpret_cast<uintptr_t>(logits) & 31) == 0;
+  if (vec && valid) {   // whole rows of a 32-byte aligned array: vector loads
+    if constexpr (HL == 8) {
+      const float4 x0 = reinterpret_cast<const float4*>(lp)[0];
+      const float4 x1 = reinterpret_cast<const float4*>(lp)[1];
+      val[0] = x0.x; val[1] = x0.y; val[2] = x0.z; val[3] = x0.w;
+      val[4] = x1.x; val[5] = x1.y; val[6] = x1.z; val[7] = x1.w;
+    } else if constexpr (HL == 4) {
+      const float4 x0 = *reinterpret_cast<const float4*>(lp);
+      val[0] = x0.x; val[1] = x0.y; val[2] = x0.z; val[3] = x0.w;
+    } else if constexpr (HL == 2) {
+      const float2 x0 = *reinterpret_cast<const float2*>(lp);
+      val[0] = x0.x; val[1] = x0.y;
+    } else {
+      val[0] = lp[0];
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < HL; ++e) val[e] = (valid && sub * HL + e < H) ? lp[e] : -INFINITY;
+  }
+  uint64_t ck[HL];
 #pragma unroll
   for (int e = 0; e < HL; ++e) {
     const int j = sub * HL + e;
-    val[e] = (valid && j < H) ? lp[j] : -INFINITY;
-    key[e] = (valid && j < H) ? logit_key(val[e]) : INT_MIN;
+    ck[e] = (valid && j < H) ? cand(logit_key(val[e]), j) : 0ull;
   }
+
   int32_t* tk = topk_idx + row * K;
   float* gk = gates + row * K;
-  int pk = INT_MAX, pj = -1;     // previous winner
-  unsigned own = 0;              // selected heads owned by this lane
+  unsigned own = 0;              // selected heads held by this lane (bit e)
+  int own_k[HL];                 // ... and the round that selected each
   float lmax = 0.f, denom = 0.f;
-  // with K <= KMAX (<= 8) the winners stay in registers and lane k of the
-  // group stores round k; otherwise lane 0 stores and rescales in place
-  int wj[KMAX];
-  float we[KMAX];
+  int wj[KMAX <= 8 ? KMAX : 1];
+  float we[KMAX <= 8 ? KMAX : 1];
 #pragma unroll
-  for (int k = 0; k < KMAX; ++k) {
+  for (int e = 0; e < HL; ++e) own_k[e] = 0;
+#pragma unroll
+  for (int k = 0; k < (KMAX <= 8 ? KMAX : 1); ++k) {
     wj[k] = 0;
     we[k] = 0.f;
   }
-#pragma unroll (KMAX <= 8 ? KMAX : 1)
+#pragma unroll(KMAX <= 8 ? KMAX : 1)
   for (int k = 0; k < (KMAX <= 8 ? KMAX : K); ++k) {
     if (KMAX <= 8 && k >= K) break;
-    int bk = INT_MIN, bj = INT_MAX;
+    uint64_t best = ck[0];
 #pragma unroll
-    for (int e = 0; e < HL; ++e) {
-      const int j = sub * HL + e;
-      const bool cand = key[e] < pk || (key[e] == pk && j > pj);
-      const bool better = cand && (key[e] > bk || (key[e] == bk && j < bj));
-      bk = better ? key[e] : bk;
-      bj = better ? j : bj;
-    }
+    for (int e = 1; e < HL; ++e) best = ck[e] > best ? ck[e] : best;
+    best = max_dpp<kDppXor1>(best);
+    best = max_dpp<kDppXor2>(best);
+    best = max_dpp<kDppHalfMirror>(best);
 #pragma unroll
-    for (int o = 1; o < kLPT; o <<= 1) {
-      const int ok = __shfl_xor(bk, o, kLPT);
-      const int oj = __shfl_xor(bj, o, kLPT);
-      const bool better = ok > bk || (ok == bk && oj < bj);
-      bk = better ? ok : bk;
-      bj = better ? oj : bj;
-    }
-    pk = bk;
-    pj = bj;
-    if (bj / HL == sub) own |= 1u << (bj - sub * HL);
-    const float v = key_logit(bk);
+    for (int e = 0; e < HL; ++e)
+      if (valid && ck[e] == best) {
+        ck[e] = 0ull;
+        own |= 1u << e;
+        own_k[e] = k;
+      }
+    const int bj = cand_head(best);
+    const float v = key_logit(cand_key(best));
     if (k == 0) lmax = v;
     const float e = expf(v - lmax);
     denom += e;
     if constexpr (KMAX <= 8) {
-      wj[k] = bj;
-      we[k] = e;
+#pragma unroll
+      for (int kk = 0; kk < KMAX; ++kk)
+        if (kk == k) {
+          wj[kk] = bj;
+          we[kk] = e;
+        }
     } else if (valid && sub == 0) {
       tk[k] = bj;
       gk[k] = e;  // unnormalised; scaled below
@@ -128,15 +177,53 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
     denom = part;
   }
   const float inv = 1.f / denom;
+  int mj = 0;
+  float me = 0.f;
   if constexpr (KMAX <= 8) {
-    int mj = 0;
-    float me = 0.f;
 #pragma unroll
     for (int k = 0; k < KMAX; ++k)
       if (sub == k) {
         mj = wj[k];
         me = we[k];
       }
+  }
+
+  // Ranks inside the chunk.  Ballot e marks the lanes holding their bit e;
+  // head h = s*HL + e lives in lane s of every token group, so the wave's
+  // tokens routed to h are ballot_e & (lanes s, s+8, ...).
+  uint64_t bal[HL];
+#pragma unroll
+  for (int e = 0; e < HL; ++e) bal[e] = __ballot((own >> e) & 1u);
+  const uint64_t same_sub = 0x0101010101010101ull << sub;
+  if (lane < HMAX) {   // wave count of head `lane`
+    const int hs = lane / HL, he = lane % HL;
+    uint64_t be = bal[0];
+#pragma unroll
+    for (int e = 1; e < HL; ++e) be = he == e ? bal[e] : be;
+    s_wcnt[wave][lane] = __popcll(be & (0x0101010101010101ull << hs));
+  }
+  __syncthreads();
+  if (valid) {
+    const uint64_t below = lanemask_lt() & same_sub;
+    int32_t* rk = slot_rank + row * K;
+#pragma unroll
+    for (int e = 0; e < HL; ++e)
+      if ((own >> e) & 1u) {
+        const int h = sub * HL + e;
+        int r = __popcll(bal[e] & below);
+        for (int w = 0; w < wave; ++w) r += s_wcnt[w][h];
+        rk[own_k[e]] = r;
+      }
+  }
+  if (tid < H) {
+    int n = 0;
+#pragma unroll
+    for (int w = 0; w < kCountWaves; ++w) n += s_wcnt[w][tid];
+    chunk_counts[(static_cast<size_t>(b) * H + tid) * nchunk + c] = n;
+  }
+  // the selections and gates are stored last: a barrier after a global
+  // store would wait for the store to complete
+  if constexpr (KMAX <= 8) {
     if (valid && sub < K) {
       tk[sub] = mj;
       gk[sub] = me * inv;
@@ -144,13 +231,6 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
   } else if (valid && sub == 0) {
     for (int k = 0; k < K; ++k) gk[k] *= inv;
   }
-  __syncthreads();
-  if (valid)
-#pragma unroll
-    for (int e = 0; e < HL; ++e)
-      if ((own >> e) & 1u) atomicAdd(&s_cnt[sub * HL + e], 1);
-  __syncthreads();
-  if (tid < H) chunk_counts[(static_cast<size_t>(b) * H + tid) * nchunk + c] = s_cnt[tid];
 }
 
 __global__ __launch_bounds__(kWave) void k_route_scan(
@@ -170,49 +250,34 @@ __global__ __launch_bounds__(kWave) void k_route_scan(
   if (lane == 0) head_len[s] = carry;
 }
 
-__global__ __launch_bounds__(kRC) void k_route_scatter(
+__global__ __launch_bounds__(kScatterThreads) void k_route_scatter(
     const int32_t* __restrict__ topk_idx, int B, int T, int H, int K, int nchunk,
     const int32_t* __restrict__ within, const int32_t* __restrict__ head_len,
     int32_t* __restrict__ seg_offsets, int32_t* __restrict__ perm_token,
     int32_t* __restrict__ slot_pos) {
-  __shared__ uint64_t s_bal[64];
   __shared__ int s_base[64];
   const int b = blockIdx.x / nchunk;
   const int c = blockIdx.x - b * nchunk;
-  const int lane = threadIdx.x;
-  const int t = c * kRC + lane;
-  const bool valid = t < T;
-  const size_t row = static_cast<size_t>(b) * T + (valid ? t : 0);
-  const int32_t* tk = topk_idx + row * K;
-
-  // segment offsets of sequence b
-  const int hl = lane < H ? head_len[static_cast<size_t>(b) * H + lane] : 0;
-  const int seg_off = b * T * K + wave_inclusive_scan(hl) - hl;
-  if (lane < H) {
-    if (c == 0) seg_offsets[static_cast<size_t>(b) * H + lane] = seg_off;
-    s_base[lane] = seg_off + within[(static_cast<size_t>(b) * H + lane) * nchunk + c];
-  }
-  if (c == 0 && b == B - 1 && lane == 0) seg_offsets[static_cast<size_t>(B) * H] = B * T * K;
-
-  uint64_t mask = 0;
-  if (valid)
-    for (int k = 0; k < K; ++k) mask |= 1ull << tk[k];
-  uint64_t mine = 0;
-  for (int h = 0; h < H; ++h) {
-    const uint64_t bal = __ballot((mask >> h) & 1ull);
-    if (lane == h) mine = bal;
-  }
-  s_bal[lane] = mine;
-  __syncthreads();
-  if (valid) {
-    const uint64_t below = lanemask_lt();
-    int32_t* sp = slot_pos + row * K;
-    for (int k = 0; k < K; ++k) {
-      const int h = tk[k];
-      const int pos = s_base[h] + __popcll(s_bal[h] & below);
-      perm_token[pos] = t;
-      sp[k] = pos;
+  const int tid = threadIdx.x;
+  if (tid < kWave) {
+    // segment offsets of sequence b and this chunk's start in each segment
+    const int hl = tid < H ? head_len[static_cast<size_t>(b) * H + tid] : 0;
+    const int seg_off = b * T * K + wave_inclusive_scan(hl) - hl;
+    if (tid < H) {
+      if (c == 0) seg_offsets[static_cast<size_t>(b) * H + tid] = seg_off;
+      s_base[tid] = seg_off + within[(static_cast<size_t>(b) * H + tid) * nchunk + c];
     }
+    if (c == 0 && b == B - 1 && tid == 0) seg_offsets[static_cast<size_t>(B) * H] = B * T * K;
+  }
+  __syncthreads();
+  const int t0 = c * kRC;
+  const int nt = min(kRC, T - t0);
+  const size_t e0 = (static_cast<size_t>(b) * T + t0) * K;
+  for (int e = tid; e < nt * K; e += kScatterThreads) {
+    const int h = topk_idx[e0 + e];
+    const int pos = s_base[h] + slot_pos[e0 + e];
+    perm_token[pos] = t0 + e / K;
+    slot_pos[e0 + e] = pos;
   }
 }
 
@@ -234,7 +299,7 @@ hipError_t launch_route(const float* logits, int B, int T, int H, int K,
   int32_t* within = cv.take<int32_t>(L);
   const dim3 grid(static_cast<unsigned>(static_cast<size_t>(B) * nchunk));
 #define NAMOH_RC(HM, KM) \
-  k_route_count<HM, KM><<<grid, kCountThreads, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, counts)
+  k_route_count<HM, KM><<<grid, kCountThreads, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, slot_pos, counts)
   const bool small_k = K <= 8;
   if (H <= 8) NAMOH_RC(8, 8);
   else if (H <= 16) { if (small_k) NAMOH_RC(16, 8); else NAMOH_RC(16, 64); }
@@ -245,8 +310,8 @@ hipError_t launch_route(const float* logits, int B, int T, int H, int K,
   if (e != hipSuccess) return e;
   k_route_scan<<<B * H, kWave, 0, st>>>(counts, nchunk, within, head_len);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  k_route_scatter<<<grid, kRC, 0, st>>>(topk_idx, B, T, H, K, nchunk, within, head_len,
-                                        seg_offsets, perm_token, slot_pos);
+  k_route_scatter<<<grid, kScatterThreads, 0, st>>>(topk_idx, B, T, H, K, nchunk, within,
+                                                    head_len, seg_offsets, perm_token, slot_pos);
   return hipGetLastError();
 }
 
