@@ -61,6 +61,12 @@ constexpr int kBN = 64;            // keys per tile
 #endif
 // NW waves per workgroup, NQT 32-query sub-tiles per wave, MINB workgroups
 // per compute unit the register allocation must allow.
+#ifndef NAMOH_D64_VPRE
+#define NAMOH_D64_VPRE 4
+#endif
+#ifndef NAMOH_D128_VPRE
+#define NAMOH_D128_VPRE 2
+#endif
 #ifndef NAMOH_D64_NS
 #define NAMOH_D64_NS 2
 #endif
@@ -546,7 +552,7 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
   // value operands: the first VPRE 16-key steps are read while the softmax
   // runs (all of them for d = 64; half for d = 128, to stay within 256
   // registers), the rest while the first P.V products execute
-  constexpr int VPRE = D == 128 ? 2 : 4;
+  constexpr int VPRE = D == 128 ? NAMOH_D128_VPRE : NAMOH_D64_VPRE;
   bf16x8 va[4][D / 32];
   auto vread = [&](int k2) {
 #pragma unroll

@@ -273,10 +273,15 @@ __global__ __launch_bounds__(kScatterThreads) void k_route_scatter(
   const int t0 = c * kRC;
   const int nt = min(kRC, T - t0);
   const size_t e0 = (static_cast<size_t>(b) * T + t0) * K;
+  const unsigned nr = static_cast<unsigned>(B) * T * K;
   for (int e = tid; e < nt * K; e += kScatterThreads) {
     const int h = topk_idx[e0 + e];
-    const int pos = s_base[h] + slot_pos[e0 + e];
-    perm_token[pos] = t0 + e / K;
+    // the head and the in-chunk rank come from k_route_count; a position
+    // outside [0, B*T*K) can only come from a corrupted workspace and is
+    // not stored
+    const int pos = static_cast<unsigned>(h) < static_cast<unsigned>(H)
+                        ? s_base[h] + slot_pos[e0 + e] : -1;
+    if (static_cast<unsigned>(pos) < nr) perm_token[pos] = t0 + e / K;
     slot_pos[e0 + e] = pos;
   }
 }
