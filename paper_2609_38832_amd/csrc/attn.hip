@@ -510,6 +510,28 @@ NAMOH_DEV void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
 }
 
+// Wave priority around the matrix-core blocks (s_setprio; 0 = unchanged).
+#ifndef NAMOH_PRIO_QK
+#define NAMOH_PRIO_QK 1
+#endif
+#ifndef NAMOH_PRIO_PV
+#define NAMOH_PRIO_PV 0
+#endif
+template <int P>
+NAMOH_DEV void wave_prio() {
+  if constexpr (P > 0) {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(P);
+  }
+}
+template <int P>
+NAMOH_DEV void wave_prio_reset() {
+  if constexpr (P > 0) {
+    __builtin_amdgcn_s_setprio(0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 // S^T = K Q^T for one 64-key tile: 2 key sub-tiles x NQT query sub-tiles.
 // All LDS operand reads of the tile are issued before the first MFMA (the
 // scheduling barrier keeps them there), so LDS latency is paid once per tile
@@ -533,6 +555,7 @@ NAMOH_DEV void qk_tile(f32x16 (&S)[2][NQT], const uint16_t* __restrict__ sKb,
     for (int qt = 0; qt < NQT; ++qt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) S[kk][qt][e] = 0.f;
+  wave_prio<NAMOH_PRIO_QK>();
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
@@ -540,6 +563,7 @@ NAMOH_DEV void qk_tile(f32x16 (&S)[2][NQT], const uint16_t* __restrict__ sKb,
 #pragma unroll
       for (int qt = 0; qt < NQT; ++qt)
         S[kk][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][kk], qB[qt][ks], S[kk][qt], 0, 0, 0);
+  wave_prio_reset<NAMOH_PRIO_QK>();
 }
 
 // Mask, online softmax and O^T += V^T P^T for one 64-key tile.
@@ -623,6 +647,7 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
   }
 #pragma unroll
   for (int k2 = VPRE; k2 < 4; ++k2) vread(k2);
+  wave_prio<NAMOH_PRIO_PV>();
 #pragma unroll
   for (int k2 = 0; k2 < 4; ++k2)
 #pragma unroll
@@ -630,6 +655,7 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
 #pragma unroll
       for (int qt = 0; qt < NQT; ++qt)
         O[mt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[k2][mt], pB[qt][k2], O[mt][qt], 0, 0, 0);
+  wave_prio_reset<NAMOH_PRIO_PV>();
 }
 
 // ---------------------------------------------------------------------------
