@@ -112,6 +112,8 @@ namoh_status namoh_route(const float* logits, int B, int T, int H, int K,
  * bf16 with d in {64, 128} runs on bf16 MFMA (float32 accumulation and
  * softmax; rotated q/k and the probabilities are rounded to bf16 before
  * their products); every other combination runs in float32 arithmetic.
+ * The bf16 MFMA path needs ceil(T/64)*64*d*2 < 2^32 bytes per segment
+ * (T below 2^24 at d = 128); longer T returns NAMOH_ERR_UNSUPPORTED.
  * ---------------------------------------------------------------------- */
 size_t namoh_attn_fwd_workspace_size(int B, int T, int H, int K, int d_head,
                                      int dtype);

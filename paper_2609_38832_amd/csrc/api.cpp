@@ -155,6 +155,14 @@ namoh_status namoh_attn_fwd(const void* q, const void* k, const void* v, int dty
   REQUIRE(!std::isnan(softmax_scale) && !std::isinf(softmax_scale), "softmax_scale must be finite");
   const long long dense = static_cast<long long>(B) * H * T * d_head;
   REQUIRE(dense < (1ll << 40), "q/k/v too large");
+  if (dtype == NAMOH_BF16 && (d_head == 64 || d_head == 128)) {
+    // the MFMA kernel addresses one segment's packed key/value tiles with
+    // 32-bit buffer offsets
+    const long long seg_bytes = (static_cast<long long>(T) + 63) / 64 * 64 * d_head * 2;
+    if (seg_bytes >= (1ll << 32))
+      return fail(NAMOH_ERR_UNSUPPORTED, "T = %d too long for d_head = %d on the bf16 path", T,
+                  d_head);
+  }
   REQUIRE_PTR(q, 16);
   REQUIRE_PTR(k, 16);
   REQUIRE_PTR(v, 16);

@@ -479,27 +479,46 @@ NAMOH_DEV int swz(int row, int gr) {
   return GPR == 16 ? (gr ^ (row & 15)) : (gr ^ ((row >> 1) & 7));
 }
 
-// Tile staging, direct global -> LDS (global_load_lds_dwordx4): KPT 16-byte
+// Tile staging, direct HBM -> LDS (buffer_load_dwordx4 ... lds): KPT 16-byte
 // granules per thread of one packed key tile or one transposed value tile
 // (contiguous in HBM).  Lane l of a wave instruction writes LDS granule
-// base + l, so the swizzle is applied on the global side: the lane that
+// base + l, so the swizzle is applied on the source side: the lane that
 // fills physical granule P = row * GPR + phys fetches logical granule
-// swz(row, phys) of that row (the XOR is its own inverse).  Completion is
-// tracked by vmcnt: wait_vmcnt<N>() before the barrier that publishes a tile
-// leaves only the N most recent loads of the wave in flight.
+// swz(row, phys) of that row (the XOR is its own inverse).  The buffer
+// resource covers the item's key (or value) tiles and the tile is selected
+// by the scalar offset, so a tile costs no vector address arithmetic; the
+// LDS base goes through M0 from scalar registers.  Completion is tracked by
+// vmcnt: wait_vmcnt<N>() before the barrier that publishes a tile leaves only
+// the N most recent loads of the wave in flight.
 typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glb_void_t;
+
+// Byte offsets (inside one tile) of the KPT granules this lane fetches.
 template <int GPR, int KPT, int NT>
-NAMOH_DEV void tile_dma(const uint16_t* __restrict__ tile, uint16_t* lds_tile, int tid) {
+NAMOH_DEV void tile_voffsets(uint32_t (&voff)[KPT], int tid) {
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
     const int P = tid + i * NT;                 // physical granule of this lane
     const int row = P / GPR, phys = P % GPR;
-    const int gr = swz<GPR>(row, phys);
-    const uint16_t* src = tile + (row * GPR + gr) * 8;
-    uint16_t* dst = lds_tile + (P - (tid & 63)) * 8;   // wave-uniform base
-    __builtin_amdgcn_global_load_lds((glb_void_t*)(src), (lds_void_t*)(dst), 16, 0, 0);
+    voff[i] = static_cast<uint32_t>((row * GPR + swz<GPR>(row, phys)) * 16);
   }
+}
+
+// One tile.  base/nbytes: the buffer (the item's key or value tiles; loads
+// past nbytes return 0); tile_bytes: byte offset of the tile in it (wave
+// uniform); lds_wave: the stage's LDS tile plus this wave's first granule.
+template <int KPT, int NT>
+NAMOH_DEV void tile_dma(const uint16_t* base, uint32_t nbytes, uint32_t tile_bytes,
+                        char* lds_wave, const uint32_t (&voff)[KPT]) {
+  // wave-uniform scalar offset (readfirstlane keeps it out of vector
+  // registers, which would force a loop over distinct values)
+  const int tb = __builtin_amdgcn_readfirstlane(static_cast<int>(tile_bytes));
+  // raw buffer resource: stride 0, num_records in bytes
+  const auto rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0,
+                                                      static_cast<int>(nbytes), 0x00020000);
+#pragma unroll
+  for (int i = 0; i < KPT; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)(lds_wave + i * NT * 16), 16,
+                                             static_cast<int>(voff[i]), tb, 0, 0);
 }
 
 // s_waitcnt vmcnt(N) (expcnt and lgkmcnt left at their "no wait" values);
@@ -512,7 +531,7 @@ NAMOH_DEV void wait_vmcnt() {
 
 // Wave priority around the matrix-core blocks (s_setprio; 0 = unchanged).
 #ifndef NAMOH_PRIO_QK
-#define NAMOH_PRIO_QK 1
+#define NAMOH_PRIO_QK 0
 #endif
 #ifndef NAMOH_PRIO_PV
 #define NAMOH_PRIO_PV 0
@@ -721,14 +740,26 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   // so the number of loads in flight is the same on every path; the
   // repeats land in stages the loop never reads and are complete before the
   // loop's last iteration)
-  constexpr size_t TS = static_cast<size_t>(kBN) * D;
-  const uint16_t* Kbase = Kp + static_cast<size_t>(tile0) * TS;
-  const uint16_t* Vbase = Vt + static_cast<size_t>(tile0) * TS;
+  constexpr size_t TS = static_cast<size_t>(kBN) * D;   // elements per tile
+  constexpr uint32_t TB = static_cast<uint32_t>(TS * 2);  // bytes per tile
+  // (the buffer resource lives in scalar registers: the item's values are
+  // uniform, and readfirstlane says so)
+  const int tile0_s = __builtin_amdgcn_readfirstlane(tile0);
+  const int kt_end_s = __builtin_amdgcn_readfirstlane(kt_end);
+  const uint16_t* const bK = Kp + static_cast<size_t>(tile0_s) * TS;
+  const uint16_t* const bV = Vt + static_cast<size_t>(tile0_s) * TS;
+  const uint32_t nb = static_cast<uint32_t>(kt_end_s) * TB;   // below 2^32 (checked on the host)
+  uint32_t voffK[KPT], voffV[KPT];
+  tile_voffsets<D / 8, KPT, NT>(voffK, tid);
+  tile_voffsets<kBN / 8, KPT, NT>(voffV, tid);
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  char* const lK = reinterpret_cast<char*>(&sK[0][0]) + wave_s * kWave * 16;
+  char* const lV = reinterpret_cast<char*>(&sV[0][0]) + wave_s * kWave * 16;
 #pragma unroll
   for (int i = 0; i < NS - 1; ++i) {
-    const int ti = min(i, kt_end - 1);
-    tile_dma<D / 8, KPT, NT>(Kbase + ti * TS, sK[i], tid);
-    tile_dma<kBN / 8, KPT, NT>(Vbase + ti * TS, sV[i], tid);
+    const uint32_t tb = static_cast<uint32_t>(min(i, kt_end_s - 1)) * TB;
+    tile_dma<KPT, NT>(bK, nb, tb, lK + i * TB, voffK);
+    tile_dma<KPT, NT>(bV, nb, tb, lV + i * TB, voffV);
   }
 
   // ---- query block: gather, rotate, round to bf16 B operands -------------
@@ -798,8 +829,9 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     __syncthreads();
     if (kt + NS - 1 < kt_end) {
       const int nst = (kt + NS - 1) % NS;
-      tile_dma<D / 8, KPT, NT>(Kbase + (kt + NS - 1) * TS, sK[nst], tid);
-      tile_dma<kBN / 8, KPT, NT>(Vbase + (kt + NS - 1) * TS, sV[nst], tid);
+      const uint32_t tb = static_cast<uint32_t>(kt + NS - 1) * TB;
+      tile_dma<KPT, NT>(bK, nb, tb, lK + nst * TB, voffK);
+      tile_dma<KPT, NT>(bV, nb, tb, lV + nst * TB, voffV);
     }
     if (kt < wave_tiles) {
       f32x16 S[2][NQT];

@@ -76,6 +76,7 @@ def _attn(lib, dtype=1, B=1, T=64, H=8, K=2, d=64, base=1e4, rope=0, scale=0.0, 
     (dict(scale=float("nan")), 1), (dict(q=None), 1), (dict(q=P(A + 8)), 1),
     (dict(gates=None), 1), (dict(out=P(A + 4)), 1), (dict(head_out=P(A + 4)), 1),
     (dict(wsb=100), 3), (dict(K=9), 1),
+    (dict(T=1 << 24, d=128), 2),                 # segment tiles past 32-bit offsets
 ])
 def test_attn_rejects(lib, kw, code):
     assert _attn(lib, **kw) == code
