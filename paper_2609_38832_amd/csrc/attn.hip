@@ -54,7 +54,7 @@ constexpr int kBN = 64;            // keys per tile
 #define NAMOH_D128_NQT 1
 #endif
 #ifndef NAMOH_D64_MINB
-#define NAMOH_D64_MINB 2
+#define NAMOH_D64_MINB 3
 #endif
 #ifndef NAMOH_D128_MINB
 #define NAMOH_D128_MINB 2
@@ -83,9 +83,10 @@ template <> struct MfmaShape<128> {
   static constexpr int NW = NAMOH_D128_NW, NQT = NAMOH_D128_NQT, MINB = NAMOH_D128_MINB,
                        NS = NAMOH_D128_NS;
 };
-// The running softmax maximum is only raised when a tile exceeds it by more
-// than 2^kLazyLog2 (probabilities then stay below 2^kLazyLog2 and the final
-// normalisation is exact), so the output accumulator is rarely rescaled.
+// The running softmax maximum (log2 units) is only raised when a tile
+// exceeds it by more than kLazyLog2 (probabilities then stay below
+// 2^kLazyLog2 and the final normalisation is exact), so the output
+// accumulator is rarely rescaled.
 constexpr float kLazyLog2 = 8.f;
 constexpr int kGenericBM = 64;
 
@@ -531,7 +532,7 @@ NAMOH_DEV void wait_vmcnt() {
 
 // Wave priority around the matrix-core blocks (s_setprio; 0 = unchanged).
 #ifndef NAMOH_PRIO_QK
-#define NAMOH_PRIO_QK 0
+#define NAMOH_PRIO_QK 1
 #endif
 #ifndef NAMOH_PRIO_PV
 #define NAMOH_PRIO_PV 0
@@ -557,7 +558,8 @@ NAMOH_DEV void wave_prio_reset() {
 // instead of once per MFMA.
 template <int D, int NQT>
 NAMOH_DEV void qk_tile(f32x16 (&S)[2][NQT], const uint16_t* __restrict__ sKb,
-                       const bf16x8 (&qB)[NQT][D / 16], int c, int g) {
+                       const bf16x8 (&qB)[NQT][D / 16], const f32x16 (&minit)[NQT], int c,
+                       int g) {
   constexpr int KS = D / 16;
   bf16x8 a[KS][2];
 #pragma unroll
@@ -568,15 +570,16 @@ NAMOH_DEV void qk_tile(f32x16 (&S)[2][NQT], const uint16_t* __restrict__ sKb,
       a[ks][kk] = *reinterpret_cast<const bf16x8*>(&sKb[row * D + swz<D / 8>(row, 2 * ks + g) * 8]);
     }
   __builtin_amdgcn_sched_barrier(0);
+  wave_prio<NAMOH_PRIO_QK>();
+  // the accumulators start at -m (the query's running maximum), so the
+  // scores leave the products already shifted
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt)
+      S[kk][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][kk], qB[qt][0], minit[qt], 0, 0, 0);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) S[kk][qt][e] = 0.f;
-  wave_prio<NAMOH_PRIO_QK>();
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks)
+  for (int ks = 1; ks < KS; ++ks)
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
@@ -586,12 +589,19 @@ NAMOH_DEV void qk_tile(f32x16 (&S)[2][NQT], const uint16_t* __restrict__ sKb,
 }
 
 // Mask, online softmax and O^T += V^T P^T for one 64-key tile.
+//
+// Scores arrive in log2 units (queries pre-scaled by scale * log2 e) and
+// already shifted by the running maximum m (the accumulator start), so the
+// common tile needs exp2 of the score and nothing else.  m is raised only
+// when a tile's shifted maximum exceeds 2^kLazyLog2 in probability, and on
+// a wave's first tile, which sets it to that tile's maximum; such a tile
+// (rare) subtracts the raise from its scores, rescales O and l, and
+// rebuilds the accumulator start.
 template <int D, int NQT, int NW>
 NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
-                          float (&m_run)[NQT], float (&l_run)[NQT],
-                          const uint16_t* __restrict__ sVb, int key0, int q0,
-                          int wave, int n, int c, int g, float scale_log2,
-                          float lazy_thr) {
+                          float (&m_run)[NQT], float (&l_run)[NQT], f32x16 (&minit)[NQT],
+                          bool first, const uint16_t* __restrict__ sVb, int key0, int q0,
+                          int wave, int n, int c, int g) {
   // value operands: the first VPRE 16-key steps are read while the softmax
   // runs (all of them for d = 64; half for d = 128, to stay within 256
   // registers), the rest while the first P.V products execute
@@ -624,28 +634,49 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
     }
   }
   bf16x8 pB[NQT][4];
-  float alpha[NQT];
+  float alpha[NQT], delta[NQT];
   bool rescale = false;
 #pragma unroll
   for (int qt = 0; qt < NQT; ++qt) {
-    float mx = -INFINITY;
+    float mx = fmaxf(S[0][qt][0], S[0][qt][1]);
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(S[kk][qt][e], S[kk][qt][e + 1]));
+    for (int i = 2; i < 32; i += 2)
+      mx = fmaxf(fmaxf(mx, S[i >> 4][qt][i & 15]), S[i >> 4][qt][(i & 15) + 1]);
     mx = pair_max32(mx);
-    const bool up = mx > m_run[qt] + lazy_thr;
-    const float mnew = up ? mx : m_run[qt];
-    alpha[qt] = up ? __builtin_amdgcn_exp2f((m_run[qt] - mnew) * scale_log2) : 1.f;
+    const bool up = first || mx > kLazyLog2;
+    delta[qt] = up ? mx : 0.f;
+    alpha[qt] = (up && !first) ? __builtin_amdgcn_exp2f(-mx) : 1.f;
     rescale |= up;
-    const float mc = mnew * scale_log2;
+  }
+  if (__any(rescale)) {
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) S[kk][qt][e] -= delta[qt];
+      m_run[qt] += delta[qt];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) minit[qt][e] = -m_run[qt];
+    }
+    if (!first) {
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt)
+#pragma unroll
+        for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) O[mt][qt][e] *= alpha[qt];
+    }
+  }
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt) {
     float ls = 0.f;
 #pragma unroll
     for (int k2 = 0; k2 < 4; ++k2) {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        pB[qt][k2][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(
-            fmaf(S[k2 >> 1][qt][8 * (k2 & 1) + e], scale_log2, -mc)));
+        pB[qt][k2][e] =
+            static_cast<__bf16>(__builtin_amdgcn_exp2f(S[k2 >> 1][qt][8 * (k2 & 1) + e]));
       // row sum of the rounded probabilities: pairs times (1, 1)
 #pragma unroll
       for (int e = 0; e < 8; e += 2) {
@@ -654,15 +685,6 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
       }
     }
     l_run[qt] = l_run[qt] * alpha[qt] + ls;
-    m_run[qt] = mnew;
-  }
-  if (__any(rescale)) {
-#pragma unroll
-    for (int qt = 0; qt < NQT; ++qt)
-#pragma unroll
-      for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) O[mt][qt][e] *= alpha[qt];
   }
 #pragma unroll
   for (int k2 = VPRE; k2 < 4; ++k2) vread(k2);
@@ -724,7 +746,6 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   const int wq_last = q0 + 32 * ((NQT - 1) * NW + wave) + 31;
   const int wave_tiles = min(ntiles, wq_last / kBN + 1);
   const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
-  const float lazy_thr = kLazyLog2 / scale_log2;
 
   // token of each query row (issued before the tile loads, so waiting for it
   // does not wait for them)
@@ -774,6 +795,7 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     const int t = min(static_cast<unsigned>(qtok[qt]), static_cast<unsigned>(T - 1));
     const uint16_t* qrow = q + (head_base + t) * D;
     const int pos = rope_mode == 0 ? rr : (rope_mode == 1 ? t : 0);
+    const float qscale = r < n ? scale_log2 : 0.f;   // padding rows: zero queries
     u32x4 qa[KS / 2], qb2[KS / 2];
     float4 cs[KS / 2][4];
 #pragma unroll
@@ -793,9 +815,9 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
       }
       rope8(x1, x2, cs[s2]);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        qB[qt][s2][e] = static_cast<__bf16>(r < n ? x1[e] : 0.f);
-        qB[qt][s2 + KS / 2][e] = static_cast<__bf16>(r < n ? x2[e] : 0.f);
+      for (int e = 0; e < 8; ++e) {   // pre-scaled: scores come out in log2 units
+        qB[qt][s2][e] = static_cast<__bf16>(x1[e] * qscale);
+        qB[qt][s2 + KS / 2][e] = static_cast<__bf16>(x2[e] * qscale);
       }
     }
   }
@@ -808,10 +830,13 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
 #pragma unroll
       for (int e = 0; e < 16; ++e) O[mt][qt][e] = 0.f;
   float m_run[NQT], l_run[NQT];
+  f32x16 minit[NQT];
 #pragma unroll
   for (int qt = 0; qt < NQT; ++qt) {
-    m_run[qt] = -1e30f;
+    m_run[qt] = 0.f;   // set from the first tile
     l_run[qt] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) minit[qt][e] = 0.f;
   }
 
   // ---- tile loop: NS-stage ring of K/V tiles, one barrier per tile -------
@@ -835,9 +860,9 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     }
     if (kt < wave_tiles) {
       f32x16 S[2][NQT];
-      qk_tile<D, NQT>(S, sK[st], qB, c, g);
-      softmax_pv<D, NQT, NW>(S, O, m_run, l_run, sV[st], kt * kBN, q0, wave, n, c, g,
-                             scale_log2, lazy_thr);
+      qk_tile<D, NQT>(S, sK[st], qB, minit, c, g);
+      softmax_pv<D, NQT, NW>(S, O, m_run, l_run, minit, kt == 0, sV[st], kt * kBN, q0, wave,
+                             n, c, g);
     }
   }
 
