@@ -493,15 +493,15 @@ NAMOH_DEV int swz(int row, int gr) {
 // the N most recent loads of the wave in flight.
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// Byte offsets (inside one tile) of the KPT granules this lane fetches.
-template <int GPR, int KPT, int NT>
-NAMOH_DEV void tile_voffsets(uint32_t (&voff)[KPT], int tid) {
-#pragma unroll
-  for (int i = 0; i < KPT; ++i) {
-    const int P = tid + i * NT;                 // physical granule of this lane
-    const int row = P / GPR, phys = P % GPR;
-    voff[i] = static_cast<uint32_t>((row * GPR + swz<GPR>(row, phys)) * 16);
-  }
+// Byte offset (inside one tile) of the first granule this lane fetches.  The
+// lane's i-th granule lies i * NT granules further: NT / GPR rows is a
+// multiple of the 16-row period of the swizzle, so the XOR term does not
+// change with i and one register serves all KPT loads.
+template <int GPR, int NT>
+NAMOH_DEV uint32_t tile_voffset(int tid) {
+  static_assert((NT / GPR) % 16 == 0, "rows per load must be a multiple of the swizzle period");
+  const int row = tid / GPR, phys = tid % GPR;
+  return static_cast<uint32_t>((row * GPR + swz<GPR>(row, phys)) * 16);
 }
 
 // One tile.  base/nbytes: the buffer (the item's key or value tiles; loads
@@ -509,17 +509,18 @@ NAMOH_DEV void tile_voffsets(uint32_t (&voff)[KPT], int tid) {
 // uniform); lds_wave: the stage's LDS tile plus this wave's first granule.
 template <int KPT, int NT>
 NAMOH_DEV void tile_dma(const uint16_t* base, uint32_t nbytes, uint32_t tile_bytes,
-                        char* lds_wave, const uint32_t (&voff)[KPT]) {
-  // wave-uniform scalar offset (readfirstlane keeps it out of vector
-  // registers, which would force a loop over distinct values)
-  const int tb = __builtin_amdgcn_readfirstlane(static_cast<int>(tile_bytes));
+                        char* lds_wave, uint32_t voff) {
   // raw buffer resource: stride 0, num_records in bytes
   const auto rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0,
                                                       static_cast<int>(nbytes), 0x00020000);
 #pragma unroll
-  for (int i = 0; i < KPT; ++i)
+  for (int i = 0; i < KPT; ++i) {
+    // wave-uniform scalar offset (readfirstlane keeps it out of vector
+    // registers, which would force a loop over distinct values)
+    const int tb = __builtin_amdgcn_readfirstlane(static_cast<int>(tile_bytes) + i * NT * 16);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)(lds_wave + i * NT * 16), 16,
-                                             static_cast<int>(voff[i]), tb, 0, 0);
+                                             static_cast<int>(voff), tb, 0, 0);
+  }
 }
 
 // s_waitcnt vmcnt(N) (expcnt and lgkmcnt left at their "no wait" values);
@@ -532,7 +533,7 @@ NAMOH_DEV void wait_vmcnt() {
 
 // Wave priority around the matrix-core blocks (s_setprio; 0 = unchanged).
 #ifndef NAMOH_PRIO_QK
-#define NAMOH_PRIO_QK 1
+#define NAMOH_PRIO_QK 0
 #endif
 #ifndef NAMOH_PRIO_PV
 #define NAMOH_PRIO_PV 0
@@ -770,9 +771,8 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   const uint16_t* const bK = Kp + static_cast<size_t>(tile0_s) * TS;
   const uint16_t* const bV = Vt + static_cast<size_t>(tile0_s) * TS;
   const uint32_t nb = static_cast<uint32_t>(kt_end_s) * TB;   // below 2^32 (checked on the host)
-  uint32_t voffK[KPT], voffV[KPT];
-  tile_voffsets<D / 8, KPT, NT>(voffK, tid);
-  tile_voffsets<kBN / 8, KPT, NT>(voffV, tid);
+  const uint32_t voffK = tile_voffset<D / 8, NT>(tid);
+  const uint32_t voffV = tile_voffset<kBN / 8, NT>(tid);
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
   char* const lK = reinterpret_cast<char*>(&sK[0][0]) + wave_s * kWave * 16;
   char* const lV = reinterpret_cast<char*>(&sV[0][0]) + wave_s * kWave * 16;
