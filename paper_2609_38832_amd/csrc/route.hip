@@ -5,7 +5,7 @@
 // every (batch, head) subsequence): the permutation is a stable counting sort
 // of the (token, head) pairs by segment b*H + h.
 //
-// Three launches; no global atomics, so every output is deterministic:
+// Two or three launches; no global atomics, so every output is deterministic:
 //   1. k_route_count   eight lanes per token, 64 tokens per workgroup: K
 //                      rounds of a cooperative argmax under the total order
 //                      (logit desc, head asc), the gates, and for every
@@ -13,7 +13,9 @@
 //                      tokens routed to that head (stored in slot_pos for
 //                      now), plus the chunk's per-head counts.
 //   2. k_route_scan    one wave per (b, h) segment: exclusive scan of the
-//                      segment's chunk counts and the head length n.
+//                      segment's chunk counts and the head length n (only
+//                      for long sequences; otherwise the scatter sums its
+//                      own prefixes from the counts, one launch fewer).
 //   3. k_route_scatter one workgroup per chunk: the segment offsets of
 //                      sequence b are b*T*K plus a scan of its H head
 //                      lengths (every sequence contributes exactly T*K
@@ -31,6 +33,7 @@ constexpr int kLPT = 8;            // lanes per token in k_route_count
 constexpr int kCountThreads = kRC * kLPT;
 constexpr int kCountWaves = kCountThreads / kWave;
 constexpr int kScatterThreads = 512;
+constexpr long kFusedScan = 8192;   // chunks x heads per sequence summed inside the scatter
 
 // Order-preserving integer key of a float logit (-0.0 first made +0.0); the
 // map is its own inverse.
@@ -250,22 +253,55 @@ __global__ __launch_bounds__(kWave) void k_route_scan(
   if (lane == 0) head_len[s] = carry;
 }
 
+// FUSED: the chunk prefixes and head lengths of sequence b are summed here
+// from the chunk counts (8 lanes per head, used when the sequence has few
+// chunks x heads), instead of being read from k_route_scan's output.
+template <bool FUSED>
 __global__ __launch_bounds__(kScatterThreads) void k_route_scatter(
     const int32_t* __restrict__ topk_idx, int B, int T, int H, int K, int nchunk,
-    const int32_t* __restrict__ within, const int32_t* __restrict__ head_len,
-    int32_t* __restrict__ seg_offsets, int32_t* __restrict__ perm_token,
-    int32_t* __restrict__ slot_pos) {
+    const int32_t* __restrict__ counts, const int32_t* __restrict__ within,
+    int32_t* __restrict__ head_len, int32_t* __restrict__ seg_offsets,
+    int32_t* __restrict__ perm_token, int32_t* __restrict__ slot_pos) {
   __shared__ int s_base[64];
+  __shared__ int s_before[64];
+  __shared__ int s_len[64];
   const int b = blockIdx.x / nchunk;
   const int c = blockIdx.x - b * nchunk;
   const int tid = threadIdx.x;
+  if constexpr (FUSED) {
+    static_assert(kScatterThreads == 8 * 64, "8 lanes per head");
+    const int h = tid / 8, j = tid % 8;
+    int before = 0, total = 0;
+    if (h < H) {
+      const int32_t* cp = counts + (static_cast<size_t>(b) * H + h) * nchunk;
+      for (int cc = j; cc < nchunk; cc += 8) {
+        const int x = cp[cc];
+        total += x;
+        before += cc < c ? x : 0;
+      }
+    }
+#pragma unroll
+    for (int o = 1; o < 8; o <<= 1) {
+      before += __shfl_xor(before, o, 8);
+      total += __shfl_xor(total, o, 8);
+    }
+    if (j == 0) {
+      s_before[h] = before;
+      s_len[h] = total;
+    }
+    __syncthreads();
+  }
   if (tid < kWave) {
     // segment offsets of sequence b and this chunk's start in each segment
-    const int hl = tid < H ? head_len[static_cast<size_t>(b) * H + tid] : 0;
+    const int hl = tid < H ? (FUSED ? s_len[tid] : head_len[static_cast<size_t>(b) * H + tid]) : 0;
     const int seg_off = b * T * K + wave_inclusive_scan(hl) - hl;
     if (tid < H) {
-      if (c == 0) seg_offsets[static_cast<size_t>(b) * H + tid] = seg_off;
-      s_base[tid] = seg_off + within[(static_cast<size_t>(b) * H + tid) * nchunk + c];
+      if (c == 0) {
+        seg_offsets[static_cast<size_t>(b) * H + tid] = seg_off;
+        if (FUSED) head_len[static_cast<size_t>(b) * H + tid] = hl;
+      }
+      s_base[tid] = seg_off + (FUSED ? s_before[tid]
+                                     : within[(static_cast<size_t>(b) * H + tid) * nchunk + c]);
     }
     if (c == 0 && b == B - 1 && tid == 0) seg_offsets[static_cast<size_t>(B) * H] = B * T * K;
   }
@@ -313,10 +349,17 @@ hipError_t launch_route(const float* logits, int B, int T, int H, int K,
 #undef NAMOH_RC
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  k_route_scan<<<B * H, kWave, 0, st>>>(counts, nchunk, within, head_len);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  k_route_scatter<<<grid, kScatterThreads, 0, st>>>(topk_idx, B, T, H, K, nchunk, within,
-                                                    head_len, seg_offsets, perm_token, slot_pos);
+  if (static_cast<long>(nchunk) * H <= kFusedScan) {
+    k_route_scatter<true><<<grid, kScatterThreads, 0, st>>>(
+        topk_idx, B, T, H, K, nchunk, counts, within, head_len, seg_offsets, perm_token,
+        slot_pos);
+  } else {
+    k_route_scan<<<B * H, kWave, 0, st>>>(counts, nchunk, within, head_len);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    k_route_scatter<false><<<grid, kScatterThreads, 0, st>>>(
+        topk_idx, B, T, H, K, nchunk, counts, within, head_len, seg_offsets, perm_token,
+        slot_pos);
+  }
   return hipGetLastError();
 }
 
