@@ -54,7 +54,7 @@ constexpr int kBN = 64;            // keys per tile
 #define NAMOH_D128_NQT 1
 #endif
 #ifndef NAMOH_D64_MINB
-#define NAMOH_D64_MINB 3
+#define NAMOH_D64_MINB 4
 #endif
 #ifndef NAMOH_D128_MINB
 #define NAMOH_D128_MINB 2
@@ -62,7 +62,7 @@ constexpr int kBN = 64;            // keys per tile
 // NW waves per workgroup, NQT 32-query sub-tiles per wave, MINB workgroups
 // per compute unit the register allocation must allow.
 #ifndef NAMOH_D64_VPRE
-#define NAMOH_D64_VPRE 4
+#define NAMOH_D64_VPRE 0
 #endif
 #ifndef NAMOH_D128_VPRE
 #define NAMOH_D128_VPRE 2
@@ -531,6 +531,10 @@ NAMOH_DEV void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
 }
 
+// 1: all key-operand LDS reads of a tile are issued before its first MFMA.
+#ifndef NAMOH_QK_PREREAD
+#define NAMOH_QK_PREREAD 0
+#endif
 // Wave priority around the matrix-core blocks (s_setprio; 0 = unchanged).
 #ifndef NAMOH_PRIO_QK
 #define NAMOH_PRIO_QK 0
@@ -570,7 +574,9 @@ NAMOH_DEV void qk_tile(f32x16 (&S)[2][NQT], const uint16_t* __restrict__ sKb,
       const int row = 32 * kk + c;
       a[ks][kk] = *reinterpret_cast<const bf16x8*>(&sKb[row * D + swz<D / 8>(row, 2 * ks + g) * 8]);
     }
+#if NAMOH_QK_PREREAD
   __builtin_amdgcn_sched_barrier(0);
+#endif
   wave_prio<NAMOH_PRIO_QK>();
   // the accumulators start at -m (the query's running maximum), so the
   // scores leave the products already shifted
