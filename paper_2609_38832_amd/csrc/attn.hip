@@ -491,7 +491,6 @@ NAMOH_DEV int swz(int row, int gr) {
 // LDS base goes through M0 from scalar registers.  Completion is tracked by
 // vmcnt: wait_vmcnt<N>() before the barrier that publishes a tile leaves only
 // the N most recent loads of the wave in flight.
-typedef __attribute__((address_space(3))) void lds_void_t;
 
 // Byte offset (inside one tile) of the first granule this lane fetches.  The
 // lane's i-th granule lies i * NT granules further: NT / GPR rows is a
@@ -504,22 +503,52 @@ NAMOH_DEV uint32_t tile_voffset(int tid) {
   return static_cast<uint32_t>((row * GPR + swz<GPR>(row, phys)) * 16);
 }
 
-// One tile.  base/nbytes: the buffer (the item's key or value tiles; loads
-// past nbytes return 0); tile_bytes: byte offset of the tile in it (wave
-// uniform); lds_wave: the stage's LDS tile plus this wave's first granule.
+// Raw buffer resource (stride 0, num_records = nbytes) in scalar registers;
+// the item's values are wave uniform, readfirstlane says so.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+NAMOH_DEV i32x4 buffer_rsrc(const uint16_t* base, uint32_t nbytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  i32x4 r;
+  r.x = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<uint32_t>(a)));
+  r.y = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<uint32_t>(a >> 32) & 0xFFFF));
+  r.z = __builtin_amdgcn_readfirstlane(static_cast<int>(nbytes));
+  r.w = 0x00020000;
+  return r;
+}
+
+// LDS byte address of a __shared__ object (the address-space cast of a
+// shared variable needs no null check).
+template <typename T>
+NAMOH_DEV uint32_t lds_address(T* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) T*)p));
+}
+
+// The loads are written as inline assembly (M0, the LDS base, is an input
+// operand the compiler sets): the compiler's wait-count pass cannot tell the
+// ring's LDS stages apart and, for its own builtin form of these loads,
+// waits for every tile load in flight before any LDS read, which would
+// serialise the ring.  Here the explicit vmcnt waits are the only ones, and
+// the memory clobber keeps the compiler from moving LDS accesses across.
+NAMOH_DEV void lds_dma16(i32x4 rsrc, uint32_t lds, uint32_t voff, int soff) {
+  asm volatile("buffer_load_dwordx4 %1, %2, %3 offen lds" ::"{m0}"(lds), "v"(voff), "s"(rsrc),
+               "s"(soff)
+               : "memory");
+}
+
+// One tile.  base/nbytes: the buffer (the item's key or value tiles);
+// tile_bytes: byte offset of the tile in it (wave uniform, in range);
+// lds_wave: LDS address of the stage's tile plus this wave's first granule
+// (wave uniform).
 template <int KPT, int NT>
 NAMOH_DEV void tile_dma(const uint16_t* base, uint32_t nbytes, uint32_t tile_bytes,
-                        char* lds_wave, uint32_t voff) {
-  // raw buffer resource: stride 0, num_records in bytes
-  const auto rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0,
-                                                      static_cast<int>(nbytes), 0x00020000);
+                        uint32_t lds_wave, uint32_t voff) {
+  const i32x4 rsrc = buffer_rsrc(base, nbytes);
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
     // wave-uniform scalar offset (readfirstlane keeps it out of vector
     // registers, which would force a loop over distinct values)
     const int tb = __builtin_amdgcn_readfirstlane(static_cast<int>(tile_bytes) + i * NT * 16);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)(lds_wave + i * NT * 16), 16,
-                                             static_cast<int>(voff), tb, 0, 0);
+    lds_dma16(rsrc, __builtin_amdgcn_readfirstlane(lds_wave + i * NT * 16), voff, tb);
   }
 }
 
@@ -750,18 +779,23 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   const int tid = threadIdx.x;
   const int wave = tid / 64, lane = tid % 64;
   const int c = lane & 31, g = lane >> 5;
+  // key tiles this wave's queries see: up to its last valid row; none when
+  // all its rows are padding past the segment's end
   const int wq_last = q0 + 32 * ((NQT - 1) * NW + wave) + 31;
-  const int wave_tiles = min(ntiles, wq_last / kBN + 1);
+  const int wave_tiles = q0 + 32 * wave < n ? min(wq_last, n - 1) / kBN + 1 : 0;
   const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
 
-  // token of each query row (issued before the tile loads, so waiting for it
-  // does not wait for them)
+  // token of each query row.  The tile loads below are invisible to the
+  // compiler's wait counting, and vmcnt retires in issue order, so a wait
+  // the compiler places for an older load would also wait for them: the
+  // tokens are waited for before the first tile load is issued.
   int qtok[NQT];
 #pragma unroll
   for (int qt = 0; qt < NQT; ++qt) {
     const int r = q0 + 32 * (qt * NW + wave) + c;
     qtok[qt] = perm_token[seg0 + (r < n ? r : n - 1)];
   }
+  wait_vmcnt<0>();
 
   // ---- first NS - 1 key/value tiles: in flight during the query gather ---
   // (always NS - 1 loads, repeating the last tile when the item has fewer,
@@ -780,8 +814,8 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   const uint32_t voffK = tile_voffset<D / 8, NT>(tid);
   const uint32_t voffV = tile_voffset<kBN / 8, NT>(tid);
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  char* const lK = reinterpret_cast<char*>(&sK[0][0]) + wave_s * kWave * 16;
-  char* const lV = reinterpret_cast<char*>(&sV[0][0]) + wave_s * kWave * 16;
+  const uint32_t lK = lds_address(&sK[0][0]) + wave_s * kWave * 16;
+  const uint32_t lV = lds_address(&sV[0][0]) + wave_s * kWave * 16;
 #pragma unroll
   for (int i = 0; i < NS - 1; ++i) {
     const uint32_t tb = static_cast<uint32_t>(min(i, kt_end_s - 1)) * TB;
@@ -827,6 +861,10 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
       }
     }
   }
+  // query rows and first tiles in: no load the compiler tracks is left for
+  // it to wait for inside the loop (where its wait would also cover the
+  // tile loads issued since)
+  wait_vmcnt<0>();
 
   f32x16 O[MT][NQT];
 #pragma unroll
@@ -873,26 +911,65 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   }
 
   // ---- epilogue: normalise and store the packed head outputs -----------
+  if constexpr (HB) {
+    // bf16 rows go out through LDS: the accumulator layout gives each lane 8
+    // bytes of 32 different rows per store, the staged layout 16 bytes of
+    // whole 128-byte lines.  The stage the loop's last barrier left unused
+    // (no tile in it is read again, no DMA targets it) holds one 32-row
+    // block per wave, 64 D bytes each; 16-byte granule G of row c is kept at
+    // granule G ^ (c mod D/8), so the writes of a wave spread over the banks
+    // and each row is still one run of D/8 granules.
+    static_assert(NQT * NW <= 4, "epilogue staging: one 32-row block per wave in one stage");
+    constexpr int NG = D / 8;          // 16-byte granules per output row
+    constexpr int RPI = kWave / NG;    // rows per coalesced store
+    const int fs = kt_end_s % NS;
+    uint16_t* const ho = static_cast<uint16_t*>(hout);
 #pragma unroll
-  for (int qt = 0; qt < NQT; ++qt) {
-    const float lt = pair_sum32(l_run[qt]);
-    const float inv = 1.f / lt;
-    const int r = q0 + 32 * (qt * NW + wave) + c;
-    if (r < n) {
-      const size_t orow = static_cast<size_t>(seg0 + r) * D;
+    for (int qt = 0; qt < NQT; ++qt) {
+      const int blk = qt * NW + wave_s;
+      char* const stage =
+          reinterpret_cast<char*>(blk < 2 ? &sK[fs][0] : &sV[fs][0]) + (blk & 1) * 64 * D;
+      const float inv = 1.f / pair_sum32(l_run[qt]);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int d0 = 32 * mt + 8 * j + 4 * g;
-          const float4 o4 = make_float4(O[mt][qt][4 * j] * inv, O[mt][qt][4 * j + 1] * inv,
-                                        O[mt][qt][4 * j + 2] * inv, O[mt][qt][4 * j + 3] * inv);
-          if constexpr (HB)
-            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(hout) + orow + d0) =
-                make_uint2(pack_bf16x2(o4.x, o4.y), pack_bf16x2(o4.z, o4.w));
-          else
-            *reinterpret_cast<float4*>(static_cast<float*>(hout) + orow + d0) = o4;
+          const int phys = (4 * mt + j) ^ (c % NG);
+          *reinterpret_cast<uint2*>(stage + c * 2 * D + phys * 16 + 8 * g) =
+              make_uint2(pack_bf16x2(O[mt][qt][4 * j] * inv, O[mt][qt][4 * j + 1] * inv),
+                         pack_bf16x2(O[mt][qt][4 * j + 2] * inv, O[mt][qt][4 * j + 3] * inv));
         }
+      // the wave reads back what its own lanes wrote: LDS work of one wave
+      // completes in order, the fence keeps the compiler from moving the
+      // reads above the writes
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+      const int row0 = q0 + 32 * blk;
+      const int gl = lane % NG;
+#pragma unroll
+      for (int i = 0; i < 32 / RPI; ++i) {
+        const int rr = i * RPI + lane / NG;
+        const uint4 v = *reinterpret_cast<const uint4*>(stage + rr * 2 * D + (gl ^ (rr % NG)) * 16);
+        if (row0 + rr < n)
+          *reinterpret_cast<uint4*>(ho + static_cast<size_t>(seg0 + row0 + rr) * D + gl * 8) = v;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+      const float inv = 1.f / pair_sum32(l_run[qt]);
+      const int r = q0 + 32 * (qt * NW + wave) + c;
+      if (r < n) {
+        const size_t orow = static_cast<size_t>(seg0 + r) * D;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            *reinterpret_cast<float4*>(static_cast<float*>(hout) + orow + 32 * mt + 8 * j + 4 * g) =
+                make_float4(O[mt][qt][4 * j] * inv, O[mt][qt][4 * j + 1] * inv,
+                            O[mt][qt][4 * j + 2] * inv, O[mt][qt][4 * j + 3] * inv);
+      }
     }
   }
 }
