@@ -156,7 +156,7 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
                              int Nr, int max_items, WorkItem* __restrict__ items,
                              int32_t* __restrict__ meta, SchedLds& L) {
   static_assert(NT % kWave == 0 && NT / kWave <= 16 && kSortBins % NT == 0, "block size");
-  const int tid = threadIdx.x;
+  const int tid = thread_x();
   const int lane = tid % kWave, wave = tid / kWave;
   const int per_qb = BM / kBN;           // key tiles added per query block
   const bool in_lds = BH <= kSegLds;
@@ -260,8 +260,15 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
 NAMOH_DEV bool my_item(const WorkItem* __restrict__ items, const int32_t* __restrict__ meta,
                        WorkItem& it) {
   const int cnt = meta[kMetaItems];
-  it = items[blockIdx.x];
-  return static_cast<int>(blockIdx.x) < cnt;
+  const WorkItem v = items[block_x()];
+  // the record is the same for the whole workgroup: keep it in scalar registers
+  it.s = __builtin_amdgcn_readfirstlane(v.s);
+  it.qb = __builtin_amdgcn_readfirstlane(v.qb);
+  it.seg0 = __builtin_amdgcn_readfirstlane(v.seg0);
+  it.n = __builtin_amdgcn_readfirstlane(v.n);
+  it.tile0 = __builtin_amdgcn_readfirstlane(v.tile0);
+  it.pad0 = it.pad1 = it.pad2 = 0;
+  return block_x() < __builtin_amdgcn_readfirstlane(cnt);
 }
 
 // ---------------------------------------------------------------------------
@@ -269,14 +276,14 @@ NAMOH_DEV bool my_item(const WorkItem* __restrict__ items, const int32_t* __rest
 // the angles formed and reduced in double.  P (longest segment for
 // head-relative positions, T for global ones) is recomputed by every
 // workgroup from seg_offsets.
-constexpr int kTableThreads = 256;
+constexpr int kTableThreads = 256, kTableBlocks = 64;
 __global__ __launch_bounds__(kTableThreads) void k_rope_table(
     const int32_t* __restrict__ seg_offsets, int BH, int T, int rope_mode, int d,
     double log_base, float2* __restrict__ table) {
   __shared__ int s_p[kTableThreads / kWave];
   __shared__ double s_theta[64];
   const int half = d / 2;
-  const int tid = threadIdx.x;
+  const int tid = thread_x();
   if (tid < half) s_theta[tid] = exp(-(2.0 * tid / d) * log_base);
   int P = T;
   if (rope_mode == 0) {
@@ -294,8 +301,8 @@ __global__ __launch_bounds__(kTableThreads) void k_rope_table(
     for (int w = 0; w < kTableThreads / kWave; ++w) P = max(P, s_p[w]);
   }
   const size_t total = static_cast<size_t>(P) * half;
-  const size_t stride = static_cast<size_t>(gridDim.x) * kTableThreads;
-  for (size_t i = static_cast<size_t>(blockIdx.x) * kTableThreads + tid; i < total; i += stride) {
+  const size_t stride = static_cast<size_t>(kTableBlocks) * kTableThreads;
+  for (size_t i = static_cast<size_t>(block_x()) * kTableThreads + tid; i < total; i += stride) {
     const int p = static_cast<int>(i / half);
     const int j = static_cast<int>(i - static_cast<size_t>(p) * half);
     table[i] = rope_cos_sin(static_cast<double>(p) * s_theta[j]);
@@ -384,12 +391,12 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
     SchedLds sched;
     PackLds<D> pack;
   } L;
-  if (blockIdx.x == 0) {
+  if (block_x() == 0) {
     attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, items, meta, L.sched);
     return;
   }
-  const int gt = blockIdx.x - 1;
-  const int tid = threadIdx.x;
+  const int gt = block_x() - 1;
+  const int tid = thread_x();
   // segment of tile gt: the last s with seg_tile0(off[s], s) <= gt
   const bool in_lds = BH <= kSegLds;
   if (in_lds) {
@@ -776,7 +783,7 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   const int tile0 = it.tile0;
   const int ntiles = (n + kBN - 1) / kBN;
   const int kt_end = min(ntiles, (q0 + BM + kBN - 1) / kBN);
-  const int tid = threadIdx.x;
+  const int tid = thread_x();
   const int wave = tid / 64, lane = tid % 64;
   const int c = lane & 31, g = lane >> 5;
   // key tiles this wave's queries see: up to its last valid row; none when
@@ -1021,7 +1028,7 @@ __global__ __launch_bounds__(64) void k_attn_generic(
   const int seg0 = it.seg0;
   const int n = it.n;
   const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
-  const int lane = threadIdx.x;
+  const int lane = thread_x();
   const int r = q0 + lane;
 
   float qv[D], acc[D], row[D];
@@ -1085,13 +1092,14 @@ __global__ __launch_bounds__(64) void k_attn_generic(
 // One thread per (token, 8 output elements).  The K slots are gathered four
 // at a time (all loads of a batch issued before their products) and summed
 // in k order.
+constexpr int kCombineThreads = 256;
 template <bool IN_BF16, bool OUT_BF16>
-__global__ __launch_bounds__(256) void k_combine(
+__global__ __launch_bounds__(kCombineThreads) void k_combine(
     const void* __restrict__ hout, const float* __restrict__ gates,
     const int32_t* __restrict__ slot_pos, long BT, int K, int D, int Nr,
     void* __restrict__ out) {
   const int C = D / 8;
-  const long idx = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const long idx = static_cast<long>(block_x()) * kCombineThreads + thread_x();
   const long tok = idx / C;
   const int cc = static_cast<int>(idx - tok * C);
   if (tok >= BT) return;
@@ -1243,7 +1251,7 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   const int Nr = B * T * K;
   const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
   if (rope_mode != 2)
-    k_rope_table<<<64, kTableThreads, 0, st>>>(seg_offsets, B * H, T, rope_mode, d, log_base,
+    k_rope_table<<<kTableBlocks, kTableThreads, 0, st>>>(seg_offsets, B * H, T, rope_mode, d, log_base,
                                                w.table);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -1271,16 +1279,16 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const long BT = static_cast<long>(B) * T;
   const long threads = BT * (d / 8);
-  const unsigned grid = static_cast<unsigned>((threads + 255) / 256);
+  const unsigned grid = static_cast<unsigned>((threads + kCombineThreads - 1) / kCombineThreads);
   prof_mark("combine", true, st);
   if (hb && out_dtype == 1)
-    k_combine<true, true><<<grid, 256, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+    k_combine<true, true><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
   else if (hb)
-    k_combine<true, false><<<grid, 256, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+    k_combine<true, false><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
   else if (out_dtype == 1)
-    k_combine<false, true><<<grid, 256, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+    k_combine<false, true><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
   else
-    k_combine<false, false><<<grid, 256, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+    k_combine<false, false><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
   prof_mark("combine", false, st);
   return hipGetLastError();
 }

@@ -39,6 +39,12 @@ NAMOH_DEV uint32_t pack_bf16x2(float lo, float hi) {
 NAMOH_DEV float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
 NAMOH_DEV float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
+// Thread / workgroup index in x, read straight from the hardware registers
+// (the threadIdx / blockIdx accessors can be left as out-of-line library
+// calls, which clobber registers at kernel entry).
+NAMOH_DEV int thread_x() { return static_cast<int>(__builtin_amdgcn_workitem_id_x()); }
+NAMOH_DEV int block_x() { return static_cast<int>(__builtin_amdgcn_workgroup_id_x()); }
+
 // Lanes below the calling lane in a 64-wide wave.
 NAMOH_DEV uint64_t lanemask_lt() {
   const int lane = __lane_id();
@@ -90,7 +96,7 @@ template <int NT>
 NAMOH_DEV int block_exclusive_scan(int x, int* s_wave, int& total) {
   static_assert(NT % kWave == 0 && NT / kWave <= kWave, "block size");
   const int lane = __lane_id();
-  const int wave = threadIdx.x / kWave;
+  const int wave = thread_x() / kWave;
   const int incl = wave_inclusive_scan(x);
   if (lane == kWave - 1) s_wave[wave] = incl;
   __syncthreads();

@@ -167,6 +167,31 @@ def test_prefill_edge_cases(dtype, d):
         check_out(got["out"], ref["out"], dtype)
 
 
+@pytest.mark.parametrize("d,K", [(64, 2), (128, 1)])
+def test_prefill_long_segment(d, K):
+    # Every token on the same K heads: one 4500-row segment per head (ragged
+    # last tile, query blocks of up to 71 key tiles) and empty segments for
+    # the others; both head-output paths (fp32 rows handed in, bf16 internal
+    # rows), and two runs that agree bit for bit.
+    w = W.WORKLOADS[2 if d == 64 else 4].with_(B=1, T=4500, H=4, K=K, d=d, qkv_scale=d ** -0.5,
+                                               zipf_bias=0.0)
+    say(f"prefill long segment d={d} K={K}")
+    inp = W.prefill_inputs(w)
+    inp["logits"] = inp["logits"].copy()
+    inp["logits"][:, :, :K] += 100.0
+    f = _f64(inp, w)
+    ref = O.prefill(inp["logits"], f["q"], f["k"], f["v"], w.K, w.rope_base)
+    got = run_prefill(w, inp, head_out=True)
+    assert_routing_exact(got, ref)
+    e1 = check_out(got["out"], ref["out"], w.dtype)
+    e2 = check_out(got["head_out"], ref["head_out"], w.dtype, "head_out")
+    got2 = run_prefill(w, inp)
+    e3 = check_out(got2["out"], ref["out"], w.dtype)
+    got3 = run_prefill(w, inp)
+    np.testing.assert_array_equal(got2["out"], got3["out"])
+    say(f"  max err out {e1:.2e} head_out {e2:.2e} out(bf16 rows) {e3:.2e}")
+
+
 def test_prefill_deterministic():
     w = W.WORKLOADS[4].with_(B=1, T=2048)
     say("prefill determinism")
