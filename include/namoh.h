@@ -128,6 +128,30 @@ namoh_status namoh_attn_fwd(const void* q, const void* k, const void* v,
                             void* stream);
 
 /* ------------------------------------------------------------------------
+ * Prefill -> decode hand-off (Sec. 3.2, efficient execution: decoding reads
+ * and extends only the active heads' caches; Eq. namoh-head-rope: keys are
+ * cached after rotation, in rank order).  For every (b, h) with n = n_{b,h}
+ * prompt tokens routed to head h, rows [0, n) of the caches receive, in
+ * rank order, the rotated keys (RoPE at the rank, the global position, or
+ * none, as in namoh_attn_fwd) and the values of those tokens, and
+ * cache_len[b,h] = n; rows [n, cap) are not touched.  namoh_decode_step can
+ * then continue the sequences.
+ *
+ * In:  k, v        [B, H, T, d] of `dtype` (the prompt's dense keys/values).
+ *      seg_offsets, perm_token: as produced by namoh_route for the prompt.
+ * Out: k_cache, v_cache [B, H, cap, d] `dtype`; cache_len int32 [B, H].
+ * cap >= T (every head's prompt fits).  No workspace; allocates nothing.
+ * Offsets that are not a packing of [0, B*T*K) leave the rows they do not
+ * describe unwritten.
+ * ---------------------------------------------------------------------- */
+namoh_status namoh_prefill_cache(const void* k, const void* v, int dtype, int B, int T,
+                                 int H, int K, int d_head, float rope_base,
+                                 int rope_mode, const int32_t* seg_offsets,
+                                 const int32_t* perm_token, void* k_cache,
+                                 void* v_cache, int32_t* cache_len, int cap,
+                                 void* stream);
+
+/* ------------------------------------------------------------------------
  * One decoding step for B sequences (Sec. 3.1: prefill and incremental
  * decoding compute the same thing; Sec. 3.2: decoding launches only the
  * active heads and reads/updates only their caches; Eq. namoh-kv-cost).

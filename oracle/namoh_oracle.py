@@ -50,7 +50,7 @@ __all__ = [
     "select_heads", "route_gates", "membership", "head_ranks", "permutation",
     "rope_rotate", "visibility_mask", "attention_definition",
     "attention_gathered", "combine_packed", "combine_dense", "prefill",
-    "prefill_rows", "decode_step", "brute_force_layer", "interaction_count",
+    "prefill_rows", "prefill_cache", "decode_step", "brute_force_layer", "interaction_count",
     "shared_head_counts",
 ]
 
@@ -333,6 +333,35 @@ def prefill_rows(q, k, v, topk_idx, gates, H, rope_base, b, tokens,
             hs[r, kk] = p @ np.asarray(v[b, h][src], dtype=np.float64)
             o[r] += gates[b, t, kk] * hs[r, kk]
     return o, hs
+
+
+# ----------------------------------------------------------------------------
+# Prefill -> decode hand-off: Sec. 3.2 (decoding reads and extends only the
+# active heads' caches), reading R6 (caches hold rotated keys in rank order)
+
+def prefill_cache(k, v, topk_idx, H, rope_base, rope_mode=ROPE_HEAD_RELATIVE):
+    """Decode caches after a prompt: for each (b, h), the keys of the tokens
+    routed to h rotated at their rank (or global position), and their
+    values, in rank order.
+
+    k, v [B,H,T,d] (any float dtype); returns k_cache, v_cache float64
+    [B,H,T,d] (rows [n_{b,h}, T) zero) and cache_len int [B,H]."""
+    B, _, T, d = k.shape
+    m = membership(topk_idx, H)
+    kc = np.zeros((B, H, T, d))
+    vc = np.zeros((B, H, T, d))
+    n = np.zeros((B, H), dtype=np.int64)
+    for b in range(B):
+        for h in range(H):
+            src = np.nonzero(m[b, :, h])[0]         # I_h in token order = rank order
+            n[b, h] = src.size
+            if src.size == 0:
+                continue
+            pos = _positions(np.arange(src.size), src, rope_mode)
+            kc[b, h, :src.size] = _rotate(np.asarray(k[b, h][src], dtype=np.float64), pos,
+                                          rope_base)
+            vc[b, h, :src.size] = np.asarray(v[b, h][src], dtype=np.float64)
+    return kc, vc, n
 
 
 # ----------------------------------------------------------------------------

@@ -30,6 +30,7 @@ ROPE_HEAD_RELATIVE, ROPE_GLOBAL, ROPE_NONE = 0, 1, 2
 EXPORTED = (
     "namoh_route_workspace_size", "namoh_route",
     "namoh_attn_fwd_workspace_size", "namoh_attn_fwd",
+    "namoh_prefill_cache",
     "namoh_decode_workspace_size", "namoh_decode_step",
     "namoh_status_string", "namoh_last_error", "namoh_version",
     "namoh_profile_enable", "namoh_profile_read",
@@ -46,6 +47,8 @@ _SIGS = {
     "namoh_attn_fwd_workspace_size": (_S, [_I, _I, _I, _I, _I, _I]),
     "namoh_attn_fwd": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F,
                             _P, _P, _P, _P, _P, _I, _P, _P, _S, _P]),
+    "namoh_prefill_cache": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _P, _P, _P, _P, _P,
+                                 _I, _P]),
     "namoh_decode_workspace_size": (_S, [_I, _I, _I, _I, _I]),
     "namoh_decode_step": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I,
                                _F, _I, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
@@ -191,6 +194,26 @@ def attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K
                                _ptr(out), dtype_code(out.dtype), _ptr(head_out),
                                _ptr(ws), ws.numel(), _stream(q.device)))
     return out
+
+
+def prefill_cache(k: torch.Tensor, v: torch.Tensor, r: dict, K: int, rope_base: float,
+                  k_cache: torch.Tensor, v_cache: torch.Tensor, cache_len: torch.Tensor,
+                  rope_mode: int = ROPE_HEAD_RELATIVE) -> None:
+    """namoh_prefill_cache: the prompt's rotated keys / values, per head in rank
+    order, into caches [B, H, cap, d]; cache_len [B, H] = the head lengths."""
+    _need_cuda(k, v, k_cache, v_cache, cache_len)
+    B, H, T, d = k.shape
+    cap = k_cache.shape[2]
+    if tuple(k_cache.shape) != (B, H, cap, d) or tuple(v_cache.shape) != (B, H, cap, d):
+        raise ValueError("caches must be [B, H, cap, d]")
+    if k_cache.dtype != k.dtype or v_cache.dtype != k.dtype or v.dtype != k.dtype:
+        raise ValueError("k, v and the caches must share one dtype")
+    if tuple(cache_len.shape) != (B, H) or cache_len.dtype != torch.int32:
+        raise ValueError("cache_len must be int32 [B, H]")
+    check(lib().namoh_prefill_cache(_ptr(k), _ptr(v), dtype_code(k.dtype), B, T, H, K, d,
+                                    float(rope_base), rope_mode, _ptr(r["seg_offsets"]),
+                                    _ptr(r["perm_token"]), _ptr(k_cache), _ptr(v_cache),
+                                    _ptr(cache_len), cap, _stream(k.device)))
 
 
 def decode_workspace_size(B, H, K, d, cap) -> int:

@@ -183,6 +183,36 @@ namoh_status namoh_attn_fwd(const void* q, const void* k, const void* v, int dty
                                        static_cast<hipStream_t>(stream)));
 }
 
+namoh_status namoh_prefill_cache(const void* k, const void* v, int dtype, int B, int T, int H,
+                                 int K, int d_head, float rope_base, int rope_mode,
+                                 const int32_t* seg_offsets, const int32_t* perm_token,
+                                 void* k_cache, void* v_cache, int32_t* cache_len, int cap,
+                                 void* stream) {
+  namoh_status s;
+  if ((s = check_sizes(B, T, H, K)) != NAMOH_OK) return s;
+  if ((s = check_head_width(d_head)) != NAMOH_OK) return s;
+  REQUIRE(dtype == NAMOH_F32 || dtype == NAMOH_BF16, "unknown dtype %d", dtype);
+  REQUIRE(rope_mode == NAMOH_ROPE_HEAD_RELATIVE || rope_mode == NAMOH_ROPE_GLOBAL ||
+              rope_mode == NAMOH_ROPE_NONE,
+          "unknown rope_mode %d", rope_mode);
+  REQUIRE(rope_mode == NAMOH_ROPE_NONE || (std::isfinite(rope_base) && rope_base > 0.f),
+          "rope_base must be finite and > 0 (got %g)", static_cast<double>(rope_base));
+  REQUIRE(cap >= T, "cap (%d) must hold a whole prompt (T = %d)", cap, T);
+  REQUIRE(static_cast<long long>(B) * H * cap * d_head < (1ll << 40), "caches too large");
+  REQUIRE_PTR(k, 16);
+  REQUIRE_PTR(v, 16);
+  REQUIRE_PTR(seg_offsets, 4);
+  REQUIRE_PTR(perm_token, 4);
+  REQUIRE_PTR(k_cache, 16);
+  REQUIRE_PTR(v_cache, 16);
+  REQUIRE_PTR(cache_len, 4);
+  clear_hip_error();
+  return hip_status(namoh::launch_prefill_cache(k, v, dtype, B, T, H, K, d_head, rope_base,
+                                                rope_mode, seg_offsets, perm_token, k_cache,
+                                                v_cache, cache_len, cap,
+                                                static_cast<hipStream_t>(stream)));
+}
+
 size_t namoh_decode_workspace_size(int B, int H, int K, int d_head, int cap) {
   if (check_sizes(B, 1, H, K) != NAMOH_OK || check_head_width(d_head) != NAMOH_OK || cap < 1)
     return 0;

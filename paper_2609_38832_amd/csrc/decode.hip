@@ -21,6 +21,11 @@
 //                          one (max, sum, acc[d]) partial per chunk.
 //   k_decode_combine       merges the chunk partials of each head by
 //                          log-sum-exp and sums the gated head outputs.
+//   k_prefill_cache        the prefill -> decode hand-off: every packed
+//                          prompt row (segment b*H + h, rank r, token t)
+//                          writes its rotated key and its value to row r of
+//                          head h's caches; cache_len = the segment lengths.
+#include <algorithm>
 #include <cmath>
 
 #include "common.h"
@@ -55,9 +60,9 @@ __global__ __launch_bounds__(64 * kAppendWaves) void k_decode_route_append(
     float qscale, int32_t* __restrict__ topk_idx, float* __restrict__ gates,
     int32_t* __restrict__ dev_status, float* __restrict__ qrot,
     int32_t* __restrict__ rows) {
-  const int b = blockIdx.x;
-  const int lane = threadIdx.x % 64;
-  const int wave = threadIdx.x / 64;
+  const int b = block_x();
+  const int lane = thread_x() % 64;
+  const int wave = thread_x() / 64;
   const bool real = lane < H;
   const float l = real ? logits[static_cast<size_t>(b) * H + lane] : 0.f;
   int rank = 0;
@@ -139,8 +144,8 @@ __global__ __launch_bounds__(256) void k_decode_attn(
   __shared__ float s_ml[RPB][2];
   __shared__ float s_acc[RPB][D];
 
-  const int bk = blockIdx.x / nchunk;
-  const int chunk = blockIdx.x - bk * nchunk;
+  const int bk = block_x() / nchunk;
+  const int chunk = block_x() - bk * nchunk;
   const int L = rows[bk];
   const int r0 = chunk * kDecChunk;
   if (r0 >= L) return;
@@ -148,7 +153,7 @@ __global__ __launch_bounds__(256) void k_decode_attn(
   const int b = bk / K;
   const int h = topk_idx[bk];
   const size_t rowbase = (static_cast<size_t>(b) * H + h) * cap;
-  const int tid = threadIdx.x;
+  const int tid = thread_x();
   const int lane = tid % 64, wave = tid / 64;
   const int sub = lane % G;
   const int grp = wave * RPW + lane / G;
@@ -264,8 +269,8 @@ __global__ __launch_bounds__(256) void k_decode_combine(
   constexpr int NWV = 4;
   constexpr int DPL = (D + 63) / 64;  // output columns per lane
   __shared__ float s_o[NWV][D];
-  const int b = blockIdx.x;
-  const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
+  const int b = block_x();
+  const int lane = thread_x() % 64, wave = thread_x() / 64;
   float o[DPL];
 #pragma unroll
   for (int i = 0; i < DPL; ++i) o[i] = 0.f;
@@ -306,12 +311,12 @@ __global__ __launch_bounds__(256) void k_decode_combine(
     if (d < D) s_o[wave][d] = o[i];
   }
   __syncthreads();
-  if (threadIdx.x < D) {
+  if (thread_x() < D) {
     float r = 0.f;
 #pragma unroll
-    for (int w = 0; w < NWV; ++w) r += s_o[w][threadIdx.x];
-    if constexpr (OUT_BF16) static_cast<uint16_t*>(out)[static_cast<size_t>(b) * D + threadIdx.x] = f32_to_bf16(r);
-    else static_cast<float*>(out)[static_cast<size_t>(b) * D + threadIdx.x] = r;
+    for (int w = 0; w < NWV; ++w) r += s_o[w][thread_x()];
+    if constexpr (OUT_BF16) static_cast<uint16_t*>(out)[static_cast<size_t>(b) * D + thread_x()] = f32_to_bf16(r);
+    else static_cast<float*>(out)[static_cast<size_t>(b) * D + thread_x()] = r;
   }
 }
 
@@ -340,6 +345,155 @@ static DecWs carve_dec(void* ws, int B, int K, int d, int cap) {
 
 size_t decode_workspace_bytes(int B, int /*H*/, int K, int d, int cap) {
   return carve_dec(nullptr, B, K, d, cap).bytes;
+}
+
+// ---------------------------------------------------------------------------
+// Prefill -> decode hand-off (Sec. 3.2, efficient execution: a decoding step
+// reads and extends only its active heads' caches, so those must hold the
+// prompt's rotated keys and values of each head in rank order, Eq.
+// namoh-head-rope).  A workgroup takes 4096 / D consecutive packed rows: the
+// segment of each row by binary search over seg_offsets (staged in LDS), then one 8-pair
+// group (elements j..j+7 and j+d/2..j+d/2+7) per thread, 16-byte loads and
+// stores, angles formed and reduced in double as in the decode append.  Rows
+// whose offsets are not a packing of [0, Nr) with ranks below cap and tokens
+// below T are skipped.
+constexpr int kCacheThreads = 256;
+constexpr int kCacheSegLds = 2048;   // segment offsets staged in LDS up to this many segments
+template <int D>
+constexpr int cache_rows() { return kCacheThreads * 16 / D; }
+
+template <bool BF16>
+NAMOH_DEV void ld8(const void* p, size_t i, float* x) {
+  if constexpr (BF16) {
+    const uint4 u = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + i);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = lo_bf16(w[e]);
+      x[2 * e + 1] = hi_bf16(w[e]);
+    }
+  } else {
+    const float4 a = *reinterpret_cast<const float4*>(static_cast<const float*>(p) + i);
+    const float4 c = *reinterpret_cast<const float4*>(static_cast<const float*>(p) + i + 4);
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+    x[4] = c.x; x[5] = c.y; x[6] = c.z; x[7] = c.w;
+  }
+}
+
+template <bool BF16>
+NAMOH_DEV void st8(void* p, size_t i, const float* x) {
+  if constexpr (BF16) {
+    *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p) + i) =
+        make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
+                   pack_bf16x2(x[6], x[7]));
+  } else {
+    *reinterpret_cast<float4*>(static_cast<float*>(p) + i) = make_float4(x[0], x[1], x[2], x[3]);
+    *reinterpret_cast<float4*>(static_cast<float*>(p) + i + 4) = make_float4(x[4], x[5], x[6], x[7]);
+  }
+}
+
+template <int D, bool BF16>
+__global__ __launch_bounds__(kCacheThreads) void k_prefill_cache(
+    const void* __restrict__ k, const void* __restrict__ v,
+    const int32_t* __restrict__ seg_offsets, const int32_t* __restrict__ perm_token, int BH,
+    int H, int T, int Nr, long cap, double log_base, int rope_mode, int nblocks,
+    void* __restrict__ k_cache, void* __restrict__ v_cache, int32_t* __restrict__ cache_len) {
+  constexpr int RW = cache_rows<D>();
+  constexpr int G = D / 16;   // 8-pair groups per row
+  static_assert(RW * G == kCacheThreads, "one group per thread");
+  __shared__ double s_theta[D / 2];
+  __shared__ int s_seg[RW], s_rank[RW], s_tok[RW];
+  __shared__ int s_off[kCacheSegLds + 1];
+  const int tid = thread_x();
+  const int row0 = block_x() * RW;
+  for (int s = block_x() * kCacheThreads + tid; s < BH; s += nblocks * kCacheThreads)
+    cache_len[s] = seg_offsets[s + 1] - seg_offsets[s];
+  if (tid < D / 2) s_theta[tid] = exp(-(2.0 * tid / D) * log_base);
+  const bool in_lds = BH <= kCacheSegLds;
+  if (in_lds)
+    for (int i = tid; i <= BH; i += kCacheThreads) s_off[i] = seg_offsets[i];
+  __syncthreads();
+  const int32_t* off = in_lds ? s_off : seg_offsets;
+  if (tid < RW) {
+    const int pr = row0 + tid;
+    int seg = -1, rank = -1, tok = -1;
+    if (pr < Nr) {
+      tok = perm_token[pr];
+      int lo = 0, hi = BH;   // the last segment starting at or before pr
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (off[mid] <= pr) lo = mid; else hi = mid;
+      }
+      seg = lo;
+      rank = pr - off[lo];
+      if (rank < 0 || rank >= cap || pr >= off[lo + 1] || tok < 0 || tok >= T) seg = -1;
+    }
+    s_seg[tid] = seg;
+    s_rank[tid] = rank;
+    s_tok[tid] = tok;
+  }
+  __syncthreads();
+  const int row = tid / G, j0 = (tid - row * G) * 8;
+  const int seg = s_seg[row];
+  if (seg < 0) return;
+  const int r = s_rank[row], t = s_tok[row];
+  const size_t src = (static_cast<size_t>(seg) * T + t) * D;
+  const size_t dst = (static_cast<size_t>(seg) * cap + r) * D;
+  float k1[8], k2[8], v1[8], v2[8];
+  ld8<BF16>(k, src + j0, k1);
+  ld8<BF16>(k, src + j0 + D / 2, k2);
+  ld8<BF16>(v, src + j0, v1);
+  ld8<BF16>(v, src + j0 + D / 2, v2);
+  if (rope_mode != 2) {
+    const double pos = rope_mode == 0 ? r : t;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float2 w = rope_cos_sin(pos * s_theta[j0 + e]);
+      const float a = k1[e], c = k2[e];
+      k1[e] = a * w.x - c * w.y;
+      k2[e] = c * w.x + a * w.y;
+    }
+  }
+  st8<BF16>(k_cache, dst + j0, k1);
+  st8<BF16>(k_cache, dst + j0 + D / 2, k2);
+  st8<BF16>(v_cache, dst + j0, v1);
+  st8<BF16>(v_cache, dst + j0 + D / 2, v2);
+}
+
+template <int D, bool BF16>
+static hipError_t run_prefill_cache(const void* k, const void* v, int B, int T, int H, int K,
+                                    float rope_base, int rope_mode, const int32_t* seg_offsets,
+                                    const int32_t* perm_token, void* k_cache, void* v_cache,
+                                    int32_t* cache_len, int cap, hipStream_t st) {
+  const int BH = B * H;
+  const long Nr = static_cast<long>(B) * T * K;
+  const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
+  constexpr int RW = cache_rows<D>();
+  const long blocks = std::max((Nr + RW - 1) / RW,
+                               static_cast<long>((BH + kCacheThreads - 1) / kCacheThreads));
+  k_prefill_cache<D, BF16><<<static_cast<unsigned>(blocks), kCacheThreads, 0, st>>>(
+      k, v, seg_offsets, perm_token, BH, H, T, static_cast<int>(Nr), cap, log_base, rope_mode,
+      static_cast<int>(blocks), k_cache, v_cache, cache_len);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_cache(const void* k, const void* v, int dtype, int B, int T, int H,
+                                int K, int d, float rope_base, int rope_mode,
+                                const int32_t* seg_offsets, const int32_t* perm_token,
+                                void* k_cache, void* v_cache, int32_t* cache_len, int cap,
+                                hipStream_t st) {
+#define NAMOH_PC(DD, BF)                                                                       \
+  return run_prefill_cache<DD, BF>(k, v, B, T, H, K, rope_base, rope_mode, seg_offsets,       \
+                                   perm_token, k_cache, v_cache, cache_len, cap, st)
+  if (dtype == 1) {
+    if (d == 32) NAMOH_PC(32, true);
+    if (d == 64) NAMOH_PC(64, true);
+    NAMOH_PC(128, true);
+  }
+  if (d == 32) NAMOH_PC(32, false);
+  if (d == 64) NAMOH_PC(64, false);
+  NAMOH_PC(128, false);
+#undef NAMOH_PC
 }
 
 template <int D, bool BF16>

@@ -55,5 +55,10 @@ hipError_t launch_decode(const float* logits, const void* q, const void* k,
                          int gate_mode, float scale, int32_t* topk_idx,
                          float* gates, void* out, int out_dtype,
                          int32_t* dev_status, void* ws, hipStream_t st);
+hipError_t launch_prefill_cache(const void* k, const void* v, int dtype, int B, int T, int H,
+                                int K, int d, float rope_base, int rope_mode,
+                                const int32_t* seg_offsets, const int32_t* perm_token,
+                                void* k_cache, void* v_cache, int32_t* cache_len, int cap,
+                                hipStream_t st);
 
 }  // namespace namoh

@@ -85,9 +85,9 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
     int32_t* __restrict__ slot_rank, int32_t* __restrict__ chunk_counts) {
   constexpr int HL = HMAX / kLPT;
   __shared__ int s_wcnt[kCountWaves][HMAX];
-  const int b = blockIdx.x / nchunk;
-  const int c = blockIdx.x - b * nchunk;
-  const int tid = threadIdx.x;
+  const int b = block_x() / nchunk;
+  const int c = block_x() - b * nchunk;
+  const int tid = thread_x();
   const int sub = tid % kLPT;
   const int wave = tid / kWave, lane = tid % kWave;
   const int t = c * kRC + tid / kLPT;
@@ -239,8 +239,8 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
 __global__ __launch_bounds__(kWave) void k_route_scan(
     const int32_t* __restrict__ counts, int nchunk, int32_t* __restrict__ within,
     int32_t* __restrict__ head_len) {
-  const int s = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int s = block_x();
+  const int lane = thread_x();
   const size_t base = static_cast<size_t>(s) * nchunk;
   int carry = 0;
   for (int i0 = 0; i0 < nchunk; i0 += kWave) {
@@ -265,9 +265,9 @@ __global__ __launch_bounds__(kScatterThreads) void k_route_scatter(
   __shared__ int s_base[64];
   __shared__ int s_before[64];
   __shared__ int s_len[64];
-  const int b = blockIdx.x / nchunk;
-  const int c = blockIdx.x - b * nchunk;
-  const int tid = threadIdx.x;
+  const int b = block_x() / nchunk;
+  const int c = block_x() - b * nchunk;
+  const int tid = thread_x();
   if constexpr (FUSED) {
     static_assert(kScatterThreads == 8 * 64, "8 lanes per head");
     const int h = tid / 8, j = tid % 8;

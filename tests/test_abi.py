@@ -115,6 +115,23 @@ def test_decode_rejects(lib, kw, code):
     assert _dec(lib, **kw) == code
 
 
+def _pcache(lib, dtype=1, B=2, T=64, H=8, K=2, d=64, base=1e4, rope=0, cap=64, k=fake(0),
+            kc=fake(4), cl=fake(6), so=fake(2)):
+    return lib.namoh_prefill_cache(k, fake(1), dtype, B, T, H, K, d, base, rope, so, fake(3),
+                                   kc, fake(5), cl, cap, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(cap=63), 1), (dict(d=48), 2), (dict(K=9), 1), (dict(dtype=3), 1), (dict(rope=5), 1),
+    (dict(base=-1.0), 1), (dict(k=None), 1), (dict(kc=P(A + 4)), 1), (dict(cl=None), 1),
+    (dict(so=P(A + 2)), 1), (dict(B=0), 1),
+    (dict(B=64, H=64, T=1 << 16, cap=1 << 22, d=128), 1),   # caches past 2^40 elements
+])
+def test_prefill_cache_rejects(lib, kw, code):
+    assert _pcache(lib, **kw) == code
+    assert L.last_error() != ""
+
+
 def test_workspace_queries(lib):
     assert lib.namoh_route_workspace_size(0, 10, 8, 2) == 0
     assert lib.namoh_route_workspace_size(1, 10, 8, 2) > 0

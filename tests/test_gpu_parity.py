@@ -192,6 +192,63 @@ def test_prefill_long_segment(d, K):
     say(f"  max err out {e1:.2e} head_out {e2:.2e} out(bf16 rows) {e3:.2e}")
 
 
+@pytest.mark.parametrize("dtype,d,rope_mode", [("bf16", 64, O.ROPE_HEAD_RELATIVE),
+                                                ("bf16", 128, O.ROPE_GLOBAL),
+                                                ("bf16", 128, O.ROPE_NONE),
+                                                ("f32", 32, O.ROPE_HEAD_RELATIVE)])
+def test_prefill_cache_then_decode(dtype, d, rope_mode):
+    # prompt of T tokens -> route, attention, hand-off to the decode caches;
+    # the caches against the oracle's (keys within the rounding of one
+    # rotation, values and lengths exact), then one GPU decode step for token
+    # T against the oracle's prefill of T + 1 tokens at that token
+    T, cap = 700, 720
+    w = W.WORKLOADS[2].with_(B=2, T=T + 1, H=8, K=2, d=d, dtype=dtype, qkv_scale=d ** -0.5)
+    say(f"prefill -> cache -> decode {dtype} d={d} rope_mode={rope_mode}")
+    inp = W.prefill_inputs(w)
+    wp = w.with_(T=T)
+    pin = {"logits": np.ascontiguousarray(inp["logits"][:, :T])}
+    for x in ("q", "k", "v"):
+        pin[x] = np.ascontiguousarray(inp[x][:, :, :T])
+    lg = torch.from_numpy(pin["logits"]).to(DEV)
+    q, k, v = (to_dev(pin[x], dtype) for x in ("q", "k", "v"))
+    r = L.route(lg, w.K)
+    L.attn_fwd(q, k, v, r, w.K, w.rope_base, rope_mode)
+    tdt = k.dtype
+    kc = torch.zeros(w.B, w.H, cap, d, dtype=tdt, device=DEV)
+    vc = torch.zeros(w.B, w.H, cap, d, dtype=tdt, device=DEV)
+    cl = torch.full((w.B, w.H), -7, dtype=torch.int32, device=DEV)
+    L.prefill_cache(k, v, r, w.K, w.rope_base, kc, vc, cl, rope_mode)
+    torch.cuda.synchronize()
+    f = _f64(pin, wp)
+    topk = O.select_heads(pin["logits"], w.K)
+    rk, rv, rn = O.prefill_cache(f["k"], f["v"], topk, w.H, w.rope_base, rope_mode)
+    np.testing.assert_array_equal(cl.cpu().numpy(), rn)
+    kcg, vcg = from_dev(kc), from_dev(vc)
+    for b in range(w.B):
+        for h in range(w.H):
+            n = int(rn[b, h])
+            gk = np.asarray(kcg[b, h, :n], dtype=np.float64)
+            tol = 2.0 ** -8 * np.abs(rk[b, h, :n]) + 1e-6 if dtype == "bf16" else 2e-6
+            assert (np.abs(gk - rk[b, h, :n]) <= tol).all(), f"k cache b={b} h={h}"
+            np.testing.assert_array_equal(np.asarray(vcg[b, h, :n], dtype=np.float64), rv[b, h, :n])
+            assert not np.asarray(kcg[b, h, n:], dtype=np.float64).any()   # rows past n untouched
+    # one decode step for token T
+    lg1 = torch.from_numpy(np.ascontiguousarray(inp["logits"][:, T])).to(DEV)
+    q1, k1, v1 = (to_dev(np.ascontiguousarray(inp[x][:, :, T]), dtype) for x in ("q", "k", "v"))
+    seq_pos = torch.full((w.B,), T, dtype=torch.int32, device=DEV) if rope_mode == O.ROPE_GLOBAL else None
+    res = L.decode_step(lg1, q1, k1, v1, kc, vc, cl, w.K, w.rope_base, rope_mode, seq_pos=seq_pos,
+                        out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    topk_full = O.select_heads(inp["logits"], w.K)
+    g_full = O.route_gates(inp["logits"], topk_full, O.GATE_SOFTMAX_SELECTED)
+    ff = _f64(inp, w)
+    for b in range(w.B):
+        o, _ = O.prefill_rows(ff["q"], ff["k"], ff["v"], topk_full, g_full, w.H, w.rope_base, b,
+                              [T], rope_mode)
+        e = check_out(from_dev(res["out"])[b:b + 1], o, dtype)
+        say(f"  b={b} decode after hand-off: max err {e:.2e}")
+
+
 def test_prefill_deterministic():
     w = W.WORKLOADS[4].with_(B=1, T=2048)
     say("prefill determinism")

@@ -349,6 +349,26 @@ def test_prefill_equals_incremental_decode(gate_mode):
                 assert res["cache_len"][b, res["topk_idx"][b, kk]] == lens[b, res["topk_idx"][b, kk]] + 1
 
 
+@pytest.mark.parametrize("rope_mode", [O.ROPE_HEAD_RELATIVE, O.ROPE_GLOBAL, O.ROPE_NONE])
+def test_prefill_cache_continues_as_the_definition(rope_mode):
+    # prefill_cache of a prompt followed by one decode step gives the layer's
+    # definition (explicit visibility mask) at the next token: a wrong rank
+    # order, rotation position or missing row would not
+    B, T, H, K, d, base = 2, 37, 5, 2, 8, 1e4
+    g = np.random.default_rng(21)
+    logits = g.standard_normal((B, T, H)).astype(np.float32)
+    q, k, v = (g.standard_normal((B, H, T, d)) for _ in range(3))
+    full = O.prefill(logits, q, k, v, K, base, rope_mode=rope_mode, form="definition")
+    for Tp in (0, 1, 17, T - 1):
+        topk = O.select_heads(logits[:, :Tp], K)
+        kc, vc, n = O.prefill_cache(k[:, :, :Tp], v[:, :, :Tp], topk, H, base, rope_mode)
+        np.testing.assert_array_equal(n, O.permutation(topk, H)[0])
+        res = O.decode_step(logits[:, Tp], q[:, :, Tp], k[:, :, Tp], v[:, :, Tp],
+                            lambda b, h, nn: kc[b, h, :nn], lambda b, h, nn: vc[b, h, :nn],
+                            n, K, base, rope_mode=rope_mode, seq_pos=np.full(B, Tp))
+        np.testing.assert_allclose(res["out"], full["out"][:, Tp], atol=1e-12)
+
+
 def test_decode_reads_only_selected_caches_and_counts():
     B, H, K, d = 3, 8, 2, 4
     g = np.random.default_rng(14)
