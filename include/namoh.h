@@ -97,6 +97,43 @@ namoh_status namoh_route(const float* logits, int B, int T, int H, int K,
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Routing with loss-free balancing biases (App. "Auxiliary-Loss-Free
+ * Balancing", Eq. namoh-biased-routing): the heads are selected by their
+ * affinity plus a per-head bias, the gates keep the affinity alone.
+ *
+ * In:  logits    float32 [B, T, H]   as for namoh_route.
+ *      bias      float32 [H]         per-head selection bias (finite).
+ * Out: as namoh_route, with
+ *      topk_idx  the K heads of largest score s_i = float(a_i + b_i),
+ *                ordered by score descending, equal scores by head index
+ *                ascending, where a = softmax over the H logits is formed
+ *                in double (exp of l - max over the token) and the sum
+ *                a_i + b_i is rounded once to float;
+ *      gates     g_k = a of the selected head, rounded to float, not
+ *                renormalised.
+ * Same workspace as namoh_route (namoh_route_workspace_size).
+ * ---------------------------------------------------------------------- */
+namoh_status namoh_route_biased(const float* logits, const float* bias, int B, int T,
+                                int H, int K, int32_t* topk_idx, float* gates,
+                                int32_t* head_len, int32_t* seg_offsets,
+                                int32_t* perm_token, int32_t* slot_pos,
+                                void* workspace, size_t workspace_bytes,
+                                void* stream);
+
+/* ------------------------------------------------------------------------
+ * Loss-free balancing bias step after a batch (App. "Auxiliary-Loss-Free
+ * Balancing", Eq. namoh-loss-free): with c_i = sum over b of head_len[b, i]
+ * and c_bar = B*T*K / H, bias[i] += eta * sign(c_bar - c_i) (sign(0) = 0,
+ * taken exactly in integers; one float add).
+ *
+ * In:  head_len  int32 [B, H] of the batch (namoh_route's output).
+ *      eta       the update rate (finite).
+ * In/out: bias   float32 [H].  No workspace.
+ * ---------------------------------------------------------------------- */
+namoh_status namoh_route_bias_update(const int32_t* head_len, int B, int T, int H, int K,
+                                     float eta, float* bias, void* stream);
+
+/* ------------------------------------------------------------------------
  * Routed causal attention and gated combine (Sec. 3.1 Eq. namoh-attention,
  * Sec. 3.2 Eq. namoh-head-rope).  Consumes namoh_route's outputs.
  *

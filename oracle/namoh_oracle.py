@@ -37,6 +37,10 @@ Readings where the paper is silent (each also listed in the design notes):
 * R6 decode caches hold keys after rotation, in rank order; the new token
   takes rank n (its head's current length) and attends to itself.
 * R7 sequences of a batch are independent (ranks restart per sequence).
+* R8 loss-free balancing selects by float32(a + b) with the affinities a
+  formed in float64; equal scores go to the lower head index; the gates are
+  a (the paper fixes no precision for the selection; one rounding step both
+  sides take keeps the decision reproducible).
 """
 from __future__ import annotations
 
@@ -47,7 +51,8 @@ import numpy as np
 __all__ = [
     "GATE_SOFTMAX_SELECTED", "GATE_SOFTMAX_ALL",
     "ROPE_HEAD_RELATIVE", "ROPE_GLOBAL", "ROPE_NONE",
-    "select_heads", "route_gates", "membership", "head_ranks", "permutation",
+    "select_heads", "route_gates", "select_heads_biased", "bias_update",
+    "membership", "head_ranks", "permutation",
     "rope_rotate", "visibility_mask", "attention_definition",
     "attention_gathered", "combine_packed", "combine_dense", "prefill",
     "prefill_rows", "prefill_cache", "decode_step", "brute_force_layer", "interaction_count",
@@ -96,6 +101,44 @@ def route_gates(logits: np.ndarray, topk_idx: np.ndarray, mode: int) -> np.ndarr
         a = e / e.sum(axis=-1, keepdims=True)          # affinities a_t
         return np.take_along_axis(a, topk_idx.astype(np.int64), axis=-1)  # g = m * a
     raise ValueError("unknown gate mode")
+
+
+# ----------------------------------------------------------------------------
+# Loss-free balancing: App. "Auxiliary-Loss-Free Balancing",
+# Eqs. (namoh-biased-routing), (namoh-loss-free); reading R8
+
+def select_heads_biased(logits: np.ndarray, bias: np.ndarray, K: int):
+    """S_K(t) = TopK_i(a_{t,i} + b_i) with a_t = softmax over the H logits;
+    gates g = a of the selected heads, not renormalised.
+
+    The score is decided in one fixed precision on every side (reading R8):
+    a in float64 (exp of l - max, divided by the sum), then a + b rounded
+    once to float32; heads ordered by score descending, then head index
+    ascending.  Returns topk int32 [..., K] and gates float64 [..., K]."""
+    l = np.asarray(logits, dtype=np.float64)
+    if np.isnan(l).any():
+        raise ValueError("router logits must not be NaN")
+    H = l.shape[-1]
+    if not 1 <= K <= H:
+        raise ValueError("need 1 <= K <= H")
+    b = np.asarray(bias, dtype=np.float32).astype(np.float64)
+    e = np.exp(l - l.max(axis=-1, keepdims=True))
+    a = e / e.sum(axis=-1, keepdims=True)
+    score = (a + b).astype(np.float32).astype(np.float64)
+    idx = np.broadcast_to(np.arange(H), l.shape)
+    topk = np.lexsort((idx, -score), axis=-1)[..., :K].astype(np.int32)
+    return topk, np.take_along_axis(a, topk.astype(np.int64), axis=-1)
+
+
+def bias_update(head_len: np.ndarray, bias: np.ndarray, eta: float, T: int, K: int):
+    """b_i <- b_i + eta sign(c_bar - c_i), c_i = sum over the batch of n_{b,i},
+    c_bar = N K / H with N = B T tokens (sign(0) = 0), as float32 [H]."""
+    n = np.asarray(head_len, dtype=np.int64)
+    B, H = n.shape
+    c = n.sum(axis=0)
+    sgn = np.sign(B * T * K - H * c)            # sign(c_bar - c_i), exact in integers
+    step = np.float32(eta) * sgn.astype(np.float32)
+    return (np.asarray(bias, dtype=np.float32) + step).astype(np.float32)
 
 
 def membership(topk_idx: np.ndarray, H: int) -> np.ndarray:

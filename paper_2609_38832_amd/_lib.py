@@ -28,7 +28,7 @@ GATE_SOFTMAX_SELECTED, GATE_SOFTMAX_ALL = 0, 1
 ROPE_HEAD_RELATIVE, ROPE_GLOBAL, ROPE_NONE = 0, 1, 2
 
 EXPORTED = (
-    "namoh_route_workspace_size", "namoh_route",
+    "namoh_route_workspace_size", "namoh_route", "namoh_route_biased", "namoh_route_bias_update",
     "namoh_attn_fwd_workspace_size", "namoh_attn_fwd",
     "namoh_prefill_cache",
     "namoh_decode_workspace_size", "namoh_decode_step",
@@ -44,6 +44,8 @@ _S = ctypes.c_size_t
 _SIGS = {
     "namoh_route_workspace_size": (_S, [_I, _I, _I, _I]),
     "namoh_route": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+    "namoh_route_biased": (_I, [_P, _P, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+    "namoh_route_bias_update": (_I, [_P, _I, _I, _I, _I, _F, _P, _P]),
     "namoh_attn_fwd_workspace_size": (_S, [_I, _I, _I, _I, _I, _I]),
     "namoh_attn_fwd": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F,
                             _P, _P, _P, _P, _P, _I, _P, _P, _S, _P]),
@@ -140,9 +142,13 @@ def route_workspace_size(B, T, H, K) -> int:
 
 
 def route(logits: torch.Tensor, K: int, gate_mode: int = GATE_SOFTMAX_SELECTED,
-          out: Optional[dict] = None, ws: Optional[torch.Tensor] = None) -> dict:
-    """namoh_route on float32 logits [B, T, H]."""
-    _need_cuda(logits)
+          out: Optional[dict] = None, ws: Optional[torch.Tensor] = None,
+          bias: Optional[torch.Tensor] = None) -> dict:
+    """namoh_route on float32 logits [B, T, H]; with a float32 [H] `bias`,
+    namoh_route_biased (loss-free balancing; gate_mode is then ignored)."""
+    _need_cuda(logits, bias)
+    if bias is not None and (bias.dtype != torch.float32 or bias.shape != (logits.shape[-1],)):
+        raise ValueError("bias must be float32 [H]")
     if logits.dtype != torch.float32 or logits.dim() != 3:
         raise ValueError("logits must be float32 [B, T, H]")
     B, T, H = logits.shape
@@ -160,11 +166,26 @@ def route(logits: torch.Tensor, K: int, gate_mode: int = GATE_SOFTMAX_SELECTED,
     nbytes = route_workspace_size(B, T, H, K)
     if ws is None:
         ws = workspace(nbytes, dev)
-    check(lib().namoh_route(_ptr(logits), B, T, H, K, gate_mode,
-                            _ptr(out["topk_idx"]), _ptr(out["gates"]), _ptr(out["head_len"]),
-                            _ptr(out["seg_offsets"]), _ptr(out["perm_token"]),
-                            _ptr(out["slot_pos"]), _ptr(ws), ws.numel(), _stream(dev)))
+    outs = (_ptr(out["topk_idx"]), _ptr(out["gates"]), _ptr(out["head_len"]),
+            _ptr(out["seg_offsets"]), _ptr(out["perm_token"]), _ptr(out["slot_pos"]))
+    if bias is None:
+        check(lib().namoh_route(_ptr(logits), B, T, H, K, gate_mode, *outs, _ptr(ws),
+                                ws.numel(), _stream(dev)))
+    else:
+        check(lib().namoh_route_biased(_ptr(logits), _ptr(bias), B, T, H, K, *outs, _ptr(ws),
+                                       ws.numel(), _stream(dev)))
     return out
+
+
+def route_bias_update(head_len: torch.Tensor, T: int, K: int, eta: float,
+                      bias: torch.Tensor) -> None:
+    """namoh_route_bias_update: bias [H] += eta * sign(B*T*K/H - sum_b head_len[b])."""
+    _need_cuda(head_len, bias)
+    B, H = head_len.shape
+    if head_len.dtype != torch.int32 or bias.dtype != torch.float32 or bias.shape != (H,):
+        raise ValueError("head_len int32 [B, H], bias float32 [H]")
+    check(lib().namoh_route_bias_update(_ptr(head_len), B, T, H, K, float(eta), _ptr(bias),
+                                        _stream(head_len.device)))
 
 
 def attn_workspace_size(B, T, H, K, d, dtype_c) -> int:

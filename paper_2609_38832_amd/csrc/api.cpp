@@ -124,9 +124,44 @@ namoh_status namoh_route(const float* logits, int B, int T, int H, int K,
                            namoh::route_workspace_bytes(B, T, H, K))) != NAMOH_OK)
     return s;
   clear_hip_error();
-  return hip_status(namoh::launch_route(logits, B, T, H, K, gate_mode, topk_idx, gates,
+  return hip_status(namoh::launch_route(logits, nullptr, B, T, H, K, gate_mode, topk_idx, gates,
                                         head_len, seg_offsets, perm_token, slot_pos,
                                         workspace, static_cast<hipStream_t>(stream)));
+}
+
+namoh_status namoh_route_biased(const float* logits, const float* bias, int B, int T, int H,
+                                int K, int32_t* topk_idx, float* gates, int32_t* head_len,
+                                int32_t* seg_offsets, int32_t* perm_token, int32_t* slot_pos,
+                                void* workspace, size_t workspace_bytes, void* stream) {
+  namoh_status s;
+  if ((s = check_sizes(B, T, H, K)) != NAMOH_OK) return s;
+  REQUIRE_PTR(logits, 4);
+  REQUIRE_PTR(bias, 4);
+  REQUIRE_PTR(topk_idx, 4);
+  REQUIRE_PTR(gates, 4);
+  REQUIRE_PTR(head_len, 4);
+  REQUIRE_PTR(seg_offsets, 4);
+  REQUIRE_PTR(perm_token, 4);
+  REQUIRE_PTR(slot_pos, 4);
+  if ((s = check_workspace(workspace, workspace_bytes,
+                           namoh::route_workspace_bytes(B, T, H, K))) != NAMOH_OK)
+    return s;
+  clear_hip_error();
+  return hip_status(namoh::launch_route(logits, bias, B, T, H, K, NAMOH_GATE_SOFTMAX_ALL,
+                                        topk_idx, gates, head_len, seg_offsets, perm_token,
+                                        slot_pos, workspace, static_cast<hipStream_t>(stream)));
+}
+
+namoh_status namoh_route_bias_update(const int32_t* head_len, int B, int T, int H, int K,
+                                     float eta, float* bias, void* stream) {
+  namoh_status s;
+  if ((s = check_sizes(B, T, H, K)) != NAMOH_OK) return s;
+  REQUIRE(std::isfinite(eta), "eta must be finite");
+  REQUIRE_PTR(head_len, 4);
+  REQUIRE_PTR(bias, 4);
+  clear_hip_error();
+  return hip_status(namoh::launch_route_bias_update(head_len, B, T, H, K, eta, bias,
+                                                    static_cast<hipStream_t>(stream)));
 }
 
 size_t namoh_attn_fwd_workspace_size(int B, int T, int H, int K, int d_head, int dtype) {

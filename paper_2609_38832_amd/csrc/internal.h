@@ -30,7 +30,10 @@ void prof_mark(const char* section, bool begin, hipStream_t st);
 // ---- routing (route.hip) -------------------------------------------------
 constexpr int kRouteChunk = 64;   // tokens per routing workgroup (one wave)
 size_t route_workspace_bytes(int B, int T, int H, int K);
-hipError_t launch_route(const float* logits, int B, int T, int H, int K,
+hipError_t launch_route_bias_update(const int32_t* head_len, int B, int T, int H, int K,
+                                   float eta, float* bias, hipStream_t st);
+// bias: NULL for the plain selection, else [H] per-head selection biases
+hipError_t launch_route(const float* logits, const float* bias, int B, int T, int H, int K,
                         int gate_mode, int32_t* topk_idx, float* gates,
                         int32_t* head_len, int32_t* seg_offsets,
                         int32_t* perm_token, int32_t* slot_pos, void* ws,

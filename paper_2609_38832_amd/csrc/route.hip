@@ -5,7 +5,9 @@
 // every (batch, head) subsequence): the permutation is a stable counting sort
 // of the (token, head) pairs by segment b*H + h.
 //
-// Two or three launches; no global atomics, so every output is deterministic:
+// Two or three launches; no global atomics, so every output is deterministic
+// (the loss-free-balancing variant orders by biased affinities, see
+// k_route_count; k_route_bias_update applies the per-batch bias step):
 //   1. k_route_count   eight lanes per token, 64 tokens per workgroup: K
 //                      rounds of a cooperative argmax under the total order
 //                      (logit desc, head asc), the gates, and for every
@@ -78,10 +80,17 @@ constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141;
 // the owning lane removes it.  K <= KMAX <= 8 keeps the winners in
 // registers and lane k of the group stores round k; otherwise lane 0 stores
 // and rescales in place.
-template <int HMAX, int KMAX>
+//
+// BIASED (loss-free balancing, App. "Auxiliary-Loss-Free Balancing", Eq.
+// namoh-biased-routing): the order is (score desc, head asc) with score =
+// float(a + b), a = softmax over the H logits formed in double (exp of
+// l - max, sum over the token's eight lanes), b the head's bias, and the
+// gates are the selected affinities a (rounded to float, not renormalised);
+// each lane writes the gates of the heads it owns.
+template <int HMAX, int KMAX, bool BIASED>
 __global__ __launch_bounds__(kCountThreads) void k_route_count(
-    const float* __restrict__ logits, int T, int H, int K, int gate_mode,
-    int nchunk, int32_t* __restrict__ topk_idx, float* __restrict__ gates,
+    const float* __restrict__ logits, const float* __restrict__ bias, int T, int H, int K,
+    int gate_mode, int nchunk, int32_t* __restrict__ topk_idx, float* __restrict__ gates,
     int32_t* __restrict__ slot_rank, int32_t* __restrict__ chunk_counts) {
   constexpr int HL = HMAX / kLPT;
   __shared__ int s_wcnt[kCountWaves][HMAX];
@@ -117,10 +126,36 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
     for (int e = 0; e < HL; ++e) val[e] = (valid && sub * HL + e < H) ? lp[e] : -INFINITY;
   }
   uint64_t ck[HL];
+  float aff[BIASED ? HL : 1];   // BIASED: the affinities of this lane's heads
+  if constexpr (BIASED) {
+    float mx = -INFINITY;
 #pragma unroll
-  for (int e = 0; e < HL; ++e) {
-    const int j = sub * HL + e;
-    ck[e] = (valid && j < H) ? cand(logit_key(val[e]), j) : 0ull;
+    for (int e = 0; e < HL; ++e)
+      if (sub * HL + e < H) mx = fmaxf(mx, val[e]);
+#pragma unroll
+    for (int o = 1; o < kLPT; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, kLPT));
+    double ex[HL], z = 0.0;
+#pragma unroll
+    for (int e = 0; e < HL; ++e) {
+      ex[e] = sub * HL + e < H ? exp(static_cast<double>(val[e]) - static_cast<double>(mx)) : 0.0;
+      z += ex[e];
+    }
+#pragma unroll
+    for (int o = 1; o < kLPT; o <<= 1) z += __shfl_xor(z, o, kLPT);
+#pragma unroll
+    for (int e = 0; e < HL; ++e) {
+      const int j = sub * HL + e;
+      const double a = ex[e] / z;
+      aff[e] = static_cast<float>(a);
+      const float score = j < H ? static_cast<float>(a + static_cast<double>(bias[j])) : 0.f;
+      ck[e] = (valid && j < H) ? cand(logit_key(score), j) : 0ull;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < HL; ++e) {
+      const int j = sub * HL + e;
+      ck[e] = (valid && j < H) ? cand(logit_key(val[e]), j) : 0ull;
+    }
   }
 
   int32_t* tk = topk_idx + row * K;
@@ -154,10 +189,13 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
         own_k[e] = k;
       }
     const int bj = cand_head(best);
-    const float v = key_logit(cand_key(best));
-    if (k == 0) lmax = v;
-    const float e = expf(v - lmax);
-    denom += e;
+    float e = 0.f;
+    if constexpr (!BIASED) {
+      const float v = key_logit(cand_key(best));
+      if (k == 0) lmax = v;
+      e = expf(v - lmax);
+      denom += e;
+    }
     if constexpr (KMAX <= 8) {
 #pragma unroll
       for (int kk = 0; kk < KMAX; ++kk)
@@ -167,10 +205,10 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
         }
     } else if (valid && sub == 0) {
       tk[k] = bj;
-      gk[k] = e;  // unnormalised; scaled below
+      if constexpr (!BIASED) gk[k] = e;  // unnormalised; scaled below
     }
   }
-  if (gate_mode == 1) {  // softmax over all H logits, no renormalisation
+  if (!BIASED && gate_mode == 1) {  // softmax over all H logits, no renormalisation
     float part = 0.f;
 #pragma unroll
     for (int e = 0; e < HL; ++e)
@@ -179,7 +217,7 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
     for (int o = 1; o < kLPT; o <<= 1) part += __shfl_xor(part, o, kLPT);
     denom = part;
   }
-  const float inv = 1.f / denom;
+  const float inv = BIASED ? 0.f : 1.f / denom;
   int mj = 0;
   float me = 0.f;
   if constexpr (KMAX <= 8) {
@@ -226,7 +264,15 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
   }
   // the selections and gates are stored last: a barrier after a global
   // store would wait for the store to complete
-  if constexpr (KMAX <= 8) {
+  if constexpr (BIASED) {
+    if constexpr (KMAX <= 8)
+      if (valid && sub < K) tk[sub] = mj;
+    if (valid) {
+#pragma unroll
+      for (int e = 0; e < HL; ++e)
+        if ((own >> e) & 1u) gk[own_k[e]] = aff[e];
+    }
+  } else if constexpr (KMAX <= 8) {
     if (valid && sub < K) {
       tk[sub] = mj;
       gk[sub] = me * inv;
@@ -234,6 +280,22 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
   } else if (valid && sub == 0) {
     for (int k = 0; k < K; ++k) gk[k] *= inv;
   }
+}
+
+// Loss-free balancing update (App. "Auxiliary-Loss-Free Balancing", Eq.
+// namoh-loss-free): c_i = sum over the batch of head_len[b][i], c_bar =
+// B T K / H, b_i += eta sign(c_bar - c_i); the sign is taken exactly as
+// sign(B T K - H c_i) in 64-bit integers, the update is one float add.
+__global__ __launch_bounds__(kWave) void k_route_bias_update(const int32_t* __restrict__ head_len,
+                                                             int B, long long total, int H,
+                                                             float eta, float* __restrict__ bias) {
+  const int h = thread_x();
+  if (h >= H) return;
+  long long c = 0;
+  for (int b = 0; b < B; ++b) c += head_len[static_cast<size_t>(b) * H + h];
+  const long long diff = total - static_cast<long long>(H) * c;
+  const float step = diff > 0 ? eta : (diff < 0 ? -eta : 0.f);
+  bias[h] = bias[h] + step;
 }
 
 __global__ __launch_bounds__(kWave) void k_route_scan(
@@ -328,7 +390,14 @@ size_t route_workspace_bytes(int B, int T, int H, int /*K*/) {
   return 2 * align_up(L * sizeof(int32_t));
 }
 
-hipError_t launch_route(const float* logits, int B, int T, int H, int K,
+hipError_t launch_route_bias_update(const int32_t* head_len, int B, int T, int H, int K,
+                                   float eta, float* bias, hipStream_t st) {
+  k_route_bias_update<<<1, kWave, 0, st>>>(head_len, B, static_cast<long long>(B) * T * K, H,
+                                            eta, bias);
+  return hipGetLastError();
+}
+
+hipError_t launch_route(const float* logits, const float* bias, int B, int T, int H, int K,
                         int gate_mode, int32_t* topk_idx, float* gates,
                         int32_t* head_len, int32_t* seg_offsets,
                         int32_t* perm_token, int32_t* slot_pos, void* ws,
@@ -339,8 +408,15 @@ hipError_t launch_route(const float* logits, int B, int T, int H, int K,
   int32_t* counts = cv.take<int32_t>(L);
   int32_t* within = cv.take<int32_t>(L);
   const dim3 grid(static_cast<unsigned>(static_cast<size_t>(B) * nchunk));
-#define NAMOH_RC(HM, KM) \
-  k_route_count<HM, KM><<<grid, kCountThreads, 0, st>>>(logits, T, H, K, gate_mode, nchunk, topk_idx, gates, slot_pos, counts)
+#define NAMOH_RC(HM, KM)                                                                   \
+  do {                                                                                     \
+    if (bias)                                                                              \
+      k_route_count<HM, KM, true><<<grid, kCountThreads, 0, st>>>(                         \
+          logits, bias, T, H, K, gate_mode, nchunk, topk_idx, gates, slot_pos, counts);    \
+    else                                                                                   \
+      k_route_count<HM, KM, false><<<grid, kCountThreads, 0, st>>>(                        \
+          logits, nullptr, T, H, K, gate_mode, nchunk, topk_idx, gates, slot_pos, counts); \
+  } while (0)
   const bool small_k = K <= 8;
   if (H <= 8) NAMOH_RC(8, 8);
   else if (H <= 16) { if (small_k) NAMOH_RC(16, 8); else NAMOH_RC(16, 64); }

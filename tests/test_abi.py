@@ -63,6 +63,30 @@ def test_route_rejects(lib, kw, code):
     assert L.last_error() != ""
 
 
+def _route_b(lib, bias=fake(8), B=1, T=64, H=8, K=2, ws=fake(9), wsb=1 << 20, logits=fake(0)):
+    return lib.namoh_route_biased(logits, bias, B, T, H, K, fake(1), fake(2), fake(3), fake(4),
+                                  fake(5), fake(6), ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(bias=None), 1), (dict(bias=P(A + 2)), 1), (dict(logits=None), 1), (dict(K=9), 1),
+    (dict(H=65), 1), (dict(wsb=16), 3),
+])
+def test_route_biased_rejects(lib, kw, code):
+    assert _route_b(lib, **kw) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(eta=float("nan")), 1), (dict(eta=float("inf")), 1), (dict(hl=None), 1),
+    (dict(bias=None), 1), (dict(bias=P(A + 1)), 1), (dict(K=0), 1), (dict(H=65), 1),
+])
+def test_route_bias_update_rejects(lib, kw, code):
+    a = dict(hl=fake(0), B=2, T=64, H=8, K=2, eta=0.01, bias=fake(1))
+    a.update(kw)
+    assert lib.namoh_route_bias_update(a["hl"], a["B"], a["T"], a["H"], a["K"], a["eta"],
+                                       a["bias"], None) == code
+
+
 def _attn(lib, dtype=1, B=1, T=64, H=8, K=2, d=64, base=1e4, rope=0, scale=0.0, out_dt=0,
           q=fake(0), out=fake(7), head_out=None, ws=fake(9), wsb=1 << 30, gates=fake(3)):
     return lib.namoh_attn_fwd(q, fake(1), fake(2), dtype, B, T, H, K, d, base, rope, scale,

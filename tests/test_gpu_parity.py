@@ -93,6 +93,73 @@ def test_route_shapes(H, K, T):
     assert_routing_exact(got, _oracle_routing({"logits": lg}, w))
 
 
+@pytest.mark.parametrize("H,K,T", [(8, 2, 300), (32, 8, 1000), (64, 8, 700), (16, 9, 200),
+                                   (64, 12, 130), (5, 5, 65)])
+def test_route_biased_bit_exact(H, K, T):
+    # loss-free balancing selection: biases of the size of the affinity gaps
+    B = 2
+    g = np.random.default_rng(100 + H + K)
+    logits = g.standard_normal((B, T, H)).astype(np.float32)
+    bias = (g.standard_normal(H) * (0.5 / H)).astype(np.float32)
+    say(f"route biased H={H} K={K} T={T}")
+    r = L.route(torch.from_numpy(logits).to(DEV), K, bias=torch.from_numpy(bias).to(DEV))
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in r.items()}
+    topk, gates = O.select_heads_biased(logits, bias, K)
+    n, off, perm, slot = O.permutation(topk, H)
+    ref = {"topk_idx": topk, "gates": gates, "head_len": n, "seg_offsets": off,
+           "perm_token": perm, "slot_pos": slot}
+    assert_routing_exact(got, ref)
+    # the bias changed the selection somewhere (the case is not vacuous)
+    assert K == H or (topk != O.select_heads(logits, K)).any()
+
+
+def test_route_biased_ties_and_bias_update():
+    # equal logits and equal biases: every score ties, the lowest heads win
+    B, T, H, K = 2, 100, 16, 4
+    logits = np.zeros((B, T, H), np.float32)
+    r = L.route(torch.from_numpy(logits).to(DEV), K, bias=torch.zeros(H, device=DEV))
+    torch.cuda.synchronize()
+    assert (r["topk_idx"].cpu().numpy() == np.arange(K)).all()
+    np.testing.assert_allclose(r["gates"].cpu().numpy(), 1.0 / H, rtol=1e-6)
+    # the bias step on a skewed batch, bit for bit, over several batches
+    g = np.random.default_rng(7)
+    bias = np.zeros(H, np.float32)
+    bias_d = torch.zeros(H, device=DEV)
+    for step in range(4):
+        lg = (g.standard_normal((B, T, H)) + np.log(1.0 / (np.arange(H) + 1.0))).astype(np.float32)
+        rr = L.route(torch.from_numpy(lg).to(DEV), K, bias=bias_d)
+        L.route_bias_update(rr["head_len"], T, K, 0.01, bias_d)
+        torch.cuda.synchronize()
+        topk, _ = O.select_heads_biased(lg, bias, K)
+        n = O.permutation(topk, H)[0]
+        np.testing.assert_array_equal(rr["head_len"].cpu().numpy(), n)
+        bias = O.bias_update(n, bias, 0.01, T, K)
+        np.testing.assert_array_equal(bias_d.cpu().numpy(), bias)
+    say(f"  bias after 4 steps: {bias.round(3).tolist()}")
+
+
+def test_prefill_biased_routing():
+    # the whole layer on a loss-free-balancing routing
+    w = W.WORKLOADS[2].with_(B=2, T=900)
+    say("prefill with biased routing")
+    inp = W.prefill_inputs(w)
+    bias = (np.random.default_rng(5).standard_normal(w.H) * 0.02).astype(np.float32)
+    lg = torch.from_numpy(inp["logits"]).to(DEV)
+    q, k, v = (to_dev(inp[x], w.dtype) for x in ("q", "k", "v"))
+    r = L.route(lg, w.K, bias=torch.from_numpy(bias).to(DEV))
+    o = L.attn_fwd(q, k, v, r, w.K, w.rope_base, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    f = _f64(inp, w)
+    topk, gates = O.select_heads_biased(inp["logits"], bias, w.K)
+    n, off, perm, slot = O.permutation(topk, w.H)
+    np.testing.assert_array_equal(r["topk_idx"].cpu().numpy(), topk)
+    hp = O.attention_gathered(f["q"], f["k"], f["v"], n, off, perm, w.H, w.rope_base)
+    ref = O.combine_packed(hp, slot, gates)
+    e = check_out(from_dev(o), ref, w.dtype)
+    say(f"  max err {e:.2e}")
+
+
 # ----------------------------------------------------------------------------
 # prefill: whole outputs at sizes the oracle finishes quickly
 

@@ -412,3 +412,65 @@ def test_workload_generator_is_deterministic_and_rounds_bf16():
     # 1 + 2^-8 is a tie -> even (1.0); 1 + 3*2^-8 is a tie -> even (1 + 2^-6)
     np.testing.assert_array_equal(W.bf16_bits_to_f32(bits)[:3], [1.0, 1.0, 1.015625])
     assert abs(W.bf16_bits_to_f32(bits)[3] / x[3] - 1) < 2 ** -8
+
+
+# ----------------------------------------------------------------------------
+# Loss-free balancing (App. "Auxiliary-Loss-Free Balancing")
+
+def test_biased_selection_without_bias_is_the_plain_selection():
+    # softmax is monotone, so TopK of the affinities is TopK of the logits
+    g = np.random.default_rng(31)
+    logits = g.standard_normal((3, 50, 16)).astype(np.float32)
+    for K in (1, 4, 16):
+        topk, gates = O.select_heads_biased(logits, np.zeros(16), K)
+        np.testing.assert_array_equal(topk, O.select_heads(logits, K))
+        np.testing.assert_allclose(gates, O.route_gates(logits, topk, O.GATE_SOFTMAX_ALL),
+                                   rtol=1e-14)
+
+
+def test_biased_selection_bias_moves_selection_not_gates():
+    g = np.random.default_rng(32)
+    H, K = 12, 3
+    logits = g.standard_normal((2, 40, H)).astype(np.float32)
+    bias = np.zeros(H)
+    bias[7] = 2.0                        # above any affinity: always selected, first
+    topk, gates = O.select_heads_biased(logits, bias, K)
+    assert (topk[..., 0] == 7).all()
+    np.testing.assert_allclose(gates, O.route_gates(logits, topk, O.GATE_SOFTMAX_ALL),
+                               rtol=1e-14)   # gates keep the unbiased affinities
+    bias = np.full(H, -2.0)
+    bias[[2, 5, 9]] = 0.0                # only these three can win
+    topk, _ = O.select_heads_biased(logits, bias, K)
+    assert (np.sort(topk, axis=-1) == [2, 5, 9]).all()
+    # the three kept heads come in affinity order
+    a = O.route_gates(logits, topk, O.GATE_SOFTMAX_ALL)
+    assert (np.diff(a, axis=-1) <= 0).all()
+
+
+def test_biased_selection_worked_example():
+    # logits (0, ln 2, 0, 0): a = (0.2, 0.4, 0.2, 0.2); bias (0.125, 0, 0.0625, 0)
+    # -> scores (0.325, 0.4, 0.2625, 0.2): heads 1 then 0, gates 0.4 and 0.2
+    logits = np.array([[[0.0, np.log(2.0), 0.0, 0.0]]], dtype=np.float32)
+    topk, gates = O.select_heads_biased(logits, np.array([0.125, 0.0, 0.0625, 0.0]), 2)
+    assert topk.tolist() == [[[1, 0]]]
+    np.testing.assert_allclose(gates[0, 0], [0.4, 0.2], rtol=1e-6)
+    # equal scores: the lower head index first
+    topk, _ = O.select_heads_biased(np.zeros((1, 1, 5), np.float32), np.zeros(5), 3)
+    assert topk.tolist() == [[[0, 1, 2]]]
+
+
+def test_bias_update_step():
+    # c = (5, 3, 2, 2), c_bar = T K / H = 6 * 2 / 4 = 3: the overloaded head
+    # steps down, the balanced one stays, the underloaded ones step up
+    b = O.bias_update(np.array([[5, 3, 2, 2]]), np.array([0.5, 0.0, -0.25, 0.0]), 0.125, 6, 2)
+    assert b.dtype == np.float32
+    assert b.tolist() == [0.375, 0.0, -0.125, 0.125]
+    # counts over a routed batch sum to N K (Eq. app-assignment-count); a
+    # non-integer c_bar never gives a zero step
+    g = np.random.default_rng(33)
+    logits = g.standard_normal((3, 37, 7)).astype(np.float32)
+    topk, _ = O.select_heads_biased(logits, g.standard_normal(7) * 0.05, 2)
+    n = O.permutation(topk, 7)[0]
+    assert n.sum() == 3 * 37 * 2
+    b = O.bias_update(n, np.zeros(7), 0.5, 37, 2)
+    assert set(np.unique(b)) <= {-0.5, 0.5}
