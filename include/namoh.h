@@ -222,6 +222,22 @@ namoh_status namoh_decode_step(const float* logits, const void* q,
                                int32_t* dev_status, void* workspace,
                                size_t workspace_bytes, void* stream);
 
+/* The same step with loss-free balancing biases (App. "Auxiliary-Loss-Free
+ * Balancing", Eq. namoh-biased-routing; the biases stay fixed during
+ * inference): heads selected by float(a + b) and gated by the affinity a
+ * exactly as in namoh_route_biased.  bias: float32 [H].  Other arguments and
+ * the workspace as for namoh_decode_step (no gate_mode). */
+namoh_status namoh_decode_step_biased(const float* logits, const float* bias,
+                                      const void* q, const void* k, const void* v,
+                                      int dtype, void* k_cache, void* v_cache,
+                                      int32_t* cache_len, const int32_t* seq_pos,
+                                      int B, int H, int K, int d_head, int cap,
+                                      float rope_base, int rope_mode,
+                                      float softmax_scale, int32_t* topk_idx,
+                                      float* gates, void* out, int out_dtype,
+                                      int32_t* dev_status, void* workspace,
+                                      size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------
  * Diagnostics (not part of the layer's computation).  Opt-in timing of the
  * dominant kernels with HIP events recorded on the call's stream: sections

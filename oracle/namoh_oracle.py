@@ -319,14 +319,18 @@ def combine_packed(h_packed, slot_pos, gates):
 
 
 def prefill(logits, q, k, v, K, rope_base, rope_mode=ROPE_HEAD_RELATIVE,
-            gate_mode=GATE_SOFTMAX_SELECTED, scale=None, form="gathered"):
+            gate_mode=GATE_SOFTMAX_SELECTED, scale=None, form="gathered", bias=None):
     """Whole layer: routing, permutation, attention, combine.
 
     q, k, v float64 [B,H,T,d].  ``form`` = 'gathered' (O2) or 'definition'
-    (O1).  Returns a dict of every intermediate the GPU library exposes."""
+    (O1).  With ``bias`` [H] the routing is select_heads_biased (gate_mode
+    ignored).  Returns a dict of every intermediate the GPU library exposes."""
     H = logits.shape[-1]
-    topk = select_heads(logits, K)
-    g = route_gates(logits, topk, gate_mode)
+    if bias is None:
+        topk = select_heads(logits, K)
+        g = route_gates(logits, topk, gate_mode)
+    else:
+        topk, g = select_heads_biased(logits, bias, K)
     head_len, seg_offsets, perm, slot = permutation(topk, H)
     if form == "definition":
         hd = attention_definition(q, k, v, topk, H, rope_base, rope_mode, scale)
@@ -413,7 +417,7 @@ def prefill_cache(k, v, topk_idx, H, rope_base, rope_mode=ROPE_HEAD_RELATIVE):
 
 def decode_step(logits, q, k, v, cache_k, cache_v, cache_len, K, rope_base,
                 rope_mode=ROPE_HEAD_RELATIVE, gate_mode=GATE_SOFTMAX_SELECTED,
-                seq_pos=None, scale=None):
+                seq_pos=None, scale=None, bias=None):
     """One decoding step for B sequences.
 
     logits [B,H]; q,k,v float64 [B,H,d]; ``cache_k(b, h, n)`` and
@@ -422,11 +426,15 @@ def decode_step(logits, q, k, v, cache_k, cache_v, cache_len, K, rope_base,
 
     Returns topk_idx [B,K], gates [B,K], out [B,d], the ungated head outputs
     [B,K,d], the appended rotated keys [B,K,d] and the updated lengths.  Only
-    the selected heads' caches are read."""
+    the selected heads' caches are read.  With ``bias`` [H] the heads are
+    selected and gated as in select_heads_biased (gate_mode ignored)."""
     B, H, d = q.shape
     scale = 1.0 / math.sqrt(d) if scale is None else scale
-    topk = select_heads(logits, K)
-    g = route_gates(logits, topk, gate_mode)
+    if bias is None:
+        topk = select_heads(logits, K)
+        g = route_gates(logits, topk, gate_mode)
+    else:
+        topk, g = select_heads_biased(logits, bias, K)
     out = np.zeros((B, d))
     heads = np.zeros((B, K, d))
     new_k = np.zeros((B, K, d))

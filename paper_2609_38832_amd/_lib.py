@@ -31,7 +31,7 @@ EXPORTED = (
     "namoh_route_workspace_size", "namoh_route", "namoh_route_biased", "namoh_route_bias_update",
     "namoh_attn_fwd_workspace_size", "namoh_attn_fwd",
     "namoh_prefill_cache",
-    "namoh_decode_workspace_size", "namoh_decode_step",
+    "namoh_decode_workspace_size", "namoh_decode_step", "namoh_decode_step_biased",
     "namoh_status_string", "namoh_last_error", "namoh_version",
     "namoh_profile_enable", "namoh_profile_read",
 )
@@ -54,6 +54,8 @@ _SIGS = {
     "namoh_decode_workspace_size": (_S, [_I, _I, _I, _I, _I]),
     "namoh_decode_step": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I,
                                _F, _I, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
+    "namoh_decode_step_biased": (_I, [_P, _P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I,
+                                      _I, _F, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
     "namoh_status_string": (ctypes.c_char_p, [_I]),
     "namoh_last_error": (ctypes.c_char_p, []),
     "namoh_version": (ctypes.c_char_p, []),
@@ -248,9 +250,11 @@ def decode_step(logits: torch.Tensor, q: torch.Tensor, k: torch.Tensor, v: torch
                 seq_pos: Optional[torch.Tensor] = None,
                 out_dtype: Optional[torch.dtype] = None,
                 dev_status: Optional[torch.Tensor] = None,
-                out: Optional[dict] = None, ws: Optional[torch.Tensor] = None) -> dict:
-    """namoh_decode_step; caches [B, H, cap, d] are updated in place."""
-    _need_cuda(logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, dev_status)
+                out: Optional[dict] = None, ws: Optional[torch.Tensor] = None,
+                bias: Optional[torch.Tensor] = None) -> dict:
+    """namoh_decode_step; caches [B, H, cap, d] are updated in place.  With a
+    float32 [H] `bias`, namoh_decode_step_biased (gate_mode is then ignored)."""
+    _need_cuda(logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, dev_status, bias)
     B, H, d = q.shape
     cap = k_cache.shape[2]
     dt = dtype_code(q.dtype)
@@ -263,12 +267,20 @@ def decode_step(logits: torch.Tensor, q: torch.Tensor, k: torch.Tensor, v: torch
         }
     if ws is None:
         ws = workspace(decode_workspace_size(B, H, K, d, cap), dev)
-    check(lib().namoh_decode_step(_ptr(logits), _ptr(q), _ptr(k), _ptr(v), dt,
-                                  _ptr(k_cache), _ptr(v_cache), _ptr(cache_len), _ptr(seq_pos),
-                                  B, H, K, d, cap, float(rope_base), rope_mode, gate_mode,
-                                  float(softmax_scale), _ptr(out["topk_idx"]), _ptr(out["gates"]),
-                                  _ptr(out["out"]), dtype_code(out["out"].dtype),
-                                  _ptr(dev_status), _ptr(ws), ws.numel(), _stream(dev)))
+    tail = (float(softmax_scale), _ptr(out["topk_idx"]), _ptr(out["gates"]), _ptr(out["out"]),
+            dtype_code(out["out"].dtype), _ptr(dev_status), _ptr(ws), ws.numel(), _stream(dev))
+    if bias is None:
+        check(lib().namoh_decode_step(_ptr(logits), _ptr(q), _ptr(k), _ptr(v), dt,
+                                      _ptr(k_cache), _ptr(v_cache), _ptr(cache_len),
+                                      _ptr(seq_pos), B, H, K, d, cap, float(rope_base),
+                                      rope_mode, gate_mode, *tail))
+    else:
+        if bias.dtype != torch.float32 or bias.shape != (H,):
+            raise ValueError("bias must be float32 [H]")
+        check(lib().namoh_decode_step_biased(_ptr(logits), _ptr(bias), _ptr(q), _ptr(k), _ptr(v),
+                                             dt, _ptr(k_cache), _ptr(v_cache), _ptr(cache_len),
+                                             _ptr(seq_pos), B, H, K, d, cap, float(rope_base),
+                                             rope_mode, *tail))
     return out
 
 

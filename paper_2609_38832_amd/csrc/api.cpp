@@ -254,13 +254,14 @@ size_t namoh_decode_workspace_size(int B, int H, int K, int d_head, int cap) {
   return namoh::decode_workspace_bytes(B, H, K, d_head, cap);
 }
 
-namoh_status namoh_decode_step(const float* logits, const void* q, const void* k,
-                               const void* v, int dtype, void* k_cache, void* v_cache,
-                               int32_t* cache_len, const int32_t* seq_pos, int B, int H,
-                               int K, int d_head, int cap, float rope_base, int rope_mode,
-                               int gate_mode, float softmax_scale, int32_t* topk_idx,
-                               float* gates, void* out, int out_dtype, int32_t* dev_status,
-                               void* workspace, size_t workspace_bytes, void* stream) {
+static namoh_status decode_common(const float* logits, const float* bias, const void* q,
+                                  const void* k, const void* v, int dtype, void* k_cache,
+                                  void* v_cache, int32_t* cache_len, const int32_t* seq_pos,
+                                  int B, int H, int K, int d_head, int cap, float rope_base,
+                                  int rope_mode, int gate_mode, float softmax_scale,
+                                  int32_t* topk_idx, float* gates, void* out, int out_dtype,
+                                  int32_t* dev_status, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
   namoh_status s;
   if ((s = check_sizes(B, 1, H, K)) != NAMOH_OK) return s;
   if ((s = check_head_width(d_head)) != NAMOH_OK) return s;
@@ -292,10 +293,39 @@ namoh_status namoh_decode_step(const float* logits, const void* q, const void* k
     return s;
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
   clear_hip_error();
-  return hip_status(namoh::launch_decode(logits, q, k, v, dtype, k_cache, v_cache, cache_len,
-                                         seq_pos, B, H, K, d_head, cap, rope_base, rope_mode,
-                                         gate_mode, scale, topk_idx, gates, out, out_dtype,
-                                         dev_status, workspace, static_cast<hipStream_t>(stream)));
+  return hip_status(namoh::launch_decode(logits, bias, q, k, v, dtype, k_cache, v_cache,
+                                         cache_len, seq_pos, B, H, K, d_head, cap, rope_base,
+                                         rope_mode, gate_mode, scale, topk_idx, gates, out,
+                                         out_dtype, dev_status, workspace,
+                                         static_cast<hipStream_t>(stream)));
+}
+
+namoh_status namoh_decode_step(const float* logits, const void* q, const void* k,
+                               const void* v, int dtype, void* k_cache, void* v_cache,
+                               int32_t* cache_len, const int32_t* seq_pos, int B, int H,
+                               int K, int d_head, int cap, float rope_base, int rope_mode,
+                               int gate_mode, float softmax_scale, int32_t* topk_idx,
+                               float* gates, void* out, int out_dtype, int32_t* dev_status,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  return decode_common(logits, nullptr, q, k, v, dtype, k_cache, v_cache, cache_len, seq_pos, B,
+                       H, K, d_head, cap, rope_base, rope_mode, gate_mode, softmax_scale,
+                       topk_idx, gates, out, out_dtype, dev_status, workspace, workspace_bytes,
+                       stream);
+}
+
+namoh_status namoh_decode_step_biased(const float* logits, const float* bias, const void* q,
+                                      const void* k, const void* v, int dtype, void* k_cache,
+                                      void* v_cache, int32_t* cache_len, const int32_t* seq_pos,
+                                      int B, int H, int K, int d_head, int cap, float rope_base,
+                                      int rope_mode, float softmax_scale, int32_t* topk_idx,
+                                      float* gates, void* out, int out_dtype,
+                                      int32_t* dev_status, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
+  REQUIRE_PTR(bias, 4);
+  return decode_common(logits, bias, q, k, v, dtype, k_cache, v_cache, cache_len, seq_pos, B, H,
+                       K, d_head, cap, rope_base, rope_mode, NAMOH_GATE_SOFTMAX_ALL,
+                       softmax_scale, topk_idx, gates, out, out_dtype, dev_status, workspace,
+                       workspace_bytes, stream);
 }
 
 }  // extern "C"

@@ -57,18 +57,34 @@ __global__ __launch_bounds__(64 * kAppendWaves) void k_decode_route_append(
     void* __restrict__ k_cache, void* __restrict__ v_cache,
     int32_t* __restrict__ cache_len, const int32_t* __restrict__ seq_pos,
     int H, int K, long cap, double log_base, int rope_mode, int gate_mode,
-    float qscale, int32_t* __restrict__ topk_idx, float* __restrict__ gates,
-    int32_t* __restrict__ dev_status, float* __restrict__ qrot,
+    const float* __restrict__ bias, float qscale, int32_t* __restrict__ topk_idx,
+    float* __restrict__ gates, int32_t* __restrict__ dev_status, float* __restrict__ qrot,
     int32_t* __restrict__ rows) {
   const int b = block_x();
   const int lane = thread_x() % 64;
   const int wave = thread_x() / 64;
   const bool real = lane < H;
   const float l = real ? logits[static_cast<size_t>(b) * H + lane] : 0.f;
+  // selection key: the logit, or with loss-free balancing biases the score
+  // float(a + b) with the affinity a = softmax of the logits in double
+  // (App. "Auxiliary-Loss-Free Balancing", Eq. namoh-biased-routing)
+  float key = l, aff = 0.f;
+  if (bias != nullptr) {
+    float mx = real ? l : -INFINITY;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    double ex = real ? exp(static_cast<double>(l) - static_cast<double>(mx)) : 0.0;
+    double z = ex;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) z += __shfl_xor(z, o);
+    const double a = ex / z;
+    aff = static_cast<float>(a);
+    key = real ? static_cast<float>(a + static_cast<double>(bias[lane])) : 0.f;
+  }
   int rank = 0;
   for (int j = 0; j < H; ++j) {
-    const float lj = __shfl(l, j);
-    rank += (lj > l) || (lj == l && j < lane);
+    const float kj = __shfl(key, j);
+    rank += (kj > key) || (kj == key && j < lane);
   }
   const bool sel = real && rank < K;
   const uint64_t first = __ballot(real && rank == 0);
@@ -79,7 +95,7 @@ __global__ __launch_bounds__(64 * kAppendWaves) void k_decode_route_append(
   for (int o = 32; o > 0; o >>= 1) e_den += __shfl_xor(e_den, o);
   if (sel && wave == 0) {
     topk_idx[static_cast<size_t>(b) * K + rank] = lane;
-    gates[static_cast<size_t>(b) * K + rank] = e_sel / e_den;
+    gates[static_cast<size_t>(b) * K + rank] = bias != nullptr ? aff : e_sel / e_den;
   }
 
   // every wave routed the token; wave w appends heads w, w + 4, ...
@@ -497,7 +513,7 @@ hipError_t launch_prefill_cache(const void* k, const void* v, int dtype, int B, 
 }
 
 template <int D, bool BF16>
-static hipError_t run_decode(const float* logits, const void* q, const void* k,
+static hipError_t run_decode(const float* logits, const float* bias, const void* q, const void* k,
                              const void* v, void* k_cache, void* v_cache,
                              int32_t* cache_len, const int32_t* seq_pos, int B,
                              int H, int K, int cap, float rope_base,
@@ -510,7 +526,7 @@ static hipError_t run_decode(const float* logits, const void* q, const void* k,
   const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
   k_decode_route_append<D, BF16><<<B, 64 * kAppendWaves, 0, st>>>(
       logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, H, K, cap, log_base,
-      rope_mode, gate_mode, scale * 1.4426950408889634f, topk_idx, gates,
+      rope_mode, gate_mode, bias, scale * 1.4426950408889634f, topk_idx, gates,
       dev_status, w.qrot, w.rows);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -527,7 +543,7 @@ static hipError_t run_decode(const float* logits, const void* q, const void* k,
   return hipGetLastError();
 }
 
-hipError_t launch_decode(const float* logits, const void* q, const void* k,
+hipError_t launch_decode(const float* logits, const float* bias, const void* q, const void* k,
                          const void* v, int dtype, void* k_cache,
                          void* v_cache, int32_t* cache_len,
                          const int32_t* seq_pos, int B, int H, int K, int d,
@@ -536,7 +552,7 @@ hipError_t launch_decode(const float* logits, const void* q, const void* k,
                          float* gates, void* out, int out_dtype,
                          int32_t* dev_status, void* ws, hipStream_t st) {
 #define NAMOH_DEC(DD, BF)                                                               \
-  return run_decode<DD, BF>(logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, B, H, \
+  return run_decode<DD, BF>(logits, bias, q, k, v, k_cache, v_cache, cache_len, seq_pos, B, H, \
                             K, cap, rope_base, rope_mode, gate_mode, scale, topk_idx,    \
                             gates, out, out_dtype, dev_status, ws, st)
   if (dtype == 1) {

@@ -50,7 +50,8 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
 
 // ---- decode (decode.hip) --------------------------------------------------
 size_t decode_workspace_bytes(int B, int H, int K, int d, int cap);
-hipError_t launch_decode(const float* logits, const void* q, const void* k,
+// bias: NULL for the plain selection, else [H] loss-free balancing biases
+hipError_t launch_decode(const float* logits, const float* bias, const void* q, const void* k,
                          const void* v, int dtype, void* k_cache,
                          void* v_cache, int32_t* cache_len,
                          const int32_t* seq_pos, int B, int H, int K, int d,

@@ -156,6 +156,22 @@ def test_prefill_cache_rejects(lib, kw, code):
     assert L.last_error() != ""
 
 
+def test_decode_biased_rejects(lib):
+    # same checks as namoh_decode_step plus the bias pointer
+    args = [fake(0), fake(11), fake(1), fake(2), fake(3), 1, fake(4), fake(5), fake(6), None,
+            2, 8, 2, 64, 128, 1e4, 0, 0.0, fake(7), fake(8), fake(10), 0, None, fake(9), 8, None]
+    assert lib.namoh_decode_step_biased(*args) == 3            # workspace too small
+    bad = list(args)
+    bad[1] = None
+    assert lib.namoh_decode_step_biased(*bad) == 1              # no bias
+    bad = list(args)
+    bad[1] = P(A + 2)
+    assert lib.namoh_decode_step_biased(*bad) == 1              # misaligned bias
+    bad = list(args)
+    bad[16] = 1
+    assert lib.namoh_decode_step_biased(*bad) == 1              # GLOBAL needs seq_pos
+
+
 def test_workspace_queries(lib):
     assert lib.namoh_route_workspace_size(0, 10, 8, 2) == 0
     assert lib.namoh_route_workspace_size(1, 10, 8, 2) > 0

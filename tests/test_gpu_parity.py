@@ -316,6 +316,37 @@ def test_prefill_cache_then_decode(dtype, d, rope_mode):
         say(f"  b={b} decode after hand-off: max err {e:.2e}")
 
 
+def test_biased_prefill_cache_then_biased_decode():
+    # loss-free balancing end to end: biased routing of the prompt, hand-off,
+    # one biased decode step against the oracle's biased layer at token T
+    T, cap = 500, 512
+    w = W.WORKLOADS[3].with_(B=3, T=T + 1, H=16, K=4)
+    say("biased prefill -> cache -> biased decode")
+    inp = W.prefill_inputs(w)
+    bias = (np.random.default_rng(9).standard_normal(w.H) * 0.03).astype(np.float32)
+    bias_d = torch.from_numpy(bias).to(DEV)
+    lg = torch.from_numpy(np.ascontiguousarray(inp["logits"][:, :T])).to(DEV)
+    k, v = (to_dev(np.ascontiguousarray(inp[x][:, :, :T]), w.dtype) for x in ("k", "v"))
+    r = L.route(lg, w.K, bias=bias_d)
+    kc = torch.zeros(w.B, w.H, cap, w.d, dtype=k.dtype, device=DEV)
+    vc = torch.zeros_like(kc)
+    cl = torch.zeros(w.B, w.H, dtype=torch.int32, device=DEV)
+    L.prefill_cache(k, v, r, w.K, w.rope_base, kc, vc, cl)
+    lg1 = torch.from_numpy(np.ascontiguousarray(inp["logits"][:, T])).to(DEV)
+    q1, k1, v1 = (to_dev(np.ascontiguousarray(inp[x][:, :, T]), w.dtype) for x in ("q", "k", "v"))
+    res = L.decode_step(lg1, q1, k1, v1, kc, vc, cl, w.K, w.rope_base, out_dtype=torch.float32,
+                        bias=bias_d)
+    torch.cuda.synchronize()
+    topk, gates = O.select_heads_biased(inp["logits"], bias, w.K)
+    np.testing.assert_array_equal(res["topk_idx"].cpu().numpy(), topk[:, T])
+    np.testing.assert_allclose(res["gates"].cpu().numpy(), gates[:, T], rtol=2e-6, atol=1e-7)
+    ff = _f64(inp, w)
+    for b in range(w.B):
+        o, _ = O.prefill_rows(ff["q"], ff["k"], ff["v"], topk, gates, w.H, w.rope_base, b, [T])
+        e = check_out(from_dev(res["out"])[b:b + 1], o, w.dtype)
+        say(f"  b={b} max err {e:.2e}")
+
+
 def test_prefill_deterministic():
     w = W.WORKLOADS[4].with_(B=1, T=2048)
     say("prefill determinism")

@@ -369,6 +369,26 @@ def test_prefill_cache_continues_as_the_definition(rope_mode):
         np.testing.assert_allclose(res["out"], full["out"][:, Tp], atol=1e-12)
 
 
+def test_biased_prefill_continues_as_biased_decode():
+    # with loss-free balancing biases, prefill_cache + one biased decode step
+    # is the biased layer's definition at the next token
+    B, T, H, K, d, base = 2, 29, 6, 2, 8, 1e4
+    g = np.random.default_rng(22)
+    logits = g.standard_normal((B, T, H)).astype(np.float32)
+    bias = (g.standard_normal(H) * 0.1).astype(np.float32)
+    q, k, v = (g.standard_normal((B, H, T, d)) for _ in range(3))
+    full = O.prefill(logits, q, k, v, K, base, form="definition", bias=bias)
+    assert (full["topk_idx"] != O.select_heads(logits, K)).any()
+    for Tp in (0, 9, T - 1):
+        topk, _ = O.select_heads_biased(logits[:, :Tp], bias, K)
+        kc, vc, n = O.prefill_cache(k[:, :, :Tp], v[:, :, :Tp], topk, H, base)
+        res = O.decode_step(logits[:, Tp], q[:, :, Tp], k[:, :, Tp], v[:, :, Tp],
+                            lambda b, h, nn: kc[b, h, :nn], lambda b, h, nn: vc[b, h, :nn],
+                            n, K, base, bias=bias)
+        np.testing.assert_allclose(res["out"], full["out"][:, Tp], atol=1e-12)
+        np.testing.assert_array_equal(res["topk_idx"], full["topk_idx"][:, Tp])
+
+
 def test_decode_reads_only_selected_caches_and_counts():
     B, H, K, d = 3, 8, 2, 4
     g = np.random.default_rng(14)
