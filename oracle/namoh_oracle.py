@@ -37,7 +37,7 @@ Readings where the paper is silent (each also listed in the design notes):
 * R6 decode caches hold keys after rotation, in rank order; the new token
   takes rank n (its head's current length) and attends to itself.
 * R7 sequences of a batch are independent (ranks restart per sequence).
-* R8 loss-free balancing selects by float32(a + b) with the affinities a
+* R12 loss-free balancing selects by float32(a + b) with the affinities a
   formed in float64; equal scores go to the lower head index; the gates are
   a (the paper fixes no precision for the selection; one rounding step both
   sides take keeps the decision reproducible).
@@ -105,13 +105,13 @@ def route_gates(logits: np.ndarray, topk_idx: np.ndarray, mode: int) -> np.ndarr
 
 # ----------------------------------------------------------------------------
 # Loss-free balancing: App. "Auxiliary-Loss-Free Balancing",
-# Eqs. (namoh-biased-routing), (namoh-loss-free); reading R8
+# Eqs. (namoh-biased-routing), (namoh-loss-free); reading R12
 
 def select_heads_biased(logits: np.ndarray, bias: np.ndarray, K: int):
     """S_K(t) = TopK_i(a_{t,i} + b_i) with a_t = softmax over the H logits;
     gates g = a of the selected heads, not renormalised.
 
-    The score is decided in one fixed precision on every side (reading R8):
+    The score is decided in one fixed precision on every side (reading R12):
     a in float64 (exp of l - max, divided by the sum), then a + b rounded
     once to float32; heads ordered by score descending, then head index
     ascending.  Returns topk int32 [..., K] and gates float64 [..., K]."""

@@ -272,40 +272,28 @@ NAMOH_DEV bool my_item(const WorkItem* __restrict__ items, const int32_t* __rest
 }
 
 // ---------------------------------------------------------------------------
-// RoPE table table[p * (d/2) + j] = (cos, sin)(p * base^(-2j/d)) for p < P,
-// the angles formed and reduced in double.  P (longest segment for
-// head-relative positions, T for global ones) is recomputed by every
-// workgroup from seg_offsets.
-constexpr int kTableThreads = 256, kTableBlocks = 64;
-__global__ __launch_bounds__(kTableThreads) void k_rope_table(
-    const int32_t* __restrict__ seg_offsets, int BH, int T, int rope_mode, int d,
-    double log_base, float2* __restrict__ table) {
-  __shared__ int s_p[kTableThreads / kWave];
+// RoPE table table[p * (d/2) + j] = (cos, sin)(p * base^(-2j/d)) for p < T,
+// the angles formed and reduced in double.  Every position a rotation can
+// use (a rank below the longest segment, or a token index) is below T, so
+// the table does not wait for the routing; kTableEntries entries per thread.
+constexpr int kTableThreads = 256, kTableEntries = 4;
+__global__ __launch_bounds__(kTableThreads) void k_rope_table(int T, int d, double log_base,
+                                                             float2* __restrict__ table) {
   __shared__ double s_theta[64];
   const int half = d / 2;
   const int tid = thread_x();
   if (tid < half) s_theta[tid] = exp(-(2.0 * tid / d) * log_base);
-  int P = T;
-  if (rope_mode == 0) {
-    int mx = 0;
-    for (int s = tid; s < BH; s += kTableThreads)
-      mx = max(mx, min(seg_offsets[s + 1] - seg_offsets[s], T));
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) mx = max(mx, __shfl_xor(mx, o));
-    if (tid % kWave == 0) s_p[tid / kWave] = mx;
-  }
   __syncthreads();
-  if (rope_mode == 0) {
-    P = 0;
+  const size_t total = static_cast<size_t>(T) * half;
+  const size_t i0 = static_cast<size_t>(block_x()) * kTableThreads * kTableEntries + tid;
 #pragma unroll
-    for (int w = 0; w < kTableThreads / kWave; ++w) P = max(P, s_p[w]);
-  }
-  const size_t total = static_cast<size_t>(P) * half;
-  const size_t stride = static_cast<size_t>(kTableBlocks) * kTableThreads;
-  for (size_t i = static_cast<size_t>(block_x()) * kTableThreads + tid; i < total; i += stride) {
-    const int p = static_cast<int>(i / half);
-    const int j = static_cast<int>(i - static_cast<size_t>(p) * half);
-    table[i] = rope_cos_sin(static_cast<double>(p) * s_theta[j]);
+  for (int e = 0; e < kTableEntries; ++e) {
+    const size_t i = i0 + static_cast<size_t>(e) * kTableThreads;
+    if (i < total) {
+      const int p = static_cast<int>(i / half);
+      const int j = static_cast<int>(i - static_cast<size_t>(p) * half);
+      table[i] = rope_cos_sin(static_cast<double>(p) * s_theta[j]);
+    }
   }
 }
 
@@ -1250,9 +1238,12 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   const int BM = block_queries(d, dtype);
   const int Nr = B * T * K;
   const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
-  if (rope_mode != 2)
-    k_rope_table<<<kTableBlocks, kTableThreads, 0, st>>>(seg_offsets, B * H, T, rope_mode, d, log_base,
-                                               w.table);
+  if (rope_mode != 2) {
+    const size_t entries = static_cast<size_t>(T) * (d / 2);
+    const size_t per_block = static_cast<size_t>(kTableThreads) * kTableEntries;
+    k_rope_table<<<static_cast<unsigned>((entries + per_block - 1) / per_block), kTableThreads, 0,
+                   st>>>(T, d, log_base, w.table);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (use_mfma(d, dtype)) {
