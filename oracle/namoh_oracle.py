@@ -56,6 +56,7 @@ __all__ = [
     "rope_rotate", "visibility_mask", "attention_definition",
     "attention_gathered", "combine_packed", "combine_dense", "prefill",
     "prefill_rows", "prefill_cache", "decode_step", "brute_force_layer", "interaction_count",
+    "attention_backward", "gates_backward",
     "shared_head_counts",
 ]
 
@@ -380,6 +381,108 @@ def prefill_rows(q, k, v, topk_idx, gates, H, rope_base, b, tokens,
             hs[r, kk] = p @ np.asarray(v[b, h][src], dtype=np.float64)
             o[r] += gates[b, t, kk] * hs[r, kk]
     return o, hs
+
+
+# ----------------------------------------------------------------------------
+# Backward of the layer (training path): the exact gradient of Eqs.
+# (namoh-gates), (namoh-head-rope), (namoh-attention) with the selection S_K
+# held fixed (it is piecewise constant), for the packed varlen attention of
+# Sec. 3.2 "Efficient execution" that training also uses.
+
+def _unrotate(dx, pos, base):
+    """Gradient through x -> x R(p): dx R(p)^T, i.e. the rotation by -p."""
+    return dx if pos is None else rope_rotate(dx, -np.asarray(pos, dtype=np.float64), base)
+
+
+def attention_backward(q, k, v, gates, seg_offsets, perm_token, slot_pos, H, rope_base,
+                       dout, rope_mode=ROPE_HEAD_RELATIVE, scale=None):
+    """Gradients of o = combine(attention(q, k, v), gates) for the upstream
+    gradient dout [B,T,d].
+
+    Per segment, with the rotated rows Q~, K~ and S = Q~ K~^T scale (causal),
+    P = softmax(S), O = P V, dO_r = g_r dout_t (g_r the gate of packed row r):
+    dV = P^T dO, dP = dO V^T, dS = P (dP - rowsum(dO O)), dQ~ = dS K~ scale,
+    dK~ = dS^T Q~ scale, then dq = dQ~ R^T (rotation by minus the angle)
+    scattered to the token rows; dgates[t,k] = <h(t, topk_k), dout_t>.
+    Returns dq, dk, dv float64 [B,H,T,d] (zero where the token is not routed
+    to the head) and dgates float64 [B,T,K]."""
+    B, _, T, d = q.shape
+    K = slot_pos.shape[-1]
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    N = int(seg_offsets[-1])
+    dout = np.asarray(dout, dtype=np.float64)
+    # packed gate and upstream row of every packed position
+    g_pack = np.zeros(N)
+    t_pack = np.zeros(N, dtype=np.int64)
+    b_pack = np.zeros(N, dtype=np.int64)
+    for b in range(B):
+        for kk in range(K):
+            sl = slot_pos[b, :, kk].astype(np.int64)
+            g_pack[sl] = gates[b, :, kk]
+            t_pack[sl] = np.arange(T)
+            b_pack[sl] = b
+    do_pack = g_pack[:, None] * dout[b_pack, t_pack]
+    dq = np.zeros((B, H, T, d))
+    dk = np.zeros((B, H, T, d))
+    dv = np.zeros((B, H, T, d))
+    h_pack = np.zeros((N, d))
+    for sid in range(B * H):
+        b, h = divmod(sid, H)
+        a, e = int(seg_offsets[sid]), int(seg_offsets[sid + 1])
+        n = e - a
+        if n == 0:
+            continue
+        tok = perm_token[a:e].astype(np.int64)
+        pos = _positions(np.arange(n), tok, rope_mode)
+        qt = _rotate(q[b, h, tok], pos, rope_base)
+        kt = _rotate(k[b, h, tok], pos, rope_base)
+        vv = np.asarray(v[b, h, tok], dtype=np.float64)
+        sc = (qt @ kt.T) * scale
+        causal = np.tril(np.ones((n, n), dtype=bool))
+        sc = np.where(causal, sc, -np.inf)
+        p = np.exp(sc - sc.max(axis=1, keepdims=True))
+        p /= p.sum(axis=1, keepdims=True)
+        o = p @ vv
+        h_pack[a:e] = o
+        dO = do_pack[a:e]
+        dv_s = p.T @ dO
+        dp = dO @ vv.T
+        ds = p * (dp - (dO * o).sum(axis=1, keepdims=True))
+        dqt = ds @ kt * scale
+        dkt = ds.T @ qt * scale
+        dq[b, h, tok] = _unrotate(dqt, pos, rope_base)
+        dk[b, h, tok] = _unrotate(dkt, pos, rope_base)
+        dv[b, h, tok] = dv_s
+    dgates = np.zeros((B, T, K))
+    for kk in range(K):
+        dgates[:, :, kk] = (h_pack[slot_pos[:, :, kk].astype(np.int64)] * dout).sum(axis=-1)
+    return dq, dk, dv, dgates
+
+
+def gates_backward(logits, topk_idx, dgates, mode):
+    """Gradient of the gates (reading R2, or loss-free balancing's affinity
+    gates, which are GATE_SOFTMAX_ALL's) with respect to the router logits,
+    the selection held fixed: SOFTMAX_SELECTED g = softmax of the selected
+    logits, dl_j = g_j (dg_j - sum_k g_k dg_k) on the selected heads, 0
+    elsewhere; SOFTMAX_ALL g_k = a(topk_k), a = softmax of all H logits,
+    dl = a (da - <a, da>) with da the gate gradients placed at their heads.
+    Returns float64 [..., H]."""
+    l = np.asarray(logits, dtype=np.float64)
+    idx = topk_idx.astype(np.int64)
+    dg = np.asarray(dgates, dtype=np.float64)
+    dl = np.zeros_like(l)
+    if mode == GATE_SOFTMAX_SELECTED:
+        g = route_gates(l, topk_idx, mode)
+        val = g * (dg - (g * dg).sum(axis=-1, keepdims=True))
+        np.put_along_axis(dl, idx, val, axis=-1)
+        return dl
+    if mode == GATE_SOFTMAX_ALL:
+        e = np.exp(l - l.max(axis=-1, keepdims=True))
+        a = e / e.sum(axis=-1, keepdims=True)
+        da = np.zeros_like(l)
+        np.put_along_axis(da, idx, dg, axis=-1)
+        return a * (da - (a * da).sum(axis=-1, keepdims=True))
+    raise ValueError("unknown gate mode")
 
 
 # ----------------------------------------------------------------------------

@@ -494,3 +494,110 @@ def test_bias_update_step():
     assert n.sum() == 3 * 37 * 2
     b = O.bias_update(n, np.zeros(7), 0.5, 37, 2)
     assert set(np.unique(b)) <= {-0.5, 0.5}
+
+
+# ----------------------------------------------------------------------------
+# Backward (training path): the exact gradient, pinned by finite differences
+# of the forward oracle and by torch autograd (float64, CPU)
+
+def _bwd_case(seed, B=2, T=11, H=4, K=2, d=8):
+    g = np.random.default_rng(seed)
+    logits = g.standard_normal((B, T, H)).astype(np.float32)
+    q, k, v = (g.standard_normal((B, H, T, d)) for _ in range(3))
+    topk = O.select_heads(logits, K)
+    gates = O.route_gates(logits, topk, O.GATE_SOFTMAX_SELECTED)
+    n, off, perm, slot = O.permutation(topk, H)
+    dout = g.standard_normal((B, T, d))
+    return logits, q, k, v, topk, gates, n, off, perm, slot, dout
+
+
+def _layer(q, k, v, gates, n, off, perm, slot, H, base, rope_mode):
+    hp = O.attention_gathered(q, k, v, n, off, perm, H, base, rope_mode)
+    return O.combine_packed(hp, slot, gates)
+
+
+@pytest.mark.parametrize("rope_mode", [O.ROPE_HEAD_RELATIVE, O.ROPE_GLOBAL, O.ROPE_NONE])
+def test_attention_backward_finite_differences(rope_mode):
+    base = 1e4
+    logits, q, k, v, topk, gates, n, off, perm, slot, dout = _bwd_case(41 + rope_mode)
+    H = q.shape[1]
+    dq, dk, dv, dg = O.attention_backward(q, k, v, gates, off, perm, slot, H, base, dout,
+                                          rope_mode)
+    loss = lambda q_, k_, v_, g_: float((_layer(q_, k_, v_, g_, n, off, perm, slot, H, base,
+                                                 rope_mode) * dout).sum())
+    rng = np.random.default_rng(5)
+    eps = 1e-6
+    for name, x, grad in (("q", q, dq), ("k", k, dk), ("v", v, dv), ("g", gates, dg)):
+        for _ in range(12):
+            idx = tuple(rng.integers(0, s) for s in x.shape)
+            xp, xm = x.copy(), x.copy()
+            xp[idx] += eps
+            xm[idx] -= eps
+            args = {"q": q, "k": k, "v": v, "g": gates}
+            fp = loss(*[xp if a == name else args[a] for a in ("q", "k", "v", "g")])
+            fm = loss(*[xm if a == name else args[a] for a in ("q", "k", "v", "g")])
+            fd = (fp - fm) / (2 * eps)
+            assert abs(fd - grad[idx]) <= 1e-7 + 1e-6 * abs(fd), (name, idx, fd, grad[idx])
+    # rows of tokens not routed to a head get no gradient
+    m = O.membership(topk, H)
+    assert not dq[~m.transpose(0, 2, 1)].any() and not dk[~m.transpose(0, 2, 1)].any()
+
+
+@pytest.mark.parametrize("mode", [O.GATE_SOFTMAX_SELECTED, O.GATE_SOFTMAX_ALL])
+def test_gates_backward_finite_differences(mode):
+    g = np.random.default_rng(43 + mode)
+    B, T, H, K = 2, 7, 6, 3
+    logits = g.standard_normal((B, T, H))
+    topk = O.select_heads(logits.astype(np.float32), K)
+    dg = g.standard_normal((B, T, K))
+    dl = O.gates_backward(logits, topk, dg, mode)
+    eps = 1e-6
+    for b in range(B):
+        for t in range(T):
+            for h in range(H):
+                lp, lm = logits.copy(), logits.copy()
+                lp[b, t, h] += eps
+                lm[b, t, h] -= eps
+                fd = ((O.route_gates(lp, topk, mode) - O.route_gates(lm, topk, mode)) * dg).sum()
+                assert abs(fd / (2 * eps) - dl[b, t, h]) <= 1e-8
+
+
+def test_attention_backward_matches_autograd():
+    torch = pytest.importorskip("torch")
+    base = 5e5
+    logits, q, k, v, topk, gates, n, off, perm, slot, dout = _bwd_case(44, B=2, T=37, H=5, K=2,
+                                                                         d=16)
+    H, d = q.shape[1], q.shape[-1]
+    dq, dk, dv, dg = O.attention_backward(q, k, v, gates, off, perm, slot, H, base, dout)
+    tq, tk, tv, tg = (torch.tensor(x, dtype=torch.float64, requires_grad=True)
+                      for x in (q, k, v, gates))
+    theta = base ** (-2.0 * torch.arange(d // 2, dtype=torch.float64) / d)
+
+    def rot(x, p):
+        ang = p[:, None].to(torch.float64) * theta
+        c, s = torch.cos(ang), torch.sin(ang)
+        x1, x2 = x[:, :d // 2], x[:, d // 2:]
+        return torch.cat([x1 * c - x2 * s, x2 * c + x1 * s], dim=1)
+
+    hp = [None] * int(off[-1])
+    for sid in range(len(off) - 1):
+        b, h = divmod(sid, H)
+        a, e = int(off[sid]), int(off[sid + 1])
+        if a == e:
+            continue
+        tok = torch.tensor(perm[a:e].astype(np.int64))
+        pos = torch.arange(e - a)
+        qq, kk = rot(tq[b, h, tok], pos), rot(tk[b, h, tok], pos)
+        sc = qq @ kk.T / np.sqrt(d)
+        sc = sc.masked_fill(~torch.tril(torch.ones(e - a, e - a, dtype=torch.bool)), float("-inf"))
+        o = torch.softmax(sc, dim=1) @ tv[b, h, tok]
+        for r in range(e - a):
+            hp[a + r] = o[r]
+    hp = torch.stack(hp)
+    out = sum(tg[:, :, kk, None] * hp[torch.tensor(slot[:, :, kk].astype(np.int64))]
+              for kk in range(slot.shape[-1]))
+    (out * torch.tensor(dout)).sum().backward()
+    np.testing.assert_allclose(tq.grad.numpy(), dq, atol=1e-11)
+    np.testing.assert_allclose(tk.grad.numpy(), dk, atol=1e-11)
+    np.testing.assert_allclose(tv.grad.numpy(), dv, atol=1e-11)
+    np.testing.assert_allclose(tg.grad.numpy(), dg, atol=1e-11)
