@@ -165,6 +165,47 @@ namoh_status namoh_attn_fwd(const void* q, const void* k, const void* v,
                             void* stream);
 
 /* ------------------------------------------------------------------------
+ * Backward of the layer (training path; Sec. 3.2 "Efficient execution":
+ * training runs the same packed varlen attention).  The exact gradient of
+ * o = namoh_attn_fwd(q, k, v, routing) with the selection held fixed, for
+ * an upstream gradient dout:
+ *   per (b, h) segment, with the rotated rows Q~, K~, S = Q~ K~^T scale
+ *   (causal), P = softmax(S), O = P V, dO_r = g_r dout_t:
+ *   dV = P^T dO, dS = P (dO V^T - rowsum(dO O)), dQ~ = dS K~ scale,
+ *   dK~ = dS^T Q~ scale, dq = dQ~ R^T (the rotation by minus the angle);
+ *   dgates[b,t,k] = <h(t, topk_idx[b,t,k]), dout_t>.
+ * The forward statistics are recomputed (fp32 arithmetic throughout), so
+ * nothing from the forward call is needed.
+ *
+ * In:  q, k, v [B, H, T, d] `dtype`; rope and scale as for namoh_attn_fwd;
+ *      topk_idx, gates, seg_offsets, perm_token from namoh_route (any gate
+ *      mode, or namoh_route_biased); dout float32 [B, T, d].
+ * Out: dq, dk, dv float32 [B, H, T, d] (rows of tokens not routed to the
+ *      head are zero); dgates float32 [B, T, K].  B*H <= 65535.
+ * ---------------------------------------------------------------------- */
+size_t namoh_attn_bwd_workspace_size(int B, int T, int H, int K, int d_head);
+
+namoh_status namoh_attn_bwd(const void* q, const void* k, const void* v, int dtype,
+                            int B, int T, int H, int K, int d_head, float rope_base,
+                            int rope_mode, float softmax_scale, const int32_t* topk_idx,
+                            const float* gates, const int32_t* seg_offsets,
+                            const int32_t* perm_token, const float* dout, float* dq,
+                            float* dk, float* dv, float* dgates, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/* Gradient of the gates with respect to the router logits, the selection
+ * held fixed (Sec. 3.1, Eq. namoh-gates; the router learns through the
+ * gates).  gate_mode SOFTMAX_SELECTED: dl_j = g_j (dg_j - sum_k g_k dg_k)
+ * on the selected heads, 0 elsewhere; SOFTMAX_ALL (also the gates of
+ * namoh_route_biased): dl = a (da - <a, da>), a = softmax of all H logits,
+ * da = dgates placed at the selected heads.
+ * In:  logits float32 [B, T, H], topk_idx, gates, dgates [B, T, K].
+ * Out: dlogits float32 [B, T, H].  No workspace. */
+namoh_status namoh_route_bwd(const float* logits, const int32_t* topk_idx,
+                             const float* gates, const float* dgates, int B, int T,
+                             int H, int K, int gate_mode, float* dlogits, void* stream);
+
+/* ------------------------------------------------------------------------
  * Prefill -> decode hand-off (Sec. 3.2, efficient execution: decoding reads
  * and extends only the active heads' caches; Eq. namoh-head-rope: keys are
  * cached after rotation, in rank order).  For every (b, h) with n = n_{b,h}

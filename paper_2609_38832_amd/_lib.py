@@ -30,7 +30,7 @@ ROPE_HEAD_RELATIVE, ROPE_GLOBAL, ROPE_NONE = 0, 1, 2
 EXPORTED = (
     "namoh_route_workspace_size", "namoh_route", "namoh_route_biased", "namoh_route_bias_update",
     "namoh_attn_fwd_workspace_size", "namoh_attn_fwd",
-    "namoh_prefill_cache",
+    "namoh_prefill_cache", "namoh_attn_bwd_workspace_size", "namoh_attn_bwd", "namoh_route_bwd",
     "namoh_decode_workspace_size", "namoh_decode_step", "namoh_decode_step_biased",
     "namoh_status_string", "namoh_last_error", "namoh_version",
     "namoh_profile_enable", "namoh_profile_read",
@@ -51,6 +51,10 @@ _SIGS = {
                             _P, _P, _P, _P, _P, _I, _P, _P, _S, _P]),
     "namoh_prefill_cache": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _P, _P, _P, _P, _P,
                                  _I, _P]),
+    "namoh_attn_bwd_workspace_size": (_S, [_I, _I, _I, _I, _I]),
+    "namoh_attn_bwd": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F, _P, _P, _P, _P, _P,
+                            _P, _P, _P, _P, _P, _S, _P]),
+    "namoh_route_bwd": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "namoh_decode_workspace_size": (_S, [_I, _I, _I, _I, _I]),
     "namoh_decode_step": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I,
                                _F, _I, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
@@ -237,6 +241,45 @@ def prefill_cache(k: torch.Tensor, v: torch.Tensor, r: dict, K: int, rope_base: 
                                     float(rope_base), rope_mode, _ptr(r["seg_offsets"]),
                                     _ptr(r["perm_token"]), _ptr(k_cache), _ptr(v_cache),
                                     _ptr(cache_len), cap, _stream(k.device)))
+
+
+def attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K: int,
+             rope_base: float, dout: torch.Tensor, rope_mode: int = ROPE_HEAD_RELATIVE,
+             softmax_scale: float = 0.0, ws: Optional[torch.Tensor] = None) -> dict:
+    """namoh_attn_bwd: gradients dq, dk, dv [B, H, T, d] and dgates [B, T, K]
+    (float32) for the upstream gradient dout float32 [B, T, d]."""
+    _need_cuda(q, k, v, dout)
+    B, H, T, d = q.shape
+    if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
+        raise ValueError("q, k, v must share shape and dtype")
+    if dout.dtype != torch.float32 or tuple(dout.shape) != (B, T, d):
+        raise ValueError("dout must be float32 [B, T, d]")
+    dev = q.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    out = {"dq": torch.empty(B, H, T, d, **f32), "dk": torch.empty(B, H, T, d, **f32),
+           "dv": torch.empty(B, H, T, d, **f32), "dgates": torch.empty(B, T, K, **f32)}
+    if ws is None:
+        ws = workspace(int(lib().namoh_attn_bwd_workspace_size(B, T, H, K, d)), dev)
+    check(lib().namoh_attn_bwd(_ptr(q), _ptr(k), _ptr(v), dtype_code(q.dtype), B, T, H, K, d,
+                               float(rope_base), rope_mode, float(softmax_scale),
+                               _ptr(routing["topk_idx"]), _ptr(routing["gates"]),
+                               _ptr(routing["seg_offsets"]), _ptr(routing["perm_token"]),
+                               _ptr(dout), _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]),
+                               _ptr(out["dgates"]), _ptr(ws), ws.numel(), _stream(dev)))
+    return out
+
+
+def route_bwd(logits: torch.Tensor, routing: dict, dgates: torch.Tensor,
+              gate_mode: int = GATE_SOFTMAX_SELECTED) -> torch.Tensor:
+    """namoh_route_bwd: d logits [B, T, H] from the gate gradients."""
+    _need_cuda(logits, dgates)
+    B, T, H = logits.shape
+    K = dgates.shape[-1]
+    dl = torch.empty(B, T, H, dtype=torch.float32, device=logits.device)
+    check(lib().namoh_route_bwd(_ptr(logits), _ptr(routing["topk_idx"]), _ptr(routing["gates"]),
+                                _ptr(dgates), B, T, H, K, gate_mode, _ptr(dl),
+                                _stream(logits.device)))
+    return dl
 
 
 def decode_workspace_size(B, H, K, d, cap) -> int:

@@ -248,6 +248,70 @@ namoh_status namoh_prefill_cache(const void* k, const void* v, int dtype, int B,
                                                 static_cast<hipStream_t>(stream)));
 }
 
+size_t namoh_attn_bwd_workspace_size(int B, int T, int H, int K, int d_head) {
+  if (check_sizes(B, T, H, K) != NAMOH_OK || check_head_width(d_head) != NAMOH_OK) return 0;
+  return namoh::attn_bwd_workspace_bytes(B, T, H, K, d_head);
+}
+
+namoh_status namoh_attn_bwd(const void* q, const void* k, const void* v, int dtype, int B, int T,
+                            int H, int K, int d_head, float rope_base, int rope_mode,
+                            float softmax_scale, const int32_t* topk_idx, const float* gates,
+                            const int32_t* seg_offsets, const int32_t* perm_token,
+                            const float* dout, float* dq, float* dk, float* dv, float* dgates,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  namoh_status s;
+  if ((s = check_sizes(B, T, H, K)) != NAMOH_OK) return s;
+  if ((s = check_head_width(d_head)) != NAMOH_OK) return s;
+  REQUIRE(dtype == NAMOH_F32 || dtype == NAMOH_BF16, "unknown dtype %d", dtype);
+  REQUIRE(rope_mode == NAMOH_ROPE_HEAD_RELATIVE || rope_mode == NAMOH_ROPE_GLOBAL ||
+              rope_mode == NAMOH_ROPE_NONE,
+          "unknown rope_mode %d", rope_mode);
+  REQUIRE(rope_mode == NAMOH_ROPE_NONE || (std::isfinite(rope_base) && rope_base > 0.f),
+          "rope_base must be finite and > 0 (got %g)", static_cast<double>(rope_base));
+  REQUIRE(!std::isnan(softmax_scale) && !std::isinf(softmax_scale), "softmax_scale must be finite");
+  REQUIRE(static_cast<long long>(B) * H * T * d_head < (1ll << 40), "q/k/v too large");
+  REQUIRE(B * H <= 65535, "B*H = %d segments exceed the backward grid", B * H);
+  REQUIRE_PTR(q, 16);
+  REQUIRE_PTR(k, 16);
+  REQUIRE_PTR(v, 16);
+  REQUIRE_PTR(topk_idx, 4);
+  REQUIRE_PTR(gates, 4);
+  REQUIRE_PTR(seg_offsets, 4);
+  REQUIRE_PTR(perm_token, 4);
+  REQUIRE_PTR(dout, 16);
+  REQUIRE_PTR(dq, 16);
+  REQUIRE_PTR(dk, 16);
+  REQUIRE_PTR(dv, 16);
+  REQUIRE_PTR(dgates, 4);
+  if ((s = check_workspace(workspace, workspace_bytes,
+                           namoh::attn_bwd_workspace_bytes(B, T, H, K, d_head))) != NAMOH_OK)
+    return s;
+  const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
+  clear_hip_error();
+  return hip_status(namoh::launch_attn_bwd(q, k, v, dtype, B, T, H, K, d_head, rope_base,
+                                           rope_mode, scale, topk_idx, gates, seg_offsets,
+                                           perm_token, dout, dq, dk, dv, dgates, workspace,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+namoh_status namoh_route_bwd(const float* logits, const int32_t* topk_idx, const float* gates,
+                             const float* dgates, int B, int T, int H, int K, int gate_mode,
+                             float* dlogits, void* stream) {
+  namoh_status s;
+  if ((s = check_sizes(B, T, H, K)) != NAMOH_OK) return s;
+  REQUIRE(gate_mode == NAMOH_GATE_SOFTMAX_SELECTED || gate_mode == NAMOH_GATE_SOFTMAX_ALL,
+          "unknown gate_mode %d", gate_mode);
+  REQUIRE_PTR(logits, 4);
+  REQUIRE_PTR(topk_idx, 4);
+  REQUIRE_PTR(gates, 4);
+  REQUIRE_PTR(dgates, 4);
+  REQUIRE_PTR(dlogits, 4);
+  clear_hip_error();
+  return hip_status(namoh::launch_route_bwd(logits, topk_idx, gates, dgates, B, T, H, K,
+                                            gate_mode, dlogits,
+                                            static_cast<hipStream_t>(stream)));
+}
+
 size_t namoh_decode_workspace_size(int B, int H, int K, int d_head, int cap) {
   if (check_sizes(B, 1, H, K) != NAMOH_OK || check_head_width(d_head) != NAMOH_OK || cap < 1)
     return 0;

@@ -65,4 +65,16 @@ hipError_t launch_prefill_cache(const void* k, const void* v, int dtype, int B, 
                                 void* k_cache, void* v_cache, int32_t* cache_len, int cap,
                                 hipStream_t st);
 
+// ---- backward (bwd.hip) ---------------------------------------------------
+size_t attn_bwd_workspace_bytes(int B, int T, int H, int K, int d);
+hipError_t launch_attn_bwd(const void* q, const void* k, const void* v, int dtype, int B, int T,
+                           int H, int K, int d, float rope_base, int rope_mode, float scale,
+                           const int32_t* topk_idx, const float* gates,
+                           const int32_t* seg_offsets, const int32_t* perm_token,
+                           const float* dout, float* dq, float* dk, float* dv, float* dgates,
+                           void* ws, hipStream_t st);
+hipError_t launch_route_bwd(const float* logits, const int32_t* topk_idx, const float* gates,
+                            const float* dgates, int B, int T, int H, int K, int gate_mode,
+                            float* dlogits, hipStream_t st);
+
 }  // namespace namoh

@@ -172,6 +172,33 @@ def test_decode_biased_rejects(lib):
     assert lib.namoh_decode_step_biased(*bad) == 1              # GLOBAL needs seq_pos
 
 
+def _bwd(lib, dtype=1, B=2, T=64, H=8, K=2, d=64, base=1e4, rope=0, scale=0.0, q=fake(0),
+         dout=fake(5), dq=fake(6), dg=fake(9), wsb=1 << 30, ws=fake(10)):
+    return lib.namoh_attn_bwd(q, fake(1), fake(2), dtype, B, T, H, K, d, base, rope, scale,
+                              fake(3), fake(4), fake(11), fake(12), dout, dq, fake(7), fake(8),
+                              dg, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(d=48), 2), (dict(dtype=4), 1), (dict(rope=3), 1), (dict(base=0.0), 1),
+    (dict(scale=float("inf")), 1), (dict(q=None), 1), (dict(dout=P(A + 4)), 1), (dict(dq=None), 1),
+    (dict(dg=P(A + 1)), 1), (dict(wsb=64), 3), (dict(ws=None), 3), (dict(K=9), 1),
+    (dict(B=64, H=1025, K=1), 1), (dict(B=1024, H=64, T=8, K=1), 1),   # H > 64; B*H > 65535
+])
+def test_attn_bwd_rejects(lib, kw, code):
+    assert _bwd(lib, **kw) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(gate=2), 1), (dict(logits=None), 1), (dict(dl=P(A + 2)), 1), (dict(K=0), 1),
+])
+def test_route_bwd_rejects(lib, kw, code):
+    a = dict(logits=fake(0), gate=0, dl=fake(4), K=2)
+    a.update(kw)
+    assert lib.namoh_route_bwd(a["logits"], fake(1), fake(2), fake(3), 2, 16, 8, a["K"],
+                               a["gate"], a["dl"], None) == code
+
+
 def test_workspace_queries(lib):
     assert lib.namoh_route_workspace_size(0, 10, 8, 2) == 0
     assert lib.namoh_route_workspace_size(1, 10, 8, 2) > 0

@@ -161,6 +161,78 @@ def test_prefill_biased_routing():
 
 
 # ----------------------------------------------------------------------------
+# backward (training path)
+
+def _check_grad(got, ref, what, rel=2e-4):
+    # fp32 arithmetic on exact inputs, reductions over up to a few thousand
+    # terms: within rel of the tensor's largest gradient, or of the element
+    got = np.asarray(got, dtype=np.float64)
+    assert np.isfinite(got).all(), f"{what}: non-finite"
+    scale = np.abs(ref).max() + 1e-30
+    bad = np.abs(got - ref) > rel * scale + rel * np.abs(ref)
+    assert not bad.any(), f"{what}: {bad.sum()} elements off, max err {np.abs(got - ref).max():.3e} (scale {scale:.3e})"
+    return float(np.abs(got - ref).max() / scale)
+
+
+BWD = {
+    "bf16_d64_rel": (W.WORKLOADS[2].with_(B=2, T=700, H=4, K=2), O.ROPE_HEAD_RELATIVE),
+    "bf16_d128_global": (W.WORKLOADS[3].with_(B=1, T=900, H=4, K=2), O.ROPE_GLOBAL),
+    "bf16_d128_rel": (W.WORKLOADS[3].with_(B=2, T=500, H=8, K=3), O.ROPE_HEAD_RELATIVE),
+    "f32_d32_none": (W.WORKLOADS[1].with_(B=2, T=400, H=4, K=2), O.ROPE_NONE),
+    "f32_d64_dense": (W.WORKLOADS[2].with_(B=1, T=300, H=4, K=4, dtype="f32"), O.ROPE_HEAD_RELATIVE),
+    "skewed_long": (W.WORKLOADS[4].with_(B=1, T=1600, H=8, K=1), O.ROPE_HEAD_RELATIVE),
+}
+
+
+@pytest.mark.parametrize("name", list(BWD))
+def test_attn_bwd_parity(name):
+    w, rope_mode = BWD[name]
+    say(f"backward {name}: {w}")
+    inp = W.prefill_inputs(w)
+    lg = torch.from_numpy(inp["logits"]).to(DEV)
+    q, k, v = (to_dev(inp[x], w.dtype) for x in ("q", "k", "v"))
+    r = L.route(lg, w.K)
+    dout = np.random.default_rng(77).standard_normal((w.B, w.T, w.d)).astype(np.float32)
+    g = L.attn_bwd(q, k, v, r, w.K, w.rope_base, torch.from_numpy(dout).to(DEV), rope_mode)
+    torch.cuda.synchronize()
+    f = _f64(inp, w)
+    ref = _oracle_routing(inp, w)
+    dq, dk, dv, dg = O.attention_backward(f["q"], f["k"], f["v"], ref["gates"], ref["seg_offsets"],
+                                          ref["perm_token"], ref["slot_pos"], w.H, w.rope_base,
+                                          dout.astype(np.float64), rope_mode)
+    errs = [_check_grad(g["dq"].cpu().numpy(), dq, "dq"), _check_grad(g["dk"].cpu().numpy(), dk, "dk"),
+            _check_grad(g["dv"].cpu().numpy(), dv, "dv"),
+            _check_grad(g["dgates"].cpu().numpy(), dg, "dgates")]
+    say(f"  rel max err dq {errs[0]:.1e} dk {errs[1]:.1e} dv {errs[2]:.1e} dgates {errs[3]:.1e}")
+    # rows of tokens not routed to the head are exactly zero
+    m = O.membership(ref["topk_idx"], w.H).transpose(0, 2, 1)
+    assert not g["dq"].cpu().numpy()[~m].any()
+
+
+@pytest.mark.parametrize("gate_mode", [O.GATE_SOFTMAX_SELECTED, O.GATE_SOFTMAX_ALL])
+def test_route_bwd_parity(gate_mode):
+    # router gradient fed by the GPU's own gate gradients (the training chain)
+    w = W.WORKLOADS[2].with_(B=2, T=300)
+    say(f"route backward gate_mode={gate_mode}")
+    inp = W.prefill_inputs(w)
+    lg = torch.from_numpy(inp["logits"]).to(DEV)
+    q, k, v = (to_dev(inp[x], w.dtype) for x in ("q", "k", "v"))
+    r = L.route(lg, w.K, gate_mode)
+    dout = np.random.default_rng(78).standard_normal((w.B, w.T, w.d)).astype(np.float32)
+    g = L.attn_bwd(q, k, v, r, w.K, w.rope_base, torch.from_numpy(dout).to(DEV))
+    dl = L.route_bwd(lg, r, g["dgates"], gate_mode)
+    torch.cuda.synchronize()
+    f = _f64(inp, w)
+    ref = _oracle_routing(inp, w, gate_mode)
+    _, _, _, dg = O.attention_backward(f["q"], f["k"], f["v"], ref["gates"], ref["seg_offsets"],
+                                       ref["perm_token"], ref["slot_pos"], w.H, w.rope_base,
+                                       dout.astype(np.float64))
+    dl_ref = O.gates_backward(inp["logits"], ref["topk_idx"], dg, gate_mode)
+    e = _check_grad(dl.cpu().numpy(), dl_ref, "dlogits", rel=1e-3)
+    say(f"  rel max err dlogits {e:.1e}")
+
+
+# ----------------------------------------------------------------------------
 # prefill: whole outputs at sizes the oracle finishes quickly
 
 MID = {
