@@ -31,6 +31,7 @@
 
 #include "common.h"
 #include "internal.h"
+#include "tile.h"
 
 namespace namoh {
 
@@ -406,7 +407,8 @@ __global__ __launch_bounds__(256) void k_bwd_scatter(
   if (t < 0 || t >= T || s < 0 || s >= BH) return;
   const int rank = r - seg_offsets[s];
   const int b = s / H;
-  if (j0 == 0 && kslot[r] >= 0) dgates[(static_cast<size_t>(b) * T + t) * K + kslot[r]] = dgp[r];
+  const int ks = kslot[r];
+  if (j0 == 0 && ks >= 0 && ks < K) dgates[(static_cast<size_t>(b) * T + t) * K + ks] = dgp[r];
   const size_t src = static_cast<size_t>(r) * D;
   const size_t dst = (static_cast<size_t>(s) * T + t) * D;
   const double pos = rope_mode == 0 ? rank : t;
@@ -428,6 +430,575 @@ __global__ __launch_bounds__(256) void k_bwd_scatter(
     dk[dst + j + D / 2] = k2 * cs - k1 * sn;
     dv[dst + j] = dVp[src + j];
     dv[dst + j + D / 2] = dVp[src + j + D / 2];
+  }
+}
+
+// ===========================================================================
+// bf16 MFMA path (d = 64 or 128).
+//
+// The forward (launch_attn_stats) leaves the rotated key tiles Kp, the
+// transposed value tiles Vt, the work list, h and the log-sum-exp of every
+// row.  k_bwd_pack adds, in the same numbering of 64-row tiles (row r of
+// segment s at packed row 64 * seg_tile0 + r, rows past n zero):
+//   Qs  = bf16(q~ * scale * log2 e), exactly the forward's query operand;
+//   dO  = bf16(g * dout);  Vp = v;  (row-major, like Kp)
+//   Qt, dOt, Kt: Qs, dO, Kp transposed per tile with the 16-row permutation
+//   of tile.h (like Vt);
+//   LD  = (lse, D) per row, D = <dO, h>; (+inf, 0) past n, so padding rows
+//   get zero probabilities.
+// k_bwd_dq (one wave per 32 queries, key tiles streamed): S^T - lse and
+// dP^T - D start from the accumulators, dS^T = exp2(S^T - lse) (dP^T - D),
+// dQ^T += Kt dS^T.  k_bwd_dkdv (one wave per 32 keys, query tiles
+// streamed from the key block on): S - lse, dP - D, dV^T += dOt P,
+// dK^T += Qt dS.  Both take the forward's work list (heaviest first); the
+// key side reads item (s, qb) as key block ceil(n / 128) - 1 - qb, whose work
+// (the later queries) is what the query block's was (the earlier keys).
+constexpr int kBwdPackThreads = 256;
+constexpr int kBwdMfmaThreads = 256;   // 4 waves of 32 rows: 128-row blocks
+constexpr int kBwdMfmaBlock = 128;
+constexpr float kLn2 = 0.6931471805599453f;
+
+template <int D>
+struct BwdPackLds {
+  uint16_t t[3][kBN][D + 8];   // q, dO, k tiles for the transposes
+  int off[kBwdSegLds + 1];
+};
+
+template <int D>
+__global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
+    const float* __restrict__ dout, const int32_t* __restrict__ topk_idx,
+    const float* __restrict__ gates, const int32_t* __restrict__ seg_offsets,
+    const int32_t* __restrict__ perm_token, const float2* __restrict__ table,
+    const uint16_t* __restrict__ Kp, const float* __restrict__ hpack,
+    const float* __restrict__ lse, int BH, int H, int T, int K, int Nr, int rope_mode,
+    float scale_log2, uint16_t* __restrict__ Qs, uint16_t* __restrict__ dO,
+    uint16_t* __restrict__ Vp, uint16_t* __restrict__ Qt, uint16_t* __restrict__ dOt,
+    uint16_t* __restrict__ Kt, float2* __restrict__ LD, float* __restrict__ dgates) {
+  __shared__ __attribute__((aligned(16))) BwdPackLds<D> L;
+  const int gt = block_x();
+  const int tid = thread_x();
+  const bool in_lds = BH <= kBwdSegLds;
+  if (in_lds) {
+    for (int i = tid; i <= BH; i += kBwdPackThreads) L.off[i] = seg_offsets[i];
+    __syncthreads();
+  }
+  const int32_t* off = in_lds ? L.off : seg_offsets;
+  int lo = 0, hi = BH;   // the segment of tile gt: last s with seg_tile0(off[s], s) <= gt
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (seg_tile0(off[mid], mid) <= gt) lo = mid; else hi = mid;
+  }
+  const int s = lo;
+  const int seg0 = off[s];
+  const int n = off[s + 1] - seg0;
+  const int r0 = (gt - seg_tile0(seg0, s)) * kBN;
+  // a tile in a gap between segments, or offsets that are not a packing
+  if (r0 < 0 || r0 >= n || seg0 < 0 || n > T || seg0 + n > Nr) return;
+  const int b = s / H, hh = s - (s / H) * H;
+  const size_t head_base = (static_cast<size_t>(b) * H + hh) * T;
+  const size_t prow0 = static_cast<size_t>(gt) * kBN;
+  // token, k slot and gate of tile row `row` (r < n)
+  auto row_info = [&](int r, int& t, int& ks, float& g) {
+    t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
+    ks = -1;
+    for (int kk = 0; kk < K; ++kk)
+      if (topk_idx[(static_cast<size_t>(b) * T + t) * K + kk] == hh) ks = kk;
+    g = ks >= 0 ? gates[(static_cast<size_t>(b) * T + t) * K + ks] : 0.f;
+  };
+
+  // rows: rotated, scaled queries (as the forward rounds them), gated output
+  // gradients, values; one 8-pair group (j, j + d/2) per unit
+  constexpr int HP = D / 16;
+  for (int u = tid; u < kBN * HP; u += kBwdPackThreads) {
+    const int row = u / HP, c = u - (u / HP) * HP;
+    const int r = r0 + row;
+    uint4 q1 = make_uint4(0, 0, 0, 0), q2 = q1, o1 = q1, o2 = q1, v1 = q1, v2 = q1;
+    if (r < n) {
+      int t, ks;
+      float g;
+      row_info(r, t, ks, g);
+      const uint16_t* qrow = q + (head_base + t) * D;
+      float x1[8], x2[8];
+      unpack8(*reinterpret_cast<const uint4*>(qrow + 8 * c), x1);
+      unpack8(*reinterpret_cast<const uint4*>(qrow + D / 2 + 8 * c), x2);
+      if (rope_mode != 2) {
+        float4 cs[4];
+        load_rope8(cs, table + static_cast<size_t>(rope_mode == 0 ? r : t) * (D / 2) + 8 * c);
+        rope8(x1, x2, cs);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        x1[e] *= scale_log2;
+        x2[e] *= scale_log2;
+      }
+      q1 = pack8(x1);
+      q2 = pack8(x2);
+      const float* drow = dout + (static_cast<size_t>(b) * T + t) * D;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        x1[e] = g * drow[8 * c + e];
+        x2[e] = g * drow[D / 2 + 8 * c + e];
+      }
+      o1 = pack8(x1);
+      o2 = pack8(x2);
+      const uint16_t* vrow = v + (head_base + t) * D;
+      v1 = *reinterpret_cast<const uint4*>(vrow + 8 * c);
+      v2 = *reinterpret_cast<const uint4*>(vrow + D / 2 + 8 * c);
+    }
+    const size_t o = (prow0 + row) * D;
+    *reinterpret_cast<uint4*>(Qs + o + 8 * c) = q1;
+    *reinterpret_cast<uint4*>(Qs + o + D / 2 + 8 * c) = q2;
+    *reinterpret_cast<uint4*>(dO + o + 8 * c) = o1;
+    *reinterpret_cast<uint4*>(dO + o + D / 2 + 8 * c) = o2;
+    *reinterpret_cast<uint4*>(Vp + o + 8 * c) = v1;
+    *reinterpret_cast<uint4*>(Vp + o + D / 2 + 8 * c) = v2;
+    *reinterpret_cast<uint4*>(&L.t[0][row][8 * c]) = q1;
+    *reinterpret_cast<uint4*>(&L.t[0][row][D / 2 + 8 * c]) = q2;
+    *reinterpret_cast<uint4*>(&L.t[1][row][8 * c]) = o1;
+    *reinterpret_cast<uint4*>(&L.t[1][row][D / 2 + 8 * c]) = o2;
+  }
+  constexpr int RG = D / 8;   // 16-byte granules per row
+  for (int u = tid; u < kBN * RG; u += kBwdPackThreads) {
+    const int row = u / RG, gr = u - (u / RG) * RG;
+    *reinterpret_cast<uint4*>(&L.t[2][row][8 * gr]) =
+        *reinterpret_cast<const uint4*>(Kp + (prow0 + row) * D + 8 * gr);
+  }
+  // per row: D = <dO, h> (dO as rounded for the products), the gate
+  // gradient <dout, h>, the log-sum-exp; four lanes per row
+  {
+    static_assert(kBwdPackThreads == 4 * kBN, "four lanes per row");
+    const int row = tid >> 2, part = tid & 3;
+    const int r = r0 + row;
+    float dd = 0.f, dg = 0.f;
+    int ks = -1, t = 0;
+    if (r < n) {
+      float g;
+      row_info(r, t, ks, g);
+      const float* hrow = hpack + static_cast<size_t>(seg0 + r) * D;
+      const float* drow = dout + (static_cast<size_t>(b) * T + t) * D;
+      for (int e = part * (D / 4); e < (part + 1) * (D / 4); ++e) {
+        const float hv = hrow[e], dv = drow[e];
+        dg = fmaf(dv, hv, dg);
+        dd = fmaf(bf16_to_f32(f32_to_bf16(g * dv)), hv, dd);
+      }
+    }
+    dd += __shfl_xor(dd, 1);
+    dd += __shfl_xor(dd, 2);
+    dg += __shfl_xor(dg, 1);
+    dg += __shfl_xor(dg, 2);
+    if (part == 0) {
+      LD[prow0 + row] = r < n ? make_float2(lse[seg0 + r], dd) : make_float2(INFINITY, 0.f);
+      if (r < n && ks >= 0) dgates[(static_cast<size_t>(b) * T + t) * K + ks] = dg;
+    }
+  }
+  __syncthreads();
+  // transposed tiles: position p of each 16-row group holds row
+  // vt_key_of_pos(p), as in the forward's value tiles
+  uint16_t* const dst[3] = {Qt, dOt, Kt};
+#pragma unroll
+  for (int x = 0; x < 3; ++x)
+    for (int u = tid; u < D * (kBN / 8); u += kBwdPackThreads) {
+      const int m = u / (kBN / 8), pg = u - (u / (kBN / 8)) * (kBN / 8);
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t a = L.t[x][vt_key_of_pos(8 * pg + 2 * e)][m];
+        const uint32_t c2 = L.t[x][vt_key_of_pos(8 * pg + 2 * e + 1)][m];
+        w[e] = a | (c2 << 16);
+      }
+      *reinterpret_cast<uint4*>(dst[x] + (static_cast<size_t>(gt) * D + m) * kBN + 8 * pg) =
+          make_uint4(w[0], w[1], w[2], w[3]);
+    }
+}
+
+// C[kk] = A[kk] B for the two 32-row halves kk of a 64-row row-major LDS
+// tile (swizzled as the tile loads store it) against D/16 register B
+// operands, the accumulators starting at init[kk].  All LDS reads are issued
+// before the first product.
+template <int D>
+NAMOH_DEV void tile_rows_x_regs(f32x16 (&C)[2], const uint16_t* __restrict__ tile,
+                                const bf16x8 (&bop)[D / 16], const f32x16 (&init)[2], int c,
+                                int g) {
+  constexpr int KS = D / 16;
+  bf16x8 a[KS][2];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int row = 32 * kk + c;
+      a[ks][kk] = *reinterpret_cast<const bf16x8*>(&tile[row * D + swz<D / 8>(row, 2 * ks + g) * 8]);
+    }
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+    C[kk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][kk], bop[0], init[kk], 0, 0, 0);
+#pragma unroll
+  for (int ks = 1; ks < KS; ++ks)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+      C[kk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][kk], bop[ks], C[kk], 0, 0, 0);
+}
+
+// acc[mt] += Tt(rows 32 mt + c) X over the tile's 64 reduction slots, Tt a
+// transposed tile [D][64] in LDS, X given as four 16-slot B operands taken
+// from C-layout accumulators (slot order as tile.h describes).
+template <int D>
+NAMOH_DEV void tposed_x_c(f32x16 (&acc)[D / 32], const uint16_t* __restrict__ tt,
+                          const bf16x8 (&x)[4], int c, int g) {
+  bf16x8 a[4][D / 32];
+#pragma unroll
+  for (int k2 = 0; k2 < 4; ++k2)
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt) {
+      const int row = 32 * mt + c;
+      a[k2][mt] = *reinterpret_cast<const bf16x8*>(&tt[row * kBN + swz<kBN / 8>(row, 2 * k2 + g) * 8]);
+    }
+#pragma unroll
+  for (int k2 = 0; k2 < 4; ++k2)
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt)
+      acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[k2][mt], x[k2], acc[mt], 0, 0, 0);
+}
+
+// (lse, D) pairs of one 64-row tile: 512 bytes, 32 lanes of wave 0 (the
+// other waves issue nothing, and every wait below is for all loads).
+NAMOH_DEV void ld_tile_dma(const float2* base, uint32_t nbytes, uint32_t tile_bytes,
+                           uint32_t lds, int wave, int lane) {
+  if (wave == 0) {
+    const i32x4 rsrc = buffer_rsrc(reinterpret_cast<const uint16_t*>(base), nbytes);
+    const int tb = __builtin_amdgcn_readfirstlane(static_cast<int>(tile_bytes));
+    if (lane < 32) lds_dma16(rsrc, __builtin_amdgcn_readfirstlane(lds), lane * 16, tb);
+  }
+}
+
+// A lane's pieces of one gradient row into the dense [B, H, T, d] output:
+// acc[mt][4j + i] holds element 32 mt + 8 j + 4 g + i, times f.  The RoPE
+// pair partner of element x < d/2 is x + d/2, in tile mt + d/64 of the same
+// lane, so the gradient goes back through the rotation in registers:
+// x' = (x1 c - x2 s, x2 c + x1 s) gives (d1 c + d2 s, d2 c - d1 s).  cs: the
+// (cos, sin) table row of the position, or NULL for no rotation.
+template <int D>
+NAMOH_DEV void store_row_unrotated(float* __restrict__ dst, const f32x16 (&acc)[D / 32], float f,
+                                   const float2* __restrict__ cs, int g) {
+  constexpr int MH = D / 64;
+#pragma unroll
+  for (int mt = 0; mt < MH; ++mt)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int x = 32 * mt + 8 * j + 4 * g;
+      float a[4], b2[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] = acc[mt][4 * j + i] * f;
+        b2[i] = acc[mt + MH][4 * j + i] * f;
+      }
+      if (cs != nullptr) {
+        const float4 w01 = *reinterpret_cast<const float4*>(cs + x);
+        const float4 w23 = *reinterpret_cast<const float4*>(cs + x + 2);
+        const float cc[4] = {w01.x, w01.z, w23.x, w23.z}, sn[4] = {w01.y, w01.w, w23.y, w23.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float d1 = a[i], d2 = b2[i];
+          a[i] = d1 * cc[i] + d2 * sn[i];
+          b2[i] = d2 * cc[i] - d1 * sn[i];
+        }
+      }
+      *reinterpret_cast<float4*>(dst + x) = make_float4(a[0], a[1], a[2], a[3]);
+      *reinterpret_cast<float4*>(dst + x + D / 2) = make_float4(b2[0], b2[1], b2[2], b2[3]);
+    }
+}
+
+// Zero rows of the dense gradients for the (token, head) pairs the routing
+// did not select (the others are written by the MFMA kernels): one float4
+// of a row per thread, rows of D / 4 threads.
+constexpr int kZeroThreads = 256;
+template <int D>
+__global__ __launch_bounds__(kZeroThreads) void k_bwd_zero_unrouted(
+    const int32_t* __restrict__ topk_idx, int H, int T, int K, size_t rows,
+    float* __restrict__ dq, float* __restrict__ dk, float* __restrict__ dv) {
+  constexpr int C4 = D / 4, RPB = kZeroThreads / C4;
+  const size_t row = static_cast<size_t>(block_x()) * RPB + thread_x() / C4;
+  const int c4 = thread_x() % C4;
+  if (row >= rows) return;
+  const size_t bh = row / T;
+  const int t = static_cast<int>(row - bh * T);
+  const int b = static_cast<int>(bh / H), h = static_cast<int>(bh - (bh / H) * H);
+  const int32_t* tk = topk_idx + (static_cast<size_t>(b) * T + t) * K;
+  bool routed = false;
+  for (int kk = 0; kk < K; ++kk) routed |= tk[kk] == h;
+  if (routed) return;
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+  const size_t o = row * D + 4 * c4;
+  *reinterpret_cast<float4*>(dq + o) = z;
+  *reinterpret_cast<float4*>(dk + o) = z;
+  *reinterpret_cast<float4*>(dv + o) = z;
+}
+
+template <int D> struct BwdMfmaShape {
+  static constexpr int MINB = D == 64 ? 2 : 1;   // workgroups per CU
+};
+
+// Query side: dQ~ of one (segment, 128-query block) item.
+template <int D>
+__global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_dq(
+    const uint16_t* __restrict__ Qs, const uint16_t* __restrict__ dO,
+    const float2* __restrict__ LD, const uint16_t* __restrict__ Kp,
+    const uint16_t* __restrict__ Vp, const uint16_t* __restrict__ Kt,
+    const WorkItem* __restrict__ items, const int32_t* __restrict__ meta,
+    const int32_t* __restrict__ perm_token, const float2* __restrict__ table, int T,
+    int rope_mode, float scale, float* __restrict__ dq) {
+  constexpr int NT = kBwdMfmaThreads, BM = kBwdMfmaBlock;
+  constexpr int KS = D / 16, MT = D / 32;
+  constexpr int KPT = kBN * D / 8 / NT;
+  constexpr size_t TS = static_cast<size_t>(kBN) * D;
+  constexpr uint32_t TB = static_cast<uint32_t>(TS * 2);
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[2][kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sKt[2][D * kBN];
+  WorkItem it;
+  if (!my_item(items, meta, it)) return;
+  const int q0 = it.qb * BM;
+  const int seg0 = it.seg0, n = it.n, tile0 = it.tile0;
+  const int ntiles = (n + kBN - 1) / kBN;
+  const int kt_end = min(ntiles, (q0 + BM + kBN - 1) / kBN);
+  const int tid = thread_x();
+  const int wave = tid / 64, lane = tid % 64;
+  const int c = lane & 31, g = lane >> 5;
+  const int r = q0 + 32 * wave + c;
+  const bool valid = r < n;
+  const int wave_tiles = q0 + 32 * wave < n ? min(q0 + 32 * wave + 31, n - 1) / kBN + 1 : 0;
+  const size_t prow = static_cast<size_t>(tile0) * kBN + (valid ? r : n - 1);
+
+  // the query's operands and statistics (padding rows: zero operands,
+  // lse = +inf, so their probabilities are 0)
+  bf16x8 qB[KS], doB[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    qB[ks] = *reinterpret_cast<const bf16x8*>(Qs + prow * D + 16 * ks + 8 * g);
+    doB[ks] = *reinterpret_cast<const bf16x8*>(dO + prow * D + 16 * ks + 8 * g);
+  }
+  const float2 ld = LD[prow];
+  wait_vmcnt<0>();
+  f32x16 init_l[2], init_d[2];
+  {
+    const float nl = valid ? -ld.x : -INFINITY, nd = valid ? -ld.y : 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      init_l[0][e] = init_l[1][e] = nl;
+      init_d[0][e] = init_d[1][e] = nd;
+    }
+  }
+
+  const int tile0_s = __builtin_amdgcn_readfirstlane(tile0);
+  const int kt_end_s = __builtin_amdgcn_readfirstlane(kt_end);
+  const uint16_t* const bK = Kp + static_cast<size_t>(tile0_s) * TS;
+  const uint16_t* const bV = Vp + static_cast<size_t>(tile0_s) * TS;
+  const uint16_t* const bKt = Kt + static_cast<size_t>(tile0_s) * TS;
+  const uint32_t nb = static_cast<uint32_t>(kt_end_s) * TB;
+  const uint32_t voffR = tile_voffset<D / 8, NT>(tid);
+  const uint32_t voffT = tile_voffset<kBN / 8, NT>(tid);
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t lK = lds_address(&sK[0][0]) + wave_s * kWave * 16;
+  const uint32_t lV = lds_address(&sV[0][0]) + wave_s * kWave * 16;
+  const uint32_t lKt = lds_address(&sKt[0][0]) + wave_s * kWave * 16;
+  tile_dma<KPT, NT>(bK, nb, 0, lK, voffR);
+  tile_dma<KPT, NT>(bV, nb, 0, lV, voffR);
+  tile_dma<KPT, NT>(bKt, nb, 0, lKt, voffT);
+
+  f32x16 acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[mt][e] = 0.f;
+  for (int kt = 0; kt < kt_end; ++kt) {
+    const int st = kt & 1;
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (kt + 1 < kt_end) {
+      const uint32_t tb = static_cast<uint32_t>(kt + 1) * TB;
+      const int ns = st ^ 1;
+      tile_dma<KPT, NT>(bK, nb, tb, lK + ns * TB, voffR);
+      tile_dma<KPT, NT>(bV, nb, tb, lV + ns * TB, voffR);
+      tile_dma<KPT, NT>(bKt, nb, tb, lKt + ns * TB, voffT);
+    }
+    if (kt < wave_tiles) {
+      f32x16 S[2], dP[2];
+      tile_rows_x_regs<D>(S, sK[st], qB, init_l, c, g);    // S^T - lse (log2 units)
+      tile_rows_x_regs<D>(dP, sV[st], doB, init_d, c, g);  // dP^T - D
+      const int key0 = kt * kBN;
+      if (key0 + kBN - 1 > q0 + 32 * wave || key0 + kBN > n) {
+        const int lim = min(r, n - 1) - key0 - 4 * g;   // key 32kk + 8j + 4g + i visible iff <= lim + 4g
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (32 * kk + 8 * j + i > lim) S[kk][4 * j + i] = -INFINITY;
+      }
+      bf16x8 dsB[4];
+#pragma unroll
+      for (int k2 = 0; k2 < 4; ++k2)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int a = 8 * (k2 & 1) + e;
+          dsB[k2][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(S[k2 >> 1][a]) * dP[k2 >> 1][a]);
+        }
+      tposed_x_c<D>(acc, sKt[st], dsB, c, g);
+    }
+  }
+  if (valid) {   // dq~ = scale sum_j dS k~_j, back through the query's rotation
+    const int t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
+    const float2* cs =
+        rope_mode == 2 ? nullptr : table + static_cast<size_t>(rope_mode == 0 ? r : t) * (D / 2);
+    store_row_unrotated<D>(dq + (static_cast<size_t>(it.s) * T + t) * D, acc, scale, cs, g);
+  }
+}
+
+// Key side: dK~ and dV of one (segment, 128-key block) item.
+template <int D>
+__global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_dkdv(
+    const uint16_t* __restrict__ Qs, const uint16_t* __restrict__ dO,
+    const uint16_t* __restrict__ Qt, const uint16_t* __restrict__ dOt,
+    const float2* __restrict__ LD, const uint16_t* __restrict__ Kp,
+    const uint16_t* __restrict__ Vp, const WorkItem* __restrict__ items,
+    const int32_t* __restrict__ meta, const int32_t* __restrict__ perm_token,
+    const float2* __restrict__ table, int T, int rope_mode, float* __restrict__ dk,
+    float* __restrict__ dv) {
+  constexpr int NT = kBwdMfmaThreads, BM = kBwdMfmaBlock;
+  constexpr int KS = D / 16, MT = D / 32;
+  constexpr int KPT = kBN * D / 8 / NT;
+  constexpr size_t TS = static_cast<size_t>(kBN) * D;
+  constexpr uint32_t TB = static_cast<uint32_t>(TS * 2);
+  constexpr uint32_t LB = kBN * sizeof(float2);
+  __shared__ __attribute__((aligned(16))) uint16_t sQ[2][kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sdO[2][kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sQt[2][D * kBN];
+  __shared__ __attribute__((aligned(16))) uint16_t sdOt[2][D * kBN];
+  __shared__ __attribute__((aligned(16))) float2 sLD[2][kBN];
+  WorkItem it;
+  if (!my_item(items, meta, it)) return;
+  const int seg0 = it.seg0, n = it.n, tile0 = it.tile0;
+  const int nkb = (n + BM - 1) / BM;
+  const int j0 = (nkb - 1 - it.qb) * BM;
+  const int ntiles = (n + kBN - 1) / kBN;
+  const int qt0 = j0 / kBN;
+  const int tid = thread_x();
+  const int wave = tid / 64, lane = tid % 64;
+  const int c = lane & 31, g = lane >> 5;
+  const int jw0 = j0 + 32 * wave;   // the wave's first key
+  const int j = jw0 + c;
+  const bool valid = j < n;
+  const bool wave_on = jw0 < n;
+  const size_t prow = static_cast<size_t>(tile0) * kBN + (valid ? j : n - 1);
+
+  bf16x8 kB[KS], vB[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    kB[ks] = *reinterpret_cast<const bf16x8*>(Kp + prow * D + 16 * ks + 8 * g);
+    vB[ks] = *reinterpret_cast<const bf16x8*>(Vp + prow * D + 16 * ks + 8 * g);
+  }
+  wait_vmcnt<0>();
+  if (!valid) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kB[ks][e] = vB[ks][e] = static_cast<__bf16>(0.f);
+  }
+
+  const int tile0_s = __builtin_amdgcn_readfirstlane(tile0);
+  const int nt_s = __builtin_amdgcn_readfirstlane(ntiles);
+  const int qt0_s = __builtin_amdgcn_readfirstlane(qt0);
+  const uint16_t* const bQ = Qs + static_cast<size_t>(tile0_s) * TS;
+  const uint16_t* const bdO = dO + static_cast<size_t>(tile0_s) * TS;
+  const uint16_t* const bQt = Qt + static_cast<size_t>(tile0_s) * TS;
+  const uint16_t* const bdOt = dOt + static_cast<size_t>(tile0_s) * TS;
+  const float2* const bLD = LD + static_cast<size_t>(tile0_s) * kBN;
+  const uint32_t nb = static_cast<uint32_t>(nt_s) * TB;
+  const uint32_t nbl = static_cast<uint32_t>(nt_s) * LB;
+  const uint32_t voffR = tile_voffset<D / 8, NT>(tid);
+  const uint32_t voffT = tile_voffset<kBN / 8, NT>(tid);
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t lQ = lds_address(&sQ[0][0]) + wave_s * kWave * 16;
+  const uint32_t ldO = lds_address(&sdO[0][0]) + wave_s * kWave * 16;
+  const uint32_t lQt = lds_address(&sQt[0][0]) + wave_s * kWave * 16;
+  const uint32_t ldOt = lds_address(&sdOt[0][0]) + wave_s * kWave * 16;
+  const uint32_t lLD = lds_address(&sLD[0][0]);
+  auto issue = [&](int qt, int stage) {
+    const uint32_t tb = static_cast<uint32_t>(qt) * TB;
+    tile_dma<KPT, NT>(bQ, nb, tb, lQ + stage * TB, voffR);
+    tile_dma<KPT, NT>(bdO, nb, tb, ldO + stage * TB, voffR);
+    tile_dma<KPT, NT>(bQt, nb, tb, lQt + stage * TB, voffT);
+    tile_dma<KPT, NT>(bdOt, nb, tb, ldOt + stage * TB, voffT);
+    ld_tile_dma(bLD, nbl, static_cast<uint32_t>(qt) * LB, lLD + stage * LB, wave_s, lane);
+  };
+  issue(qt0_s, 0);
+
+  f32x16 aK[MT], aV[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) aK[mt][e] = aV[mt][e] = 0.f;
+  for (int qt = qt0; qt < ntiles; ++qt) {
+    const int st = (qt - qt0) & 1;
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (qt + 1 < ntiles) issue(qt + 1, st ^ 1);
+    const int i0 = qt * kBN;
+    // queries i0 .. i0 + 63 against the wave's keys: none visible when the
+    // tile ends before the first key
+    if (wave_on && i0 + kBN - 1 >= jw0) {
+      // accumulator starts: -lse and -D of query rows 32kk + 8jj + 4g + i
+      f32x16 S[2], dP[2];
+      {
+        f32x16 il[2], id[2];
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) {
+            const float4* p = reinterpret_cast<const float4*>(&sLD[st][32 * kk + 8 * jj + 4 * g]);
+            const float4 a = p[0], bq = p[1];
+            il[kk][4 * jj] = -a.x;     id[kk][4 * jj] = -a.y;
+            il[kk][4 * jj + 1] = -a.z; id[kk][4 * jj + 1] = -a.w;
+            il[kk][4 * jj + 2] = -bq.x; id[kk][4 * jj + 2] = -bq.y;
+            il[kk][4 * jj + 3] = -bq.z; id[kk][4 * jj + 3] = -bq.w;
+          }
+        tile_rows_x_regs<D>(S, sQ[st], kB, il, c, g);    // S - lse (log2 units)
+        tile_rows_x_regs<D>(dP, sdO[st], vB, id, c, g);  // dP - D
+      }
+      if (i0 < jw0 + 32) {   // the diagonal: key j visible to query i iff j <= i
+        const int lim = j - i0 - 4 * g;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (32 * kk + 8 * jj + i < lim) S[kk][4 * jj + i] = -INFINITY;
+      }
+      bf16x8 pB[4], dsB[4];
+#pragma unroll
+      for (int k2 = 0; k2 < 4; ++k2)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int a = 8 * (k2 & 1) + e;
+          const float p = __builtin_amdgcn_exp2f(S[k2 >> 1][a]);
+          pB[k2][e] = static_cast<__bf16>(p);
+          dsB[k2][e] = static_cast<__bf16>(p * dP[k2 >> 1][a]);
+        }
+      tposed_x_c<D>(aV, sdOt[st], pB, c, g);
+      tposed_x_c<D>(aK, sQt[st], dsB, c, g);
+    }
+  }
+  if (valid) {
+    // the queries were scaled by scale * log2 e: dk~ = ln 2 * sum dS Qs,
+    // back through the key's rotation; dv as it is
+    const int t = min(static_cast<unsigned>(perm_token[seg0 + j]), static_cast<unsigned>(T - 1));
+    const size_t o = (static_cast<size_t>(it.s) * T + t) * D;
+    const float2* cs =
+        rope_mode == 2 ? nullptr : table + static_cast<size_t>(rope_mode == 0 ? j : t) * (D / 2);
+    store_row_unrotated<D>(dk + o, aK, kLn2, cs, g);
+    store_row_unrotated<D>(dv + o, aV, 1.f, nullptr, g);
   }
 }
 
@@ -458,8 +1029,83 @@ static BwdWs carve_bwd(void* ws, int B, int T, int K, int d) {
   return w;
 }
 
-size_t attn_bwd_workspace_bytes(int B, int T, int /*H*/, int K, int d) {
-  return carve_bwd(nullptr, B, T, K, d).bytes;
+struct BwdMfmaWs {
+  void* attn;
+  float* lse;
+  uint16_t *Qs, *dO, *Vp, *Qt, *dOt, *Kt;
+  float2* LD;
+  size_t rows, bytes;
+};
+
+static BwdMfmaWs carve_bwd_mfma(void* ws, int B, int T, int H, int K, int d) {
+  const size_t Nr = static_cast<size_t>(B) * T * K;
+  const size_t BH = static_cast<size_t>(B) * H;
+  Carver cv(ws);
+  BwdMfmaWs w;
+  w.rows = (Nr / kBN + BH + 1) * kBN;   // every 64-row tile a segment can use
+  w.attn = cv.take<char>(attn_workspace_bytes(B, T, H, K, d, 1));
+  w.lse = cv.take<float>(Nr);
+  w.Qs = cv.take<uint16_t>(w.rows * d);
+  w.dO = cv.take<uint16_t>(w.rows * d);
+  w.Vp = cv.take<uint16_t>(w.rows * d);
+  w.Qt = cv.take<uint16_t>(w.rows * d);
+  w.dOt = cv.take<uint16_t>(w.rows * d);
+  w.Kt = cv.take<uint16_t>(w.rows * d);
+  w.LD = cv.take<float2>(w.rows);
+  w.bytes = cv.off;
+  return w;
+}
+
+static bool bwd_uses_mfma(int dtype, int d) { return dtype == 1 && (d == 64 || d == 128); }
+
+// Large enough for either path (the size query takes no dtype).
+size_t attn_bwd_workspace_bytes(int B, int T, int H, int K, int d) {
+  size_t bytes = carve_bwd(nullptr, B, T, K, d).bytes;
+  if (d == 64 || d == 128) bytes = std::max(bytes, carve_bwd_mfma(nullptr, B, T, H, K, d).bytes);
+  return bytes;
+}
+
+template <int D>
+static hipError_t run_bwd_mfma(const void* q, const void* k, const void* v, int B, int T, int H,
+                               int K, float rope_base, int rope_mode, float scale,
+                               const int32_t* topk_idx, const float* gates,
+                               const int32_t* seg_offsets, const int32_t* perm_token,
+                               const float* dout, float* dq, float* dk, float* dv,
+                               float* dgates, void* ws, hipStream_t st) {
+  const BwdMfmaWs w = carve_bwd_mfma(ws, B, T, H, K, D);
+  const int BH = B * H;
+  const int Nr = B * T * K;
+  AttnTiles tl;
+  hipError_t e = launch_attn_stats(q, k, v, B, T, H, K, D, rope_base, rope_mode, scale,
+                                   seg_offsets, perm_token, w.lse, w.attn, tl, st);
+  if (e != hipSuccess) return e;
+  if (tl.BM != kBwdMfmaBlock || static_cast<size_t>(tl.max_tiles) * kBN > w.rows)
+    return hipErrorInvalidValue;   // the forward's blocks and tiles must match these kernels
+  const size_t rows = static_cast<size_t>(BH) * T;
+  constexpr int RPB = kZeroThreads / (D / 4);
+  k_bwd_zero_unrouted<D><<<static_cast<unsigned>((rows + RPB - 1) / RPB), kZeroThreads, 0, st>>>(
+      topk_idx, H, T, K, rows, dq, dk, dv);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const float2* table = static_cast<const float2*>(tl.table);
+  prof_mark("bwd_pack", true, st);
+  k_bwd_pack<D><<<static_cast<unsigned>(tl.max_tiles), kBwdPackThreads, 0, st>>>(
+      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(v), dout, topk_idx, gates,
+      seg_offsets, perm_token, table, tl.Kp, tl.h, w.lse, BH, H, T, K, Nr, rope_mode,
+      scale * kLog2e, w.Qs, w.dO, w.Vp, w.Qt, w.dOt, w.Kt, w.LD, dgates);
+  prof_mark("bwd_pack", false, st);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  prof_mark("bwd_dq", true, st);
+  k_bwd_dq<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
+      w.Qs, w.dO, w.LD, tl.Kp, w.Vp, w.Kt, tl.items, tl.meta, perm_token, table, T, rope_mode,
+      scale, dq);
+  prof_mark("bwd_dq", false, st);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  prof_mark("bwd_dkdv", true, st);
+  k_bwd_dkdv<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
+      w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, table, T,
+      rope_mode, dk, dv);
+  prof_mark("bwd_dkdv", false, st);
+  return hipGetLastError();
 }
 
 template <int D, bool BF16>
@@ -508,11 +1154,14 @@ hipError_t launch_attn_bwd(const void* q, const void* k, const void* v, int dtyp
 #define NAMOH_BWD(DD, BF)                                                                      \
   return run_bwd<DD, BF>(q, k, v, B, T, H, K, rope_base, rope_mode, scale, topk_idx, gates,   \
                          seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st)
-  if (dtype == 1) {
-    if (d == 32) NAMOH_BWD(32, true);
-    if (d == 64) NAMOH_BWD(64, true);
-    NAMOH_BWD(128, true);
+  if (bwd_uses_mfma(dtype, d)) {
+    if (d == 64)
+      return run_bwd_mfma<64>(q, k, v, B, T, H, K, rope_base, rope_mode, scale, topk_idx, gates,
+                              seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st);
+    return run_bwd_mfma<128>(q, k, v, B, T, H, K, rope_base, rope_mode, scale, topk_idx, gates,
+                             seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st);
   }
+  if (dtype == 1) NAMOH_BWD(32, true);
   if (d == 32) NAMOH_BWD(32, false);
   if (d == 64) NAMOH_BWD(64, false);
   NAMOH_BWD(128, false);

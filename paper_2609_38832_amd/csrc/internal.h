@@ -48,6 +48,22 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
                        const int32_t* slot_pos, void* out, int out_dtype,
                        float* head_out, void* ws, hipStream_t st);
 
+struct WorkItem;
+// Where launch_attn_stats leaves the forward's pieces inside its workspace.
+struct AttnTiles {
+  const uint16_t* Kp;      // rotated keys, bf16, 64-row tiles [max_tiles * 64, d]
+  const uint16_t* Vt;      // values, bf16, per tile transposed [max_tiles, d, 64]
+  const void* table;       // RoPE (cos, sin) float pairs [T, d / 2]
+  const WorkItem* items;   // (segment, query block) work list, heaviest first
+  const int32_t* meta;     // item count, validity flag
+  float* h;                // head outputs, f32 packed [Nr, d]
+  int max_items, max_tiles, BM;
+};
+hipError_t launch_attn_stats(const void* q, const void* k, const void* v, int B, int T, int H,
+                             int K, int d, float rope_base, int rope_mode, float scale,
+                             const int32_t* seg_offsets, const int32_t* perm_token, float* lse,
+                             void* ws, AttnTiles& tiles, hipStream_t st);
+
 // ---- decode (decode.hip) --------------------------------------------------
 size_t decode_workspace_bytes(int B, int H, int K, int d, int cap);
 // bias: NULL for the plain selection, else [H] loss-free balancing biases

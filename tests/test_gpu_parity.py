@@ -163,15 +163,33 @@ def test_prefill_biased_routing():
 # ----------------------------------------------------------------------------
 # backward (training path)
 
-def _check_grad(got, ref, what, rel=2e-4):
-    # fp32 arithmetic on exact inputs, reductions over up to a few thousand
-    # terms: within rel of the tensor's largest gradient, or of the element
+def _check_grad(got, ref, what, rel=2e-4, rel_l2=None):
+    # within rel of the tensor's largest gradient plus rel of the element,
+    # and (bf16 products) a relative L2 bound over the whole tensor
     got = np.asarray(got, dtype=np.float64)
     assert np.isfinite(got).all(), f"{what}: non-finite"
     scale = np.abs(ref).max() + 1e-30
-    bad = np.abs(got - ref) > rel * scale + rel * np.abs(ref)
-    assert not bad.any(), f"{what}: {bad.sum()} elements off, max err {np.abs(got - ref).max():.3e} (scale {scale:.3e})"
-    return float(np.abs(got - ref).max() / scale)
+    err = np.abs(got - ref)
+    bad = err > rel * scale + rel * np.abs(ref)
+    assert not bad.any(), f"{what}: {bad.sum()} elements off, max err {err.max():.3e} (scale {scale:.3e})"
+    if rel_l2 is not None:
+        l2 = np.linalg.norm(got - ref) / (np.linalg.norm(ref) + 1e-30)
+        assert l2 <= rel_l2, f"{what}: relative L2 error {l2:.3e}"
+    return float(err.max() / scale)
+
+
+# Gradient tolerances.  fp32 path: fp32 arithmetic on exact inputs, sums of
+# up to a few thousand terms.  bf16 MFMA path (d = 64, 128): the rotated
+# q/k, the probabilities, dS and g*dout are rounded to bf16 (2^-9 relative
+# each) before their products, accumulation in fp32; the errors are those of
+# the forward's bf16 path, so the same bounds apply, taken relative to the
+# tensor's largest gradient.
+GRAD_TOL_F32 = dict(rel=2e-4)
+GRAD_TOL_BF16 = dict(rel=2e-2, rel_l2=1e-2)
+
+
+def _grad_tol(w):
+    return GRAD_TOL_BF16 if w.dtype == "bf16" and w.d in (64, 128) else GRAD_TOL_F32
 
 
 BWD = {
@@ -179,6 +197,8 @@ BWD = {
     "bf16_d128_global": (W.WORKLOADS[3].with_(B=1, T=900, H=4, K=2), O.ROPE_GLOBAL),
     "bf16_d128_rel": (W.WORKLOADS[3].with_(B=2, T=500, H=8, K=3), O.ROPE_HEAD_RELATIVE),
     "f32_d32_none": (W.WORKLOADS[1].with_(B=2, T=400, H=4, K=2), O.ROPE_NONE),
+    "bf16_d32_rel": (W.WORKLOADS[1].with_(B=1, T=300, H=4, K=2, dtype="bf16"), O.ROPE_HEAD_RELATIVE),
+    "bf16_d64_none": (W.WORKLOADS[2].with_(B=1, T=600, H=3, K=3), O.ROPE_NONE),
     "f32_d64_dense": (W.WORKLOADS[2].with_(B=1, T=300, H=4, K=4, dtype="f32"), O.ROPE_HEAD_RELATIVE),
     "skewed_long": (W.WORKLOADS[4].with_(B=1, T=1600, H=8, K=1), O.ROPE_HEAD_RELATIVE),
 }
@@ -200,9 +220,11 @@ def test_attn_bwd_parity(name):
     dq, dk, dv, dg = O.attention_backward(f["q"], f["k"], f["v"], ref["gates"], ref["seg_offsets"],
                                           ref["perm_token"], ref["slot_pos"], w.H, w.rope_base,
                                           dout.astype(np.float64), rope_mode)
-    errs = [_check_grad(g["dq"].cpu().numpy(), dq, "dq"), _check_grad(g["dk"].cpu().numpy(), dk, "dk"),
-            _check_grad(g["dv"].cpu().numpy(), dv, "dv"),
-            _check_grad(g["dgates"].cpu().numpy(), dg, "dgates")]
+    tol = _grad_tol(w)
+    errs = [_check_grad(g["dq"].cpu().numpy(), dq, "dq", **tol),
+            _check_grad(g["dk"].cpu().numpy(), dk, "dk", **tol),
+            _check_grad(g["dv"].cpu().numpy(), dv, "dv", **tol),
+            _check_grad(g["dgates"].cpu().numpy(), dg, "dgates", **tol)]
     say(f"  rel max err dq {errs[0]:.1e} dk {errs[1]:.1e} dv {errs[2]:.1e} dgates {errs[3]:.1e}")
     # rows of tokens not routed to the head are exactly zero
     m = O.membership(ref["topk_idx"], w.H).transpose(0, 2, 1)
@@ -228,7 +250,7 @@ def test_route_bwd_parity(gate_mode):
                                        ref["perm_token"], ref["slot_pos"], w.H, w.rope_base,
                                        dout.astype(np.float64))
     dl_ref = O.gates_backward(inp["logits"], ref["topk_idx"], dg, gate_mode)
-    e = _check_grad(dl.cpu().numpy(), dl_ref, "dlogits", rel=1e-3)
+    e = _check_grad(dl.cpu().numpy(), dl_ref, "dlogits", **_grad_tol(w))
     say(f"  rel max err dlogits {e:.1e}")
 
 
