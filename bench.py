@@ -206,6 +206,86 @@ def cpu_baseline_prefill(w, inp, head_len, budget_s):
 
 
 # ----------------------------------------------------------------------------
+def bench_backward(w, args, torch, L, DI):
+    """One training step of the layer: route, forward, backward of the
+    attention (dq, dk, dv, dgates) and of the gates (d logits)."""
+    dev = torch.device("cuda:0")
+    log(f"generating inputs for {w.name} (training step)")
+    inp = W.prefill_inputs(w)
+    logits = torch.from_numpy(inp["logits"]).to(dev)
+    q, k, v = (DI.to_device(inp[n], w.dtype, dev) for n in ("q", "k", "v"))
+    B, T, H, K, d = w.B, w.T, w.H, w.K, w.d
+    g = torch.Generator(device="cpu").manual_seed(w.seed + 77)
+    dout = (torch.randn(B, T, d, generator=g, dtype=torch.float32) * 0.1).to(dev)
+    routing = L.route(logits, K)
+    rws = L.workspace(L.route_workspace_size(B, T, H, K), dev)
+    dt = L.dtype_code(q.dtype)
+    aws = L.workspace(L.attn_workspace_size(B, T, H, K, d, dt), dev)
+    bws = L.workspace(int(L.lib().namoh_attn_bwd_workspace_size(B, T, H, K, d)), dev)
+    out = torch.empty(B, T, d, dtype=q.dtype, device=dev)
+    f32 = dict(dtype=torch.float32, device=dev)
+    grads = {"dq": torch.empty(B, H, T, d, **f32), "dk": torch.empty(B, H, T, d, **f32),
+             "dv": torch.empty(B, H, T, d, **f32), "dgates": torch.empty(B, T, K, **f32)}
+
+    def step():
+        L.route(logits, K, L.GATE_SOFTMAX_SELECTED, out=routing, ws=rws)
+        L.attn_fwd(q, k, v, routing, K, w.rope_base, L.ROPE_HEAD_RELATIVE, out=out, ws=aws)
+        L.attn_bwd(q, k, v, routing, K, w.rope_base, dout, ws=bws, out=grads)
+        L.route_bwd(logits, routing, grads["dgates"])
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    n = routing["head_len"].cpu().numpy().astype(np.int64)
+    c_attn = int((n * (n + 1) // 2).sum())
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    L.profile_enable(2 * args.steps)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    kern = {}
+    for sec in ("attn", "pack", "combine", "bwd_pack", "bwd_dq", "bwd_dkdv"):
+        r = L.profile_read(sec)
+        if r is not None and r[1] > 0:
+            kern[sec] = r[0] / r[1]
+    L.profile_enable(0)
+    mfma = w.dtype == "bf16" and d in (64, 128)
+    # the backward's products per causal (query, key) pair: dP = dO V^T, the
+    # recomputed scores, dV += P^T dO, dQ += dS K, dK += dS^T Q: 2d FLOP each;
+    # the algorithmic count is 10 d (scores counted once); the two kernels
+    # execute 6 d (dq: S, dP, dQ) and 8 d (dkdv: S, dP, dV, dK)
+    bwd_ms = kern.get("bwd_dq", float("nan")) + kern.get("bwd_dkdv", float("nan"))
+    flops = 10.0 * d * c_attn
+    achieved = flops / (bwd_ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if mfma else PEAK_FP32_TFLOPS
+    res = {"metric": "routed-attn training step tokens/s (route + forward + backward), "
+                     "backward MFMA kernels % of bf16 peak (1 GPU)",
+           "value": round(B * T / (ms_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": w.dtype, "data": "synthetic",
+           "config": {"workload": w.name, "B": B, "T": T, "H": H, "K": K, "d_head": d,
+                      "pass": "training step", "rope": "head-relative",
+                      "rope_base": w.rope_base, "gates": "softmax over selected"},
+           "roofline": {"kernel": "k_bwd_dq + k_bwd_dkdv" if mfma else "k_bwd_q + k_bwd_kv",
+                        "bound": "mfma" if mfma else "alu", "achieved": round(achieved, 2),
+                        "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                        "traffic": None,
+                        "algorithmic_per_launch": {"flops": flops, "C_attn": c_attn},
+                        "kernel_ms": round(bwd_ms, 4)},
+           "kernels_ms": {k2: round(v2, 4) for k2, v2 in kern.items()}}
+    return res
+
+
+# ----------------------------------------------------------------------------
 def bench_decode(w, args, torch, L, DI):
     dev = torch.device("cuda:0")
     log(f"prior head lengths for {w.name}")
@@ -320,6 +400,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", type=int, default=2, choices=sorted(W.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--backward", action="store_true",
+                    help="time a training step (route, forward, backward) of a prefill "
+                         "workload instead of the forward step")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for the CPU baseline sample")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -352,7 +435,13 @@ def main():
     from paper_2609_38832_amd import _lib as L
     from paper_2609_38832_amd import device_inputs as DI
     L.lib()
-    res = (bench_decode if w.decode else bench_prefill)(w, args, torch, L, DI)
+    if args.backward:
+        if w.decode:
+            print(json.dumps({"error": "--backward needs a prefill workload"}))
+            sys.exit(2)
+        res = bench_backward(w, args, torch, L, DI)
+    else:
+        res = (bench_decode if w.decode else bench_prefill)(w, args, torch, L, DI)
     print(json.dumps(res), flush=True)
 
 

@@ -245,9 +245,11 @@ def prefill_cache(k: torch.Tensor, v: torch.Tensor, r: dict, K: int, rope_base: 
 
 def attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K: int,
              rope_base: float, dout: torch.Tensor, rope_mode: int = ROPE_HEAD_RELATIVE,
-             softmax_scale: float = 0.0, ws: Optional[torch.Tensor] = None) -> dict:
+             softmax_scale: float = 0.0, ws: Optional[torch.Tensor] = None,
+             out: Optional[dict] = None) -> dict:
     """namoh_attn_bwd: gradients dq, dk, dv [B, H, T, d] and dgates [B, T, K]
-    (float32) for the upstream gradient dout float32 [B, T, d]."""
+    (float32) for the upstream gradient dout float32 [B, T, d]; `out` may
+    hold preallocated tensors of those shapes under the same keys."""
     _need_cuda(q, k, v, dout)
     B, H, T, d = q.shape
     if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
@@ -256,8 +258,14 @@ def attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K
         raise ValueError("dout must be float32 [B, T, d]")
     dev = q.device
     f32 = dict(dtype=torch.float32, device=dev)
-    out = {"dq": torch.empty(B, H, T, d, **f32), "dk": torch.empty(B, H, T, d, **f32),
-           "dv": torch.empty(B, H, T, d, **f32), "dgates": torch.empty(B, T, K, **f32)}
+    if out is None:
+        out = {"dq": torch.empty(B, H, T, d, **f32), "dk": torch.empty(B, H, T, d, **f32),
+               "dv": torch.empty(B, H, T, d, **f32), "dgates": torch.empty(B, T, K, **f32)}
+    for key, shape in (("dq", (B, H, T, d)), ("dk", (B, H, T, d)), ("dv", (B, H, T, d)),
+                       ("dgates", (B, T, K))):
+        if out[key].dtype != torch.float32 or tuple(out[key].shape) != shape \
+                or not out[key].is_contiguous():
+            raise ValueError(f"out[{key!r}] must be contiguous float32 {shape}")
     if ws is None:
         ws = workspace(int(lib().namoh_attn_bwd_workspace_size(B, T, H, K, d)), dev)
     check(lib().namoh_attn_bwd(_ptr(q), _ptr(k), _ptr(v), dtype_code(q.dtype), B, T, H, K, d,

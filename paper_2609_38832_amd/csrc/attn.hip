@@ -134,9 +134,24 @@ struct SchedLds {
   int wave[17];
 };
 
+// Serpentine placement: the hardware puts workgroup i on the compute unit of
+// workgroup i mod (number of compute units) as long as every unit has room,
+// so in heaviest-first order unit u would receive ranks u, P + u, 2P + u, ...
+// (P units), all near the top of their block of P ranks.  Reversing every
+// other block of P ranks gives unit u the ranks u, 2P - 1 - u, 2P + u, ...,
+// whose sums are nearly equal.  The map is a permutation of [0, total).
+NAMOH_DEV int serpentine(int rank, int total, int period) {
+  if (period <= 1) return rank;
+  const int blk = rank / period;
+  if ((blk & 1) == 0) return rank;
+  const int first = blk * period;
+  const int len = min(period, total - first);
+  return first + len - 1 - (rank - first);
+}
+
 template <int NT>
 NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, int T, int BM,
-                             int Nr, int max_items, WorkItem* __restrict__ items,
+                             int Nr, int max_items, int period, WorkItem* __restrict__ items,
                              int32_t* __restrict__ meta, SchedLds& L) {
   static_assert(NT % kWave == 0 && NT / kWave <= 16 && kSortBins % NT == 0, "block size");
   const int tid = thread_x();
@@ -215,12 +230,14 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
     run += h[i];
   }
   __syncthreads();
+  const int placed = min(total, max_items);
   for (long g0 = 0; g0 < grid_items; g0 += NT) {
     const long g = g0 + tid;
     int sg = 0, qb = 0, seg0 = 0, n = 0, key = 0;
     const bool act = g < grid_items && cell(g, sg, qb, seg0, n, key);
-    const int pos = wave_bin_add(L.hist, key, act);
-    if (act && pos < max_items) {
+    const int rank = wave_bin_add(L.hist, key, act);
+    if (act && rank < placed) {
+      const int pos = serpentine(rank, placed, period);
       WorkItem wi;
       wi.s = sg;
       wi.qb = qb;
@@ -232,7 +249,7 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
     }
   }
   if (tid == 0) {
-    meta[kMetaItems] = min(total, max_items);
+    meta[kMetaItems] = placed;
     meta[kMetaBad] = 0;
   }
 }
@@ -267,9 +284,9 @@ __global__ __launch_bounds__(kTableThreads) void k_rope_table(int T, int d, doub
 // builds it in its workgroup 0).
 __global__ __launch_bounds__(kPackThreads) void k_attn_schedule(
     const int32_t* __restrict__ seg_offsets, int BH, int T, int BM, int Nr, int max_items,
-    WorkItem* __restrict__ items, int32_t* __restrict__ meta) {
+    int period, WorkItem* __restrict__ items, int32_t* __restrict__ meta) {
   __shared__ SchedLds L;
-  attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, items, meta, L);
+  attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, period, items, meta, L);
 }
 
 // ---------------------------------------------------------------------------
@@ -280,31 +297,52 @@ template <int D>
 struct PackLds {
   uint16_t sv[kBN][D + 8];
   int off[kSegLds + 1];
+  float wnorm[kPackThreads / kWave];
+  double freq[D / 2];
 };
+
+// theta_j / (2 pi) = base^(-2j/d) / (2 pi) for the rotation pairs j < d/2,
+// in double.
+NAMOH_DEV double rope_freq_rev(int j, int d, double log_base) {
+  return exp(-(2.0 * j / d) * log_base) * 0.15915494309189535;
+}
+
+// Squared norm of 8 packed bf16 values.
+NAMOH_DEV float sumsq8(const uint4 x) {
+  float f[8];
+  unpack8(x, f);
+  float a = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) a = fmaf(f[e], f[e], a);
+  return a;
+}
 
 template <int D>
 __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
-    const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    const float2* __restrict__ table, const int32_t* __restrict__ seg_offsets,
+    const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, double log_base,
+    double* __restrict__ freq_out, const int32_t* __restrict__ seg_offsets,
     const int32_t* __restrict__ perm_token, int BH, int T, int H, int Nr, int rope_mode,
-    int BM, int max_items, WorkItem* __restrict__ items, int32_t* __restrict__ meta,
-    uint16_t* __restrict__ Kp, uint16_t* __restrict__ Vt) {
+    int BM, int max_items, int period, WorkItem* __restrict__ items, int32_t* __restrict__ meta,
+    uint16_t* __restrict__ Kp, uint16_t* __restrict__ Vt, float* __restrict__ knorm) {
   __shared__ __attribute__((aligned(16))) union {
     SchedLds sched;
     PackLds<D> pack;
   } L;
   if (block_x() == 0) {
-    attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, items, meta, L.sched);
+    // the rotation frequencies for the attention kernel, then the schedule
+    if (thread_x() < D / 2) freq_out[thread_x()] = rope_freq_rev(thread_x(), D, log_base);
+    attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, period, items, meta,
+                                L.sched);
     return;
   }
   const int gt = block_x() - 1;
   const int tid = thread_x();
+  if (rope_mode != 2 && tid < D / 2) L.pack.freq[tid] = rope_freq_rev(tid, D, log_base);
   // segment of tile gt: the last s with seg_tile0(off[s], s) <= gt
   const bool in_lds = BH <= kSegLds;
-  if (in_lds) {
+  if (in_lds)
     for (int i = tid; i <= BH; i += kPackThreads) L.pack.off[i] = seg_offsets[i];
-    __syncthreads();
-  }
+  __syncthreads();
   const int32_t* off = in_lds ? L.pack.off : seg_offsets;
   int lo = 0, hi = BH;
   while (hi - lo > 1) {
@@ -323,6 +361,8 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
   const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
 
   constexpr int HP = D / 16;  // 8-element granule pairs (j, j + d/2) per row
+  static_assert(kPackThreads % HP == 0 && kWave % HP == 0, "a row's units share one wave");
+  float rmax = 0.f;   // largest squared norm of a packed (rounded) key row seen
   for (int u = tid; u < kBN * HP; u += kPackThreads) {
     const int row = u / HP, c = u - (u / HP) * HP;
     const int r = r0 + row;
@@ -338,7 +378,7 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
         unpack8(bb, x2);
         const int pos = rope_mode == 0 ? r : t;
         float4 cs[4];
-        load_rope8(cs, table + static_cast<size_t>(pos) * (D / 2) + 8 * c);
+        rope8_rev(cs, static_cast<double>(pos), &L.pack.freq[8 * c]);
         rope8(x1, x2, cs);
         o1 = pack8(x1);
         o2 = pack8(x2);
@@ -350,7 +390,17 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
     uint16_t* dst = Kp + (static_cast<size_t>(gt) * kBN + row) * D;
     *reinterpret_cast<uint4*>(dst + 8 * c) = o1;
     *reinterpret_cast<uint4*>(dst + D / 2 + 8 * c) = o2;
+    // the row's squared norm: its HP units are consecutive lanes
+    float ss = sumsq8(o1) + sumsq8(o2);
+#pragma unroll
+    for (int o = 1; o < HP; o <<= 1) ss += __shfl_xor(ss, o);
+    rmax = fmaxf(rmax, ss);
   }
+  // the tile's largest key norm (bounds every score of the tile, see
+  // k_attn_mfma); written by the one workgroup that packs the tile
+#pragma unroll
+  for (int o = HP; o < kWave; o <<= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, o));
+  if (tid % kWave == 0) L.pack.wnorm[tid / kWave] = rmax;
   constexpr int RG = D / 8;  // granules per value row
   for (int u = tid; u < kBN * RG; u += kPackThreads) {
     const int row = u / RG, gr = u - (u / RG) * RG;
@@ -363,6 +413,12 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
     *reinterpret_cast<uint4*>(&sv[row][8 * gr]) = x;
   }
   __syncthreads();
+  if (tid == 0) {
+    float mx = 0.f;
+#pragma unroll
+    for (int w2 = 0; w2 < kPackThreads / kWave; ++w2) mx = fmaxf(mx, L.pack.wnorm[w2]);
+    knorm[gt] = sqrtf(mx);
+  }
   for (int u = tid; u < D * (kBN / 8); u += kPackThreads) {
     const int m = u / (kBN / 8), pg = u - (u / (kBN / 8)) * (kBN / 8);
     uint32_t w[4];
@@ -453,8 +509,8 @@ NAMOH_DEV void qk_tile(f32x16 (&S)[2][NQT], const uint16_t* __restrict__ sKb,
 template <int D, int NQT, int NW>
 NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
                           float (&m_run)[NQT], float (&l_run)[NQT], f32x16 (&minit)[NQT],
-                          bool first, const uint16_t* __restrict__ sVb, int key0, int q0,
-                          int wave, int n, int c, int g) {
+                          bool first, bool fast, const uint16_t* __restrict__ sVb, int key0,
+                          int q0, int wave, int n, int c, int g) {
   // value operands: the first VPRE 16-key steps are read while the softmax
   // runs (all of them for d = 64; half for d = 128, to stay within 256
   // registers), the rest while the first P.V products execute
@@ -490,18 +546,24 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
   float alpha[NQT], delta[NQT];
   bool rescale = false;
 #pragma unroll
-  for (int qt = 0; qt < NQT; ++qt) {
-    float mx = fmaxf(S[0][qt][0], S[0][qt][1]);
+  for (int qt = 0; qt < NQT; ++qt) alpha[qt] = 1.f;
+  // fast: the tile's norm bound already keeps every score within kLazyLog2
+  // of the running maximum, so the maximum is not needed
+  if (!fast) {
 #pragma unroll
-    for (int i = 2; i < 32; i += 2)
-      mx = fmaxf(fmaxf(mx, S[i >> 4][qt][i & 15]), S[i >> 4][qt][(i & 15) + 1]);
-    mx = pair_max32(mx);
-    const bool up = first || mx > kLazyLog2;
-    delta[qt] = up ? mx : 0.f;
-    alpha[qt] = (up && !first) ? __builtin_amdgcn_exp2f(-mx) : 1.f;
-    rescale |= up;
+    for (int qt = 0; qt < NQT; ++qt) {
+      float mx = fmaxf(S[0][qt][0], S[0][qt][1]);
+#pragma unroll
+      for (int i = 2; i < 32; i += 2)
+        mx = fmaxf(fmaxf(mx, S[i >> 4][qt][i & 15]), S[i >> 4][qt][(i & 15) + 1]);
+      mx = pair_max32(mx);
+      const bool up = first || mx > kLazyLog2;
+      delta[qt] = up ? mx : 0.f;
+      alpha[qt] = (up && !first) ? __builtin_amdgcn_exp2f(-mx) : 1.f;
+      rescale |= up;
+    }
   }
-  if (__any(rescale)) {
+  if (!fast && __any(rescale)) {
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
 #pragma unroll
@@ -564,10 +626,10 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
 template <int D, int NQT, int NW, bool HB>
 __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kp,
-    const uint16_t* __restrict__ Vt, const float2* __restrict__ table,
+    const uint16_t* __restrict__ Vt, const double* __restrict__ freq,
     const int32_t* __restrict__ perm_token, const WorkItem* __restrict__ items,
-    const int32_t* __restrict__ meta, int T, int H, int rope_mode, float scale_log2,
-    void* __restrict__ hout, float* __restrict__ lse_out) {
+    const int32_t* __restrict__ meta, const float* __restrict__ knorm, int T, int H,
+    int rope_mode, float scale_log2, void* __restrict__ hout, float* __restrict__ lse_out) {
   constexpr int BM = 32 * NQT * NW;
   constexpr int KS = D / 16;  // reduction steps of S^T = K Q^T
   constexpr int MT = D / 32;  // 32-row tiles of O^T
@@ -608,6 +670,20 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     const int r = q0 + 32 * (qt * NW + wave) + c;
     qtok[qt] = perm_token[seg0 + (r < n ? r : n - 1)];
   }
+  // largest key norm over the item's key tiles (lane-wise here, reduced
+  // across the wave after the query gather); four independent loads per
+  // lane per round, all issued before the wait below
+  float kmax = 0.f;
+  for (int i0 = 0; i0 < kt_end; i0 += 4 * kWave) {
+    float kv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = i0 + j * kWave + lane;
+      kv[j] = i < kt_end ? knorm[tile0 + i] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) kmax = fmaxf(kmax, kv[j]);
+  }
   wait_vmcnt<0>();
 
   // ---- first NS - 1 key/value tiles: in flight during the query gather ---
@@ -637,9 +713,9 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   }
 
   // ---- query block: gather, rotate, round to bf16 B operands -------------
-  // (the query rows and their RoPE factors are loaded together; the table
-  // has T rows, so the read in the no-RoPE mode, replaced by the identity
-  // rotation, is in bounds)
+  // (the query rows and the frequencies of the lane's rotation pairs are
+  // loaded together; the frequencies are read in the no-RoPE mode too, where
+  // the identity rotation replaces them)
   bf16x8 qB[NQT][KS];
 #pragma unroll
   for (int qt = 0; qt < NQT; ++qt) {
@@ -650,23 +726,31 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     const int pos = rope_mode == 0 ? rr : (rope_mode == 1 ? t : 0);
     const float qscale = r < n ? scale_log2 : 0.f;   // padding rows: zero queries
     u32x4 qa[KS / 2], qb2[KS / 2];
-    float4 cs[KS / 2][4];
+    double fr[KS / 2][8];
 #pragma unroll
     for (int s2 = 0; s2 < KS / 2; ++s2) {
       qa[s2] = *reinterpret_cast<const u32x4*>(qrow + 16 * s2 + 8 * g);
       qb2[s2] = *reinterpret_cast<const u32x4*>(qrow + D / 2 + 16 * s2 + 8 * g);
-      load_rope8(cs[s2], table + static_cast<size_t>(pos) * (D / 2) + 16 * s2 + 8 * g);
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const double2 f2 = *reinterpret_cast<const double2*>(freq + 16 * s2 + 8 * g + e);
+        fr[s2][e] = f2.x;
+        fr[s2][e + 1] = f2.y;
+      }
     }
 #pragma unroll
     for (int s2 = 0; s2 < KS / 2; ++s2) {
       float x1[8], x2[8];
       unpack8(make_uint4(qa[s2][0], qa[s2][1], qa[s2][2], qa[s2][3]), x1);
       unpack8(make_uint4(qb2[s2][0], qb2[s2][1], qb2[s2][2], qb2[s2][3]), x2);
+      float4 cs[4];
       if (rope_mode == 2) {   // identity rotation
 #pragma unroll
-        for (int e = 0; e < 4; ++e) cs[s2][e] = make_float4(1.f, 0.f, 1.f, 0.f);
+        for (int e = 0; e < 4; ++e) cs[e] = make_float4(1.f, 0.f, 1.f, 0.f);
+      } else {
+        rope8_rev(cs, static_cast<double>(pos), fr[s2]);
       }
-      rope8(x1, x2, cs[s2]);
+      rope8(x1, x2, cs);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {   // pre-scaled: scores come out in log2 units
         qB[qt][s2][e] = static_cast<__bf16>(x1[e] * qscale);
@@ -678,6 +762,26 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   // it to wait for inside the loop (where its wait would also cover the
   // tile loads issued since)
   wait_vmcnt<0>();
+  // Norm bound of the scores.  Every (log2-unit) score of a query against
+  // the item's keys is at most |q~| * max |k~| in magnitude (Cauchy-Schwarz
+  // on the rounded operands; the small factor covers the fp32
+  // accumulation), so while that product stays within kLazyLog2 of the
+  // running maximum a tile's exact maximum is not needed.
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) kmax = fmaxf(kmax, __shfl_xor(kmax, o));
+  float qn[NQT];
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt) {
+    float ss = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = static_cast<float>(qB[qt][ks][e]);
+        ss = fmaf(x, x, ss);
+      }
+    qn[qt] = sqrtf(pair_sum32(ss)) * kmax * 1.001f;
+  }
 
   f32x16 O[MT][NQT];
 #pragma unroll
@@ -718,8 +822,11 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     if (kt < wave_tiles) {
       f32x16 S[2][NQT];
       qk_tile<D, NQT>(S, sK[st], qB, minit, c, g);
-      softmax_pv<D, NQT, NW>(S, O, m_run, l_run, minit, kt == 0, sV[st], kt * kBN, q0, wave,
-                             n, c, g);
+      bool within = true;
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt) within &= qn[qt] <= m_run[qt] + kLazyLog2;
+      softmax_pv<D, NQT, NW>(S, O, m_run, l_run, minit, kt == 0, __all(within), sV[st], kt * kBN,
+                             q0, wave, n, c, g);
     }
   }
 
@@ -966,6 +1073,16 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
 // ---------------------------------------------------------------------------
 static bool use_mfma(int d, int dtype) { return dtype == 1 && (d == 64 || d == 128); }
 
+// Compute units of the current device (the period of the hardware's
+// workgroup placement); 0 if the query fails, which turns the serpentine
+// order off.
+static int device_cu_count() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return n;
+}
+
 static int block_queries(int d, int dtype) {
   if (!use_mfma(d, dtype)) return kGenericBM;
   return d == 64 ? 32 * MfmaShape<64>::NQT * MfmaShape<64>::NW
@@ -978,6 +1095,8 @@ struct AttnWs {
   float2* table;
   uint16_t* Kp;
   uint16_t* Vt;
+  float* knorm;
+  double* freq;
   float* hpack;
   size_t bytes;
   size_t max_items, max_tiles;
@@ -997,8 +1116,12 @@ static AttnWs carve_attn(void* ws, int B, int T, int H, int K, int d, int dtype)
   if (use_mfma(d, dtype)) {
     w.Kp = cv.take<uint16_t>(w.max_tiles * kBN * d);
     w.Vt = cv.take<uint16_t>(w.max_tiles * kBN * d);
+    w.knorm = cv.take<float>(w.max_tiles);
+    w.freq = cv.take<double>(64);
   } else {
     w.Kp = w.Vt = nullptr;
+    w.knorm = nullptr;
+    w.freq = nullptr;
   }
   w.hpack = cv.take<float>(Nr * d);
   w.bytes = cv.off;
@@ -1011,26 +1134,27 @@ size_t attn_workspace_bytes(int B, int T, int H, int K, int d, int dtype) {
 
 template <int D>
 static void launch_mfma(const AttnWs& w, const void* q, const void* k, const void* v,
-                        int B, int T, int H, int Nr, int rope_mode, float scale_log2,
-                        const int32_t* seg_offsets, const int32_t* perm_token,
+                        int B, int T, int H, int Nr, int rope_mode, double log_base,
+                        float scale_log2, const int32_t* seg_offsets, const int32_t* perm_token,
                         void* hout, bool hout_bf16, float* lse, hipStream_t st) {
   constexpr int NW = MfmaShape<D>::NW, NQT = MfmaShape<D>::NQT;
   prof_mark("pack", true, st);
   k_pack_kv<D><<<static_cast<unsigned>(1 + w.max_tiles), kPackThreads, 0, st>>>(
-      static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), w.table, seg_offsets,
+      static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), log_base, w.freq,
+      seg_offsets,
       perm_token, B * H, T, H, Nr, rope_mode, 32 * NQT * NW, static_cast<int>(w.max_items),
-      w.items, w.meta, w.Kp, w.Vt);
+      device_cu_count(), w.items, w.meta, w.Kp, w.Vt, w.knorm);
   prof_mark("pack", false, st);
   prof_mark("attn", true, st);
   const unsigned grid = static_cast<unsigned>(w.max_items);
   if (hout_bf16)
     k_attn_mfma<D, NQT, NW, true><<<grid, NW * 64, 0, st>>>(
-        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.table, perm_token, w.items, w.meta, T,
-        H, rope_mode, scale_log2, hout, nullptr);
+        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.freq, perm_token, w.items, w.meta,
+        w.knorm, T, H, rope_mode, scale_log2, hout, nullptr);
   else
     k_attn_mfma<D, NQT, NW, false><<<grid, NW * 64, 0, st>>>(
-        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.table, perm_token, w.items, w.meta, T,
-        H, rope_mode, scale_log2, hout, lse);
+        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.freq, perm_token, w.items, w.meta,
+        w.knorm, T, H, rope_mode, scale_log2, hout, lse);
   prof_mark("attn", false, st);
 }
 
@@ -1060,7 +1184,9 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   const int BM = block_queries(d, dtype);
   const int Nr = B * T * K;
   const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
-  if (rope_mode != 2) {
+  // the MFMA path forms its rotation factors in the kernels; the fp32 path
+  // reads them from the table
+  if (rope_mode != 2 && !use_mfma(d, dtype)) {
     const size_t entries = static_cast<size_t>(T) * (d / 2);
     const size_t per_block = static_cast<size_t>(kTableThreads) * kTableEntries;
     k_rope_table<<<static_cast<unsigned>((entries + per_block - 1) / per_block), kTableThreads, 0,
@@ -1071,14 +1197,15 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   if (use_mfma(d, dtype)) {
     const float sl2 = scale * 1.4426950408889634f;
     if (d == 64)
-      launch_mfma<64>(w, q, k, v, B, T, H, Nr, rope_mode, sl2, seg_offsets, perm_token, hout, hb,
-                      nullptr, st);
+      launch_mfma<64>(w, q, k, v, B, T, H, Nr, rope_mode, log_base, sl2, seg_offsets, perm_token,
+                      hout, hb, nullptr, st);
     else
-      launch_mfma<128>(w, q, k, v, B, T, H, Nr, rope_mode, sl2, seg_offsets, perm_token, hout, hb,
-                       nullptr, st);
+      launch_mfma<128>(w, q, k, v, B, T, H, Nr, rope_mode, log_base, sl2, seg_offsets,
+                       perm_token, hout, hb, nullptr, st);
   } else {
     k_attn_schedule<<<1, kPackThreads, 0, st>>>(seg_offsets, B * H, T, BM, Nr,
-                                                static_cast<int>(w.max_items), w.items, w.meta);
+                                                static_cast<int>(w.max_items), device_cu_count(),
+                                                w.items, w.meta);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const bool bf = dtype == 1;
 #define NAMOH_GEN(DD)                                                                        \
@@ -1128,11 +1255,11 @@ hipError_t launch_attn_stats(const void* q, const void* k, const void* v, int B,
   if (e != hipSuccess) return e;
   const float sl2 = scale * 1.4426950408889634f;
   if (d == 64)
-    launch_mfma<64>(w, q, k, v, B, T, H, Nr, rope_mode, sl2, seg_offsets, perm_token, w.hpack,
-                    false, lse, st);
+    launch_mfma<64>(w, q, k, v, B, T, H, Nr, rope_mode, log_base, sl2, seg_offsets, perm_token,
+                    w.hpack, false, lse, st);
   else
-    launch_mfma<128>(w, q, k, v, B, T, H, Nr, rope_mode, sl2, seg_offsets, perm_token, w.hpack,
-                     false, lse, st);
+    launch_mfma<128>(w, q, k, v, B, T, H, Nr, rope_mode, log_base, sl2, seg_offsets, perm_token,
+                     w.hpack, false, lse, st);
   tiles.Kp = w.Kp;
   tiles.Vt = w.Vt;
   tiles.table = w.table;

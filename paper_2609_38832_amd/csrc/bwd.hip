@@ -462,6 +462,8 @@ template <int D>
 struct BwdPackLds {
   uint16_t t[3][kBN][D + 8];   // q, dO, k tiles for the transposes
   int off[kBwdSegLds + 1];
+  int tok[kBN], ks[kBN];       // per tile row: token, k slot (-1: none)
+  float g[kBN];                // per tile row: gate
 };
 
 template <int D>
@@ -498,14 +500,19 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
   const int b = s / H, hh = s - (s / H) * H;
   const size_t head_base = (static_cast<size_t>(b) * H + hh) * T;
   const size_t prow0 = static_cast<size_t>(gt) * kBN;
-  // token, k slot and gate of tile row `row` (r < n)
-  auto row_info = [&](int r, int& t, int& ks, float& g) {
-    t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
-    ks = -1;
+  // token, k slot and gate of each tile row, once per row (r < n)
+  if (tid < kBN && r0 + tid < n) {
+    const int t = min(static_cast<unsigned>(perm_token[seg0 + r0 + tid]),
+                      static_cast<unsigned>(T - 1));
+    const int32_t* sel = topk_idx + (static_cast<size_t>(b) * T + t) * K;
+    int ks = -1;
     for (int kk = 0; kk < K; ++kk)
-      if (topk_idx[(static_cast<size_t>(b) * T + t) * K + kk] == hh) ks = kk;
-    g = ks >= 0 ? gates[(static_cast<size_t>(b) * T + t) * K + ks] : 0.f;
-  };
+      if (sel[kk] == hh) ks = kk;
+    L.tok[tid] = t;
+    L.ks[tid] = ks;
+    L.g[tid] = ks >= 0 ? gates[(static_cast<size_t>(b) * T + t) * K + ks] : 0.f;
+  }
+  __syncthreads();
 
   // rows: rotated, scaled queries (as the forward rounds them), gated output
   // gradients, values; one 8-pair group (j, j + d/2) per unit
@@ -515,9 +522,8 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
     const int r = r0 + row;
     uint4 q1 = make_uint4(0, 0, 0, 0), q2 = q1, o1 = q1, o2 = q1, v1 = q1, v2 = q1;
     if (r < n) {
-      int t, ks;
-      float g;
-      row_info(r, t, ks, g);
+      const int t = L.tok[row];
+      const float g = L.g[row];
       const uint16_t* qrow = q + (head_base + t) * D;
       float x1[8], x2[8];
       unpack8(*reinterpret_cast<const uint4*>(qrow + 8 * c), x1);
@@ -534,11 +540,12 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
       }
       q1 = pack8(x1);
       q2 = pack8(x2);
-      const float* drow = dout + (static_cast<size_t>(b) * T + t) * D;
+      const float4* drow = reinterpret_cast<const float4*>(dout + (static_cast<size_t>(b) * T + t) * D);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        x1[e] = g * drow[8 * c + e];
-        x2[e] = g * drow[D / 2 + 8 * c + e];
+      for (int e = 0; e < 2; ++e) {
+        const float4 a = drow[2 * c + e], a2 = drow[D / 8 + 2 * c + e];
+        x1[4 * e] = g * a.x; x1[4 * e + 1] = g * a.y; x1[4 * e + 2] = g * a.z; x1[4 * e + 3] = g * a.w;
+        x2[4 * e] = g * a2.x; x2[4 * e + 1] = g * a2.y; x2[4 * e + 2] = g * a2.z; x2[4 * e + 3] = g * a2.w;
       }
       o1 = pack8(x1);
       o2 = pack8(x2);
@@ -573,14 +580,20 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
     float dd = 0.f, dg = 0.f;
     int ks = -1, t = 0;
     if (r < n) {
-      float g;
-      row_info(r, t, ks, g);
-      const float* hrow = hpack + static_cast<size_t>(seg0 + r) * D;
-      const float* drow = dout + (static_cast<size_t>(b) * T + t) * D;
-      for (int e = part * (D / 4); e < (part + 1) * (D / 4); ++e) {
-        const float hv = hrow[e], dv = drow[e];
-        dg = fmaf(dv, hv, dg);
-        dd = fmaf(bf16_to_f32(f32_to_bf16(g * dv)), hv, dd);
+      t = L.tok[row];
+      ks = L.ks[row];
+      const float g = L.g[row];
+      const float4* hrow = reinterpret_cast<const float4*>(hpack + static_cast<size_t>(seg0 + r) * D);
+      const float4* drow = reinterpret_cast<const float4*>(dout + (static_cast<size_t>(b) * T + t) * D);
+#pragma unroll
+      for (int e4 = part * (D / 16); e4 < (part + 1) * (D / 16); ++e4) {
+        const float4 h4 = hrow[e4], d4 = drow[e4];
+        const float hv[4] = {h4.x, h4.y, h4.z, h4.w}, dv[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          dg = fmaf(dv[i], hv[i], dg);
+          dd = fmaf(bf16_to_f32(f32_to_bf16(g * dv[i])), hv[i], dd);
+        }
       }
     }
     dd += __shfl_xor(dd, 1);
@@ -1172,44 +1185,60 @@ hipError_t launch_attn_bwd(const void* q, const void* k, const void* v, int dtyp
 // Router gradient through the gates (selection fixed): one thread per token.
 // SOFTMAX_SELECTED: dl_j = g_j (dg_j - sum_k g_k dg_k) on the selected heads;
 // SOFTMAX_ALL (and the loss-free balancing gates): dl = a (da - <a, da>).
+// One workgroup per kRouteBwdTokens tokens: one thread per token forms the
+// token's gradient row in LDS (dense, H entries), then the block of rows is
+// written out with consecutive threads on consecutive floats.
+constexpr int kRouteBwdTokens = 128;
 __global__ __launch_bounds__(256) void k_route_bwd(const float* __restrict__ logits,
                                                    const int32_t* __restrict__ topk_idx,
                                                    const float* __restrict__ gates,
                                                    const float* __restrict__ dgates, long BT,
                                                    int H, int K, int gate_mode,
                                                    float* __restrict__ dlogits) {
-  const long tok = static_cast<long>(block_x()) * 256 + thread_x();
-  if (tok >= BT) return;
-  const float* l = logits + tok * H;
-  const int32_t* tk = topk_idx + tok * K;
-  const float* g = gates + tok * K;
-  const float* dg = dgates + tok * K;
-  float* dl = dlogits + tok * H;
-  for (int h = 0; h < H; ++h) dl[h] = 0.f;
-  for (int kk = 0; kk < K; ++kk)
-    if (tk[kk] < 0 || tk[kk] >= H) return;   // not a selection: no gradient
-  if (gate_mode == 0) {
-    float sum = 0.f;
-    for (int kk = 0; kk < K; ++kk) sum = fmaf(g[kk], dg[kk], sum);
-    for (int kk = 0; kk < K; ++kk) dl[tk[kk]] = g[kk] * (dg[kk] - sum);
-  } else {
-    float mx = l[0];
-    for (int h = 1; h < H; ++h) mx = fmaxf(mx, l[h]);
-    float z = 0.f;
-    for (int h = 0; h < H; ++h) z += expf(l[h] - mx);
-    const float iz = 1.f / z;
-    float sum = 0.f;   // <a, da>
-    for (int kk = 0; kk < K; ++kk) sum = fmaf(expf(l[tk[kk]] - mx) * iz, dg[kk], sum);
-    for (int h = 0; h < H; ++h) dl[h] = -expf(l[h] - mx) * iz * sum;
-    for (int kk = 0; kk < K; ++kk) dl[tk[kk]] += expf(l[tk[kk]] - mx) * iz * dg[kk];
+  __shared__ float s_dl[kRouteBwdTokens * 64];
+  const int tid = thread_x();
+  const long tok0 = static_cast<long>(block_x()) * kRouteBwdTokens;
+  const int ntok = static_cast<int>(min(static_cast<long>(kRouteBwdTokens), BT - tok0));
+  for (int i = tid; i < ntok * H; i += 256) s_dl[i] = 0.f;
+  __syncthreads();
+  if (tid < ntok) {
+    const long tok = tok0 + tid;
+    const float* l = logits + tok * H;
+    const int32_t* tk = topk_idx + tok * K;
+    const float* g = gates + tok * K;
+    const float* dg = dgates + tok * K;
+    float* dl = s_dl + tid * H;
+    bool valid = true;
+    for (int kk = 0; kk < K; ++kk) valid &= tk[kk] >= 0 && tk[kk] < H;
+    if (valid) {   // not a selection: no gradient
+      if (gate_mode == 0) {
+        float sum = 0.f;
+        for (int kk = 0; kk < K; ++kk) sum = fmaf(g[kk], dg[kk], sum);
+        for (int kk = 0; kk < K; ++kk) dl[tk[kk]] = g[kk] * (dg[kk] - sum);
+      } else {
+        float mx = l[0];
+        for (int h = 1; h < H; ++h) mx = fmaxf(mx, l[h]);
+        float z = 0.f;
+        for (int h = 0; h < H; ++h) z += expf(l[h] - mx);
+        const float iz = 1.f / z;
+        float sum = 0.f;   // <a, da>
+        for (int kk = 0; kk < K; ++kk) sum = fmaf(expf(l[tk[kk]] - mx) * iz, dg[kk], sum);
+        for (int h = 0; h < H; ++h) dl[h] = -expf(l[h] - mx) * iz * sum;
+        for (int kk = 0; kk < K; ++kk) dl[tk[kk]] += expf(l[tk[kk]] - mx) * iz * dg[kk];
+      }
+    }
   }
+  __syncthreads();
+  float* out = dlogits + tok0 * H;
+  for (int i = tid; i < ntok * H; i += 256) out[i] = s_dl[i];
 }
 
 hipError_t launch_route_bwd(const float* logits, const int32_t* topk_idx, const float* gates,
                             const float* dgates, int B, int T, int H, int K, int gate_mode,
                             float* dlogits, hipStream_t st) {
   const long BT = static_cast<long>(B) * T;
-  k_route_bwd<<<static_cast<unsigned>((BT + 255) / 256), 256, 0, st>>>(
+  if (H > 64) return hipErrorInvalidValue;   // the API allows H <= 64
+  k_route_bwd<<<static_cast<unsigned>((BT + kRouteBwdTokens - 1) / kRouteBwdTokens), 256, 0, st>>>(
       logits, topk_idx, gates, dgates, BT, H, K, gate_mode, dlogits);
   return hipGetLastError();
 }
