@@ -37,6 +37,12 @@ Readings where the paper is silent (each also listed in the design notes):
 * R6 decode caches hold keys after rotation, in rank order; the new token
   takes rank n (its head's current length) and attends to itself.
 * R7 sequences of a batch are independent (ranks restart per sequence).
+* R16 routed projections (Eq. namoh-qkv and the output aggregation of Eq.
+  namoh-attention with W_O^(i) kept): per-head weights are stored as linear
+  maps out x in, W_QKV [H, 3, d, d_model] (rows 0 / 1 / 2: query, key,
+  value; q_{t,i} = x_t W_QKV[i, 0]^T, the paper's x_t W_Q^(i)) and
+  W_O [H, d_model, d] (h_{t,i} W_O^(i) = h_{t,i} W_O[i]^T).  Only routed
+  (token, head) pairs are projected.
 * R12 loss-free balancing selects by float32(a + b) with the affinities a
   formed in float64; equal scores go to the lower head index; the gates are
   a (the paper fixes no precision for the selection; one rounding step both
@@ -57,6 +63,7 @@ __all__ = [
     "attention_gathered", "combine_packed", "combine_dense", "prefill",
     "prefill_rows", "prefill_cache", "decode_step", "brute_force_layer", "interaction_count",
     "attention_backward", "gates_backward",
+    "qkv_projection", "output_projection",
     "shared_head_counts",
 ]
 
@@ -267,6 +274,48 @@ def combine_dense(h_dense, topk_idx, gates):
         hk = topk_idx[:, :, kk].astype(np.int64)
         sel = h_dense[np.arange(B)[:, None], hk, np.arange(T)[None, :]]
         o += gates[:, :, kk, None] * sel
+    return o
+
+
+# ----------------------------------------------------------------------------
+# Routed projections: Sec. 3.1, Eq. (namoh-qkv) and the output aggregation of
+# Eq. (namoh-attention), R16
+
+def qkv_projection(x, w_qkv, topk_idx):
+    """Queries, keys and values of the routed (token, head) pairs only.
+
+    x [B, T, d_model]; w_qkv [H, 3, d, d_model] (linear maps out x in).
+    Returns q, k, v [B, H, T, d] and the membership mask m [B, T, H]; rows of
+    pairs with m = 0 are NaN (such pairs produce no vectors, Eq. namoh-qkv)."""
+    B, T, dm = x.shape
+    H, three, d, dm2 = w_qkv.shape
+    assert three == 3 and dm2 == dm
+    m = membership(topk_idx, H)
+    out = [np.full((B, H, T, d), np.nan) for _ in range(3)]
+    for b in range(B):
+        for i in range(H):
+            rows = np.nonzero(m[b, :, i])[0]          # the ordered index set I_i
+            if rows.size == 0:
+                continue
+            xi = x[b, rows]                             # dispatch before projection
+            for j in range(3):
+                out[j][b, i, rows] = xi @ w_qkv[i, j].T
+    return out[0], out[1], out[2], m
+
+
+def output_projection(h_dense, topk_idx, gates, w_o):
+    """o_t = sum over the selected heads i of g_{t,i} h_{t,i} W_O^(i).
+
+    h_dense [B, H, T, d] (rows of unselected pairs are never read);
+    w_o [H, d_model, d].  Returns o [B, T, d_model]."""
+    B, H, T, d = h_dense.shape
+    dm = w_o.shape[1]
+    o = np.zeros((B, T, dm))
+    for b in range(B):
+        for t in range(T):
+            for kk in range(topk_idx.shape[-1]):
+                i = int(topk_idx[b, t, kk])
+                o[b, t] += gates[b, t, kk] * (w_o[i] @ h_dense[b, i, t])
     return o
 
 

@@ -601,3 +601,105 @@ def test_attention_backward_matches_autograd():
     np.testing.assert_allclose(tk.grad.numpy(), dk, atol=1e-11)
     np.testing.assert_allclose(tv.grad.numpy(), dv, atol=1e-11)
     np.testing.assert_allclose(tg.grad.numpy(), dg, atol=1e-11)
+
+
+# ----------------------------------------------------------------------------
+# routed projections (Eq. namoh-qkv; output aggregation of Eq. namoh-attention)
+
+def _proj_case(seed, B=2, T=9, H=4, K=2, d=4, dm=6):
+    g = np.random.default_rng(seed)
+    logits = g.standard_normal((B, T, H)).astype(np.float32)
+    x = g.standard_normal((B, T, dm))
+    w_qkv = g.standard_normal((H, 3, d, dm))
+    w_o = g.standard_normal((H, dm, d))
+    return logits, x, w_qkv, w_o
+
+
+def test_qkv_projection_all_heads_is_dense_multihead_projection():
+    # K = H: every pair is routed, so the projections are those of standard
+    # multi-head attention, computed here with the concatenated weight matrix
+    logits, x, w_qkv, _ = _proj_case(71, H=3, K=3, d=5, dm=7)
+    B, T, dm = x.shape
+    H, d = 3, 5
+    topk = O.select_heads(logits, 3)
+    q, k, v, m = O.qkv_projection(x, w_qkv, topk)
+    assert m.all()
+    for j, got in enumerate((q, k, v)):
+        w_cat = w_qkv[:, j].reshape(H * d, dm)           # [H*d, d_model]
+        dense = (x.reshape(B * T, dm) @ w_cat.T).reshape(B, T, H, d).transpose(0, 2, 1, 3)
+        np.testing.assert_allclose(got, dense, rtol=1e-12, atol=1e-12)
+
+
+def test_qkv_projection_brute_force_and_unrouted_pairs():
+    logits, x, w_qkv, _ = _proj_case(72)
+    topk = O.select_heads(logits, 2)
+    q, k, v, m = O.qkv_projection(x, w_qkv, topk)
+    B, T, dm = x.shape
+    H, _, d, _ = w_qkv.shape
+    for b in range(B):
+        for t in range(T):
+            sel = [int(i) for i in topk[b, t]]
+            for i in range(H):
+                for j, arr in enumerate((q, k, v)):
+                    if i in sel:
+                        for c in range(d):
+                            want = sum(x[b, t, e] * w_qkv[i, j, c, e] for e in range(dm))
+                            assert abs(arr[b, i, t, c] - want) < 1e-12
+                    else:
+                        assert np.isnan(arr[b, i, t]).all()   # no vectors for inactive pairs
+    # each token is projected into exactly K heads
+    assert (m.sum(-1) == 2).all()
+
+
+def test_output_projection_identity_is_the_combine():
+    # W_O^(i) = I (d_model = d) reduces the aggregation to the gated combine
+    logits, x, w_qkv, _ = _proj_case(73, d=4, dm=4)
+    topk = O.select_heads(logits, 2)
+    gates = O.route_gates(logits, topk, O.GATE_SOFTMAX_SELECTED)
+    h = np.random.default_rng(5).standard_normal((2, 4, 9, 4))
+    eye = np.broadcast_to(np.eye(4), (4, 4, 4)).copy()
+    np.testing.assert_allclose(O.output_projection(h, topk, gates, eye),
+                               O.combine_dense(h, topk, gates), rtol=1e-13, atol=1e-13)
+
+
+def test_output_projection_all_heads_is_dense_output_projection():
+    # K = H: o_t = concat_i(g_{t,i} h_{t,i}) W_O, the standard output
+    # projection with the concatenated [d_model, H*d] weight
+    logits, x, _, w_o = _proj_case(74, H=3, K=3, d=5, dm=7)
+    B, T = 2, 9
+    H, d, dm = 3, 5, 7
+    topk = O.select_heads(logits, 3)
+    gates = O.route_gates(logits, topk, O.GATE_SOFTMAX_SELECTED)
+    h = np.random.default_rng(6).standard_normal((B, H, T, d))
+    g_dense = np.zeros((B, T, H))
+    np.put_along_axis(g_dense, topk.astype(np.int64), gates, axis=-1)
+    gh = (h * g_dense.transpose(0, 2, 1)[..., None]).transpose(0, 2, 1, 3).reshape(B, T, H * d)
+    w_cat = w_o.transpose(1, 0, 2).reshape(dm, H * d)
+    np.testing.assert_allclose(O.output_projection(h, topk, gates, w_o), gh @ w_cat.T,
+                               rtol=1e-12, atol=1e-12)
+
+
+def test_projected_layer_reads_only_routed_pairs():
+    # the unrouted rows of q/k/v are NaN: a layer that read any of them would
+    # return NaN; the gathered attention and the aggregation read none
+    logits, x, w_qkv, w_o = _proj_case(75, B=2, T=13, H=5, K=2, d=4, dm=6)
+    topk = O.select_heads(logits, 2)
+    q, k, v, _ = O.qkv_projection(x, w_qkv, topk)
+    ref = O.prefill(logits, q, k, v, 2, 1e4)
+    H = 5
+    h = np.full(q.shape, np.nan)
+    n, off, perm, slot = O.permutation(topk, H)
+    for sid in range(2 * H):
+        b, i = divmod(sid, H)
+        a, e = int(off[sid]), int(off[sid + 1])
+        h[b, i, perm[a:e]] = ref["head_out"][a:e]
+    o = O.output_projection(h, topk, ref["gates"], w_o)
+    assert np.isfinite(o).all()
+    # and the aggregation equals the packed form: per routed row h W_O^(i),
+    # then the gated combine over the K slots
+    y = np.zeros((int(off[-1]), w_o.shape[1]))
+    for sid in range(2 * H):
+        b, i = divmod(sid, H)
+        a, e = int(off[sid]), int(off[sid + 1])
+        y[a:e] = ref["head_out"][a:e] @ w_o[i].T
+    np.testing.assert_allclose(O.combine_packed(y, slot, ref["gates"]), o, rtol=1e-12, atol=1e-12)
