@@ -206,6 +206,85 @@ def cpu_baseline_prefill(w, inp, head_len, budget_s):
 
 
 # ----------------------------------------------------------------------------
+def bench_layer(w, args, torch, L, DI):
+    """The layer with its routed projections: route, Q/K/V projections of
+    the routed pairs, routed attention (head outputs), output projections of
+    the routed pairs with the gated combine."""
+    dev = torch.device("cuda:0")
+    log(f"generating inputs for {w.name}")
+    inp = W.projection_inputs(w)
+    logits = torch.from_numpy(inp["logits"]).to(dev)
+    x, wq, wo = (DI.to_device(inp[n], "bf16", dev) for n in ("x", "w_qkv", "w_o"))
+    B, T, H, K, d, dm = w.B, w.T, w.H, w.K, w.d, w.d_model
+    routing = L.route(logits, K)
+    rws = L.workspace(L.route_workspace_size(B, T, H, K), dev)
+    qkv = {n: torch.empty(B, H, T, d, dtype=torch.bfloat16, device=dev) for n in ("q", "k", "v")}
+    aws = L.workspace(L.attn_workspace_size(B, T, H, K, d, L.BF16), dev)
+    ho = torch.empty(B * T * K, d, dtype=torch.float32, device=dev)
+    ows = L.workspace(L.out_proj_workspace_size(B, T, H, K, dm), dev)
+    out = torch.empty(B, T, dm, dtype=torch.bfloat16, device=dev)
+
+    def step():
+        L.route(logits, K, L.GATE_SOFTMAX_SELECTED, out=routing, ws=rws)
+        L.qkv_proj(x, wq, routing, H, K, out=qkv)
+        L.attn_fwd(qkv["q"], qkv["k"], qkv["v"], routing, K, w.rope_base, head_out=ho, out=False,
+                   ws=aws)
+        L.out_proj(ho, wo, routing, B, T, H, K, out=out, ws=ows)
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    n = routing["head_len"].cpu().numpy().astype(np.int64)
+    Nr = B * T * K
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    L.profile_enable(args.steps)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    kern = {}
+    for sec in ("qkv_proj", "pack", "attn", "out_proj", "out_combine"):
+        r = L.profile_read(sec)
+        if r is not None and r[1] > 0:
+            kern[sec] = r[0] / r[1]
+    L.profile_enable(0)
+    # algorithmic work: 2 d_model 3d FLOP per routed pair for Q/K/V, 2 d d_model
+    # for the output projection, 4 d sum n(n+1)/2 for the attention
+    f_qkv = 2.0 * Nr * dm * 3 * d
+    f_out = 2.0 * Nr * d * dm
+    f_attn = 4.0 * d * float((n * (n + 1) // 2).sum())
+    qkv_ms = kern.get("qkv_proj", float("nan"))
+    achieved = f_qkv / (qkv_ms * 1e-3) / 1e12
+    res = {"metric": "routed-attn layer with routed projections, tokens/s (1 GPU)",
+           "value": round(B * T / (ms_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic",
+           "config": {"workload": w.name, "B": B, "T": T, "H": H, "K": K, "d_head": d,
+                      "d_model": dm, "rope": "head-relative", "rope_base": w.rope_base,
+                      "gates": "softmax over selected"},
+           "roofline": {"kernel": "k_proj_gemm<QKV>", "bound": "mfma",
+                        "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                        "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                        "traffic": None,
+                        "algorithmic_per_launch": {"flops": f_qkv},
+                        "kernel_ms": round(qkv_ms, 4)},
+           "work": {"qkv_flops": f_qkv, "attn_flops": f_attn, "out_flops": f_out,
+                    "out_rows_bytes": 2.0 * Nr * dm * 2},
+           "kernels_ms": {k2: round(v2, 4) for k2, v2 in kern.items()}}
+    if "out_proj" in kern:
+        res["out_proj_gemm_tflops"] = round(f_out / (kern["out_proj"] * 1e-3) / 1e12, 1)
+    return res
+
+
+# ----------------------------------------------------------------------------
 def bench_backward(w, args, torch, L, DI):
     """One training step of the layer: route, forward, backward of the
     attention (dq, dk, dv, dgates) and of the gates (d logits)."""
@@ -440,6 +519,8 @@ def main():
             print(json.dumps({"error": "--backward needs a prefill workload"}))
             sys.exit(2)
         res = bench_backward(w, args, torch, L, DI)
+    elif w.d_model:
+        res = bench_layer(w, args, torch, L, DI)
     else:
         res = (bench_decode if w.decode else bench_prefill)(w, args, torch, L, DI)
     print(json.dumps(res), flush=True)

@@ -143,7 +143,9 @@ namoh_status namoh_route_bias_update(const int32_t* head_len, int B, int T, int 
  *      softmax_scale  <= 0 selects 1/sqrt(d).
  *      gates, seg_offsets, perm_token, slot_pos: as produced by namoh_route.
  * Out: out         [B, T, d] of `out_dtype`:
- *                  o_t = sum_k gates[b,t,k] * h(t, topk_idx[b,t,k]).
+ *                  o_t = sum_k gates[b,t,k] * h(t, topk_idx[b,t,k]);
+ *                  may be NULL when head_out is given (the combine is then
+ *                  skipped, e.g. before namoh_out_proj).
  *      head_out    optional float32 [B*T*K, d]: ungated head outputs h at
  *                  their packed positions; NULL to skip.
  * bf16 with d in {64, 128} runs on bf16 MFMA (float32 accumulation and
@@ -204,6 +206,50 @@ namoh_status namoh_attn_bwd(const void* q, const void* k, const void* v, int dty
 namoh_status namoh_route_bwd(const float* logits, const int32_t* topk_idx,
                              const float* gates, const float* dgates, int B, int T,
                              int H, int K, int gate_mode, float* dlogits, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Routed per-head projections (Sec. 3.1, Eq. namoh-qkv: tokens are
+ * dispatched to their heads before projection, and only active (token, head)
+ * pairs compute q, k, v; Eq. namoh-attention: o_t = sum over the selected
+ * heads of g_{t,i} h_{t,i} W_O^(i)).  With these two calls around
+ * namoh_attn_fwd the layer keeps its per-head output projections instead of
+ * taking them as the identity.
+ *
+ * Weights are stored as linear maps (out x in), bf16, 16-byte aligned:
+ *   w_qkv [H, 3, d, d_model]: rows 0 / 1 / 2 of head i are its query, key
+ *     and value maps, q_{t,i} = x_t w_qkv[i, 0]^T (the paper's x_t W_Q^(i));
+ *   w_o   [H, d_model, d]: h_{t,i} W_O^(i) = h_{t,i} w_o[i]^T.
+ * Supported: bf16 x and weights, d_head in {64, 128}, d_model a multiple
+ * of 128 (else NAMOH_ERR_UNSUPPORTED).  fp32 accumulation on the matrix
+ * cores; results rounded to bf16 (the output projection's per-pair rows are
+ * rounded to bf16 before the fp32 gated sum).
+ * ---------------------------------------------------------------------- */
+
+/* In:  x [B, T, d_model] bf16; w_qkv as above; seg_offsets, perm_token from
+ *      namoh_route.
+ * Out: q, k, v [B, H, T, d] bf16: the row (b, i, t) is written for every
+ *      routed pair (token t of sequence b selected head i) and no other row
+ *      is touched (namoh_attn_fwd reads only routed rows).  No workspace. */
+namoh_status namoh_qkv_proj(const void* x, const void* w_qkv, int B, int T, int H, int K,
+                            int d_head, int d_model, const int32_t* seg_offsets,
+                            const int32_t* perm_token, void* q, void* k, void* v,
+                            void* stream);
+
+size_t namoh_out_proj_workspace_size(int B, int T, int H, int K, int d_model);
+
+/* In:  head_out [B*T*K, d] packed ungated head outputs (as namoh_attn_fwd
+ *      writes them to its head_out argument), float32 (head_out_dtype
+ *      NAMOH_F32) or bf16; w_o as above; gates, slot_pos, seg_offsets from
+ *      namoh_route.
+ * Out: out [B, T, d_model] of out_dtype: o_t = sum over k in ascending order
+ *      of gates[b,t,k] * (h W_O^(topk_idx[b,t,k])) at the pair's packed row.
+ * Workspace: namoh_out_proj_workspace_size bytes (the per-pair projected rows,
+ *      bf16 [B*T*K, d_model]). */
+namoh_status namoh_out_proj(const void* head_out, int head_out_dtype, const void* w_o,
+                            const float* gates, const int32_t* slot_pos,
+                            const int32_t* seg_offsets, int B, int T, int H, int K, int d_head,
+                            int d_model, void* out, int out_dtype, void* workspace,
+                            size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Prefill -> decode hand-off (Sec. 3.2, efficient execution: decoding reads

@@ -32,6 +32,7 @@ EXPORTED = (
     "namoh_attn_fwd_workspace_size", "namoh_attn_fwd",
     "namoh_prefill_cache", "namoh_attn_bwd_workspace_size", "namoh_attn_bwd", "namoh_route_bwd",
     "namoh_decode_workspace_size", "namoh_decode_step", "namoh_decode_step_biased",
+    "namoh_qkv_proj", "namoh_out_proj_workspace_size", "namoh_out_proj",
     "namoh_status_string", "namoh_last_error", "namoh_version",
     "namoh_profile_enable", "namoh_profile_read",
 )
@@ -60,6 +61,9 @@ _SIGS = {
                                _F, _I, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
     "namoh_decode_step_biased": (_I, [_P, _P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I,
                                       _I, _F, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
+    "namoh_qkv_proj": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P]),
+    "namoh_out_proj_workspace_size": (_S, [_I, _I, _I, _I, _I]),
+    "namoh_out_proj": (_I, [_P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _S, _P]),
     "namoh_status_string": (ctypes.c_char_p, [_I]),
     "namoh_last_error": (ctypes.c_char_p, []),
     "namoh_version": (ctypes.c_char_p, []),
@@ -203,13 +207,18 @@ def attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K
              softmax_scale: float = 0.0, out_dtype: Optional[torch.dtype] = None,
              head_out: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
              ws: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """namoh_attn_fwd on dense q/k/v [B, H, T, d]; returns out [B, T, d]."""
-    _need_cuda(q, k, v, head_out, out)
+    """namoh_attn_fwd on dense q/k/v [B, H, T, d]; returns out [B, T, d].
+    With out_dtype=None and head_out given, pass out=False to skip the
+    combine (returns head_out)."""
+    _need_cuda(q, k, v, head_out, None if out is False else out)
     B, H, T, d = q.shape
     if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
         raise ValueError("q, k, v must share shape and dtype")
     dt = dtype_code(q.dtype)
     odt = q.dtype if out_dtype is None else out_dtype
+    skip = out is False
+    if skip and head_out is None:
+        raise ValueError("out=False needs head_out")
     if out is None:
         out = torch.empty(B, T, d, dtype=odt, device=q.device)
     if ws is None:
@@ -218,9 +227,10 @@ def attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K
                                float(rope_base), rope_mode, float(softmax_scale),
                                _ptr(routing["gates"]), _ptr(routing["seg_offsets"]),
                                _ptr(routing["perm_token"]), _ptr(routing["slot_pos"]),
-                               _ptr(out), dtype_code(out.dtype), _ptr(head_out),
-                               _ptr(ws), ws.numel(), _stream(q.device)))
-    return out
+                               None if skip else _ptr(out),
+                               dtype_code(odt) if skip else dtype_code(out.dtype),
+                               _ptr(head_out), _ptr(ws), ws.numel(), _stream(q.device)))
+    return head_out if skip else out
 
 
 def prefill_cache(k: torch.Tensor, v: torch.Tensor, r: dict, K: int, rope_base: float,
@@ -288,6 +298,58 @@ def route_bwd(logits: torch.Tensor, routing: dict, dgates: torch.Tensor,
                                 _ptr(dgates), B, T, H, K, gate_mode, _ptr(dl),
                                 _stream(logits.device)))
     return dl
+
+
+def qkv_proj(x: torch.Tensor, w_qkv: torch.Tensor, routing: dict, H: int, K: int,
+             out: Optional[dict] = None) -> dict:
+    """namoh_qkv_proj: q, k, v [B, H, T, d] (bf16) of the routed pairs from
+    x [B, T, d_model] and w_qkv [H, 3, d, d_model] (bf16).  Rows of unrouted
+    pairs are left as they are (uninitialised unless `out` is given)."""
+    _need_cuda(x, w_qkv)
+    if x.dtype != torch.bfloat16 or w_qkv.dtype != torch.bfloat16:
+        raise ValueError("x and w_qkv must be bfloat16")
+    B, T, dm = x.shape
+    if w_qkv.dim() != 4 or w_qkv.shape[0] != H or w_qkv.shape[1] != 3 or w_qkv.shape[3] != dm:
+        raise ValueError("w_qkv must be [H, 3, d, d_model]")
+    d = w_qkv.shape[2]
+    if out is None:
+        out = {n: torch.empty(B, H, T, d, dtype=torch.bfloat16, device=x.device)
+               for n in ("q", "k", "v")}
+    for n in ("q", "k", "v"):
+        _need_cuda(out[n])
+        if out[n].dtype != torch.bfloat16 or tuple(out[n].shape) != (B, H, T, d):
+            raise ValueError(f"out[{n!r}] must be bfloat16 [B, H, T, d]")
+    check(lib().namoh_qkv_proj(_ptr(x), _ptr(w_qkv), B, T, H, K, d, dm,
+                               _ptr(routing["seg_offsets"]), _ptr(routing["perm_token"]),
+                               _ptr(out["q"]), _ptr(out["k"]), _ptr(out["v"]), _stream(x.device)))
+    return out
+
+
+def out_proj_workspace_size(B, T, H, K, d_model) -> int:
+    return int(lib().namoh_out_proj_workspace_size(B, T, H, K, d_model))
+
+
+def out_proj(head_out: torch.Tensor, w_o: torch.Tensor, routing: dict, B: int, T: int, H: int,
+             K: int, out_dtype: torch.dtype = torch.float32, out: Optional[torch.Tensor] = None,
+             ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """namoh_out_proj: o [B, T, d_model] = sum_k gate * (h W_O^(i)) from the
+    packed head outputs head_out [B*T*K, d] (float32 or bf16) and
+    w_o [H, d_model, d] (bf16)."""
+    _need_cuda(head_out, w_o, out)
+    if w_o.dtype != torch.bfloat16 or w_o.dim() != 3 or w_o.shape[0] != H:
+        raise ValueError("w_o must be bfloat16 [H, d_model, d]")
+    dm, d = w_o.shape[1], w_o.shape[2]
+    if tuple(head_out.shape) != (B * T * K, d):
+        raise ValueError("head_out must be [B*T*K, d]")
+    if out is None:
+        out = torch.empty(B, T, dm, dtype=out_dtype, device=w_o.device)
+    if ws is None:
+        ws = workspace(out_proj_workspace_size(B, T, H, K, dm), w_o.device)
+    check(lib().namoh_out_proj(_ptr(head_out), dtype_code(head_out.dtype), _ptr(w_o),
+                               _ptr(routing["gates"]), _ptr(routing["slot_pos"]),
+                               _ptr(routing["seg_offsets"]), B, T, H, K, d, dm, _ptr(out),
+                               dtype_code(out.dtype), _ptr(ws), ws.numel(), _stream(w_o.device)))
+    return out
 
 
 def decode_workspace_size(B, H, K, d, cap) -> int:

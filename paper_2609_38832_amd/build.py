@@ -20,7 +20,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libnamoh.so")
 ARCH = "gfx950"
 
-SOURCES = ["route.hip", "attn.hip", "decode.hip", "bwd.hip", "api.cpp", "profile.cpp"]
+SOURCES = ["route.hip", "attn.hip", "decode.hip", "bwd.hip", "proj.hip", "api.cpp", "profile.cpp"]
 
 COMMON = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

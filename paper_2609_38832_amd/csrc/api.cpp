@@ -205,7 +205,8 @@ namoh_status namoh_attn_fwd(const void* q, const void* k, const void* v, int dty
   REQUIRE_PTR(seg_offsets, 4);
   REQUIRE_PTR(perm_token, 4);
   REQUIRE_PTR(slot_pos, 4);
-  REQUIRE_PTR(out, 16);
+  REQUIRE(out != nullptr || head_out != nullptr, "out and head_out are both NULL");
+  if (out != nullptr) REQUIRE_PTR(out, 16);
   if (head_out != nullptr) REQUIRE_PTR(head_out, 16);
   if ((s = check_workspace(workspace, workspace_bytes,
                            namoh::attn_workspace_bytes(B, T, H, K, d_head, dtype))) != NAMOH_OK)
@@ -246,6 +247,69 @@ namoh_status namoh_prefill_cache(const void* k, const void* v, int dtype, int B,
                                                 rope_mode, seg_offsets, perm_token, k_cache,
                                                 v_cache, cache_len, cap,
                                                 static_cast<hipStream_t>(stream)));
+}
+
+namespace {
+namoh_status check_proj(int B, int T, int H, int K, int d_head, int d_model) {
+  namoh_status s;
+  if ((s = check_sizes(B, T, H, K)) != NAMOH_OK) return s;
+  if (d_head != 64 && d_head != 128)
+    return fail(NAMOH_ERR_UNSUPPORTED, "projections need d_head 64 or 128 (got %d)", d_head);
+  if (d_model < 128 || d_model % 128 != 0 || d_model > 65536)
+    return fail(NAMOH_ERR_UNSUPPORTED, "d_model must be a multiple of 128 in [128, 65536] (got %d)",
+                d_model);
+  REQUIRE(static_cast<long long>(B) * T * K * d_model < (1ll << 40), "projection too large");
+  REQUIRE(static_cast<long long>(B) * H * T * d_head < (1ll << 40), "q/k/v too large");
+  return NAMOH_OK;
+}
+}  // namespace
+
+namoh_status namoh_qkv_proj(const void* x, const void* w_qkv, int B, int T, int H, int K,
+                            int d_head, int d_model, const int32_t* seg_offsets,
+                            const int32_t* perm_token, void* q, void* k, void* v, void* stream) {
+  namoh_status s;
+  if ((s = check_proj(B, T, H, K, d_head, d_model)) != NAMOH_OK) return s;
+  REQUIRE_PTR(x, 16);
+  REQUIRE_PTR(w_qkv, 16);
+  REQUIRE_PTR(seg_offsets, 4);
+  REQUIRE_PTR(perm_token, 4);
+  REQUIRE_PTR(q, 16);
+  REQUIRE_PTR(k, 16);
+  REQUIRE_PTR(v, 16);
+  clear_hip_error();
+  return hip_status(namoh::launch_qkv_proj(x, w_qkv, B, T, H, K, d_head, d_model, seg_offsets,
+                                           perm_token, q, k, v, static_cast<hipStream_t>(stream)));
+}
+
+size_t namoh_out_proj_workspace_size(int B, int T, int H, int K, int d_model) {
+  if (check_proj(B, T, H, K, 64, d_model) != NAMOH_OK) return 0;
+  return namoh::out_proj_workspace_bytes(B, T, K, d_model);
+}
+
+namoh_status namoh_out_proj(const void* head_out, int head_out_dtype, const void* w_o,
+                            const float* gates, const int32_t* slot_pos,
+                            const int32_t* seg_offsets, int B, int T, int H, int K, int d_head,
+                            int d_model, void* out, int out_dtype, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  namoh_status s;
+  if ((s = check_proj(B, T, H, K, d_head, d_model)) != NAMOH_OK) return s;
+  REQUIRE(head_out_dtype == NAMOH_F32 || head_out_dtype == NAMOH_BF16,
+          "unknown head_out_dtype %d", head_out_dtype);
+  REQUIRE(out_dtype == NAMOH_F32 || out_dtype == NAMOH_BF16, "unknown out_dtype %d", out_dtype);
+  REQUIRE_PTR(head_out, 16);
+  REQUIRE_PTR(w_o, 16);
+  REQUIRE_PTR(gates, 4);
+  REQUIRE_PTR(slot_pos, 4);
+  REQUIRE_PTR(seg_offsets, 4);
+  REQUIRE_PTR(out, 16);
+  if ((s = check_workspace(workspace, workspace_bytes,
+                           namoh::out_proj_workspace_bytes(B, T, K, d_model))) != NAMOH_OK)
+    return s;
+  clear_hip_error();
+  return hip_status(namoh::launch_out_proj(head_out, head_out_dtype, w_o, gates, slot_pos,
+                                           seg_offsets, B, T, H, K, d_head, d_model, out,
+                                           out_dtype, workspace,
+                                           static_cast<hipStream_t>(stream)));
 }
 
 size_t namoh_attn_bwd_workspace_size(int B, int T, int H, int K, int d_head) {

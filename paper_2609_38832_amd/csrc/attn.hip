@@ -344,12 +344,25 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
     for (int i = tid; i <= BH; i += kPackThreads) L.pack.off[i] = seg_offsets[i];
   __syncthreads();
   const int32_t* off = in_lds ? L.pack.off : seg_offsets;
-  int lo = 0, hi = BH;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (seg_tile0(off[mid], mid) <= gt) lo = mid; else hi = mid;
+  int s;
+  if (in_lds) {
+    // seg_tile0(off[s], s) increases strictly with s, so the segment is the
+    // number of segments whose first tile is at most gt, minus one: one
+    // ballot per 64 segments (every wave computes it; no barrier)
+    int cnt = 0;
+    for (int s0 = 0; s0 < BH; s0 += kWave) {
+      const int si = s0 + tid % kWave;
+      cnt += __popcll(__ballot(si < BH && seg_tile0(off[si], si) <= gt));
+    }
+    s = cnt - 1;
+  } else {
+    int lo = 0, hi = BH;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (seg_tile0(off[mid], mid) <= gt) lo = mid; else hi = mid;
+    }
+    s = lo;
   }
-  const int s = lo;
   const int seg0 = off[s];
   const int n = off[s + 1] - seg0;
   const int r0 = (gt - seg_tile0(seg0, s)) * kBN;
@@ -360,32 +373,58 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
   const int b = s / H, h = s - (s / H) * H;
   const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
 
-  constexpr int HP = D / 16;  // 8-element granule pairs (j, j + d/2) per row
-  static_assert(kPackThreads % HP == 0 && kWave % HP == 0, "a row's units share one wave");
-  float rmax = 0.f;   // largest squared norm of a packed (rounded) key row seen
-  for (int u = tid; u < kBN * HP; u += kPackThreads) {
-    const int row = u / HP, c = u - (u / HP) * HP;
+  // Every load of the tile is issued before any of them is used: the
+  // thread's rows' tokens, then its key granule pairs and value granules.
+  constexpr int HP = D / 16;  // 8-element granule pairs (j, j + d/2) per key row
+  constexpr int RG = D / 8;   // 16-byte granules per value row
+  constexpr int KU = kBN * HP / kPackThreads, VU = kBN * RG / kPackThreads;
+  static_assert(KU * kPackThreads == kBN * HP && VU * kPackThreads == kBN * RG, "units");
+  static_assert(kWave % HP == 0, "a key row's units share one wave");
+  auto token_of = [&](int row) {   // -1 past the segment's end
     const int r = r0 + row;
-    float x1[8], x2[8];
-    uint4 o1 = make_uint4(0, 0, 0, 0), o2 = o1;
-    if (r < n) {
-      const int t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
-      const uint16_t* src = k + (head_base + t) * D;
-      const uint4 a = *reinterpret_cast<const uint4*>(src + 8 * c);
-      const uint4 bb = *reinterpret_cast<const uint4*>(src + D / 2 + 8 * c);
-      if (rope_mode != 2) {
-        unpack8(a, x1);
-        unpack8(bb, x2);
-        const int pos = rope_mode == 0 ? r : t;
-        float4 cs[4];
-        rope8_rev(cs, static_cast<double>(pos), &L.pack.freq[8 * c]);
-        rope8(x1, x2, cs);
-        o1 = pack8(x1);
-        o2 = pack8(x2);
-      } else {
-        o1 = a;
-        o2 = bb;
-      }
+    return r < n ? static_cast<int>(min(static_cast<unsigned>(perm_token[seg0 + r]),
+                                        static_cast<unsigned>(T - 1)))
+                 : -1;
+  };
+  int ktok[KU], vtok[VU];
+#pragma unroll
+  for (int i = 0; i < KU; ++i) ktok[i] = token_of((tid + i * kPackThreads) / HP);
+#pragma unroll
+  for (int i = 0; i < VU; ++i) vtok[i] = token_of((tid + i * kPackThreads) / RG);
+  uint4 ka[KU], kb[KU], vx[VU];
+#pragma unroll
+  for (int i = 0; i < KU; ++i) {
+    const int c = (tid + i * kPackThreads) % HP;
+    ka[i] = kb[i] = make_uint4(0, 0, 0, 0);
+    if (ktok[i] >= 0) {
+      const uint16_t* src = k + (head_base + ktok[i]) * D;
+      ka[i] = *reinterpret_cast<const uint4*>(src + 8 * c);
+      kb[i] = *reinterpret_cast<const uint4*>(src + D / 2 + 8 * c);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < VU; ++i) {
+    const int gr = (tid + i * kPackThreads) % RG;
+    vx[i] = make_uint4(0, 0, 0, 0);
+    if (vtok[i] >= 0) vx[i] = *reinterpret_cast<const uint4*>(v + (head_base + vtok[i]) * D + 8 * gr);
+  }
+
+  float rmax = 0.f;   // largest squared norm of a packed (rounded) key row seen
+#pragma unroll
+  for (int i = 0; i < KU; ++i) {
+    const int u = tid + i * kPackThreads;
+    const int row = u / HP, c = u % HP;
+    uint4 o1 = ka[i], o2 = kb[i];
+    if (ktok[i] >= 0 && rope_mode != 2) {
+      float x1[8], x2[8];
+      unpack8(ka[i], x1);
+      unpack8(kb[i], x2);
+      const int pos = rope_mode == 0 ? r0 + row : ktok[i];
+      float4 cs[4];
+      rope8_rev(cs, static_cast<double>(pos), &L.pack.freq[8 * c]);
+      rope8(x1, x2, cs);
+      o1 = pack8(x1);
+      o2 = pack8(x2);
     }
     uint16_t* dst = Kp + (static_cast<size_t>(gt) * kBN + row) * D;
     *reinterpret_cast<uint4*>(dst + 8 * c) = o1;
@@ -401,16 +440,10 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
 #pragma unroll
   for (int o = HP; o < kWave; o <<= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, o));
   if (tid % kWave == 0) L.pack.wnorm[tid / kWave] = rmax;
-  constexpr int RG = D / 8;  // granules per value row
-  for (int u = tid; u < kBN * RG; u += kPackThreads) {
-    const int row = u / RG, gr = u - (u / RG) * RG;
-    const int r = r0 + row;
-    uint4 x = make_uint4(0, 0, 0, 0);
-    if (r < n) {
-      const int t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
-      x = *reinterpret_cast<const uint4*>(v + (head_base + t) * D + 8 * gr);
-    }
-    *reinterpret_cast<uint4*>(&sv[row][8 * gr]) = x;
+#pragma unroll
+  for (int i = 0; i < VU; ++i) {
+    const int u = tid + i * kPackThreads;
+    *reinterpret_cast<uint4*>(&sv[u / RG][8 * (u % RG)]) = vx[i];
   }
   __syncthreads();
   if (tid == 0) {
@@ -1025,18 +1058,21 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
   for (int e = 0; e < 8; ++e) acc[e] = 0.f;
   const int32_t* sp = slot_pos + tok * K;
   const float* gp = gates + tok * K;
-  for (int k0 = 0; k0 < K; k0 += 4) {
-    int p[4];
-    float gk[4];
-    float x[4][8];
+  // rounds of KC selected heads: their slots and gates, then all their head
+  // rows in flight at once; the sum runs over k in ascending order
+  constexpr int KC = 8;
+  for (int k0 = 0; k0 < K; k0 += KC) {
+    int p[KC];
+    float gk[KC];
+    float x[KC][8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < KC; ++i) {
       const bool in = k0 + i < K;
       p[i] = in ? sp[k0 + i] : -1;
       gk[i] = in ? gp[k0 + i] : 0.f;
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < KC; ++i) {
       if (static_cast<unsigned>(p[i]) < static_cast<unsigned>(Nr)) {
         if constexpr (IN_BF16) {
           const uint4 u =
@@ -1056,7 +1092,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
       }
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < KC; ++i)
       if (k0 + i < K)
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] = fmaf(gk[i], x[i][e], acc[e]);
@@ -1217,6 +1253,7 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
 #undef NAMOH_GEN
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (out == nullptr) return hipSuccess;   // head outputs only
   const long BT = static_cast<long>(B) * T;
   const long threads = BT * (d / 8);
   const unsigned grid = static_cast<unsigned>((threads + kCombineThreads - 1) / kCombineThreads);
@@ -1230,6 +1267,18 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   else
     k_combine<false, false><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
   prof_mark("combine", false, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_rows(const uint16_t* rows, const float* gates, const int32_t* slot_pos,
+                               long BT, int K, int D, int Nr, void* out, int out_dtype,
+                               hipStream_t st) {
+  const long threads = BT * (D / 8);
+  const unsigned grid = static_cast<unsigned>((threads + kCombineThreads - 1) / kCombineThreads);
+  if (out_dtype == 1)
+    k_combine<true, true><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D, Nr, out);
+  else
+    k_combine<true, false><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D, Nr, out);
   return hipGetLastError();
 }
 

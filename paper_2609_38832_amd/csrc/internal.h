@@ -64,6 +64,22 @@ hipError_t launch_attn_stats(const void* q, const void* k, const void* v, int B,
                              const int32_t* seg_offsets, const int32_t* perm_token, float* lse,
                              void* ws, AttnTiles& tiles, hipStream_t st);
 
+// Gated combine of bf16 rows [Nr, D]: out[t] = sum_k gates[t,k] rows[slot_pos[t,k]]
+// (attn.hip; D a multiple of 8).
+hipError_t launch_combine_rows(const uint16_t* rows, const float* gates, const int32_t* slot_pos,
+                               long BT, int K, int D, int Nr, void* out, int out_dtype,
+                               hipStream_t st);
+
+// ---- routed projections (proj.hip) ---------------------------------------
+hipError_t launch_qkv_proj(const void* x, const void* w_qkv, int B, int T, int H, int K, int d,
+                           int d_model, const int32_t* seg_offsets, const int32_t* perm_token,
+                           void* q, void* k, void* v, hipStream_t st);
+size_t out_proj_workspace_bytes(int B, int T, int K, int d_model);
+hipError_t launch_out_proj(const void* head_out, int head_out_dtype, const void* w_o,
+                           const float* gates, const int32_t* slot_pos,
+                           const int32_t* seg_offsets, int B, int T, int H, int K, int d,
+                           int d_model, void* out, int out_dtype, void* ws, hipStream_t st);
+
 // ---- decode (decode.hip) --------------------------------------------------
 size_t decode_workspace_bytes(int B, int H, int K, int d, int cap);
 // bias: NULL for the plain selection, else [H] loss-free balancing biases

@@ -11,7 +11,10 @@ Recipe (every tensor is drawn independently):
   (``h`` = 0 for tensors that are not per-head), ``seed = 260938832 + workload
   index`` for the named workloads;
 * tensor ids: logits 0, q 1, k 2, v 3, decode-cache keys 4, decode-cache
-  values 5, decode new-token q/k/v 6/7/8, prior-history routing 9;
+  values 5, decode new-token q/k/v 6/7/8, prior-history routing 9; for the
+  layer with projections: token inputs x 10, per-head projection weights
+  W_QKV 11 and W_O 12 (x N(0,1), W_QKV N(0,1)/sqrt(d_model), W_O
+  N(0,1)/sqrt(d), all bf16);
 * draws: ``standard_normal`` in float32, multiplied by the float32 scale, then
   rounded to bfloat16 (round to nearest even) for bf16 tensors;
 * logits: float32 N(0,1); the skewed workload adds the per-head bias
@@ -39,6 +42,7 @@ TID_LOGITS, TID_Q, TID_K, TID_V = 0, 1, 2, 3
 TID_KCACHE, TID_VCACHE = 4, 5
 TID_DEC_Q, TID_DEC_K, TID_DEC_V = 6, 7, 8
 TID_PRIOR = 9
+TID_X, TID_WQKV, TID_WO = 10, 11, 12
 
 
 @dataclass(frozen=True)
@@ -57,6 +61,7 @@ class Workload:
     prior: int = 0               # decode: routed prior tokens per sequence
     seed: int = BASE_SEED
     decode: bool = False
+    d_model: int = 0             # > 0: the layer with its per-head projections
 
     def with_(self, **kw) -> "Workload":
         return replace(self, **kw)
@@ -78,6 +83,12 @@ WORKLOADS = {
     5: Workload("decode_bf16_B64_prior131072_H64_K8_d128", B=64, T=1, H=64,
                 K=8, d=128, dtype="bf16", qkv_scale=1 / math.sqrt(128),
                 rope_base=5e5, prior=131072, seed=BASE_SEED + 5, decode=True),
+    # the balanced prefill shape with the paper's model width (Sec. 4.1:
+    # d_model 2048, head width 64, 32 heads with 8 active): routed Q/K/V
+    # projections, attention, routed output projections
+    6: Workload("layer_bf16_B4_T4096_H32_K8_d64_dm2048", B=4, T=4096, H=32, K=8,
+                d=64, dtype="bf16", qkv_scale=1 / 8, rope_base=1e4,
+                seed=BASE_SEED + 6, d_model=2048),
 }
 
 
@@ -170,6 +181,22 @@ def prefill_qkv(w: Workload, which: str) -> np.ndarray:
 def prefill_inputs(w: Workload) -> dict:
     return {"logits": prefill_logits(w), "q": prefill_qkv(w, "q"),
             "k": prefill_qkv(w, "k"), "v": prefill_qkv(w, "v")}
+
+
+def projection_inputs(w: Workload) -> dict:
+    """Token inputs x [B, T, d_model] and the per-head weights stored as
+    linear maps (out x in): w_qkv [H, 3, d, d_model] (query, key, value rows)
+    and w_o [H, d_model, d]; all bf16 bit patterns (uint16)."""
+    dm = w.d_model
+    x = np.empty((w.B, w.T, dm), dtype=np.uint16)
+    for b in range(w.B):
+        x[b] = normal_block(w.seed, TID_X, b, 0, (w.T, dm), 1.0, "bf16")
+    w_qkv = np.empty((w.H, 3, w.d, dm), dtype=np.uint16)
+    w_o = np.empty((w.H, dm, w.d), dtype=np.uint16)
+    for h in range(w.H):
+        w_qkv[h] = normal_block(w.seed, TID_WQKV, 0, h, (3, w.d, dm), 1.0 / math.sqrt(dm), "bf16")
+        w_o[h] = normal_block(w.seed, TID_WO, 0, h, (dm, w.d), 1.0 / math.sqrt(w.d), "bf16")
+    return {"logits": prefill_logits(w), "x": x, "w_qkv": w_qkv, "w_o": w_o}
 
 
 # ----------------------------------------------------------------------------

@@ -199,6 +199,38 @@ def test_route_bwd_rejects(lib, kw, code):
                                a["gate"], a["dl"], None) == code
 
 
+def _qkv(lib, B=2, T=64, H=8, K=2, d=64, dm=256, x=fake(0), w=fake(1), so=fake(2), q=fake(4)):
+    return lib.namoh_qkv_proj(x, w, B, T, H, K, d, dm, so, fake(3), q, fake(5), fake(6), None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(d=32), 2), (dict(d=48), 2), (dict(dm=192), 2), (dict(dm=0), 2), (dict(x=None), 1),
+    (dict(w=P(A + 8)), 1), (dict(so=None), 1), (dict(q=P(A + 2)), 1), (dict(K=9), 1),
+    (dict(H=65, K=1), 1),
+])
+def test_qkv_proj_rejects(lib, kw, code):
+    assert _qkv(lib, **kw) == code
+
+
+def _oproj(lib, B=2, T=64, H=8, K=2, d=64, dm=256, h=fake(0), hdt=0, odt=0, out=fake(5),
+           wsb=1 << 30, ws=fake(6)):
+    return lib.namoh_out_proj(h, hdt, fake(1), fake(2), fake(3), fake(4), B, T, H, K, d, dm, out,
+                              odt, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(d=32), 2), (dict(dm=200), 2), (dict(hdt=2), 1), (dict(odt=5), 1), (dict(h=None), 1),
+    (dict(out=P(A + 4)), 1), (dict(wsb=1024), 3), (dict(ws=None), 3), (dict(K=0), 1),
+])
+def test_out_proj_rejects(lib, kw, code):
+    assert _oproj(lib, **kw) == code
+
+
+def test_out_proj_workspace_size(lib):
+    assert lib.namoh_out_proj_workspace_size(4, 4096, 32, 8, 2048) >= 4 * 4096 * 8 * 2048 * 2
+    assert lib.namoh_out_proj_workspace_size(4, 4096, 32, 8, 100) == 0
+
+
 def test_workspace_queries(lib):
     assert lib.namoh_route_workspace_size(0, 10, 8, 2) == 0
     assert lib.namoh_route_workspace_size(1, 10, 8, 2) > 0
