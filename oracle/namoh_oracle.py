@@ -43,6 +43,12 @@ Readings where the paper is silent (each also listed in the design notes):
   value; q_{t,i} = x_t W_QKV[i, 0]^T, the paper's x_t W_Q^(i)) and
   W_O [H, d_model, d] (h_{t,i} W_O^(i) = h_{t,i} W_O[i]^T).  Only routed
   (token, head) pairs are projected.
+* R17 KV-group routing (App. "GQA+NAMOH", adopted KV-group routing): the
+  H query heads form H/g groups of g consecutive heads (group j holds heads
+  j*g .. j*g + g - 1) sharing one key/value head; the router selects K/g of
+  the H/g groups (same selection rule), all g query heads of a selected
+  group attend over the group's subsequence with the group's gate, and RoPE
+  uses the group-local rank for the queries and the shared key.
 * R12 loss-free balancing selects by float32(a + b) with the affinities a
   formed in float64; equal scores go to the lower head index; the gates are
   a (the paper fixes no precision for the selection; one rounding step both
@@ -64,6 +70,7 @@ __all__ = [
     "prefill_rows", "prefill_cache", "decode_step", "brute_force_layer", "interaction_count",
     "attention_backward", "gates_backward",
     "qkv_projection", "output_projection",
+    "attention_kv_groups", "combine_kv_groups",
     "shared_head_counts",
 ]
 
@@ -316,6 +323,74 @@ def output_projection(h_dense, topk_idx, gates, w_o):
             for kk in range(topk_idx.shape[-1]):
                 i = int(topk_idx[b, t, kk])
                 o[b, t] += gates[b, t, kk] * (w_o[i] @ h_dense[b, i, t])
+    return o
+
+
+# ----------------------------------------------------------------------------
+# KV-group routing (App. GQA+NAMOH, adopted KV-group routing), R17
+
+def attention_kv_groups(q, k, v, topk_groups, g, rope_base, rope_mode=ROPE_HEAD_RELATIVE,
+                        scale=None, form="gathered"):
+    """Ungated head outputs [B, H, T, d] (NaN where the token's group is not
+    selected) for query heads q [B, H, T, d] and group keys/values
+    k, v [B, H/g, T, d]; topk_groups [B, T, K/g] are the selected groups.
+
+    form 'definition': the explicit visibility mask of each group over
+    global indices, Vis_j[t, s] = m_{t,j} m_{s,j} [s <= t], applied to every
+    query head of the group; 'gathered': each group's routed rows as one
+    causal sequence."""
+    B, H, T, d = q.shape
+    G = H // g
+    assert k.shape[1] == G and v.shape[1] == G
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    m = membership(topk_groups, G)                  # [B, T, G]
+    rank = head_ranks(m)                            # group-local ranks
+    out = np.full((B, H, T, d), np.nan)
+    tpos = np.arange(T)
+    for b in range(B):
+        for j in range(G):
+            rows = np.nonzero(m[b, :, j])[0]
+            if rows.size == 0:
+                continue
+            if form == "definition":
+                pos = _positions(rank[b, :, j], tpos, rope_mode)
+                kt = _rotate(k[b, j], pos, rope_base)
+                vis = visibility_mask(m[b, :, j], rows)        # [n, T]
+                for u in range(g):
+                    h = j * g + u
+                    qt = _rotate(q[b, h, rows], None if pos is None else pos[rows], rope_base)
+                    sc = np.where(vis, (qt @ kt.T) * scale, -np.inf)
+                    sc = sc - sc.max(axis=1, keepdims=True)
+                    p = np.where(vis, np.exp(sc), 0.0)
+                    p /= p.sum(axis=1, keepdims=True)
+                    out[b, h, rows] = p @ v[b, j]
+            else:
+                n = rows.size
+                pos = _positions(np.arange(n), rows, rope_mode)
+                kt = _rotate(k[b, j, rows], pos, rope_base)
+                vv = v[b, j, rows]
+                causal = np.arange(n)[None, :] <= np.arange(n)[:, None]
+                for u in range(g):
+                    h = j * g + u
+                    qt = _rotate(q[b, h, rows], pos, rope_base)
+                    sc = np.where(causal, (qt @ kt.T) * scale, -np.inf)
+                    sc = sc - sc.max(axis=1, keepdims=True)
+                    p = np.exp(sc)
+                    p /= p.sum(axis=1, keepdims=True)
+                    out[b, h, rows] = p @ vv
+    return out
+
+
+def combine_kv_groups(h_dense, topk_groups, gates, g):
+    """o_t = sum over the selected groups j of g_{t,j} sum_u h_{t, j*g + u}
+    (the group's query heads share its gate; W_O = I, R3)."""
+    B, H, T, d = h_dense.shape
+    o = np.zeros((B, T, d))
+    for kk in range(topk_groups.shape[-1]):
+        j = topk_groups[:, :, kk].astype(np.int64)
+        for u in range(g):
+            sel = h_dense[np.arange(B)[:, None], j * g + u, np.arange(T)[None, :]]
+            o += gates[:, :, kk, None] * sel
     return o
 
 

@@ -703,3 +703,116 @@ def test_projected_layer_reads_only_routed_pairs():
         a, e = int(off[sid]), int(off[sid + 1])
         y[a:e] = ref["head_out"][a:e] @ w_o[i].T
     np.testing.assert_allclose(O.combine_packed(y, slot, ref["gates"]), o, rtol=1e-12, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# KV-group routing (App. GQA+NAMOH, adopted KV-group routing)
+
+def _gqa_case(seed, B=2, T=23, G=4, Kg=2, g=2, d=8):
+    r = np.random.default_rng(seed)
+    logits = r.standard_normal((B, T, G)).astype(np.float32)
+    q = r.standard_normal((B, G * g, T, d))
+    k = r.standard_normal((B, G, T, d))
+    v = r.standard_normal((B, G, T, d))
+    return logits, q, k, v, O.select_heads(logits, Kg)
+
+
+@pytest.mark.parametrize("rope_mode", [O.ROPE_HEAD_RELATIVE, O.ROPE_GLOBAL, O.ROPE_NONE])
+def test_kv_groups_of_one_are_the_routed_heads(rope_mode):
+    # g = 1: every query head has its own key/value head; the result is the
+    # per-head routed attention
+    logits, q, k, v, topk = _gqa_case(81, G=5, Kg=2, g=1)
+    h = O.attention_kv_groups(q, k, v, topk, 1, 1e4, rope_mode)
+    n, off, perm, slot = O.permutation(topk, 5)
+    hp = O.attention_gathered(q, k, v, n, off, perm, 5, 1e4, rope_mode)
+    for sid in range(2 * 5):
+        b, i = divmod(sid, 5)
+        a, e = int(off[sid]), int(off[sid + 1])
+        np.testing.assert_allclose(h[b, i, perm[a:e]], hp[a:e], rtol=1e-12, atol=1e-12)
+
+
+def test_kv_groups_all_selected_is_dense_gqa():
+    # all H/g groups selected: standard causal grouped-query attention with
+    # standard RoPE (torch scaled_dot_product_attention, float64, keys and
+    # values repeated for the g query heads of each group)
+    torch = pytest.importorskip("torch")
+    F = torch.nn.functional
+    logits, q, k, v, topk = _gqa_case(82, B=2, T=19, G=3, Kg=3, g=2, d=6)
+    B, H, T, d = q.shape
+    base = 1e4
+    pos = np.arange(T)
+    qr = O.rope_rotate(q, np.broadcast_to(pos, (B, H, T)), base)
+    kr = O.rope_rotate(k, np.broadcast_to(pos, (B, 3, T)), base)
+    kt = torch.from_numpy(kr).repeat_interleave(2, dim=1)
+    vt = torch.from_numpy(v).repeat_interleave(2, dim=1)
+    ref = F.scaled_dot_product_attention(torch.from_numpy(qr), kt, vt, is_causal=True).numpy()
+    for form in ("definition", "gathered"):
+        got = O.attention_kv_groups(q, k, v, topk, 2, base, O.ROPE_HEAD_RELATIVE, form=form)
+        np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-11)
+
+
+@pytest.mark.parametrize("rope_mode", [O.ROPE_HEAD_RELATIVE, O.ROPE_GLOBAL, O.ROPE_NONE])
+def test_kv_groups_definition_equals_gathered(rope_mode):
+    logits, q, k, v, topk = _gqa_case(83, B=2, T=31, G=4, Kg=2, g=3, d=8)
+    a = O.attention_kv_groups(q, k, v, topk, 3, 1e4, rope_mode, form="definition")
+    b = O.attention_kv_groups(q, k, v, topk, 3, 1e4, rope_mode, form="gathered")
+    np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-12, equal_nan=True)
+    # unselected (token, group) pairs produce nothing; selected ones are finite
+    m = O.membership(topk, 4)
+    for j in range(4):
+        for u in range(3):
+            assert np.isnan(a[:, j * 3 + u][~m[:, :, j]]).all()
+            assert np.isfinite(a[:, j * 3 + u][m[:, :, j]]).all()
+
+
+def test_kv_groups_interaction_count_closed_form():
+    # Eq. app-group-prefill: C_attn = g/2 sum n_j^2 + g/2 sum n_j, counted
+    # here from the explicit visibility masks of every query head
+    logits, q, k, v, topk = _gqa_case(84, B=1, T=40, G=4, Kg=2, g=3, d=4)
+    G, g = 4, 3
+    m = O.membership(topk, G)
+    pairs = 0
+    for j in range(G):
+        rows = np.nonzero(m[0, :, j])[0]
+        pairs += g * int(O.visibility_mask(m[0, :, j], rows).sum())
+    n = m[0].sum(0)
+    assert n.sum() == 40 * 2                     # sum_j n_j = T K/g (K/g = 2 groups per token)
+    assert pairs == g * (n * n).sum() // 2 + g * n.sum() // 2
+
+
+def test_kv_groups_brute_force_and_combine():
+    # scalar loops over (t, head, s) for one tiny sequence, then the gated
+    # group combine against its definition
+    logits, q, k, v, topk = _gqa_case(85, B=1, T=9, G=3, Kg=2, g=2, d=4)
+    base = 1e4
+    sel = [[int(j) for j in topk[0, t]] for t in range(9)]
+
+    def rot(vec, p):
+        half = 2
+        out = [0.0] * 4
+        for jj in range(half):
+            ang = p * base ** (-2.0 * jj / 4)
+            c, s_ = math.cos(ang), math.sin(ang)
+            out[jj] = vec[jj] * c - vec[jj + half] * s_
+            out[jj + half] = vec[jj + half] * c + vec[jj] * s_
+        return out
+
+    h = O.attention_kv_groups(q, k, v, topk, 2, base)
+    gates = O.route_gates(logits, topk, O.GATE_SOFTMAX_SELECTED)
+    o = O.combine_kv_groups(h, topk, gates, 2)
+    for t in range(9):
+        want_o = [0.0] * 4
+        for kk, j in enumerate(sel[t]):
+            hist = [s for s in range(t + 1) if j in sel[s]]
+            rank = {s: r for r, s in enumerate(hist)}
+            for u in range(2):
+                qv = rot(list(q[0, j * 2 + u, t]), rank[t])
+                sc = [sum(a * b for a, b in zip(qv, rot(list(k[0, j, s]), rank[s]))) / 2.0
+                      for s in hist]
+                mx = max(sc)
+                e = [math.exp(x - mx) for x in sc]
+                hv = [sum(e[i] * v[0, j, s, c] for i, s in enumerate(hist)) / sum(e) for c in range(4)]
+                np.testing.assert_allclose(h[0, j * 2 + u, t], hv, rtol=1e-12, atol=1e-12)
+                for c in range(4):
+                    want_o[c] += gates[0, t, kk] * hv[c]
+        np.testing.assert_allclose(o[0, t], want_o, rtol=1e-12, atol=1e-12)
