@@ -285,6 +285,74 @@ def bench_layer(w, args, torch, L, DI):
 
 
 # ----------------------------------------------------------------------------
+def bench_grouped(w, args, torch, L, DI):
+    """Key/value-group routing on a prefill workload: the H query heads form
+    H/g groups sharing one key/value head; K/g groups are selected per token."""
+    g = args.kv_group
+    if w.H % g or w.K % g:
+        raise SystemExit(f"--kv-group {g} must divide H = {w.H} and K = {w.K}")
+    dev = torch.device("cuda:0")
+    wk = w.with_(H=w.H // g, K=w.K // g)
+    log(f"generating inputs for {w.name} with key/value groups of {g}")
+    logits = torch.from_numpy(W.prefill_logits(wk)).to(dev)
+    q = DI.to_device(W.prefill_qkv(w, "q"), w.dtype, dev)
+    k, v = (DI.to_device(W.prefill_qkv(wk, n), w.dtype, dev) for n in ("k", "v"))
+    B, T, Hkv, Kkv, d = w.B, w.T, wk.H, wk.K, w.d
+    routing = L.route(logits, Kkv)
+    rws = L.workspace(L.route_workspace_size(B, T, Hkv, Kkv), dev)
+    aws = L.workspace(int(L.lib().namoh_attn_fwd_grouped_workspace_size(B, T, Hkv, Kkv, g, d,
+                                                                         L.dtype_code(q.dtype))),
+                      dev)
+    out = torch.empty(B, T, d, dtype=q.dtype, device=dev)
+
+    def step():
+        L.route(logits, Kkv, L.GATE_SOFTMAX_SELECTED, out=routing, ws=rws)
+        L.attn_fwd_grouped(q, k, v, routing, Kkv, w.rope_base, out=out, ws=aws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    n = routing["head_len"].cpu().numpy().astype(np.int64)
+    # Eq. app-group-prefill: every routed row of a group carries g queries
+    c_attn = g * int((n * (n + 1) // 2).sum())
+    flops = 4.0 * d * c_attn
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    L.profile_enable(args.steps)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    kern = {}
+    for sec in ("attn", "pack", "combine"):
+        r = L.profile_read(sec)
+        if r is not None and r[1] > 0:
+            kern[sec] = r[0] / r[1]
+    L.profile_enable(0)
+    attn_ms = kern.get("attn", float("nan"))
+    achieved = flops / (attn_ms * 1e-3) / 1e12
+    return {"metric": "routed-attn prefill with key/value-group routing, tokens/s (1 GPU)",
+            "value": round(B * T / (ms_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+            "data": "synthetic",
+            "config": {"workload": w.name, "kv_group": g, "B": B, "T": T, "H": w.H, "K": w.K,
+                       "H_kv": Hkv, "K_kv": Kkv, "d_head": d, "rope": "head-relative",
+                       "rope_base": w.rope_base, "gates": "softmax over selected"},
+            "roofline": {"kernel": "k_attn_mfma", "bound": "mfma", "achieved": round(achieved, 2),
+                         "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                         "algorithmic_per_launch": {"flops": flops, "C_attn": c_attn},
+                         "kernel_ms": round(attn_ms, 4)},
+            "kernels_ms": {k2: round(v2, 4) for k2, v2 in kern.items()}}
+
+
+# ----------------------------------------------------------------------------
 def bench_backward(w, args, torch, L, DI):
     """One training step of the layer: route, forward, backward of the
     attention (dq, dk, dv, dgates) and of the gates (d logits)."""
@@ -479,6 +547,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", type=int, default=2, choices=sorted(W.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kv-group", type=int, default=1,
+                    help="key/value-group routing with groups of this many query heads "
+                         "(prefill workloads; K/g of H/g groups selected per token)")
     ap.add_argument("--backward", action="store_true",
                     help="time a training step (route, forward, backward) of a prefill "
                          "workload instead of the forward step")
@@ -521,6 +592,11 @@ def main():
         res = bench_backward(w, args, torch, L, DI)
     elif w.d_model:
         res = bench_layer(w, args, torch, L, DI)
+    elif args.kv_group > 1:
+        if w.decode:
+            print(json.dumps({"error": "--kv-group needs a prefill workload"}))
+            sys.exit(2)
+        res = bench_grouped(w, args, torch, L, DI)
     else:
         res = (bench_decode if w.decode else bench_prefill)(w, args, torch, L, DI)
     print(json.dumps(res), flush=True)

@@ -208,6 +208,36 @@ namoh_status namoh_route_bwd(const float* logits, const int32_t* topk_idx,
                              int H, int K, int gate_mode, float* dlogits, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Key/value-group routing (App. "GQA+NAMOH", adopted KV-group routing): the
+ * H = H_kv * g query heads form H_kv groups of g consecutive heads (group j:
+ * heads j*g .. j*g + g - 1) that share one key/value head.  The router
+ * selects K_kv of the H_kv groups per token (namoh_route on group logits
+ * [B, T, H_kv] with K = K_kv); every query head of a selected group attends
+ * causally over the group's routed subsequence (RoPE at the group-local
+ * rank for the queries and the shared key), and the g head outputs are
+ * summed with the group's gate:
+ *   o_t = sum_k gates[b,t,k] * sum_{u<g} h(t, topk_idx[b,t,k] * g + u).
+ * In:  q [B, H_kv*g, T, d], k, v [B, H_kv, T, d]: bf16, d in {64, 128}
+ *      (else NAMOH_ERR_UNSUPPORTED); 1 <= group_size <= 16.
+ *      rope/scale and the routing arrays as for namoh_attn_fwd (routing of
+ *      the groups).
+ * Out: out [B, T, d] of out_dtype (may be NULL when head_out is given);
+ *      head_out optional float32 [B*T*K_kv, g, d]: head u of the pair at
+ *      packed row p is row p*g + u.
+ * group_size 1 computes exactly what namoh_attn_fwd computes.
+ * ---------------------------------------------------------------------- */
+size_t namoh_attn_fwd_grouped_workspace_size(int B, int T, int H_kv, int K_kv, int group_size,
+                                             int d_head, int dtype);
+
+namoh_status namoh_attn_fwd_grouped(const void* q, const void* k, const void* v, int dtype,
+                                    int B, int T, int H_kv, int K_kv, int group_size, int d_head,
+                                    float rope_base, int rope_mode, float softmax_scale,
+                                    const float* gates, const int32_t* seg_offsets,
+                                    const int32_t* perm_token, const int32_t* slot_pos,
+                                    void* out, int out_dtype, float* head_out, void* workspace,
+                                    size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Routed per-head projections (Sec. 3.1, Eq. namoh-qkv: tokens are
  * dispatched to their heads before projection, and only active (token, head)
  * pairs compute q, k, v; Eq. namoh-attention: o_t = sum over the selected

@@ -33,6 +33,7 @@ EXPORTED = (
     "namoh_prefill_cache", "namoh_attn_bwd_workspace_size", "namoh_attn_bwd", "namoh_route_bwd",
     "namoh_decode_workspace_size", "namoh_decode_step", "namoh_decode_step_biased",
     "namoh_qkv_proj", "namoh_out_proj_workspace_size", "namoh_out_proj",
+    "namoh_attn_fwd_grouped_workspace_size", "namoh_attn_fwd_grouped",
     "namoh_status_string", "namoh_last_error", "namoh_version",
     "namoh_profile_enable", "namoh_profile_read",
 )
@@ -61,6 +62,9 @@ _SIGS = {
                                _F, _I, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
     "namoh_decode_step_biased": (_I, [_P, _P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I,
                                       _I, _F, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
+    "namoh_attn_fwd_grouped_workspace_size": (_S, [_I, _I, _I, _I, _I, _I, _I]),
+    "namoh_attn_fwd_grouped": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _I, _F,
+                                    _P, _P, _P, _P, _P, _I, _P, _P, _S, _P]),
     "namoh_qkv_proj": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P]),
     "namoh_out_proj_workspace_size": (_S, [_I, _I, _I, _I, _I]),
     "namoh_out_proj": (_I, [_P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _S, _P]),
@@ -230,6 +234,39 @@ def attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K
                                None if skip else _ptr(out),
                                dtype_code(odt) if skip else dtype_code(out.dtype),
                                _ptr(head_out), _ptr(ws), ws.numel(), _stream(q.device)))
+    return head_out if skip else out
+
+
+def attn_fwd_grouped(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict,
+                     K_kv: int, rope_base: float, rope_mode: int = ROPE_HEAD_RELATIVE,
+                     softmax_scale: float = 0.0, out_dtype: Optional[torch.dtype] = None,
+                     head_out: Optional[torch.Tensor] = None, out=None,
+                     ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """namoh_attn_fwd_grouped: query heads q [B, H_kv*g, T, d] over
+    key/value groups k, v [B, H_kv, T, d] (bf16) with the groups' routing;
+    returns out [B, T, d] (or head_out [B*T*K_kv, g, d] with out=False)."""
+    _need_cuda(q, k, v, head_out, None if out is False else out)
+    B, Hq, T, d = q.shape
+    Hkv = k.shape[1]
+    if k.shape != v.shape or k.shape[0] != B or k.shape[2:] != q.shape[2:] or Hq % Hkv:
+        raise ValueError("q [B, H_kv*g, T, d], k and v [B, H_kv, T, d]")
+    g = Hq // Hkv
+    dt = dtype_code(q.dtype)
+    odt = q.dtype if out_dtype is None else out_dtype
+    skip = out is False
+    if skip and head_out is None:
+        raise ValueError("out=False needs head_out")
+    if out is None:
+        out = torch.empty(B, T, d, dtype=odt, device=q.device)
+    if ws is None:
+        ws = workspace(int(lib().namoh_attn_fwd_grouped_workspace_size(B, T, Hkv, K_kv, g, d, dt)),
+                       q.device)
+    check(lib().namoh_attn_fwd_grouped(
+        _ptr(q), _ptr(k), _ptr(v), dt, B, T, Hkv, K_kv, g, d, float(rope_base), rope_mode,
+        float(softmax_scale), _ptr(routing["gates"]), _ptr(routing["seg_offsets"]),
+        _ptr(routing["perm_token"]), _ptr(routing["slot_pos"]), None if skip else _ptr(out),
+        dtype_code(odt) if skip else dtype_code(out.dtype), _ptr(head_out), _ptr(ws), ws.numel(),
+        _stream(q.device)))
     return head_out if skip else out
 
 

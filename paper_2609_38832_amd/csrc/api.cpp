@@ -249,6 +249,63 @@ namoh_status namoh_prefill_cache(const void* k, const void* v, int dtype, int B,
                                                 static_cast<hipStream_t>(stream)));
 }
 
+size_t namoh_attn_fwd_grouped_workspace_size(int B, int T, int H_kv, int K_kv, int group_size,
+                                             int d_head, int dtype) {
+  if (check_sizes(B, T, H_kv, K_kv) != NAMOH_OK || group_size < 1 || group_size > 16 ||
+      (d_head != 64 && d_head != 128) || dtype != NAMOH_BF16)
+    return 0;
+  return namoh::attn_workspace_bytes(B, T, H_kv, K_kv, d_head, dtype, group_size);
+}
+
+namoh_status namoh_attn_fwd_grouped(const void* q, const void* k, const void* v, int dtype,
+                                    int B, int T, int H_kv, int K_kv, int group_size, int d_head,
+                                    float rope_base, int rope_mode, float softmax_scale,
+                                    const float* gates, const int32_t* seg_offsets,
+                                    const int32_t* perm_token, const int32_t* slot_pos,
+                                    void* out, int out_dtype, float* head_out, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  namoh_status s;
+  if ((s = check_sizes(B, T, H_kv, K_kv)) != NAMOH_OK) return s;
+  REQUIRE(group_size >= 1 && group_size <= 16, "group_size must be in [1, 16] (got %d)",
+          group_size);
+  REQUIRE(dtype == NAMOH_F32 || dtype == NAMOH_BF16, "unknown dtype %d", dtype);
+  if (dtype != NAMOH_BF16 || (d_head != 64 && d_head != 128))
+    return fail(NAMOH_ERR_UNSUPPORTED, "key/value groups need bf16 and d_head 64 or 128");
+  REQUIRE(out_dtype == NAMOH_F32 || out_dtype == NAMOH_BF16, "unknown out_dtype %d", out_dtype);
+  REQUIRE(rope_mode == NAMOH_ROPE_HEAD_RELATIVE || rope_mode == NAMOH_ROPE_GLOBAL ||
+              rope_mode == NAMOH_ROPE_NONE,
+          "unknown rope_mode %d", rope_mode);
+  REQUIRE(rope_mode == NAMOH_ROPE_NONE || (std::isfinite(rope_base) && rope_base > 0.f),
+          "rope_base must be finite and > 0 (got %g)", static_cast<double>(rope_base));
+  REQUIRE(!std::isnan(softmax_scale) && !std::isinf(softmax_scale), "softmax_scale must be finite");
+  REQUIRE(static_cast<long long>(B) * H_kv * group_size * T * d_head < (1ll << 40),
+          "q too large");
+  // the MFMA path addresses one segment's key tiles with 32-bit byte offsets
+  if ((static_cast<long long>(T) + 63) / 64 * 64 * d_head * 2 >= (1ll << 32))
+    return fail(NAMOH_ERR_UNSUPPORTED, "T = %d too long for d_head = %d on the bf16 path", T,
+                d_head);
+  REQUIRE_PTR(q, 16);
+  REQUIRE_PTR(k, 16);
+  REQUIRE_PTR(v, 16);
+  REQUIRE_PTR(gates, 4);
+  REQUIRE_PTR(seg_offsets, 4);
+  REQUIRE_PTR(perm_token, 4);
+  REQUIRE_PTR(slot_pos, 4);
+  REQUIRE(out != nullptr || head_out != nullptr, "out and head_out are both NULL");
+  if (out != nullptr) REQUIRE_PTR(out, 16);
+  if (head_out != nullptr) REQUIRE_PTR(head_out, 16);
+  if ((s = check_workspace(workspace, workspace_bytes,
+                           namoh::attn_workspace_bytes(B, T, H_kv, K_kv, d_head, dtype,
+                                                       group_size))) != NAMOH_OK)
+    return s;
+  const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
+  clear_hip_error();
+  return hip_status(namoh::launch_attn(q, k, v, dtype, B, T, H_kv, K_kv, d_head, rope_base,
+                                       rope_mode, scale, gates, seg_offsets, perm_token,
+                                       slot_pos, out, out_dtype, head_out, workspace,
+                                       static_cast<hipStream_t>(stream), group_size));
+}
+
 namespace {
 namoh_status check_proj(int B, int T, int H, int K, int d_head, int d_model) {
   namoh_status s;

@@ -151,8 +151,9 @@ NAMOH_DEV int serpentine(int rank, int total, int period) {
 
 template <int NT>
 NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, int T, int BM,
-                             int Nr, int max_items, int period, WorkItem* __restrict__ items,
-                             int32_t* __restrict__ meta, SchedLds& L) {
+                             int Nr, int max_items, int period, int G,
+                             WorkItem* __restrict__ items, int32_t* __restrict__ meta,
+                             SchedLds& L) {
   static_assert(NT % kWave == 0 && NT / kWave <= 16 && kSortBins % NT == 0, "block size");
   const int tid = thread_x();
   const int lane = tid % kWave, wave = tid / kWave;
@@ -195,11 +196,14 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
     return;
   }
   const int max_nqb = (maxn + BM - 1) / BM;
-  const long grid_items = static_cast<long>(max_nqb) * BH;
-  // grid cell g = qb * BH + s; the work key is the bin index (heaviest first)
-  auto cell = [&](long g, int& s, int& qb, int& seg0, int& n, int& key) {
-    qb = static_cast<int>(g / BH);
-    s = static_cast<int>(g - static_cast<long>(qb) * BH);
+  const long grid_items = static_cast<long>(max_nqb) * BH * G;
+  // grid cell g = (qb * BH + s) * G + u (u: query head of a key/value group,
+  // G = 1 without groups); the work key is the bin index (heaviest first)
+  auto cell = [&](long g, int& s, int& qb, int& u, int& seg0, int& n, int& key) {
+    const long c = g / G;
+    u = static_cast<int>(g - c * G);
+    qb = static_cast<int>(c / BH);
+    s = static_cast<int>(c - static_cast<long>(qb) * BH);
     seg0 = off[s];
     n = off[s + 1] - seg0;
     const int w = min((n + kBN - 1) / kBN, (qb + 1) * per_qb);
@@ -208,8 +212,8 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
   };
   for (long g0 = 0; g0 < grid_items; g0 += NT) {
     const long g = g0 + tid;
-    int sg = 0, qb = 0, seg0 = 0, n = 0, key = 0;
-    const bool act = g < grid_items && cell(g, sg, qb, seg0, n, key);
+    int sg = 0, qb = 0, u = 0, seg0 = 0, n = 0, key = 0;
+    const bool act = g < grid_items && cell(g, sg, qb, u, seg0, n, key);
     wave_bin_add(L.hist, key, act);
   }
   __syncthreads();
@@ -233,8 +237,8 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
   const int placed = min(total, max_items);
   for (long g0 = 0; g0 < grid_items; g0 += NT) {
     const long g = g0 + tid;
-    int sg = 0, qb = 0, seg0 = 0, n = 0, key = 0;
-    const bool act = g < grid_items && cell(g, sg, qb, seg0, n, key);
+    int sg = 0, qb = 0, u = 0, seg0 = 0, n = 0, key = 0;
+    const bool act = g < grid_items && cell(g, sg, qb, u, seg0, n, key);
     const int rank = wave_bin_add(L.hist, key, act);
     if (act && rank < placed) {
       const int pos = serpentine(rank, placed, period);
@@ -244,7 +248,8 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
       wi.seg0 = seg0;
       wi.n = n;
       wi.tile0 = seg_tile0(seg0, sg);
-      wi.pad0 = wi.pad1 = wi.pad2 = 0;
+      wi.qh = u;
+      wi.pad1 = wi.pad2 = 0;
       items[pos] = wi;
     }
   }
@@ -286,7 +291,7 @@ __global__ __launch_bounds__(kPackThreads) void k_attn_schedule(
     const int32_t* __restrict__ seg_offsets, int BH, int T, int BM, int Nr, int max_items,
     int period, WorkItem* __restrict__ items, int32_t* __restrict__ meta) {
   __shared__ SchedLds L;
-  attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, period, items, meta, L);
+  attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, period, 1, items, meta, L);
 }
 
 // ---------------------------------------------------------------------------
@@ -322,8 +327,9 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, double log_base,
     double* __restrict__ freq_out, const int32_t* __restrict__ seg_offsets,
     const int32_t* __restrict__ perm_token, int BH, int T, int H, int Nr, int rope_mode,
-    int BM, int max_items, int period, WorkItem* __restrict__ items, int32_t* __restrict__ meta,
-    uint16_t* __restrict__ Kp, uint16_t* __restrict__ Vt, float* __restrict__ knorm) {
+    int BM, int max_items, int period, int G, WorkItem* __restrict__ items,
+    int32_t* __restrict__ meta, uint16_t* __restrict__ Kp, uint16_t* __restrict__ Vt,
+    float* __restrict__ knorm) {
   __shared__ __attribute__((aligned(16))) union {
     SchedLds sched;
     PackLds<D> pack;
@@ -331,7 +337,7 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
   if (block_x() == 0) {
     // the rotation frequencies for the attention kernel, then the schedule
     if (thread_x() < D / 2) freq_out[thread_x()] = rope_freq_rev(thread_x(), D, log_base);
-    attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, period, items, meta,
+    attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, period, G, items, meta,
                                 L.sched);
     return;
   }
@@ -661,7 +667,7 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kp,
     const uint16_t* __restrict__ Vt, const double* __restrict__ freq,
     const int32_t* __restrict__ perm_token, const WorkItem* __restrict__ items,
-    const int32_t* __restrict__ meta, const float* __restrict__ knorm, int T, int H,
+    const int32_t* __restrict__ meta, const float* __restrict__ knorm, int T, int H, int G,
     int rope_mode, float scale_log2, void* __restrict__ hout, float* __restrict__ lse_out) {
   constexpr int BM = 32 * NQT * NW;
   constexpr int KS = D / 16;  // reduction steps of S^T = K Q^T
@@ -691,7 +697,11 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   // all its rows are padding past the segment's end
   const int wq_last = q0 + 32 * ((NQT - 1) * NW + wave) + 31;
   const int wave_tiles = q0 + 32 * wave < n ? min(wq_last, n - 1) / kBN + 1 : 0;
-  const size_t head_base = (static_cast<size_t>(b) * H + h) * T;
+  // query head of the item: head h of the key/value segment, or with key/value
+  // groups of G query heads, head h * G + qh; its head outputs are row
+  // (packed row) * G + qh
+  const int qh = it.qh;
+  const size_t head_base = ((static_cast<size_t>(b) * H + h) * G + qh) * T;
 
   // token of each query row.  The tile loads below are invisible to the
   // compiler's wait counting, and vmcnt retires in issue order, so a wait
@@ -905,7 +915,8 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
         const int rr = i * RPI + lane / NG;
         const uint4 v = *reinterpret_cast<const uint4*>(stage + rr * 2 * D + (gl ^ (rr % NG)) * 16);
         if (row0 + rr < n)
-          *reinterpret_cast<uint4*>(ho + static_cast<size_t>(seg0 + row0 + rr) * D + gl * 8) = v;
+          *reinterpret_cast<uint4*>(
+              ho + (static_cast<size_t>(seg0 + row0 + rr) * G + qh) * D + gl * 8) = v;
       }
     }
   } else {
@@ -917,8 +928,9 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
       if (r < n) {
         // log-sum-exp of the row's scores in log2 units (the backward's
         // statistics): the probabilities were exp2(score - m_run)
-        if (lse_out != nullptr && g == 0) lse_out[seg0 + r] = m_run[qt] + log2f(lsum);
-        const size_t orow = static_cast<size_t>(seg0 + r) * D;
+        if (lse_out != nullptr && g == 0)
+          lse_out[static_cast<size_t>(seg0 + r) * G + qh] = m_run[qt] + log2f(lsum);
+        const size_t orow = (static_cast<size_t>(seg0 + r) * G + qh) * D;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -1046,7 +1058,7 @@ constexpr int kCombineThreads = 256;
 template <bool IN_BF16, bool OUT_BF16>
 __global__ __launch_bounds__(kCombineThreads) void k_combine(
     const void* __restrict__ hout, const float* __restrict__ gates,
-    const int32_t* __restrict__ slot_pos, long BT, int K, int D, int Nr,
+    const int32_t* __restrict__ slot_pos, long BT, int K, int D, int Nr, int G,
     void* __restrict__ out) {
   const int C = D / 8;
   const long idx = static_cast<long>(block_x()) * kCombineThreads + thread_x();
@@ -1058,22 +1070,28 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
   for (int e = 0; e < 8; ++e) acc[e] = 0.f;
   const int32_t* sp = slot_pos + tok * K;
   const float* gp = gates + tok * K;
-  // rounds of KC selected heads: their slots and gates, then all their head
-  // rows in flight at once; the sum runs over k in ascending order
+  // Rounds of KC rows: row v = k * G + u is head output u of selected slot k
+  // (G = 1 without key/value groups), weighted by the slot's gate; first
+  // their slots and gates, then all their rows in flight at once; the sum
+  // runs over v in ascending order.
   constexpr int KC = 8;
-  for (int k0 = 0; k0 < K; k0 += KC) {
+  const int KV = K * G;
+  for (int k0 = 0; k0 < KV; k0 += KC) {
     int p[KC];
     float gk[KC];
     float x[KC][8];
 #pragma unroll
     for (int i = 0; i < KC; ++i) {
-      const bool in = k0 + i < K;
-      p[i] = in ? sp[k0 + i] : -1;
-      gk[i] = in ? gp[k0 + i] : 0.f;
+      const int vr = k0 + i;
+      const bool in = vr < KV;
+      const int kk = G == 1 ? vr : vr / G;
+      const int sl = in ? sp[kk] : -1;
+      p[i] = static_cast<unsigned>(sl) < static_cast<unsigned>(Nr) ? sl * G + (vr - kk * G) : -1;
+      gk[i] = in ? gp[kk] : 0.f;
     }
 #pragma unroll
     for (int i = 0; i < KC; ++i) {
-      if (static_cast<unsigned>(p[i]) < static_cast<unsigned>(Nr)) {
+      if (p[i] >= 0) {
         if constexpr (IN_BF16) {
           const uint4 u =
               reinterpret_cast<const uint4*>(hout)[static_cast<size_t>(p[i]) * C + cc];
@@ -1093,7 +1111,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
     }
 #pragma unroll
     for (int i = 0; i < KC; ++i)
-      if (k0 + i < K)
+      if (k0 + i < KV)
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] = fmaf(gk[i], x[i][e], acc[e]);
   }
@@ -1138,12 +1156,14 @@ struct AttnWs {
   size_t max_items, max_tiles;
 };
 
-static AttnWs carve_attn(void* ws, int B, int T, int H, int K, int d, int dtype) {
+// H, K: key/value heads (segments per sequence) and selected segments per
+// token; G query heads per key/value head (1 without groups).
+static AttnWs carve_attn(void* ws, int B, int T, int H, int K, int d, int dtype, int G = 1) {
   const size_t BH = static_cast<size_t>(B) * H;
   const size_t Nr = static_cast<size_t>(B) * T * K;
   const int BM = block_queries(d, dtype);
   AttnWs w;
-  w.max_items = Nr / BM + BH + 1;
+  w.max_items = (Nr / BM + BH + 1) * G;
   w.max_tiles = Nr / kBN + BH + 1;
   Carver cv(ws);
   w.meta = cv.take<int32_t>(kMetaCount);
@@ -1159,18 +1179,18 @@ static AttnWs carve_attn(void* ws, int B, int T, int H, int K, int d, int dtype)
     w.knorm = nullptr;
     w.freq = nullptr;
   }
-  w.hpack = cv.take<float>(Nr * d);
+  w.hpack = cv.take<float>(Nr * G * d);
   w.bytes = cv.off;
   return w;
 }
 
-size_t attn_workspace_bytes(int B, int T, int H, int K, int d, int dtype) {
-  return carve_attn(nullptr, B, T, H, K, d, dtype).bytes;
+size_t attn_workspace_bytes(int B, int T, int H, int K, int d, int dtype, int G) {
+  return carve_attn(nullptr, B, T, H, K, d, dtype, G).bytes;
 }
 
 template <int D>
 static void launch_mfma(const AttnWs& w, const void* q, const void* k, const void* v,
-                        int B, int T, int H, int Nr, int rope_mode, double log_base,
+                        int B, int T, int H, int G, int Nr, int rope_mode, double log_base,
                         float scale_log2, const int32_t* seg_offsets, const int32_t* perm_token,
                         void* hout, bool hout_bf16, float* lse, hipStream_t st) {
   constexpr int NW = MfmaShape<D>::NW, NQT = MfmaShape<D>::NQT;
@@ -1179,18 +1199,18 @@ static void launch_mfma(const AttnWs& w, const void* q, const void* k, const voi
       static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), log_base, w.freq,
       seg_offsets,
       perm_token, B * H, T, H, Nr, rope_mode, 32 * NQT * NW, static_cast<int>(w.max_items),
-      device_cu_count(), w.items, w.meta, w.Kp, w.Vt, w.knorm);
+      device_cu_count(), G, w.items, w.meta, w.Kp, w.Vt, w.knorm);
   prof_mark("pack", false, st);
   prof_mark("attn", true, st);
   const unsigned grid = static_cast<unsigned>(w.max_items);
   if (hout_bf16)
     k_attn_mfma<D, NQT, NW, true><<<grid, NW * 64, 0, st>>>(
         static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.freq, perm_token, w.items, w.meta,
-        w.knorm, T, H, rope_mode, scale_log2, hout, nullptr);
+        w.knorm, T, H, G, rope_mode, scale_log2, hout, nullptr);
   else
     k_attn_mfma<D, NQT, NW, false><<<grid, NW * 64, 0, st>>>(
         static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.freq, perm_token, w.items, w.meta,
-        w.knorm, T, H, rope_mode, scale_log2, hout, lse);
+        w.knorm, T, H, G, rope_mode, scale_log2, hout, lse);
   prof_mark("attn", false, st);
 }
 
@@ -1210,8 +1230,8 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
                        int rope_mode, float scale, const float* gates,
                        const int32_t* seg_offsets, const int32_t* perm_token,
                        const int32_t* slot_pos, void* out, int out_dtype,
-                       float* head_out, void* ws, hipStream_t st) {
-  const AttnWs w = carve_attn(ws, B, T, H, K, d, dtype);
+                       float* head_out, void* ws, hipStream_t st, int G) {
+  const AttnWs w = carve_attn(ws, B, T, H, K, d, dtype, G);
   // Without a caller-supplied head_out, the MFMA path keeps the packed head
   // outputs in bf16 (half the traffic of the attention epilogue and of the
   // combine); the combine accumulates in fp32 either way.
@@ -1233,12 +1253,13 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   if (use_mfma(d, dtype)) {
     const float sl2 = scale * 1.4426950408889634f;
     if (d == 64)
-      launch_mfma<64>(w, q, k, v, B, T, H, Nr, rope_mode, log_base, sl2, seg_offsets, perm_token,
-                      hout, hb, nullptr, st);
+      launch_mfma<64>(w, q, k, v, B, T, H, G, Nr, rope_mode, log_base, sl2, seg_offsets,
+                      perm_token, hout, hb, nullptr, st);
     else
-      launch_mfma<128>(w, q, k, v, B, T, H, Nr, rope_mode, log_base, sl2, seg_offsets,
+      launch_mfma<128>(w, q, k, v, B, T, H, G, Nr, rope_mode, log_base, sl2, seg_offsets,
                        perm_token, hout, hb, nullptr, st);
   } else {
+    if (G != 1) return hipErrorInvalidValue;   // key/value groups run on the MFMA path only
     k_attn_schedule<<<1, kPackThreads, 0, st>>>(seg_offsets, B * H, T, BM, Nr,
                                                 static_cast<int>(w.max_items), device_cu_count(),
                                                 w.items, w.meta);
@@ -1259,13 +1280,13 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   const unsigned grid = static_cast<unsigned>((threads + kCombineThreads - 1) / kCombineThreads);
   prof_mark("combine", true, st);
   if (hb && out_dtype == 1)
-    k_combine<true, true><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+    k_combine<true, true><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, G, out);
   else if (hb)
-    k_combine<true, false><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+    k_combine<true, false><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, G, out);
   else if (out_dtype == 1)
-    k_combine<false, true><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+    k_combine<false, true><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, G, out);
   else
-    k_combine<false, false><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, out);
+    k_combine<false, false><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, G, out);
   prof_mark("combine", false, st);
   return hipGetLastError();
 }
@@ -1276,9 +1297,11 @@ hipError_t launch_combine_rows(const uint16_t* rows, const float* gates, const i
   const long threads = BT * (D / 8);
   const unsigned grid = static_cast<unsigned>((threads + kCombineThreads - 1) / kCombineThreads);
   if (out_dtype == 1)
-    k_combine<true, true><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D, Nr, out);
+    k_combine<true, true><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D, Nr, 1,
+                                                           out);
   else
-    k_combine<true, false><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D, Nr, out);
+    k_combine<true, false><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D, Nr,
+                                                            1, out);
   return hipGetLastError();
 }
 
@@ -1304,11 +1327,11 @@ hipError_t launch_attn_stats(const void* q, const void* k, const void* v, int B,
   if (e != hipSuccess) return e;
   const float sl2 = scale * 1.4426950408889634f;
   if (d == 64)
-    launch_mfma<64>(w, q, k, v, B, T, H, Nr, rope_mode, log_base, sl2, seg_offsets, perm_token,
-                    w.hpack, false, lse, st);
+    launch_mfma<64>(w, q, k, v, B, T, H, 1, Nr, rope_mode, log_base, sl2, seg_offsets,
+                    perm_token, w.hpack, false, lse, st);
   else
-    launch_mfma<128>(w, q, k, v, B, T, H, Nr, rope_mode, log_base, sl2, seg_offsets, perm_token,
-                     w.hpack, false, lse, st);
+    launch_mfma<128>(w, q, k, v, B, T, H, 1, Nr, rope_mode, log_base, sl2, seg_offsets,
+                     perm_token, w.hpack, false, lse, st);
   tiles.Kp = w.Kp;
   tiles.Vt = w.Vt;
   tiles.table = w.table;

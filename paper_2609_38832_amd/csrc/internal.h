@@ -40,13 +40,15 @@ hipError_t launch_route(const float* logits, const float* bias, int B, int T, in
                         hipStream_t st);
 
 // ---- prefill attention (attn.hip) ----------------------------------------
-size_t attn_workspace_bytes(int B, int T, int H, int K, int d, int dtype);
+// H, K: key/value heads and selected key/value heads per token; G query heads
+// per key/value head (key/value-group routing; 1 = one query head per head).
+size_t attn_workspace_bytes(int B, int T, int H, int K, int d, int dtype, int G = 1);
 hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
                        int B, int T, int H, int K, int d, float rope_base,
                        int rope_mode, float scale, const float* gates,
                        const int32_t* seg_offsets, const int32_t* perm_token,
                        const int32_t* slot_pos, void* out, int out_dtype,
-                       float* head_out, void* ws, hipStream_t st);
+                       float* head_out, void* ws, hipStream_t st, int G = 1);
 
 struct WorkItem;
 // Where launch_attn_stats leaves the forward's pieces inside its workspace.

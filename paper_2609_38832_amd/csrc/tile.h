@@ -32,7 +32,8 @@ NAMOH_DEV int seg_tile0(int seg0, int s) { return seg0 / kBN + s; }
 // global read.
 struct __attribute__((aligned(32))) WorkItem {
   int s, qb, seg0, n;            // segment b*H + h, query block, first packed row, length
-  int tile0, pad0, pad1, pad2;   // first packed key tile of the segment
+  int tile0, qh, pad1, pad2;     // first packed key tile of the segment; query head of
+                                 // the item within its key/value group (0 without groups)
 };
 
 // Work item of this workgroup, or false if it has none.  The record is read
@@ -48,7 +49,8 @@ NAMOH_DEV bool my_item(const WorkItem* __restrict__ items, const int32_t* __rest
   it.seg0 = __builtin_amdgcn_readfirstlane(v.seg0);
   it.n = __builtin_amdgcn_readfirstlane(v.n);
   it.tile0 = __builtin_amdgcn_readfirstlane(v.tile0);
-  it.pad0 = it.pad1 = it.pad2 = 0;
+  it.qh = __builtin_amdgcn_readfirstlane(v.qh);
+  it.pad1 = it.pad2 = 0;
   return block_x() < __builtin_amdgcn_readfirstlane(cnt);
 }
 

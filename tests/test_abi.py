@@ -231,6 +231,29 @@ def test_out_proj_workspace_size(lib):
     assert lib.namoh_out_proj_workspace_size(4, 4096, 32, 8, 100) == 0
 
 
+def _grp(lib, dtype=1, B=2, T=64, H=8, K=2, g=2, d=64, base=1e4, rope=0, q=fake(0), out=fake(7),
+         ho=None, wsb=1 << 30, ws=fake(9)):
+    return lib.namoh_attn_fwd_grouped(q, fake(1), fake(2), dtype, B, T, H, K, g, d, base, rope, 0.0,
+                                      fake(3), fake(4), fake(5), fake(6), out, 0, ho, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(g=0), 1), (dict(g=17), 1), (dict(dtype=0), 2), (dict(d=32), 2), (dict(dtype=3), 1),
+    (dict(rope=7), 1), (dict(base=-1.0), 1), (dict(q=None), 1), (dict(out=None), 1),
+    (dict(out=P(A + 8)), 1), (dict(wsb=16), 3), (dict(K=9), 1), (dict(T=1 << 25, d=128), 2),
+])
+def test_attn_fwd_grouped_rejects(lib, kw, code):
+    assert _grp(lib, **kw) == code
+
+
+def test_grouped_workspace_grows_with_the_group(lib):
+    a = lib.namoh_attn_fwd_grouped_workspace_size(2, 1024, 8, 2, 1, 64, 1)
+    b = lib.namoh_attn_fwd_grouped_workspace_size(2, 1024, 8, 2, 4, 64, 1)
+    assert a == lib.namoh_attn_fwd_workspace_size(2, 1024, 8, 2, 64, 1)
+    assert b > a
+    assert lib.namoh_attn_fwd_grouped_workspace_size(2, 1024, 8, 2, 4, 64, 0) == 0
+
+
 def test_workspace_queries(lib):
     assert lib.namoh_route_workspace_size(0, 10, 8, 2) == 0
     assert lib.namoh_route_workspace_size(1, 10, 8, 2) > 0
