@@ -49,6 +49,11 @@ Readings where the paper is silent (each also listed in the design notes):
   the H/g groups (same selection rule), all g query heads of a selected
   group attend over the group's subsequence with the group's gate, and RoPE
   uses the group-local rank for the queries and the shared key.
+* R18 always-active shared heads (Sec. 5, shared heads for local context):
+  H_s heads outside the routing attend, for every token, to the full causal
+  prefix or to the most recent w original tokens including the token itself
+  (t - w < s <= t), with RoPE at the global position; their outputs are
+  added to the routed output without a gate (W_O = I, R3).
 * R12 loss-free balancing selects by float32(a + b) with the affinities a
   formed in float64; equal scores go to the lower head index; the gates are
   a (the paper fixes no precision for the selection; one rounding step both
@@ -71,6 +76,7 @@ __all__ = [
     "attention_backward", "gates_backward",
     "qkv_projection", "output_projection",
     "attention_kv_groups", "combine_kv_groups",
+    "always_active_heads",
     "shared_head_counts",
 ]
 
@@ -392,6 +398,33 @@ def combine_kv_groups(h_dense, topk_groups, gates, g):
             sel = h_dense[np.arange(B)[:, None], j * g + u, np.arange(T)[None, :]]
             o += gates[:, :, kk, None] * sel
     return o
+
+
+# ----------------------------------------------------------------------------
+# Always-active shared heads (Sec. 5, shared heads for local context), R18
+
+def always_active_heads(q, k, v, window, rope_base, rope_mode=ROPE_GLOBAL, scale=None):
+    """Outputs [B, Hs, T, d] of always-active heads: token t attends to
+    tokens s with s <= t (window 0) or t - window < s <= t, through the
+    explicit visibility mask; RoPE at the global position t (or none)."""
+    B, Hs, T, d = q.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    t = np.arange(T)
+    vis = t[None, :] <= t[:, None]
+    if window > 0:
+        vis &= t[None, :] > t[:, None] - window
+    pos = None if rope_mode == ROPE_NONE else t
+    out = np.empty((B, Hs, T, d))
+    for b in range(B):
+        for h in range(Hs):
+            qt = _rotate(q[b, h], pos, rope_base)
+            kt = _rotate(k[b, h], pos, rope_base)
+            sc = np.where(vis, (qt @ kt.T) * scale, -np.inf)
+            sc = sc - sc.max(axis=1, keepdims=True)
+            p = np.where(vis, np.exp(sc), 0.0)
+            p /= p.sum(axis=1, keepdims=True)
+            out[b, h] = p @ v[b, h]
+    return out
 
 
 # ----------------------------------------------------------------------------

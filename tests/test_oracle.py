@@ -816,3 +816,65 @@ def test_kv_groups_brute_force_and_combine():
                 for c in range(4):
                     want_o[c] += gates[0, t, kk] * hv[c]
         np.testing.assert_allclose(o[0, t], want_o, rtol=1e-12, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# always-active shared heads (Sec. 5, shared heads for local context)
+
+def _shared_case(seed, B=2, Hs=2, T=40, d=8):
+    r = np.random.default_rng(seed)
+    return (r.standard_normal((B, Hs, T, d)) for _ in range(3))
+
+
+def test_shared_full_prefix_is_causal_attention_with_rope():
+    torch = pytest.importorskip("torch")
+    F = torch.nn.functional
+    q, k, v = _shared_case(91)
+    B, Hs, T, d = q.shape
+    pos = np.broadcast_to(np.arange(T), (B, Hs, T))
+    ref = F.scaled_dot_product_attention(torch.from_numpy(O.rope_rotate(q, pos, 1e4)),
+                                         torch.from_numpy(O.rope_rotate(k, pos, 1e4)),
+                                         torch.from_numpy(v), is_causal=True).numpy()
+    np.testing.assert_allclose(O.always_active_heads(q, k, v, 0, 1e4), ref, rtol=1e-12, atol=1e-12)
+    # a window at least as long as the sequence is the full prefix
+    np.testing.assert_allclose(O.always_active_heads(q, k, v, T, 1e4), ref, rtol=1e-12, atol=1e-12)
+
+
+def test_shared_sliding_window_against_a_library_mask():
+    # the band mask t - w < s <= t handed to torch's attention as a boolean mask
+    torch = pytest.importorskip("torch")
+    F = torch.nn.functional
+    q, k, v = _shared_case(92, T=37)
+    B, Hs, T, d = q.shape
+    w = 5
+    pos = np.broadcast_to(np.arange(T), (B, Hs, T))
+    i = torch.arange(T)
+    band = (i[None, :] <= i[:, None]) & (i[None, :] > i[:, None] - w)
+    ref = F.scaled_dot_product_attention(torch.from_numpy(O.rope_rotate(q, pos, 1e4)),
+                                         torch.from_numpy(O.rope_rotate(k, pos, 1e4)),
+                                         torch.from_numpy(v), attn_mask=band).numpy()
+    np.testing.assert_allclose(O.always_active_heads(q, k, v, w, 1e4), ref, rtol=1e-12, atol=1e-12)
+
+
+def test_shared_window_special_cases():
+    q, k, v = _shared_case(93, T=20)
+    # w = 1: every token attends to itself only
+    np.testing.assert_allclose(O.always_active_heads(q, k, v, 1, 1e4), v, rtol=1e-13, atol=1e-13)
+    # constant values give that constant, whatever the window
+    c = np.full_like(v, 0.75)
+    np.testing.assert_allclose(O.always_active_heads(q, k, c, 4, 1e4), c, rtol=1e-13, atol=1e-13)
+    # q = 0: the mean of the window's values (closed form)
+    z = np.zeros_like(q)
+    got = O.always_active_heads(z, k, v, 3, 1e4, O.ROPE_NONE)
+    for t in range(20):
+        lo = max(0, t - 2)
+        np.testing.assert_allclose(got[:, :, t], v[:, :, lo:t + 1].mean(axis=2), rtol=1e-12,
+                                   atol=1e-12)
+    # global RoPE: shifting every position by the same amount leaves the
+    # output unchanged (scores depend on position differences only)
+    a = O.always_active_heads(q, k, v, 6, 1e4, O.ROPE_GLOBAL)
+    B, Hs, T, d = q.shape
+    pos = np.broadcast_to(np.arange(T) + 9, (B, Hs, T))
+    qs, ks = O.rope_rotate(q, pos, 1e4), O.rope_rotate(k, pos, 1e4)
+    b = O.always_active_heads(qs, ks, v, 6, 1e4, O.ROPE_NONE)
+    np.testing.assert_allclose(a, b, rtol=1e-10, atol=1e-10)
