@@ -353,6 +353,64 @@ def bench_grouped(w, args, torch, L, DI):
 
 
 # ----------------------------------------------------------------------------
+def bench_shared(w, args, torch, L, DI):
+    """A prefill step with always-active shared heads added: routing, routed
+    attention, then Hs shared heads (causal or sliding window) summed into
+    the same output."""
+    hs, win = (int(x) for x in args.shared.split(":"))
+    dev = torch.device("cuda:0")
+    log(f"generating inputs for {w.name} with {hs} shared heads, window {win}")
+    inp = W.prefill_inputs(w)
+    logits = torch.from_numpy(inp["logits"]).to(dev)
+    q, k, v = (DI.to_device(inp[n], w.dtype, dev) for n in ("q", "k", "v"))
+    ws_ = w.with_(H=hs, K=1, seed=w.seed + 100)
+    qs, ks, vs = (DI.to_device(W.prefill_qkv(ws_, n), w.dtype, dev) for n in ("q", "k", "v"))
+    B, T, H, K, d = w.B, w.T, w.H, w.K, w.d
+    routing = L.route(logits, K)
+    rws = L.workspace(L.route_workspace_size(B, T, H, K), dev)
+    aws = L.workspace(L.attn_workspace_size(B, T, H, K, d, L.dtype_code(q.dtype)), dev)
+    sws = L.workspace(int(L.lib().namoh_shared_attn_workspace_size(B, T, hs, d)), dev)
+    out = torch.empty(B, T, d, dtype=q.dtype, device=dev)
+
+    def step():
+        L.route(logits, K, L.GATE_SOFTMAX_SELECTED, out=routing, ws=rws)
+        L.attn_fwd(q, k, v, routing, K, w.rope_base, out=out, ws=aws)
+        L.shared_attn(qs, ks, vs, win, w.rope_base, out=out, accumulate=True, ws=sws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    L.profile_enable(2 * args.steps)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    r = L.profile_read("attn")
+    L.profile_enable(0)
+    # the "attn" section holds the routed and the shared attention launches of
+    # every step, in that order
+    times = None if r is None else r[0] / r[1]
+    t = np.arange(T, dtype=np.int64)
+    pairs = int((np.minimum(t + 1, win) if win > 0 else t + 1).sum()) * B * hs
+    return {"metric": "routed-attn prefill plus always-active shared heads, tokens/s (1 GPU)",
+            "value": round(B * T / (ms_step * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+            "data": "synthetic",
+            "config": {"workload": w.name, "shared_heads": hs, "window": win, "B": B, "T": T,
+                       "H": H, "K": K, "d_head": d, "rope": "head-relative (routed), global "
+                       "(shared)", "rope_base": w.rope_base},
+            "shared_attention": {"flops": 4.0 * d * pairs, "pairs": pairs},
+            "attn_kernels_mean_ms": None if times is None else round(times, 4)}
+
+
+# ----------------------------------------------------------------------------
 def bench_backward(w, args, torch, L, DI):
     """One training step of the layer: route, forward, backward of the
     attention (dq, dk, dv, dgates) and of the gates (d logits)."""
@@ -550,6 +608,9 @@ def main():
     ap.add_argument("--kv-group", type=int, default=1,
                     help="key/value-group routing with groups of this many query heads "
                          "(prefill workloads; K/g of H/g groups selected per token)")
+    ap.add_argument("--shared", type=str, default=None,
+                    help="HS:W - add HS always-active shared heads with a window of W tokens "
+                         "(0 = full causal prefix) to a prefill workload")
     ap.add_argument("--backward", action="store_true",
                     help="time a training step (route, forward, backward) of a prefill "
                          "workload instead of the forward step")
@@ -592,6 +653,11 @@ def main():
         res = bench_backward(w, args, torch, L, DI)
     elif w.d_model:
         res = bench_layer(w, args, torch, L, DI)
+    elif args.shared:
+        if w.decode:
+            print(json.dumps({"error": "--shared needs a prefill workload"}))
+            sys.exit(2)
+        res = bench_shared(w, args, torch, L, DI)
     elif args.kv_group > 1:
         if w.decode:
             print(json.dumps({"error": "--kv-group needs a prefill workload"}))

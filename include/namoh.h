@@ -238,6 +238,30 @@ namoh_status namoh_attn_fwd_grouped(const void* q, const void* k, const void* v,
                                     size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Always-active shared heads (Sec. 5, "shared heads for local context"):
+ * Hs heads outside the routing, each attending for every token either to
+ * the full causal prefix (window = 0, or window >= T) or to the most recent
+ * `window` tokens including the token itself (t - window < s <= t), with
+ * RoPE at the global position t (rope_mode GLOBAL; HEAD_RELATIVE is the same
+ * position here, since every token is in every shared head; NONE: no
+ * rotation).  Their outputs are added to the layer output without a gate:
+ *   out[b, t] = (accumulate ? out[b, t] : 0) + sum_{s < Hs} h_s(b, t),
+ * with the heads summed in order (call it after namoh_attn_fwd to add the
+ * shared heads to the routed output).
+ * In:  q, k, v [B, Hs, T, d] bf16 (d in {64, 128}, else UNSUPPORTED).
+ * Out: out [B, T, d] of out_dtype (may be NULL when head_out is given);
+ *      head_out optional float32 [B, Hs, T, d] (the per-head outputs).
+ * Limits: Hs >= 1, B*Hs*T < 2^31, window >= 0.
+ * ---------------------------------------------------------------------- */
+size_t namoh_shared_attn_workspace_size(int B, int T, int Hs, int d_head);
+
+namoh_status namoh_shared_attn(const void* q, const void* k, const void* v, int dtype, int B,
+                               int T, int Hs, int d_head, int window, float rope_base,
+                               int rope_mode, float softmax_scale, void* out, int out_dtype,
+                               int accumulate, float* head_out, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Routed per-head projections (Sec. 3.1, Eq. namoh-qkv: tokens are
  * dispatched to their heads before projection, and only active (token, head)
  * pairs compute q, k, v; Eq. namoh-attention: o_t = sum over the selected

@@ -34,6 +34,7 @@ EXPORTED = (
     "namoh_decode_workspace_size", "namoh_decode_step", "namoh_decode_step_biased",
     "namoh_qkv_proj", "namoh_out_proj_workspace_size", "namoh_out_proj",
     "namoh_attn_fwd_grouped_workspace_size", "namoh_attn_fwd_grouped",
+    "namoh_shared_attn_workspace_size", "namoh_shared_attn",
     "namoh_status_string", "namoh_last_error", "namoh_version",
     "namoh_profile_enable", "namoh_profile_read",
 )
@@ -65,6 +66,9 @@ _SIGS = {
     "namoh_attn_fwd_grouped_workspace_size": (_S, [_I, _I, _I, _I, _I, _I, _I]),
     "namoh_attn_fwd_grouped": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _I, _F,
                                     _P, _P, _P, _P, _P, _I, _P, _P, _S, _P]),
+    "namoh_shared_attn_workspace_size": (_S, [_I, _I, _I, _I]),
+    "namoh_shared_attn": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F, _P, _I, _I, _P,
+                               _P, _S, _P]),
     "namoh_qkv_proj": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P]),
     "namoh_out_proj_workspace_size": (_S, [_I, _I, _I, _I, _I]),
     "namoh_out_proj": (_I, [_P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _S, _P]),
@@ -267,6 +271,35 @@ def attn_fwd_grouped(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing:
         _ptr(routing["perm_token"]), _ptr(routing["slot_pos"]), None if skip else _ptr(out),
         dtype_code(odt) if skip else dtype_code(out.dtype), _ptr(head_out), _ptr(ws), ws.numel(),
         _stream(q.device)))
+    return head_out if skip else out
+
+
+def shared_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, window: int,
+                rope_base: float, rope_mode: int = ROPE_GLOBAL, softmax_scale: float = 0.0,
+                out=None, accumulate: bool = False, out_dtype: Optional[torch.dtype] = None,
+                head_out: Optional[torch.Tensor] = None,
+                ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """namoh_shared_attn: always-active heads q, k, v [B, Hs, T, d] (bf16),
+    causal (window 0) or inside a sliding window; out [B, T, d] (+)= the sum
+    of the heads (accumulate adds to the given out).  out=False with
+    head_out given skips the sum (returns head_out [B, Hs, T, d] float32)."""
+    skip = out is False
+    _need_cuda(q, k, v, None if skip else out, head_out)
+    B, Hs, T, d = q.shape
+    if k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v must share [B, Hs, T, d]")
+    if skip and head_out is None:
+        raise ValueError("out=False needs head_out")
+    if out is None:
+        out = torch.zeros(B, T, d, dtype=q.dtype if out_dtype is None else out_dtype,
+                          device=q.device)
+    if ws is None:
+        ws = workspace(int(lib().namoh_shared_attn_workspace_size(B, T, Hs, d)), q.device)
+    check(lib().namoh_shared_attn(_ptr(q), _ptr(k), _ptr(v), dtype_code(q.dtype), B, T, Hs, d,
+                                  int(window), float(rope_base), rope_mode, float(softmax_scale),
+                                  None if skip else _ptr(out),
+                                  F32 if skip else dtype_code(out.dtype), int(bool(accumulate)),
+                                  _ptr(head_out), _ptr(ws), ws.numel(), _stream(q.device)))
     return head_out if skip else out
 
 

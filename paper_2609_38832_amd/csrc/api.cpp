@@ -249,6 +249,60 @@ namoh_status namoh_prefill_cache(const void* k, const void* v, int dtype, int B,
                                                 static_cast<hipStream_t>(stream)));
 }
 
+namespace {
+namoh_status check_shared(int B, int T, int Hs, int d_head) {
+  REQUIRE(B >= 1, "B must be >= 1 (got %d)", B);
+  REQUIRE(T >= 1, "T must be >= 1 (got %d)", T);
+  REQUIRE(Hs >= 1 && Hs <= 1024, "Hs must be in [1, 1024] (got %d)", Hs);
+  REQUIRE(static_cast<long long>(B) * Hs * T < (1ll << 31), "B*Hs*T must be < 2^31");
+  if (d_head != 64 && d_head != 128)
+    return fail(NAMOH_ERR_UNSUPPORTED, "shared heads need d_head 64 or 128 (got %d)", d_head);
+  if ((static_cast<long long>(T) + 63) / 64 * 64 * d_head * 2 >= (1ll << 32))
+    return fail(NAMOH_ERR_UNSUPPORTED, "T = %d too long for d_head = %d on the bf16 path", T,
+                d_head);
+  return NAMOH_OK;
+}
+}  // namespace
+
+size_t namoh_shared_attn_workspace_size(int B, int T, int Hs, int d_head) {
+  if (check_shared(B, T, Hs, d_head) != NAMOH_OK) return 0;
+  return namoh::shared_workspace_bytes(B, T, Hs, d_head);
+}
+
+namoh_status namoh_shared_attn(const void* q, const void* k, const void* v, int dtype, int B,
+                               int T, int Hs, int d_head, int window, float rope_base,
+                               int rope_mode, float softmax_scale, void* out, int out_dtype,
+                               int accumulate, float* head_out, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  namoh_status s;
+  if ((s = check_shared(B, T, Hs, d_head)) != NAMOH_OK) return s;
+  REQUIRE(dtype == NAMOH_F32 || dtype == NAMOH_BF16, "unknown dtype %d", dtype);
+  if (dtype != NAMOH_BF16) return fail(NAMOH_ERR_UNSUPPORTED, "shared heads need bf16 inputs");
+  REQUIRE(window >= 0, "window must be >= 0 (got %d)", window);
+  REQUIRE(out_dtype == NAMOH_F32 || out_dtype == NAMOH_BF16, "unknown out_dtype %d", out_dtype);
+  REQUIRE(rope_mode == NAMOH_ROPE_HEAD_RELATIVE || rope_mode == NAMOH_ROPE_GLOBAL ||
+              rope_mode == NAMOH_ROPE_NONE,
+          "unknown rope_mode %d", rope_mode);
+  REQUIRE(rope_mode == NAMOH_ROPE_NONE || (std::isfinite(rope_base) && rope_base > 0.f),
+          "rope_base must be finite and > 0 (got %g)", static_cast<double>(rope_base));
+  REQUIRE(!std::isnan(softmax_scale) && !std::isinf(softmax_scale), "softmax_scale must be finite");
+  REQUIRE_PTR(q, 16);
+  REQUIRE_PTR(k, 16);
+  REQUIRE_PTR(v, 16);
+  REQUIRE(out != nullptr || head_out != nullptr, "out and head_out are both NULL");
+  if (out != nullptr) REQUIRE_PTR(out, 16);
+  if (head_out != nullptr) REQUIRE_PTR(head_out, 16);
+  if ((s = check_workspace(workspace, workspace_bytes,
+                           namoh::shared_workspace_bytes(B, T, Hs, d_head))) != NAMOH_OK)
+    return s;
+  const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
+  clear_hip_error();
+  return hip_status(namoh::launch_shared(q, k, v, B, T, Hs, d_head, window, rope_base,
+                                         rope_mode == NAMOH_ROPE_NONE ? 2 : 1, scale, out,
+                                         out_dtype, accumulate, head_out, workspace,
+                                         static_cast<hipStream_t>(stream)));
+}
+
 size_t namoh_attn_fwd_grouped_workspace_size(int B, int T, int H_kv, int K_kv, int group_size,
                                              int d_head, int dtype) {
   if (check_sizes(B, T, H_kv, K_kv) != NAMOH_OK || group_size < 1 || group_size > 16 ||

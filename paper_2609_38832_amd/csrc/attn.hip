@@ -545,11 +545,16 @@ NAMOH_DEV void qk_tile(f32x16 (&S)[2][NQT], const uint16_t* __restrict__ sKb,
 // a wave's first tile, which sets it to that tile's maximum; such a tile
 // (rare) subtracts the raise from its scores, rescales O and l, and
 // rebuilds the accumulator start.
-template <int D, int NQT, int NW>
+// WIN: keys are visible only inside the window qr - window < key <= qr, and a
+// lane's first tile with a visible key (fresh[qt]) sets its running maximum
+// (without a window the item's first tile always holds key 0, visible to
+// every query, and `first` plays that part for the whole wave).
+template <int D, int NQT, int NW, bool WIN = false>
 NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
                           float (&m_run)[NQT], float (&l_run)[NQT], f32x16 (&minit)[NQT],
                           bool first, bool fast, const uint16_t* __restrict__ sVb, int key0,
-                          int q0, int wave, int n, int c, int g) {
+                          int q0, int wave, int n, int c, int g, int window = 0,
+                          bool* fresh = nullptr) {
   // value operands: the first VPRE 16-key steps are read while the softmax
   // runs (all of them for d = 64; half for d = 128, to stay within 256
   // registers), the rest while the first P.V products execute
@@ -581,6 +586,23 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
             if (32 * kk + 8 * j + i > lim) S[kk][qt][4 * j + i] = -INFINITY;
     }
   }
+  if constexpr (WIN) {
+    // the window's lower end: key >= qr - window + 1, i.e. index >= lo
+    if (key0 < q0 + 32 * ((NQT - 1) * NW + wave) + 31 - window + 1) {
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt) {
+        const int qr = q0 + 32 * (qt * NW + wave) + c;
+        const int lo = qr - window + 1 - key0 - 4 * g;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (32 * kk + 8 * j + i < lo) S[kk][qt][4 * j + i] = -INFINITY;
+      }
+    }
+  }
   bf16x8 pB[NQT][4];
   float alpha[NQT], delta[NQT];
   bool rescale = false;
@@ -596,11 +618,26 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
       for (int i = 2; i < 32; i += 2)
         mx = fmaxf(fmaxf(mx, S[i >> 4][qt][i & 15]), S[i >> 4][qt][(i & 15) + 1]);
       mx = pair_max32(mx);
-      const bool up = first || mx > kLazyLog2;
-      delta[qt] = up ? mx : 0.f;
-      alpha[qt] = (up && !first) ? __builtin_amdgcn_exp2f(-mx) : 1.f;
-      rescale |= up;
+      if constexpr (WIN) {
+        // a lane with no visible key yet takes the first finite maximum (a
+        // row fully masked in this tile keeps m = 0 and adds nothing)
+        const bool fr = fresh[qt];
+        const bool up = fr ? mx > -INFINITY : mx > kLazyLog2;
+        delta[qt] = up ? mx : 0.f;
+        alpha[qt] = (up && !fr) ? __builtin_amdgcn_exp2f(-mx) : 1.f;
+        fresh[qt] = fr && !up;
+        rescale |= up;
+      } else {
+        const bool up = first || mx > kLazyLog2;
+        delta[qt] = up ? mx : 0.f;
+        alpha[qt] = (up && !first) ? __builtin_amdgcn_exp2f(-mx) : 1.f;
+        rescale |= up;
+      }
     }
+  } else if constexpr (WIN) {
+    // the norm bound holds: m = 0 is the reference from here on
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) fresh[qt] = false;
   }
   if (!fast && __any(rescale)) {
 #pragma unroll
@@ -613,7 +650,7 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
 #pragma unroll
       for (int e = 0; e < 16; ++e) minit[qt][e] = -m_run[qt];
     }
-    if (!first) {
+    if (WIN || !first) {   // (fresh lanes have alpha = 1 and O = 0)
 #pragma unroll
       for (int qt = 0; qt < NQT; ++qt)
 #pragma unroll
@@ -662,13 +699,16 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
 // in-lane plus one exchange with lane c ^ 32.  The probabilities leave the
 // accumulators in B-operand order for O^T += V^T P^T, against the value
 // tile stored transposed with the keys of each 16-key group permuted.
-template <int D, int NQT, int NW, bool HB>
+// WIN: sliding-window attention (keys qr - window < key <= qr); the item then
+// starts at the first key tile that meets its first query's window.
+template <int D, int NQT, int NW, bool HB, bool WIN = false>
 __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kp,
     const uint16_t* __restrict__ Vt, const double* __restrict__ freq,
     const int32_t* __restrict__ perm_token, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ meta, const float* __restrict__ knorm, int T, int H, int G,
-    int rope_mode, float scale_log2, void* __restrict__ hout, float* __restrict__ lse_out) {
+    int rope_mode, float scale_log2, void* __restrict__ hout, float* __restrict__ lse_out,
+    int window) {
   constexpr int BM = 32 * NQT * NW;
   constexpr int KS = D / 16;  // reduction steps of S^T = K Q^T
   constexpr int MT = D / 32;  // 32-row tiles of O^T
@@ -697,6 +737,9 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   // all its rows are padding past the segment's end
   const int wq_last = q0 + 32 * ((NQT - 1) * NW + wave) + 31;
   const int wave_tiles = q0 + 32 * wave < n ? min(wq_last, n - 1) / kBN + 1 : 0;
+  // first key tile of the item and of this wave (0 without a window)
+  const int kb = WIN ? max(0, q0 - window + 1) / kBN : 0;
+  const int wave_first = WIN ? max(0, q0 + 32 * wave - window + 1) / kBN : 0;
   // query head of the item: head h of the key/value segment, or with key/value
   // groups of G query heads, head h * G + qh; its head outputs are row
   // (packed row) * G + qh
@@ -740,6 +783,7 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   // uniform, and readfirstlane says so)
   const int tile0_s = __builtin_amdgcn_readfirstlane(tile0);
   const int kt_end_s = __builtin_amdgcn_readfirstlane(kt_end);
+  const int kb_s = __builtin_amdgcn_readfirstlane(kb);
   const uint16_t* const bK = Kp + static_cast<size_t>(tile0_s) * TS;
   const uint16_t* const bV = Vt + static_cast<size_t>(tile0_s) * TS;
   const uint32_t nb = static_cast<uint32_t>(kt_end_s) * TB;   // below 2^32 (checked on the host)
@@ -750,7 +794,7 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   const uint32_t lV = lds_address(&sV[0][0]) + wave_s * kWave * 16;
 #pragma unroll
   for (int i = 0; i < NS - 1; ++i) {
-    const uint32_t tb = static_cast<uint32_t>(min(i, kt_end_s - 1)) * TB;
+    const uint32_t tb = static_cast<uint32_t>(min(kb_s + i, kt_end_s - 1)) * TB;
     tile_dma<KPT, NT>(bK, nb, tb, lK + i * TB, voffK);
     tile_dma<KPT, NT>(bV, nb, tb, lV + i * TB, voffV);
   }
@@ -849,27 +893,30 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   // kt (near the end fewer tiles are in flight and the wait is for all).
   // After the barrier every wave has finished tile kt - 1, so its stage
   // receives tile kt + NS - 1.
-  for (int kt = 0; kt < kt_end; ++kt) {
-    const int st = kt % NS;
+  bool fresh[NQT];   // (WIN) no visible key seen yet by the lane's query
+#pragma unroll
+  for (int qt = 0; qt < NQT; ++qt) fresh[qt] = true;
+  for (int kt = kb; kt < kt_end; ++kt) {
+    const int st = (kt - kb) % NS;
     if (kt + NS - 2 < kt_end)
       wait_vmcnt<2 * KPT * (NS - 2)>();
     else
       wait_vmcnt<0>();
     __syncthreads();
     if (kt + NS - 1 < kt_end) {
-      const int nst = (kt + NS - 1) % NS;
+      const int nst = (kt - kb + NS - 1) % NS;
       const uint32_t tb = static_cast<uint32_t>(kt + NS - 1) * TB;
       tile_dma<KPT, NT>(bK, nb, tb, lK + nst * TB, voffK);
       tile_dma<KPT, NT>(bV, nb, tb, lV + nst * TB, voffV);
     }
-    if (kt < wave_tiles) {
+    if (kt < wave_tiles && kt >= wave_first) {
       f32x16 S[2][NQT];
       qk_tile<D, NQT>(S, sK[st], qB, minit, c, g);
       bool within = true;
 #pragma unroll
       for (int qt = 0; qt < NQT; ++qt) within &= qn[qt] <= m_run[qt] + kLazyLog2;
-      softmax_pv<D, NQT, NW>(S, O, m_run, l_run, minit, kt == 0, __all(within), sV[st], kt * kBN,
-                             q0, wave, n, c, g);
+      softmax_pv<D, NQT, NW, WIN>(S, O, m_run, l_run, minit, kt == 0, __all(within), sV[st],
+                                  kt * kBN, q0, wave, n, c, g, window, fresh);
     }
   }
 
@@ -885,7 +932,7 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     static_assert(NQT * NW <= 4, "epilogue staging: one 32-row block per wave in one stage");
     constexpr int NG = D / 8;          // 16-byte granules per output row
     constexpr int RPI = kWave / NG;    // rows per coalesced store
-    const int fs = kt_end_s % NS;
+    const int fs = (kt_end_s - kb_s) % NS;
     uint16_t* const ho = static_cast<uint16_t*>(hout);
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
@@ -1192,7 +1239,7 @@ template <int D>
 static void launch_mfma(const AttnWs& w, const void* q, const void* k, const void* v,
                         int B, int T, int H, int G, int Nr, int rope_mode, double log_base,
                         float scale_log2, const int32_t* seg_offsets, const int32_t* perm_token,
-                        void* hout, bool hout_bf16, float* lse, hipStream_t st) {
+                        void* hout, bool hout_bf16, float* lse, hipStream_t st, int window = 0) {
   constexpr int NW = MfmaShape<D>::NW, NQT = MfmaShape<D>::NQT;
   prof_mark("pack", true, st);
   k_pack_kv<D><<<static_cast<unsigned>(1 + w.max_tiles), kPackThreads, 0, st>>>(
@@ -1203,14 +1250,22 @@ static void launch_mfma(const AttnWs& w, const void* q, const void* k, const voi
   prof_mark("pack", false, st);
   prof_mark("attn", true, st);
   const unsigned grid = static_cast<unsigned>(w.max_items);
-  if (hout_bf16)
+  if (window > 0 && hout_bf16)
+    k_attn_mfma<D, NQT, NW, true, true><<<grid, NW * 64, 0, st>>>(
+        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.freq, perm_token, w.items, w.meta,
+        w.knorm, T, H, G, rope_mode, scale_log2, hout, nullptr, window);
+  else if (window > 0)
+    k_attn_mfma<D, NQT, NW, false, true><<<grid, NW * 64, 0, st>>>(
+        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.freq, perm_token, w.items, w.meta,
+        w.knorm, T, H, G, rope_mode, scale_log2, hout, nullptr, window);
+  else if (hout_bf16)
     k_attn_mfma<D, NQT, NW, true><<<grid, NW * 64, 0, st>>>(
         static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.freq, perm_token, w.items, w.meta,
-        w.knorm, T, H, G, rope_mode, scale_log2, hout, nullptr);
+        w.knorm, T, H, G, rope_mode, scale_log2, hout, nullptr, 0);
   else
     k_attn_mfma<D, NQT, NW, false><<<grid, NW * 64, 0, st>>>(
         static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.freq, perm_token, w.items, w.meta,
-        w.knorm, T, H, G, rope_mode, scale_log2, hout, lse);
+        w.knorm, T, H, G, rope_mode, scale_log2, hout, lse, 0);
   prof_mark("attn", false, st);
 }
 
@@ -1302,6 +1357,131 @@ hipError_t launch_combine_rows(const uint16_t* rows, const float* gates, const i
   else
     k_combine<true, false><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D, Nr,
                                                             1, out);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Always-active shared heads (Sec. 5, shared heads for local context): every
+// (sequence, shared head) is one segment holding all T tokens in order (so
+// the rank is the global position), attended causally or inside a window of
+// `window` tokens, and the heads' outputs are added to the layer output.
+__global__ __launch_bounds__(256) void k_shared_setup(int BH, int T, int32_t* __restrict__ seg_offsets,
+                                                      int32_t* __restrict__ perm_token) {
+  const size_t i = static_cast<size_t>(block_x()) * 256 + thread_x();
+  const size_t n = static_cast<size_t>(BH) * T;
+  if (i <= static_cast<size_t>(BH)) seg_offsets[i] = static_cast<int32_t>(i * T);
+  if (i < n) perm_token[i] = static_cast<int32_t>(i % T);
+}
+
+// out[b, t] = (ACC ? out[b, t] : 0) + sum over shared heads s (in order) of
+// h[(b * Hs + s) * T + t]; one thread per 8 columns.
+template <bool IN_BF16, bool OUT_BF16, bool ACC>
+__global__ __launch_bounds__(256) void k_shared_add(const void* __restrict__ h, int B, int T,
+                                                    int Hs, int D, void* __restrict__ out) {
+  const int C = D / 8;
+  const long idx = static_cast<long>(block_x()) * 256 + thread_x();
+  const long bt = idx / C;
+  const int cc = static_cast<int>(idx - bt * C);
+  if (bt >= static_cast<long>(B) * T) return;
+  const long b = bt / T, t = bt - b * T;
+  float acc[8];
+  if constexpr (ACC) {
+    if constexpr (OUT_BF16) {
+      unpack8(reinterpret_cast<const uint4*>(out)[idx], acc);
+    } else {
+      const float4* o = reinterpret_cast<const float4*>(out) + idx * 2;
+      const float4 a = o[0], c = o[1];
+      acc[0] = a.x; acc[1] = a.y; acc[2] = a.z; acc[3] = a.w;
+      acc[4] = c.x; acc[5] = c.y; acc[6] = c.z; acc[7] = c.w;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  }
+  for (int sh = 0; sh < Hs; ++sh) {
+    const size_t row = (static_cast<size_t>(b) * Hs + sh) * T + t;
+    float x[8];
+    if constexpr (IN_BF16) {
+      unpack8(reinterpret_cast<const uint4*>(h)[row * C + cc], x);
+    } else {
+      const float4* src = reinterpret_cast<const float4*>(h) + (row * C + cc) * 2;
+      const float4 a = src[0], c = src[1];
+      x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+      x[4] = c.x; x[5] = c.y; x[6] = c.z; x[7] = c.w;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += x[e];
+  }
+  if constexpr (OUT_BF16) {
+    reinterpret_cast<uint4*>(out)[idx] = pack8(acc);
+  } else {
+    float4* dst = reinterpret_cast<float4*>(out) + idx * 2;
+    dst[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    dst[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+  }
+}
+
+struct SharedWs {
+  AttnWs attn;
+  int32_t* seg_offsets;
+  int32_t* perm_token;
+  size_t bytes;
+};
+
+static SharedWs carve_shared(void* ws, int B, int T, int Hs, int d) {
+  SharedWs w;
+  // every token is a row of every shared head: H = K = Hs
+  w.attn = carve_attn(ws, B, T, Hs, Hs, d, 1);
+  Carver cv(ws == nullptr ? nullptr : static_cast<char*>(ws) + w.attn.bytes);
+  w.seg_offsets = cv.take<int32_t>(static_cast<size_t>(B) * Hs + 1);
+  w.perm_token = cv.take<int32_t>(static_cast<size_t>(B) * Hs * T);
+  w.bytes = w.attn.bytes + cv.off;
+  return w;
+}
+
+size_t shared_workspace_bytes(int B, int T, int Hs, int d) {
+  return carve_shared(nullptr, B, T, Hs, d).bytes;
+}
+
+hipError_t launch_shared(const void* q, const void* k, const void* v, int B, int T, int Hs, int d,
+                         int window, float rope_base, int rope_mode, float scale, void* out,
+                         int out_dtype, int accumulate, float* head_out, void* ws,
+                         hipStream_t st) {
+  const SharedWs w = carve_shared(ws, B, T, Hs, d);
+  const int BH = B * Hs;
+  const int Nr = B * T * Hs;
+  const size_t n = static_cast<size_t>(BH) * T + 1;
+  k_shared_setup<<<static_cast<unsigned>((n + 255) / 256), 256, 0, st>>>(BH, T, w.seg_offsets,
+                                                                         w.perm_token);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const bool hb = head_out == nullptr;
+  void* hout = hb ? static_cast<void*>(w.attn.hpack) : static_cast<void*>(head_out);
+  const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
+  const float sl2 = scale * 1.4426950408889634f;
+  // a window at least T long is the full causal prefix
+  const int win = window >= T ? 0 : window;
+  if (d == 64)
+    launch_mfma<64>(w.attn, q, k, v, B, T, Hs, 1, Nr, rope_mode, log_base, sl2, w.seg_offsets,
+                    w.perm_token, hout, hb, nullptr, st, win);
+  else
+    launch_mfma<128>(w.attn, q, k, v, B, T, Hs, 1, Nr, rope_mode, log_base, sl2, w.seg_offsets,
+                     w.perm_token, hout, hb, nullptr, st, win);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (out == nullptr) return hipSuccess;
+  const long threads = static_cast<long>(B) * T * (d / 8);
+  const unsigned grid = static_cast<unsigned>((threads + 255) / 256);
+#define NAMOH_SADD(IB, OB, AC) \
+  k_shared_add<IB, OB, AC><<<grid, 256, 0, st>>>(hout, B, T, Hs, d, out)
+  const bool ob = out_dtype == 1;
+  if (hb) {
+    if (ob) { if (accumulate) NAMOH_SADD(true, true, true); else NAMOH_SADD(true, true, false); }
+    else { if (accumulate) NAMOH_SADD(true, false, true); else NAMOH_SADD(true, false, false); }
+  } else {
+    if (ob) { if (accumulate) NAMOH_SADD(false, true, true); else NAMOH_SADD(false, true, false); }
+    else { if (accumulate) NAMOH_SADD(false, false, true); else NAMOH_SADD(false, false, false); }
+  }
+#undef NAMOH_SADD
   return hipGetLastError();
 }
 

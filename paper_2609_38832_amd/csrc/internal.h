@@ -66,6 +66,14 @@ hipError_t launch_attn_stats(const void* q, const void* k, const void* v, int B,
                              const int32_t* seg_offsets, const int32_t* perm_token, float* lse,
                              void* ws, AttnTiles& tiles, hipStream_t st);
 
+// Always-active shared heads (attn.hip): Hs heads over all T tokens, causal
+// (window 0) or inside a window of `window` tokens; out (+)= sum of the heads.
+size_t shared_workspace_bytes(int B, int T, int Hs, int d);
+hipError_t launch_shared(const void* q, const void* k, const void* v, int B, int T, int Hs, int d,
+                         int window, float rope_base, int rope_mode, float scale, void* out,
+                         int out_dtype, int accumulate, float* head_out, void* ws,
+                         hipStream_t st);
+
 // Gated combine of bf16 rows [Nr, D]: out[t] = sum_k gates[t,k] rows[slot_pos[t,k]]
 // (attn.hip; D a multiple of 8).
 hipError_t launch_combine_rows(const uint16_t* rows, const float* gates, const int32_t* slot_pos,

@@ -254,6 +254,22 @@ def test_grouped_workspace_grows_with_the_group(lib):
     assert lib.namoh_attn_fwd_grouped_workspace_size(2, 1024, 8, 2, 4, 64, 0) == 0
 
 
+def _shared(lib, dtype=1, B=2, T=300, Hs=2, d=64, window=128, base=1e4, rope=1, q=fake(0),
+            out=fake(3), odt=0, ho=None, wsb=1 << 30, ws=fake(5)):
+    return lib.namoh_shared_attn(q, fake(1), fake(2), dtype, B, T, Hs, d, window, base, rope, 0.0,
+                                 out, odt, 1, ho, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=0), 2), (dict(d=32), 2), (dict(dtype=2), 1), (dict(window=-1), 1),
+    (dict(Hs=0), 1), (dict(B=0), 1), (dict(rope=4), 1), (dict(base=0.0), 1), (dict(q=None), 1),
+    (dict(out=None), 1), (dict(out=P(A + 2)), 1), (dict(odt=3), 1), (dict(wsb=8), 3),
+    (dict(B=1 << 20, T=1 << 12, Hs=1), 1),
+])
+def test_shared_attn_rejects(lib, kw, code):
+    assert _shared(lib, **kw) == code
+
+
 def test_workspace_queries(lib):
     assert lib.namoh_route_workspace_size(0, 10, 8, 2) == 0
     assert lib.namoh_route_workspace_size(1, 10, 8, 2) > 0
