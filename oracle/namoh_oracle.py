@@ -75,7 +75,7 @@ __all__ = [
     "prefill_rows", "prefill_cache", "decode_step", "brute_force_layer", "interaction_count",
     "attention_backward", "gates_backward",
     "qkv_projection", "output_projection",
-    "attention_kv_groups", "combine_kv_groups",
+    "attention_kv_groups", "combine_kv_groups", "decode_step_kv_groups",
     "always_active_heads",
     "shared_head_counts",
 ]
@@ -719,6 +719,47 @@ def decode_step(logits, q, k, v, cache_k, cache_v, cache_len, K, rope_base,
             new_len[b, h] = n + 1
     return {"topk_idx": topk, "gates": g, "out": out, "head_out": heads,
             "new_k": new_k, "cache_len": new_len}
+
+
+def decode_step_kv_groups(logits, q, k, v, cache_k, cache_v, cache_len, K_kv, g, rope_base,
+                          rope_mode=ROPE_HEAD_RELATIVE, gate_mode=GATE_SOFTMAX_SELECTED,
+                          seq_pos=None, scale=None):
+    """One decoding step with key/value-group routing (R17).
+
+    logits [B, H_kv] (group logits); q float64 [B, H_kv*g, d]; k, v float64
+    [B, H_kv, d]; ``cache_k(b, j, n)`` / ``cache_v(b, j, n)`` return rows
+    [0, n) of group j's rotated keys / values; cache_len [B, H_kv].  The new
+    token takes rank n_j in each selected group j, appends one key/value row
+    there, and each of the group's g query heads attends over the group's
+    n_j + 1 rows.  Returns topk_idx [B, K_kv], gates, out [B, d] (the gated
+    sum over selected groups of the sum of their g head outputs), head_out
+    [B, K_kv, g, d] and the updated lengths."""
+    B, Hq, d = q.shape
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    topk = select_heads(logits, K_kv)
+    gt = route_gates(logits, topk, gate_mode)
+    out = np.zeros((B, d))
+    heads = np.zeros((B, K_kv, g, d))
+    new_len = np.array(cache_len, dtype=np.int64, copy=True)
+    for b in range(B):
+        for kk in range(K_kv):
+            j = int(topk[b, kk])
+            n = int(cache_len[b, j])
+            p = n if rope_mode == ROPE_HEAD_RELATIVE else (
+                None if rope_mode == ROPE_NONE else int(seq_pos[b]))
+            pos = None if p is None else np.array([p])
+            kt = _rotate(k[b, j][None], pos, rope_base)[0]
+            Kc = np.concatenate([np.asarray(cache_k(b, j, n), dtype=np.float64).reshape(n, d), kt[None]])
+            Vc = np.concatenate([np.asarray(cache_v(b, j, n), dtype=np.float64).reshape(n, d), v[b, j][None]])
+            for u in range(g):
+                qt = _rotate(q[b, j * g + u][None], pos, rope_base)[0]
+                sc = (Kc @ qt) * scale
+                w = np.exp(sc - sc.max())
+                w /= w.sum()
+                heads[b, kk, u] = w @ Vc
+                out[b] += gt[b, kk] * heads[b, kk, u]
+            new_len[b, j] = n + 1
+    return {"topk_idx": topk, "gates": gt, "out": out, "head_out": heads, "cache_len": new_len}
 
 
 # ----------------------------------------------------------------------------

@@ -878,3 +878,53 @@ def test_shared_window_special_cases():
     qs, ks = O.rope_rotate(q, pos, 1e4), O.rope_rotate(k, pos, 1e4)
     b = O.always_active_heads(qs, ks, v, 6, 1e4, O.ROPE_NONE)
     np.testing.assert_allclose(a, b, rtol=1e-10, atol=1e-10)
+
+
+def test_kv_group_decode_of_one_is_the_decode_step():
+    r = np.random.default_rng(86)
+    B, H, K, d, cap = 2, 5, 2, 8, 12
+    logits = r.standard_normal((B, H)).astype(np.float32)
+    q, k, v = (r.standard_normal((B, H, d)) for _ in range(3))
+    ck, cv = r.standard_normal((B, H, cap, d)), r.standard_normal((B, H, cap, d))
+    n = r.integers(0, cap - 1, size=(B, H))
+    a = O.decode_step(logits, q, k, v, lambda b, h, m: ck[b, h, :m], lambda b, h, m: cv[b, h, :m],
+                      n, K, 1e4)
+    b_ = O.decode_step_kv_groups(logits, q, k, v, lambda b, h, m: ck[b, h, :m],
+                                 lambda b, h, m: cv[b, h, :m], n, K, 1, 1e4)
+    np.testing.assert_allclose(b_["out"], a["out"], rtol=1e-13, atol=1e-13)
+    np.testing.assert_array_equal(b_["cache_len"], a["cache_len"])
+
+
+@pytest.mark.parametrize("rope_mode", [O.ROPE_HEAD_RELATIVE, O.ROPE_GLOBAL, O.ROPE_NONE])
+def test_kv_group_prefill_then_decode_is_the_definition(rope_mode):
+    # decoding token T from the grouped prefill's caches gives the grouped
+    # attention (definition form) of T + 1 tokens at its last row
+    r = np.random.default_rng(87)
+    B, T, G, Kg, g, d = 2, 17, 4, 2, 3, 8
+    base = 1e4
+    logits = r.standard_normal((B, T + 1, G)).astype(np.float32)
+    q = r.standard_normal((B, G * g, T + 1, d))
+    k = r.standard_normal((B, G, T + 1, d))
+    v = r.standard_normal((B, G, T + 1, d))
+    topk = O.select_heads(logits, Kg)
+    full = O.attention_kv_groups(q, k, v, topk, g, base, rope_mode, form="definition")
+    gates = O.route_gates(logits, topk, O.GATE_SOFTMAX_SELECTED)
+    o_full = O.combine_kv_groups(full, topk, gates, g)[:, T]
+    # caches of the first T tokens: each group's rotated keys and values in rank order
+    m = O.membership(topk[:, :T], G)
+    rank = O.head_ranks(m)
+    caches_k, caches_v, n = {}, {}, np.zeros((B, G), dtype=np.int64)
+    for b in range(B):
+        for j in range(G):
+            rows = np.nonzero(m[b, :, j])[0]
+            n[b, j] = rows.size
+            pos = {O.ROPE_HEAD_RELATIVE: rank[b, rows, j], O.ROPE_GLOBAL: rows,
+                   O.ROPE_NONE: None}[rope_mode]
+            caches_k[b, j] = k[b, j, rows] if pos is None else O.rope_rotate(k[b, j, rows], pos, base)
+            caches_v[b, j] = v[b, j, rows]
+    res = O.decode_step_kv_groups(logits[:, T], q[:, :, T], k[:, :, T], v[:, :, T],
+                                  lambda b, j, nn: caches_k[b, j][:nn],
+                                  lambda b, j, nn: caches_v[b, j][:nn], n, Kg, g, base, rope_mode,
+                                  seq_pos=np.full(B, T))
+    np.testing.assert_array_equal(res["topk_idx"], topk[:, T])
+    np.testing.assert_allclose(res["out"], o_full, rtol=1e-11, atol=1e-11)
