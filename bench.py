@@ -493,6 +493,12 @@ def bench_backward(w, args, torch, L, DI):
 # ----------------------------------------------------------------------------
 def bench_decode(w, args, torch, L, DI):
     dev = torch.device("cuda:0")
+    g = args.kv_group
+    wq = w
+    if g > 1:   # key/value groups: the routing, caches and lengths are per group
+        if w.H % g or w.K % g:
+            raise SystemExit(f"--kv-group {g} must divide H = {w.H} and K = {w.K}")
+        w = w.with_(H=w.H // g, K=w.K // g)
     log(f"prior head lengths for {w.name}")
     lengths = W.decode_prior_lengths(w)
     cap = W.decode_cache_capacity(lengths, steps=args.warmup + 2 * args.steps + 1)
@@ -500,16 +506,25 @@ def bench_decode(w, args, torch, L, DI):
     kc, vc = DI.decode_caches(w.B, w.H, cap, w.d, w.dtype, w.seed, w.qkv_scale, dev)
     step_in = W.decode_step_inputs(w)
     logits = torch.from_numpy(step_in["logits"]).to(dev)
-    q, k, v = (DI.to_device(step_in[n], w.dtype, dev) for n in ("q", "k", "v"))
+    q_in = step_in["q"] if g == 1 else W.decode_step_inputs(wq)["q"]
+    q = DI.to_device(q_in, w.dtype, dev)
+    k, v = (DI.to_device(step_in[n], w.dtype, dev) for n in ("k", "v"))
     cache_len = torch.from_numpy(lengths).to(dev)
     B, H, K, d = w.B, w.H, w.K, w.d
     outd = {"topk_idx": torch.empty(B, K, dtype=torch.int32, device=dev),
             "gates": torch.empty(B, K, dtype=torch.float32, device=dev),
             "out": torch.empty(B, d, dtype=q.dtype, device=dev)}
-    ws = L.workspace(L.decode_workspace_size(B, H, K, d, cap), dev)
+    if g == 1:
+        ws = L.workspace(L.decode_workspace_size(B, H, K, d, cap), dev)
 
-    def step():
-        L.decode_step(logits, q, k, v, kc, vc, cache_len, K, w.rope_base, out=outd, ws=ws)
+        def step():
+            L.decode_step(logits, q, k, v, kc, vc, cache_len, K, w.rope_base, out=outd, ws=ws)
+    else:
+        ws = L.workspace(int(L.lib().namoh_decode_grouped_workspace_size(B, H, K, g, d, cap)), dev)
+
+        def step():
+            r = L.decode_step_grouped(logits, q, k, v, kc, vc, cache_len, K, w.rope_base, ws=ws)
+            outd.update(r)
 
     log(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):
@@ -549,7 +564,8 @@ def bench_decode(w, args, torch, L, DI):
            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
-           "config": {"workload": w.name, "B": B, "prior_tokens": w.prior, "H": H, "K": K,
+           "config": {"workload": wq.name, "B": B, "prior_tokens": w.prior, "H": wq.H, "K": wq.K,
+                      "kv_group": g, "H_kv": H, "K_kv": K,
                       "d_head": d, "cap": cap, "rope": "head-relative", "rope_base": w.rope_base},
            "roofline": {"kernel": "k_decode_attn", "bound": "hbm", "achieved": round(gbs_kern, 1),
                         "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -559,7 +575,7 @@ def bench_decode(w, args, torch, L, DI):
                                                    "rows": float(np.mean(rows[args.steps:]))},
                         "kernel_ms": round(kern_ms, 4)},
            "tokens_per_s": round(B / (ms_step * 1e-3), 1)}
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and g == 1:
         res["cpu_baseline"] = cpu_baseline_decode(w, step_in, kc, vc, len0, topk, args.cpu_budget, torch)
     del kc, vc
     return res
@@ -658,10 +674,7 @@ def main():
             print(json.dumps({"error": "--shared needs a prefill workload"}))
             sys.exit(2)
         res = bench_shared(w, args, torch, L, DI)
-    elif args.kv_group > 1:
-        if w.decode:
-            print(json.dumps({"error": "--kv-group needs a prefill workload"}))
-            sys.exit(2)
+    elif args.kv_group > 1 and not w.decode:
         res = bench_grouped(w, args, torch, L, DI)
     else:
         res = (bench_decode if w.decode else bench_prefill)(w, args, torch, L, DI)

@@ -238,6 +238,36 @@ namoh_status namoh_attn_fwd_grouped(const void* q, const void* k, const void* v,
                                     size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * One decoding step with key/value-group routing (App. "GQA+NAMOH", adopted
+ * KV-group routing; the decode counterpart of namoh_attn_fwd_grouped): the
+ * new token selects K_kv of the H_kv groups from its group logits (as
+ * namoh_decode_step selects heads), appends one rotated key and its value
+ * to each selected group's cache at rank n = cache_len (RoPE at the
+ * group-local rank, the global position, or none), and each of the group's
+ * g query heads attends over the group's n + 1 rows; the step reads each
+ * cached row once for all g heads.
+ *   out[b] = sum_k gates[b,k] * sum_{u<g} h(query head topk_idx[b,k]*g + u).
+ * In:  logits [B, H_kv] f32; q [B, H_kv*g, d]; k, v [B, H_kv, d] (only the
+ *      selected groups read); caches [B, H_kv, cap, d], cache_len [B, H_kv]
+ *      as for namoh_decode_step.  bf16, d in {64, 128}, group_size in
+ *      {1, 2, 4, 8} (else UNSUPPORTED / INVALID_ARG).
+ * Out: topk_idx, gates [B, K_kv]; out [B, d] of out_dtype; caches and
+ *      cache_len updated; dev_status as for namoh_decode_step.
+ * Workspace: namoh_decode_grouped_workspace_size bytes.
+ * ---------------------------------------------------------------------- */
+size_t namoh_decode_grouped_workspace_size(int B, int H_kv, int K_kv, int group_size, int d_head,
+                                           int cap);
+
+namoh_status namoh_decode_step_grouped(const float* logits, const void* q, const void* k,
+                                       const void* v, int dtype, void* k_cache, void* v_cache,
+                                       int32_t* cache_len, const int32_t* seq_pos, int B, int H_kv,
+                                       int K_kv, int group_size, int d_head, int cap,
+                                       float rope_base, int rope_mode, int gate_mode,
+                                       float softmax_scale, int32_t* topk_idx, float* gates,
+                                       void* out, int out_dtype, int32_t* dev_status,
+                                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Always-active shared heads (Sec. 5, "shared heads for local context"):
  * Hs heads outside the routing, each attending for every token either to
  * the full causal prefix (window = 0, or window >= T) or to the most recent

@@ -35,6 +35,7 @@ EXPORTED = (
     "namoh_qkv_proj", "namoh_out_proj_workspace_size", "namoh_out_proj",
     "namoh_attn_fwd_grouped_workspace_size", "namoh_attn_fwd_grouped",
     "namoh_shared_attn_workspace_size", "namoh_shared_attn",
+    "namoh_decode_grouped_workspace_size", "namoh_decode_step_grouped",
     "namoh_status_string", "namoh_last_error", "namoh_version",
     "namoh_profile_enable", "namoh_profile_read",
 )
@@ -69,6 +70,9 @@ _SIGS = {
     "namoh_shared_attn_workspace_size": (_S, [_I, _I, _I, _I]),
     "namoh_shared_attn": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F, _P, _I, _I, _P,
                                _P, _S, _P]),
+    "namoh_decode_grouped_workspace_size": (_S, [_I, _I, _I, _I, _I, _I]),
+    "namoh_decode_step_grouped": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I,
+                                       _I, _F, _I, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
     "namoh_qkv_proj": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P]),
     "namoh_out_proj_workspace_size": (_S, [_I, _I, _I, _I, _I]),
     "namoh_out_proj": (_I, [_P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _S, _P]),
@@ -368,6 +372,40 @@ def route_bwd(logits: torch.Tensor, routing: dict, dgates: torch.Tensor,
                                 _ptr(dgates), B, T, H, K, gate_mode, _ptr(dl),
                                 _stream(logits.device)))
     return dl
+
+
+def decode_step_grouped(logits: torch.Tensor, q: torch.Tensor, k: torch.Tensor,
+                        v: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                        cache_len: torch.Tensor, K_kv: int, rope_base: float,
+                        rope_mode: int = ROPE_HEAD_RELATIVE,
+                        gate_mode: int = GATE_SOFTMAX_SELECTED, softmax_scale: float = 0.0,
+                        seq_pos: Optional[torch.Tensor] = None,
+                        out_dtype: Optional[torch.dtype] = None,
+                        dev_status: Optional[torch.Tensor] = None,
+                        ws: Optional[torch.Tensor] = None) -> dict:
+    """namoh_decode_step_grouped: group logits [B, H_kv], q [B, H_kv*g, d],
+    k, v [B, H_kv, d], caches [B, H_kv, cap, d] (bf16), updated in place."""
+    _need_cuda(logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, dev_status)
+    B, Hq, d = q.shape
+    Hkv = k.shape[1]
+    if Hq % Hkv or k.shape != v.shape or k.shape[0] != B or k.shape[2] != d:
+        raise ValueError("q [B, H_kv*g, d], k and v [B, H_kv, d]")
+    g = Hq // Hkv
+    cap = k_cache.shape[2]
+    dev = q.device
+    odt = q.dtype if out_dtype is None else out_dtype
+    res = {"topk_idx": torch.empty(B, K_kv, dtype=torch.int32, device=dev),
+           "gates": torch.empty(B, K_kv, dtype=torch.float32, device=dev),
+           "out": torch.empty(B, d, dtype=odt, device=dev)}
+    if ws is None:
+        ws = workspace(int(lib().namoh_decode_grouped_workspace_size(B, Hkv, K_kv, g, d, cap)), dev)
+    check(lib().namoh_decode_step_grouped(
+        _ptr(logits), _ptr(q), _ptr(k), _ptr(v), dtype_code(q.dtype), _ptr(k_cache),
+        _ptr(v_cache), _ptr(cache_len), _ptr(seq_pos), B, Hkv, K_kv, g, d, cap, float(rope_base),
+        rope_mode, gate_mode, float(softmax_scale), _ptr(res["topk_idx"]), _ptr(res["gates"]),
+        _ptr(res["out"]), dtype_code(odt), _ptr(dev_status), _ptr(ws), ws.numel(),
+        _stream(dev)))
+    return res
 
 
 def qkv_proj(x: torch.Tensor, w_qkv: torch.Tensor, routing: dict, H: int, K: int,

@@ -493,6 +493,14 @@ size_t namoh_decode_workspace_size(int B, int H, int K, int d_head, int cap) {
   return namoh::decode_workspace_bytes(B, H, K, d_head, cap);
 }
 
+size_t namoh_decode_grouped_workspace_size(int B, int H_kv, int K_kv, int group_size, int d_head,
+                                           int cap) {
+  if (check_sizes(B, 1, H_kv, K_kv) != NAMOH_OK || (d_head != 64 && d_head != 128) || cap < 1 ||
+      (group_size != 1 && group_size != 2 && group_size != 4 && group_size != 8))
+    return 0;
+  return namoh::decode_workspace_bytes(B, H_kv, K_kv, d_head, cap, group_size);
+}
+
 static namoh_status decode_common(const float* logits, const float* bias, const void* q,
                                   const void* k, const void* v, int dtype, void* k_cache,
                                   void* v_cache, int32_t* cache_len, const int32_t* seq_pos,
@@ -500,10 +508,18 @@ static namoh_status decode_common(const float* logits, const float* bias, const 
                                   int rope_mode, int gate_mode, float softmax_scale,
                                   int32_t* topk_idx, float* gates, void* out, int out_dtype,
                                   int32_t* dev_status, void* workspace, size_t workspace_bytes,
-                                  void* stream) {
+                                  void* stream, int group_size = 0) {
+  // group_size 0: the per-head step; >= 1: key/value groups of that many
+  // query heads (namoh_decode_step_grouped)
   namoh_status s;
   if ((s = check_sizes(B, 1, H, K)) != NAMOH_OK) return s;
   if ((s = check_head_width(d_head)) != NAMOH_OK) return s;
+  if (group_size != 0) {
+    REQUIRE(group_size == 1 || group_size == 2 || group_size == 4 || group_size == 8,
+            "group_size must be 1, 2, 4 or 8 (got %d)", group_size);
+    if (dtype != NAMOH_BF16 || (d_head != 64 && d_head != 128))
+      return fail(NAMOH_ERR_UNSUPPORTED, "grouped decode needs bf16 and d_head 64 or 128");
+  }
   REQUIRE(cap >= 1, "cap must be >= 1 (got %d)", cap);
   REQUIRE(dtype == NAMOH_F32 || dtype == NAMOH_BF16, "unknown dtype %d", dtype);
   REQUIRE(out_dtype == NAMOH_F32 || out_dtype == NAMOH_BF16, "unknown out_dtype %d", out_dtype);
@@ -528,10 +544,17 @@ static namoh_status decode_common(const float* logits, const float* bias, const 
   REQUIRE_PTR(out, 16);
   if (dev_status != nullptr) REQUIRE_PTR(dev_status, 4);
   if ((s = check_workspace(workspace, workspace_bytes,
-                           namoh::decode_workspace_bytes(B, H, K, d_head, cap))) != NAMOH_OK)
+                           namoh::decode_workspace_bytes(B, H, K, d_head, cap,
+                                                         group_size > 0 ? group_size : 1))) !=
+      NAMOH_OK)
     return s;
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
   clear_hip_error();
+  if (group_size != 0)
+    return hip_status(namoh::launch_decode_grouped(
+        logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, B, H, K, group_size, d_head, cap,
+        rope_base, rope_mode, gate_mode, scale, topk_idx, gates, out, out_dtype, dev_status,
+        workspace, static_cast<hipStream_t>(stream)));
   return hip_status(namoh::launch_decode(logits, bias, q, k, v, dtype, k_cache, v_cache,
                                          cache_len, seq_pos, B, H, K, d_head, cap, rope_base,
                                          rope_mode, gate_mode, scale, topk_idx, gates, out,
@@ -565,6 +588,22 @@ namoh_status namoh_decode_step_biased(const float* logits, const float* bias, co
                        K, d_head, cap, rope_base, rope_mode, NAMOH_GATE_SOFTMAX_ALL,
                        softmax_scale, topk_idx, gates, out, out_dtype, dev_status, workspace,
                        workspace_bytes, stream);
+}
+
+namoh_status namoh_decode_step_grouped(const float* logits, const void* q, const void* k,
+                                       const void* v, int dtype, void* k_cache, void* v_cache,
+                                       int32_t* cache_len, const int32_t* seq_pos, int B, int H_kv,
+                                       int K_kv, int group_size, int d_head, int cap,
+                                       float rope_base, int rope_mode, int gate_mode,
+                                       float softmax_scale, int32_t* topk_idx, float* gates,
+                                       void* out, int out_dtype, int32_t* dev_status,
+                                       void* workspace, size_t workspace_bytes, void* stream) {
+  if (group_size < 1) return fail(NAMOH_ERR_INVALID_ARG, "group_size must be >= 1 (got %d)",
+                                  group_size);
+  return decode_common(logits, nullptr, q, k, v, dtype, k_cache, v_cache, cache_len, seq_pos, B,
+                       H_kv, K_kv, d_head, cap, rope_base, rope_mode, gate_mode, softmax_scale,
+                       topk_idx, gates, out, out_dtype, dev_status, workspace, workspace_bytes,
+                       stream, group_size);
 }
 
 }  // extern "C"

@@ -59,7 +59,7 @@ __global__ __launch_bounds__(64 * kAppendWaves) void k_decode_route_append(
     int H, int K, long cap, double log_base, int rope_mode, int gate_mode,
     const float* __restrict__ bias, float qscale, int32_t* __restrict__ topk_idx,
     float* __restrict__ gates, int32_t* __restrict__ dev_status, float* __restrict__ qrot,
-    int32_t* __restrict__ rows) {
+    int32_t* __restrict__ rows, int G) {
   const int b = block_x();
   const int lane = thread_x() % 64;
   const int wave = thread_x() / 64;
@@ -131,13 +131,18 @@ __global__ __launch_bounds__(64 * kAppendWaves) void k_decode_route_append(
         sn = w.y;
       }
       const float k1 = ld_elem<BF16>(k, src + j), k2 = ld_elem<BF16>(k, src + j + D / 2);
-      const float q1 = ld_elem<BF16>(q, src + j), q2 = ld_elem<BF16>(q, src + j + D / 2);
       st_elem<BF16>(k_cache, dst + j, k1 * cs - k2 * sn);
       st_elem<BF16>(k_cache, dst + j + D / 2, k2 * cs + k1 * sn);
       st_elem<BF16>(v_cache, dst + j, ld_elem<BF16>(v, src + j));
       st_elem<BF16>(v_cache, dst + j + D / 2, ld_elem<BF16>(v, src + j + D / 2));
-      qrot[bk * D + j] = (q1 * cs - q2 * sn) * qscale;
-      qrot[bk * D + j + D / 2] = (q2 * cs + q1 * sn) * qscale;
+      // the head's G query heads (G = 1 without key/value groups), rotated at
+      // the same rank
+      for (int u = 0; u < G; ++u) {
+        const size_t qs = (bh * G + u) * D;
+        const float q1 = ld_elem<BF16>(q, qs + j), q2 = ld_elem<BF16>(q, qs + j + D / 2);
+        qrot[(bk * G + u) * D + j] = (q1 * cs - q2 * sn) * qscale;
+        qrot[(bk * G + u) * D + j + D / 2] = (q2 * cs + q1 * sn) * qscale;
+      }
     }
     if (lane == 0) {
       cache_len[bh] = n + 1;
@@ -146,7 +151,11 @@ __global__ __launch_bounds__(64 * kAppendWaves) void k_decode_route_append(
   }
 }
 
-template <int D, bool BF16>
+// GQ queries per history row (the query heads of a key/value group; 1
+// without groups): each row is read once and scored against all of them, with
+// one online softmax per query; the partial of query u of selected head bk is
+// (bk * GQ + u) * nchunk + chunk.
+template <int D, bool BF16, int GQ = 1>
 __global__ __launch_bounds__(256) void k_decode_attn(
     const void* __restrict__ k_cache, const void* __restrict__ v_cache,
     const int32_t* __restrict__ topk_idx, const int32_t* __restrict__ rows,
@@ -156,9 +165,10 @@ __global__ __launch_bounds__(256) void k_decode_attn(
   constexpr int G = D / EPG;          // lanes per row
   constexpr int RPW = 64 / G;         // rows per wave per step
   constexpr int RPB = 4 * RPW;        // rows per workgroup per step
-  constexpr int U = kDecUnroll;
-  __shared__ float s_ml[RPB][2];
-  __shared__ float s_acc[RPB][D];
+  // rows per lane in flight, fewer with more queries per row (registers)
+  constexpr int U = GQ <= 2 ? kDecUnroll : (GQ == 4 ? kDecUnroll / 2 : kDecUnroll / 4);
+  __shared__ float s_ml[GQ][RPB][2];
+  __shared__ float s_acc[GQ][RPB][D];
 
   const int bk = block_x() / nchunk;
   const int chunk = block_x() - bk * nchunk;
@@ -174,12 +184,20 @@ __global__ __launch_bounds__(256) void k_decode_attn(
   const int sub = lane % G;
   const int grp = wave * RPW + lane / G;
 
-  float qv[EPG];
+  float qv[GQ][EPG];
 #pragma unroll
-  for (int e = 0; e < EPG; ++e) qv[e] = qrot[static_cast<size_t>(bk) * D + sub * EPG + e];
-  float m = -1e30f, lsum = 0.f, acc[EPG];
+  for (int u = 0; u < GQ; ++u)
 #pragma unroll
-  for (int e = 0; e < EPG; ++e) acc[e] = 0.f;
+    for (int e = 0; e < EPG; ++e)
+      qv[u][e] = qrot[(static_cast<size_t>(bk) * GQ + u) * D + sub * EPG + e];
+  float m[GQ], lsum[GQ], acc[GQ][EPG];
+#pragma unroll
+  for (int u = 0; u < GQ; ++u) {
+    m[u] = -1e30f;
+    lsum[u] = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPG; ++e) acc[u][e] = 0.f;
+  }
 
   const u32x4* kc = reinterpret_cast<const u32x4*>(k_cache);
   const u32x4* vc = reinterpret_cast<const u32x4*>(v_cache);
@@ -197,7 +215,7 @@ __global__ __launch_bounds__(256) void k_decode_attn(
         vx[u] = kx[u];
       }
     }
-    float sc[U];
+    float sc[GQ][U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       float f[EPG];
@@ -212,25 +230,36 @@ __global__ __launch_bounds__(256) void k_decode_attn(
         f[0] = __uint_as_float(kx[u].x); f[1] = __uint_as_float(kx[u].y);
         f[2] = __uint_as_float(kx[u].z); f[3] = __uint_as_float(kx[u].w);
       }
-      float dsum = 0.f;
 #pragma unroll
-      for (int e = 0; e < EPG; ++e) dsum = fmaf(qv[e], f[e], dsum);
+      for (int qq = 0; qq < GQ; ++qq) {
+        float dsum = 0.f;
 #pragma unroll
-      for (int o = G / 2; o > 0; o >>= 1) dsum += __shfl_xor(dsum, o);
-      sc[u] = (rb + u * RPB + grp < r1) ? dsum : -INFINITY;
+        for (int e = 0; e < EPG; ++e) dsum = fmaf(qv[qq][e], f[e], dsum);
+#pragma unroll
+        for (int o = G / 2; o > 0; o >>= 1) dsum += __shfl_xor(dsum, o);
+        sc[qq][u] = (rb + u * RPB + grp < r1) ? dsum : -INFINITY;
+      }
     }
-    float mx = sc[0];
+    float p[GQ][U];
 #pragma unroll
-    for (int u = 1; u < U; ++u) mx = fmaxf(mx, sc[u]);
-    const float mnew = fmaxf(m, mx);
-    const float corr = __builtin_amdgcn_exp2f(m - mnew);
-    lsum *= corr;
+    for (int qq = 0; qq < GQ; ++qq) {
+      float mx = sc[qq][0];
 #pragma unroll
-    for (int e = 0; e < EPG; ++e) acc[e] *= corr;
+      for (int u = 1; u < U; ++u) mx = fmaxf(mx, sc[qq][u]);
+      const float mnew = fmaxf(m[qq], mx);
+      const float corr = __builtin_amdgcn_exp2f(m[qq] - mnew);
+      lsum[qq] *= corr;
+#pragma unroll
+      for (int e = 0; e < EPG; ++e) acc[qq][e] *= corr;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        p[qq][u] = __builtin_amdgcn_exp2f(sc[qq][u] - mnew);
+        lsum[qq] += p[qq][u];
+      }
+      m[qq] = mnew;
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const float p = __builtin_amdgcn_exp2f(sc[u] - mnew);
-      lsum += p;
       float f[EPG];
       if constexpr (BF16) {
         const uint32_t w[4] = {vx[u].x, vx[u].y, vx[u].z, vx[u].w};
@@ -244,29 +273,34 @@ __global__ __launch_bounds__(256) void k_decode_attn(
         f[2] = __uint_as_float(vx[u].z); f[3] = __uint_as_float(vx[u].w);
       }
 #pragma unroll
-      for (int e = 0; e < EPG; ++e) acc[e] = fmaf(p, f[e], acc[e]);
+      for (int qq = 0; qq < GQ; ++qq)
+#pragma unroll
+        for (int e = 0; e < EPG; ++e) acc[qq][e] = fmaf(p[qq][u], f[e], acc[qq][e]);
     }
-    m = mnew;
-  }
-  if (sub == 0) {
-    s_ml[grp][0] = m;
-    s_ml[grp][1] = lsum;
   }
 #pragma unroll
-  for (int e = 0; e < EPG; ++e) s_acc[grp][sub * EPG + e] = acc[e];
+  for (int qq = 0; qq < GQ; ++qq) {
+    if (sub == 0) {
+      s_ml[qq][grp][0] = m[qq];
+      s_ml[qq][grp][1] = lsum[qq];
+    }
+#pragma unroll
+    for (int e = 0; e < EPG; ++e) s_acc[qq][grp][sub * EPG + e] = acc[qq][e];
+  }
   __syncthreads();
-  if (tid < D) {
+  for (int t2 = tid; t2 < GQ * D; t2 += 256) {
+    const int qq = t2 / D, dd = t2 - (t2 / D) * D;
     float M = -1e30f;
-    for (int gi = 0; gi < RPB; ++gi) M = fmaxf(M, s_ml[gi][0]);
+    for (int gi = 0; gi < RPB; ++gi) M = fmaxf(M, s_ml[qq][gi][0]);
     float Ls = 0.f, A = 0.f;
     for (int gi = 0; gi < RPB; ++gi) {
-      const float w = __builtin_amdgcn_exp2f(s_ml[gi][0] - M);
-      Ls = fmaf(s_ml[gi][1], w, Ls);
-      A = fmaf(s_acc[gi][tid], w, A);
+      const float w = __builtin_amdgcn_exp2f(s_ml[qq][gi][0] - M);
+      Ls = fmaf(s_ml[qq][gi][1], w, Ls);
+      A = fmaf(s_acc[qq][gi][dd], w, A);
     }
-    const size_t pi = static_cast<size_t>(bk) * nchunk + chunk;
-    part_acc[pi * D + tid] = A;
-    if (tid == 0) {
+    const size_t pi = (static_cast<size_t>(bk) * GQ + qq) * nchunk + chunk;
+    part_acc[pi * D + dd] = A;
+    if (dd == 0) {
       part_ml[2 * pi] = M;
       part_ml[2 * pi + 1] = Ls;
     }
@@ -277,11 +311,13 @@ __global__ __launch_bounds__(256) void k_decode_attn(
 // w, w + 4, ... (lane c holds chunk c's max and sum; the accumulators are
 // read column-wise, d = lane + 64 i), then the gated head outputs are summed
 // in head order.
+// With key/value groups (G query heads per selected head) the G heads of a
+// slot share its gate and are summed in head order.
 template <int D, bool OUT_BF16>
 __global__ __launch_bounds__(256) void k_decode_combine(
     const float* __restrict__ gates, const int32_t* __restrict__ rows,
     const float* __restrict__ part_acc, const float* __restrict__ part_ml,
-    int K, int nchunk, void* __restrict__ out) {
+    int K, int nchunk, void* __restrict__ out, int G) {
   constexpr int NWV = 4;
   constexpr int DPL = (D + 63) / 64;  // output columns per lane
   __shared__ float s_o[NWV][D];
@@ -290,12 +326,14 @@ __global__ __launch_bounds__(256) void k_decode_combine(
   float o[DPL];
 #pragma unroll
   for (int i = 0; i < DPL; ++i) o[i] = 0.f;
-  for (int kk = wave; kk < K; kk += NWV) {
+  for (int vk = wave; vk < K * G; vk += NWV) {
+    const int kk = vk / G;
     const size_t bk = static_cast<size_t>(b) * K + kk;
+    const size_t bq = bk * G + (vk - kk * G);   // the head's partials
     const int L = rows[bk];
     if (L == 0) continue;
     const int nc = (L + kDecChunk - 1) / kDecChunk;
-    const float* ml = part_ml + bk * nchunk * 2;
+    const float* ml = part_ml + bq * nchunk * 2;
     float M = -1e30f;
     for (int c = lane; c < nc; c += 64) M = fmaxf(M, ml[2 * c]);
 #pragma unroll
@@ -308,7 +346,7 @@ __global__ __launch_bounds__(256) void k_decode_combine(
     float a[DPL];
 #pragma unroll
     for (int i = 0; i < DPL; ++i) a[i] = 0.f;
-    const float* pa = part_acc + bk * nchunk * D;
+    const float* pa = part_acc + bq * nchunk * D;
 #pragma unroll 4
     for (int c = 0; c < nc; ++c) {
       const float w = __builtin_amdgcn_exp2f(ml[2 * c] - M);
@@ -346,21 +384,21 @@ struct DecWs {
   size_t bytes;
 };
 
-static DecWs carve_dec(void* ws, int B, int K, int d, int cap) {
+static DecWs carve_dec(void* ws, int B, int K, int d, int cap, int G = 1) {
   const size_t BK = static_cast<size_t>(B) * K;
   const size_t nc = dec_nchunk(cap);
   Carver cv(ws);
   DecWs w;
-  w.qrot = cv.take<float>(BK * d);
+  w.qrot = cv.take<float>(BK * G * d);
   w.rows = cv.take<int32_t>(BK);
-  w.part_acc = cv.take<float>(BK * nc * d);
-  w.part_ml = cv.take<float>(BK * nc * 2);
+  w.part_acc = cv.take<float>(BK * G * nc * d);
+  w.part_ml = cv.take<float>(BK * G * nc * 2);
   w.bytes = cv.off;
   return w;
 }
 
-size_t decode_workspace_bytes(int B, int /*H*/, int K, int d, int cap) {
-  return carve_dec(nullptr, B, K, d, cap).bytes;
+size_t decode_workspace_bytes(int B, int /*H*/, int K, int d, int cap, int G) {
+  return carve_dec(nullptr, B, K, d, cap, G).bytes;
 }
 
 // ---------------------------------------------------------------------------
@@ -512,7 +550,7 @@ hipError_t launch_prefill_cache(const void* k, const void* v, int dtype, int B, 
 #undef NAMOH_PC
 }
 
-template <int D, bool BF16>
+template <int D, bool BF16, int GQ = 1>
 static hipError_t run_decode(const float* logits, const float* bias, const void* q, const void* k,
                              const void* v, void* k_cache, void* v_cache,
                              int32_t* cache_len, const int32_t* seq_pos, int B,
@@ -521,25 +559,27 @@ static hipError_t run_decode(const float* logits, const float* bias, const void*
                              int32_t* topk_idx, float* gates, void* out,
                              int out_dtype, int32_t* dev_status, void* ws,
                              hipStream_t st) {
-  const DecWs w = carve_dec(ws, B, K, D, cap);
+  const DecWs w = carve_dec(ws, B, K, D, cap, GQ);
   const int nc = dec_nchunk(cap);
   const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
   k_decode_route_append<D, BF16><<<B, 64 * kAppendWaves, 0, st>>>(
       logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, H, K, cap, log_base,
       rope_mode, gate_mode, bias, scale * 1.4426950408889634f, topk_idx, gates,
-      dev_status, w.qrot, w.rows);
+      dev_status, w.qrot, w.rows, GQ);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t grid = static_cast<size_t>(B) * K * nc;
   prof_mark("decode_attn", true, st);
-  k_decode_attn<D, BF16><<<static_cast<unsigned>(grid), 256, 0, st>>>(
+  k_decode_attn<D, BF16, GQ><<<static_cast<unsigned>(grid), 256, 0, st>>>(
       k_cache, v_cache, topk_idx, w.rows, w.qrot, H, K, cap, nc, w.part_acc, w.part_ml);
   prof_mark("decode_attn", false, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (out_dtype == 1)
-    k_decode_combine<D, true><<<B, 256, 0, st>>>(gates, w.rows, w.part_acc, w.part_ml, K, nc, out);
+    k_decode_combine<D, true><<<B, 256, 0, st>>>(gates, w.rows, w.part_acc, w.part_ml, K, nc, out,
+                                                GQ);
   else
-    k_decode_combine<D, false><<<B, 256, 0, st>>>(gates, w.rows, w.part_acc, w.part_ml, K, nc, out);
+    k_decode_combine<D, false><<<B, 256, 0, st>>>(gates, w.rows, w.part_acc, w.part_ml, K, nc,
+                                                 out, GQ);
   return hipGetLastError();
 }
 
@@ -564,6 +604,31 @@ hipError_t launch_decode(const float* logits, const float* bias, const void* q, 
   if (d == 64) NAMOH_DEC(64, false);
   NAMOH_DEC(128, false);
 #undef NAMOH_DEC
+}
+
+hipError_t launch_decode_grouped(const float* logits, const void* q, const void* k, const void* v,
+                                 void* k_cache, void* v_cache, int32_t* cache_len,
+                                 const int32_t* seq_pos, int B, int H, int K, int G, int d, int cap,
+                                 float rope_base, int rope_mode, int gate_mode, float scale,
+                                 int32_t* topk_idx, float* gates, void* out, int out_dtype,
+                                 int32_t* dev_status, void* ws, hipStream_t st) {
+#define NAMOH_DECG(DD, GG)                                                                    \
+  return run_decode<DD, true, GG>(logits, nullptr, q, k, v, k_cache, v_cache, cache_len, seq_pos, \
+                                  B, H, K, cap, rope_base, rope_mode, gate_mode, scale, topk_idx, \
+                                  gates, out, out_dtype, dev_status, ws, st)
+  if (d == 64) {
+    if (G == 1) NAMOH_DECG(64, 1);
+    if (G == 2) NAMOH_DECG(64, 2);
+    if (G == 4) NAMOH_DECG(64, 4);
+    if (G == 8) NAMOH_DECG(64, 8);
+  } else if (d == 128) {
+    if (G == 1) NAMOH_DECG(128, 1);
+    if (G == 2) NAMOH_DECG(128, 2);
+    if (G == 4) NAMOH_DECG(128, 4);
+    if (G == 8) NAMOH_DECG(128, 8);
+  }
+#undef NAMOH_DECG
+  return hipErrorInvalidValue;
 }
 
 }  // namespace namoh

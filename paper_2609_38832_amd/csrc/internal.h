@@ -91,7 +91,7 @@ hipError_t launch_out_proj(const void* head_out, int head_out_dtype, const void*
                            int d_model, void* out, int out_dtype, void* ws, hipStream_t st);
 
 // ---- decode (decode.hip) --------------------------------------------------
-size_t decode_workspace_bytes(int B, int H, int K, int d, int cap);
+size_t decode_workspace_bytes(int B, int H, int K, int d, int cap, int G = 1);
 // bias: NULL for the plain selection, else [H] loss-free balancing biases
 hipError_t launch_decode(const float* logits, const float* bias, const void* q, const void* k,
                          const void* v, int dtype, void* k_cache,
@@ -101,6 +101,13 @@ hipError_t launch_decode(const float* logits, const float* bias, const void* q, 
                          int gate_mode, float scale, int32_t* topk_idx,
                          float* gates, void* out, int out_dtype,
                          int32_t* dev_status, void* ws, hipStream_t st);
+// bf16, d in {64, 128}, G in {1, 2, 4, 8} query heads per key/value head
+hipError_t launch_decode_grouped(const float* logits, const void* q, const void* k, const void* v,
+                                 void* k_cache, void* v_cache, int32_t* cache_len,
+                                 const int32_t* seq_pos, int B, int H, int K, int G, int d, int cap,
+                                 float rope_base, int rope_mode, int gate_mode, float scale,
+                                 int32_t* topk_idx, float* gates, void* out, int out_dtype,
+                                 int32_t* dev_status, void* ws, hipStream_t st);
 hipError_t launch_prefill_cache(const void* k, const void* v, int dtype, int B, int T, int H,
                                 int K, int d, float rope_base, int rope_mode,
                                 const int32_t* seg_offsets, const int32_t* perm_token,

@@ -270,6 +270,20 @@ def test_shared_attn_rejects(lib, kw, code):
     assert _shared(lib, **kw) == code
 
 
+def _gdec(lib, dtype=1, B=2, H=8, K=2, g=4, d=64, cap=100, q=fake(1), wsb=1 << 30):
+    return lib.namoh_decode_step_grouped(fake(0), q, fake(2), fake(3), dtype, fake(4), fake(5),
+                                         fake(6), None, B, H, K, g, d, cap, 1e4, 0, 0, 0.0,
+                                         fake(7), fake(8), fake(9), 0, None, fake(10), wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(g=0), 1), (dict(g=3), 1), (dict(g=16), 1), (dict(dtype=0), 2), (dict(d=32), 2),
+    (dict(cap=0), 1), (dict(q=None), 1), (dict(wsb=4), 3), (dict(K=9), 1),
+])
+def test_decode_step_grouped_rejects(lib, kw, code):
+    assert _gdec(lib, **kw) == code
+
+
 def test_workspace_queries(lib):
     assert lib.namoh_route_workspace_size(0, 10, 8, 2) == 0
     assert lib.namoh_route_workspace_size(1, 10, 8, 2) > 0

@@ -92,3 +92,105 @@ def test_group_of_one_equals_the_routed_attention():
     b = L.attn_fwd_grouped(q, k, v, r, w.K, w.rope_base, out_dtype=torch.float32)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+# ----------------------------------------------------------------------------
+# decode step with key/value groups
+
+def _grouped_decode_inputs(B, Hkv, g, d, cap, seed):
+    wk = W.WORKLOADS[5].with_(B=B, H=Hkv, K=1, d=d, qkv_scale=d ** -0.5, seed=W.BASE_SEED + seed)
+    wq = wk.with_(H=Hkv * g)
+    kc = np.stack([np.stack([W.decode_cache_block(wk, b, h, cap, "k") for h in range(Hkv)])
+                   for b in range(B)])
+    vc = np.stack([np.stack([W.decode_cache_block(wk, b, h, cap, "v") for h in range(Hkv)])
+                   for b in range(B)])
+    step_q = W.decode_step_inputs(wq)["q"]
+    step_kv = W.decode_step_inputs(wk)
+    return wk, step_kv["logits"], step_q, step_kv["k"], step_kv["v"], kc, vc
+
+
+@pytest.mark.parametrize("g,d,rope", [(2, 64, O.ROPE_HEAD_RELATIVE), (4, 128, O.ROPE_GLOBAL),
+                                      (8, 64, O.ROPE_NONE), (8, 128, O.ROPE_HEAD_RELATIVE)])
+def test_grouped_decode_parity(g, d, rope):
+    B, Hkv, Kkv, cap = 3, 6, 2, 1200
+    say(f"grouped decode g={g} d={d} rope={rope}")
+    wk, logits, q, k, v, kc, vc = _grouped_decode_inputs(B, Hkv, g, d, cap, 40 + g + d)
+    r = np.random.default_rng(g * d)
+    lengths = r.integers(0, cap - 1, size=(B, Hkv))
+    lengths[0, 0] = 0
+    seq_pos = r.integers(100, 9000, size=B) if rope == O.ROPE_GLOBAL else None
+    kcd, vcd = to_dev(kc, "bf16"), to_dev(vc, "bf16")
+    cl = torch.from_numpy(lengths.astype(np.int32)).to(DEV)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    sp = None if seq_pos is None else torch.from_numpy(seq_pos.astype(np.int32)).to(DEV)
+    res = L.decode_step_grouped(torch.from_numpy(logits).to(DEV), to_dev(q, "bf16"),
+                                to_dev(k, "bf16"), to_dev(v, "bf16"), kcd, vcd, cl, Kkv,
+                                wk.rope_base, rope, seq_pos=sp, out_dtype=torch.float32,
+                                dev_status=st)
+    torch.cuda.synchronize()
+    kf, vf = W.as_float64(kc, "bf16"), W.as_float64(vc, "bf16")
+    ref = O.decode_step_kv_groups(logits, W.as_float64(q, "bf16"), W.as_float64(k, "bf16"),
+                                  W.as_float64(v, "bf16"), lambda b, j, n: kf[b, j, :n],
+                                  lambda b, j, n: vf[b, j, :n], lengths, Kkv, g, wk.rope_base,
+                                  rope, seq_pos=seq_pos)
+    np.testing.assert_array_equal(res["topk_idx"].cpu().numpy(), ref["topk_idx"])
+    np.testing.assert_array_equal(cl.cpu().numpy(), ref["cache_len"])
+    assert int(st.item()) == 0
+    check_out(from_dev(res["out"]), ref["out"], "bf16", what=f"grouped decode g={g}")
+    vd = from_dev(vcd)
+    for b in range(B):
+        for kk in range(Kkv):
+            j = ref["topk_idx"][b, kk]
+            np.testing.assert_array_equal(vd[b, j, lengths[b, j]], W.as_float64(v, "bf16")[b, j])
+
+
+def test_grouped_decode_of_one_equals_the_decode_step():
+    B, H, K, d, cap = 4, 8, 3, 128, 900
+    say("grouped decode g = 1 against namoh_decode_step")
+    wk, logits, q, k, v, kc, vc = _grouped_decode_inputs(B, H, 1, d, cap, 77)
+    lengths = np.random.default_rng(5).integers(0, cap - 1, size=(B, H)).astype(np.int32)
+    outs = []
+    for fn in (L.decode_step, L.decode_step_grouped):
+        kcd, vcd = to_dev(kc, "bf16"), to_dev(vc, "bf16")
+        cl = torch.from_numpy(lengths).to(DEV)
+        res = fn(torch.from_numpy(logits).to(DEV), to_dev(q, "bf16"), to_dev(k, "bf16"),
+                 to_dev(v, "bf16"), kcd, vcd, cl, K, wk.rope_base, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        outs.append((res["out"].clone(), kcd.clone(), cl.clone()))
+    assert torch.equal(outs[0][0], outs[1][0])
+    assert torch.equal(outs[0][1], outs[1][1])
+    assert torch.equal(outs[0][2], outs[1][2])
+
+
+def test_grouped_prefill_cache_then_grouped_decode():
+    # grouped prompt -> per-group caches (namoh_prefill_cache on the groups) ->
+    # one grouped decode step, against the definition form at token T
+    B, T, Hkv, Kkv, g, d = 2, 500, 4, 2, 4, 64
+    base = 1e4
+    say("grouped prefill, hand-off, grouped decode")
+    wk = W.WORKLOADS[2].with_(B=B, T=T + 1, H=Hkv, K=Kkv, d=d)
+    wq = wk.with_(H=Hkv * g)
+    logits = W.prefill_logits(wk)
+    q, k, v = W.prefill_qkv(wq, "q"), W.prefill_qkv(wk, "k"), W.prefill_qkv(wk, "v")
+    # the prompt: the first T tokens
+    r = L.route(torch.from_numpy(np.ascontiguousarray(logits[:, :T])).to(DEV), Kkv)
+    kp = to_dev(np.ascontiguousarray(k[:, :, :T]), "bf16")
+    vp = to_dev(np.ascontiguousarray(v[:, :, :T]), "bf16")
+    cap = T + 8
+    kc = torch.zeros(B, Hkv, cap, d, dtype=torch.bfloat16, device=DEV)
+    vc = torch.zeros_like(kc)
+    cl = torch.zeros(B, Hkv, dtype=torch.int32, device=DEV)
+    L.prefill_cache(kp, vp, r, Kkv, base, kc, vc, cl)
+    res = L.decode_step_grouped(torch.from_numpy(np.ascontiguousarray(logits[:, T])).to(DEV),
+                                to_dev(np.ascontiguousarray(q[:, :, T]), "bf16"),
+                                to_dev(np.ascontiguousarray(k[:, :, T]), "bf16"),
+                                to_dev(np.ascontiguousarray(v[:, :, T]), "bf16"), kc, vc, cl, Kkv,
+                                base, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    topk = O.select_heads(logits, Kkv)
+    f = [W.as_float64(x, "bf16") for x in (q, k, v)]
+    h = O.attention_kv_groups(f[0], f[1], f[2], topk, g, base, O.ROPE_HEAD_RELATIVE,
+                              form="definition")
+    gates = O.route_gates(logits, topk, O.GATE_SOFTMAX_SELECTED)
+    o_ref = O.combine_kv_groups(h, topk, gates, g)[:, T]
+    check_out(from_dev(res["out"]), o_ref, "bf16", what="grouped hand-off + decode")
