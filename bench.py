@@ -221,7 +221,7 @@ def bench_layer(w, args, torch, L, DI):
     qkv = {n: torch.empty(B, H, T, d, dtype=torch.bfloat16, device=dev) for n in ("q", "k", "v")}
     aws = L.workspace(L.attn_workspace_size(B, T, H, K, d, L.BF16), dev)
     ho = torch.empty(B * T * K, d, dtype=torch.float32, device=dev)
-    ows = L.workspace(L.out_proj_workspace_size(B, T, H, K, dm), dev)
+    ows = L.workspace(L.out_proj_workspace_size(B, T, H, K, w.d, dm), dev)
     out = torch.empty(B, T, dm, dtype=torch.bfloat16, device=dev)
 
     def step():
@@ -279,8 +279,14 @@ def bench_layer(w, args, torch, L, DI):
            "work": {"qkv_flops": f_qkv, "attn_flops": f_attn, "out_flops": f_out,
                     "out_rows_bytes": 2.0 * Nr * dm * 2},
            "kernels_ms": {k2: round(v2, 4) for k2, v2 in kern.items()}}
+    # the library's output-projection form (dense over all heads when H d <= 384 K)
+    dense = H * d <= 384 * K and H <= 64
+    res["out_proj_form"] = "dense" if dense else "per-pair"
     if "out_proj" in kern:
         res["out_proj_gemm_tflops"] = round(f_out / (kern["out_proj"] * 1e-3) / 1e12, 1)
+        if dense:
+            f_exec = 2.0 * B * T * H * d * dm
+            res["out_proj_executed_tflops"] = round(f_exec / (kern["out_proj"] * 1e-3) / 1e12, 1)
     return res
 
 

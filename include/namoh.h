@@ -305,8 +305,15 @@ namoh_status namoh_shared_attn(const void* q, const void* k, const void* v, int 
  *   w_o   [H, d_model, d]: h_{t,i} W_O^(i) = h_{t,i} w_o[i]^T.
  * Supported: bf16 x and weights, d_head in {64, 128}, d_model a multiple
  * of 128 (else NAMOH_ERR_UNSUPPORTED).  fp32 accumulation on the matrix
- * cores; results rounded to bf16 (the output projection's per-pair rows are
- * rounded to bf16 before the fp32 gated sum).
+ * cores; q/k/v rounded to bf16.  The output projection takes one of two
+ * forms, chosen from H, K and d (the dense form when H * d <= 384 * K and
+ * H <= 64):
+ *   per-pair: every routed pair's row h W_O^(i) is formed (rounded to bf16)
+ *     and the K rows of a token are summed with their gates in k order;
+ *   dense:    each token's gated head rows g h (rounded to bf16) enter one
+ *     product with the stacked W_O over all H heads (unselected heads
+ *     contribute exact zeros) and are summed in head order in fp32: H/K
+ *     times the multiply-adds, no per-pair rows.
  * ---------------------------------------------------------------------- */
 
 /* In:  x [B, T, d_model] bf16; w_qkv as above; seg_offsets, perm_token from
@@ -319,16 +326,18 @@ namoh_status namoh_qkv_proj(const void* x, const void* w_qkv, int B, int T, int 
                             const int32_t* perm_token, void* q, void* k, void* v,
                             void* stream);
 
-size_t namoh_out_proj_workspace_size(int B, int T, int H, int K, int d_model);
+size_t namoh_out_proj_workspace_size(int B, int T, int H, int K, int d_head, int d_model);
 
 /* In:  head_out [B*T*K, d] packed ungated head outputs (as namoh_attn_fwd
  *      writes them to its head_out argument), float32 (head_out_dtype
  *      NAMOH_F32) or bf16; w_o as above; gates, slot_pos, seg_offsets from
  *      namoh_route.
- * Out: out [B, T, d_model] of out_dtype: o_t = sum over k in ascending order
- *      of gates[b,t,k] * (h W_O^(topk_idx[b,t,k])) at the pair's packed row.
- * Workspace: namoh_out_proj_workspace_size bytes (the per-pair projected rows,
- *      bf16 [B*T*K, d_model]). */
+ * Out: out [B, T, d_model] of out_dtype: o_t = sum over the token's k of
+ *      gates[b,t,k] * (h W_O^(topk_idx[b,t,k])) at the pair's packed row
+ *      (the head of a packed row is that of its segment).
+ * Workspace: namoh_out_proj_workspace_size bytes: per-pair form, the
+ *      projected rows (bf16 [B*T*K, d_model]); dense form, the per-token head
+ *      map (int32 pairs [B*T, H]). */
 namoh_status namoh_out_proj(const void* head_out, int head_out_dtype, const void* w_o,
                             const float* gates, const int32_t* slot_pos,
                             const int32_t* seg_offsets, int B, int T, int H, int K, int d_head,

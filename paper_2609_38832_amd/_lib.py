@@ -74,7 +74,7 @@ _SIGS = {
     "namoh_decode_step_grouped": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I,
                                        _I, _F, _I, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
     "namoh_qkv_proj": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P]),
-    "namoh_out_proj_workspace_size": (_S, [_I, _I, _I, _I, _I]),
+    "namoh_out_proj_workspace_size": (_S, [_I, _I, _I, _I, _I, _I]),
     "namoh_out_proj": (_I, [_P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _P, _S, _P]),
     "namoh_status_string": (ctypes.c_char_p, [_I]),
     "namoh_last_error": (ctypes.c_char_p, []),
@@ -433,8 +433,8 @@ def qkv_proj(x: torch.Tensor, w_qkv: torch.Tensor, routing: dict, H: int, K: int
     return out
 
 
-def out_proj_workspace_size(B, T, H, K, d_model) -> int:
-    return int(lib().namoh_out_proj_workspace_size(B, T, H, K, d_model))
+def out_proj_workspace_size(B, T, H, K, d, d_model) -> int:
+    return int(lib().namoh_out_proj_workspace_size(B, T, H, K, d, d_model))
 
 
 def out_proj(head_out: torch.Tensor, w_o: torch.Tensor, routing: dict, B: int, T: int, H: int,
@@ -452,7 +452,7 @@ def out_proj(head_out: torch.Tensor, w_o: torch.Tensor, routing: dict, B: int, T
     if out is None:
         out = torch.empty(B, T, dm, dtype=out_dtype, device=w_o.device)
     if ws is None:
-        ws = workspace(out_proj_workspace_size(B, T, H, K, dm), w_o.device)
+        ws = workspace(out_proj_workspace_size(B, T, H, K, d, dm), w_o.device)
     check(lib().namoh_out_proj(_ptr(head_out), dtype_code(head_out.dtype), _ptr(w_o),
                                _ptr(routing["gates"]), _ptr(routing["slot_pos"]),
                                _ptr(routing["seg_offsets"]), B, T, H, K, d, dm, _ptr(out),

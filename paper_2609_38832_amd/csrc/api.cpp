@@ -392,9 +392,9 @@ namoh_status namoh_qkv_proj(const void* x, const void* w_qkv, int B, int T, int 
                                            perm_token, q, k, v, static_cast<hipStream_t>(stream)));
 }
 
-size_t namoh_out_proj_workspace_size(int B, int T, int H, int K, int d_model) {
-  if (check_proj(B, T, H, K, 64, d_model) != NAMOH_OK) return 0;
-  return namoh::out_proj_workspace_bytes(B, T, K, d_model);
+size_t namoh_out_proj_workspace_size(int B, int T, int H, int K, int d_head, int d_model) {
+  if (check_proj(B, T, H, K, d_head, d_model) != NAMOH_OK) return 0;
+  return namoh::out_proj_workspace_bytes(B, T, H, K, d_head, d_model);
 }
 
 namoh_status namoh_out_proj(const void* head_out, int head_out_dtype, const void* w_o,
@@ -414,7 +414,7 @@ namoh_status namoh_out_proj(const void* head_out, int head_out_dtype, const void
   REQUIRE_PTR(seg_offsets, 4);
   REQUIRE_PTR(out, 16);
   if ((s = check_workspace(workspace, workspace_bytes,
-                           namoh::out_proj_workspace_bytes(B, T, K, d_model))) != NAMOH_OK)
+                           namoh::out_proj_workspace_bytes(B, T, H, K, d_head, d_model))) != NAMOH_OK)
     return s;
   clear_hip_error();
   return hip_status(namoh::launch_out_proj(head_out, head_out_dtype, w_o, gates, slot_pos,

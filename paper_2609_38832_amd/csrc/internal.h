@@ -84,7 +84,8 @@ hipError_t launch_combine_rows(const uint16_t* rows, const float* gates, const i
 hipError_t launch_qkv_proj(const void* x, const void* w_qkv, int B, int T, int H, int K, int d,
                            int d_model, const int32_t* seg_offsets, const int32_t* perm_token,
                            void* q, void* k, void* v, hipStream_t st);
-size_t out_proj_workspace_bytes(int B, int T, int K, int d_model);
+size_t out_proj_workspace_bytes(int B, int T, int H, int K, int d, int d_model);
+bool out_proj_dense(int H, int K, int d);
 hipError_t launch_out_proj(const void* head_out, int head_out_dtype, const void* w_o,
                            const float* gates, const int32_t* slot_pos,
                            const int32_t* seg_offsets, int B, int T, int H, int K, int d,

@@ -227,8 +227,14 @@ def test_out_proj_rejects(lib, kw, code):
 
 
 def test_out_proj_workspace_size(lib):
-    assert lib.namoh_out_proj_workspace_size(4, 4096, 32, 8, 2048) >= 4 * 4096 * 8 * 2048 * 2
-    assert lib.namoh_out_proj_workspace_size(4, 4096, 32, 8, 100) == 0
+    # dense form (H d <= 384 K): the per-token head map and the gated bf16 rows
+    assert lib.namoh_out_proj_workspace_size(4, 4096, 32, 8, 64, 2048) >= \
+        4 * 4096 * 32 * 4 + 4 * 4096 * 8 * 64 * 2
+    assert lib.namoh_out_proj_workspace_size(4, 4096, 32, 8, 64, 2048) < 4 * 4096 * 8 * 2048 * 2
+    # per-pair form: the bf16 per-pair rows
+    assert lib.namoh_out_proj_workspace_size(4, 4096, 64, 8, 128, 2048) >= 4 * 4096 * 8 * 2048 * 2
+    assert lib.namoh_out_proj_workspace_size(4, 4096, 32, 8, 64, 100) == 0
+    assert lib.namoh_out_proj_workspace_size(4, 4096, 32, 8, 96, 2048) == 0
 
 
 def _grp(lib, dtype=1, B=2, T=64, H=8, K=2, g=2, d=64, base=1e4, rope=0, q=fake(0), out=fake(7),

@@ -36,7 +36,15 @@ CASES = {
     "d128_dm384_ragged": dict(B=1, T=257, H=5, K=3, d=128, d_model=384),
     "all_heads": dict(B=2, T=200, H=4, K=4, d=64, d_model=128),
     "one_head": dict(B=1, T=130, H=1, K=1, d=64, d_model=128),
+    # H d > 384 K: the per-pair form of the output projection
+    "pairs_d64_h16_k2": dict(B=2, T=200, H=16, K=2, d=64, d_model=256),
+    "pairs_d128_h8_k2_ragged": dict(B=1, T=333, H=8, K=2, d=128, d_model=384),
 }
+
+
+def _dense_form(w):
+    # the library's choice between the dense and the per-pair output projection
+    return w.H * w.d <= 384 * w.K and w.H <= 64
 
 
 def _case(name):
@@ -85,11 +93,17 @@ def _packed_to_dense(hp, topk, H, T, d):
     return h
 
 
-@pytest.mark.parametrize("name", ["d64_dm256", "d128_dm384_ragged", "all_heads"])
+@pytest.mark.parametrize("name", ["d64_dm256", "d128_dm384_ragged", "all_heads", "one_head",
+                                  "pairs_d64_h16_k2", "pairs_d128_h8_k2_ragged"])
 @pytest.mark.parametrize("hdt,odt", [("f32", torch.float32), ("bf16", torch.bfloat16)])
 def test_out_proj_parity(name, hdt, odt):
     w = _case(name)
-    say(f"output projection {name} head_out={hdt} out={odt}")
+    form = "dense" if _dense_form(w) else "per-pair"
+    say(f"output projection {name} ({form} form) head_out={hdt} out={odt}")
+    ws_bytes = L.out_proj_workspace_size(w.B, w.T, w.H, w.K, w.d, w.d_model)
+    need = (w.B * w.T * w.H * 4 + w.B * w.T * w.K * w.d * 2 if form == "dense"
+            else w.B * w.T * w.K * w.d_model * 2)
+    assert need <= ws_bytes < need + 4096
     inp = W.projection_inputs(w)
     r, topk = _route(inp, w)
     Nr = w.B * w.T * w.K
