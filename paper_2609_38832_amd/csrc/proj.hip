@@ -322,32 +322,43 @@ __global__ __launch_bounds__(256) void k_out_map(
 //     H * d (chunk c is head c / (d / 64)); the rows are the tokens' gated
 //     head rows G found through the head map (zero for unselected heads).
 constexpr int kBigRows = 256;
+constexpr int kQkvRows = 256;   // Q/K/V tiles (128: two workgroups per CU, measured no faster)
+constexpr int kXcds = 8;        // XCDs of the device; workgroup i runs on XCD i % 8
 
-NAMOH_DEV int seg_btile0(int seg0, int s) { return seg0 / kBigRows + s; }
+template <int TM>
+NAMOH_DEV int seg_btile0(int seg0, int s) { return seg0 / TM + s; }
 
-template <int TN, int HM>
+template <int TM, int TN, int HM>
 struct BigLds {
-  uint16_t x[2][kBigRows * kProjKC];
+  uint16_t x[2][TM * kProjKC];
   uint16_t w[2][TN * kProjKC];
-  int32_t map[kBigRows * HM];   // OUT: the tile's head map (HM >= H); 160 KB in all at most
+  int32_t map[TM * HM];   // OUT: the tile's head map (HM >= H); 160 KB in all at most
+};
+template <int TM, int TN>
+struct BigLds<TM, TN, 0> {   // Q/K/V: no map (two 128-row workgroups fit one CU)
+  uint16_t x[2][TM * kProjKC];
+  uint16_t w[2][TN * kProjKC];
 };
 
 // Largest head count whose map tile fits beside the stages of a TN-wide tile.
 constexpr int big_map_heads(int TN) { return TN == 256 ? 32 : 64; }
 
-template <int MODE, int TN, bool OUT_BF16>
-__global__ __launch_bounds__(kProjThreads, 1) void k_proj_big(
+template <int MODE, int TM, int TN, bool OUT_BF16>
+__global__ __launch_bounds__(kProjThreads, TM == 128 ? 2 : 1) void k_proj_big(
     const uint16_t* __restrict__ src, const uint16_t* __restrict__ w,
     const int32_t* __restrict__ seg_offsets, const int32_t* __restrict__ perm_token,
     const int32_t* __restrict__ map, int BH, int H, int T, long BT, int Nr, int kdim, int N, int d,
-    int n_col_tiles, void* __restrict__ dst0, void* __restrict__ dst1, void* __restrict__ dst2) {
+    int n_col_tiles, int classes, void* __restrict__ dst0, void* __restrict__ dst1,
+    void* __restrict__ dst2) {
   constexpr int CT = TN / 64;                                  // 32-column tiles per wave
-  constexpr int XG = kBigRows * kProjKC / 8 / kProjThreads;    // data granules per thread (8)
+  constexpr int RT = TM / 64;                                   // 32-row tiles per wave
+  constexpr int XG = TM * kProjKC / 8 / kProjThreads;          // data granules per thread
   constexpr int WG = TN * kProjKC / 8 / kProjThreads;          // weight granules per thread
-  static_assert(TN % 64 == 0 && XG == 8 && WG * kProjThreads * 8 == TN * kProjKC, "tile shape");
-  constexpr int HM = MODE == kProjOut ? big_map_heads(TN) : 1;
-  __shared__ __attribute__((aligned(16))) BigLds<TN, HM> L;
-  static_assert(sizeof(BigLds<TN, HM>) <= 160 * 1024, "LDS");
+  static_assert((TM == 128 || TM == 256) && TN % 64 == 0 && WG * kProjThreads * 8 == TN * kProjKC,
+                "tile shape");
+  constexpr int HM = MODE == kProjOut ? big_map_heads(TN) : 0;
+  __shared__ __attribute__((aligned(16))) BigLds<TM, TN, HM> L;
+  static_assert(sizeof(BigLds<TM, TN, HM>) <= 160 * 1024, "LDS");
   const int tid = thread_x();
   const int lane = tid % kWave, wave = tid / kWave;
   const int c = lane & 31, g = lane >> 5;
@@ -355,7 +366,7 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_big(
   const int gr = tid % 8;   // the thread's 16-byte granule of a 64-wide chunk
   const int bid = block_x();
   const int rt0 = bid / n_col_tiles;
-  const int n0 = (bid - rt0 * n_col_tiles) * TN;
+  int n0 = (bid - rt0 * n_col_tiles) * TN;
 
   // ---- the tile's data rows -------------------------------------------------
   int hh = 0, b = 0, seg0 = 0, nrow;
@@ -368,31 +379,71 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_big(
       for (int i = tid; i <= BH; i += kProjThreads) off[i] = seg_offsets[i];
     __syncthreads();
     const int32_t* so = in_lds ? off : seg_offsets;
-    int s;
-    if (in_lds) {
+    int s, r0;
+    if (classes > 1) {
+      // XCD classes: workgroup bid runs on XCD bid % classes (dispatch is
+      // round-robin over the XCDs) and takes the tiles of the heads h with
+      // h % classes == bid % classes, so each XCD's L2 holds the weights of
+      // its H / classes heads.  Class members (h, b) in order; tile j of the
+      // class is found by a wave-wide scan of per-lane tile counts.
+      const int x = bid % classes, i = bid / classes;
+      n0 = (i % n_col_tiles) * TN;
+      const int j = i / n_col_tiles;
+      const int nb = BH / H;
+      const int hc = x < H ? (H - x + classes - 1) / classes : 0;
+      const int M = nb * hc;
+      const int per = (M + kWave - 1) / kWave;
+      const int m0 = min(M, lane * per), m1 = min(M, m0 + per);
+      auto member = [&](int m) { return (m % nb) * H + x + classes * (m / nb); };
+      int cnt = 0;
+      for (int m = m0; m < m1; ++m) {
+        const int sm = member(m);
+        cnt += (max(0, so[sm + 1] - so[sm]) + TM - 1) / TM;
+      }
+      const int incl = wave_inclusive_scan(cnt);
+      const uint64_t bal = __ballot(j >= incl - cnt && j < incl);
+      int fs = -1, fr = 0;
+      if (bal != 0 && lane == __ffsll(static_cast<unsigned long long>(bal)) - 1) {
+        int acc = incl - cnt;
+        for (int m = m0; m < m1; ++m) {
+          const int sm = member(m);
+          const int tcount = (max(0, so[sm + 1] - so[sm]) + TM - 1) / TM;
+          if (j < acc + tcount) {
+            fs = sm;
+            fr = (j - acc) * TM;
+            break;
+          }
+          acc += tcount;
+        }
+      }
+      const int src_lane = bal != 0 ? __ffsll(static_cast<unsigned long long>(bal)) - 1 : 0;
+      s = __shfl(fs, src_lane);
+      r0 = __shfl(fr, src_lane);
+    } else if (in_lds) {
       int cnt = 0;
       for (int s0 = 0; s0 < BH; s0 += kWave) {
         const int si = s0 + lane;
-        cnt += __popcll(__ballot(si < BH && seg_btile0(so[si], si) <= rt0));
+        cnt += __popcll(__ballot(si < BH && seg_btile0<TM>(so[si], si) <= rt0));
       }
       s = cnt - 1;
+      r0 = (rt0 - seg_btile0<TM>(so[s], s)) * TM;
     } else {
       int lo = 0, hi = BH;
       while (hi - lo > 1) {
         const int mid = (lo + hi) >> 1;
-        if (seg_btile0(so[mid], mid) <= rt0) lo = mid; else hi = mid;
+        if (seg_btile0<TM>(so[mid], mid) <= rt0) lo = mid; else hi = mid;
       }
       s = lo;
+      r0 = (rt0 - seg_btile0<TM>(so[s], s)) * TM;
     }
-    seg0 = so[s];
-    const int n = so[s + 1] - seg0;
-    const int r0 = (rt0 - seg_btile0(seg0, s)) * kBigRows;
+    const int n = s >= 0 ? so[s + 1] - so[s] : 0;
+    seg0 = s >= 0 ? so[s] : 0;
     __syncthreads();   // the staged offsets are read; the ring may be written
-    if (r0 < 0 || r0 >= n || seg0 < 0 || n > T || seg0 + n > Nr) return;
+    if (s < 0 || r0 < 0 || r0 >= n || seg0 < 0 || n > T || seg0 + n > Nr) return;
     b = s / H;
     hh = s - (s / H) * H;
     seg0 += r0;
-    nrow = min(kBigRows, n - r0);
+    nrow = min(TM, n - r0);
     // padding rows past the tile's end load the last row (their results are
     // never stored), so that no load needs a branch
 #pragma unroll
@@ -404,11 +455,13 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_big(
   } else {
     // the tile's head map into LDS (rows past the end repeat the last row;
     // their results are never stored)
-    t0 = static_cast<long>(rt0) * kBigRows;
-    nrow = static_cast<int>(min(static_cast<long>(kBigRows), BT - t0));
-    for (int i = tid; i < kBigRows * H; i += kProjThreads) {
-      const int r = min(i / H, nrow - 1);
-      const int32_t m = map[(static_cast<size_t>(t0) + r) * H + (i - (i / H) * H)];
+    t0 = static_cast<long>(rt0) * TM;
+    nrow = static_cast<int>(min(static_cast<long>(TM), BT - t0));
+    // stored head-major ([h][row]): the 8 rows a wave reads for one head are
+    // consecutive words, free of bank conflicts
+    for (int i = tid; i < TM * H; i += kProjThreads) {
+      const int row = i % TM, h = i / TM;
+      const int32_t m = map[(static_cast<size_t>(t0) + min(row, nrow - 1)) * H + h];
       L.map[i] = static_cast<unsigned>(m) <= static_cast<unsigned>(Nr) ? m : Nr;
     }
     __syncthreads();
@@ -417,7 +470,11 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_big(
   const int nchunk = MODE == kProjQKV ? kdim / kProjKC : H * cph;
   const int last = nchunk - 1;
 
-  u32x4 xs0[XG], xs1[XG], wv[WG];
+  // two register sets for the weight rows too where the registers allow
+  // (QKV; OUT with TN = 128): their loads are then also issued three chunks
+  // ahead instead of two
+  constexpr bool W2 = (MODE == kProjQKV && TM == 256) || (MODE == kProjOut && TN <= 128);
+  u32x4 xs0[XG], xs1[XG], wv0[WG], wv1[W2 ? WG : 1];
   auto load_x = [&](u32x4 (&xs)[XG], int ch) {
 #pragma unroll
     for (int e = 0; e < XG; ++e) {
@@ -425,12 +482,12 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_big(
         xs[e] = *reinterpret_cast<const u32x4*>(src + xrow[e] + ch * kProjKC + 8 * gr);
       } else {   // the gated row of the token's head (the zero row Nr if unselected)
         const int h = ch / cph, dd0 = (ch - h * cph) * kProjKC;
-        const int m = L.map[(tid / 8 + 32 * e) * H + h];
+        const int m = L.map[h * TM + tid / 8 + 32 * e];
         xs[e] = *reinterpret_cast<const u32x4*>(src + static_cast<size_t>(m) * d + dd0 + 8 * gr);
       }
     }
   };
-  auto load_w = [&](int ch) {
+  auto load_w = [&](u32x4 (&wv)[WG], int ch) {
     const uint16_t* wb;
     size_t stride;
     if constexpr (MODE == kProjQKV) {
@@ -445,7 +502,7 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_big(
     for (int e = 0; e < WG; ++e)
       wv[e] = *reinterpret_cast<const u32x4*>(wb + static_cast<size_t>(tid / 8 + 32 * e) * stride + 8 * gr);
   };
-  auto store = [&](const u32x4 (&xs)[XG], int stg) {
+  auto store = [&](const u32x4 (&xs)[XG], const u32x4 (&wv)[WG], int stg) {
 #pragma unroll
     for (int e = 0; e < XG; ++e) {
       const int row = tid / 8 + 32 * e;
@@ -458,22 +515,22 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_big(
     }
   };
 
-  f32x16 C[CT][4];
+  f32x16 C[CT][RT];
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) C[ct][rt][e] = 0.f;
 
   auto compute = [&](int stg) {
     // operand fragments in two register sets: the reads of step ks + 1 are
     // issued before the MFMAs of step ks (scheduling barriers keep them there)
-    bf16x8 bx[2][4], aw[2][CT];
+    bf16x8 bx[2][RT], aw[2][CT];
     auto read_frags = [&](int ks, int set) {
 #pragma unroll
-      for (int rt = 0; rt < 4; ++rt) {
-        const int drow = 128 * wr + 32 * rt + c;
+      for (int rt = 0; rt < RT; ++rt) {
+        const int drow = (TM / 2) * wr + 32 * rt + c;
         bx[set][rt] =
             *reinterpret_cast<const bf16x8*>(&L.x[stg][drow * kProjKC + swz<8>(drow, 2 * ks + g) * 8]);
       }
@@ -492,7 +549,7 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_big(
 #pragma unroll
       for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt)
+        for (int rt = 0; rt < RT; ++rt)
           C[ct][rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aw[ks & 1][ct], bx[ks & 1][rt],
                                                               C[ct][rt], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
@@ -506,34 +563,38 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_big(
   // in order, so it would also wait for every load issued before); indices
   // past the end are clamped to the last chunk and land in the stage that is
   // no longer read.
-  auto step = [&](int ch, u32x4 (&xn)[XG], int stg) {
-    store(xn, stg ^ 1);
-    load_w(min(ch + 2, last));
+  auto step = [&](int ch, u32x4 (&xn)[XG], u32x4 (&wn)[WG], int stg) {
+    store(xn, wn, stg ^ 1);
+    load_w(wn, min(ch + (W2 ? 3 : 2), last));
     load_x(xn, min(ch + 3, last));
     __builtin_amdgcn_sched_barrier(0);
     compute(stg);
     __syncthreads();
   };
 
+  auto& wv1s = [&]() -> u32x4(&)[WG] {
+    if constexpr (W2) return wv1; else return wv0;
+  }();
   load_x(xs0, 0);
-  load_w(0);
-  store(xs0, 0);
+  load_w(wv0, 0);
+  store(xs0, wv0, 0);
   load_x(xs1, min(1, last));
-  load_w(min(1, last));
+  load_w(wv1s, min(1, last));
   load_x(xs0, min(2, last));
+  if constexpr (W2) load_w(wv0, min(2, last));
   __syncthreads();
   int ch = 0;
   for (; ch + 1 < nchunk; ch += 2) {
-    step(ch, xs1, 0);
-    step(ch + 1, xs0, 1);
+    step(ch, xs1, wv1s, 0);
+    step(ch + 1, xs0, wv0, 1);
   }
-  if (ch < nchunk) step(ch, xs1, 0);
+  if (ch < nchunk) step(ch, xs1, wv1s, 0);
 
   // ---- epilogue: lane (c, g) holds data row 128 wr + 32 rt + c, output
   // columns n0 + TN/2 wc + 32 ct + 8 j + 4 g + i in accumulator 4 j + i ----
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt) {
-    const int r = 128 * wr + 32 * rt + c;
+  for (int rt = 0; rt < RT; ++rt) {
+    const int r = (TM / 2) * wr + 32 * rt + c;
     if (r >= nrow) continue;
     size_t orow;
     if constexpr (MODE == kProjQKV) {
@@ -577,11 +638,11 @@ static void launch_out_big(const uint16_t* grows, const uint16_t* w_o, const int
   const int nct = d_model / TN;
   const unsigned grid = static_cast<unsigned>(((BT + kBigRows - 1) / kBigRows) * nct);
   if (out_bf16)
-    k_proj_big<kProjOut, TN, true><<<grid, kProjThreads, 0, st>>>(
-        grows, w_o, nullptr, nullptr, map, 0, H, 0, BT, Nr, d, d_model, d, nct, out, nullptr, nullptr);
+    k_proj_big<kProjOut, kBigRows, TN, true><<<grid, kProjThreads, 0, st>>>(
+        grows, w_o, nullptr, nullptr, map, 0, H, 0, BT, Nr, d, d_model, d, nct, 1, out, nullptr, nullptr);
   else
-    k_proj_big<kProjOut, TN, false><<<grid, kProjThreads, 0, st>>>(
-        grows, w_o, nullptr, nullptr, map, 0, H, 0, BT, Nr, d, d_model, d, nct, out, nullptr, nullptr);
+    k_proj_big<kProjOut, kBigRows, TN, false><<<grid, kProjThreads, 0, st>>>(
+        grows, w_o, nullptr, nullptr, map, 0, H, 0, BT, Nr, d, d_model, d, nct, 1, out, nullptr, nullptr);
 }
 
 // ---------------------------------------------------------------------------
@@ -597,13 +658,24 @@ hipError_t launch_qkv_proj(const void* x, const void* w_qkv, int B, int T, int H
   if (N % 192 != 0 || d_model % kProjKC != 0) return hipErrorInvalidValue;
   const size_t Nr = static_cast<size_t>(B) * T * K;
   const int nct = N / 192;
-  const unsigned grid =
-      static_cast<unsigned>((Nr / kBigRows + static_cast<size_t>(B) * H + 1) * nct);
+  constexpr int TM = kQkvRows;
+  // XCD classes (heads h % 8 on XCD h % 8) when the offsets fit in LDS; the
+  // grid then holds, per class, the most tiles a class can have (B T
+  // min(K, H/8) / TM + B H/8 + 1); the rest of its workgroups find no tile
+  const int classes = B * H <= kProjSegLds && H >= kXcds ? kXcds : 1;
+  size_t tiles;
+  if (classes > 1) {
+    const size_t hc = (H + classes - 1) / classes;
+    tiles = classes * (static_cast<size_t>(B) * T * std::min<size_t>(K, hc) / TM + B * hc + 1);
+  } else {
+    tiles = Nr / TM + static_cast<size_t>(B) * H + 1;
+  }
+  const unsigned grid = static_cast<unsigned>(tiles * nct);
   prof_mark("qkv_proj", true, st);
-  k_proj_big<kProjQKV, 192, false><<<grid, kProjThreads, 0, st>>>(
+  k_proj_big<kProjQKV, TM, 192, false><<<grid, kProjThreads, 0, st>>>(
       static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_qkv), seg_offsets,
       perm_token, nullptr, B * H, H, T,
-      static_cast<long>(B) * T, B * T * K, d_model, N, d, nct, q, k, v);
+      static_cast<long>(B) * T, B * T * K, d_model, N, d, nct, classes, q, k, v);
   prof_mark("qkv_proj", false, st);
   return hipGetLastError();
 }
