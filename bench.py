@@ -270,7 +270,7 @@ def bench_layer(w, args, torch, L, DI):
            "config": {"workload": w.name, "B": B, "T": T, "H": H, "K": K, "d_head": d,
                       "d_model": dm, "rope": "head-relative", "rope_base": w.rope_base,
                       "gates": "softmax over selected"},
-           "roofline": {"kernel": "k_proj_gemm<QKV>", "bound": "mfma",
+           "roofline": {"kernel": "k_proj_big<QKV>", "bound": "mfma",
                         "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                         "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                         "traffic": None,

@@ -5,25 +5,24 @@
 // (batch b, head i) segment the packed rows r < n_{b,i} are the tokens of the
 // ordered index set I_i, and only those pairs are projected.
 //
-//   k_proj_gemm<QKV>  [q|k|v]_{t,i} = x_t W_QKV[i]^T for the segment's rows:
+//   k_proj_big<QKV>   [q|k|v]_{t,i} = x_t W_QKV[i]^T for the segment's rows:
 //                     a grouped GEMM (M = n_{b,i}, N = 3d, K = d_model) whose
 //                     data rows are gathered by token; the 4-column runs of
 //                     each result row go straight to the dense q, k, v rows
 //                     of the pair (other rows are never written).
-//   k_proj_gemm<OUT>  Y_r = h_r W_O[i]^T for every packed head-output row r
-//                     of the segment (M = n_{b,i}, N = d_model, K = d), bf16
-//                     rows in packed order; k_combine then forms
-//                     o_t = sum_k g_{t,k} Y[slot_pos(t,k)] in k order.
+//   k_out_map +       dense output projection (H d <= 384 K): the tokens'
+//   k_proj_big<OUT>   gated head rows against the stacked W_O over all heads.
+//   k_proj_gemm +     per-pair output projection (otherwise): Y_r = h_r
+//   k_combine         W_O[i]^T for every packed head-output row r (bf16 rows
+//                     in packed order), then o_t = sum_k g_{t,k}
+//                     Y[slot_pos(t,k)] in k order.
 //
-// One workgroup computes 128 rows x NT columns of one segment with four
-// waves of 32 rows.  The product is formed transposed, C^T = W X^T, on
+// The products are formed transposed, C^T = W X^T, on
 // v_mfma_f32_32x32x16_bf16 (weights as the A operand, data rows as the B
 // operand; operand order in tile.h), so each lane holds 16 output columns of
 // one data row, as four runs of 4 consecutive columns.  K is walked in
-// chunks of 64: the next chunk is loaded into registers while the current
-// one is multiplied from LDS (one LDS stage, rows of 128 bytes with the
-// 64-bank granule swizzle).  fp32 accumulation; operands bf16 (fp32 head
-// outputs are rounded to bf16 as they are staged).
+// chunks of 64 staged through LDS (rows of 128 bytes with the 64-bank
+// granule swizzle).  fp32 accumulation; operands bf16.
 #include "common.h"
 #include "internal.h"
 #include "tile.h"
@@ -85,11 +84,12 @@ NAMOH_DEV void proj_load(u32x4 (&xr)[XG], u32x4 (&wr)[WG], const void* __restric
   }
 }
 
-// MODE kProjQKV: src = x [B, T, d_model] bf16, w = W_QKV [H, 3d, d_model] bf16,
-//   kdim = d_model, N = 3d; outputs q, k, v [B, H, T, d] bf16 (dst0/1/2).
-// MODE kProjOut: src = packed head outputs [Nr, d] (f32 if SRC_F32, else
-//   bf16), w = W_O [H, d_model, d] bf16, kdim = d, N = d_model; output Y
-//   [Nr, d_model] bf16 (dst0).
+// Per-pair output projection: one workgroup computes 128 packed rows x NT
+// columns of one segment with four waves of 32 rows; the next chunk is loaded
+// into registers while the current one is multiplied from LDS.  src = packed
+// head outputs [Nr, d] (f32 if SRC_F32, else bf16; rounded to bf16 as they
+// are staged), w = W_O [H, d_model, d] bf16, kdim = d, N = d_model; output Y
+// [Nr, d_model] bf16 (dst0).
 template <int MODE, int NT, bool SRC_F32>
 __global__ __launch_bounds__(kProjThreads, 2) void k_proj_gemm(
     const void* __restrict__ src, const uint16_t* __restrict__ w,
@@ -134,7 +134,7 @@ __global__ __launch_bounds__(kProjThreads, 2) void k_proj_gemm(
   const int r0 = (gt - seg_ptile0(seg0, s)) * kProjRows;
   // a tile in a gap between segments, or offsets that are not a packing
   if (r0 < 0 || r0 >= n || seg0 < 0 || n > T || seg0 + n > Nr) return;
-  const int b = s / H, hh = s - (s / H) * H;
+  const int hh = s - (s / H) * H;
 
   // ---- the thread's data rows and weight rows -----------------------------
   // data granule u = tid + 256 e: row u / 8, 16-byte granule u % 8 of the
@@ -144,14 +144,7 @@ __global__ __launch_bounds__(kProjThreads, 2) void k_proj_gemm(
   for (int e = 0; e < XG; ++e) {
     const int r = r0 + (tid + e * kProjThreads) / 8;
     xrow[e] = ~static_cast<size_t>(0);
-    if (r < n) {
-      if constexpr (MODE == kProjQKV) {
-        const int t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
-        xrow[e] = (static_cast<size_t>(b) * T + t) * kdim;
-      } else {
-        xrow[e] = static_cast<size_t>(seg0 + r) * kdim;
-      }
-    }
+    if (r < n) xrow[e] = static_cast<size_t>(seg0 + r) * kdim;
   }
   const uint16_t* wbase = w + (static_cast<size_t>(hh) * N + n0) * kdim;
 
@@ -196,21 +189,7 @@ __global__ __launch_bounds__(kProjThreads, 2) void k_proj_gemm(
   // n0 + 32 t2 + 8 j + 4 g + i (i < 4) in accumulator 4 j + i ---------------
   const int r = r0 + drow;
   if (r >= n) return;
-  if constexpr (MODE == kProjQKV) {
-    const int t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
-    const size_t orow = ((static_cast<size_t>(b) * H + hh) * T + t) * d;
-#pragma unroll
-    for (int t2 = 0; t2 < CT; ++t2)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int col = n0 + 32 * t2 + 8 * j + 4 * g;   // 4-column run inside one of q, k, v
-        const int which = col / d, cc = col - (col / d) * d;
-        uint16_t* dst = which == 0 ? dst0 : (which == 1 ? dst1 : dst2);
-        *reinterpret_cast<uint2*>(dst + orow + cc) =
-            make_uint2(pack_bf16x2(C[t2][4 * j], C[t2][4 * j + 1]),
-                       pack_bf16x2(C[t2][4 * j + 2], C[t2][4 * j + 3]));
-      }
-  } else {
+  {
     const size_t orow = static_cast<size_t>(seg0 + r) * N;
 #pragma unroll
     for (int t2 = 0; t2 < CT; ++t2)
