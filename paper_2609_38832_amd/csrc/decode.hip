@@ -307,6 +307,190 @@ __global__ __launch_bounds__(256) void k_decode_attn(
   }
 }
 
+// Grouped decode on the matrix cores (GQ = 4 or 8 query heads share each
+// cached row).  A wave takes 128 rows of the chunk in blocks of 32 and uses
+// v_mfma_f32_16x16x32_bf16 (lane l: A row / B column / C column l % 16,
+// reduction slots 8 (l / 16) .. + 7; C rows 4 (l / 16) + i in accumulator
+// i):
+//   S[q][r] = Q K^T for two 16-row tiles: A = the GQ rotated queries (rows
+//     >= GQ zero), B = the cached key rows, loaded straight from the cache;
+//   online softmax per query in exp2 units: the 16 lanes of one reduction
+//     group hold a query's 16 scores of a tile;
+//   O[q][d] += P V over the 32 rows: A = P and B = V^T read from wave-private
+//     LDS tiles (P as [query][row], V^T as [d][row], both 16-byte reads).
+// The reduction group kg = l / 16 of every layout holds queries 4 kg .. 4 kg
+// + 3, so a lane's rescale factors apply to its own output accumulators.
+// Partials as in k_decode_attn: (bk * GQ + q) * nchunk + chunk.
+template <int D, int GQ>
+__global__ __launch_bounds__(256, 2) void k_decode_attn_mfma(
+    const uint16_t* __restrict__ k_cache, const uint16_t* __restrict__ v_cache,
+    const int32_t* __restrict__ topk_idx, const int32_t* __restrict__ rows,
+    const float* __restrict__ qrot, int H, int K, long cap, int nchunk,
+    float* __restrict__ part_acc, float* __restrict__ part_ml) {
+  static_assert(GQ == 4 || GQ == 8, "queries per cached row");
+  static_assert(D == 64 || D == 128, "head width");
+  constexpr int KS = D / 32;           // reduction steps of the score product
+  constexpr int NT = D / 16;           // 16-column output tiles
+  constexpr int VG = D / 16;           // value granules per lane per 32-row block
+  constexpr int VP = 40;               // padded row length (elements) of the LDS tiles
+  constexpr int RPW = kDecChunk / 4;   // rows per wave
+  // the V^T tiles are dead after the loop; the per-wave output rows reuse them
+  static_assert(4 * GQ * D * 4 <= 4 * D * VP * 2, "output rows fit the V^T tiles");
+  __shared__ __attribute__((aligned(16))) uint16_t s_vt[4][D * VP];
+  __shared__ __attribute__((aligned(16))) uint16_t s_p[4][16 * VP];
+  __shared__ float s_ml[4][GQ][2];
+  float (*s_o)[GQ][D] = reinterpret_cast<float (*)[GQ][D]>(&s_vt[0][0]);
+
+  const int bk = block_x() / nchunk;
+  const int chunk = block_x() - bk * nchunk;
+  const int L = rows[bk];
+  const int r0 = chunk * kDecChunk;
+  if (r0 >= L) return;
+  const int r1 = min(L, r0 + kDecChunk);
+  const int b = bk / K;
+  const int h = topk_idx[bk];
+  const size_t rowbase = (static_cast<size_t>(b) * H + h) * cap;
+  const int tid = thread_x();
+  const int lane = tid % 64, wave = tid / 64;
+  const int j16 = lane & 15, kg = lane >> 4;
+  const int w0 = r0 + wave * RPW;
+  const int w1 = min(r1, w0 + RPW);
+
+  bf16x8 qa[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    float f[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      f[e] = j16 < GQ ? qrot[(static_cast<size_t>(bk) * GQ + j16) * D + 32 * s + 8 * kg + e] : 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) qa[s][e] = static_cast<__bf16>(f[e]);
+  }
+  float m[4], l[4];
+  f32x4 O[NT];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    m[i] = -1e30f;
+    l[i] = 0.f;
+  }
+#pragma unroll
+  for (int t = 0; t < NT; ++t) O[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const u32x4* kc = reinterpret_cast<const u32x4*>(k_cache);
+  const u32x4* vc = reinterpret_cast<const u32x4*>(v_cache);
+  uint16_t* vt = s_vt[wave];
+  uint16_t* pt = s_p[wave];
+  // rows past the wave's end read its last row (finite values; masked); the
+  // next block is loaded while the current one is processed (its loads are
+  // issued unconditionally, clamped like the tail)
+  u32x4 kx[2][KS], vx[VG], kn[2][KS], vn[VG];
+  auto load_block = [&](int rb, u32x4 (&kd)[2][KS], u32x4 (&vd)[VG]) {
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      const size_t row = rowbase + min(rb + 16 * tt + j16, w1 - 1);
+#pragma unroll
+      for (int s = 0; s < KS; ++s) kd[tt][s] = kc[row * (D / 8) + 4 * s + kg];
+    }
+    const size_t row = rowbase + min(rb + (lane & 31), w1 - 1);
+#pragma unroll
+    for (int i = 0; i < VG; ++i) vd[i] = vc[row * (D / 8) + 2 * i + (lane >> 5)];
+  };
+  if (w0 < w1) load_block(w0, kx, vx);
+  for (int rb = w0; rb < w1; rb += 32) {
+    load_block(min(rb + 32, w1 - 1), kn, vn);
+    f32x4 S[2];
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      S[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+        S[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[s], __builtin_bit_cast(bf16x8, kx[tt][s]),
+                                                        S[tt], 0, 0, 0);
+    }
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+      if (rb + 16 * tt + j16 >= w1) S[tt] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float mx = fmaxf(S[0][i], S[1][i]);
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      const float mnew = fmaxf(m[i], mx);
+      const float corr = __builtin_amdgcn_exp2f(m[i] - mnew);
+      m[i] = mnew;
+      const float p0 = __builtin_amdgcn_exp2f(S[0][i] - mnew);
+      const float p1 = __builtin_amdgcn_exp2f(S[1][i] - mnew);
+      float ps = p0 + p1;
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) ps += __shfl_xor(ps, o);
+      l[i] = l[i] * corr + ps;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) O[t][i] *= corr;
+      pt[(4 * kg + i) * VP + j16] = f32_to_bf16(p0);
+      pt[(4 * kg + i) * VP + 16 + j16] = f32_to_bf16(p1);
+    }
+    // V^T tile: lane writes its row (lane & 31) of granules 2 i + lane / 32
+#pragma unroll
+    for (int i = 0; i < VG; ++i) {
+      const int d0 = 8 * (2 * i + (lane >> 5));
+      const uint32_t w[4] = {vx[i].x, vx[i].y, vx[i].z, vx[i].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        vt[(d0 + 2 * e) * VP + (lane & 31)] = static_cast<uint16_t>(w[e] & 0xFFFFu);
+        vt[(d0 + 2 * e + 1) * VP + (lane & 31)] = static_cast<uint16_t>(w[e] >> 16);
+      }
+    }
+    // the tiles are wave-private: LDS operations of one wave complete in order
+    const bf16x8 pa = *reinterpret_cast<const bf16x8*>(&pt[j16 * VP + 8 * kg]);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const bf16x8 vb = *reinterpret_cast<const bf16x8*>(&vt[(16 * t + j16) * VP + 8 * kg]);
+      O[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, O[t], 0, 0, 0);
+    }
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int s = 0; s < KS; ++s) kx[tt][s] = kn[tt][s];
+#pragma unroll
+    for (int i = 0; i < VG; ++i) vx[i] = vn[i];
+  }
+
+  // ---- merge the four waves' partials of every query -----------------------
+  __syncthreads();   // every wave is done with its V^T tile (reused for s_o)
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int q = 4 * kg + i;
+    if (q < GQ) {
+      if (j16 == 0) {
+        s_ml[wave][q][0] = m[i];
+        s_ml[wave][q][1] = l[i];
+      }
+#pragma unroll
+      for (int t = 0; t < NT; ++t) s_o[wave][q][16 * t + j16] = O[t][i];
+    }
+  }
+  __syncthreads();
+  for (int t2 = tid; t2 < GQ * D; t2 += 256) {
+    const int q = t2 / D, dd = t2 - (t2 / D) * D;
+    float M = -1e30f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_ml[w][q][0]);
+    float Ls = 0.f, A = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float sc = __builtin_amdgcn_exp2f(s_ml[w][q][0] - M);
+      Ls = fmaf(s_ml[w][q][1], sc, Ls);
+      A = fmaf(s_o[w][q][dd], sc, A);
+    }
+    const size_t pi = (static_cast<size_t>(bk) * GQ + q) * nchunk + chunk;
+    part_acc[pi * D + dd] = A;
+    if (dd == 0) {
+      part_ml[2 * pi] = M;
+      part_ml[2 * pi + 1] = Ls;
+    }
+  }
+}
+
 // One workgroup per sequence; wave w merges the chunk partials of heads
 // w, w + 4, ... (lane c holds chunk c's max and sum; the accumulators are
 // read column-wise, d = lane + 64 i), then the gated head outputs are summed
@@ -570,8 +754,13 @@ static hipError_t run_decode(const float* logits, const float* bias, const void*
   if (e != hipSuccess) return e;
   const size_t grid = static_cast<size_t>(B) * K * nc;
   prof_mark("decode_attn", true, st);
-  k_decode_attn<D, BF16, GQ><<<static_cast<unsigned>(grid), 256, 0, st>>>(
-      k_cache, v_cache, topk_idx, w.rows, w.qrot, H, K, cap, nc, w.part_acc, w.part_ml);
+  if constexpr (BF16 && (GQ == 4 || GQ == 8))
+    k_decode_attn_mfma<D, GQ><<<static_cast<unsigned>(grid), 256, 0, st>>>(
+        static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache), topk_idx,
+        w.rows, w.qrot, H, K, cap, nc, w.part_acc, w.part_ml);
+  else
+    k_decode_attn<D, BF16, GQ><<<static_cast<unsigned>(grid), 256, 0, st>>>(
+        k_cache, v_cache, topk_idx, w.rows, w.qrot, H, K, cap, nc, w.part_acc, w.part_ml);
   prof_mark("decode_attn", false, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (out_dtype == 1)
