@@ -110,7 +110,8 @@ def _grouped_decode_inputs(B, Hkv, g, d, cap, seed):
 
 
 @pytest.mark.parametrize("g,d,rope", [(2, 64, O.ROPE_HEAD_RELATIVE), (4, 128, O.ROPE_GLOBAL),
-                                      (8, 64, O.ROPE_NONE), (8, 128, O.ROPE_HEAD_RELATIVE)])
+                                      (4, 64, O.ROPE_HEAD_RELATIVE), (8, 64, O.ROPE_NONE),
+                                      (8, 128, O.ROPE_HEAD_RELATIVE)])
 def test_grouped_decode_parity(g, d, rope):
     B, Hkv, Kkv, cap = 3, 6, 2, 1200
     say(f"grouped decode g={g} d={d} rope={rope}")

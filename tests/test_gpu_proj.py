@@ -39,6 +39,9 @@ CASES = {
     # H d > 384 K: the per-pair form of the output projection
     "pairs_d64_h16_k2": dict(B=2, T=200, H=16, K=2, d=64, d_model=256),
     "pairs_d128_h8_k2_ragged": dict(B=1, T=333, H=8, K=2, d=128, d_model=384),
+    # more than 1024 (b, h) segments: segment offsets read from global memory
+    "many_segments_dense": dict(B=17, T=40, H=64, K=11, d=64, d_model=128),
+    "many_segments_pairs": dict(B=20, T=70, H=64, K=4, d=64, d_model=128),
 }
 
 
@@ -94,7 +97,8 @@ def _packed_to_dense(hp, topk, H, T, d):
 
 
 @pytest.mark.parametrize("name", ["d64_dm256", "d128_dm384_ragged", "all_heads", "one_head",
-                                  "pairs_d64_h16_k2", "pairs_d128_h8_k2_ragged"])
+                                  "pairs_d64_h16_k2", "pairs_d128_h8_k2_ragged",
+                                  "many_segments_dense", "many_segments_pairs"])
 @pytest.mark.parametrize("hdt,odt", [("f32", torch.float32), ("bf16", torch.bfloat16)])
 def test_out_proj_parity(name, hdt, odt):
     w = _case(name)
