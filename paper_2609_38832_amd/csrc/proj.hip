@@ -454,19 +454,18 @@ __global__ __launch_bounds__(kProjThreads, TM == 128 ? 2 : 1) void k_proj_big(
   // ahead instead of two
   constexpr bool W2 = (MODE == kProjQKV && TM == 256) || (MODE == kProjOut && TN <= 128);
   u32x4 xs0[XG], xs1[XG], wv0[WG], wv1[W2 ? WG : 1];
-  auto load_x = [&](u32x4 (&xs)[XG], int ch) {
-#pragma unroll
-    for (int e = 0; e < XG; ++e) {
-      if constexpr (MODE == kProjQKV) {
-        xs[e] = *reinterpret_cast<const u32x4*>(src + xrow[e] + ch * kProjKC + 8 * gr);
-      } else {   // the gated row of the token's head (the zero row Nr if unselected)
-        const int h = ch / cph, dd0 = (ch - h * cph) * kProjKC;
-        const int m = L.map[h * TM + tid / 8 + 32 * e];
-        xs[e] = *reinterpret_cast<const u32x4*>(src + static_cast<size_t>(m) * d + dd0 + 8 * gr);
-      }
+  // one 16-byte granule e of the thread's data rows (rows tid / 8 + 32 e) or
+  // weight rows of chunk ch
+  auto load_x = [&](u32x4 (&xs)[XG], int ch, int e) {
+    if constexpr (MODE == kProjQKV) {
+      xs[e] = *reinterpret_cast<const u32x4*>(src + xrow[e] + ch * kProjKC + 8 * gr);
+    } else {   // the gated row of the token's head (the zero row Nr if unselected)
+      const int h = ch / cph, dd0 = (ch - h * cph) * kProjKC;
+      const int m = L.map[h * TM + tid / 8 + 32 * e];
+      xs[e] = *reinterpret_cast<const u32x4*>(src + static_cast<size_t>(m) * d + dd0 + 8 * gr);
     }
   };
-  auto load_w = [&](u32x4 (&wv)[WG], int ch) {
+  auto load_w = [&](u32x4 (&wv)[WG], int ch, int e) {
     const uint16_t* wb;
     size_t stride;
     if constexpr (MODE == kProjQKV) {
@@ -477,21 +476,15 @@ __global__ __launch_bounds__(kProjThreads, TM == 128 ? 2 : 1) void k_proj_big(
       wb = w + (static_cast<size_t>(h) * N + n0) * d + dd0;
       stride = d;
     }
-#pragma unroll
-    for (int e = 0; e < WG; ++e)
-      wv[e] = *reinterpret_cast<const u32x4*>(wb + static_cast<size_t>(tid / 8 + 32 * e) * stride + 8 * gr);
+    wv[e] = *reinterpret_cast<const u32x4*>(wb + static_cast<size_t>(tid / 8 + 32 * e) * stride + 8 * gr);
   };
-  auto store = [&](const u32x4 (&xs)[XG], const u32x4 (&wv)[WG], int stg) {
-#pragma unroll
-    for (int e = 0; e < XG; ++e) {
-      const int row = tid / 8 + 32 * e;
-      *reinterpret_cast<u32x4*>(&L.x[stg][row * kProjKC + swz<8>(row, gr) * 8]) = xs[e];
-    }
-#pragma unroll
-    for (int e = 0; e < WG; ++e) {
-      const int row = tid / 8 + 32 * e;
-      *reinterpret_cast<u32x4*>(&L.w[stg][row * kProjKC + swz<8>(row, gr) * 8]) = wv[e];
-    }
+  auto store_x = [&](const u32x4 (&xs)[XG], int stg, int e) {
+    const int row = tid / 8 + 32 * e;
+    *reinterpret_cast<u32x4*>(&L.x[stg][row * kProjKC + swz<8>(row, gr) * 8]) = xs[e];
+  };
+  auto store_w = [&](const u32x4 (&wv)[WG], int stg, int e) {
+    const int row = tid / 8 + 32 * e;
+    *reinterpret_cast<u32x4*>(&L.w[stg][row * kProjKC + swz<8>(row, gr) * 8]) = wv[e];
   };
 
   f32x16 C[CT][RT];
@@ -502,9 +495,20 @@ __global__ __launch_bounds__(kProjThreads, TM == 128 ? 2 : 1) void k_proj_big(
 #pragma unroll
       for (int e = 0; e < 16; ++e) C[ct][rt][e] = 0.f;
 
-  auto compute = [&](int stg) {
-    // operand fragments in two register sets: the reads of step ks + 1 are
-    // issued before the MFMAs of step ks (scheduling barriers keep them there)
+  // One chunk step: chunk ch is multiplied from stage stg in four 16-wide
+  // steps; behind the MFMAs of each step go a quarter of the LDS stores of
+  // X(ch+1) (register set xn) and W(ch+1) into the free stage, each followed
+  // by the load of the same granule of X(ch+3) and W(ch+2 or ch+3) into the
+  // register it freed, so the staging runs in the shadow of the matrix work.
+  // Operand fragments use two register sets: the reads of step ks + 1 are
+  // issued before the MFMAs of step ks (scheduling barriers keep each step's
+  // instructions together).  No branch surrounds a load or store (a load
+  // under a branch is waited for where the branch joins, and the wait
+  // counter is in order, so it would also wait for every load issued
+  // before); indices past the end are clamped to the last chunk and land in
+  // the stage that is no longer read.
+  auto step = [&](int ch, u32x4 (&xn)[XG], u32x4 (&wn)[WG], int stg) {
+    const int chx = min(ch + 3, last), chw = min(ch + (W2 ? 3 : 2), last);
     bf16x8 bx[2][RT], aw[2][CT];
     auto read_frags = [&](int ks, int set) {
 #pragma unroll
@@ -531,36 +535,42 @@ __global__ __launch_bounds__(kProjThreads, TM == 128 ? 2 : 1) void k_proj_big(
         for (int rt = 0; rt < RT; ++rt)
           C[ct][rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aw[ks & 1][ct], bx[ks & 1][rt],
                                                               C[ct][rt], 0, 0, 0);
+#pragma unroll
+      for (int e = ks * XG / 4; e < (ks + 1) * XG / 4; ++e) {
+        store_x(xn, stg ^ 1, e);
+        load_x(xn, chx, e);
+      }
+#pragma unroll
+      for (int e = ks * WG / 4; e < (ks + 1) * WG / 4; ++e) {
+        store_w(wn, stg ^ 1, e);
+        load_w(wn, chw, e);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
-  };
-
-  // One chunk step: X(ch+1) (in register set xn) and W(ch+1) go to the free
-  // stage, W(ch+2) and X(ch+3) are loaded (X into the set just stored), then
-  // chunk ch is multiplied.  No branch surrounds a load or store (a load under
-  // a branch is waited for where the branch joins, and the wait counter is
-  // in order, so it would also wait for every load issued before); indices
-  // past the end are clamped to the last chunk and land in the stage that is
-  // no longer read.
-  auto step = [&](int ch, u32x4 (&xn)[XG], u32x4 (&wn)[WG], int stg) {
-    store(xn, wn, stg ^ 1);
-    load_w(wn, min(ch + (W2 ? 3 : 2), last));
-    load_x(xn, min(ch + 3, last));
-    __builtin_amdgcn_sched_barrier(0);
-    compute(stg);
     __syncthreads();
   };
 
   auto& wv1s = [&]() -> u32x4(&)[WG] {
     if constexpr (W2) return wv1; else return wv0;
   }();
-  load_x(xs0, 0);
-  load_w(wv0, 0);
-  store(xs0, wv0, 0);
-  load_x(xs1, min(1, last));
-  load_w(wv1s, min(1, last));
-  load_x(xs0, min(2, last));
-  if constexpr (W2) load_w(wv0, min(2, last));
+#pragma unroll
+  for (int e = 0; e < XG; ++e) load_x(xs0, 0, e);
+#pragma unroll
+  for (int e = 0; e < WG; ++e) load_w(wv0, 0, e);
+#pragma unroll
+  for (int e = 0; e < XG; ++e) store_x(xs0, 0, e);
+#pragma unroll
+  for (int e = 0; e < WG; ++e) store_w(wv0, 0, e);
+#pragma unroll
+  for (int e = 0; e < XG; ++e) load_x(xs1, min(1, last), e);
+#pragma unroll
+  for (int e = 0; e < WG; ++e) load_w(wv1s, min(1, last), e);
+#pragma unroll
+  for (int e = 0; e < XG; ++e) load_x(xs0, min(2, last), e);
+  if constexpr (W2) {
+#pragma unroll
+    for (int e = 0; e < WG; ++e) load_w(wv0, min(2, last), e);
+  }
   __syncthreads();
   int ch = 0;
   for (; ch + 1 < nchunk; ch += 2) {
