@@ -1098,11 +1098,12 @@ __global__ __launch_bounds__(64) void k_attn_generic(
 }
 
 // ---------------------------------------------------------------------------
-// One thread per (token, 8 output elements).  The K slots are gathered four
+// One thread per (token, 8 output elements).  The K slots are gathered eight
 // at a time (all loads of a batch issued before their products) and summed
-// in k order.
+// in k order.  GC = 1 fixes G = 1 at compile time (no per-row division,
+// whose branch would split the batch of loads).
 constexpr int kCombineThreads = 256;
-template <bool IN_BF16, bool OUT_BF16>
+template <bool IN_BF16, bool OUT_BF16, int GC = 0>
 __global__ __launch_bounds__(kCombineThreads) void k_combine(
     const void* __restrict__ hout, const float* __restrict__ gates,
     const int32_t* __restrict__ slot_pos, long BT, int K, int D, int Nr, int G,
@@ -1120,41 +1121,42 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
   // Rounds of KC rows: row v = k * G + u is head output u of selected slot k
   // (G = 1 without key/value groups), weighted by the slot's gate; first
   // their slots and gates, then all their rows in flight at once; the sum
-  // runs over v in ascending order.
+  // runs over v in ascending order.  No load sits under a branch (a load
+  // under a branch is waited for where the branch joins, which would
+  // serialise the rows): indices are clamped, and rows past K * G or with a
+  // slot outside the packed rows are replaced by zeros after the load.
   constexpr int KC = 8;
+  if constexpr (GC == 1) G = 1;
   const int KV = K * G;
   for (int k0 = 0; k0 < KV; k0 += KC) {
     int p[KC];
+    bool ok[KC];
     float gk[KC];
     float x[KC][8];
 #pragma unroll
     for (int i = 0; i < KC; ++i) {
       const int vr = k0 + i;
-      const bool in = vr < KV;
-      const int kk = G == 1 ? vr : vr / G;
-      const int sl = in ? sp[kk] : -1;
-      p[i] = static_cast<unsigned>(sl) < static_cast<unsigned>(Nr) ? sl * G + (vr - kk * G) : -1;
-      gk[i] = in ? gp[kk] : 0.f;
+      const int kk = min(GC == 1 ? vr : vr / G, K - 1);
+      const int sl = sp[kk];
+      const float gv = gp[kk];
+      ok[i] = vr < KV && static_cast<unsigned>(sl) < static_cast<unsigned>(Nr);
+      p[i] = ok[i] ? sl * G + (vr - kk * G) : 0;
+      gk[i] = ok[i] ? gv : 0.f;
     }
 #pragma unroll
     for (int i = 0; i < KC; ++i) {
-      if (p[i] >= 0) {
-        if constexpr (IN_BF16) {
-          const uint4 u =
-              reinterpret_cast<const uint4*>(hout)[static_cast<size_t>(p[i]) * C + cc];
-          unpack8(u, x[i]);
-        } else {
-          const float4* src =
-              reinterpret_cast<const float4*>(hout) + (static_cast<size_t>(p[i]) * C + cc) * 2;
-          const float4 a = src[0], bb = src[1];
-          x[i][0] = a.x; x[i][1] = a.y; x[i][2] = a.z; x[i][3] = a.w;
-          x[i][4] = bb.x; x[i][5] = bb.y; x[i][6] = bb.z; x[i][7] = bb.w;
-        }
+      if constexpr (IN_BF16) {
+        const uint4 u = reinterpret_cast<const uint4*>(hout)[static_cast<size_t>(p[i]) * C + cc];
+        unpack8(u, x[i]);
       } else {
-        gk[i] = 0.f;   // slot outside the packed rows contributes nothing
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[i][e] = 0.f;
+        const float4* src =
+            reinterpret_cast<const float4*>(hout) + (static_cast<size_t>(p[i]) * C + cc) * 2;
+        const float4 a = src[0], bb = src[1];
+        x[i][0] = a.x; x[i][1] = a.y; x[i][2] = a.z; x[i][3] = a.w;
+        x[i][4] = bb.x; x[i][5] = bb.y; x[i][6] = bb.z; x[i][7] = bb.w;
       }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[i][e] = ok[i] ? x[i][e] : 0.f;
     }
 #pragma unroll
     for (int i = 0; i < KC; ++i)
@@ -1335,13 +1337,17 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   const unsigned grid = static_cast<unsigned>((threads + kCombineThreads - 1) / kCombineThreads);
   prof_mark("combine", true, st);
   if (hb && out_dtype == 1)
-    k_combine<true, true><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, G, out);
+    (G == 1 ? k_combine<true, true, 1> : k_combine<true, true>)<<<grid, kCombineThreads, 0, st>>>(
+        hout, gates, slot_pos, BT, K, d, Nr, G, out);
   else if (hb)
-    k_combine<true, false><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, G, out);
+    (G == 1 ? k_combine<true, false, 1> : k_combine<true, false>)<<<grid, kCombineThreads, 0, st>>>(
+        hout, gates, slot_pos, BT, K, d, Nr, G, out);
   else if (out_dtype == 1)
-    k_combine<false, true><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, G, out);
+    (G == 1 ? k_combine<false, true, 1> : k_combine<false, true>)<<<grid, kCombineThreads, 0, st>>>(
+        hout, gates, slot_pos, BT, K, d, Nr, G, out);
   else
-    k_combine<false, false><<<grid, kCombineThreads, 0, st>>>(hout, gates, slot_pos, BT, K, d, Nr, G, out);
+    (G == 1 ? k_combine<false, false, 1> : k_combine<false, false>)<<<grid, kCombineThreads, 0, st>>>(
+        hout, gates, slot_pos, BT, K, d, Nr, G, out);
   prof_mark("combine", false, st);
   return hipGetLastError();
 }
@@ -1352,11 +1358,11 @@ hipError_t launch_combine_rows(const uint16_t* rows, const float* gates, const i
   const long threads = BT * (D / 8);
   const unsigned grid = static_cast<unsigned>((threads + kCombineThreads - 1) / kCombineThreads);
   if (out_dtype == 1)
-    k_combine<true, true><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D, Nr, 1,
-                                                           out);
+    k_combine<true, true, 1><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D, Nr,
+                                                              1, out);
   else
-    k_combine<true, false><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D, Nr,
-                                                            1, out);
+    k_combine<true, false, 1><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D,
+                                                               Nr, 1, out);
   return hipGetLastError();
 }
 
