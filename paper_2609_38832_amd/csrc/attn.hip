@@ -381,16 +381,21 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
 
   // Every load of the tile is issued before any of them is used: the
   // thread's rows' tokens, then its key granule pairs and value granules.
+  // No load sits under a branch (a load under a branch is waited for where
+  // the branch joins, which would serialise them): rows past the segment's
+  // end load its last row and are zeroed after the load.
   constexpr int HP = D / 16;  // 8-element granule pairs (j, j + d/2) per key row
   constexpr int RG = D / 8;   // 16-byte granules per value row
   constexpr int KU = kBN * HP / kPackThreads, VU = kBN * RG / kPackThreads;
   static_assert(KU * kPackThreads == kBN * HP && VU * kPackThreads == kBN * RG, "units");
   static_assert(kWave % HP == 0, "a key row's units share one wave");
-  auto token_of = [&](int row) {   // -1 past the segment's end
-    const int r = r0 + row;
-    return r < n ? static_cast<int>(min(static_cast<unsigned>(perm_token[seg0 + r]),
-                                        static_cast<unsigned>(T - 1)))
-                 : -1;
+  auto token_of = [&](int row) {   // the segment's last row past its end
+    const int r = min(r0 + row, n - 1);
+    return static_cast<int>(min(static_cast<unsigned>(perm_token[seg0 + r]),
+                                static_cast<unsigned>(T - 1)));
+  };
+  auto zero_unless = [](uint4 x, bool keep) {
+    return keep ? x : make_uint4(0, 0, 0, 0);
   };
   int ktok[KU], vtok[VU];
 #pragma unroll
@@ -401,19 +406,23 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
 #pragma unroll
   for (int i = 0; i < KU; ++i) {
     const int c = (tid + i * kPackThreads) % HP;
-    ka[i] = kb[i] = make_uint4(0, 0, 0, 0);
-    if (ktok[i] >= 0) {
-      const uint16_t* src = k + (head_base + ktok[i]) * D;
-      ka[i] = *reinterpret_cast<const uint4*>(src + 8 * c);
-      kb[i] = *reinterpret_cast<const uint4*>(src + D / 2 + 8 * c);
-    }
+    const uint16_t* src = k + (head_base + ktok[i]) * D;
+    ka[i] = *reinterpret_cast<const uint4*>(src + 8 * c);
+    kb[i] = *reinterpret_cast<const uint4*>(src + D / 2 + 8 * c);
   }
 #pragma unroll
   for (int i = 0; i < VU; ++i) {
     const int gr = (tid + i * kPackThreads) % RG;
-    vx[i] = make_uint4(0, 0, 0, 0);
-    if (vtok[i] >= 0) vx[i] = *reinterpret_cast<const uint4*>(v + (head_base + vtok[i]) * D + 8 * gr);
+    vx[i] = *reinterpret_cast<const uint4*>(v + (head_base + vtok[i]) * D + 8 * gr);
   }
+#pragma unroll
+  for (int i = 0; i < KU; ++i) {
+    const bool in = r0 + (tid + i * kPackThreads) / HP < n;
+    ka[i] = zero_unless(ka[i], in);
+    kb[i] = zero_unless(kb[i], in);
+  }
+#pragma unroll
+  for (int i = 0; i < VU; ++i) vx[i] = zero_unless(vx[i], r0 + (tid + i * kPackThreads) / RG < n);
 
   float rmax = 0.f;   // largest squared norm of a packed (rounded) key row seen
 #pragma unroll
@@ -421,7 +430,7 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
     const int u = tid + i * kPackThreads;
     const int row = u / HP, c = u % HP;
     uint4 o1 = ka[i], o2 = kb[i];
-    if (ktok[i] >= 0 && rope_mode != 2) {
+    if (rope_mode != 2) {   // rows past the end are zero and stay zero
       float x1[8], x2[8];
       unpack8(ka[i], x1);
       unpack8(kb[i], x2);
