@@ -334,12 +334,19 @@ __global__ __launch_bounds__(kScatterThreads) void k_route_scatter(
     static_assert(kScatterThreads == 8 * 64, "8 lanes per head");
     const int h = tid / 8, j = tid % 8;
     int before = 0, total = 0;
-    if (h < H) {
-      const int32_t* cp = counts + (static_cast<size_t>(b) * H + h) * nchunk;
-      for (int cc = j; cc < nchunk; cc += 8) {
-        const int x = cp[cc];
-        total += x;
-        before += cc < c ? x : 0;
+    // eight independent loads per round (indices clamped, no load under a
+    // branch, so they are in flight together); lanes of heads >= H add 0
+    const int32_t* cp = counts + (static_cast<size_t>(b) * H + min(h, H - 1)) * nchunk;
+    for (int c0 = j; c0 < nchunk; c0 += 64) {
+      int x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[u] = cp[min(c0 + 8 * u, nchunk - 1)];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int cc = c0 + 8 * u;
+        const int v = cc < nchunk && h < H ? x[u] : 0;
+        total += v;
+        before += cc < c ? v : 0;
       }
     }
 #pragma unroll
@@ -374,11 +381,12 @@ __global__ __launch_bounds__(kScatterThreads) void k_route_scatter(
   const unsigned nr = static_cast<unsigned>(B) * T * K;
   for (int e = tid; e < nt * K; e += kScatterThreads) {
     const int h = topk_idx[e0 + e];
+    const int rank = slot_pos[e0 + e];
     // the head and the in-chunk rank come from k_route_count; a position
     // outside [0, B*T*K) can only come from a corrupted workspace and is
     // not stored
     const int pos = static_cast<unsigned>(h) < static_cast<unsigned>(H)
-                        ? s_base[h] + slot_pos[e0 + e] : -1;
+                        ? s_base[min(max(h, 0), H - 1)] + rank : -1;
     if (static_cast<unsigned>(pos) < nr) perm_token[pos] = t0 + e / K;
     slot_pos[e0 + e] = pos;
   }
