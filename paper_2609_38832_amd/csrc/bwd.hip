@@ -95,9 +95,17 @@ __global__ __launch_bounds__(256) void k_bwd_gather(
   }
   const int b = s / H, h = s - (s / H) * H;
   int ks = -1;   // which of the token's K selections this segment is
-  for (int kk = 0; kk < K; ++kk)
-    if (topk_idx[(static_cast<size_t>(b) * T + t) * K + kk] == h) ks = kk;
-  const float g = ks >= 0 ? gates[(static_cast<size_t>(b) * T + t) * K + ks] : 0.f;
+  const int32_t* sel = topk_idx + (static_cast<size_t>(b) * T + t) * K;
+  for (int k0 = 0; k0 < K; k0 += 8) {   // eight independent loads per round
+    int sv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) sv[u] = sel[min(k0 + u, K - 1)];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (k0 + u < K && sv[u] == h) ks = k0 + u;
+  }
+  const float gv = gates[(static_cast<size_t>(b) * T + t) * K + max(ks, 0)];
+  const float g = ks >= 0 ? gv : 0.f;
   if (j0 == 0) {
     seg_of[r] = s;
     kslot[r] = ks;
@@ -505,12 +513,21 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
     const int t = min(static_cast<unsigned>(perm_token[seg0 + r0 + tid]),
                       static_cast<unsigned>(T - 1));
     const int32_t* sel = topk_idx + (static_cast<size_t>(b) * T + t) * K;
+    // the token's slot of head hh: eight independent loads per round (no
+    // load under a branch, so they are in flight together)
     int ks = -1;
-    for (int kk = 0; kk < K; ++kk)
-      if (sel[kk] == hh) ks = kk;
+    for (int k0 = 0; k0 < K; k0 += 8) {
+      int sv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sv[u] = sel[min(k0 + u, K - 1)];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (k0 + u < K && sv[u] == hh) ks = k0 + u;
+    }
+    const float gv = gates[(static_cast<size_t>(b) * T + t) * K + max(ks, 0)];
     L.tok[tid] = t;
     L.ks[tid] = ks;
-    L.g[tid] = ks >= 0 ? gates[(static_cast<size_t>(b) * T + t) * K + ks] : 0.f;
+    L.g[tid] = ks >= 0 ? gv : 0.f;
   }
   __syncthreads();
 
@@ -738,7 +755,13 @@ __global__ __launch_bounds__(kZeroThreads) void k_bwd_zero_unrouted(
   const int b = static_cast<int>(bh / H), h = static_cast<int>(bh - (bh / H) * H);
   const int32_t* tk = topk_idx + (static_cast<size_t>(b) * T + t) * K;
   bool routed = false;
-  for (int kk = 0; kk < K; ++kk) routed |= tk[kk] == h;
+  for (int k0 = 0; k0 < K; k0 += 8) {   // eight independent loads per round
+    int sv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) sv[u] = tk[min(k0 + u, K - 1)];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) routed |= sv[u] == h;   // clamped repeats change nothing
+  }
   if (routed) return;
   const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
   const size_t o = row * D + 4 * c4;
