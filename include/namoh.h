@@ -250,7 +250,11 @@ namoh_status namoh_attn_fwd_grouped(const void* q, const void* k, const void* v,
  * In:  logits [B, H_kv] f32; q [B, H_kv*g, d]; k, v [B, H_kv, d] (only the
  *      selected groups read); caches [B, H_kv, cap, d], cache_len [B, H_kv]
  *      as for namoh_decode_step.  bf16, d in {64, 128}, group_size in
- *      {1, 2, 4, 8} (else UNSUPPORTED / INVALID_ARG).
+ *      {1, 2, 4, 8} (else UNSUPPORTED / INVALID_ARG).  With 4 or 8 heads
+ *      per group the scores and the probability-weighted values run on the
+ *      matrix cores: the rotated, scaled queries and the probabilities are
+ *      rounded to bf16 before their products (float32 accumulation and
+ *      softmax, as in the bf16 prefill); with 1 or 2 they stay float32.
  * Out: topk_idx, gates [B, K_kv]; out [B, d] of out_dtype; caches and
  *      cache_len updated; dev_status as for namoh_decode_step.
  * Workspace: namoh_decode_grouped_workspace_size bytes.
