@@ -331,12 +331,15 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn_mfma(
   static_assert(D == 64 || D == 128, "head width");
   constexpr int KS = D / 32;           // reduction steps of the score product
   constexpr int NT = D / 16;           // 16-column output tiles
-  constexpr int VG = D / 16;           // value granules per lane per 32-row block
   constexpr int VP = 40;               // padded row length (elements) of the LDS tiles
   constexpr int RPW = kDecChunk / 4;   // rows per wave
   // the V^T tiles are dead after the loop; the per-wave output rows reuse them
   static_assert(4 * GQ * D * 4 <= 4 * D * VP * 2, "output rows fit the V^T tiles");
+  constexpr int KP = D + 8;             // padded key row (elements) of the LDS key tile
+  constexpr int GR = D / 8;             // 16-byte granules per cached row
+  constexpr int RPL = GR / 2;           // rows per lane per 32-row block (coalesced loads)
   __shared__ __attribute__((aligned(16))) uint16_t s_vt[4][D * VP];
+  __shared__ __attribute__((aligned(16))) uint16_t s_k[4][32 * KP];
   __shared__ __attribute__((aligned(16))) uint16_t s_p[4][16 * VP];
   __shared__ float s_ml[4][GQ][2];
   float (*s_o)[GQ][D] = reinterpret_cast<float (*)[GQ][D]>(&s_vt[0][0]);
@@ -380,32 +383,55 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn_mfma(
   const u32x4* vc = reinterpret_cast<const u32x4*>(v_cache);
   uint16_t* vt = s_vt[wave];
   uint16_t* pt = s_p[wave];
-  // rows past the wave's end read its last row (finite values; masked); the
-  // next block is loaded while the current one is processed (its loads are
-  // issued unconditionally, clamped like the tail)
-  u32x4 kx[2][KS], vx[VG], kn[2][KS], vn[VG];
-  auto load_block = [&](int rb, u32x4 (&kd)[2][KS], u32x4 (&vd)[VG]) {
+  // Coalesced loads: lane (granule lane % GR, row group lane / GR) reads rows
+  // RPL * group + i, i < RPL, of the block, so each load instruction covers
+  // whole rows.  Rows past the wave's end read its last row (finite values;
+  // masked).  The next block is loaded while the current one is processed
+  // (its loads are issued unconditionally, clamped like the tail).
+  const int lg = lane % GR, lq = lane / GR;
+  u32x4 kx[RPL], vx[RPL], kn[RPL], vn[RPL];
+  auto load_block = [&](int rb, u32x4 (&kd)[RPL], u32x4 (&vd)[RPL]) {
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      const size_t row = rowbase + min(rb + 16 * tt + j16, w1 - 1);
-#pragma unroll
-      for (int s = 0; s < KS; ++s) kd[tt][s] = kc[row * (D / 8) + 4 * s + kg];
+    for (int i = 0; i < RPL; ++i) {
+      const size_t row = rowbase + min(rb + RPL * lq + i, w1 - 1);
+      kd[i] = kc[row * GR + lg];
+      vd[i] = vc[row * GR + lg];
     }
-    const size_t row = rowbase + min(rb + (lane & 31), w1 - 1);
-#pragma unroll
-    for (int i = 0; i < VG; ++i) vd[i] = vc[row * (D / 8) + 2 * i + (lane >> 5)];
   };
   if (w0 < w1) load_block(w0, kx, vx);
   for (int rb = w0; rb < w1; rb += 32) {
     load_block(min(rb + 32, w1 - 1), kn, vn);
+    // key rows into the wave's LDS tile (row-major, padded rows), values
+    // transposed into V^T: lane's RPL consecutive rows of one granule become,
+    // per column, one RPL-element run of a V^T row
+    uint16_t* kt = s_k[wave];
+#pragma unroll
+    for (int i = 0; i < RPL; ++i)
+      *reinterpret_cast<u32x4*>(&kt[(RPL * lq + i) * KP + 8 * lg]) = kx[i];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint32_t run[RPL / 2];
+#pragma unroll
+      for (int m = 0; m < RPL / 2; ++m) {
+        const uint32_t a = vx[2 * m][e / 2], c2 = vx[2 * m + 1][e / 2];
+        run[m] = (e & 1) ? ((a >> 16) | (c2 & 0xFFFF0000u)) : ((a & 0xFFFFu) | (c2 << 16));
+      }
+      uint16_t* dst = &s_vt[wave][(8 * lg + e) * VP + RPL * lq];
+      if constexpr (RPL == 8)
+        *reinterpret_cast<u32x4*>(dst) = u32x4{run[0], run[1], run[2], run[3]};
+      else
+        *reinterpret_cast<uint2*>(dst) = make_uint2(run[0], run[1]);
+    }
     f32x4 S[2];
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
       S[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s = 0; s < KS; ++s)
-        S[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[s], __builtin_bit_cast(bf16x8, kx[tt][s]),
-                                                        S[tt], 0, 0, 0);
+      for (int s = 0; s < KS; ++s) {
+        const bf16x8 kb =
+            *reinterpret_cast<const bf16x8*>(&kt[(16 * tt + j16) * KP + 32 * s + 8 * kg]);
+        S[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[s], kb, S[tt], 0, 0, 0);
+      }
     }
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt)
@@ -429,17 +455,6 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn_mfma(
       pt[(4 * kg + i) * VP + j16] = f32_to_bf16(p0);
       pt[(4 * kg + i) * VP + 16 + j16] = f32_to_bf16(p1);
     }
-    // V^T tile: lane writes its row (lane & 31) of granules 2 i + lane / 32
-#pragma unroll
-    for (int i = 0; i < VG; ++i) {
-      const int d0 = 8 * (2 * i + (lane >> 5));
-      const uint32_t w[4] = {vx[i].x, vx[i].y, vx[i].z, vx[i].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vt[(d0 + 2 * e) * VP + (lane & 31)] = static_cast<uint16_t>(w[e] & 0xFFFFu);
-        vt[(d0 + 2 * e + 1) * VP + (lane & 31)] = static_cast<uint16_t>(w[e] >> 16);
-      }
-    }
     // the tiles are wave-private: LDS operations of one wave complete in order
     const bf16x8 pa = *reinterpret_cast<const bf16x8*>(&pt[j16 * VP + 8 * kg]);
 #pragma unroll
@@ -448,11 +463,10 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn_mfma(
       O[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, O[t], 0, 0, 0);
     }
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-      for (int s = 0; s < KS; ++s) kx[tt][s] = kn[tt][s];
-#pragma unroll
-    for (int i = 0; i < VG; ++i) vx[i] = vn[i];
+    for (int i = 0; i < RPL; ++i) {
+      kx[i] = kn[i];
+      vx[i] = vn[i];
+    }
   }
 
   // ---- merge the four waves' partials of every query -----------------------
