@@ -7,13 +7,21 @@ A step is one pass of the whole layer over one batch of seeded synthetic
 input already resident in HBM: for prefill workloads route (top-K, gates,
 permutation) + attention (packing with RoPE, MFMA attention, gated combine);
 for the decode workload one decode step (route, append, history attention,
-combine).  Prints one JSON line.  The default workload is the balanced bf16
-prefill (B=4, T=4096, H=32, K=8, d=64).
+combine).  Prints one JSON line.
+
+Without --workload the line's headline is the largest prefill workload, the
+skewed-routing one (B=2, T=16384, H=32, K=4, d=128: 327 GFLOP of causal
+attention per step), and the line carries one object per other workload
+under "workloads": the balanced prefill (B=4, T=4096, H=32, K=8, d=64), the
+long-context head-scaling prefill (B=1, T=32768, H=64, K=8, d=128) and the
+decode step (64 sequences, 131072 prior tokens, H=64, K=8, d=128), each with
+its own roofline and CPU baseline.  --workload N runs one workload alone.
 
 The roofline entry is for the dominant kernel (routed attention for prefill,
 history attention for decode): algorithmic FLOPs (4*d*sum n(n+1)/2) or bytes
 (sum over active heads of (n+1)*2*d*2) per launch divided by its average
-duration, timed with HIP events recorded by the library on the launch stream.
+duration, timed with HIP events that the library attaches to the kernel's
+dispatch on the launch stream (the interval a kernel trace records).
 The cpu_baseline entry times the CPU oracle (float64 numpy) on a bounded
 sample of the same workload on this host.
 """
@@ -85,6 +93,29 @@ def cpu_info():
     return cores, threads, model
 
 
+def warm_up(step, args, torch):
+    """args.warmup untimed steps, then more until at least args.settle_ms of
+    continuous GPU work has run: the first tens of milliseconds of sustained
+    load on the part run at transient clocks (kernel times move by up to 40 %
+    over the first ~40 ms), so the timed steps start from the steady state.
+    Returns the number of untimed steps run."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.warmup):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    done = args.warmup
+    per = e0.elapsed_time(e1) / max(args.warmup, 1)
+    if args.settle_ms > 0:
+        more = max(0, int(math.ceil(args.settle_ms / max(per, 1e-3))) - args.warmup)
+        for _ in range(more):
+            step()
+        torch.cuda.synchronize()
+        done += more
+    return done
+
+
 # ----------------------------------------------------------------------------
 def bench_prefill(w, args, torch, L, DI):
     dev = torch.device("cuda:0")
@@ -111,10 +142,8 @@ def bench_prefill(w, args, torch, L, DI):
         L.route(logits, K, L.GATE_SOFTMAX_SELECTED, out=routing, ws=rws)
         L.attn_fwd(q, k, v, routing, K, w.rope_base, L.ROPE_HEAD_RELATIVE, out=out, ws=aws)
 
-    log(f"warmup {args.warmup} steps")
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} steps, settle {args.settle_ms} ms")
+    warm = warm_up(step, args, torch)
     n = routing["head_len"].cpu().numpy().astype(np.int64)
     c_attn = int((n * (n + 1) // 2).sum())
     flops = 4.0 * d * c_attn
@@ -161,7 +190,8 @@ def bench_prefill(w, args, torch, L, DI):
                       "rope": "head-relative", "rope_base": w.rope_base,
                       "gates": "softmax over selected"},
            "roofline": roof,
-           "kernels_ms": {k2: round(v2, 4) for k2, v2 in kern.items()}}
+           "kernels_ms": {k2: round(v2, 4) for k2, v2 in kern.items()},
+           "warmup_steps_run": warm, "settle_ms": args.settle_ms}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline_prefill(w, inp, n, args.cpu_budget)
     return res
@@ -232,9 +262,7 @@ def bench_layer(w, args, torch, L, DI):
         L.out_proj(ho, wo, routing, B, T, H, K, out=out, ws=ows)
 
     log(f"warmup {args.warmup} steps")
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    warm_up(step, args, torch)
     n = routing["head_len"].cpu().numpy().astype(np.int64)
     Nr = B * T * K
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -315,9 +343,7 @@ def bench_grouped(w, args, torch, L, DI):
         L.route(logits, Kkv, L.GATE_SOFTMAX_SELECTED, out=routing, ws=rws)
         L.attn_fwd_grouped(q, k, v, routing, Kkv, w.rope_base, out=out, ws=aws)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    warm_up(step, args, torch)
     n = routing["head_len"].cpu().numpy().astype(np.int64)
     # Eq. app-group-prefill: every routed row of a group carries g queries
     c_attn = g * int((n * (n + 1) // 2).sum())
@@ -383,9 +409,7 @@ def bench_shared(w, args, torch, L, DI):
         L.attn_fwd(q, k, v, routing, K, w.rope_base, out=out, ws=aws)
         L.shared_attn(qs, ks, vs, win, w.rope_base, out=out, accumulate=True, ws=sws)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    warm_up(step, args, torch)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(args.steps):
@@ -445,9 +469,7 @@ def bench_backward(w, args, torch, L, DI):
         L.route_bwd(logits, routing, grads["dgates"])
 
     log(f"warmup {args.warmup} steps")
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    warm_up(step, args, torch)
     n = routing["head_len"].cpu().numpy().astype(np.int64)
     c_attn = int((n * (n + 1) // 2).sum())
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -507,7 +529,10 @@ def bench_decode(w, args, torch, L, DI):
         w = w.with_(H=w.H // g, K=w.K // g)
     log(f"prior head lengths for {w.name}")
     lengths = W.decode_prior_lengths(w)
-    cap = W.decode_cache_capacity(lengths, steps=args.warmup + 2 * args.steps + 1)
+    # room for every append: warm-up, settle (a decode step takes more than
+    # 0.4 ms, so settle_ms / 0.4 bounds the settle steps), timed and event-timed steps
+    cap = W.decode_cache_capacity(
+        lengths, steps=2 * args.warmup + 2 * args.steps + int(args.settle_ms / 0.4) + 8)
     log(f"filling caches on the device: 2 x [{w.B},{w.H},{cap},{w.d}] {w.dtype}")
     kc, vc = DI.decode_caches(w.B, w.H, cap, w.d, w.dtype, w.seed, w.qkv_scale, dev)
     step_in = W.decode_step_inputs(w)
@@ -532,7 +557,12 @@ def bench_decode(w, args, torch, L, DI):
             r = L.decode_step_grouped(logits, q, k, v, kc, vc, cache_len, K, w.rope_base, ws=ws)
             outd.update(r)
 
-    log(f"warmup {args.warmup} steps")
+    # warm-up, then settle with steps on a copy of the lengths, so the timed
+    # and the kernel-timed steps below append at known positions
+    log(f"warmup {args.warmup} steps, settle {args.settle_ms} ms")
+    len_start = cache_len.clone()
+    warm = warm_up(step, args, torch)
+    cache_len.copy_(len_start)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -580,7 +610,8 @@ def bench_decode(w, args, torch, L, DI):
                         "algorithmic_per_launch": {"kv_bytes": mean_bytes,
                                                    "rows": float(np.mean(rows[args.steps:]))},
                         "kernel_ms": round(kern_ms, 4)},
-           "tokens_per_s": round(B / (ms_step * 1e-3), 1)}
+           "tokens_per_s": round(B / (ms_step * 1e-3), 1),
+           "warmup_steps_run": warm + args.warmup, "settle_ms": args.settle_ms}
     if not args.no_cpu_baseline and g == 1:
         res["cpu_baseline"] = cpu_baseline_decode(w, step_in, kc, vc, len0, topk, args.cpu_budget, torch)
     del kc, vc
@@ -620,12 +651,43 @@ def cpu_baseline_decode(w, step_in, kc, vc, lengths, topk, budget_s, torch):
 
 
 # ----------------------------------------------------------------------------
+HEADLINE = 4          # skewed prefill: the largest prefill workload
+SUITE_OTHERS = (2, 3, 5)
+
+
+def bench_suite(args, torch, L, DI):
+    """The headline workload's line, with one object per other workload."""
+    if args.backward or args.shared or args.kv_group > 1:
+        raise SystemExit("--backward, --shared and --kv-group need --workload")
+    budget = args.cpu_budget
+    res = bench_prefill(W.WORKLOADS[HEADLINE], args, torch, L, DI)
+    torch.cuda.empty_cache()
+    others = {}
+    for n in SUITE_OTHERS:
+        w = W.WORKLOADS[n]
+        sub = argparse.Namespace(**vars(args))
+        sub.cpu_budget = min(budget, 8.0)
+        if w.decode:
+            sub.steps = max(1, min(args.steps, 20))
+            sub.warmup = max(1, min(args.warmup, 5))
+        r = (bench_decode if w.decode else bench_prefill)(w, sub, torch, L, DI)
+        torch.cuda.empty_cache()
+        keep = ("value", "unit", "ms_per_step", "steps", "warmup", "warmup_steps_run",
+                "settle_ms", "dtype", "config", "roofline", "kernels_ms", "tokens_per_s",
+                "cpu_baseline")
+        others[w.name] = {k: r[k] for k in keep if k in r}
+    res["workloads"] = others
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
-    ap.add_argument("--workload", type=int, default=2, choices=sorted(W.WORKLOADS))
+    ap.add_argument("--workload", type=int, default=None, choices=sorted(W.WORKLOADS),
+                    help="run one workload alone (default: the skewed prefill as the "
+                         "headline plus the balanced, head-scaling and decode workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kv-group", type=int, default=1,
                     help="key/value-group routing with groups of this many query heads "
@@ -636,6 +698,9 @@ def main():
     ap.add_argument("--backward", action="store_true",
                     help="time a training step (route, forward, backward) of a prefill "
                          "workload instead of the forward step")
+    ap.add_argument("--settle-ms", type=float, default=100.0,
+                    help="after the warm-up steps, further untimed steps until this much "
+                         "continuous GPU work has run (0: warm-up steps only)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle work for the CPU baseline sample")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -656,7 +721,8 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU only; the path is sharded by "
                           "batch or head across GPUs in design only", "n_gpus": args.gpus}))
         sys.exit(2)
-    w = W.WORKLOADS[args.workload]
+    suite = args.workload is None
+    w = W.WORKLOADS[HEADLINE if suite else args.workload]
     if args.steps is None:
         args.steps = 20 if w.decode else 50
     if args.warmup is None:
@@ -668,7 +734,9 @@ def main():
     from paper_2609_38832_amd import _lib as L
     from paper_2609_38832_amd import device_inputs as DI
     L.lib()
-    if args.backward:
+    if suite:
+        res = bench_suite(args, torch, L, DI)
+    elif args.backward:
         if w.decode:
             print(json.dumps({"error": "--backward needs a prefill workload"}))
             sys.exit(2)

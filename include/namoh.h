@@ -272,7 +272,7 @@ namoh_status namoh_decode_step_grouped(const float* logits, const void* q, const
                                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
- * Always-active shared heads (Sec. 5, "shared heads for local context"):
+ * Always-active shared heads (Sec. 4.4, "shared heads for local context"):
  * Hs heads outside the routing, each attending for every token either to
  * the full causal prefix (window = 0, or window >= T) or to the most recent
  * `window` tokens including the token itself (t - window < s <= t), with

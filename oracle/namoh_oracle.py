@@ -17,7 +17,7 @@ Mixture-of-Head"):
   replaces rho_i(t) by t.
 * Sec. 3.2, "Efficient execution": each (batch, head) subsequence is an
   independent packed sequence; decoding touches only the selected heads.
-* App. D.3 (NAMOH complexity), Eqs. (app-assignment-count),
+* App. B.5 (NAMOH complexity), Eqs. (app-assignment-count),
   (app-routed-kv), (app-routed-interactions): sum_i n_i = TK, M_KV = TK,
   A_KV = sum over the next token's heads of n_i, C_attn = 1/2 sum n_i(n_i+1).
 
@@ -49,7 +49,7 @@ Readings where the paper is silent (each also listed in the design notes):
   the H/g groups (same selection rule), all g query heads of a selected
   group attend over the group's subsequence with the group's gate, and RoPE
   uses the group-local rank for the queries and the shared key.
-* R18 always-active shared heads (Sec. 5, shared heads for local context):
+* R18 always-active shared heads (Sec. 4.4, shared heads for local context):
   H_s heads outside the routing attend, for every token, to the full causal
   prefix or to the most recent w original tokens including the token itself
   (t - w < s <= t), with RoPE at the global position; their outputs are
@@ -401,7 +401,7 @@ def combine_kv_groups(h_dense, topk_groups, gates, g):
 
 
 # ----------------------------------------------------------------------------
-# Always-active shared heads (Sec. 5, shared heads for local context), R18
+# Always-active shared heads (Sec. 4.4, shared heads for local context), R18
 
 def always_active_heads(q, k, v, window, rope_base, rope_mode=ROPE_GLOBAL, scale=None):
     """Outputs [B, Hs, T, d] of always-active heads: token t attends to
@@ -821,7 +821,7 @@ def brute_force_layer(logits, q, k, v, K, rope_base, rope_mode=ROPE_HEAD_RELATIV
 
 
 # ----------------------------------------------------------------------------
-# Cost accounting: App. D.3
+# Cost accounting: App. B.5
 
 def interaction_count(head_len) -> int:
     """C_attn = 1/2 sum_i n_i (n_i + 1) (Eq. app-routed-interactions)."""

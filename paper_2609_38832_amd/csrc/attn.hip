@@ -35,6 +35,7 @@
 
 #include "common.h"
 #include "internal.h"
+#include "launch.h"
 #include "tile.h"
 
 namespace namoh {
@@ -1252,32 +1253,28 @@ static void launch_mfma(const AttnWs& w, const void* q, const void* k, const voi
                         float scale_log2, const int32_t* seg_offsets, const int32_t* perm_token,
                         void* hout, bool hout_bf16, float* lse, hipStream_t st, int window = 0) {
   constexpr int NW = MfmaShape<D>::NW, NQT = MfmaShape<D>::NQT;
-  prof_mark("pack", true, st);
-  k_pack_kv<D><<<static_cast<unsigned>(1 + w.max_tiles), kPackThreads, 0, st>>>(
-      static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), log_base, w.freq,
-      seg_offsets,
-      perm_token, B * H, T, H, Nr, rope_mode, 32 * NQT * NW, static_cast<int>(w.max_items),
-      device_cu_count(), G, w.items, w.meta, w.Kp, w.Vt, w.knorm);
-  prof_mark("pack", false, st);
-  prof_mark("attn", true, st);
-  const unsigned grid = static_cast<unsigned>(w.max_items);
+  launch_k("pack", k_pack_kv<D>, dim3(static_cast<unsigned>(1 + w.max_tiles)), dim3(kPackThreads),
+           st, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), log_base, w.freq,
+           seg_offsets, perm_token, B * H, T, H, Nr, rope_mode, 32 * NQT * NW,
+           static_cast<int>(w.max_items), device_cu_count(), G, w.items, w.meta, w.Kp, w.Vt,
+           w.knorm);
+  const dim3 grid(static_cast<unsigned>(w.max_items)), block(NW * 64);
+  const uint16_t* q16 = static_cast<const uint16_t*>(q);
   if (window > 0 && hout_bf16)
-    k_attn_mfma<D, NQT, NW, true, true><<<grid, NW * 64, 0, st>>>(
-        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.freq, perm_token, w.items, w.meta,
-        w.knorm, T, H, G, rope_mode, scale_log2, hout, nullptr, window);
+    launch_k("attn", k_attn_mfma<D, NQT, NW, true, true>, grid, block, st, q16, w.Kp, w.Vt,
+             w.freq, perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout,
+             static_cast<float*>(nullptr), window);
   else if (window > 0)
-    k_attn_mfma<D, NQT, NW, false, true><<<grid, NW * 64, 0, st>>>(
-        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.freq, perm_token, w.items, w.meta,
-        w.knorm, T, H, G, rope_mode, scale_log2, hout, nullptr, window);
+    launch_k("attn", k_attn_mfma<D, NQT, NW, false, true>, grid, block, st, q16, w.Kp, w.Vt,
+             w.freq, perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout,
+             static_cast<float*>(nullptr), window);
   else if (hout_bf16)
-    k_attn_mfma<D, NQT, NW, true><<<grid, NW * 64, 0, st>>>(
-        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.freq, perm_token, w.items, w.meta,
-        w.knorm, T, H, G, rope_mode, scale_log2, hout, nullptr, 0);
+    launch_k("attn", k_attn_mfma<D, NQT, NW, true>, grid, block, st, q16, w.Kp, w.Vt, w.freq,
+             perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout,
+             static_cast<float*>(nullptr), 0);
   else
-    k_attn_mfma<D, NQT, NW, false><<<grid, NW * 64, 0, st>>>(
-        static_cast<const uint16_t*>(q), w.Kp, w.Vt, w.freq, perm_token, w.items, w.meta,
-        w.knorm, T, H, G, rope_mode, scale_log2, hout, lse, 0);
-  prof_mark("attn", false, st);
+    launch_k("attn", k_attn_mfma<D, NQT, NW, false>, grid, block, st, q16, w.Kp, w.Vt, w.freq,
+             perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout, lse, 0);
 }
 
 template <int D, bool BF16>
@@ -1285,10 +1282,8 @@ static void launch_generic(const AttnWs& w, const void* q, const void* k, const 
                            int T, int H, int rope_mode, float scale,
                            const int32_t* seg_offsets, const int32_t* perm_token,
                            float* hout, hipStream_t st) {
-  prof_mark("attn", true, st);
-  k_attn_generic<D, BF16><<<static_cast<unsigned>(w.max_items), 64, 0, st>>>(
-      q, k, v, w.table, perm_token, w.items, w.meta, T, H, rope_mode, scale, hout);
-  prof_mark("attn", false, st);
+  launch_k("attn", k_attn_generic<D, BF16>, dim3(static_cast<unsigned>(w.max_items)), dim3(64),
+           st, q, k, v, w.table, perm_token, w.items, w.meta, T, H, rope_mode, scale, hout);
 }
 
 hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
@@ -1344,20 +1339,19 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   const long BT = static_cast<long>(B) * T;
   const long threads = BT * (d / 8);
   const unsigned grid = static_cast<unsigned>((threads + kCombineThreads - 1) / kCombineThreads);
-  prof_mark("combine", true, st);
+  const dim3 cg(grid), cb(kCombineThreads);
   if (hb && out_dtype == 1)
-    (G == 1 ? k_combine<true, true, 1> : k_combine<true, true>)<<<grid, kCombineThreads, 0, st>>>(
-        hout, gates, slot_pos, BT, K, d, Nr, G, out);
+    launch_k("combine", G == 1 ? k_combine<true, true, 1> : k_combine<true, true>, cg, cb, st,
+             hout, gates, slot_pos, BT, K, d, Nr, G, out);
   else if (hb)
-    (G == 1 ? k_combine<true, false, 1> : k_combine<true, false>)<<<grid, kCombineThreads, 0, st>>>(
-        hout, gates, slot_pos, BT, K, d, Nr, G, out);
+    launch_k("combine", G == 1 ? k_combine<true, false, 1> : k_combine<true, false>, cg, cb, st,
+             hout, gates, slot_pos, BT, K, d, Nr, G, out);
   else if (out_dtype == 1)
-    (G == 1 ? k_combine<false, true, 1> : k_combine<false, true>)<<<grid, kCombineThreads, 0, st>>>(
-        hout, gates, slot_pos, BT, K, d, Nr, G, out);
+    launch_k("combine", G == 1 ? k_combine<false, true, 1> : k_combine<false, true>, cg, cb, st,
+             hout, gates, slot_pos, BT, K, d, Nr, G, out);
   else
-    (G == 1 ? k_combine<false, false, 1> : k_combine<false, false>)<<<grid, kCombineThreads, 0, st>>>(
-        hout, gates, slot_pos, BT, K, d, Nr, G, out);
-  prof_mark("combine", false, st);
+    launch_k("combine", G == 1 ? k_combine<false, false, 1> : k_combine<false, false>, cg, cb,
+             st, hout, gates, slot_pos, BT, K, d, Nr, G, out);
   return hipGetLastError();
 }
 
@@ -1376,7 +1370,7 @@ hipError_t launch_combine_rows(const uint16_t* rows, const float* gates, const i
 }
 
 // ---------------------------------------------------------------------------
-// Always-active shared heads (Sec. 5, shared heads for local context): every
+// Always-active shared heads (Sec. 4.4, shared heads for local context): every
 // (sequence, shared head) is one segment holding all T tokens in order (so
 // the rank is the global position), attended causally or inside a window of
 // `window` tokens, and the heads' outputs are added to the layer output.

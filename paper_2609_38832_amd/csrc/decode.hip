@@ -30,6 +30,7 @@
 
 #include "common.h"
 #include "internal.h"
+#include "launch.h"
 
 namespace namoh {
 
@@ -767,15 +768,15 @@ static hipError_t run_decode(const float* logits, const float* bias, const void*
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t grid = static_cast<size_t>(B) * K * nc;
-  prof_mark("decode_attn", true, st);
   if constexpr (BF16 && (GQ == 4 || GQ == 8))
-    k_decode_attn_mfma<D, GQ><<<static_cast<unsigned>(grid), 256, 0, st>>>(
-        static_cast<const uint16_t*>(k_cache), static_cast<const uint16_t*>(v_cache), topk_idx,
-        w.rows, w.qrot, H, K, cap, nc, w.part_acc, w.part_ml);
+    launch_k("decode_attn", k_decode_attn_mfma<D, GQ>, dim3(static_cast<unsigned>(grid)),
+             dim3(256), st, static_cast<const uint16_t*>(k_cache),
+             static_cast<const uint16_t*>(v_cache), topk_idx, w.rows, w.qrot, H, K, cap, nc,
+             w.part_acc, w.part_ml);
   else
-    k_decode_attn<D, BF16, GQ><<<static_cast<unsigned>(grid), 256, 0, st>>>(
-        k_cache, v_cache, topk_idx, w.rows, w.qrot, H, K, cap, nc, w.part_acc, w.part_ml);
-  prof_mark("decode_attn", false, st);
+    launch_k("decode_attn", k_decode_attn<D, BF16, GQ>, dim3(static_cast<unsigned>(grid)),
+             dim3(256), st, k_cache, v_cache, topk_idx, w.rows, w.qrot, H, K, cap, nc,
+             w.part_acc, w.part_ml);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (out_dtype == 1)
     k_decode_combine<D, true><<<B, 256, 0, st>>>(gates, w.rows, w.part_acc, w.part_ml, K, nc, out,

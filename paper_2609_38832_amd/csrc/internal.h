@@ -26,6 +26,9 @@ struct Carver {
 
 // ---- opt-in event timing (profile.cpp) ------------------------------------
 void prof_mark(const char* section, bool begin, hipStream_t st);
+// The next pair of events of `section` for a launch through hipExtLaunchKernel
+// (false, and null events, when timing is off or the section is full).
+bool prof_pair(const char* section, hipEvent_t* start, hipEvent_t* stop);
 
 // ---- routing (route.hip) -------------------------------------------------
 constexpr int kRouteChunk = 64;   // tokens per routing workgroup (one wave)

@@ -1,8 +1,11 @@
 // Opt-in kernel timing with HIP events (diagnostics; off by default).
 //
-// When enabled, the launchers bracket their dominant kernel of each call
-// with a pair of events on the call's stream.  Reading the results
-// synchronises on the recorded events.  Not safe for concurrent use from
+// When enabled, the launchers time their main kernels of each call with a
+// pair of events on the call's stream: either events attached to the kernel
+// dispatch itself (prof_pair, launched through hipExtLaunchKernel, so the
+// interval is the kernel's own start and end, as a kernel trace records
+// it), or events recorded before and after a group of launches (prof_mark).
+// Reading the results synchronises on the recorded events.  Not safe for concurrent use from
 // several host threads; enabling allocates events, so it is meant for
 // benchmarks, not for code that must not allocate.
 #include <hip/hip_runtime.h>
@@ -67,6 +70,21 @@ void prof_mark(const char* section, bool begin, hipStream_t st) {
     (void)hipEventRecord(e, st);
     ++s->used;
   }
+}
+
+bool prof_pair(const char* section, hipEvent_t* start, hipEvent_t* stop) {
+  *start = *stop = nullptr;
+  if (!g_prof.on) return false;
+  Section* s = g_prof.find(section, true);
+  if (s->used >= g_prof.capacity) return false;
+  hipEvent_t& a = s->start[s->used];
+  hipEvent_t& b = s->stop[s->used];
+  if (!a && hipEventCreate(&a) != hipSuccess) { a = nullptr; return false; }
+  if (!b && hipEventCreate(&b) != hipSuccess) { b = nullptr; return false; }
+  *start = a;
+  *stop = b;
+  ++s->used;
+  return true;
 }
 
 }  // namespace namoh

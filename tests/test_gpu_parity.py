@@ -2,10 +2,14 @@
 
 Routing and permutation indices are compared bit for bit; outputs within
 max abs 1e-4 (fp32) or 2e-2 + 1e-2*|ref| (bf16) of the float64 oracle.
-Full-size workloads compare every index and a sample of output rows that the
-oracle computes one token at a time; mid-sized cases (several tiles and
+Full-size workloads compare every index and every output row (against the
+gathered oracle run one segment at a time, plus a sample of rows that the
+oracle computes one token at a time); mid-sized cases (several tiles and
 ragged tails) compare every output.
 """
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 
@@ -267,6 +271,10 @@ MID = {
     "fp32_d64": W.WORKLOADS[2].with_(B=1, T=700, dtype="f32"),
     "fp32_d128": W.WORKLOADS[3].with_(T=600, H=8, dtype="f32"),
     "bf16_d32": W.WORKLOADS[1].with_(T=800, dtype="bf16"),
+    # more than 1024 (batch, head) segments: segment offsets read from global
+    # memory by the work list and the packing (not staged in LDS)
+    "many_segments_d64": W.WORKLOADS[2].with_(B=20, T=300, H=64, K=4),
+    "many_segments_d128": W.WORKLOADS[3].with_(B=20, T=300, K=4),
 }
 
 
@@ -452,7 +460,7 @@ def test_prefill_deterministic():
 
 
 # ----------------------------------------------------------------------------
-# prefill at the full workload sizes: every index, sampled output rows
+# prefill at the full workload sizes: every index and every output row
 
 class _Rows:
     """Lazy float64 view of a dense [B,H,T,d] input, converted per (b, h)."""
@@ -467,23 +475,58 @@ class _Rows:
         return self.cache[bh]
 
 
+def _oracle_by_segment(inp, w, ref):
+    """The gathered oracle (O2) run one (batch, head) segment at a time, each
+    segment's rows converted to float64 on their own (the whole float64
+    tensors of the long workloads would take gigabytes); segments run in a
+    thread pool (numpy releases the interpreter lock in its kernels)."""
+    off, perm = ref["seg_offsets"], ref["perm_token"]
+    hp = np.zeros((int(off[-1]), w.d))
+
+    def seg(sid):
+        b, h = divmod(sid, w.H)
+        a, e = int(off[sid]), int(off[sid + 1])
+        if e == a:
+            return
+        sub = {x: W.as_float64(inp[x][b:b + 1, h:h + 1], w.dtype) for x in ("q", "k", "v")}
+        hp[a:e] = O.attention_gathered(sub["q"], sub["k"], sub["v"], None,
+                                       np.array([0, e - a]), perm[a:e], 1, w.rope_base)
+
+    with ThreadPoolExecutor(max(1, min(16, len(os.sched_getaffinity(0))))) as ex:
+        list(ex.map(seg, range(w.B * w.H)))
+    return hp, O.combine_packed(hp, ref["slot_pos"], ref["gates"])
+
+
 @pytest.mark.parametrize("cfg", [2, 3, 4])
-def test_prefill_full_size_sampled(cfg):
+def test_prefill_full_size_elementwise(cfg):
+    # Every output row and every ungated head-output row of the full
+    # workload against the gathered oracle: all work items of the heaviest-
+    # first schedule, including the items past the resident workgroup slots
+    # and the reversed (serpentine) blocks of ranks.
     w = W.WORKLOADS[cfg]
-    say(f"prefill full size: {w.name}")
+    say(f"prefill full size, element-wise: {w.name}")
     inp = W.prefill_inputs(w)
-    got = run_prefill(w, inp)
     ref = _oracle_routing(inp, w)
+    # the benchmark's launch: bf16 output, head rows kept in bf16 inside
+    got = run_prefill(w, inp, out_dtype=torch.bfloat16)
     assert_routing_exact(got, ref)
-    assert np.isfinite(got["out"]).all()
+    hp, o = _oracle_by_segment(inp, w, ref)
+    e1 = check_out(got["out"], o, w.dtype)
+    # float32 head rows handed in by the caller
+    got2 = run_prefill(w, inp, head_out=True)
+    assert_routing_exact(got2, ref)
+    e2 = check_out(got2["head_out"], hp, w.dtype, "head_out")
+    e3 = check_out(got2["out"], o, w.dtype)
+    say(f"  max err out(bf16) {e1:.2e} head_out {e2:.2e} out(f32) {e3:.2e}")
+    # a sample of tokens from the one-token-at-a-time form, an independent
+    # evaluation of the same definition
     g = np.random.default_rng(cfg)
     for b in range(w.B):
-        toks = sorted(set([0, 1, w.T - 1] + list(g.choice(w.T, 13, replace=False))))
-        o, _ = O.prefill_rows(_Rows(inp["q"], w.dtype), _Rows(inp["k"], w.dtype),
-                              _Rows(inp["v"], w.dtype), ref["topk_idx"], ref["gates"],
-                              w.H, w.rope_base, b, toks)
-        e = check_out(got["out"][b, toks], o, w.dtype)
-        say(f"  b={b} sampled {len(toks)} tokens, max err {e:.2e}")
+        toks = sorted(set([0, 1, w.T - 1] + list(g.choice(w.T, 5, replace=False))))
+        o1, _ = O.prefill_rows(_Rows(inp["q"], w.dtype), _Rows(inp["k"], w.dtype),
+                               _Rows(inp["v"], w.dtype), ref["topk_idx"], ref["gates"],
+                               w.H, w.rope_base, b, toks)
+        check_out(got2["out"][b, toks], o1, w.dtype)
 
 
 # ----------------------------------------------------------------------------

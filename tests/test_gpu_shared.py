@@ -1,4 +1,4 @@
-"""GPU parity of always-active shared heads (Sec. 5, shared heads for local
+"""GPU parity of always-active shared heads (Sec. 4.4, shared heads for local
 context) through the C ABI, against the float64 oracle: full causal prefix
 or a sliding window of w tokens, global RoPE, outputs added to the routed
 layer output.  bf16 bound |got - ref| <= 2e-2 + 1e-2 |ref|, relative L2

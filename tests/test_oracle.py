@@ -1,7 +1,7 @@
 """Pins of the CPU oracle against what the paper and mathematics fix.
 
 Each test checks the oracle against something other than itself: values the
-paper prints for its worked example, closed forms of App. D.3, library
+paper prints for its worked example, closed forms of App. B.5, library
 routines (numpy stable sort, scipy softmax, torch scaled-dot-product
 attention), an independent complex-number form of RoPE, brute force with
 scalar loops, and invariants.  No GPU is touched.
@@ -91,7 +91,7 @@ def test_gates_K_equals_H_modes_agree():
 
 
 # ----------------------------------------------------------------------------
-# membership, ranks, permutation: worked example of Fig. 2 and App. D.3
+# membership, ranks, permutation: worked example of Fig. 2 and App. B.5
 
 def test_worked_example_fig2():
     fx = json.load(open(os.path.join(HERE, "golden", "worked_example_fig2.json")))
@@ -155,7 +155,7 @@ def test_kv_storage_unchanged_as_H_grows(H):
 
 
 # ----------------------------------------------------------------------------
-# visibility mask and interaction counts (Sec. 4.3, App. D.3)
+# visibility mask and interaction counts (Sec. 4.3, App. B.5)
 
 def _all_vis(m_b):
     T, H = m_b.shape
@@ -819,7 +819,7 @@ def test_kv_groups_brute_force_and_combine():
 
 
 # ----------------------------------------------------------------------------
-# always-active shared heads (Sec. 5, shared heads for local context)
+# always-active shared heads (Sec. 4.4, shared heads for local context)
 
 def _shared_case(seed, B=2, Hs=2, T=40, d=8):
     r = np.random.default_rng(seed)
