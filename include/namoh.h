@@ -406,6 +406,29 @@ namoh_status namoh_decode_step(const float* logits, const void* q,
                                int32_t* dev_status, void* workspace,
                                size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * namoh_decode_step for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same step, the same arguments and results, but no
+ * workspace argument.  The step's workspace lives in a fixed device array
+ * inside the library: NAMOH_DECODE_NOALLOC_SCRATCH_BYTES (32 MiB) per GPU,
+ * held from the first call on that GPU until the process ends.  Calls whose
+ * workspace would exceed it (namoh_decode_workspace_size(B, H, K, d_head,
+ * cap) > 32 MiB) return NAMOH_ERR_WORKSPACE and launch nothing.  Every call
+ * on one GPU uses that GPU's array: calls that overlap on one GPU (several
+ * streams or host threads) race, so serialise them.  The call allocates
+ * nothing; its first call on a device looks up the array's address there.
+ * ---------------------------------------------------------------------- */
+#define NAMOH_DECODE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+namoh_status namoh_decode_step_noalloc(const float* logits, const void* q, const void* k,
+                                       const void* v, int dtype, void* k_cache, void* v_cache,
+                                       int32_t* cache_len, const int32_t* seq_pos, int B, int H,
+                                       int K, int d_head, int cap, float rope_base, int rope_mode,
+                                       int gate_mode, float softmax_scale, int32_t* topk_idx,
+                                       float* gates, void* out, int out_dtype, int32_t* dev_status,
+                                       void* stream);
+
 /* The same step with loss-free balancing biases (App. "Auxiliary-Loss-Free
  * Balancing", Eq. namoh-biased-routing; the biases stay fixed during
  * inference): heads selected by float(a + b) and gated by the affinity a

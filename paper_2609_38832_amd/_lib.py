@@ -32,6 +32,7 @@ EXPORTED = (
     "namoh_attn_fwd_workspace_size", "namoh_attn_fwd",
     "namoh_prefill_cache", "namoh_attn_bwd_workspace_size", "namoh_attn_bwd", "namoh_route_bwd",
     "namoh_decode_workspace_size", "namoh_decode_step", "namoh_decode_step_biased",
+    "namoh_decode_step_noalloc",
     "namoh_qkv_proj", "namoh_out_proj_workspace_size", "namoh_out_proj",
     "namoh_attn_fwd_grouped_workspace_size", "namoh_attn_fwd_grouped",
     "namoh_shared_attn_workspace_size", "namoh_shared_attn",
@@ -62,6 +63,8 @@ _SIGS = {
     "namoh_decode_workspace_size": (_S, [_I, _I, _I, _I, _I]),
     "namoh_decode_step": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I,
                                _F, _I, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
+    "namoh_decode_step_noalloc": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I,
+                                       _F, _I, _I, _F, _P, _P, _P, _I, _P, _P]),
     "namoh_decode_step_biased": (_I, [_P, _P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I,
                                       _I, _F, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
     "namoh_attn_fwd_grouped_workspace_size": (_S, [_I, _I, _I, _I, _I, _I, _I]),
@@ -502,6 +505,28 @@ def decode_step(logits: torch.Tensor, q: torch.Tensor, k: torch.Tensor, v: torch
                                              dt, _ptr(k_cache), _ptr(v_cache), _ptr(cache_len),
                                              _ptr(seq_pos), B, H, K, d, cap, float(rope_base),
                                              rope_mode, *tail))
+    return out
+
+
+def decode_step_noalloc(logits: torch.Tensor, q: torch.Tensor, k: torch.Tensor,
+                        v: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                        cache_len: torch.Tensor, K: int, rope_base: float,
+                        rope_mode: int = ROPE_HEAD_RELATIVE,
+                        gate_mode: int = GATE_SOFTMAX_SELECTED, softmax_scale: float = 0.0,
+                        seq_pos: Optional[torch.Tensor] = None,
+                        dev_status: Optional[torch.Tensor] = None, out: dict = None) -> dict:
+    """namoh_decode_step_noalloc: the decode step without a workspace (the
+    library's fixed per-GPU scratch).  `out` holds caller-allocated
+    topk_idx [B, K] int32, gates [B, K] float32 and out [B, d]."""
+    _need_cuda(logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, dev_status,
+               out["topk_idx"], out["gates"], out["out"])
+    B, H, d = q.shape
+    cap = k_cache.shape[2]
+    check(lib().namoh_decode_step_noalloc(
+        _ptr(logits), _ptr(q), _ptr(k), _ptr(v), dtype_code(q.dtype), _ptr(k_cache),
+        _ptr(v_cache), _ptr(cache_len), _ptr(seq_pos), B, H, K, d, cap, float(rope_base),
+        rope_mode, gate_mode, float(softmax_scale), _ptr(out["topk_idx"]), _ptr(out["gates"]),
+        _ptr(out["out"]), dtype_code(out["out"].dtype), _ptr(dev_status), _stream(q.device)))
     return out
 
 

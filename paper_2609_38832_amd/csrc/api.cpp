@@ -508,9 +508,11 @@ static namoh_status decode_common(const float* logits, const float* bias, const 
                                   int rope_mode, int gate_mode, float softmax_scale,
                                   int32_t* topk_idx, float* gates, void* out, int out_dtype,
                                   int32_t* dev_status, void* workspace, size_t workspace_bytes,
-                                  void* stream, int group_size = 0) {
+                                  void* stream, int group_size = 0, bool noalloc = false) {
   // group_size 0: the per-head step; >= 1: key/value groups of that many
-  // query heads (namoh_decode_step_grouped)
+  // query heads (namoh_decode_step_grouped).  noalloc: the workspace is the
+  // library's fixed scratch (namoh_decode_step_noalloc), resolved after every
+  // other argument has been checked.
   namoh_status s;
   if ((s = check_sizes(B, 1, H, K)) != NAMOH_OK) return s;
   if ((s = check_head_width(d_head)) != NAMOH_OK) return s;
@@ -543,11 +545,20 @@ static namoh_status decode_common(const float* logits, const float* bias, const 
   REQUIRE_PTR(gates, 4);
   REQUIRE_PTR(out, 16);
   if (dev_status != nullptr) REQUIRE_PTR(dev_status, 4);
-  if ((s = check_workspace(workspace, workspace_bytes,
-                           namoh::decode_workspace_bytes(B, H, K, d_head, cap,
-                                                         group_size > 0 ? group_size : 1))) !=
-      NAMOH_OK)
-    return s;
+  const size_t need =
+      namoh::decode_workspace_bytes(B, H, K, d_head, cap, group_size > 0 ? group_size : 1);
+  if (noalloc) {
+    workspace_bytes = namoh::decode_scratch_bytes();
+    if (need > workspace_bytes)
+      return fail(NAMOH_ERR_WORKSPACE,
+                  "namoh_decode_step_noalloc: B=%d K=%d d_head=%d cap=%d needs %zu bytes of "
+                  "scratch, above its fixed %zu bytes (use namoh_decode_step with a workspace)",
+                  B, K, d_head, cap, need, workspace_bytes);
+    clear_hip_error();
+    const hipError_t e = namoh::decode_scratch(&workspace);
+    if (e != hipSuccess) return hip_status(e);
+  }
+  if ((s = check_workspace(workspace, workspace_bytes, need)) != NAMOH_OK) return s;
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
   clear_hip_error();
   if (group_size != 0)
@@ -573,6 +584,18 @@ namoh_status namoh_decode_step(const float* logits, const void* q, const void* k
                        H, K, d_head, cap, rope_base, rope_mode, gate_mode, softmax_scale,
                        topk_idx, gates, out, out_dtype, dev_status, workspace, workspace_bytes,
                        stream);
+}
+
+namoh_status namoh_decode_step_noalloc(const float* logits, const void* q, const void* k,
+                                       const void* v, int dtype, void* k_cache, void* v_cache,
+                                       int32_t* cache_len, const int32_t* seq_pos, int B, int H,
+                                       int K, int d_head, int cap, float rope_base, int rope_mode,
+                                       int gate_mode, float softmax_scale, int32_t* topk_idx,
+                                       float* gates, void* out, int out_dtype, int32_t* dev_status,
+                                       void* stream) {
+  return decode_common(logits, nullptr, q, k, v, dtype, k_cache, v_cache, cache_len, seq_pos, B,
+                       H, K, d_head, cap, rope_base, rope_mode, gate_mode, softmax_scale,
+                       topk_idx, gates, out, out_dtype, dev_status, nullptr, 0, stream, 0, true);
 }
 
 namoh_status namoh_decode_step_biased(const float* logits, const float* bias, const void* q,

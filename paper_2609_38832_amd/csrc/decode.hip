@@ -27,6 +27,7 @@
 //                          head h's caches; cache_len = the segment lengths.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "common.h"
 #include "internal.h"
@@ -598,6 +599,43 @@ static DecWs carve_dec(void* ws, int B, int K, int d, int cap, int G = 1) {
 
 size_t decode_workspace_bytes(int B, int /*H*/, int K, int d, int cap, int G) {
   return carve_dec(nullptr, B, K, d, cap, G).bytes;
+}
+
+// ---------------------------------------------------------------------------
+// Scratch of the decode step that allocates nothing (namoh_decode_step_noalloc):
+// the step's workspace (rotated queries, history lengths, per-chunk partials)
+// in a file-scope device array.  Every GPU the library runs on holds its own
+// copy for the life of the process; every call on one GPU uses that GPU's
+// copy, so calls that overlap on one GPU race.  Nothing in it needs to start
+// at zero: the append kernel writes every row length and rotated query the
+// attention reads, and each chunk writes the partial the combine reads.
+constexpr size_t kDecodeScratchBytes = static_cast<size_t>(32) << 20;
+static __device__ __attribute__((aligned(256))) unsigned char scratch[kDecodeScratchBytes];
+
+size_t decode_scratch_bytes() { return kDecodeScratchBytes; }
+
+// Device address of the array on the current device.  In host code the
+// array's name only stands in for the symbol; its device address comes from
+// hipGetSymbolAddress, taken once per device (with that device current) and
+// kept.
+hipError_t decode_scratch(void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  *ptr = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 // ---------------------------------------------------------------------------

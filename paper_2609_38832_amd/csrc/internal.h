@@ -105,6 +105,10 @@ hipError_t launch_decode(const float* logits, const float* bias, const void* q, 
                          int gate_mode, float scale, int32_t* topk_idx,
                          float* gates, void* out, int out_dtype,
                          int32_t* dev_status, void* ws, hipStream_t st);
+// The no-allocation decode step's scratch: its size, and the device address
+// of the current device's copy (resolved once per device).
+size_t decode_scratch_bytes();
+hipError_t decode_scratch(void** ptr);
 // bf16, d in {64, 128}, G in {1, 2, 4, 8} query heads per key/value head
 hipError_t launch_decode_grouped(const float* logits, const void* q, const void* k, const void* v,
                                  void* k_cache, void* v_cache, int32_t* cache_len,

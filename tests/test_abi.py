@@ -139,6 +139,37 @@ def test_decode_rejects(lib, kw, code):
     assert _dec(lib, **kw) == code
 
 
+def _dec_na(lib, B=2, H=8, K=2, d=64, cap=128, dtype=1, rope=0, kc=fake(4)):
+    return lib.namoh_decode_step_noalloc(fake(0), fake(1), fake(2), fake(3), dtype, kc, fake(5),
+                                         fake(6), None, B, H, K, d, cap, 1e4, rope, 0, 0.0,
+                                         fake(7), fake(8), fake(10), 0, None, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(cap=0), 1), (dict(d=16), 2), (dict(K=9), 1), (dict(rope=1), 1), (dict(kc=None), 1),
+    (dict(kc=P(A + 2)), 1),
+    # the step's workspace above the fixed scratch (64 sequences, 8 heads, d = 128, 70000 rows)
+    (dict(B=64, H=64, K=8, d=128, cap=70000), 3),
+])
+def test_decode_noalloc_rejects(lib, kw, code):
+    assert _dec_na(lib, **kw) == code
+    if code == 3:
+        assert "noalloc" in L.last_error() and "scratch" in L.last_error()
+
+
+def test_decode_noalloc_scratch_limit(lib):
+    # the decode workload's step (64 sequences, 8 of 64 heads, d = 128, about
+    # 17k rows of history) fits in the 32 MiB scratch; 70000 rows do not
+    assert lib.namoh_decode_workspace_size(64, 64, 8, 128, 17152) <= 32 << 20
+    assert lib.namoh_decode_workspace_size(64, 64, 8, 128, 70000) > 32 << 20
+
+
+def test_decode_noalloc_without_device(lib):
+    if _has_gpu():
+        pytest.skip("a GPU is visible")
+    assert _dec_na(lib) == 4     # valid arguments; no device to hold the scratch
+
+
 def _pcache(lib, dtype=1, B=2, T=64, H=8, K=2, d=64, base=1e4, rope=0, cap=64, k=fake(0),
             kc=fake(4), cl=fake(6), so=fake(2)):
     return lib.namoh_prefill_cache(k, fake(1), dtype, B, T, H, K, d, base, rope, so, fake(3),
