@@ -128,12 +128,50 @@ NAMOH_DEV int wave_bin_add(int* bins, int key, bool active) {
 // Offsets that are not a valid packing of Nr rows (out of order, a segment
 // longer than T, or not ending at Nr) produce an empty list.  The global
 // stores come last: a barrier after a store would wait for it.
+//
+// Key-range parts (split_slots > 0).  With `split_slots` resident workgroups,
+// a slot's fair share of the work is F = ceil(total key tiles / split_slots).
+// An item with more than F key tiles (and at least kSplitMinTiles) would
+// outlast the rest of the kernel on its compute unit, so it is cut into P
+// parts of at most L = ceil(w / P0) tiles (P0 = min(kSplitMaxParts,
+// ceil(w / F))), taken from the end of its key range (the last part holds
+// the diagonal tiles, every other part only keys before the block's first
+// query); each part writes an unnormalised partial (O, m, l) that
+// k_attn_merge combines.  Below kSplitMinTiles a part's fixed cost (query
+// gather, first tiles, partial rows) outweighs the balance it buys.  The
+// parts add at most split_slots items, at most 2 split_slots partial slots
+// and at most split_slots split items (sum of w over the split items is at
+// least (number of split items) F, and each adds at most w / F parts).
+constexpr int kSplitMinTiles = 32;
+constexpr int kSplitMaxParts = 8;
+
 struct SchedLds {
   int hist[kSortBins];
   int off[kSegLds + 1];
   int wmax[16], wbad[16];
   int wave[17];
+  long wsum[16];
+  int nparts, nsplit;
+  int cst[kSegLds + 1];   // first cell of each segment (cells enumerated segment by segment)
 };
+
+// A split item: the query block, its parts' partial slots [base, base + P).
+struct SplitItem {
+  int s, qb, seg0, n, qh, P, base, pad;
+};
+
+// Parts of an item of w key tiles with fair share F: count P, length L; part
+// p covers [max(0, w - (P - p) L), w - (P - 1 - p) L).
+NAMOH_DEV void split_parts(int w, int F, int& P, int& L) {
+  if (w > F && w >= kSplitMinTiles) {
+    const int P0 = min(kSplitMaxParts, (w + F - 1) / F);
+    L = (w + P0 - 1) / P0;
+    P = (w + L - 1) / L;
+  } else {
+    P = 1;
+    L = w;
+  }
+}
 
 // Serpentine placement: the hardware puts workgroup i on the compute unit of
 // workgroup i mod (number of compute units) as long as every unit has room,
@@ -154,7 +192,8 @@ template <int NT>
 NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, int T, int BM,
                              int Nr, int max_items, int period, int G,
                              WorkItem* __restrict__ items, int32_t* __restrict__ meta,
-                             SchedLds& L) {
+                             SchedLds& L, int split_slots = 0,
+                             SplitItem* __restrict__ splits = nullptr) {
   static_assert(NT % kWave == 0 && NT / kWave <= 16 && kSortBins % NT == 0, "block size");
   const int tid = thread_x();
   const int lane = tid % kWave, wave = tid / kWave;
@@ -163,6 +202,7 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
   if (in_lds)
     for (int i = tid; i <= BH; i += NT) L.off[i] = seg_offsets_g[i];
   for (int i = tid; i < kSortBins; i += NT) L.hist[i] = 0;
+  if (tid == 0) L.nparts = L.nsplit = 0;
   __syncthreads();
   const int32_t* off = in_lds ? L.off : seg_offsets_g;
   // validity and the longest segment
@@ -193,29 +233,108 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
     if (tid == 0) {
       meta[kMetaItems] = 0;
       meta[kMetaBad] = 1;
+      meta[kMetaSplit] = 0;
     }
     return;
   }
-  const int max_nqb = (maxn + BM - 1) / BM;
-  const long grid_items = static_cast<long>(max_nqb) * BH * G;
-  // grid cell g = (qb * BH + s) * G + u (u: query head of a key/value group,
-  // G = 1 without groups); the work key is the bin index (heaviest first)
-  auto cell = [&](long g, int& s, int& qb, int& u, int& seg0, int& n, int& key) {
-    const long c = g / G;
-    u = static_cast<int>(g - c * G);
-    qb = static_cast<int>(c / BH);
-    s = static_cast<int>(c - static_cast<long>(qb) * BH);
+  // The cells (segment, query block, query head u of a key/value group; G = 1
+  // without groups), w: a cell's key tiles.  With the segment table in LDS
+  // only the real cells are visited, numbered segment by segment (cst[s]: the
+  // first cell of segment s, found back by binary search), and ranked with
+  // one LDS atomic per lane: a wave's cells then hold distinct keys, which
+  // the atomics of one instruction serve together.  Otherwise, or when the
+  // full (query block, segment) grid holds at most twice the real cells, the
+  // grid is visited (cells past a segment's end inactive), in an order that
+  // gives a wave's cells a few shared keys, ranked by wave-aggregated atomics.
+  const long grid_cells = static_cast<long>((maxn + BM - 1) / BM) * BH * G;
+  bool compact = in_lds;
+  long ncells = grid_cells;
+  if (compact) {
+    constexpr int SPT = (kSegLds + NT - 1) / NT;
+    int cnt[SPT];
+    int csum = 0;
+#pragma unroll
+    for (int i = 0; i < SPT; ++i) {
+      const int sg = tid * SPT + i;
+      cnt[i] = sg < BH ? (off[sg + 1] - off[sg] + BM - 1) / BM * G : 0;
+      csum += cnt[i];
+    }
+    int ctot = 0;
+    int crun = block_exclusive_scan<NT>(csum, L.wave, ctot);
+#pragma unroll
+    for (int i = 0; i < SPT; ++i) {
+      const int sg = tid * SPT + i;
+      if (sg < BH) L.cst[sg] = crun;
+      crun += cnt[i];
+    }
+    __syncthreads();
+    // the grid when it holds at most twice the real cells (no search needed)
+    if (grid_cells > 2L * ctot) ncells = ctot;
+    else compact = false;
+  }
+  auto cell = [&](long g, int& s, int& qb, int& u, int& seg0, int& n, int& w) {
+    if (compact) {
+      int lo = 0, hi = BH - 1;   // the last segment whose first cell is at most g
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (L.cst[mid] <= g) lo = mid; else hi = mid - 1;
+      }
+      s = lo;
+      const int local = static_cast<int>(g) - L.cst[lo];
+      qb = G == 1 ? local : local / G;
+      u = local - qb * G;
+    } else {
+      const long c = g / G;
+      u = static_cast<int>(g - c * G);
+      qb = static_cast<int>(c / BH);
+      s = static_cast<int>(c - static_cast<long>(qb) * BH);
+    }
     seg0 = off[s];
     n = off[s + 1] - seg0;
-    const int w = min((n + kBN - 1) / kBN, (qb + 1) * per_qb);
-    key = kSortBins - 1 - min(w, kSortBins - 1);
+    w = min((n + kBN - 1) / kBN, (qb + 1) * per_qb);
     return qb * BM < n;
   };
-  for (long g0 = 0; g0 < grid_items; g0 += NT) {
+  // rank of an active lane's key among the cells placed so far
+  auto bin_add = [&](int key, bool act) {
+    if (compact) return act ? atomicAdd(&L.hist[key], 1) : 0;
+    return wave_bin_add(L.hist, key, act);
+  };
+  auto key_of = [](int tiles) { return kSortBins - 1 - min(tiles, kSortBins - 1); };
+  // the fair share of a slot (no parts without split_slots); a segment of
+  // nt key tiles and nq query blocks holds sum over q < nq of
+  // min(nt, per_qb (q + 1)) key tiles of work per query head
+  int F = 0x7fffffff;
+  if (split_slots > 0) {
+    long work = 0;
+    for (int sg = tid; sg < BH; sg += NT) {
+      const long n = off[sg + 1] - off[sg];
+      const long nt = (n + kBN - 1) / kBN, nq = (n + BM - 1) / BM;
+      const long m = min(nq, nt / per_qb);
+      work += per_qb * m * (m + 1) / 2 + (nq - m) * nt;
+    }
+    work *= G;
+    // exact 64-bit total: the bounds on parts and partial slots rest on it
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) work += __shfl_xor(work, o);
+    if (lane == 0) L.wsum[wave] = work;
+    __syncthreads();
+    long wtot = 0;
+#pragma unroll
+    for (int w = 0; w < NT / kWave; ++w) wtot += L.wsum[w];
+    F = static_cast<int>(min((wtot + split_slots - 1) / split_slots, 0x7fffffffL));
+    F = max(F, 1);
+  }
+  for (long g0 = 0; g0 < ncells; g0 += NT) {
     const long g = g0 + tid;
-    int sg = 0, qb = 0, u = 0, seg0 = 0, n = 0, key = 0;
-    const bool act = g < grid_items && cell(g, sg, qb, u, seg0, n, key);
-    wave_bin_add(L.hist, key, act);
+    int sg = 0, qb = 0, u = 0, seg0 = 0, n = 0, w = 0;
+    const bool act = g < ncells && cell(g, sg, qb, u, seg0, n, w);
+    int P = 1, Lp = w;
+    if (act) split_parts(w, F, P, Lp);
+    for (int p = 0; p < kSplitMaxParts; ++p) {
+      if (!__any(act && p < P)) break;
+      const int hi = w - (P - 1 - p) * Lp;
+      bin_add(key_of(hi - max(0, hi - Lp)), act && p < P);
+    }
   }
   __syncthreads();
   // exclusive scan of the histogram -> insertion cursors (heaviest first)
@@ -236,27 +355,52 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
   }
   __syncthreads();
   const int placed = min(total, max_items);
-  for (long g0 = 0; g0 < grid_items; g0 += NT) {
+  for (long g0 = 0; g0 < ncells; g0 += NT) {
     const long g = g0 + tid;
-    int sg = 0, qb = 0, u = 0, seg0 = 0, n = 0, key = 0;
-    const bool act = g < grid_items && cell(g, sg, qb, u, seg0, n, key);
-    const int rank = wave_bin_add(L.hist, key, act);
-    if (act && rank < placed) {
-      const int pos = serpentine(rank, placed, period);
-      WorkItem wi;
-      wi.s = sg;
-      wi.qb = qb;
-      wi.seg0 = seg0;
-      wi.n = n;
-      wi.tile0 = seg_tile0(seg0, sg);
-      wi.qh = u;
-      wi.pad1 = wi.pad2 = 0;
-      items[pos] = wi;
+    int sg = 0, qb = 0, u = 0, seg0 = 0, n = 0, w = 0;
+    const bool act = g < ncells && cell(g, sg, qb, u, seg0, n, w);
+    int P = 1, Lp = w;
+    if (act) split_parts(w, F, P, Lp);
+    int base = -1;
+    if (act && P > 1) {
+      base = atomicAdd(&L.nparts, P);
+      const int j = atomicAdd(&L.nsplit, 1);
+      SplitItem si;
+      si.s = sg;
+      si.qb = qb;
+      si.seg0 = seg0;
+      si.n = n;
+      si.qh = u;
+      si.P = P;
+      si.base = base;
+      si.pad = 0;
+      splits[j] = si;
+    }
+    for (int p = 0; p < kSplitMaxParts; ++p) {
+      if (!__any(act && p < P)) break;
+      const int hi = w - (P - 1 - p) * Lp;
+      const int lo = max(0, hi - Lp);
+      const int rank = bin_add(key_of(hi - lo), act && p < P);
+      if (act && p < P && rank < placed) {
+        const int pos = serpentine(rank, placed, period);
+        WorkItem wi;
+        wi.s = sg;
+        wi.qb = qb;
+        wi.seg0 = seg0;
+        wi.n = n;
+        wi.tile0 = seg_tile0(seg0, sg);
+        wi.qh = u | ((P > 1 ? base + p + 1 : 0) << kQhBits);
+        wi.kt_lo = lo;
+        wi.kt_hi = hi;
+        items[pos] = wi;
+      }
     }
   }
+  __syncthreads();
   if (tid == 0) {
     meta[kMetaItems] = placed;
     meta[kMetaBad] = 0;
+    meta[kMetaSplit] = L.nsplit;
   }
 }
 
@@ -330,7 +474,7 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
     const int32_t* __restrict__ perm_token, int BH, int T, int H, int Nr, int rope_mode,
     int BM, int max_items, int period, int G, WorkItem* __restrict__ items,
     int32_t* __restrict__ meta, uint16_t* __restrict__ Kp, uint16_t* __restrict__ Vt,
-    float* __restrict__ knorm) {
+    float* __restrict__ knorm, int split_slots, SplitItem* __restrict__ splits) {
   __shared__ __attribute__((aligned(16))) union {
     SchedLds sched;
     PackLds<D> pack;
@@ -339,7 +483,7 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
     // the rotation frequencies for the attention kernel, then the schedule
     if (thread_x() < D / 2) freq_out[thread_x()] = rope_freq_rev(thread_x(), D, log_base);
     attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, period, G, items, meta,
-                                L.sched);
+                                L.sched, split_slots, splits);
     return;
   }
   const int gt = block_x() - 1;
@@ -718,7 +862,7 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     const int32_t* __restrict__ perm_token, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ meta, const float* __restrict__ knorm, int T, int H, int G,
     int rope_mode, float scale_log2, void* __restrict__ hout, float* __restrict__ lse_out,
-    int window) {
+    int window, float* __restrict__ part_o, float* __restrict__ part_ml) {
   constexpr int BM = 32 * NQT * NW;
   constexpr int KS = D / 16;  // reduction steps of S^T = K Q^T
   constexpr int MT = D / 32;  // 32-row tiles of O^T
@@ -739,7 +883,10 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   const int n = it.n;
   const int tile0 = it.tile0;
   const int ntiles = (n + kBN - 1) / kBN;
-  const int kt_end = min(ntiles, (q0 + BM + kBN - 1) / kBN);
+  // key tiles of the item: the causal range, or a key-range part of it
+  // (kt_lo, kt_hi) whose unnormalised partial k_attn_merge combines
+  const int kt_end = WIN ? min(ntiles, (q0 + BM + kBN - 1) / kBN) : it.kt_hi;
+  const int part = (it.qh >> kQhBits) - 1;   // partial slot, -1 for a whole item
   const int tid = thread_x();
   const int wave = tid / 64, lane = tid % 64;
   const int c = lane & 31, g = lane >> 5;
@@ -747,13 +894,13 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   // all its rows are padding past the segment's end
   const int wq_last = q0 + 32 * ((NQT - 1) * NW + wave) + 31;
   const int wave_tiles = q0 + 32 * wave < n ? min(wq_last, n - 1) / kBN + 1 : 0;
-  // first key tile of the item and of this wave (0 without a window)
-  const int kb = WIN ? max(0, q0 - window + 1) / kBN : 0;
-  const int wave_first = WIN ? max(0, q0 + 32 * wave - window + 1) / kBN : 0;
+  // first key tile of the item and of this wave
+  const int kb = WIN ? max(0, q0 - window + 1) / kBN : it.kt_lo;
+  const int wave_first = WIN ? max(0, q0 + 32 * wave - window + 1) / kBN : kb;
   // query head of the item: head h of the key/value segment, or with key/value
   // groups of G query heads, head h * G + qh; its head outputs are row
   // (packed row) * G + qh
-  const int qh = it.qh;
+  const int qh = it.qh & ((1 << kQhBits) - 1);
   const size_t head_base = ((static_cast<size_t>(b) * H + h) * G + qh) * T;
 
   // token of each query row.  The tile loads below are invisible to the
@@ -770,7 +917,7 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   // across the wave after the query gather); four independent loads per
   // lane per round, all issued before the wait below
   float kmax = 0.f;
-  for (int i0 = 0; i0 < kt_end; i0 += 4 * kWave) {
+  for (int i0 = kb; i0 < kt_end; i0 += 4 * kWave) {
     float kv[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -925,12 +1072,35 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
       bool within = true;
 #pragma unroll
       for (int qt = 0; qt < NQT; ++qt) within &= qn[qt] <= m_run[qt] + kLazyLog2;
-      softmax_pv<D, NQT, NW, WIN>(S, O, m_run, l_run, minit, kt == 0, __all(within), sV[st],
+      softmax_pv<D, NQT, NW, WIN>(S, O, m_run, l_run, minit, kt == kb, __all(within), sV[st],
                                   kt * kBN, q0, wave, n, c, g, window, fresh);
     }
   }
 
   // ---- epilogue: normalise and store the packed head outputs -----------
+  if (!WIN && part >= 0) {
+    // a key-range part: unnormalised rows O, the running maximum m (log2
+    // units) and the row sum l, for k_attn_merge
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
+      const int ri = 32 * (qt * NW + wave) + c;   // row within the block
+      const float lsum = pair_sum32(l_run[qt]);
+      if (q0 + ri < n) {
+        float* const orow = part_o + (static_cast<size_t>(part) * BM + ri) * D;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            *reinterpret_cast<float4*>(orow + 32 * mt + 8 * j + 4 * g) =
+                make_float4(O[mt][qt][4 * j], O[mt][qt][4 * j + 1], O[mt][qt][4 * j + 2],
+                            O[mt][qt][4 * j + 3]);
+        if (g == 0)
+          *reinterpret_cast<float2*>(part_ml + (static_cast<size_t>(part) * BM + ri) * 2) =
+              make_float2(m_run[qt], lsum);
+      }
+    }
+    return;
+  }
   if constexpr (HB) {
     // bf16 rows go out through LDS: the accumulator layout gives each lane 8
     // bytes of 32 different rows per store, the staged layout 16 bytes of
@@ -995,6 +1165,78 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
             *reinterpret_cast<float4*>(static_cast<float*>(hout) + orow + 32 * mt + 8 * j + 4 * g) =
                 make_float4(O[mt][qt][4 * j] * inv, O[mt][qt][4 * j + 1] * inv,
                             O[mt][qt][4 * j + 2] * inv, O[mt][qt][4 * j + 3] * inv);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Merge of key-range parts (see attn_schedule): every row of a split item's
+// query block from its P partials (O_p unnormalised, m_p, l_p):
+//   M = max over p of m_p,  h = sum_p 2^(m_p - M) O_p / sum_p 2^(m_p - M) l_p,
+// written as the block's head-output row (bf16; or f32 with the row's
+// log-sum-exp M + log2 of the denominator).  Workgroups stride over the split
+// items; eight columns per thread.
+constexpr int kMergeThreads = 256;
+template <int D, bool HB>
+__global__ __launch_bounds__(kMergeThreads) void k_attn_merge(
+    const SplitItem* __restrict__ splits, const int32_t* __restrict__ meta,
+    const float* __restrict__ part_o, const float* __restrict__ part_ml, int BM, int G,
+    int nblocks, void* __restrict__ hout, float* __restrict__ lse_out) {
+  constexpr int TPR = D / 8;                   // threads per row
+  constexpr int RPP = kMergeThreads / TPR;     // rows per pass
+  const int nsplit = meta[kMetaSplit];
+  const int tid = thread_x();
+  const int sub = tid % TPR, rw = tid / TPR;
+  for (int j = block_x(); j < nsplit; j += nblocks) {
+    const SplitItem si = splits[j];
+    const int q0 = si.qb * BM;
+    const int rows = min(BM, si.n - q0);
+    const int P = min(si.P, kSplitMaxParts);
+    for (int r = rw; r < rows; r += RPP) {
+      float mp[kSplitMaxParts], lp[kSplitMaxParts];
+      float M = -INFINITY;
+#pragma unroll
+      for (int p = 0; p < kSplitMaxParts; ++p) {
+        mp[p] = 0.f;
+        lp[p] = 0.f;
+        if (p < P) {
+          const float2 ml = *reinterpret_cast<const float2*>(
+              part_ml + (static_cast<size_t>(si.base + p) * BM + r) * 2);
+          mp[p] = ml.x;
+          lp[p] = ml.y;
+          if (ml.y > 0.f) M = fmaxf(M, ml.x);
+        }
+      }
+      float acc[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+      float den = 0.f;
+#pragma unroll
+      for (int p = 0; p < kSplitMaxParts; ++p) {
+        if (p < P) {
+          const float wgt = lp[p] > 0.f ? __builtin_amdgcn_exp2f(mp[p] - M) : 0.f;
+          den = fmaf(wgt, lp[p], den);
+          const float4* src = reinterpret_cast<const float4*>(
+              part_o + (static_cast<size_t>(si.base + p) * BM + r) * D + 8 * sub);
+          const float4 a = src[0], b = src[1];
+          acc[0] = fmaf(wgt, a.x, acc[0]); acc[1] = fmaf(wgt, a.y, acc[1]);
+          acc[2] = fmaf(wgt, a.z, acc[2]); acc[3] = fmaf(wgt, a.w, acc[3]);
+          acc[4] = fmaf(wgt, b.x, acc[4]); acc[5] = fmaf(wgt, b.y, acc[5]);
+          acc[6] = fmaf(wgt, b.z, acc[6]); acc[7] = fmaf(wgt, b.w, acc[7]);
+        }
+      }
+      const float inv = den > 0.f ? 1.f / den : 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] *= inv;
+      const size_t row = static_cast<size_t>(si.seg0 + q0 + r) * G + si.qh;
+      if constexpr (HB) {
+        reinterpret_cast<uint4*>(static_cast<uint16_t*>(hout) + row * D)[sub] = pack8(acc);
+      } else {
+        float4* dst = reinterpret_cast<float4*>(static_cast<float*>(hout) + row * D + 8 * sub);
+        dst[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        dst[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+        if (lse_out != nullptr && sub == 0) lse_out[row] = M + log2f(den);
       }
     }
   }
@@ -1211,9 +1453,18 @@ struct AttnWs {
   float* knorm;
   double* freq;
   float* hpack;
+  SplitItem* splits;   // split items, at most split_slots
+  float* part_o;       // partial rows [2 split_slots][BM][d]
+  float* part_ml;      // partial (m, l) [2 split_slots][BM]
   size_t bytes;
   size_t max_items, max_tiles;
+  int split_slots;     // resident workgroups the fair share assumes (0: no parts)
 };
+
+// Resident workgroups of the MFMA attention on one MI355X (256 compute units
+// times the workgroups each holds): the count the key-range parts' fair share
+// and the workspace for them are sized with.
+constexpr int kSplitCUs = 256;
 
 // H, K: key/value heads (segments per sequence) and selected segments per
 // token; G query heads per key/value head (1 without groups).
@@ -1222,7 +1473,10 @@ static AttnWs carve_attn(void* ws, int B, int T, int H, int K, int d, int dtype,
   const size_t Nr = static_cast<size_t>(B) * T * K;
   const int BM = block_queries(d, dtype);
   AttnWs w;
-  w.max_items = (Nr / BM + BH + 1) * G;
+  w.split_slots = !use_mfma(d, dtype)
+                      ? 0
+                      : kSplitCUs * (d == 64 ? MfmaShape<64>::MINB : MfmaShape<128>::MINB);
+  w.max_items = (Nr / BM + BH + 1) * G + static_cast<size_t>(w.split_slots);
   w.max_tiles = Nr / kBN + BH + 1;
   Carver cv(ws);
   w.meta = cv.take<int32_t>(kMetaCount);
@@ -1239,6 +1493,10 @@ static AttnWs carve_attn(void* ws, int B, int T, int H, int K, int d, int dtype,
     w.freq = nullptr;
   }
   w.hpack = cv.take<float>(Nr * G * d);
+  const size_t ps = 2 * static_cast<size_t>(w.split_slots);
+  w.splits = cv.take<SplitItem>(static_cast<size_t>(w.split_slots));
+  w.part_o = cv.take<float>(ps * BM * d);
+  w.part_ml = cv.take<float>(ps * BM * 2);
   w.bytes = cv.off;
   return w;
 }
@@ -1251,30 +1509,46 @@ template <int D>
 static void launch_mfma(const AttnWs& w, const void* q, const void* k, const void* v,
                         int B, int T, int H, int G, int Nr, int rope_mode, double log_base,
                         float scale_log2, const int32_t* seg_offsets, const int32_t* perm_token,
-                        void* hout, bool hout_bf16, float* lse, hipStream_t st, int window = 0) {
+                        void* hout, bool hout_bf16, float* lse, hipStream_t st, int window = 0,
+                        bool split = false) {
   constexpr int NW = MfmaShape<D>::NW, NQT = MfmaShape<D>::NQT;
+  constexpr int BM = 32 * NQT * NW;
+  // key-range parts only for the whole-prefix forward (the window variant and
+  // the backward's work list keep whole items)
+  const int slots = split && window == 0 ? w.split_slots : 0;
   launch_k("pack", k_pack_kv<D>, dim3(static_cast<unsigned>(1 + w.max_tiles)), dim3(kPackThreads),
            st, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), log_base, w.freq,
-           seg_offsets, perm_token, B * H, T, H, Nr, rope_mode, 32 * NQT * NW,
+           seg_offsets, perm_token, B * H, T, H, Nr, rope_mode, BM,
            static_cast<int>(w.max_items), device_cu_count(), G, w.items, w.meta, w.Kp, w.Vt,
-           w.knorm);
+           w.knorm, slots, w.splits);
   const dim3 grid(static_cast<unsigned>(w.max_items)), block(NW * 64);
   const uint16_t* q16 = static_cast<const uint16_t*>(q);
+  float* const nof = nullptr;
   if (window > 0 && hout_bf16)
     launch_k("attn", k_attn_mfma<D, NQT, NW, true, true>, grid, block, st, q16, w.Kp, w.Vt,
              w.freq, perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout,
-             static_cast<float*>(nullptr), window);
+             nof, window, nof, nof);
   else if (window > 0)
     launch_k("attn", k_attn_mfma<D, NQT, NW, false, true>, grid, block, st, q16, w.Kp, w.Vt,
              w.freq, perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout,
-             static_cast<float*>(nullptr), window);
+             nof, window, nof, nof);
   else if (hout_bf16)
     launch_k("attn", k_attn_mfma<D, NQT, NW, true>, grid, block, st, q16, w.Kp, w.Vt, w.freq,
-             perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout,
-             static_cast<float*>(nullptr), 0);
+             perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout, nof, 0,
+             w.part_o, w.part_ml);
   else
     launch_k("attn", k_attn_mfma<D, NQT, NW, false>, grid, block, st, q16, w.Kp, w.Vt, w.freq,
-             perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout, lse, 0);
+             perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout, lse, 0,
+             w.part_o, w.part_ml);
+  if (slots > 0) {
+    constexpr int kMergeBlocks = 256;
+    if (hout_bf16)
+      launch_k("merge", k_attn_merge<D, true>, dim3(kMergeBlocks), dim3(kMergeThreads), st,
+               w.splits, w.meta, w.part_o, w.part_ml, BM, G, kMergeBlocks, hout, nof);
+    else
+      launch_k("merge", k_attn_merge<D, false>, dim3(kMergeBlocks), dim3(kMergeThreads), st,
+               w.splits, w.meta, w.part_o, w.part_ml, BM, G, kMergeBlocks, hout, lse);
+  }
 }
 
 template <int D, bool BF16>
@@ -1315,10 +1589,10 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
     const float sl2 = scale * 1.4426950408889634f;
     if (d == 64)
       launch_mfma<64>(w, q, k, v, B, T, H, G, Nr, rope_mode, log_base, sl2, seg_offsets,
-                      perm_token, hout, hb, nullptr, st);
+                      perm_token, hout, hb, nullptr, st, 0, true);
     else
       launch_mfma<128>(w, q, k, v, B, T, H, G, Nr, rope_mode, log_base, sl2, seg_offsets,
-                       perm_token, hout, hb, nullptr, st);
+                       perm_token, hout, hb, nullptr, st, 0, true);
   } else {
     if (G != 1) return hipErrorInvalidValue;   // key/value groups run on the MFMA path only
     k_attn_schedule<<<1, kPackThreads, 0, st>>>(seg_offsets, B * H, T, BM, Nr,

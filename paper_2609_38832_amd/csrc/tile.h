@@ -18,7 +18,7 @@ namespace namoh {
 
 constexpr int kBN = 64;            // keys per tile
 
-enum Meta { kMetaItems = 0, kMetaBad = 1, kMetaCount = 4 };
+enum Meta { kMetaItems = 0, kMetaBad = 1, kMetaSplit = 2, kMetaCount = 4 };
 
 // Packed key tiles of segment s (first packed row seg0, length n) are
 // numbered from seg_tile0 = floor(seg0 / 64) + s.  The ranges of successive
@@ -27,14 +27,18 @@ enum Meta { kMetaItems = 0, kMetaBad = 1, kMetaCount = 4 };
 // index stays below Nr / 64 + BH + 1, so no running sum is needed.
 NAMOH_DEV int seg_tile0(int seg0, int s) { return seg0 / kBN + s; }
 
-// One work item, a (segment, query block) pair with everything the attention
-// workgroup needs before its first load, so an item costs one dependent
-// global read.
+// One work item, a (segment, query block) pair, or one key-range part of
+// one, with everything the attention workgroup needs before its first load,
+// so an item costs one dependent global read.
 struct __attribute__((aligned(32))) WorkItem {
   int s, qb, seg0, n;            // segment b*H + h, query block, first packed row, length
-  int tile0, qh, pad1, pad2;     // first packed key tile of the segment; query head of
-                                 // the item within its key/value group (0 without groups)
+  int tile0;                     // first packed key tile of the segment
+  int qh;                        // bits 0-2: query head of the item within its key/value
+                                 // group (0 without groups); bits 3-: 1 + partial slot of a
+                                 // key-range part, 0 for a whole item
+  int kt_lo, kt_hi;              // key tiles [kt_lo, kt_hi) of the segment the item covers
 };
+constexpr int kQhBits = 3;
 
 // Work item of this workgroup, or false if it has none.  The record is read
 // together with the item count (the grid has max_items workgroups, so the
@@ -50,7 +54,8 @@ NAMOH_DEV bool my_item(const WorkItem* __restrict__ items, const int32_t* __rest
   it.n = __builtin_amdgcn_readfirstlane(v.n);
   it.tile0 = __builtin_amdgcn_readfirstlane(v.tile0);
   it.qh = __builtin_amdgcn_readfirstlane(v.qh);
-  it.pad1 = it.pad2 = 0;
+  it.kt_lo = __builtin_amdgcn_readfirstlane(v.kt_lo);
+  it.kt_hi = __builtin_amdgcn_readfirstlane(v.kt_hi);
   return block_x() < __builtin_amdgcn_readfirstlane(cnt);
 }
 
