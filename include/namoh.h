@@ -28,6 +28,9 @@
  *  - Workspace: query its size with the matching *_workspace_size() call;
  *    pass at least that many bytes, 256-byte aligned (NULL allowed when the
  *    size is 0).  Its contents need not be initialised and are garbage after.
+ *  - Debugging: with NAMOH_SYNC_CHECK=1 in the environment (read once per
+ *    process), every call that launched work synchronises its stream before
+ *    returning and reports an error of its kernels as NAMOH_ERR_HIP.
  */
 #ifndef NAMOH_H_
 #define NAMOH_H_

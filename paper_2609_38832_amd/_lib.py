@@ -15,7 +15,9 @@ from typing import Optional
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libnamoh.so")
+# NAMOH_LIB selects another build of the same library (the host-sanitizer
+# build the CPU tests use); by default the in-tree libnamoh.so
+LIB_PATH = os.environ.get("NAMOH_LIB") or os.path.join(_HERE, "libnamoh.so")
 
 NAMOH_OK = 0
 NAMOH_ERR_INVALID_ARG = 1

@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 
 #include "../../include/namoh.h"
@@ -76,6 +77,28 @@ namoh_status hip_status(hipError_t e) {
   return fail(NAMOH_ERR_HIP, "HIP error %d: %s", static_cast<int>(e), hipGetErrorString(e));
 }
 
+// NAMOH_SYNC_CHECK=1 in the environment (read once): every call that
+// launched work synchronises its stream and reports an asynchronous error of
+// its kernels as NAMOH_ERR_HIP (debugging aid; the calls otherwise never
+// synchronise).
+bool sync_check_on() {
+  static const bool on = [] {
+    const char* v = std::getenv("NAMOH_SYNC_CHECK");
+    return v != nullptr && v[0] != '\0' && v[0] != '0';
+  }();
+  return on;
+}
+
+// Status of a call whose launches returned e.
+namoh_status launched(void* stream, hipError_t e) {
+  if (e != hipSuccess || !sync_check_on()) return hip_status(e);
+  const hipError_t se = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+  if (se != hipSuccess)
+    return fail(NAMOH_ERR_HIP, "NAMOH_SYNC_CHECK: error in the call's kernels: HIP error %d: %s",
+                static_cast<int>(se), hipGetErrorString(se));
+  return ok();
+}
+
 // Clears a sticky error left by an earlier unrelated call so that the
 // launches below report their own status.
 void clear_hip_error() { (void)hipGetLastError(); }
@@ -124,7 +147,7 @@ namoh_status namoh_route(const float* logits, int B, int T, int H, int K,
                            namoh::route_workspace_bytes(B, T, H, K))) != NAMOH_OK)
     return s;
   clear_hip_error();
-  return hip_status(namoh::launch_route(logits, nullptr, B, T, H, K, gate_mode, topk_idx, gates,
+  return launched(stream, namoh::launch_route(logits, nullptr, B, T, H, K, gate_mode, topk_idx, gates,
                                         head_len, seg_offsets, perm_token, slot_pos,
                                         workspace, static_cast<hipStream_t>(stream)));
 }
@@ -147,7 +170,7 @@ namoh_status namoh_route_biased(const float* logits, const float* bias, int B, i
                            namoh::route_workspace_bytes(B, T, H, K))) != NAMOH_OK)
     return s;
   clear_hip_error();
-  return hip_status(namoh::launch_route(logits, bias, B, T, H, K, NAMOH_GATE_SOFTMAX_ALL,
+  return launched(stream, namoh::launch_route(logits, bias, B, T, H, K, NAMOH_GATE_SOFTMAX_ALL,
                                         topk_idx, gates, head_len, seg_offsets, perm_token,
                                         slot_pos, workspace, static_cast<hipStream_t>(stream)));
 }
@@ -160,7 +183,7 @@ namoh_status namoh_route_bias_update(const int32_t* head_len, int B, int T, int 
   REQUIRE_PTR(head_len, 4);
   REQUIRE_PTR(bias, 4);
   clear_hip_error();
-  return hip_status(namoh::launch_route_bias_update(head_len, B, T, H, K, eta, bias,
+  return launched(stream, namoh::launch_route_bias_update(head_len, B, T, H, K, eta, bias,
                                                     static_cast<hipStream_t>(stream)));
 }
 
@@ -213,7 +236,7 @@ namoh_status namoh_attn_fwd(const void* q, const void* k, const void* v, int dty
     return s;
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
   clear_hip_error();
-  return hip_status(namoh::launch_attn(q, k, v, dtype, B, T, H, K, d_head, rope_base, rope_mode,
+  return launched(stream, namoh::launch_attn(q, k, v, dtype, B, T, H, K, d_head, rope_base, rope_mode,
                                        scale, gates, seg_offsets, perm_token, slot_pos, out,
                                        out_dtype, head_out, workspace,
                                        static_cast<hipStream_t>(stream)));
@@ -243,7 +266,7 @@ namoh_status namoh_prefill_cache(const void* k, const void* v, int dtype, int B,
   REQUIRE_PTR(v_cache, 16);
   REQUIRE_PTR(cache_len, 4);
   clear_hip_error();
-  return hip_status(namoh::launch_prefill_cache(k, v, dtype, B, T, H, K, d_head, rope_base,
+  return launched(stream, namoh::launch_prefill_cache(k, v, dtype, B, T, H, K, d_head, rope_base,
                                                 rope_mode, seg_offsets, perm_token, k_cache,
                                                 v_cache, cache_len, cap,
                                                 static_cast<hipStream_t>(stream)));
@@ -297,7 +320,7 @@ namoh_status namoh_shared_attn(const void* q, const void* k, const void* v, int 
     return s;
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
   clear_hip_error();
-  return hip_status(namoh::launch_shared(q, k, v, B, T, Hs, d_head, window, rope_base,
+  return launched(stream, namoh::launch_shared(q, k, v, B, T, Hs, d_head, window, rope_base,
                                          rope_mode == NAMOH_ROPE_NONE ? 2 : 1, scale, out,
                                          out_dtype, accumulate, head_out, workspace,
                                          static_cast<hipStream_t>(stream)));
@@ -354,7 +377,7 @@ namoh_status namoh_attn_fwd_grouped(const void* q, const void* k, const void* v,
     return s;
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
   clear_hip_error();
-  return hip_status(namoh::launch_attn(q, k, v, dtype, B, T, H_kv, K_kv, d_head, rope_base,
+  return launched(stream, namoh::launch_attn(q, k, v, dtype, B, T, H_kv, K_kv, d_head, rope_base,
                                        rope_mode, scale, gates, seg_offsets, perm_token,
                                        slot_pos, out, out_dtype, head_out, workspace,
                                        static_cast<hipStream_t>(stream), group_size));
@@ -388,7 +411,7 @@ namoh_status namoh_qkv_proj(const void* x, const void* w_qkv, int B, int T, int 
   REQUIRE_PTR(k, 16);
   REQUIRE_PTR(v, 16);
   clear_hip_error();
-  return hip_status(namoh::launch_qkv_proj(x, w_qkv, B, T, H, K, d_head, d_model, seg_offsets,
+  return launched(stream, namoh::launch_qkv_proj(x, w_qkv, B, T, H, K, d_head, d_model, seg_offsets,
                                            perm_token, q, k, v, static_cast<hipStream_t>(stream)));
 }
 
@@ -417,7 +440,7 @@ namoh_status namoh_out_proj(const void* head_out, int head_out_dtype, const void
                            namoh::out_proj_workspace_bytes(B, T, H, K, d_head, d_model))) != NAMOH_OK)
     return s;
   clear_hip_error();
-  return hip_status(namoh::launch_out_proj(head_out, head_out_dtype, w_o, gates, slot_pos,
+  return launched(stream, namoh::launch_out_proj(head_out, head_out_dtype, w_o, gates, slot_pos,
                                            seg_offsets, B, T, H, K, d_head, d_model, out,
                                            out_dtype, workspace,
                                            static_cast<hipStream_t>(stream)));
@@ -463,7 +486,7 @@ namoh_status namoh_attn_bwd(const void* q, const void* k, const void* v, int dty
     return s;
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
   clear_hip_error();
-  return hip_status(namoh::launch_attn_bwd(q, k, v, dtype, B, T, H, K, d_head, rope_base,
+  return launched(stream, namoh::launch_attn_bwd(q, k, v, dtype, B, T, H, K, d_head, rope_base,
                                            rope_mode, scale, topk_idx, gates, seg_offsets,
                                            perm_token, dout, dq, dk, dv, dgates, workspace,
                                            static_cast<hipStream_t>(stream)));
@@ -482,7 +505,7 @@ namoh_status namoh_route_bwd(const float* logits, const int32_t* topk_idx, const
   REQUIRE_PTR(dgates, 4);
   REQUIRE_PTR(dlogits, 4);
   clear_hip_error();
-  return hip_status(namoh::launch_route_bwd(logits, topk_idx, gates, dgates, B, T, H, K,
+  return launched(stream, namoh::launch_route_bwd(logits, topk_idx, gates, dgates, B, T, H, K,
                                             gate_mode, dlogits,
                                             static_cast<hipStream_t>(stream)));
 }
@@ -562,11 +585,11 @@ static namoh_status decode_common(const float* logits, const float* bias, const 
   const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
   clear_hip_error();
   if (group_size != 0)
-    return hip_status(namoh::launch_decode_grouped(
+    return launched(stream, namoh::launch_decode_grouped(
         logits, q, k, v, k_cache, v_cache, cache_len, seq_pos, B, H, K, group_size, d_head, cap,
         rope_base, rope_mode, gate_mode, scale, topk_idx, gates, out, out_dtype, dev_status,
         workspace, static_cast<hipStream_t>(stream)));
-  return hip_status(namoh::launch_decode(logits, bias, q, k, v, dtype, k_cache, v_cache,
+  return launched(stream, namoh::launch_decode(logits, bias, q, k, v, dtype, k_cache, v_cache,
                                          cache_len, seq_pos, B, H, K, d_head, cap, rope_base,
                                          rope_mode, gate_mode, scale, topk_idx, gates, out,
                                          out_dtype, dev_status, workspace,

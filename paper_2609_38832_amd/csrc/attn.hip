@@ -40,48 +40,18 @@
 
 namespace namoh {
 
-// mfma kernel shape: waves per workgroup and 32-query sub-tiles per wave
-#ifndef NAMOH_D64_NW
-#define NAMOH_D64_NW 4
-#endif
-#ifndef NAMOH_D64_NQT
-#define NAMOH_D64_NQT 1
-#endif
-#ifndef NAMOH_D128_NW
-#define NAMOH_D128_NW 4
-#endif
-#ifndef NAMOH_D128_NQT
-#define NAMOH_D128_NQT 1
-#endif
-#ifndef NAMOH_D64_MINB
-#define NAMOH_D64_MINB 4
-#endif
-#ifndef NAMOH_D128_MINB
-#define NAMOH_D128_MINB 2
-#endif
-// NW waves per workgroup, NQT 32-query sub-tiles per wave, MINB workgroups
-// per compute unit the register allocation must allow.
-#ifndef NAMOH_D64_VPRE
-#define NAMOH_D64_VPRE 0
-#endif
-#ifndef NAMOH_D128_VPRE
-#define NAMOH_D128_VPRE 2
-#endif
-#ifndef NAMOH_D64_NS
-#define NAMOH_D64_NS 2
-#endif
-#ifndef NAMOH_D128_NS
-#define NAMOH_D128_NS 2
-#endif
-// NS key/value tile stages in LDS (NS - 1 tiles in flight while one is used).
+// MFMA kernel shape: NW waves per workgroup, NQT 32-query sub-tiles per wave,
+// MINB workgroups per compute unit the register allocation must allow, NS
+// key/value tile stages in LDS (NS - 1 tiles in flight while one is used),
+// VPRE 16-key steps of value operands read from LDS while the softmax runs
+// (the rest while the first P.V products execute; d = 128 reads half early
+// to stay within 256 registers).
 template <int D> struct MfmaShape;
 template <> struct MfmaShape<64> {
-  static constexpr int NW = NAMOH_D64_NW, NQT = NAMOH_D64_NQT, MINB = NAMOH_D64_MINB,
-                       NS = NAMOH_D64_NS;
+  static constexpr int NW = 4, NQT = 1, MINB = 4, NS = 2, VPRE = 0;
 };
 template <> struct MfmaShape<128> {
-  static constexpr int NW = NAMOH_D128_NW, NQT = NAMOH_D128_NQT, MINB = NAMOH_D128_MINB,
-                       NS = NAMOH_D128_NS;
+  static constexpr int NW = 4, NQT = 1, MINB = 2, NS = 2, VPRE = 2;
 };
 // The running softmax maximum (log2 units) is only raised when a tile
 // exceeds it by more than kLazyLog2 (probabilities then stay below
@@ -626,32 +596,6 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
   }
 }
 
-// 1: all key-operand LDS reads of a tile are issued before its first MFMA.
-#ifndef NAMOH_QK_PREREAD
-#define NAMOH_QK_PREREAD 0
-#endif
-// Wave priority around the matrix-core blocks (s_setprio; 0 = unchanged).
-#ifndef NAMOH_PRIO_QK
-#define NAMOH_PRIO_QK 0
-#endif
-#ifndef NAMOH_PRIO_PV
-#define NAMOH_PRIO_PV 0
-#endif
-template <int P>
-NAMOH_DEV void wave_prio() {
-  if constexpr (P > 0) {
-    __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_setprio(P);
-  }
-}
-template <int P>
-NAMOH_DEV void wave_prio_reset() {
-  if constexpr (P > 0) {
-    __builtin_amdgcn_s_setprio(0);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-}
-
 // S^T = K Q^T for one 64-key tile: 2 key sub-tiles x NQT query sub-tiles.
 // All LDS operand reads of the tile are issued before the first MFMA (the
 // scheduling barrier keeps them there), so LDS latency is paid once per tile
@@ -669,10 +613,6 @@ NAMOH_DEV void qk_tile(f32x16 (&S)[2][NQT], const uint16_t* __restrict__ sKb,
       const int row = 32 * kk + c;
       a[ks][kk] = *reinterpret_cast<const bf16x8*>(&sKb[row * D + swz<D / 8>(row, 2 * ks + g) * 8]);
     }
-#if NAMOH_QK_PREREAD
-  __builtin_amdgcn_sched_barrier(0);
-#endif
-  wave_prio<NAMOH_PRIO_QK>();
   // the accumulators start at -m (the query's running maximum), so the
   // scores leave the products already shifted
 #pragma unroll
@@ -687,7 +627,6 @@ NAMOH_DEV void qk_tile(f32x16 (&S)[2][NQT], const uint16_t* __restrict__ sKb,
 #pragma unroll
       for (int qt = 0; qt < NQT; ++qt)
         S[kk][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][kk], qB[qt][ks], S[kk][qt], 0, 0, 0);
-  wave_prio_reset<NAMOH_PRIO_QK>();
 }
 
 // Mask, online softmax and O^T += V^T P^T for one 64-key tile.
@@ -712,7 +651,7 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
   // value operands: the first VPRE 16-key steps are read while the softmax
   // runs (all of them for d = 64; half for d = 128, to stay within 256
   // registers), the rest while the first P.V products execute
-  constexpr int VPRE = D == 128 ? NAMOH_D128_VPRE : NAMOH_D64_VPRE;
+  constexpr int VPRE = MfmaShape<D>::VPRE;
   bf16x8 va[4][D / 32];
   auto vread = [&](int k2) {
 #pragma unroll
@@ -833,7 +772,6 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
   }
 #pragma unroll
   for (int k2 = VPRE; k2 < 4; ++k2) vread(k2);
-  wave_prio<NAMOH_PRIO_PV>();
 #pragma unroll
   for (int k2 = 0; k2 < 4; ++k2)
 #pragma unroll
@@ -841,7 +779,6 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
 #pragma unroll
       for (int qt = 0; qt < NQT; ++qt)
         O[mt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[k2][mt], pB[qt][k2], O[mt][qt], 0, 0, 0);
-  wave_prio_reset<NAMOH_PRIO_PV>();
 }
 
 // ---------------------------------------------------------------------------

@@ -314,12 +314,21 @@ __global__ __launch_bounds__(256) void k_decode_attn(
 // v_mfma_f32_16x16x32_bf16 (lane l: A row / B column / C column l % 16,
 // reduction slots 8 (l / 16) .. + 7; C rows 4 (l / 16) + i in accumulator
 // i):
+//   the block's key and value rows are loaded whole (each lane a 16-byte
+//     granule of D / 16 consecutive rows: coalesced 16-byte loads) and
+//     rearranged through wave-private LDS: key rows row-major with padded
+//     rows (s_k), and each lane's run of rows of one column written as one
+//     run of a V^T row (s_vt); the next block's loads are issued before the
+//     current block is processed;
 //   S[q][r] = Q K^T for two 16-row tiles: A = the GQ rotated queries (rows
-//     >= GQ zero), B = the cached key rows, loaded straight from the cache;
+//     >= GQ zero), B = the key rows read back from s_k;
 //   online softmax per query in exp2 units: the 16 lanes of one reduction
 //     group hold a query's 16 scores of a tile;
-//   O[q][d] += P V over the 32 rows: A = P and B = V^T read from wave-private
-//     LDS tiles (P as [query][row], V^T as [d][row], both 16-byte reads).
+//   O[q][d] += P V over the 32 rows: A = P and B = V^T read from the
+//     wave-private LDS tiles (P as [query][row], V^T as [d][row], both
+//     16-byte reads).
+// LDS: about 81 KB per workgroup at D = 128, so the two workgroups per
+// compute unit that the launch bounds ask for fill its 160 KB.
 // The reduction group kg = l / 16 of every layout holds queries 4 kg .. 4 kg
 // + 3, so a lane's rescale factors apply to its own output accumulators.
 // Partials as in k_decode_attn: (bk * GQ + q) * nchunk + chunk.
