@@ -459,14 +459,20 @@ def bench_backward(w, args, torch, L, DI):
     bws = L.workspace(int(L.lib().namoh_attn_bwd_workspace_size(B, T, H, K, d)), dev)
     out = torch.empty(B, T, d, dtype=q.dtype, device=dev)
     f32 = dict(dtype=torch.float32, device=dev)
-    grads = {"dq": torch.empty(B, H, T, d, **f32), "dk": torch.empty(B, H, T, d, **f32),
+    Nr = B * T * K
+    # gradients of the routed pairs in the routing's packed order (what a
+    # routed projection's backward consumes); the dense form is timed beside
+    grads = {"dq": torch.empty(Nr, d, **f32), "dk": torch.empty(Nr, d, **f32),
+             "dv": torch.empty(Nr, d, **f32), "dgates": torch.empty(B, T, K, **f32)}
+    dense = {"dq": torch.empty(B, H, T, d, **f32), "dk": torch.empty(B, H, T, d, **f32),
              "dv": torch.empty(B, H, T, d, **f32), "dgates": torch.empty(B, T, K, **f32)}
 
-    def step():
+    def step(packed=True):
         L.route(logits, K, L.GATE_SOFTMAX_SELECTED, out=routing, ws=rws)
         L.attn_fwd(q, k, v, routing, K, w.rope_base, L.ROPE_HEAD_RELATIVE, out=out, ws=aws)
-        L.attn_bwd(q, k, v, routing, K, w.rope_base, dout, ws=bws, out=grads)
-        L.route_bwd(logits, routing, grads["dgates"])
+        g = grads if packed else dense
+        L.attn_bwd(q, k, v, routing, K, w.rope_base, dout, ws=bws, out=g, packed=packed)
+        L.route_bwd(logits, routing, g["dgates"])
 
     log(f"warmup {args.warmup} steps")
     warm_up(step, args, torch)
@@ -480,6 +486,14 @@ def bench_backward(w, args, torch, L, DI):
     e1.record()
     torch.cuda.synchronize()
     ms_step = e0.elapsed_time(e1) / args.steps
+    for _ in range(args.warmup):
+        step(packed=False)
+    e0.record()
+    for _ in range(args.steps):
+        step(packed=False)
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step_dense = e0.elapsed_time(e1) / args.steps
     L.profile_enable(2 * args.steps)
     for _ in range(args.steps):
         step()
@@ -505,8 +519,10 @@ def bench_backward(w, args, torch, L, DI):
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": w.dtype, "data": "synthetic",
+           "ms_per_step_dense_grads": round(ms_step_dense, 4),
            "config": {"workload": w.name, "B": B, "T": T, "H": H, "K": K, "d_head": d,
-                      "pass": "training step", "rope": "head-relative",
+                      "pass": "training step", "gradients": "packed (routed pairs)",
+                      "rope": "head-relative",
                       "rope_base": w.rope_base, "gates": "softmax over selected"},
            "roofline": {"kernel": "k_bwd_dq + k_bwd_dkdv" if mfma else "k_bwd_q + k_bwd_kv",
                         "bound": "mfma" if mfma else "alu", "achieved": round(achieved, 2),

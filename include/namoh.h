@@ -198,6 +198,21 @@ namoh_status namoh_attn_bwd(const void* q, const void* k, const void* v, int dty
                             float* dk, float* dv, float* dgates, void* workspace,
                             size_t workspace_bytes, void* stream);
 
+/* The same backward with the gradients of the routed (token, head) pairs
+ * only, in the routing's packed order: dq, dk, dv float32 [B*T*K, d], row
+ * seg_offsets[b*H + h] + rho of the pair (token perm_token[row], head h);
+ * that is the layout a routed projection's backward consumes (Sec. 3.1,
+ * Eq. namoh-qkv: only routed pairs are projected), and it needs no zero fill
+ * of the unrouted rows.  Same inputs, workspace and limits as
+ * namoh_attn_bwd; dgates as there. */
+namoh_status namoh_attn_bwd_packed(const void* q, const void* k, const void* v, int dtype,
+                                   int B, int T, int H, int K, int d_head, float rope_base,
+                                   int rope_mode, float softmax_scale, const int32_t* topk_idx,
+                                   const float* gates, const int32_t* seg_offsets,
+                                   const int32_t* perm_token, const float* dout, float* dq,
+                                   float* dk, float* dv, float* dgates, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
 /* Gradient of the gates with respect to the router logits, the selection
  * held fixed (Sec. 3.1, Eq. namoh-gates; the router learns through the
  * gates).  gate_mode SOFTMAX_SELECTED: dl_j = g_j (dg_j - sum_k g_k dg_k)

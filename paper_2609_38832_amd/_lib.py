@@ -32,7 +32,8 @@ ROPE_HEAD_RELATIVE, ROPE_GLOBAL, ROPE_NONE = 0, 1, 2
 EXPORTED = (
     "namoh_route_workspace_size", "namoh_route", "namoh_route_biased", "namoh_route_bias_update",
     "namoh_attn_fwd_workspace_size", "namoh_attn_fwd",
-    "namoh_prefill_cache", "namoh_attn_bwd_workspace_size", "namoh_attn_bwd", "namoh_route_bwd",
+    "namoh_prefill_cache", "namoh_attn_bwd_workspace_size", "namoh_attn_bwd",
+    "namoh_attn_bwd_packed", "namoh_route_bwd",
     "namoh_decode_workspace_size", "namoh_decode_step", "namoh_decode_step_biased",
     "namoh_decode_step_noalloc",
     "namoh_qkv_proj", "namoh_out_proj_workspace_size", "namoh_out_proj",
@@ -61,6 +62,8 @@ _SIGS = {
     "namoh_attn_bwd_workspace_size": (_S, [_I, _I, _I, _I, _I]),
     "namoh_attn_bwd": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F, _P, _P, _P, _P, _P,
                             _P, _P, _P, _P, _P, _S, _P]),
+    "namoh_attn_bwd_packed": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F, _P, _P, _P,
+                                   _P, _P, _P, _P, _P, _P, _P, _S, _P]),
     "namoh_route_bwd": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "namoh_decode_workspace_size": (_S, [_I, _I, _I, _I, _I]),
     "namoh_decode_step": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I,
@@ -335,10 +338,12 @@ def prefill_cache(k: torch.Tensor, v: torch.Tensor, r: dict, K: int, rope_base: 
 def attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K: int,
              rope_base: float, dout: torch.Tensor, rope_mode: int = ROPE_HEAD_RELATIVE,
              softmax_scale: float = 0.0, ws: Optional[torch.Tensor] = None,
-             out: Optional[dict] = None) -> dict:
+             out: Optional[dict] = None, packed: bool = False) -> dict:
     """namoh_attn_bwd: gradients dq, dk, dv [B, H, T, d] and dgates [B, T, K]
     (float32) for the upstream gradient dout float32 [B, T, d]; `out` may
-    hold preallocated tensors of those shapes under the same keys."""
+    hold preallocated tensors of those shapes under the same keys.  With
+    packed=True, namoh_attn_bwd_packed: dq, dk, dv [B*T*K, d] in the
+    routing's packed order."""
     _need_cuda(q, k, v, dout)
     B, H, T, d = q.shape
     if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
@@ -347,17 +352,18 @@ def attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K
         raise ValueError("dout must be float32 [B, T, d]")
     dev = q.device
     f32 = dict(dtype=torch.float32, device=dev)
+    gshape = (B * T * K, d) if packed else (B, H, T, d)
     if out is None:
-        out = {"dq": torch.empty(B, H, T, d, **f32), "dk": torch.empty(B, H, T, d, **f32),
-               "dv": torch.empty(B, H, T, d, **f32), "dgates": torch.empty(B, T, K, **f32)}
-    for key, shape in (("dq", (B, H, T, d)), ("dk", (B, H, T, d)), ("dv", (B, H, T, d)),
-                       ("dgates", (B, T, K))):
+        out = {"dq": torch.empty(*gshape, **f32), "dk": torch.empty(*gshape, **f32),
+               "dv": torch.empty(*gshape, **f32), "dgates": torch.empty(B, T, K, **f32)}
+    for key, shape in (("dq", gshape), ("dk", gshape), ("dv", gshape), ("dgates", (B, T, K))):
         if out[key].dtype != torch.float32 or tuple(out[key].shape) != shape \
                 or not out[key].is_contiguous():
             raise ValueError(f"out[{key!r}] must be contiguous float32 {shape}")
     if ws is None:
         ws = workspace(int(lib().namoh_attn_bwd_workspace_size(B, T, H, K, d)), dev)
-    check(lib().namoh_attn_bwd(_ptr(q), _ptr(k), _ptr(v), dtype_code(q.dtype), B, T, H, K, d,
+    fn = lib().namoh_attn_bwd_packed if packed else lib().namoh_attn_bwd
+    check(fn(_ptr(q), _ptr(k), _ptr(v), dtype_code(q.dtype), B, T, H, K, d,
                                float(rope_base), rope_mode, float(softmax_scale),
                                _ptr(routing["topk_idx"]), _ptr(routing["gates"]),
                                _ptr(routing["seg_offsets"]), _ptr(routing["perm_token"]),

@@ -451,12 +451,13 @@ size_t namoh_attn_bwd_workspace_size(int B, int T, int H, int K, int d_head) {
   return namoh::attn_bwd_workspace_bytes(B, T, H, K, d_head);
 }
 
-namoh_status namoh_attn_bwd(const void* q, const void* k, const void* v, int dtype, int B, int T,
-                            int H, int K, int d_head, float rope_base, int rope_mode,
-                            float softmax_scale, const int32_t* topk_idx, const float* gates,
-                            const int32_t* seg_offsets, const int32_t* perm_token,
-                            const float* dout, float* dq, float* dk, float* dv, float* dgates,
-                            void* workspace, size_t workspace_bytes, void* stream) {
+static namoh_status attn_bwd_common(const void* q, const void* k, const void* v, int dtype,
+                                    int B, int T, int H, int K, int d_head, float rope_base,
+                                    int rope_mode, float softmax_scale, const int32_t* topk_idx,
+                                    const float* gates, const int32_t* seg_offsets,
+                                    const int32_t* perm_token, const float* dout, float* dq,
+                                    float* dk, float* dv, float* dgates, void* workspace,
+                                    size_t workspace_bytes, void* stream, bool packed) {
   namoh_status s;
   if ((s = check_sizes(B, T, H, K)) != NAMOH_OK) return s;
   if ((s = check_head_width(d_head)) != NAMOH_OK) return s;
@@ -489,7 +490,30 @@ namoh_status namoh_attn_bwd(const void* q, const void* k, const void* v, int dty
   return launched(stream, namoh::launch_attn_bwd(q, k, v, dtype, B, T, H, K, d_head, rope_base,
                                            rope_mode, scale, topk_idx, gates, seg_offsets,
                                            perm_token, dout, dq, dk, dv, dgates, workspace,
-                                           static_cast<hipStream_t>(stream)));
+                                           static_cast<hipStream_t>(stream), packed));
+}
+
+namoh_status namoh_attn_bwd(const void* q, const void* k, const void* v, int dtype, int B, int T,
+                            int H, int K, int d_head, float rope_base, int rope_mode,
+                            float softmax_scale, const int32_t* topk_idx, const float* gates,
+                            const int32_t* seg_offsets, const int32_t* perm_token,
+                            const float* dout, float* dq, float* dk, float* dv, float* dgates,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  return attn_bwd_common(q, k, v, dtype, B, T, H, K, d_head, rope_base, rope_mode, softmax_scale,
+                         topk_idx, gates, seg_offsets, perm_token, dout, dq, dk, dv, dgates,
+                         workspace, workspace_bytes, stream, false);
+}
+
+namoh_status namoh_attn_bwd_packed(const void* q, const void* k, const void* v, int dtype, int B,
+                                   int T, int H, int K, int d_head, float rope_base,
+                                   int rope_mode, float softmax_scale, const int32_t* topk_idx,
+                                   const float* gates, const int32_t* seg_offsets,
+                                   const int32_t* perm_token, const float* dout, float* dq,
+                                   float* dk, float* dv, float* dgates, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  return attn_bwd_common(q, k, v, dtype, B, T, H, K, d_head, rope_base, rope_mode, softmax_scale,
+                         topk_idx, gates, seg_offsets, perm_token, dout, dq, dk, dv, dgates,
+                         workspace, workspace_bytes, stream, true);
 }
 
 namoh_status namoh_route_bwd(const float* logits, const int32_t* topk_idx, const float* gates,

@@ -400,7 +400,7 @@ __global__ __launch_bounds__(256) void k_bwd_scatter(
     const int32_t* __restrict__ kslot, const int32_t* __restrict__ seg_offsets,
     const int32_t* __restrict__ perm_token, int BH, int H, int T, int K, int Nr, int rope_mode,
     double log_base, float* __restrict__ dq, float* __restrict__ dk, float* __restrict__ dv,
-    float* __restrict__ dgates) {
+    float* __restrict__ dgates, int packed) {
   constexpr int G = D / 16;
   constexpr int RW = 256 / G;
   __shared__ double s_theta[D / 2];
@@ -418,7 +418,8 @@ __global__ __launch_bounds__(256) void k_bwd_scatter(
   const int ks = kslot[r];
   if (j0 == 0 && ks >= 0 && ks < K) dgates[(static_cast<size_t>(b) * T + t) * K + ks] = dgp[r];
   const size_t src = static_cast<size_t>(r) * D;
-  const size_t dst = (static_cast<size_t>(s) * T + t) * D;
+  // dense [B, H, T, d] rows, or (packed) the routed row's own packed row
+  const size_t dst = packed ? static_cast<size_t>(r) * D : (static_cast<size_t>(s) * T + t) * D;
   const double pos = rope_mode == 0 ? rank : t;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -782,7 +783,7 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
     const uint16_t* __restrict__ Vp, const uint16_t* __restrict__ Kt,
     const WorkItem* __restrict__ items, const int32_t* __restrict__ meta,
     const int32_t* __restrict__ perm_token, const float2* __restrict__ table, int T,
-    int rope_mode, float scale, float* __restrict__ dq) {
+    int rope_mode, float scale, float* __restrict__ dq, int packed) {
   constexpr int NT = kBwdMfmaThreads, BM = kBwdMfmaBlock;
   constexpr int KS = D / 16, MT = D / 32;
   constexpr int KPT = kBN * D / 8 / NT;
@@ -887,7 +888,8 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
     const int t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
     const float2* cs =
         rope_mode == 2 ? nullptr : table + static_cast<size_t>(rope_mode == 0 ? r : t) * (D / 2);
-    store_row_unrotated<D>(dq + (static_cast<size_t>(it.s) * T + t) * D, acc, scale, cs, g);
+    const size_t o = packed ? static_cast<size_t>(seg0 + r) * D : (static_cast<size_t>(it.s) * T + t) * D;
+    store_row_unrotated<D>(dq + o, acc, scale, cs, g);
   }
 }
 
@@ -900,7 +902,7 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
     const uint16_t* __restrict__ Vp, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ meta, const int32_t* __restrict__ perm_token,
     const float2* __restrict__ table, int T, int rope_mode, float* __restrict__ dk,
-    float* __restrict__ dv) {
+    float* __restrict__ dv, int packed) {
   constexpr int NT = kBwdMfmaThreads, BM = kBwdMfmaBlock;
   constexpr int KS = D / 16, MT = D / 32;
   constexpr int KPT = kBN * D / 8 / NT;
@@ -1030,7 +1032,7 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
     // the queries were scaled by scale * log2 e: dk~ = ln 2 * sum dS Qs,
     // back through the key's rotation; dv as it is
     const int t = min(static_cast<unsigned>(perm_token[seg0 + j]), static_cast<unsigned>(T - 1));
-    const size_t o = (static_cast<size_t>(it.s) * T + t) * D;
+    const size_t o = packed ? static_cast<size_t>(seg0 + j) * D : (static_cast<size_t>(it.s) * T + t) * D;
     const float2* cs =
         rope_mode == 2 ? nullptr : table + static_cast<size_t>(rope_mode == 0 ? j : t) * (D / 2);
     store_row_unrotated<D>(dk + o, aK, kLn2, cs, g);
@@ -1107,7 +1109,7 @@ static hipError_t run_bwd_mfma(const void* q, const void* k, const void* v, int 
                                const int32_t* topk_idx, const float* gates,
                                const int32_t* seg_offsets, const int32_t* perm_token,
                                const float* dout, float* dq, float* dk, float* dv,
-                               float* dgates, void* ws, hipStream_t st) {
+                               float* dgates, void* ws, hipStream_t st, bool packed) {
   const BwdMfmaWs w = carve_bwd_mfma(ws, B, T, H, K, D);
   const int BH = B * H;
   const int Nr = B * T * K;
@@ -1117,11 +1119,13 @@ static hipError_t run_bwd_mfma(const void* q, const void* k, const void* v, int 
   if (e != hipSuccess) return e;
   if (tl.BM != kBwdMfmaBlock || static_cast<size_t>(tl.max_tiles) * kBN > w.rows)
     return hipErrorInvalidValue;   // the forward's blocks and tiles must match these kernels
-  const size_t rows = static_cast<size_t>(BH) * T;
-  constexpr int RPB = kZeroThreads / (D / 4);
-  k_bwd_zero_unrouted<D><<<static_cast<unsigned>((rows + RPB - 1) / RPB), kZeroThreads, 0, st>>>(
-      topk_idx, H, T, K, rows, dq, dk, dv);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (!packed) {   // dense gradients: rows of tokens not routed to the head are zero
+    const size_t rows = static_cast<size_t>(BH) * T;
+    constexpr int RPB = kZeroThreads / (D / 4);
+    k_bwd_zero_unrouted<D><<<static_cast<unsigned>((rows + RPB - 1) / RPB), kZeroThreads, 0,
+                             st>>>(topk_idx, H, T, K, rows, dq, dk, dv);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   const float2* table = static_cast<const float2*>(tl.table);
   prof_mark("bwd_pack", true, st);
   k_bwd_pack<D><<<static_cast<unsigned>(tl.max_tiles), kBwdPackThreads, 0, st>>>(
@@ -1133,13 +1137,13 @@ static hipError_t run_bwd_mfma(const void* q, const void* k, const void* v, int 
   prof_mark("bwd_dq", true, st);
   k_bwd_dq<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
       w.Qs, w.dO, w.LD, tl.Kp, w.Vp, w.Kt, tl.items, tl.meta, perm_token, table, T, rope_mode,
-      scale, dq);
+      scale, dq, packed ? 1 : 0);
   prof_mark("bwd_dq", false, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_mark("bwd_dkdv", true, st);
   k_bwd_dkdv<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
       w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, table, T,
-      rope_mode, dk, dv);
+      rope_mode, dk, dv, packed ? 1 : 0);
   prof_mark("bwd_dkdv", false, st);
   return hipGetLastError();
 }
@@ -1149,17 +1153,19 @@ static hipError_t run_bwd(const void* q, const void* k, const void* v, int B, in
                           float rope_base, int rope_mode, float scale, const int32_t* topk_idx,
                           const float* gates, const int32_t* seg_offsets,
                           const int32_t* perm_token, const float* dout, float* dq, float* dk,
-                          float* dv, float* dgates, void* ws, hipStream_t st) {
+                          float* dv, float* dgates, void* ws, hipStream_t st, bool packed) {
   const BwdWs w = carve_bwd(ws, B, T, K, D);
   const int BH = B * H;
   const int Nr = B * T * K;
   const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
-  const size_t n4 = static_cast<size_t>(BH) * T * D / 4;
-  k_bwd_zero<<<static_cast<unsigned>((n4 + 255) / 256), 256, 0, st>>>(
-      reinterpret_cast<float4*>(dq), reinterpret_cast<float4*>(dk), reinterpret_cast<float4*>(dv),
-      n4);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
+  if (!packed) {   // dense gradients: rows of tokens not routed to the head are zero
+    const size_t n4 = static_cast<size_t>(BH) * T * D / 4;
+    k_bwd_zero<<<static_cast<unsigned>((n4 + 255) / 256), 256, 0, st>>>(
+        reinterpret_cast<float4*>(dq), reinterpret_cast<float4*>(dk),
+        reinterpret_cast<float4*>(dv), n4);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   constexpr int RW = 256 / (D / 16);
   const unsigned rgrid = static_cast<unsigned>((Nr + RW - 1) / RW);
   k_bwd_gather<D, BF16><<<rgrid, 256, 0, st>>>(q, k, v, topk_idx, gates, dout, seg_offsets,
@@ -1177,7 +1183,7 @@ static hipError_t run_bwd(const void* q, const void* k, const void* v, int B, in
   if ((e = hipGetLastError()) != hipSuccess) return e;
   k_bwd_scatter<D><<<rgrid, 256, 0, st>>>(w.dQr, w.dKr, w.dVp, w.dgp, w.seg_of, w.kslot,
                                           seg_offsets, perm_token, BH, H, T, K, Nr, rope_mode,
-                                          log_base, dq, dk, dv, dgates);
+                                          log_base, dq, dk, dv, dgates, packed ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -1186,16 +1192,16 @@ hipError_t launch_attn_bwd(const void* q, const void* k, const void* v, int dtyp
                            const int32_t* topk_idx, const float* gates,
                            const int32_t* seg_offsets, const int32_t* perm_token,
                            const float* dout, float* dq, float* dk, float* dv, float* dgates,
-                           void* ws, hipStream_t st) {
+                           void* ws, hipStream_t st, bool packed) {
 #define NAMOH_BWD(DD, BF)                                                                      \
   return run_bwd<DD, BF>(q, k, v, B, T, H, K, rope_base, rope_mode, scale, topk_idx, gates,   \
-                         seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st)
+                         seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st, packed)
   if (bwd_uses_mfma(dtype, d)) {
     if (d == 64)
       return run_bwd_mfma<64>(q, k, v, B, T, H, K, rope_base, rope_mode, scale, topk_idx, gates,
-                              seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st);
+                              seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st, packed);
     return run_bwd_mfma<128>(q, k, v, B, T, H, K, rope_base, rope_mode, scale, topk_idx, gates,
-                             seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st);
+                             seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st, packed);
   }
   if (dtype == 1) NAMOH_BWD(32, true);
   if (d == 32) NAMOH_BWD(32, false);

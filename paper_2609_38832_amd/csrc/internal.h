@@ -129,7 +129,7 @@ hipError_t launch_attn_bwd(const void* q, const void* k, const void* v, int dtyp
                            const int32_t* topk_idx, const float* gates,
                            const int32_t* seg_offsets, const int32_t* perm_token,
                            const float* dout, float* dq, float* dk, float* dv, float* dgates,
-                           void* ws, hipStream_t st);
+                           void* ws, hipStream_t st, bool packed = false);
 hipError_t launch_route_bwd(const float* logits, const int32_t* topk_idx, const float* gates,
                             const float* dgates, int B, int T, int H, int K, int gate_mode,
                             float* dlogits, hipStream_t st);

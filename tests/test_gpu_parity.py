@@ -205,6 +205,10 @@ BWD = {
     "bf16_d64_none": (W.WORKLOADS[2].with_(B=1, T=600, H=3, K=3), O.ROPE_NONE),
     "f32_d64_dense": (W.WORKLOADS[2].with_(B=1, T=300, H=4, K=4, dtype="f32"), O.ROPE_HEAD_RELATIVE),
     "skewed_long": (W.WORKLOADS[4].with_(B=1, T=1600, H=8, K=1), O.ROPE_HEAD_RELATIVE),
+    # the balanced workload's shape with two sequences (64 segments of ~1024
+    # rows), and 16 heads of ~4096 rows at d = 128
+    "balanced_b2": (W.WORKLOADS[2].with_(B=2), O.ROPE_HEAD_RELATIVE),
+    "long_d128": (W.WORKLOADS[3].with_(T=8192, H=16), O.ROPE_HEAD_RELATIVE),
 }
 
 
@@ -233,6 +237,42 @@ def test_attn_bwd_parity(name):
     # rows of tokens not routed to the head are exactly zero
     m = O.membership(ref["topk_idx"], w.H).transpose(0, 2, 1)
     assert not g["dq"].cpu().numpy()[~m].any()
+
+
+@pytest.mark.parametrize("name", ["bf16_d64_rel", "bf16_d128_global", "f32_d32_none",
+                                  "bf16_d32_rel", "balanced_b2", "long_d128"])
+def test_attn_bwd_packed(name):
+    # namoh_attn_bwd_packed: the routed pairs' gradients in the routing's
+    # packed order, against the oracle's gradients at those pairs, and bit
+    # for bit the dense call's rows gathered at the same pairs
+    w, rope_mode = BWD[name]
+    say(f"backward, packed gradients {name}: {w}")
+    inp = W.prefill_inputs(w)
+    lg = torch.from_numpy(inp["logits"]).to(DEV)
+    q, k, v = (to_dev(inp[x], w.dtype) for x in ("q", "k", "v"))
+    r = L.route(lg, w.K)
+    dout = np.random.default_rng(77).standard_normal((w.B, w.T, w.d)).astype(np.float32)
+    dd = torch.from_numpy(dout).to(DEV)
+    gp = L.attn_bwd(q, k, v, r, w.K, w.rope_base, dd, rope_mode, packed=True)
+    gd = L.attn_bwd(q, k, v, r, w.K, w.rope_base, dd, rope_mode)
+    torch.cuda.synchronize()
+    off = r["seg_offsets"].cpu().numpy().astype(np.int64)
+    perm = r["perm_token"].cpu().numpy().astype(np.int64)
+    seg = np.repeat(np.arange(w.B * w.H), np.diff(off))
+    bb, hh = seg // w.H, seg % w.H
+    f = _f64(inp, w)
+    ref = _oracle_routing(inp, w)
+    dq, dk, dv, dg = O.attention_backward(f["q"], f["k"], f["v"], ref["gates"], ref["seg_offsets"],
+                                          ref["perm_token"], ref["slot_pos"], w.H, w.rope_base,
+                                          dout.astype(np.float64), rope_mode)
+    tol = _grad_tol(w)
+    for key, full in (("dq", dq), ("dk", dk), ("dv", dv)):
+        got = gp[key].cpu().numpy()
+        assert got.shape == (w.B * w.T * w.K, w.d)
+        _check_grad(got, full[bb, hh, perm], key, **tol)
+        np.testing.assert_array_equal(got, gd[key].cpu().numpy()[bb, hh, perm], err_msg=key)
+    np.testing.assert_array_equal(gp["dgates"].cpu().numpy(), gd["dgates"].cpu().numpy())
+    _check_grad(gp["dgates"].cpu().numpy(), dg, "dgates", **tol)
 
 
 @pytest.mark.parametrize("gate_mode", [O.GATE_SOFTMAX_SELECTED, O.GATE_SOFTMAX_ALL])
