@@ -115,6 +115,27 @@ NAMOH_DEV int wave_bin_add(int* bins, int key, bool active) {
 constexpr int kSplitMinTiles = 32;
 constexpr int kSplitMaxParts = 8;
 
+// Late pairs (split_slots > 0, S = split_slots resident slots, E = items - S
+// with 0 < E <= S / kPairMaxFrac).  The E items past the slots would start
+// only when a slot frees, late in the kernel, and end it.  The hardware puts
+// workgroup i on XCD i mod 8, and on compute unit i mod (units) while every
+// unit has room; a unit issues for its oldest wave first, so the workgroups
+// of the first block of positions run ahead and the youngest lag.  Pair j
+// (j < E) joins the lightest extra item (rank S + j) with the lightest
+// placed one (rank S - 1 - j, whose serpentine position is in the last,
+// reversed block, on unit j): the light item takes position j, the oldest
+// on unit j, and finishes first; the other items of unit j each move one
+// block later, keeping their order; and rank S - 1 - j is dispatched after
+// all slots are taken, at S + k with k = j (mod 8), so it waits for a slot on
+// the light item's XCD.  Within a residue class the largest j (the lightest
+// extra, finishing first) frees the slot of the first late workgroup, which
+// holds the heaviest late item.  A unit's total work is unchanged.  Used
+// when the geometry fits: the period (compute units) a multiple of 8
+// dividing S into an even number of blocks (MINB 2 or 4 on 256 units), E at
+// most one block.
+constexpr int kPairMaxFrac = 8;
+constexpr int kXcds = 8;
+
 struct SchedLds {
   int hist[kSortBins];
   int off[kSegLds + 1];
@@ -156,6 +177,28 @@ NAMOH_DEV int serpentine(int rank, int total, int period) {
   const int first = blk * period;
   const int len = min(period, total - first);
   return first + len - 1 - (rank - first);
+}
+
+NAMOH_DEV bool late_pairs_fit(int slots, int extra, int period) {
+  return extra > 0 && period > 1 && period % kXcds == 0 && slots % period == 0 &&
+         (slots / period) % 2 == 0 && extra <= slots / kPairMaxFrac && extra <= period;
+}
+
+// Dispatch position of rank `rank` with `extra` late pairs over `slots`
+// resident slots (see kPairMaxFrac); a permutation of [0, slots + extra).
+NAMOH_DEV int late_pair_pos(int rank, int slots, int extra, int period) {
+  const int S = slots, E = extra;
+  if (rank < S - E) {
+    const int p = serpentine(rank, S, period);
+    return p % period < E ? p + period : p;   // one block younger on a paired unit
+  }
+  if (rank >= S) return rank - S;       // the light item of pair rank - S
+  // late item of pair j: residue a = j mod 8, t = j / 8; the class holds
+  // ceil((E - a) / 8) pairs, taken largest t first
+  const int j = S - 1 - rank;
+  const int a = j % kXcds, t = j / kXcds;
+  const int Ta = (E - a + kXcds - 1) / kXcds;
+  return S + kXcds * (Ta - 1 - t) + a;
 }
 
 template <int NT>
@@ -325,6 +368,9 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
   }
   __syncthreads();
   const int placed = min(total, max_items);
+  const int extra = split_slots > 0 && late_pairs_fit(split_slots, placed - split_slots, period)
+                        ? placed - split_slots
+                        : 0;
   for (long g0 = 0; g0 < ncells; g0 += NT) {
     const long g = g0 + tid;
     int sg = 0, qb = 0, u = 0, seg0 = 0, n = 0, w = 0;
@@ -352,7 +398,8 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
       const int lo = max(0, hi - Lp);
       const int rank = bin_add(key_of(hi - lo), act && p < P);
       if (act && p < P && rank < placed) {
-        const int pos = serpentine(rank, placed, period);
+        const int pos = extra > 0 ? late_pair_pos(rank, split_slots, extra, period)
+                                  : serpentine(rank, placed, period);
         WorkItem wi;
         wi.s = sg;
         wi.qb = qb;
