@@ -370,15 +370,27 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn_mfma(
   const int w0 = r0 + wave * RPW;
   const int w1 = min(r1, w0 + RPW);
 
+  // A operand rows >= GQ are zero: they read query GQ - 1 and are cleared
+  // after the loads (a load under a branch would be waited for at the join,
+  // one round trip per load)
   bf16x8 qa[KS];
+  {
+    const float4* qrow = reinterpret_cast<const float4*>(
+        qrot + (static_cast<size_t>(bk) * GQ + min(j16, GQ - 1)) * D + 8 * kg);
+    float4 f[KS][2];
 #pragma unroll
-  for (int s = 0; s < KS; ++s) {
-    float f[8];
+    for (int s = 0; s < KS; ++s) {
+      f[s][0] = qrow[8 * s];
+      f[s][1] = qrow[8 * s + 1];
+    }
+    const bool keep = j16 < GQ;
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      f[e] = j16 < GQ ? qrot[(static_cast<size_t>(bk) * GQ + j16) * D + 32 * s + 8 * kg + e] : 0.f;
+    for (int s = 0; s < KS; ++s) {
+      const float x[8] = {f[s][0].x, f[s][0].y, f[s][0].z, f[s][0].w,
+                          f[s][1].x, f[s][1].y, f[s][1].z, f[s][1].w};
 #pragma unroll
-    for (int e = 0; e < 8; ++e) qa[s][e] = static_cast<__bf16>(f[e]);
+      for (int e = 0; e < 8; ++e) qa[s][e] = static_cast<__bf16>(keep ? x[e] : 0.f);
+    }
   }
   float m[4], l[4];
   f32x4 O[NT];
