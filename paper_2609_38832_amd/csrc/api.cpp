@@ -54,6 +54,9 @@ namoh_status check_sizes(int B, int T, int H, int K) {
   REQUIRE(K >= 1 && K <= H, "K must be in [1, H] (got K=%d, H=%d)", K, H);
   const long long nr = static_cast<long long>(B) * T * K;
   REQUIRE(nr < (1ll << 31), "B*T*K must be < 2^31 (got %lld)", nr);
+  // the attention work list's (64-query block, segment) grid is indexed in int
+  const long long cells = (static_cast<long long>(T) + 63) / 64 * B * H;
+  REQUIRE(cells < (1ll << 31), "ceil(T/64)*B*H must be < 2^31 (got %lld)", cells);
   return NAMOH_OK;
 }
 

@@ -65,36 +65,14 @@ constexpr int kSegLds = 1024;      // segment offsets staged in LDS up to this m
 constexpr int kPackThreads = 256;
 
 // ---------------------------------------------------------------------------
-// LDS atomic add of `add` to bins[key] for the active lanes of a wave, one
-// atomic per distinct key (lanes with equal keys are served by the lowest of
-// them); returns, for each active lane, the bin's old value plus the number
-// of lower lanes of the wave with the same key.
-NAMOH_DEV int wave_bin_add(int* bins, int key, bool active) {
-  const int lane = __lane_id();
-  uint64_t todo = __ballot(active);
-  int result = 0;
-  while (todo) {
-    const int leader = __ffsll(static_cast<unsigned long long>(todo)) - 1;
-    const int k = __shfl(key, leader);
-    const uint64_t m = __ballot(active && key == k);
-    int base = 0;
-    if (lane == leader) base = atomicAdd(&bins[k], __popcll(m));
-    base = __shfl(base, leader);
-    if (active && key == k) result = base + __popcll(m & lanemask_lt());
-    todo &= ~m;
-  }
-  return result;
-}
-
-// ---------------------------------------------------------------------------
 // The work list: items sorted by causal work (key tiles), heaviest first,
 // by a counting sort; workgroup i runs item i, and the hardware dispatches
 // workgroups in index order, which makes the assignment to compute units
 // longest-processing-time first.  (Placing items by XCD so that a segment's
 // key/value tiles stay in one L2 measured no faster: the tiles are re-read
 // from the shared last-level cache at a rate the kernel does not saturate.)
-// The sort visits the items as a (query block, segment) grid, one item per
-// thread per round, so every round is a few wave-aggregated LDS atomics.
+// The sort visits one (segment, query block) cell per thread per round and
+// reserves its ranks with LDS atomics (two per cell at most).
 // Offsets that are not a valid packing of Nr rows (out of order, a segment
 // longer than T, or not ending at Nr) produce an empty list.  The global
 // stores come last: a barrier after a store would wait for it.
@@ -141,7 +119,7 @@ struct SchedLds {
   int off[kSegLds + 1];
   int wmax[16], wbad[16];
   int wave[17];
-  long wsum[16];
+  double wsum[16];
   int nparts, nsplit;
   int cst[kSegLds + 1];   // first cell of each segment (cells enumerated segment by segment)
 };
@@ -225,11 +203,8 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
     mx = max(mx, n);
     bad |= n < 0 || n > T;
   }
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    mx = max(mx, __shfl_xor(mx, o));
-    bad |= __shfl_xor(bad, o);
-  }
+  mx = wave_max_i(mx);
+  bad = __ballot(bad) != 0;
   if (lane == 0) {
     L.wmax[wave] = mx;
     L.wbad[wave] = bad;
@@ -250,18 +225,17 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
     }
     return;
   }
-  // The cells (segment, query block, query head u of a key/value group; G = 1
-  // without groups), w: a cell's key tiles.  With the segment table in LDS
-  // only the real cells are visited, numbered segment by segment (cst[s]: the
-  // first cell of segment s, found back by binary search), and ranked with
-  // one LDS atomic per lane: a wave's cells then hold distinct keys, which
-  // the atomics of one instruction serve together.  Otherwise, or when the
-  // full (query block, segment) grid holds at most twice the real cells, the
-  // grid is visited (cells past a segment's end inactive), in an order that
-  // gives a wave's cells a few shared keys, ranked by wave-aggregated atomics.
-  const long grid_cells = static_cast<long>((maxn + BM - 1) / BM) * BH * G;
+  // The cells (segment, query block), w: a cell's key tiles; with key/value
+  // groups each cell stands for G items (query heads u < G) of the same
+  // work, which take G consecutive ranks.  With the segment table in LDS
+  // only the real cells are visited, numbered segment by segment (cst[s]:
+  // the first cell of segment s, found back by binary search).  Otherwise,
+  // or when the full (query block, segment) grid holds at most twice the
+  // real cells, the grid is visited qb-major (cells past a segment's end
+  // inactive; a thread steps its (qb, s) by NT cells without dividing).
+  const int grid_cells = (maxn + BM - 1) / BM * BH;   // below 2^31 (checked on the host)
   bool compact = in_lds;
-  long ncells = grid_cells;
+  int ncells = grid_cells;
   if (compact) {
     constexpr int SPT = (kSegLds + NT - 1) / NT;
     int cnt[SPT];
@@ -269,7 +243,7 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
 #pragma unroll
     for (int i = 0; i < SPT; ++i) {
       const int sg = tid * SPT + i;
-      cnt[i] = sg < BH ? (off[sg + 1] - off[sg] + BM - 1) / BM * G : 0;
+      cnt[i] = sg < BH ? (off[sg + 1] - off[sg] + BM - 1) / BM : 0;
       csum += cnt[i];
     }
     int ctot = 0;
@@ -282,36 +256,40 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
     }
     __syncthreads();
     // the grid when it holds at most twice the real cells (no search needed)
-    if (grid_cells > 2L * ctot) ncells = ctot;
+    if (grid_cells > 2 * ctot) ncells = ctot;
     else compact = false;
   }
-  auto cell = [&](long g, int& s, int& qb, int& u, int& seg0, int& n, int& w) {
+  // a thread's cells are tid, tid + NT, ...; in grid order cell c is
+  // (qb, s) = (c / BH, c mod BH), advanced by (NT / BH, NT mod BH) per round
+  const int dq = NT / BH, ds = NT - (NT / BH) * BH;
+  const int qb_first = tid / BH, s_first = tid - (tid / BH) * BH;
+  auto cell = [&](int c, int& s, int& qb, int& seg0, int& n, int& w) {
     if (compact) {
-      int lo = 0, hi = BH - 1;   // the last segment whose first cell is at most g
+      int lo = 0, hi = BH - 1;   // the last segment whose first cell is at most c
       while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        if (L.cst[mid] <= g) lo = mid; else hi = mid - 1;
+        if (L.cst[mid] <= c) lo = mid; else hi = mid - 1;
       }
       s = lo;
-      const int local = static_cast<int>(g) - L.cst[lo];
-      qb = G == 1 ? local : local / G;
-      u = local - qb * G;
-    } else {
-      const long c = g / G;
-      u = static_cast<int>(g - c * G);
-      qb = static_cast<int>(c / BH);
-      s = static_cast<int>(c - static_cast<long>(qb) * BH);
-    }
+      qb = c - L.cst[lo];
+    }   // else (s, qb) are the caller's stepped values
     seg0 = off[s];
     n = off[s + 1] - seg0;
     w = min((n + kBN - 1) / kBN, (qb + 1) * per_qb);
     return qb * BM < n;
   };
-  // rank of an active lane's key among the cells placed so far
-  auto bin_add = [&](int key, bool act) {
-    if (compact) return act ? atomicAdd(&L.hist[key], 1) : 0;
-    return wave_bin_add(L.hist, key, act);
+  auto step = [&](int& s, int& qb) {
+    s += ds;
+    qb += dq;
+    if (s >= BH) {
+      s -= BH;
+      ++qb;
+    }
   };
+  // rank of the first of `cnt` items of key `key` among those placed so far
+  // (one LDS atomic per lane: the LDS serves the lanes of one instruction
+  // together, conflicts on one key in turn)
+  auto bin_add = [&](int key, int cnt) { return atomicAdd(&L.hist[key], cnt); };
   auto key_of = [](int tiles) { return kSortBins - 1 - min(tiles, kSortBins - 1); };
   // the fair share of a slot (no parts without split_slots); a segment of
   // nt key tiles and nq query blocks holds sum over q < nq of
@@ -320,33 +298,38 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
   if (split_slots > 0) {
     long work = 0;
     for (int sg = tid; sg < BH; sg += NT) {
-      const long n = off[sg + 1] - off[sg];
-      const long nt = (n + kBN - 1) / kBN, nq = (n + BM - 1) / BM;
+      const int n = off[sg + 1] - off[sg];
+      const int nt = (n + kBN - 1) / kBN, nq = (n + BM - 1) / BM;
       const long m = min(nq, nt / per_qb);
-      work += per_qb * m * (m + 1) / 2 + (nq - m) * nt;
+      work += per_qb * m * (m + 1) / 2 + static_cast<long>(nq - m) * nt;
     }
     work *= G;
-    // exact 64-bit total: the bounds on parts and partial slots rest on it
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) work += __shfl_xor(work, o);
-    if (lane == 0) L.wsum[wave] = work;
+    // exact total (the bounds on parts and partial slots rest on it): the
+    // per-lane counts are integers far below 2^53, summed in double
+    const double wsum = wave_sum_d(static_cast<double>(work));
+    if (lane == 0) L.wsum[wave] = wsum;
     __syncthreads();
-    long wtot = 0;
+    double wt = 0.0;
 #pragma unroll
-    for (int w = 0; w < NT / kWave; ++w) wtot += L.wsum[w];
+    for (int w = 0; w < NT / kWave; ++w) wt += L.wsum[w];
+    const long wtot = static_cast<long>(wt);
     F = static_cast<int>(min((wtot + split_slots - 1) / split_slots, 0x7fffffffL));
     F = max(F, 1);
   }
-  for (long g0 = 0; g0 < ncells; g0 += NT) {
-    const long g = g0 + tid;
-    int sg = 0, qb = 0, u = 0, seg0 = 0, n = 0, w = 0;
-    const bool act = g < ncells && cell(g, sg, qb, u, seg0, n, w);
-    int P = 1, Lp = w;
-    if (act) split_parts(w, F, P, Lp);
-    for (int p = 0; p < kSplitMaxParts; ++p) {
-      if (!__any(act && p < P)) break;
-      const int hi = w - (P - 1 - p) * Lp;
-      bin_add(key_of(hi - max(0, hi - Lp)), act && p < P);
+  {
+    int sg = s_first, qb = qb_first;
+    for (int c0 = 0; c0 < ncells; c0 += NT) {
+      const int c = c0 + tid;
+      int seg0 = 0, n = 0, w = 0;
+      const bool act = c < ncells && cell(c, sg, qb, seg0, n, w);
+      int P = 1, Lp = w;
+      if (act) {
+        // part 0 holds w - (P - 1) L tiles, parts 1 .. P - 1 L each
+        split_parts(w, F, P, Lp);
+        bin_add(key_of(w - (P - 1) * Lp), G);
+        if (P > 1) bin_add(key_of(Lp), (P - 1) * G);
+      }
+      if (!compact) step(sg, qb);
     }
   }
   __syncthreads();
@@ -371,46 +354,65 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
   const int extra = split_slots > 0 && late_pairs_fit(split_slots, placed - split_slots, period)
                         ? placed - split_slots
                         : 0;
-  for (long g0 = 0; g0 < ncells; g0 += NT) {
-    const long g = g0 + tid;
-    int sg = 0, qb = 0, u = 0, seg0 = 0, n = 0, w = 0;
-    const bool act = g < ncells && cell(g, sg, qb, u, seg0, n, w);
-    int P = 1, Lp = w;
-    if (act) split_parts(w, F, P, Lp);
-    int base = -1;
-    if (act && P > 1) {
-      base = atomicAdd(&L.nparts, P);
-      const int j = atomicAdd(&L.nsplit, 1);
-      SplitItem si;
-      si.s = sg;
-      si.qb = qb;
-      si.seg0 = seg0;
-      si.n = n;
-      si.qh = u;
-      si.P = P;
-      si.base = base;
-      si.pad = 0;
-      splits[j] = si;
-    }
-    for (int p = 0; p < kSplitMaxParts; ++p) {
-      if (!__any(act && p < P)) break;
-      const int hi = w - (P - 1 - p) * Lp;
-      const int lo = max(0, hi - Lp);
-      const int rank = bin_add(key_of(hi - lo), act && p < P);
-      if (act && p < P && rank < placed) {
-        const int pos = extra > 0 ? late_pair_pos(rank, split_slots, extra, period)
-                                  : serpentine(rank, placed, period);
-        WorkItem wi;
-        wi.s = sg;
-        wi.qb = qb;
-        wi.seg0 = seg0;
-        wi.n = n;
-        wi.tile0 = seg_tile0(seg0, sg);
-        wi.qh = u | ((P > 1 ? base + p + 1 : 0) << kQhBits);
-        wi.kt_lo = lo;
-        wi.kt_hi = hi;
-        items[pos] = wi;
+  {
+    int sg = s_first, qb = qb_first;
+    for (int c0 = 0; c0 < ncells; c0 += NT) {
+      const int c = c0 + tid;
+      int seg0 = 0, n = 0, w = 0;
+      const bool act = c < ncells && cell(c, sg, qb, seg0, n, w);
+      int P = 1, Lp = w;
+      if (act) split_parts(w, F, P, Lp);
+      // a split cell: G split items (one per query head u) with partial slots
+      // [base + u P, base + (u + 1) P)
+      int base = -1;
+      if (act && P > 1) {
+        base = atomicAdd(&L.nparts, P * G);
+        const int j = atomicAdd(&L.nsplit, G);
+        for (int u = 0; u < G; ++u) {
+          SplitItem si;
+          si.s = sg;
+          si.qb = qb;
+          si.seg0 = seg0;
+          si.n = n;
+          si.qh = u;
+          si.P = P;
+          si.base = base + u * P;
+          si.pad = 0;
+          splits[j + u] = si;
+        }
       }
+      // ranks: part 0 of query head u at r0 + u, part p >= 1 at
+      // rL + (p - 1) G + u
+      int r0 = 0, rL = 0;
+      if (act) {
+        r0 = bin_add(key_of(w - (P - 1) * Lp), G);
+        if (P > 1) rL = bin_add(key_of(Lp), (P - 1) * G);
+      }
+      for (int p = 0; p < kSplitMaxParts; ++p) {
+        if (!__any(act && p < P)) break;
+        const int hi = w - (P - 1 - p) * Lp;
+        const int lo = max(0, hi - Lp);
+        const int rank = p == 0 ? r0 : rL + (p - 1) * G;
+        if (act && p < P) {
+          for (int u = 0; u < G; ++u) {
+            const int r = rank + u;
+            if (r >= placed) break;
+            const int pos = extra > 0 ? late_pair_pos(r, split_slots, extra, period)
+                                      : serpentine(r, placed, period);
+            WorkItem wi;
+            wi.s = sg;
+            wi.qb = qb;
+            wi.seg0 = seg0;
+            wi.n = n;
+            wi.tile0 = seg_tile0(seg0, sg);
+            wi.qh = u | ((P > 1 ? base + u * P + p + 1 : 0) << kQhBits);
+            wi.kt_lo = lo;
+            wi.kt_hi = hi;
+            items[pos] = wi;
+          }
+        }
+      }
+      if (!compact) step(sg, qb);
     }
   }
   __syncthreads();
@@ -608,14 +610,12 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
     *reinterpret_cast<uint4*>(dst + D / 2 + 8 * c) = o2;
     // the row's squared norm: its HP units are consecutive lanes
     float ss = sumsq8(o1) + sumsq8(o2);
-#pragma unroll
-    for (int o = 1; o < HP; o <<= 1) ss += __shfl_xor(ss, o);
+    ss = group_sum<HP>(ss);
     rmax = fmaxf(rmax, ss);
   }
   // the tile's largest key norm (bounds every score of the tile, see
   // k_attn_mfma); written by the one workgroup that packs the tile
-#pragma unroll
-  for (int o = HP; o < kWave; o <<= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, o));
+  rmax = group_max<kWave>(rmax);
   if (tid % kWave == 0) L.pack.wnorm[tid / kWave] = rmax;
 #pragma unroll
   for (int i = 0; i < VU; ++i) {
@@ -995,8 +995,7 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   // on the rounded operands; the small factor covers the fp32
   // accumulation), so while that product stays within kLazyLog2 of the
   // running maximum a tile's exact maximum is not needed.
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) kmax = fmaxf(kmax, __shfl_xor(kmax, o));
+  kmax = group_max<kWave>(kmax);
   float qn[NQT];
 #pragma unroll
   for (int qt = 0; qt < NQT; ++qt) {

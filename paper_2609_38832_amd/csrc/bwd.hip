@@ -154,7 +154,7 @@ template <int D> struct BwdShape {
 
 template <int LPR>
 NAMOH_DEV float row_sum(float x) {
-  if constexpr (LPR == 2) x += __shfl_xor(x, 1);
+  if constexpr (LPR == 2) x = group_sum<2>(x);
   return x;
 }
 
@@ -614,10 +614,8 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
         }
       }
     }
-    dd += __shfl_xor(dd, 1);
-    dd += __shfl_xor(dd, 2);
-    dg += __shfl_xor(dg, 1);
-    dg += __shfl_xor(dg, 2);
+    dd = group_sum<4>(dd);
+    dg = group_sum<4>(dg);
     if (part == 0) {
       LD[prow0 + row] = r < n ? make_float2(lse[seg0 + r], dd) : make_float2(INFINITY, 0.f);
       if (r < n && ks >= 0) dgates[(static_cast<size_t>(b) * T + t) * K + ks] = dg;

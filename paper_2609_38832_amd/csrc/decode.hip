@@ -237,8 +237,7 @@ __global__ __launch_bounds__(256) void k_decode_attn(
         float dsum = 0.f;
 #pragma unroll
         for (int e = 0; e < EPG; ++e) dsum = fmaf(qv[qq][e], f[e], dsum);
-#pragma unroll
-        for (int o = G / 2; o > 0; o >>= 1) dsum += __shfl_xor(dsum, o);
+        dsum = group_sum<G>(dsum);
         sc[qq][u] = (rb + u * RPB + grp < r1) ? dsum : -INFINITY;
       }
     }
@@ -462,16 +461,14 @@ __global__ __launch_bounds__(256, 2) void k_decode_attn_mfma(
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float mx = fmaxf(S[0][i], S[1][i]);
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      mx = group_max<16>(mx);
       const float mnew = fmaxf(m[i], mx);
       const float corr = __builtin_amdgcn_exp2f(m[i] - mnew);
       m[i] = mnew;
       const float p0 = __builtin_amdgcn_exp2f(S[0][i] - mnew);
       const float p1 = __builtin_amdgcn_exp2f(S[1][i] - mnew);
       float ps = p0 + p1;
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) ps += __shfl_xor(ps, o);
+      ps = group_sum<16>(ps);
       l[i] = l[i] * corr + ps;
 #pragma unroll
       for (int t = 0; t < NT; ++t) O[t][i] *= corr;
@@ -557,12 +554,10 @@ __global__ __launch_bounds__(256) void k_decode_combine(
     const float* ml = part_ml + bq * nchunk * 2;
     float M = -1e30f;
     for (int c = lane; c < nc; c += 64) M = fmaxf(M, ml[2 * c]);
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+    M = group_max<64>(M);
     float Ls = 0.f;
     for (int c = lane; c < nc; c += 64) Ls += ml[2 * c + 1] * __builtin_amdgcn_exp2f(ml[2 * c] - M);
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) Ls += __shfl_xor(Ls, off);
+    Ls = group_sum<64>(Ls);
     const float scale = gates[bk] / Ls;
     float a[DPL];
 #pragma unroll

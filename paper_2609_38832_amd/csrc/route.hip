@@ -71,7 +71,6 @@ NAMOH_DEV uint64_t max_dpp(uint64_t x) {
                      static_cast<uint32_t>(lo);
   return y > x ? y : x;
 }
-constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141;
 
 // 8 lanes per token, lane `sub` holding heads sub*HL .. sub*HL + HL - 1.
 // Round k: every lane takes the largest of its remaining candidates, three
@@ -180,7 +179,7 @@ __global__ __launch_bounds__(kCountThreads) void k_route_count(
     for (int e = 1; e < HL; ++e) best = ck[e] > best ? ck[e] : best;
     best = max_dpp<kDppXor1>(best);
     best = max_dpp<kDppXor2>(best);
-    best = max_dpp<kDppHalfMirror>(best);
+    best = max_dpp<kDppRowHalfMirror>(best);
 #pragma unroll
     for (int e = 0; e < HL; ++e)
       if (valid && ck[e] == best) {
@@ -349,11 +348,8 @@ __global__ __launch_bounds__(kScatterThreads) void k_route_scatter(
         before += cc < c ? v : 0;
       }
     }
-#pragma unroll
-    for (int o = 1; o < 8; o <<= 1) {
-      before += __shfl_xor(before, o, 8);
-      total += __shfl_xor(total, o, 8);
-    }
+    before = group_sum_i<8>(before);
+    total = group_sum_i<8>(total);
     if (j == 0) {
       s_before[h] = before;
       s_len[h] = total;
