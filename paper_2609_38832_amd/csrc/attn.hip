@@ -1158,9 +1158,56 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
 // query block from its P partials (O_p unnormalised, m_p, l_p):
 //   M = max over p of m_p,  h = sum_p 2^(m_p - M) O_p / sum_p 2^(m_p - M) l_p,
 // written as the block's head-output row (bf16; or f32 with the row's
-// log-sum-exp M + log2 of the denominator).  Workgroups stride over the split
-// items; eight columns per thread.
+// log-sum-exp M + log2 of the denominator).  The work units are (split item,
+// pass of RPP rows), strided over the workgroups; eight columns per thread.
+// P is a template argument, so a row's 3P loads are issued together (a load
+// under a branch would be waited for where the branch joins).
 constexpr int kMergeThreads = 256;
+template <int D, bool HB, int P>
+NAMOH_DEV void merge_row(const SplitItem& si, int q0, int r, int sub,
+                         const float* __restrict__ part_o, const float* __restrict__ part_ml,
+                         int BM, int G, void* __restrict__ hout, float* __restrict__ lse_out) {
+  float2 ml[P];
+  float4 a[P][2];
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    const size_t pr = static_cast<size_t>(si.base + p) * BM + r;
+    ml[p] = *reinterpret_cast<const float2*>(part_ml + pr * 2);
+    const float4* src = reinterpret_cast<const float4*>(part_o + pr * D + 8 * sub);
+    a[p][0] = src[0];
+    a[p][1] = src[1];
+  }
+  float M = -INFINITY;
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+    if (ml[p].y > 0.f) M = fmaxf(M, ml[p].x);
+  float acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  float den = 0.f;
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    const float wgt = ml[p].y > 0.f ? __builtin_amdgcn_exp2f(ml[p].x - M) : 0.f;
+    den = fmaf(wgt, ml[p].y, den);
+    acc[0] = fmaf(wgt, a[p][0].x, acc[0]); acc[1] = fmaf(wgt, a[p][0].y, acc[1]);
+    acc[2] = fmaf(wgt, a[p][0].z, acc[2]); acc[3] = fmaf(wgt, a[p][0].w, acc[3]);
+    acc[4] = fmaf(wgt, a[p][1].x, acc[4]); acc[5] = fmaf(wgt, a[p][1].y, acc[5]);
+    acc[6] = fmaf(wgt, a[p][1].z, acc[6]); acc[7] = fmaf(wgt, a[p][1].w, acc[7]);
+  }
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] *= inv;
+  const size_t row = static_cast<size_t>(si.seg0 + q0 + r) * G + si.qh;
+  if constexpr (HB) {
+    reinterpret_cast<uint4*>(static_cast<uint16_t*>(hout) + row * D)[sub] = pack8(acc);
+  } else {
+    float4* dst = reinterpret_cast<float4*>(static_cast<float*>(hout) + row * D + 8 * sub);
+    dst[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    dst[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+    if (lse_out != nullptr && sub == 0) lse_out[row] = M + log2f(den);
+  }
+}
+
 template <int D, bool HB>
 __global__ __launch_bounds__(kMergeThreads) void k_attn_merge(
     const SplitItem* __restrict__ splits, const int32_t* __restrict__ meta,
@@ -1168,60 +1215,30 @@ __global__ __launch_bounds__(kMergeThreads) void k_attn_merge(
     int nblocks, void* __restrict__ hout, float* __restrict__ lse_out) {
   constexpr int TPR = D / 8;                   // threads per row
   constexpr int RPP = kMergeThreads / TPR;     // rows per pass
+  static_assert(kSplitMaxParts == 8, "merge_row instances");
   const int nsplit = meta[kMetaSplit];
+  const int npass = (BM + RPP - 1) / RPP;
   const int tid = thread_x();
   const int sub = tid % TPR, rw = tid / TPR;
-  for (int j = block_x(); j < nsplit; j += nblocks) {
+  for (int u = block_x(); u < nsplit * npass; u += nblocks) {
+    const int j = u / npass;
+    const int r = (u - j * npass) * RPP + rw;
     const SplitItem si = splits[j];
     const int q0 = si.qb * BM;
-    const int rows = min(BM, si.n - q0);
-    const int P = min(si.P, kSplitMaxParts);
-    for (int r = rw; r < rows; r += RPP) {
-      float mp[kSplitMaxParts], lp[kSplitMaxParts];
-      float M = -INFINITY;
-#pragma unroll
-      for (int p = 0; p < kSplitMaxParts; ++p) {
-        mp[p] = 0.f;
-        lp[p] = 0.f;
-        if (p < P) {
-          const float2 ml = *reinterpret_cast<const float2*>(
-              part_ml + (static_cast<size_t>(si.base + p) * BM + r) * 2);
-          mp[p] = ml.x;
-          lp[p] = ml.y;
-          if (ml.y > 0.f) M = fmaxf(M, ml.x);
-        }
-      }
-      float acc[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-      float den = 0.f;
-#pragma unroll
-      for (int p = 0; p < kSplitMaxParts; ++p) {
-        if (p < P) {
-          const float wgt = lp[p] > 0.f ? __builtin_amdgcn_exp2f(mp[p] - M) : 0.f;
-          den = fmaf(wgt, lp[p], den);
-          const float4* src = reinterpret_cast<const float4*>(
-              part_o + (static_cast<size_t>(si.base + p) * BM + r) * D + 8 * sub);
-          const float4 a = src[0], b = src[1];
-          acc[0] = fmaf(wgt, a.x, acc[0]); acc[1] = fmaf(wgt, a.y, acc[1]);
-          acc[2] = fmaf(wgt, a.z, acc[2]); acc[3] = fmaf(wgt, a.w, acc[3]);
-          acc[4] = fmaf(wgt, b.x, acc[4]); acc[5] = fmaf(wgt, b.y, acc[5]);
-          acc[6] = fmaf(wgt, b.z, acc[6]); acc[7] = fmaf(wgt, b.w, acc[7]);
-        }
-      }
-      const float inv = den > 0.f ? 1.f / den : 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] *= inv;
-      const size_t row = static_cast<size_t>(si.seg0 + q0 + r) * G + si.qh;
-      if constexpr (HB) {
-        reinterpret_cast<uint4*>(static_cast<uint16_t*>(hout) + row * D)[sub] = pack8(acc);
-      } else {
-        float4* dst = reinterpret_cast<float4*>(static_cast<float*>(hout) + row * D + 8 * sub);
-        dst[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
-        dst[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
-        if (lse_out != nullptr && sub == 0) lse_out[row] = M + log2f(den);
-      }
+    if (r >= min(BM, si.n - q0)) continue;
+#define NAMOH_MERGE(PP) \
+  merge_row<D, HB, PP>(si, q0, r, sub, part_o, part_ml, BM, G, hout, lse_out)
+    switch (si.P) {
+      case 2: NAMOH_MERGE(2); break;
+      case 3: NAMOH_MERGE(3); break;
+      case 4: NAMOH_MERGE(4); break;
+      case 5: NAMOH_MERGE(5); break;
+      case 6: NAMOH_MERGE(6); break;
+      case 7: NAMOH_MERGE(7); break;
+      case 8: NAMOH_MERGE(8); break;
+      default: break;   // (a split item has 2 .. kSplitMaxParts parts)
     }
+#undef NAMOH_MERGE
   }
 }
 
@@ -1524,7 +1541,7 @@ static void launch_mfma(const AttnWs& w, const void* q, const void* k, const voi
              perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout, lse, 0,
              w.part_o, w.part_ml);
   if (slots > 0) {
-    constexpr int kMergeBlocks = 256;
+    constexpr int kMergeBlocks = 512;   // about one (item, row pass) unit each
     if (hout_bf16)
       launch_k("merge", k_attn_merge<D, true>, dim3(kMergeBlocks), dim3(kMergeThreads), st,
                w.splits, w.meta, w.part_o, w.part_ml, BM, G, kMergeBlocks, hout, nof);
