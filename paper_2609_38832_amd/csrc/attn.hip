@@ -855,7 +855,9 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   static_assert(kBN * D / 8 % NT == 0, "tile/thread mismatch");
 
   constexpr int NS = MfmaShape<D>::NS;
-  static_assert(NS >= 2 && 2 * KPT * (NS - 2) < 64, "tile stages");
+  // two stages: each tile is published by a full vmcnt wait and a barrier
+  // (partial waits are not relied on for LDS-DMA loads, see tile_dma)
+  static_assert(NS == 2, "tile stages");
   __shared__ __attribute__((aligned(16))) uint16_t sK[NS][kBN * D];
   __shared__ __attribute__((aligned(16))) uint16_t sV[NS][D * kBN];
   WorkItem it;
@@ -1027,21 +1029,17 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     for (int e = 0; e < 16; ++e) minit[qt][e] = 0.f;
   }
 
-  // ---- tile loop: NS-stage ring of K/V tiles, one barrier per tile -------
-  // At the top of iteration kt the wave has tiles kt .. kt + NS - 2 in
-  // flight; waiting until at most NS - 2 tiles' loads remain completes tile
-  // kt (near the end fewer tiles are in flight and the wait is for all).
-  // After the barrier every wave has finished tile kt - 1, so its stage
-  // receives tile kt + NS - 1.
+  // ---- tile loop: two-stage ring of K/V tiles, one barrier per tile -------
+  // At the top of iteration kt the wave's loads of tile kt are the only ones
+  // in flight: waiting for them and the barrier publish the tile.  After the
+  // barrier every wave has finished tile kt - 1, so its stage receives tile
+  // kt + 1.
   bool fresh[NQT];   // (WIN) no visible key seen yet by the lane's query
 #pragma unroll
   for (int qt = 0; qt < NQT; ++qt) fresh[qt] = true;
   for (int kt = kb; kt < kt_end; ++kt) {
     const int st = (kt - kb) % NS;
-    if (kt + NS - 2 < kt_end)
-      wait_vmcnt<2 * KPT * (NS - 2)>();
-    else
-      wait_vmcnt<0>();
+    wait_vmcnt<0>();
     __syncthreads();
     if (kt + NS - 1 < kt_end) {
       const int nst = (kt - kb + NS - 1) % NS;

@@ -647,8 +647,8 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
 // before the first product.
 template <int D>
 NAMOH_DEV void tile_rows_x_regs(f32x16 (&C)[2], const uint16_t* __restrict__ tile,
-                                const bf16x8 (&bop)[D / 16], const f32x16 (&init)[2], int c,
-                                int g) {
+                                const bf16x8 (&bop)[D / 16], const f32x16& init0,
+                                const f32x16& init1, int c, int g) {
   constexpr int KS = D / 16;
   bf16x8 a[KS][2];
 #pragma unroll
@@ -660,7 +660,7 @@ NAMOH_DEV void tile_rows_x_regs(f32x16 (&C)[2], const uint16_t* __restrict__ til
     }
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk)
-    C[kk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][kk], bop[0], init[kk], 0, 0, 0);
+    C[kk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][kk], bop[0], kk == 0 ? init0 : init1, 0, 0, 0);
 #pragma unroll
   for (int ks = 1; ks < KS; ++ks)
 #pragma unroll
@@ -770,12 +770,13 @@ __global__ __launch_bounds__(kZeroThreads) void k_bwd_zero_unrouted(
 }
 
 template <int D> struct BwdMfmaShape {
-  static constexpr int MINB = D == 64 ? 2 : 1;   // workgroups per CU
+  static constexpr int MINB = D == 64 ? 2 : 1;   // workgroups per CU (key side)
+  static constexpr int MINB_Q = 2;               // (query side; 3 at d = 64 spills)
 };
 
 // Query side: dQ~ of one (segment, 128-query block) item.
 template <int D>
-__global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_dq(
+__global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bwd_dq(
     const uint16_t* __restrict__ Qs, const uint16_t* __restrict__ dO,
     const float2* __restrict__ LD, const uint16_t* __restrict__ Kp,
     const uint16_t* __restrict__ Vp, const uint16_t* __restrict__ Kt,
@@ -787,9 +788,12 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
   constexpr int KPT = kBN * D / 8 / NT;
   constexpr size_t TS = static_cast<size_t>(kBN) * D;
   constexpr uint32_t TB = static_cast<uint32_t>(TS * 2);
+  // K and V tiles double-buffered; the transposed key tile (read last) has
+  // one stage, loaded behind the tile's first products (at d = 128 the
+  // workgroup then takes 80 KB, two per compute unit)
   __shared__ __attribute__((aligned(16))) uint16_t sK[2][kBN * D];
   __shared__ __attribute__((aligned(16))) uint16_t sV[2][kBN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t sKt[2][D * kBN];
+  __shared__ __attribute__((aligned(16))) uint16_t sKt[kBN * D];
   WorkItem it;
   if (!my_item(items, meta, it)) return;
   const int q0 = it.qb * BM;
@@ -814,13 +818,15 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
   }
   const float2 ld = LD[prow];
   wait_vmcnt<0>();
-  f32x16 init_l[2], init_d[2];
+  // every accumulator of the lane's query starts at -lse (scores) and -D
+  // (probability gradients): one tuple each serves both key halves
+  f32x16 init_l, init_d;
   {
     const float nl = valid ? -ld.x : -INFINITY, nd = valid ? -ld.y : 0.f;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      init_l[0][e] = init_l[1][e] = nl;
-      init_d[0][e] = init_d[1][e] = nd;
+      init_l[e] = nl;
+      init_d[e] = nd;
     }
   }
 
@@ -835,31 +841,40 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
   const uint32_t lK = lds_address(&sK[0][0]) + wave_s * kWave * 16;
   const uint32_t lV = lds_address(&sV[0][0]) + wave_s * kWave * 16;
-  const uint32_t lKt = lds_address(&sKt[0][0]) + wave_s * kWave * 16;
+  const uint32_t lKt = lds_address(&sKt[0]) + wave_s * kWave * 16;
   tile_dma<KPT, NT>(bK, nb, 0, lK, voffR);
   tile_dma<KPT, NT>(bV, nb, 0, lV, voffR);
-  tile_dma<KPT, NT>(bKt, nb, 0, lKt, voffT);
 
   f32x16 acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[mt][e] = 0.f;
+  // Per tile: wait for K, V of tile kt; the barrier also ends every wave's
+  // reads of the previous transposed tile, so tile kt's goes in now,
+  // together with K, V of tile kt + 1, all behind the tile's first products;
+  // a full wait and a second barrier before the dQ products make every
+  // wave's part of it visible.  (A partial wait, leaving the next tile's
+  // loads in flight, gave wrong transposed tiles: LDS-DMA loads are not
+  // known to complete in issue order.)
   for (int kt = 0; kt < kt_end; ++kt) {
     const int st = kt & 1;
     wait_vmcnt<0>();
     __syncthreads();
-    if (kt + 1 < kt_end) {
+    tile_dma<KPT, NT>(bKt, nb, static_cast<uint32_t>(kt) * TB, lKt, voffT);
+    const bool more = kt + 1 < kt_end;
+    if (more) {
       const uint32_t tb = static_cast<uint32_t>(kt + 1) * TB;
       const int ns = st ^ 1;
       tile_dma<KPT, NT>(bK, nb, tb, lK + ns * TB, voffR);
       tile_dma<KPT, NT>(bV, nb, tb, lV + ns * TB, voffR);
-      tile_dma<KPT, NT>(bKt, nb, tb, lKt + ns * TB, voffT);
     }
-    if (kt < wave_tiles) {
+    const bool act = kt < wave_tiles;
+    bf16x8 dsB[4];
+    if (act) {
       f32x16 S[2], dP[2];
-      tile_rows_x_regs<D>(S, sK[st], qB, init_l, c, g);    // S^T - lse (log2 units)
-      tile_rows_x_regs<D>(dP, sV[st], doB, init_d, c, g);  // dP^T - D
+      tile_rows_x_regs<D>(S, sK[st], qB, init_l, init_l, c, g);    // S^T - lse (log2 units)
+      tile_rows_x_regs<D>(dP, sV[st], doB, init_d, init_d, c, g);  // dP^T - D
       const int key0 = kt * kBN;
       if (key0 + kBN - 1 > q0 + 32 * wave || key0 + kBN > n) {
         const int lim = min(r, n - 1) - key0 - 4 * g;   // key 32kk + 8j + 4g + i visible iff <= lim + 4g
@@ -871,7 +886,6 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
             for (int i = 0; i < 4; ++i)
               if (32 * kk + 8 * j + i > lim) S[kk][4 * j + i] = -INFINITY;
       }
-      bf16x8 dsB[4];
 #pragma unroll
       for (int k2 = 0; k2 < 4; ++k2)
 #pragma unroll
@@ -879,8 +893,10 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
           const int a = 8 * (k2 & 1) + e;
           dsB[k2][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(S[k2 >> 1][a]) * dP[k2 >> 1][a]);
         }
-      tposed_x_c<D>(acc, sKt[st], dsB, c, g);
     }
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (act) tposed_x_c<D>(acc, sKt, dsB, c, g);
   }
   if (valid) {   // dq~ = scale sum_j dS k~_j, back through the query's rotation
     const int t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
@@ -999,8 +1015,8 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
             il[kk][4 * jj + 2] = -bq.x; id[kk][4 * jj + 2] = -bq.y;
             il[kk][4 * jj + 3] = -bq.z; id[kk][4 * jj + 3] = -bq.w;
           }
-        tile_rows_x_regs<D>(S, sQ[st], kB, il, c, g);    // S - lse (log2 units)
-        tile_rows_x_regs<D>(dP, sdO[st], vB, id, c, g);  // dP - D
+        tile_rows_x_regs<D>(S, sQ[st], kB, il[0], il[1], c, g);    // S - lse (log2 units)
+        tile_rows_x_regs<D>(dP, sdO[st], vB, id[0], id[1], c, g);  // dP - D
       }
       if (i0 < jw0 + 32) {   // the diagonal: key j visible to query i iff j <= i
         const int lim = j - i0 - 4 * g;

@@ -155,8 +155,10 @@ NAMOH_DEV int swz(int row, int gr) {
 // resource covers the item's key (or value) tiles and the tile is selected
 // by the scalar offset, so a tile costs no vector address arithmetic; the
 // LDS base goes through M0 from scalar registers.  Completion is tracked by
-// vmcnt: wait_vmcnt<N>() before the barrier that publishes a tile leaves only
-// the N most recent loads of the wave in flight.
+// vmcnt; a tile is published by wait_vmcnt<0>() and a barrier (a partial
+// wait, meant to leave only the newest loads in flight, let a transposed
+// tile be read before all of it had landed in LDS: these loads are not
+// relied on to complete in issue order).
 
 // Byte offset (inside one tile) of the first granule this lane fetches.  The
 // lane's i-th granule lies i * NT granules further: NT / GPR rows is a
