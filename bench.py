@@ -722,7 +722,32 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for the "
                          "HBM byte counters of rocprofv3) and exit")
+    ap.add_argument("--hbm-calibration", action="store_true",
+                    help="only time a 4 GiB device-to-device copy with HIP events "
+                         "(an achievable HBM rate to set the roofline fractions "
+                         "against) and exit")
     args = ap.parse_args()
+    if args.hbm_calibration:
+        import torch
+        n = 4 << 30
+        src = torch.ones(n // 4, dtype=torch.int32, device="cuda:0")
+        dst = torch.empty_like(src)
+        res = {}
+        for name, fn, nbytes in (("copy", lambda: dst.copy_(src), 2 * n),):
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(10):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / 10
+            res[name] = {"bytes": nbytes, "ms": round(ms, 4),
+                         "GB_per_s": round(nbytes / ms / 1e6, 1)}
+        print(json.dumps({"hbm_calibration": res, "peak_GB_per_s": 8000.0}))
+        return
     if args.copy_calibration:
         import torch
         n = 1 << 30
