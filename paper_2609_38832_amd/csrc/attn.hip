@@ -890,9 +890,9 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   const size_t head_base = ((static_cast<size_t>(b) * H + h) * G + qh) * T;
 
   // token of each query row.  The tile loads below are invisible to the
-  // compiler's wait counting, and vmcnt retires in issue order, so a wait
-  // the compiler places for an older load would also wait for them: the
-  // tokens are waited for before the first tile load is issued.
+  // compiler's wait counting: a count it places for the tokens would also
+  // have to cover them, so the tokens are waited for before the first tile
+  // load is issued.
   int qtok[NQT];
 #pragma unroll
   for (int qt = 0; qt < NQT; ++qt) {
