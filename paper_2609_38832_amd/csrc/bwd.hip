@@ -689,6 +689,38 @@ NAMOH_DEV void tposed_x_c(f32x16 (&acc)[D / 32], const uint16_t* __restrict__ tt
       acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[k2][mt], x[k2], acc[mt], 0, 0, 0);
 }
 
+// One 32-row half of tile_rows_x_regs: rows 32 kk .. 32 kk + 31 (kk wave
+// uniform) of the tile against the register B operands.
+template <int D>
+NAMOH_DEV void tile_half_x_regs(f32x16& C, const uint16_t* __restrict__ tile,
+                                const bf16x8 (&bop)[D / 16], const f32x16& init, int kk, int c,
+                                int g) {
+  constexpr int KS = D / 16;
+  const int row = 32 * kk + c;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const bf16x8 a =
+        *reinterpret_cast<const bf16x8*>(&tile[row * D + swz<D / 8>(row, 2 * ks + g) * 8]);
+    C = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bop[ks], ks == 0 ? init : C, 0, 0, 0);
+  }
+}
+
+// tposed_x_c over the 32 reduction slots 32 kk .. 32 kk + 31 (kk wave
+// uniform), X given as their two 16-slot B operands.
+template <int D>
+NAMOH_DEV void tposed_half_x_c(f32x16 (&acc)[D / 32], const uint16_t* __restrict__ tt,
+                               const bf16x8 (&x)[2], int kk, int c, int g) {
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt) {
+      const int row = 32 * mt + c;
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+          &tt[row * kBN + swz<kBN / 8>(row, 2 * (2 * kk + kh) + g) * 8]);
+      acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, x[kh], acc[mt], 0, 0, 0);
+    }
+}
+
 // (lse, D) pairs of one 64-row tile: 512 bytes, 32 lanes of wave 0 (the
 // other waves issue nothing, and every wait below is for all loads).
 NAMOH_DEV void ld_tile_dma(const float2* base, uint32_t nbytes, uint32_t tile_bytes,
@@ -1054,6 +1086,185 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
   }
 }
 
+// Key side at d = 128 with two waves per SIMD: eight waves, wave w takes the
+// keys of group w mod 4 (32 keys, as in k_bwd_dkdv) against query half
+// w / 4 (rows 32 qh .. 32 qh + 31) of every query tile, so S, dP, P and dS
+// are half as large per wave and a SIMD interleaves two waves of one
+// workgroup (k_bwd_dkdv's 430 registers allow one).  The two halves' dK and
+// dV partials of a key are summed through LDS at the end.
+template <int D>
+__global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
+    const uint16_t* __restrict__ Qs, const uint16_t* __restrict__ dO,
+    const uint16_t* __restrict__ Qt, const uint16_t* __restrict__ dOt,
+    const float2* __restrict__ LD, const uint16_t* __restrict__ Kp,
+    const uint16_t* __restrict__ Vp, const WorkItem* __restrict__ items,
+    const int32_t* __restrict__ meta, const int32_t* __restrict__ perm_token,
+    const float2* __restrict__ table, int T, int rope_mode, float* __restrict__ dk,
+    float* __restrict__ dv, int packed) {
+  constexpr int NT = 2 * kBwdMfmaThreads, BM = kBwdMfmaBlock;
+  constexpr int KS = D / 16, MT = D / 32;
+  constexpr int KPT = kBN * D / 8 / NT;
+  constexpr size_t TS = static_cast<size_t>(kBN) * D;
+  constexpr uint32_t TB = static_cast<uint32_t>(TS * 2);
+  constexpr uint32_t LB = kBN * sizeof(float2);
+  static_assert(KPT >= 1 && KPT * NT * 8 == kBN * D, "tile/thread mismatch");
+  __shared__ __attribute__((aligned(16))) uint16_t sQ[2][kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sdO[2][kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sQt[2][D * kBN];
+  __shared__ __attribute__((aligned(16))) uint16_t sdOt[2][D * kBN];
+  __shared__ __attribute__((aligned(16))) float2 sLD[2][kBN];
+  // the partials of query half 1, one 2 * MT * 16 * 64-float block per key
+  // group, in the tile stages once the loop is done
+  static_assert(sizeof(sQ) >= 2 * MT * 16 * 64 * sizeof(float), "partial staging");
+  WorkItem it;
+  if (!my_item(items, meta, it)) return;
+  const int seg0 = it.seg0, n = it.n, tile0 = it.tile0;
+  const int nkb = (n + BM - 1) / BM;
+  const int j0 = (nkb - 1 - it.qb) * BM;
+  const int ntiles = (n + kBN - 1) / kBN;
+  const int qt0 = j0 / kBN;
+  const int tid = thread_x();
+  const int wave = tid / 64, lane = tid % 64;
+  const int kgw = wave % 4, qh = wave / 4;   // key group, query half
+  const int c = lane & 31, g = lane >> 5;
+  const int jw0 = j0 + 32 * kgw;   // the wave's first key
+  const int j = jw0 + c;
+  const bool valid = j < n;
+  const bool wave_on = jw0 < n;
+  const size_t prow = static_cast<size_t>(tile0) * kBN + (valid ? j : n - 1);
+
+  bf16x8 kB[KS], vB[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    kB[ks] = *reinterpret_cast<const bf16x8*>(Kp + prow * D + 16 * ks + 8 * g);
+    vB[ks] = *reinterpret_cast<const bf16x8*>(Vp + prow * D + 16 * ks + 8 * g);
+  }
+  wait_vmcnt<0>();
+  if (!valid) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kB[ks][e] = vB[ks][e] = static_cast<__bf16>(0.f);
+  }
+
+  const int tile0_s = __builtin_amdgcn_readfirstlane(tile0);
+  const int nt_s = __builtin_amdgcn_readfirstlane(ntiles);
+  const int qt0_s = __builtin_amdgcn_readfirstlane(qt0);
+  const int qh_s = __builtin_amdgcn_readfirstlane(qh);
+  const uint16_t* const bQ = Qs + static_cast<size_t>(tile0_s) * TS;
+  const uint16_t* const bdO = dO + static_cast<size_t>(tile0_s) * TS;
+  const uint16_t* const bQt = Qt + static_cast<size_t>(tile0_s) * TS;
+  const uint16_t* const bdOt = dOt + static_cast<size_t>(tile0_s) * TS;
+  const float2* const bLD = LD + static_cast<size_t>(tile0_s) * kBN;
+  const uint32_t nb = static_cast<uint32_t>(nt_s) * TB;
+  const uint32_t nbl = static_cast<uint32_t>(nt_s) * LB;
+  const uint32_t voffR = tile_voffset<D / 8, NT>(tid);
+  const uint32_t voffT = tile_voffset<kBN / 8, NT>(tid);
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t lQ = lds_address(&sQ[0][0]) + wave_s * kWave * 16;
+  const uint32_t ldO = lds_address(&sdO[0][0]) + wave_s * kWave * 16;
+  const uint32_t lQt = lds_address(&sQt[0][0]) + wave_s * kWave * 16;
+  const uint32_t ldOt = lds_address(&sdOt[0][0]) + wave_s * kWave * 16;
+  const uint32_t lLD = lds_address(&sLD[0][0]);
+  auto issue = [&](int qt, int stage) {
+    const uint32_t tb = static_cast<uint32_t>(qt) * TB;
+    tile_dma<KPT, NT>(bQ, nb, tb, lQ + stage * TB, voffR);
+    tile_dma<KPT, NT>(bdO, nb, tb, ldO + stage * TB, voffR);
+    tile_dma<KPT, NT>(bQt, nb, tb, lQt + stage * TB, voffT);
+    tile_dma<KPT, NT>(bdOt, nb, tb, ldOt + stage * TB, voffT);
+    ld_tile_dma(bLD, nbl, static_cast<uint32_t>(qt) * LB, lLD + stage * LB, wave_s, lane);
+  };
+  issue(qt0_s, 0);
+
+  f32x16 aK[MT], aV[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) aK[mt][e] = aV[mt][e] = 0.f;
+  for (int qt = qt0; qt < ntiles; ++qt) {
+    const int st = (qt - qt0) & 1;
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (qt + 1 < ntiles) issue(qt + 1, st ^ 1);
+    const int i0 = qt * kBN + 32 * qh_s;   // the wave's first query of the tile
+    // its 32 queries against its keys: none visible when they end before
+    // the first key
+    if (wave_on && i0 + 31 >= jw0) {
+      // accumulator starts: -lse and -D of query rows 8jj + 4g + i
+      f32x16 S, dP;
+      {
+        f32x16 il, id;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const float4* p = reinterpret_cast<const float4*>(&sLD[st][32 * qh_s + 8 * jj + 4 * g]);
+          const float4 a = p[0], bq = p[1];
+          il[4 * jj] = -a.x;     id[4 * jj] = -a.y;
+          il[4 * jj + 1] = -a.z; id[4 * jj + 1] = -a.w;
+          il[4 * jj + 2] = -bq.x; id[4 * jj + 2] = -bq.y;
+          il[4 * jj + 3] = -bq.z; id[4 * jj + 3] = -bq.w;
+        }
+        tile_half_x_regs<D>(S, sQ[st], kB, il, qh_s, c, g);    // S - lse (log2 units)
+        tile_half_x_regs<D>(dP, sdO[st], vB, id, qh_s, c, g);  // dP - D
+      }
+      if (i0 < jw0 + 32) {   // the diagonal: key j visible to query i iff j <= i
+        const int lim = j - i0 - 4 * g;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (8 * jj + i < lim) S[4 * jj + i] = -INFINITY;
+      }
+      bf16x8 pB[2], dsB[2];
+#pragma unroll
+      for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int a = 8 * kh + e;
+          const float p = __builtin_amdgcn_exp2f(S[a]);
+          pB[kh][e] = static_cast<__bf16>(p);
+          dsB[kh][e] = static_cast<__bf16>(p * dP[a]);
+        }
+      tposed_half_x_c<D>(aV, sdOt[st], pB, qh_s, c, g);
+      tposed_half_x_c<D>(aK, sQt[st], dsB, qh_s, c, g);
+    }
+  }
+  // the two query halves' partials of each key: half 1 stages them in LDS
+  // (the tile stages of its key group), half 0 adds them and stores
+  __syncthreads();   // every wave is done with the tiles
+  float* const stage = kgw == 0 ? reinterpret_cast<float*>(&sQ[0][0])
+                     : kgw == 1 ? reinterpret_cast<float*>(&sdO[0][0])
+                     : kgw == 2 ? reinterpret_cast<float*>(&sQt[0][0])
+                                : reinterpret_cast<float*>(&sdOt[0][0]);
+  if (qh == 1) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        stage[((0 * MT + mt) * 16 + e) * 64 + lane] = aK[mt][e];
+        stage[((1 * MT + mt) * 16 + e) * 64 + lane] = aV[mt][e];
+      }
+  }
+  __syncthreads();
+  if (qh == 1) return;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      aK[mt][e] += stage[((0 * MT + mt) * 16 + e) * 64 + lane];
+      aV[mt][e] += stage[((1 * MT + mt) * 16 + e) * 64 + lane];
+    }
+  if (valid) {
+    // the queries were scaled by scale * log2 e: dk~ = ln 2 * sum dS Qs,
+    // back through the key's rotation; dv as it is
+    const int t = min(static_cast<unsigned>(perm_token[seg0 + j]), static_cast<unsigned>(T - 1));
+    const size_t o = packed ? static_cast<size_t>(seg0 + j) * D : (static_cast<size_t>(it.s) * T + t) * D;
+    const float2* cs =
+        rope_mode == 2 ? nullptr : table + static_cast<size_t>(rope_mode == 0 ? j : t) * (D / 2);
+    store_row_unrotated<D>(dk + o, aK, kLn2, cs, g);
+    store_row_unrotated<D>(dv + o, aV, 1.f, nullptr, g);
+  }
+}
+
 // ---------------------------------------------------------------------------
 struct BwdWs {
   float *Qr, *Kr, *Vp, *dOp, *dQr, *dKr, *dVp, *lse, *Dr, *dgp;
@@ -1155,9 +1366,14 @@ static hipError_t run_bwd_mfma(const void* q, const void* k, const void* v, int 
   prof_mark("bwd_dq", false, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_mark("bwd_dkdv", true, st);
-  k_bwd_dkdv<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
-      w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, table, T,
-      rope_mode, dk, dv, packed ? 1 : 0);
+  if constexpr (D == 128)
+    k_bwd_dkdv8<D><<<static_cast<unsigned>(tl.max_items), 2 * kBwdMfmaThreads, 0, st>>>(
+        w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, table, T,
+        rope_mode, dk, dv, packed ? 1 : 0);
+  else
+    k_bwd_dkdv<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
+        w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, table, T,
+        rope_mode, dk, dv, packed ? 1 : 0);
   prof_mark("bwd_dkdv", false, st);
   return hipGetLastError();
 }
