@@ -1777,15 +1777,8 @@ hipError_t launch_attn_stats(const void* q, const void* k, const void* v, int B,
                              void* ws, AttnTiles& tiles, hipStream_t st) {
   const AttnWs w = carve_attn(ws, B, T, H, K, d, 1);
   const int Nr = B * T * K;
+  // (the backward rotates with the forward's frequencies, no table)
   const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
-  if (rope_mode != 2) {
-    const size_t entries = static_cast<size_t>(T) * (d / 2);
-    const size_t per_block = static_cast<size_t>(kTableThreads) * kTableEntries;
-    k_rope_table<<<static_cast<unsigned>((entries + per_block - 1) / per_block), kTableThreads, 0,
-                   st>>>(T, d, log_base, w.table);
-  }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
   const float sl2 = scale * 1.4426950408889634f;
   if (d == 64)
     launch_mfma<64>(w, q, k, v, B, T, H, 1, Nr, rope_mode, log_base, sl2, seg_offsets,
@@ -1795,7 +1788,7 @@ hipError_t launch_attn_stats(const void* q, const void* k, const void* v, int B,
                      perm_token, w.hpack, false, lse, st);
   tiles.Kp = w.Kp;
   tiles.Vt = w.Vt;
-  tiles.table = w.table;
+  tiles.freq = w.freq;
   tiles.items = w.items;
   tiles.meta = w.meta;
   tiles.h = w.hpack;

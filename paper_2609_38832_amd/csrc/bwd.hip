@@ -473,6 +473,7 @@ struct BwdPackLds {
   int off[kBwdSegLds + 1];
   int tok[kBN], ks[kBN];       // per tile row: token, k slot (-1: none)
   float g[kBN];                // per tile row: gate
+  double freq[D / 2];          // RoPE theta_j / (2 pi)
 };
 
 template <int D>
@@ -480,7 +481,7 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ v,
     const float* __restrict__ dout, const int32_t* __restrict__ topk_idx,
     const float* __restrict__ gates, const int32_t* __restrict__ seg_offsets,
-    const int32_t* __restrict__ perm_token, const float2* __restrict__ table,
+    const int32_t* __restrict__ perm_token, const double* __restrict__ freq,
     const uint16_t* __restrict__ Kp, const float* __restrict__ hpack,
     const float* __restrict__ lse, int BH, int H, int T, int K, int Nr, int rope_mode,
     float scale_log2, uint16_t* __restrict__ Qs, uint16_t* __restrict__ dO,
@@ -490,6 +491,8 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
   const int gt = block_x();
   const int tid = thread_x();
   const bool in_lds = BH <= kBwdSegLds;
+  // (published by the barrier before the rows are packed)
+  if (rope_mode != 2 && tid < D / 2) L.freq[tid] = freq[tid];
   if (in_lds) {
     for (int i = tid; i <= BH; i += kBwdPackThreads) L.off[i] = seg_offsets[i];
     __syncthreads();
@@ -548,7 +551,8 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
       unpack8(*reinterpret_cast<const uint4*>(qrow + D / 2 + 8 * c), x2);
       if (rope_mode != 2) {
         float4 cs[4];
-        load_rope8(cs, table + static_cast<size_t>(rope_mode == 0 ? r : t) * (D / 2) + 8 * c);
+        // the factors the forward rotated its queries with
+        rope8_rev(cs, static_cast<double>(rope_mode == 0 ? r : t), &L.freq[8 * c]);
         rope8(x1, x2, cs);
       }
 #pragma unroll
@@ -736,11 +740,12 @@ NAMOH_DEV void ld_tile_dma(const float2* base, uint32_t nbytes, uint32_t tile_by
 // acc[mt][4j + i] holds element 32 mt + 8 j + 4 g + i, times f.  The RoPE
 // pair partner of element x < d/2 is x + d/2, in tile mt + d/64 of the same
 // lane, so the gradient goes back through the rotation in registers:
-// x' = (x1 c - x2 s, x2 c + x1 s) gives (d1 c + d2 s, d2 c - d1 s).  cs: the
-// (cos, sin) table row of the position, or NULL for no rotation.
+// x' = (x1 c - x2 s, x2 c + x1 s) gives (d1 c + d2 s, d2 c - d1 s).  The
+// factors of position pos are formed as the forward's (freq: theta_j /
+// (2 pi) of the pairs, or NULL for no rotation).
 template <int D>
 NAMOH_DEV void store_row_unrotated(float* __restrict__ dst, const f32x16 (&acc)[D / 32], float f,
-                                   const float2* __restrict__ cs, int g) {
+                                   const double* __restrict__ freq, double pos, int g) {
   constexpr int MH = D / 64;
 #pragma unroll
   for (int mt = 0; mt < MH; ++mt)
@@ -753,15 +758,13 @@ NAMOH_DEV void store_row_unrotated(float* __restrict__ dst, const f32x16 (&acc)[
         a[i] = acc[mt][4 * j + i] * f;
         b2[i] = acc[mt + MH][4 * j + i] * f;
       }
-      if (cs != nullptr) {
-        const float4 w01 = *reinterpret_cast<const float4*>(cs + x);
-        const float4 w23 = *reinterpret_cast<const float4*>(cs + x + 2);
-        const float cc[4] = {w01.x, w01.z, w23.x, w23.z}, sn[4] = {w01.y, w01.w, w23.y, w23.w};
+      if (freq != nullptr) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
+          const float2 w = rope_cs_rev(pos, freq[x + i]);
           const float d1 = a[i], d2 = b2[i];
-          a[i] = d1 * cc[i] + d2 * sn[i];
-          b2[i] = d2 * cc[i] - d1 * sn[i];
+          a[i] = d1 * w.x + d2 * w.y;
+          b2[i] = d2 * w.x - d1 * w.y;
         }
       }
       *reinterpret_cast<float4*>(dst + x) = make_float4(a[0], a[1], a[2], a[3]);
@@ -813,7 +816,7 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
     const float2* __restrict__ LD, const uint16_t* __restrict__ Kp,
     const uint16_t* __restrict__ Vp, const uint16_t* __restrict__ Kt,
     const WorkItem* __restrict__ items, const int32_t* __restrict__ meta,
-    const int32_t* __restrict__ perm_token, const float2* __restrict__ table, int T,
+    const int32_t* __restrict__ perm_token, const double* __restrict__ freq, int T,
     int rope_mode, float scale, float* __restrict__ dq, int packed) {
   constexpr int NT = kBwdMfmaThreads, BM = kBwdMfmaBlock;
   constexpr int KS = D / 16, MT = D / 32;
@@ -932,10 +935,10 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
   }
   if (valid) {   // dq~ = scale sum_j dS k~_j, back through the query's rotation
     const int t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
-    const float2* cs =
-        rope_mode == 2 ? nullptr : table + static_cast<size_t>(rope_mode == 0 ? r : t) * (D / 2);
+    const double* fq = rope_mode == 2 ? nullptr : freq;
+    const double pos = rope_mode == 0 ? r : t;
     const size_t o = packed ? static_cast<size_t>(seg0 + r) * D : (static_cast<size_t>(it.s) * T + t) * D;
-    store_row_unrotated<D>(dq + o, acc, scale, cs, g);
+    store_row_unrotated<D>(dq + o, acc, scale, fq, pos, g);
   }
 }
 
@@ -947,7 +950,7 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
     const float2* __restrict__ LD, const uint16_t* __restrict__ Kp,
     const uint16_t* __restrict__ Vp, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ meta, const int32_t* __restrict__ perm_token,
-    const float2* __restrict__ table, int T, int rope_mode, float* __restrict__ dk,
+    const double* __restrict__ freq, int T, int rope_mode, float* __restrict__ dk,
     float* __restrict__ dv, int packed) {
   constexpr int NT = kBwdMfmaThreads, BM = kBwdMfmaBlock;
   constexpr int KS = D / 16, MT = D / 32;
@@ -1079,10 +1082,10 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
     // back through the key's rotation; dv as it is
     const int t = min(static_cast<unsigned>(perm_token[seg0 + j]), static_cast<unsigned>(T - 1));
     const size_t o = packed ? static_cast<size_t>(seg0 + j) * D : (static_cast<size_t>(it.s) * T + t) * D;
-    const float2* cs =
-        rope_mode == 2 ? nullptr : table + static_cast<size_t>(rope_mode == 0 ? j : t) * (D / 2);
-    store_row_unrotated<D>(dk + o, aK, kLn2, cs, g);
-    store_row_unrotated<D>(dv + o, aV, 1.f, nullptr, g);
+    const double* fq = rope_mode == 2 ? nullptr : freq;
+    const double pos = rope_mode == 0 ? j : t;
+    store_row_unrotated<D>(dk + o, aK, kLn2, fq, pos, g);
+    store_row_unrotated<D>(dv + o, aV, 1.f, nullptr, 0.0, g);
   }
 }
 
@@ -1099,7 +1102,7 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
     const float2* __restrict__ LD, const uint16_t* __restrict__ Kp,
     const uint16_t* __restrict__ Vp, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ meta, const int32_t* __restrict__ perm_token,
-    const float2* __restrict__ table, int T, int rope_mode, float* __restrict__ dk,
+    const double* __restrict__ freq, int T, int rope_mode, float* __restrict__ dk,
     float* __restrict__ dv, int packed) {
   constexpr int NT = 2 * kBwdMfmaThreads, BM = kBwdMfmaBlock;
   constexpr int KS = D / 16, MT = D / 32;
@@ -1258,10 +1261,10 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
     // back through the key's rotation; dv as it is
     const int t = min(static_cast<unsigned>(perm_token[seg0 + j]), static_cast<unsigned>(T - 1));
     const size_t o = packed ? static_cast<size_t>(seg0 + j) * D : (static_cast<size_t>(it.s) * T + t) * D;
-    const float2* cs =
-        rope_mode == 2 ? nullptr : table + static_cast<size_t>(rope_mode == 0 ? j : t) * (D / 2);
-    store_row_unrotated<D>(dk + o, aK, kLn2, cs, g);
-    store_row_unrotated<D>(dv + o, aV, 1.f, nullptr, g);
+    const double* fq = rope_mode == 2 ? nullptr : freq;
+    const double pos = rope_mode == 0 ? j : t;
+    store_row_unrotated<D>(dk + o, aK, kLn2, fq, pos, g);
+    store_row_unrotated<D>(dv + o, aV, 1.f, nullptr, 0.0, g);
   }
 }
 
@@ -1351,28 +1354,28 @@ static hipError_t run_bwd_mfma(const void* q, const void* k, const void* v, int 
                              st>>>(topk_idx, H, T, K, rows, dq, dk, dv);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  const float2* table = static_cast<const float2*>(tl.table);
+  const double* freq = tl.freq;
   prof_mark("bwd_pack", true, st);
   k_bwd_pack<D><<<static_cast<unsigned>(tl.max_tiles), kBwdPackThreads, 0, st>>>(
       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(v), dout, topk_idx, gates,
-      seg_offsets, perm_token, table, tl.Kp, tl.h, w.lse, BH, H, T, K, Nr, rope_mode,
+      seg_offsets, perm_token, freq, tl.Kp, tl.h, w.lse, BH, H, T, K, Nr, rope_mode,
       scale * kLog2e, w.Qs, w.dO, w.Vp, w.Qt, w.dOt, w.Kt, w.LD, dgates);
   prof_mark("bwd_pack", false, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_mark("bwd_dq", true, st);
   k_bwd_dq<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
-      w.Qs, w.dO, w.LD, tl.Kp, w.Vp, w.Kt, tl.items, tl.meta, perm_token, table, T, rope_mode,
+      w.Qs, w.dO, w.LD, tl.Kp, w.Vp, w.Kt, tl.items, tl.meta, perm_token, freq, T, rope_mode,
       scale, dq, packed ? 1 : 0);
   prof_mark("bwd_dq", false, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_mark("bwd_dkdv", true, st);
   if constexpr (D == 128)
     k_bwd_dkdv8<D><<<static_cast<unsigned>(tl.max_items), 2 * kBwdMfmaThreads, 0, st>>>(
-        w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, table, T,
+        w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, freq, T,
         rope_mode, dk, dv, packed ? 1 : 0);
   else
     k_bwd_dkdv<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
-        w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, table, T,
+        w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, freq, T,
         rope_mode, dk, dv, packed ? 1 : 0);
   prof_mark("bwd_dkdv", false, st);
   return hipGetLastError();

@@ -58,7 +58,7 @@ struct WorkItem;
 struct AttnTiles {
   const uint16_t* Kp;      // rotated keys, bf16, 64-row tiles [max_tiles * 64, d]
   const uint16_t* Vt;      // values, bf16, per tile transposed [max_tiles, d, 64]
-  const void* table;       // RoPE (cos, sin) float pairs [T, d / 2]
+  const double* freq;      // RoPE theta_j / (2 pi), double [d / 2] (as the forward rotates)
   const WorkItem* items;   // (segment, query block) work list, heaviest first
   const int32_t* meta;     // item count, validity flag
   float* h;                // head outputs, f32 packed [Nr, d]
