@@ -467,11 +467,21 @@ def bench_backward(w, args, torch, L, DI):
     dense = {"dq": torch.empty(B, H, T, d, **f32), "dk": torch.empty(B, H, T, d, **f32),
              "dv": torch.empty(B, H, T, d, **f32), "dgates": torch.empty(B, T, K, **f32)}
 
-    def step(packed=True):
+    mfma = w.dtype == "bf16" and d in (64, 128)
+
+    def step(packed=True, saved=True):
+        # saved: the training forward leaves its statistics and tiles in the
+        # backward's workspace, which the backward reuses; otherwise the
+        # stateless forward, and a backward that reruns the forward itself
         L.route(logits, K, L.GATE_SOFTMAX_SELECTED, out=routing, ws=rws)
-        L.attn_fwd(q, k, v, routing, K, w.rope_base, L.ROPE_HEAD_RELATIVE, out=out, ws=aws)
         g = grads if packed else dense
-        L.attn_bwd(q, k, v, routing, K, w.rope_base, dout, ws=bws, out=g, packed=packed)
+        if saved and mfma:
+            L.attn_fwd_train(q, k, v, routing, K, w.rope_base, bws, out=out)
+            L.attn_bwd(q, k, v, routing, K, w.rope_base, dout, ws=bws, out=g, packed=packed,
+                       saved=True)
+        else:
+            L.attn_fwd(q, k, v, routing, K, w.rope_base, L.ROPE_HEAD_RELATIVE, out=out, ws=aws)
+            L.attn_bwd(q, k, v, routing, K, w.rope_base, dout, ws=bws, out=g, packed=packed)
         L.route_bwd(logits, routing, g["dgates"])
 
     log(f"warmup {args.warmup} steps")
@@ -494,6 +504,14 @@ def bench_backward(w, args, torch, L, DI):
     e1.record()
     torch.cuda.synchronize()
     ms_step_dense = e0.elapsed_time(e1) / args.steps
+    for _ in range(args.warmup):
+        step(saved=False)
+    e0.record()
+    for _ in range(args.steps):
+        step(saved=False)
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step_rerun = e0.elapsed_time(e1) / args.steps
     L.profile_enable(2 * args.steps)
     for _ in range(args.steps):
         step()
@@ -504,7 +522,6 @@ def bench_backward(w, args, torch, L, DI):
         if r is not None and r[1] > 0:
             kern[sec] = r[0] / r[1]
     L.profile_enable(0)
-    mfma = w.dtype == "bf16" and d in (64, 128)
     # the backward's products per causal (query, key) pair: dP = dO V^T, the
     # recomputed scores, dV += P^T dO, dQ += dS K, dK += dS^T Q: 2d FLOP each;
     # the algorithmic count is 10 d (scores counted once); the two kernels
@@ -520,8 +537,10 @@ def bench_backward(w, args, torch, L, DI):
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": w.dtype, "data": "synthetic",
            "ms_per_step_dense_grads": round(ms_step_dense, 4),
+           "ms_per_step_forward_rerun": round(ms_step_rerun, 4),
            "config": {"workload": w.name, "B": B, "T": T, "H": H, "K": K, "d_head": d,
                       "pass": "training step", "gradients": "packed (routed pairs)",
+                      "forward_state": "saved by the training forward" if mfma else "recomputed",
                       "rope": "head-relative",
                       "rope_base": w.rope_base, "gates": "softmax over selected"},
            "roofline": {"kernel": "k_bwd_dq + k_bwd_dkdv" if mfma else "k_bwd_q + k_bwd_kv",

@@ -213,6 +213,38 @@ namoh_status namoh_attn_bwd_packed(const void* q, const void* k, const void* v, 
                                    float* dk, float* dv, float* dgates, void* workspace,
                                    size_t workspace_bytes, void* stream);
 
+/* Training forward, Sec. 3.2 "Efficient execution" (training runs the same
+ * packed varlen attention as prefill) with Sec. 3.1, Eq. namoh-attention:
+ * the layer output of namoh_attn_fwd (same inputs; out [B, T, d] in
+ * out_dtype, combined from float32 head outputs) and, in `workspace`, what
+ * the backward needs from the forward: every routed row's log-sum-exp and
+ * head output, the rotated key / value tiles and the work list.
+ * namoh_attn_bwd_saved then takes them from there instead of running the
+ * forward a second time.  dtype must be NAMOH_BF16 and d_head 64 or 128
+ * (otherwise NAMOH_ERR_UNSUPPORTED).  Workspace: at least
+ * namoh_attn_bwd_workspace_size(B, T, H, K, d_head) bytes, 256-byte
+ * aligned; the caller keeps it unchanged until the backward has run. */
+namoh_status namoh_attn_fwd_train(const void* q, const void* k, const void* v, int dtype,
+                                  int B, int T, int H, int K, int d_head, float rope_base,
+                                  int rope_mode, float softmax_scale, const float* gates,
+                                  const int32_t* seg_offsets, const int32_t* perm_token,
+                                  const int32_t* slot_pos, void* out, int out_dtype,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* namoh_attn_bwd (packed = 0) or namoh_attn_bwd_packed (packed = 1) on the
+ * state a namoh_attn_fwd_train with the same inputs, sizes and routing left
+ * in `workspace`: the gradients are those of the stateless calls, bit for
+ * bit.  dtype NAMOH_BF16, d_head 64 or 128 (otherwise
+ * NAMOH_ERR_UNSUPPORTED); other arguments, outputs and limits as there.
+ * The workspace may not have been used by another call in between. */
+namoh_status namoh_attn_bwd_saved(const void* q, const void* k, const void* v, int dtype, int B,
+                                  int T, int H, int K, int d_head, float rope_base,
+                                  int rope_mode, float softmax_scale, const int32_t* topk_idx,
+                                  const float* gates, const int32_t* seg_offsets,
+                                  const int32_t* perm_token, const float* dout, float* dq,
+                                  float* dk, float* dv, float* dgates, int packed,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
 /* Gradient of the gates with respect to the router logits, the selection
  * held fixed (Sec. 3.1, Eq. namoh-gates; the router learns through the
  * gates).  gate_mode SOFTMAX_SELECTED: dl_j = g_j (dg_j - sum_k g_k dg_k)

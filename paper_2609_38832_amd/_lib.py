@@ -33,7 +33,7 @@ EXPORTED = (
     "namoh_route_workspace_size", "namoh_route", "namoh_route_biased", "namoh_route_bias_update",
     "namoh_attn_fwd_workspace_size", "namoh_attn_fwd",
     "namoh_prefill_cache", "namoh_attn_bwd_workspace_size", "namoh_attn_bwd",
-    "namoh_attn_bwd_packed", "namoh_route_bwd",
+    "namoh_attn_bwd_packed", "namoh_attn_fwd_train", "namoh_attn_bwd_saved", "namoh_route_bwd",
     "namoh_decode_workspace_size", "namoh_decode_step", "namoh_decode_step_biased",
     "namoh_decode_step_noalloc",
     "namoh_qkv_proj", "namoh_out_proj_workspace_size", "namoh_out_proj",
@@ -64,6 +64,10 @@ _SIGS = {
                             _P, _P, _P, _P, _P, _S, _P]),
     "namoh_attn_bwd_packed": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F, _P, _P, _P,
                                    _P, _P, _P, _P, _P, _P, _P, _S, _P]),
+    "namoh_attn_fwd_train": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F,
+                                  _P, _P, _P, _P, _P, _I, _P, _S, _P]),
+    "namoh_attn_bwd_saved": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F, _P, _P, _P,
+                                  _P, _P, _P, _P, _P, _P, _I, _P, _S, _P]),
     "namoh_route_bwd": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "namoh_decode_workspace_size": (_S, [_I, _I, _I, _I, _I]),
     "namoh_decode_step": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I,
@@ -335,15 +339,39 @@ def prefill_cache(k: torch.Tensor, v: torch.Tensor, r: dict, K: int, rope_base: 
                                     _ptr(cache_len), cap, _stream(k.device)))
 
 
+def attn_fwd_train(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K: int,
+                   rope_base: float, ws: torch.Tensor, rope_mode: int = ROPE_HEAD_RELATIVE,
+                   softmax_scale: float = 0.0, out_dtype: Optional[torch.dtype] = None,
+                   out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """namoh_attn_fwd_train: the layer output [B, T, d]; `ws` (at least
+    namoh_attn_bwd_workspace_size bytes) keeps the state attn_bwd(...,
+    saved=True) reads back."""
+    _need_cuda(q, k, v, out, ws)
+    B, H, T, d = q.shape
+    if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
+        raise ValueError("q, k, v must share shape and dtype")
+    odt = q.dtype if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty(B, T, d, dtype=odt, device=q.device)
+    check(lib().namoh_attn_fwd_train(_ptr(q), _ptr(k), _ptr(v), dtype_code(q.dtype), B, T, H, K,
+                                     d, float(rope_base), rope_mode, float(softmax_scale),
+                                     _ptr(routing["gates"]), _ptr(routing["seg_offsets"]),
+                                     _ptr(routing["perm_token"]), _ptr(routing["slot_pos"]),
+                                     _ptr(out), dtype_code(out.dtype), _ptr(ws), ws.numel(),
+                                     _stream(q.device)))
+    return out
+
+
 def attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K: int,
              rope_base: float, dout: torch.Tensor, rope_mode: int = ROPE_HEAD_RELATIVE,
              softmax_scale: float = 0.0, ws: Optional[torch.Tensor] = None,
-             out: Optional[dict] = None, packed: bool = False) -> dict:
+             out: Optional[dict] = None, packed: bool = False, saved: bool = False) -> dict:
     """namoh_attn_bwd: gradients dq, dk, dv [B, H, T, d] and dgates [B, T, K]
     (float32) for the upstream gradient dout float32 [B, T, d]; `out` may
     hold preallocated tensors of those shapes under the same keys.  With
     packed=True, namoh_attn_bwd_packed: dq, dk, dv [B*T*K, d] in the
-    routing's packed order."""
+    routing's packed order.  With saved=True, namoh_attn_bwd_saved on the
+    state attn_fwd_train left in `ws`."""
     _need_cuda(q, k, v, dout)
     B, H, T, d = q.shape
     if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
@@ -361,14 +389,19 @@ def attn_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, routing: dict, K
                 or not out[key].is_contiguous():
             raise ValueError(f"out[{key!r}] must be contiguous float32 {shape}")
     if ws is None:
+        if saved:
+            raise ValueError("saved=True needs the workspace attn_fwd_train used")
         ws = workspace(int(lib().namoh_attn_bwd_workspace_size(B, T, H, K, d)), dev)
-    fn = lib().namoh_attn_bwd_packed if packed else lib().namoh_attn_bwd
-    check(fn(_ptr(q), _ptr(k), _ptr(v), dtype_code(q.dtype), B, T, H, K, d,
-                               float(rope_base), rope_mode, float(softmax_scale),
-                               _ptr(routing["topk_idx"]), _ptr(routing["gates"]),
-                               _ptr(routing["seg_offsets"]), _ptr(routing["perm_token"]),
-                               _ptr(dout), _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]),
-                               _ptr(out["dgates"]), _ptr(ws), ws.numel(), _stream(dev)))
+    args = (_ptr(q), _ptr(k), _ptr(v), dtype_code(q.dtype), B, T, H, K, d, float(rope_base),
+            rope_mode, float(softmax_scale), _ptr(routing["topk_idx"]), _ptr(routing["gates"]),
+            _ptr(routing["seg_offsets"]), _ptr(routing["perm_token"]), _ptr(dout),
+            _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]), _ptr(out["dgates"]))
+    if saved:
+        check(lib().namoh_attn_bwd_saved(*args, 1 if packed else 0, _ptr(ws), ws.numel(),
+                                         _stream(dev)))
+    else:
+        fn = lib().namoh_attn_bwd_packed if packed else lib().namoh_attn_bwd
+        check(fn(*args, _ptr(ws), ws.numel(), _stream(dev)))
     return out
 
 

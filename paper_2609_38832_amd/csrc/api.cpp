@@ -60,6 +60,18 @@ namoh_status check_sizes(int B, int T, int H, int K) {
   return NAMOH_OK;
 }
 
+// The MFMA kernels address one segment's packed key/value tiles with 32-bit
+// buffer offsets.
+namoh_status check_segment_bytes(int dtype, int T, int d_head) {
+  if (dtype == NAMOH_BF16 && (d_head == 64 || d_head == 128)) {
+    const long long seg_bytes = (static_cast<long long>(T) + 63) / 64 * 64 * d_head * 2;
+    if (seg_bytes >= (1ll << 32))
+      return fail(NAMOH_ERR_UNSUPPORTED, "T = %d too long for d_head = %d on the bf16 path", T,
+                  d_head);
+  }
+  return NAMOH_OK;
+}
+
 namoh_status check_head_width(int d) {
   if (d != 32 && d != 64 && d != 128)
     return fail(NAMOH_ERR_UNSUPPORTED, "d_head must be 32, 64 or 128 (got %d)", d);
@@ -216,14 +228,7 @@ namoh_status namoh_attn_fwd(const void* q, const void* k, const void* v, int dty
   REQUIRE(!std::isnan(softmax_scale) && !std::isinf(softmax_scale), "softmax_scale must be finite");
   const long long dense = static_cast<long long>(B) * H * T * d_head;
   REQUIRE(dense < (1ll << 40), "q/k/v too large");
-  if (dtype == NAMOH_BF16 && (d_head == 64 || d_head == 128)) {
-    // the MFMA kernel addresses one segment's packed key/value tiles with
-    // 32-bit buffer offsets
-    const long long seg_bytes = (static_cast<long long>(T) + 63) / 64 * 64 * d_head * 2;
-    if (seg_bytes >= (1ll << 32))
-      return fail(NAMOH_ERR_UNSUPPORTED, "T = %d too long for d_head = %d on the bf16 path", T,
-                  d_head);
-  }
+  if ((s = check_segment_bytes(dtype, T, d_head)) != NAMOH_OK) return s;
   REQUIRE_PTR(q, 16);
   REQUIRE_PTR(k, 16);
   REQUIRE_PTR(v, 16);
@@ -460,7 +465,8 @@ static namoh_status attn_bwd_common(const void* q, const void* k, const void* v,
                                     const float* gates, const int32_t* seg_offsets,
                                     const int32_t* perm_token, const float* dout, float* dq,
                                     float* dk, float* dv, float* dgates, void* workspace,
-                                    size_t workspace_bytes, void* stream, bool packed) {
+                                    size_t workspace_bytes, void* stream, bool packed,
+                                    bool saved = false) {
   namoh_status s;
   if ((s = check_sizes(B, T, H, K)) != NAMOH_OK) return s;
   if ((s = check_head_width(d_head)) != NAMOH_OK) return s;
@@ -473,6 +479,11 @@ static namoh_status attn_bwd_common(const void* q, const void* k, const void* v,
   REQUIRE(!std::isnan(softmax_scale) && !std::isinf(softmax_scale), "softmax_scale must be finite");
   REQUIRE(static_cast<long long>(B) * H * T * d_head < (1ll << 40), "q/k/v too large");
   REQUIRE(B * H <= 65535, "B*H = %d segments exceed the backward grid", B * H);
+  if ((s = check_segment_bytes(dtype, T, d_head)) != NAMOH_OK) return s;
+  if (saved && !namoh::attn_train_supported(dtype, d_head))
+    return fail(NAMOH_ERR_UNSUPPORTED,
+                "namoh_attn_bwd_saved needs dtype bf16 and d_head 64 or 128 (got dtype %d, "
+                "d_head %d)", dtype, d_head);
   REQUIRE_PTR(q, 16);
   REQUIRE_PTR(k, 16);
   REQUIRE_PTR(v, 16);
@@ -493,7 +504,7 @@ static namoh_status attn_bwd_common(const void* q, const void* k, const void* v,
   return launched(stream, namoh::launch_attn_bwd(q, k, v, dtype, B, T, H, K, d_head, rope_base,
                                            rope_mode, scale, topk_idx, gates, seg_offsets,
                                            perm_token, dout, dq, dk, dv, dgates, workspace,
-                                           static_cast<hipStream_t>(stream), packed));
+                                           static_cast<hipStream_t>(stream), packed, saved));
 }
 
 namoh_status namoh_attn_bwd(const void* q, const void* k, const void* v, int dtype, int B, int T,
@@ -517,6 +528,61 @@ namoh_status namoh_attn_bwd_packed(const void* q, const void* k, const void* v, 
   return attn_bwd_common(q, k, v, dtype, B, T, H, K, d_head, rope_base, rope_mode, softmax_scale,
                          topk_idx, gates, seg_offsets, perm_token, dout, dq, dk, dv, dgates,
                          workspace, workspace_bytes, stream, true);
+}
+
+namoh_status namoh_attn_bwd_saved(const void* q, const void* k, const void* v, int dtype, int B,
+                                  int T, int H, int K, int d_head, float rope_base,
+                                  int rope_mode, float softmax_scale, const int32_t* topk_idx,
+                                  const float* gates, const int32_t* seg_offsets,
+                                  const int32_t* perm_token, const float* dout, float* dq,
+                                  float* dk, float* dv, float* dgates, int packed,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+  REQUIRE(packed == 0 || packed == 1, "packed must be 0 or 1 (got %d)", packed);
+  return attn_bwd_common(q, k, v, dtype, B, T, H, K, d_head, rope_base, rope_mode, softmax_scale,
+                         topk_idx, gates, seg_offsets, perm_token, dout, dq, dk, dv, dgates,
+                         workspace, workspace_bytes, stream, packed == 1, true);
+}
+
+namoh_status namoh_attn_fwd_train(const void* q, const void* k, const void* v, int dtype, int B,
+                                  int T, int H, int K, int d_head, float rope_base,
+                                  int rope_mode, float softmax_scale, const float* gates,
+                                  const int32_t* seg_offsets, const int32_t* perm_token,
+                                  const int32_t* slot_pos, void* out, int out_dtype,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+  namoh_status s;
+  if ((s = check_sizes(B, T, H, K)) != NAMOH_OK) return s;
+  if ((s = check_head_width(d_head)) != NAMOH_OK) return s;
+  REQUIRE(dtype == NAMOH_F32 || dtype == NAMOH_BF16, "unknown dtype %d", dtype);
+  REQUIRE(out_dtype == NAMOH_F32 || out_dtype == NAMOH_BF16, "unknown out_dtype %d", out_dtype);
+  REQUIRE(rope_mode == NAMOH_ROPE_HEAD_RELATIVE || rope_mode == NAMOH_ROPE_GLOBAL ||
+              rope_mode == NAMOH_ROPE_NONE,
+          "unknown rope_mode %d", rope_mode);
+  REQUIRE(rope_mode == NAMOH_ROPE_NONE || (std::isfinite(rope_base) && rope_base > 0.f),
+          "rope_base must be finite and > 0 (got %g)", static_cast<double>(rope_base));
+  REQUIRE(!std::isnan(softmax_scale) && !std::isinf(softmax_scale), "softmax_scale must be finite");
+  REQUIRE(static_cast<long long>(B) * H * T * d_head < (1ll << 40), "q/k/v too large");
+  if ((s = check_segment_bytes(dtype, T, d_head)) != NAMOH_OK) return s;
+  if (!namoh::attn_train_supported(dtype, d_head))
+    return fail(NAMOH_ERR_UNSUPPORTED,
+                "namoh_attn_fwd_train needs dtype bf16 and d_head 64 or 128 (got dtype %d, "
+                "d_head %d)", dtype, d_head);
+  REQUIRE_PTR(q, 16);
+  REQUIRE_PTR(k, 16);
+  REQUIRE_PTR(v, 16);
+  REQUIRE_PTR(gates, 4);
+  REQUIRE_PTR(seg_offsets, 4);
+  REQUIRE_PTR(perm_token, 4);
+  REQUIRE_PTR(slot_pos, 4);
+  REQUIRE_PTR(out, 16);
+  if ((s = check_workspace(workspace, workspace_bytes,
+                           namoh::attn_bwd_workspace_bytes(B, T, H, K, d_head))) != NAMOH_OK)
+    return s;
+  const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
+  clear_hip_error();
+  return launched(stream, namoh::launch_train_fwd(q, k, v, dtype, B, T, H, K, d_head, rope_base,
+                                                  rope_mode, scale, gates, seg_offsets,
+                                                  perm_token, slot_pos, out, out_dtype,
+                                                  workspace, static_cast<hipStream_t>(stream)));
 }
 
 namoh_status namoh_route_bwd(const float* logits, const int32_t* topk_idx, const float* gates,

@@ -1627,6 +1627,20 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   return hipGetLastError();
 }
 
+hipError_t launch_combine_f32(const float* rows, const float* gates, const int32_t* slot_pos,
+                              long BT, int K, int D, int Nr, void* out, int out_dtype,
+                              hipStream_t st) {
+  const long threads = BT * (D / 8);
+  const unsigned grid = static_cast<unsigned>((threads + kCombineThreads - 1) / kCombineThreads);
+  if (out_dtype == 1)
+    launch_k("combine", k_combine<false, true, 1>, dim3(grid), dim3(kCombineThreads), st, rows,
+             gates, slot_pos, BT, K, D, Nr, 1, out);
+  else
+    launch_k("combine", k_combine<false, false, 1>, dim3(grid), dim3(kCombineThreads), st, rows,
+             gates, slot_pos, BT, K, D, Nr, 1, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_combine_rows(const uint16_t* rows, const float* gates, const int32_t* slot_pos,
                                long BT, int K, int D, int Nr, void* out, int out_dtype,
                                hipStream_t st) {
@@ -1771,6 +1785,19 @@ hipError_t launch_shared(const void* q, const void* k, const void* v, int B, int
 // packed head outputs and the per-row log-sum-exp in log2 units of the
 // scores scaled by scale * log2 e.  The workspace is laid out as for
 // launch_attn; `tiles` receives where each piece lives.
+void attn_stats_tiles(void* ws, int B, int T, int H, int K, int d, AttnTiles& tiles) {
+  const AttnWs w = carve_attn(ws, B, T, H, K, d, 1);
+  tiles.Kp = w.Kp;
+  tiles.Vt = w.Vt;
+  tiles.freq = w.freq;
+  tiles.items = w.items;
+  tiles.meta = w.meta;
+  tiles.h = w.hpack;
+  tiles.max_items = static_cast<int>(w.max_items);
+  tiles.max_tiles = static_cast<int>(w.max_tiles);
+  tiles.BM = block_queries(d, 1);
+}
+
 hipError_t launch_attn_stats(const void* q, const void* k, const void* v, int B, int T, int H,
                              int K, int d, float rope_base, int rope_mode, float scale,
                              const int32_t* seg_offsets, const int32_t* perm_token, float* lse,
@@ -1786,15 +1813,7 @@ hipError_t launch_attn_stats(const void* q, const void* k, const void* v, int B,
   else
     launch_mfma<128>(w, q, k, v, B, T, H, 1, Nr, rope_mode, log_base, sl2, seg_offsets,
                      perm_token, w.hpack, false, lse, st);
-  tiles.Kp = w.Kp;
-  tiles.Vt = w.Vt;
-  tiles.freq = w.freq;
-  tiles.items = w.items;
-  tiles.meta = w.meta;
-  tiles.h = w.hpack;
-  tiles.max_items = static_cast<int>(w.max_items);
-  tiles.max_tiles = static_cast<int>(w.max_tiles);
-  tiles.BM = block_queries(d, 1);
+  attn_stats_tiles(ws, B, T, H, K, d, tiles);
   return hipGetLastError();
 }
 

@@ -1337,13 +1337,18 @@ static hipError_t run_bwd_mfma(const void* q, const void* k, const void* v, int 
                                const int32_t* topk_idx, const float* gates,
                                const int32_t* seg_offsets, const int32_t* perm_token,
                                const float* dout, float* dq, float* dk, float* dv,
-                               float* dgates, void* ws, hipStream_t st, bool packed) {
+                               float* dgates, void* ws, hipStream_t st, bool packed,
+                               bool saved) {
   const BwdMfmaWs w = carve_bwd_mfma(ws, B, T, H, K, D);
   const int BH = B * H;
   const int Nr = B * T * K;
   AttnTiles tl;
-  hipError_t e = launch_attn_stats(q, k, v, B, T, H, K, D, rope_base, rope_mode, scale,
-                                   seg_offsets, perm_token, w.lse, w.attn, tl, st);
+  hipError_t e = hipSuccess;
+  if (saved)   // launch_train_fwd left the statistics and tiles in this workspace
+    attn_stats_tiles(w.attn, B, T, H, K, D, tl);
+  else
+    e = launch_attn_stats(q, k, v, B, T, H, K, D, rope_base, rope_mode, scale, seg_offsets,
+                          perm_token, w.lse, w.attn, tl, st);
   if (e != hipSuccess) return e;
   if (tl.BM != kBwdMfmaBlock || static_cast<size_t>(tl.max_tiles) * kBN > w.rows)
     return hipErrorInvalidValue;   // the forward's blocks and tiles must match these kernels
@@ -1425,22 +1430,45 @@ hipError_t launch_attn_bwd(const void* q, const void* k, const void* v, int dtyp
                            const int32_t* topk_idx, const float* gates,
                            const int32_t* seg_offsets, const int32_t* perm_token,
                            const float* dout, float* dq, float* dk, float* dv, float* dgates,
-                           void* ws, hipStream_t st, bool packed) {
+                           void* ws, hipStream_t st, bool packed, bool saved) {
 #define NAMOH_BWD(DD, BF)                                                                      \
   return run_bwd<DD, BF>(q, k, v, B, T, H, K, rope_base, rope_mode, scale, topk_idx, gates,   \
                          seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st, packed)
   if (bwd_uses_mfma(dtype, d)) {
     if (d == 64)
       return run_bwd_mfma<64>(q, k, v, B, T, H, K, rope_base, rope_mode, scale, topk_idx, gates,
-                              seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st, packed);
+                              seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st, packed,
+                              saved);
     return run_bwd_mfma<128>(q, k, v, B, T, H, K, rope_base, rope_mode, scale, topk_idx, gates,
-                             seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st, packed);
+                             seg_offsets, perm_token, dout, dq, dk, dv, dgates, ws, st, packed,
+                             saved);
   }
+  if (saved) return hipErrorInvalidValue;   // (the host checks: matrix-core path only)
   if (dtype == 1) NAMOH_BWD(32, true);
   if (d == 32) NAMOH_BWD(32, false);
   if (d == 64) NAMOH_BWD(64, false);
   NAMOH_BWD(128, false);
 #undef NAMOH_BWD
+}
+
+bool attn_train_supported(int dtype, int d) { return bwd_uses_mfma(dtype, d); }
+
+// Training forward: the forward with the row statistics into the backward's
+// workspace (what launch_attn_bwd with saved = true reads back), and the
+// layer output combined from its f32 head outputs.
+hipError_t launch_train_fwd(const void* q, const void* k, const void* v, int dtype, int B,
+                            int T, int H, int K, int d, float rope_base, int rope_mode,
+                            float scale, const float* gates, const int32_t* seg_offsets,
+                            const int32_t* perm_token, const int32_t* slot_pos, void* out,
+                            int out_dtype, void* ws, hipStream_t st) {
+  if (!bwd_uses_mfma(dtype, d)) return hipErrorInvalidValue;
+  const BwdMfmaWs w = carve_bwd_mfma(ws, B, T, H, K, d);
+  AttnTiles tl;
+  hipError_t e = launch_attn_stats(q, k, v, B, T, H, K, d, rope_base, rope_mode, scale,
+                                   seg_offsets, perm_token, w.lse, w.attn, tl, st);
+  if (e != hipSuccess) return e;
+  return launch_combine_f32(tl.h, gates, slot_pos, static_cast<long>(B) * T, K, d, B * T * K,
+                            out, out_dtype, st);
 }
 
 // ---------------------------------------------------------------------------

@@ -68,6 +68,13 @@ hipError_t launch_attn_stats(const void* q, const void* k, const void* v, int B,
                              int K, int d, float rope_base, int rope_mode, float scale,
                              const int32_t* seg_offsets, const int32_t* perm_token, float* lse,
                              void* ws, AttnTiles& tiles, hipStream_t st);
+// The tiles a launch_attn_stats on the same workspace and sizes left there
+// (nothing is launched).
+void attn_stats_tiles(void* ws, int B, int T, int H, int K, int d, AttnTiles& tiles);
+// out[t] = sum over k of gates[t, k] * rows[slot_pos[t, k]] with f32 rows.
+hipError_t launch_combine_f32(const float* rows, const float* gates, const int32_t* slot_pos,
+                              long BT, int K, int D, int Nr, void* out, int out_dtype,
+                              hipStream_t st);
 
 // Always-active shared heads (attn.hip): Hs heads over all T tokens, causal
 // (window 0) or inside a window of `window` tokens; out (+)= sum of the heads.
@@ -129,7 +136,15 @@ hipError_t launch_attn_bwd(const void* q, const void* k, const void* v, int dtyp
                            const int32_t* topk_idx, const float* gates,
                            const int32_t* seg_offsets, const int32_t* perm_token,
                            const float* dout, float* dq, float* dk, float* dv, float* dgates,
-                           void* ws, hipStream_t st, bool packed = false);
+                           void* ws, hipStream_t st, bool packed = false, bool saved = false);
+// The training forward (matrix-core path: bf16, d = 64 or 128): output plus
+// the state launch_attn_bwd(saved = true) reuses from the same workspace.
+bool attn_train_supported(int dtype, int d);
+hipError_t launch_train_fwd(const void* q, const void* k, const void* v, int dtype, int B,
+                            int T, int H, int K, int d, float rope_base, int rope_mode,
+                            float scale, const float* gates, const int32_t* seg_offsets,
+                            const int32_t* perm_token, const int32_t* slot_pos, void* out,
+                            int out_dtype, void* ws, hipStream_t st);
 hipError_t launch_route_bwd(const float* logits, const int32_t* topk_idx, const float* gates,
                             const float* dgates, int B, int T, int H, int K, int gate_mode,
                             float* dlogits, hipStream_t st);

@@ -220,6 +220,47 @@ def test_attn_bwd_rejects(lib, kw, code):
     assert _bwd(lib, **kw) == code
 
 
+def _bwd_saved(lib, dtype=1, B=2, T=64, H=8, K=2, d=64, base=1e4, rope=0, scale=0.0,
+               q=fake(0), dout=fake(5), dq=fake(6), dg=fake(9), packed=0, wsb=1 << 30,
+               ws=fake(10)):
+    return lib.namoh_attn_bwd_saved(q, fake(1), fake(2), dtype, B, T, H, K, d, base, rope, scale,
+                                    fake(3), fake(4), fake(11), fake(12), dout, dq, fake(7),
+                                    fake(8), dg, packed, ws, wsb, None)
+
+
+def _fwd_train(lib, dtype=1, B=2, T=64, H=8, K=2, d=64, base=1e4, rope=0, scale=0.0,
+               q=fake(0), slot=fake(6), out=fake(7), odt=1, wsb=1 << 30, ws=fake(10)):
+    return lib.namoh_attn_fwd_train(q, fake(1), fake(2), dtype, B, T, H, K, d, base, rope,
+                                    scale, fake(3), fake(4), fake(5), slot, out, odt, ws, wsb,
+                                    None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=0), 2), (dict(d=32), 2), (dict(d=48), 2), (dict(dtype=4), 1), (dict(packed=2), 1),
+    (dict(rope=3), 1), (dict(q=None), 1), (dict(dout=P(A + 4)), 1), (dict(dg=None), 1),
+    (dict(wsb=64), 3), (dict(K=9), 1),
+])
+def test_attn_bwd_saved_rejects(lib, kw, code):
+    assert _bwd_saved(lib, **kw) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=0), 2), (dict(d=32), 2), (dict(odt=3), 1), (dict(base=-1.0), 1),
+    (dict(q=None), 1), (dict(slot=None), 1), (dict(out=None), 1), (dict(out=P(A + 8)), 1),
+    (dict(wsb=64), 3), (dict(ws=None), 3), (dict(T=1 << 25, B=1, H=2, K=1, d=128), 2),
+])
+def test_attn_fwd_train_rejects(lib, kw, code):
+    assert _fwd_train(lib, **kw) == code
+
+
+def test_train_calls_without_device(lib):
+    if _has_gpu():
+        pytest.skip("a GPU is present")
+    need = lib.namoh_attn_bwd_workspace_size(2, 64, 8, 2, 64)
+    assert _fwd_train(lib, wsb=need) == L.NAMOH_ERR_HIP
+    assert _bwd_saved(lib, wsb=need) == L.NAMOH_ERR_HIP
+
+
 @pytest.mark.parametrize("kw,code", [
     (dict(gate=2), 1), (dict(logits=None), 1), (dict(dl=P(A + 2)), 1), (dict(K=0), 1),
 ])

@@ -275,6 +275,40 @@ def test_attn_bwd_packed(name):
     _check_grad(gp["dgates"].cpu().numpy(), dg, "dgates", **tol)
 
 
+@pytest.mark.parametrize("name", ["bf16_d64_rel", "bf16_d128_global", "bf16_d128_rel",
+                                  "bf16_d64_none", "balanced_b2", "long_d128"])
+def test_attn_train_saved(name):
+    # namoh_attn_fwd_train: the layer output against the oracle; then
+    # namoh_attn_bwd_saved on its workspace: bit for bit the gradients of the
+    # stateless calls (dense and packed), which rerun the forward themselves
+    w, rope_mode = BWD[name]
+    say(f"training forward + saved backward {name}: {w}")
+    inp = W.prefill_inputs(w)
+    lg = torch.from_numpy(inp["logits"]).to(DEV)
+    q, k, v = (to_dev(inp[x], w.dtype) for x in ("q", "k", "v"))
+    r = L.route(lg, w.K)
+    dout = np.random.default_rng(77).standard_normal((w.B, w.T, w.d)).astype(np.float32)
+    dd = torch.from_numpy(dout).to(DEV)
+    ws = L.workspace(int(L.lib().namoh_attn_bwd_workspace_size(w.B, w.T, w.H, w.K, w.d)), DEV)
+    o = L.attn_fwd_train(q, k, v, r, w.K, w.rope_base, ws, rope_mode, out_dtype=torch.float32)
+    gs = L.attn_bwd(q, k, v, r, w.K, w.rope_base, dd, rope_mode, ws=ws, saved=True)
+    gsp = L.attn_bwd(q, k, v, r, w.K, w.rope_base, dd, rope_mode, ws=ws, saved=True, packed=True)
+    gd = L.attn_bwd(q, k, v, r, w.K, w.rope_base, dd, rope_mode)
+    gp = L.attn_bwd(q, k, v, r, w.K, w.rope_base, dd, rope_mode, packed=True)
+    torch.cuda.synchronize()
+    for key in ("dq", "dk", "dv", "dgates"):
+        np.testing.assert_array_equal(gs[key].cpu().numpy(), gd[key].cpu().numpy(), err_msg=key)
+        np.testing.assert_array_equal(gsp[key].cpu().numpy(), gp[key].cpu().numpy(),
+                                      err_msg=key)
+    ref = _oracle_routing(inp, w)
+    f = _f64(inp, w)
+    hp = O.attention_gathered(f["q"], f["k"], f["v"], ref["head_len"], ref["seg_offsets"],
+                              ref["perm_token"], w.H, w.rope_base, rope_mode)
+    want = O.combine_packed(hp, ref["slot_pos"], ref["gates"])
+    e = check_out(o.cpu().numpy().astype(np.float64), want, w.dtype)
+    say(f"  output max err {e:.2e}")
+
+
 @pytest.mark.parametrize("gate_mode", [O.GATE_SOFTMAX_SELECTED, O.GATE_SOFTMAX_ALL])
 def test_route_bwd_parity(gate_mode):
     # router gradient fed by the GPU's own gate gradients (the training chain)
