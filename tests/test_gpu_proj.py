@@ -42,6 +42,8 @@ CASES = {
     # more than 1024 (b, h) segments: segment offsets read from global memory
     "many_segments_dense": dict(B=17, T=40, H=64, K=11, d=64, d_model=128),
     "many_segments_pairs": dict(B=20, T=70, H=64, K=4, d=64, d_model=128),
+    # K > 32, d = 128
+    "k40_d128": dict(B=2, T=150, H=64, K=40, d=128, d_model=256),
 }
 
 
@@ -96,9 +98,7 @@ def _packed_to_dense(hp, topk, H, T, d):
     return h
 
 
-@pytest.mark.parametrize("name", ["d64_dm256", "d128_dm384_ragged", "all_heads", "one_head",
-                                  "pairs_d64_h16_k2", "pairs_d128_h8_k2_ragged",
-                                  "many_segments_dense", "many_segments_pairs"])
+@pytest.mark.parametrize("name", list(CASES))
 @pytest.mark.parametrize("hdt,odt", [("f32", torch.float32), ("bf16", torch.bfloat16)])
 def test_out_proj_parity(name, hdt, odt):
     w = _case(name)
@@ -124,6 +124,27 @@ def test_out_proj_parity(name, hdt, odt):
     ref = O.output_projection(_packed_to_dense(hp64, topk, w.H, w.T, w.d), topk, gates,
                               _f64(inp["w_o"]))
     check_out(from_dev(o), ref, "bf16", what=f"{name} out_proj")
+
+
+@pytest.mark.parametrize("K", [2, 3])   # per-pair form, dense form
+def test_out_proj_skewed_routing(K):
+    # a few heads take most tokens: segments of very different lengths
+    w = _case("pairs_d64_h16_k2").with_(T=700, K=K)
+    say(f"output projection, skewed routing ({'dense' if _dense_form(w) else 'per-pair'}): {w}")
+    inp = W.projection_inputs(w)
+    inp["logits"][..., :2] += 2.5
+    r, topk = _route(inp, w)
+    n = np.bincount(topk.reshape(-1), minlength=w.H)
+    assert n.max() > 4 * max(1, n.min())
+    Nr = w.B * w.T * w.K
+    hp_bits = W.f32_to_bf16_bits(np.random.default_rng(18).standard_normal((Nr, w.d)).astype(np.float32))
+    wo = to_dev(inp["w_o"], "bf16")
+    o = L.out_proj(to_dev(hp_bits, "bf16"), wo, r, w.B, w.T, w.H, w.K)
+    torch.cuda.synchronize()
+    gates = r["gates"].cpu().numpy().astype(np.float64)
+    ref = O.output_projection(_packed_to_dense(_f64(hp_bits), topk, w.H, w.T, w.d), topk, gates,
+                              _f64(inp["w_o"]))
+    check_out(from_dev(o), ref, "bf16", what="skewed out_proj")
 
 
 def test_projected_layer():
