@@ -165,7 +165,7 @@ def bench_prefill(w, args, torch, L, DI):
         step()
     torch.cuda.synchronize()
     kern = {}
-    for sec in ("attn", "pack", "combine"):
+    for sec in ("route_count", "route_scan", "route_scatter", "pack", "attn", "merge", "combine"):
         r = L.profile_read(sec)
         if r is not None and r[1] > 0:
             kern[sec] = r[0] / r[1]
@@ -191,10 +191,41 @@ def bench_prefill(w, args, torch, L, DI):
                       "gates": "softmax over selected"},
            "roofline": roof,
            "kernels_ms": {k2: round(v2, 4) for k2, v2 in kern.items()},
+           "kernels_hbm": hbm_kernels(kern, w),
            "warmup_steps_run": warm, "settle_ms": args.settle_ms}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline_prefill(w, inp, n, args.cpu_budget)
     return res
+
+
+def hbm_kernels(kern, w):
+    """Algorithmic HBM bytes and GB/s of the routing, packing and combine
+    kernels (reported, not the graded roofline).  Nr = B T K routed pairs:
+      route_count   logits [B,T,H] f32 in; top-K index, gate, in-chunk rank
+                    [B,T,K] i32/f32 and the chunk counts out;
+      route_scatter top-K index and rank in; token of each packed row and
+                    packed row of each (t, k) out;
+      pack          the routed key and value rows in, packed key tiles and
+                    transposed value tiles out (all of the inputs' dtype);
+      combine       the packed head rows (bf16) and gates / slots in, the
+                    layer output out."""
+    B, T, H, K, d = w.B, w.T, w.H, w.K, w.d
+    Nr = B * T * K
+    esz = 2 if w.dtype == "bf16" else 4
+    nchunk = (T + 63) // 64
+    counts = B * H * nchunk * 4
+    nbytes = {
+        "route_count": B * T * H * 4 + 3 * Nr * 4 + counts,
+        "route_scatter": 2 * Nr * 4 + 2 * Nr * 4 + counts,
+        "pack": 4 * Nr * d * esz,
+        "combine": Nr * d * (2 if esz == 2 else 4) + 2 * Nr * 4 + B * T * d * esz,
+    }
+    out = {}
+    for k, b in nbytes.items():
+        if k in kern and kern[k] > 0:
+            out[k] = {"bytes": b, "GB/s": round(b / (kern[k] * 1e-3) / 1e9, 1),
+                      "frac_of_8TB/s": round(b / (kern[k] * 1e-3) / 1e9 / PEAK_HBM_GBS, 3)}
+    return out
 
 
 def cpu_baseline_prefill(w, inp, head_len, budget_s):
@@ -708,8 +739,8 @@ def bench_suite(args, torch, L, DI):
         r = (bench_decode if w.decode else bench_prefill)(w, sub, torch, L, DI)
         torch.cuda.empty_cache()
         keep = ("value", "unit", "ms_per_step", "steps", "warmup", "warmup_steps_run",
-                "settle_ms", "dtype", "config", "roofline", "kernels_ms", "tokens_per_s",
-                "cpu_baseline")
+                "settle_ms", "dtype", "config", "roofline", "kernels_ms", "kernels_hbm",
+                "tokens_per_s", "cpu_baseline")
         others[w.name] = {k: r[k] for k in keep if k in r}
     res["workloads"] = others
     return res

@@ -27,6 +27,7 @@
 
 #include "common.h"
 #include "internal.h"
+#include "launch.h"
 
 namespace namoh {
 
@@ -415,11 +416,13 @@ hipError_t launch_route(const float* logits, const float* bias, int B, int T, in
 #define NAMOH_RC(HM, KM)                                                                   \
   do {                                                                                     \
     if (bias)                                                                              \
-      k_route_count<HM, KM, true><<<grid, kCountThreads, 0, st>>>(                         \
-          logits, bias, T, H, K, gate_mode, nchunk, topk_idx, gates, slot_pos, counts);    \
+      launch_k("route_count", k_route_count<HM, KM, true>, grid, dim3(kCountThreads), st,  \
+               logits, bias, T, H, K, gate_mode, nchunk, topk_idx, gates, slot_pos,        \
+               counts);                                                                    \
     else                                                                                   \
-      k_route_count<HM, KM, false><<<grid, kCountThreads, 0, st>>>(                        \
-          logits, nullptr, T, H, K, gate_mode, nchunk, topk_idx, gates, slot_pos, counts); \
+      launch_k("route_count", k_route_count<HM, KM, false>, grid, dim3(kCountThreads), st, \
+               logits, nullptr, T, H, K, gate_mode, nchunk, topk_idx, gates, slot_pos,     \
+               counts);                                                                    \
   } while (0)
   const bool small_k = K <= 8;
   if (H <= 8) NAMOH_RC(8, 8);
@@ -430,15 +433,14 @@ hipError_t launch_route(const float* logits, const float* bias, int B, int T, in
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (static_cast<long>(nchunk) * H <= kFusedScan) {
-    k_route_scatter<true><<<grid, kScatterThreads, 0, st>>>(
-        topk_idx, B, T, H, K, nchunk, counts, within, head_len, seg_offsets, perm_token,
-        slot_pos);
+    launch_k("route_scatter", k_route_scatter<true>, grid, dim3(kScatterThreads), st, topk_idx,
+             B, T, H, K, nchunk, counts, within, head_len, seg_offsets, perm_token, slot_pos);
   } else {
-    k_route_scan<<<B * H, kWave, 0, st>>>(counts, nchunk, within, head_len);
+    launch_k("route_scan", k_route_scan, dim3(B * H), dim3(kWave), st, counts, nchunk, within,
+             head_len);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    k_route_scatter<false><<<grid, kScatterThreads, 0, st>>>(
-        topk_idx, B, T, H, K, nchunk, counts, within, head_len, seg_offsets, perm_token,
-        slot_pos);
+    launch_k("route_scatter", k_route_scatter<false>, grid, dim3(kScatterThreads), st, topk_idx,
+             B, T, H, K, nchunk, counts, within, head_len, seg_offsets, perm_token, slot_pos);
   }
   return hipGetLastError();
 }
