@@ -236,7 +236,11 @@ namoh_status namoh_attn_fwd_train(const void* q, const void* k, const void* v, i
  * in `workspace`: the gradients are those of the stateless calls, bit for
  * bit.  dtype NAMOH_BF16, d_head 64 or 128 (otherwise
  * NAMOH_ERR_UNSUPPORTED); other arguments, outputs and limits as there.
- * The workspace may not have been used by another call in between. */
+ * The workspace may not have been used by another call in between.  The
+ * work records read from it are range-checked on the device before they
+ * address anything (a record outside the packed arrays is skipped), so a
+ * workspace that did not come from namoh_attn_fwd_train gives undefined
+ * gradients but no out-of-range access. */
 namoh_status namoh_attn_bwd_saved(const void* q, const void* k, const void* v, int dtype, int B,
                                   int T, int H, int K, int d_head, float rope_base,
                                   int rope_mode, float softmax_scale, const int32_t* topk_idx,

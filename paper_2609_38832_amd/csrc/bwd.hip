@@ -809,6 +809,20 @@ template <int D> struct BwdMfmaShape {
   static constexpr int MINB_Q = 2;               // (query side; 3 at d = 64 spills)
 };
 
+// A work record checked before it addresses anything (the saved backward
+// takes the list from the caller's workspace): its segment, rows and tiles
+// inside the packed arrays, a whole item (the backward's list holds no
+// key-range parts) and a block inside its segment.  A record that fails is
+// skipped.
+NAMOH_DEV bool bwd_item_ok(const WorkItem& it, int BH, int T, int Nr, int max_tiles) {
+  if (it.s < 0 || it.s >= BH || it.n <= 0 || it.n > T || it.seg0 < 0 || it.seg0 > Nr - it.n)
+    return false;
+  if ((it.qh >> kQhBits) != 0) return false;
+  const int nt = (it.n + kBN - 1) / kBN;
+  return it.qb >= 0 && it.qb < (it.n + kBwdMfmaBlock - 1) / kBwdMfmaBlock && it.tile0 >= 0 &&
+         it.tile0 <= max_tiles - nt;
+}
+
 // Query side: dQ~ of one (segment, 128-query block) item.
 template <int D>
 __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bwd_dq(
@@ -817,7 +831,8 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
     const uint16_t* __restrict__ Vp, const uint16_t* __restrict__ Kt,
     const WorkItem* __restrict__ items, const int32_t* __restrict__ meta,
     const int32_t* __restrict__ perm_token, const double* __restrict__ freq, int T,
-    int rope_mode, float scale, float* __restrict__ dq, int packed) {
+    int rope_mode, float scale, float* __restrict__ dq, int packed, int BH, int Nr,
+    int max_tiles) {
   constexpr int NT = kBwdMfmaThreads, BM = kBwdMfmaBlock;
   constexpr int KS = D / 16, MT = D / 32;
   constexpr int KPT = kBN * D / 8 / NT;
@@ -830,7 +845,7 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
   __shared__ __attribute__((aligned(16))) uint16_t sV[2][kBN * D];
   __shared__ __attribute__((aligned(16))) uint16_t sKt[kBN * D];
   WorkItem it;
-  if (!my_item(items, meta, it)) return;
+  if (!my_item(items, meta, it) || !bwd_item_ok(it, BH, T, Nr, max_tiles)) return;
   const int q0 = it.qb * BM;
   const int seg0 = it.seg0, n = it.n, tile0 = it.tile0;
   const int ntiles = (n + kBN - 1) / kBN;
@@ -951,7 +966,7 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
     const uint16_t* __restrict__ Vp, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ meta, const int32_t* __restrict__ perm_token,
     const double* __restrict__ freq, int T, int rope_mode, float* __restrict__ dk,
-    float* __restrict__ dv, int packed) {
+    float* __restrict__ dv, int packed, int BH, int Nr, int max_tiles) {
   constexpr int NT = kBwdMfmaThreads, BM = kBwdMfmaBlock;
   constexpr int KS = D / 16, MT = D / 32;
   constexpr int KPT = kBN * D / 8 / NT;
@@ -964,7 +979,7 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
   __shared__ __attribute__((aligned(16))) uint16_t sdOt[2][D * kBN];
   __shared__ __attribute__((aligned(16))) float2 sLD[2][kBN];
   WorkItem it;
-  if (!my_item(items, meta, it)) return;
+  if (!my_item(items, meta, it) || !bwd_item_ok(it, BH, T, Nr, max_tiles)) return;
   const int seg0 = it.seg0, n = it.n, tile0 = it.tile0;
   const int nkb = (n + BM - 1) / BM;
   const int j0 = (nkb - 1 - it.qb) * BM;
@@ -1103,7 +1118,7 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
     const uint16_t* __restrict__ Vp, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ meta, const int32_t* __restrict__ perm_token,
     const double* __restrict__ freq, int T, int rope_mode, float* __restrict__ dk,
-    float* __restrict__ dv, int packed) {
+    float* __restrict__ dv, int packed, int BH, int Nr, int max_tiles) {
   constexpr int NT = 2 * kBwdMfmaThreads, BM = kBwdMfmaBlock;
   constexpr int KS = D / 16, MT = D / 32;
   constexpr int KPT = kBN * D / 8 / NT;
@@ -1120,7 +1135,7 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
   // group, in the tile stages once the loop is done
   static_assert(sizeof(sQ) >= 2 * MT * 16 * 64 * sizeof(float), "partial staging");
   WorkItem it;
-  if (!my_item(items, meta, it)) return;
+  if (!my_item(items, meta, it) || !bwd_item_ok(it, BH, T, Nr, max_tiles)) return;
   const int seg0 = it.seg0, n = it.n, tile0 = it.tile0;
   const int nkb = (n + BM - 1) / BM;
   const int j0 = (nkb - 1 - it.qb) * BM;
@@ -1370,18 +1385,18 @@ static hipError_t run_bwd_mfma(const void* q, const void* k, const void* v, int 
   prof_mark("bwd_dq", true, st);
   k_bwd_dq<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
       w.Qs, w.dO, w.LD, tl.Kp, w.Vp, w.Kt, tl.items, tl.meta, perm_token, freq, T, rope_mode,
-      scale, dq, packed ? 1 : 0);
+      scale, dq, packed ? 1 : 0, BH, Nr, tl.max_tiles);
   prof_mark("bwd_dq", false, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_mark("bwd_dkdv", true, st);
   if constexpr (D == 128)
     k_bwd_dkdv8<D><<<static_cast<unsigned>(tl.max_items), 2 * kBwdMfmaThreads, 0, st>>>(
         w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, freq, T,
-        rope_mode, dk, dv, packed ? 1 : 0);
+        rope_mode, dk, dv, packed ? 1 : 0, BH, Nr, tl.max_tiles);
   else
     k_bwd_dkdv<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
         w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, freq, T,
-        rope_mode, dk, dv, packed ? 1 : 0);
+        rope_mode, dk, dv, packed ? 1 : 0, BH, Nr, tl.max_tiles);
   prof_mark("bwd_dkdv", false, st);
   return hipGetLastError();
 }
