@@ -350,6 +350,53 @@ namoh_status namoh_shared_attn(const void* q, const void* k, const void* v, int 
                                size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Shared heads in the decode step (Sec. 4.4 "Shared heads for local
+ * context"; Sec. 3.2: decoding extends the caches one token at a time).
+ * The new token of sequence b, at global position p = cache_len[b] (the
+ * number of tokens before it), enters every one of the Hs always-active
+ * heads: its key, rotated at p (HEAD_RELATIVE and GLOBAL both mean the
+ * position p here, every token being in every shared head; NONE: no
+ * rotation), and its value are written to row p mod cap of the head's
+ * caches, and its query (rotated at p) attends over the keys at positions
+ * max(0, p + 1 - window) .. p (window 0: 0 .. p), itself included.  The head
+ * outputs are added without a gate:
+ *   out[b] = (accumulate ? out[b] : 0) + sum_{s < Hs} h_s(b),
+ * so after namoh_decode_step (accumulate = 1) out holds the routed heads
+ * plus the shared ones; cache_len[b] = p + 1.
+ * In:  q, k, v [B, Hs, d] of `dtype` (f32 or bf16; d 32, 64 or 128).
+ * In/out: k_cache, v_cache [B, Hs, cap, d] `dtype` (keys stored rotated);
+ *      with window > 0 they are rings that keep the most recent cap tokens
+ *      (cap >= window, else NAMOH_ERR_INVALID_ARG), row t mod cap holding
+ *      token t; with window = 0 row t holds token t and a step with p >= cap
+ *      skips the sequence: nothing is written, cache_len[b] stays, out[b]
+ *      gets no shared-head term and *dev_status (if non-NULL) is set to 1.
+ *      cache_len int32 [B].
+ * Out: out [B, d] of out_dtype.  Workspace: namoh_shared_decode_workspace_size
+ *      bytes (rotated queries, history extents, per-512-row partials).
+ * Limits: Hs <= 1024, B*Hs*ceil(cap/512) < 2^31.
+ * ---------------------------------------------------------------------- */
+size_t namoh_shared_decode_workspace_size(int B, int Hs, int d_head, int cap);
+
+namoh_status namoh_shared_decode_step(const void* q, const void* k, const void* v, int dtype,
+                                      int B, int Hs, int d_head, int cap, int window,
+                                      float rope_base, int rope_mode, float softmax_scale,
+                                      void* k_cache, void* v_cache, int32_t* cache_len, void* out,
+                                      int out_dtype, int accumulate, int32_t* dev_status,
+                                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Prefill -> decode hand-off of the shared heads (the counterpart of
+ * namoh_prefill_cache): for every sequence b and shared head s, the prompt's
+ * tokens t (keys rotated at t as above, values as given) go to row t mod cap
+ * of the head's caches, for the last min(T, cap) tokens; cache_len[b] = T.
+ * window as in namoh_shared_decode_step (0: cap >= T required, else
+ * NAMOH_ERR_INVALID_ARG).  In: k, v [B, Hs, T, d] of `dtype`.  No workspace;
+ * allocates nothing. */
+namoh_status namoh_shared_prefill_cache(const void* k, const void* v, int dtype, int B, int T,
+                                        int Hs, int d_head, int cap, int window, float rope_base,
+                                        int rope_mode, void* k_cache, void* v_cache,
+                                        int32_t* cache_len, void* stream);
+
+/* ------------------------------------------------------------------------
  * Routed per-head projections (Sec. 3.1, Eq. namoh-qkv: tokens are
  * dispatched to their heads before projection, and only active (token, head)
  * pairs compute q, k, v; Eq. namoh-attention: o_t = sum over the selected

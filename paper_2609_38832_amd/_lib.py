@@ -39,6 +39,7 @@ EXPORTED = (
     "namoh_qkv_proj", "namoh_out_proj_workspace_size", "namoh_out_proj",
     "namoh_attn_fwd_grouped_workspace_size", "namoh_attn_fwd_grouped",
     "namoh_shared_attn_workspace_size", "namoh_shared_attn",
+    "namoh_shared_decode_workspace_size", "namoh_shared_decode_step", "namoh_shared_prefill_cache",
     "namoh_decode_grouped_workspace_size", "namoh_decode_step_grouped",
     "namoh_status_string", "namoh_last_error", "namoh_version",
     "namoh_profile_enable", "namoh_profile_read",
@@ -82,6 +83,11 @@ _SIGS = {
     "namoh_shared_attn_workspace_size": (_S, [_I, _I, _I, _I]),
     "namoh_shared_attn": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F, _P, _I, _I, _P,
                                _P, _S, _P]),
+    "namoh_shared_decode_workspace_size": (_S, [_I, _I, _I, _I]),
+    "namoh_shared_decode_step": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _F, _P, _P, _P,
+                                      _P, _I, _I, _P, _P, _S, _P]),
+    "namoh_shared_prefill_cache": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _I, _P, _P, _P,
+                                        _P]),
     "namoh_decode_grouped_workspace_size": (_S, [_I, _I, _I, _I, _I, _I]),
     "namoh_decode_step_grouped": (_I, [_P, _P, _P, _P, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I,
                                        _I, _F, _I, _I, _F, _P, _P, _P, _I, _P, _P, _S, _P]),
@@ -317,6 +323,61 @@ def shared_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, window: int,
                                   F32 if skip else dtype_code(out.dtype), int(bool(accumulate)),
                                   _ptr(head_out), _ptr(ws), ws.numel(), _stream(q.device)))
     return head_out if skip else out
+
+
+def _shared_caches(k_cache, v_cache, cache_len, B, Hs, d, dtype):
+    cap = k_cache.shape[2]
+    if tuple(k_cache.shape) != (B, Hs, cap, d) or tuple(v_cache.shape) != (B, Hs, cap, d):
+        raise ValueError("caches must be [B, Hs, cap, d]")
+    if k_cache.dtype != dtype or v_cache.dtype != dtype:
+        raise ValueError("the caches must have the inputs' dtype")
+    if tuple(cache_len.shape) != (B,) or cache_len.dtype != torch.int32:
+        raise ValueError("cache_len must be int32 [B]")
+    return cap
+
+
+def shared_decode_step(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                       k_cache: torch.Tensor, v_cache: torch.Tensor, cache_len: torch.Tensor,
+                       window: int, rope_base: float, rope_mode: int = ROPE_GLOBAL,
+                       softmax_scale: float = 0.0, out: Optional[torch.Tensor] = None,
+                       accumulate: bool = False, out_dtype: Optional[torch.dtype] = None,
+                       dev_status: Optional[torch.Tensor] = None,
+                       ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """namoh_shared_decode_step: the new token's q, k, v [B, Hs, d] for the Hs
+    shared heads; caches [B, Hs, cap, d] (rings of the last cap tokens when
+    window > 0), cache_len int32 [B]; out [B, d] (+)= the heads' sum."""
+    _need_cuda(q, k, v, k_cache, v_cache, cache_len, out, dev_status, ws)
+    B, Hs, d = q.shape
+    if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
+        raise ValueError("q, k, v must share [B, Hs, d] and dtype")
+    cap = _shared_caches(k_cache, v_cache, cache_len, B, Hs, d, q.dtype)
+    if out is None:
+        out = torch.zeros(B, d, dtype=q.dtype if out_dtype is None else out_dtype, device=q.device)
+    if ws is None:
+        ws = workspace(int(lib().namoh_shared_decode_workspace_size(B, Hs, d, cap)), q.device)
+    check(lib().namoh_shared_decode_step(_ptr(q), _ptr(k), _ptr(v), dtype_code(q.dtype), B, Hs, d,
+                                         cap, int(window), float(rope_base), rope_mode,
+                                         float(softmax_scale), _ptr(k_cache), _ptr(v_cache),
+                                         _ptr(cache_len), _ptr(out), dtype_code(out.dtype),
+                                         int(bool(accumulate)), _ptr(dev_status), _ptr(ws),
+                                         ws.numel(), _stream(q.device)))
+    return out
+
+
+def shared_prefill_cache(k: torch.Tensor, v: torch.Tensor, k_cache: torch.Tensor,
+                         v_cache: torch.Tensor, cache_len: torch.Tensor, window: int,
+                         rope_base: float, rope_mode: int = ROPE_GLOBAL) -> None:
+    """namoh_shared_prefill_cache: the prompt's shared-head keys (rotated) and
+    values k, v [B, Hs, T, d] into the decode caches; cache_len [B] = T."""
+    _need_cuda(k, v, k_cache, v_cache, cache_len)
+    B, Hs, T, d = k.shape
+    if v.shape != k.shape or v.dtype != k.dtype:
+        raise ValueError("k and v must share [B, Hs, T, d] and dtype")
+    cap = _shared_caches(k_cache, v_cache, cache_len, B, Hs, d, k.dtype)
+    check(lib().namoh_shared_prefill_cache(_ptr(k), _ptr(v), dtype_code(k.dtype), B, T, Hs, d,
+                                           cap, int(window), float(rope_base), rope_mode,
+                                           _ptr(k_cache), _ptr(v_cache), _ptr(cache_len),
+                                           _stream(k.device)))
 
 
 def prefill_cache(k: torch.Tensor, v: torch.Tensor, r: dict, K: int, rope_base: float,

@@ -334,6 +334,92 @@ namoh_status namoh_shared_attn(const void* q, const void* k, const void* v, int 
                                          static_cast<hipStream_t>(stream)));
 }
 
+namespace {
+namoh_status check_shared_decode(int B, int Hs, int d_head, int cap, int window, int dtype,
+                                 int rope_mode, float rope_base) {
+  namoh_status s;
+  REQUIRE(B >= 1, "B must be >= 1 (got %d)", B);
+  REQUIRE(Hs >= 1 && Hs <= 1024, "Hs must be in [1, 1024] (got %d)", Hs);
+  if ((s = check_head_width(d_head)) != NAMOH_OK) return s;
+  REQUIRE(dtype == NAMOH_F32 || dtype == NAMOH_BF16, "unknown dtype %d", dtype);
+  REQUIRE(cap >= 1, "cap must be >= 1 (got %d)", cap);
+  REQUIRE(window >= 0, "window must be >= 0 (got %d)", window);
+  REQUIRE(window == 0 || cap >= window, "cap (%d) must hold the window (%d)", cap, window);
+  REQUIRE(static_cast<long long>(B) * Hs * ((cap + 511) / 512) < (1ll << 31),
+          "B*Hs*ceil(cap/512) must be < 2^31");
+  REQUIRE(static_cast<long long>(B) * Hs * cap * d_head < (1ll << 40), "caches too large");
+  REQUIRE(rope_mode == NAMOH_ROPE_HEAD_RELATIVE || rope_mode == NAMOH_ROPE_GLOBAL ||
+              rope_mode == NAMOH_ROPE_NONE,
+          "unknown rope_mode %d", rope_mode);
+  REQUIRE(rope_mode == NAMOH_ROPE_NONE || (std::isfinite(rope_base) && rope_base > 0.f),
+          "rope_base must be finite and > 0 (got %g)", static_cast<double>(rope_base));
+  return NAMOH_OK;
+}
+}  // namespace
+
+size_t namoh_shared_decode_workspace_size(int B, int Hs, int d_head, int cap) {
+  if (check_shared_decode(B, Hs, d_head, cap, 0, NAMOH_BF16, NAMOH_ROPE_NONE, 1.f) != NAMOH_OK)
+    return 0;
+  return namoh::shared_decode_workspace_bytes(B, Hs, d_head, cap);
+}
+
+namoh_status namoh_shared_decode_step(const void* q, const void* k, const void* v, int dtype,
+                                      int B, int Hs, int d_head, int cap, int window,
+                                      float rope_base, int rope_mode, float softmax_scale,
+                                      void* k_cache, void* v_cache, int32_t* cache_len, void* out,
+                                      int out_dtype, int accumulate, int32_t* dev_status,
+                                      void* workspace, size_t workspace_bytes, void* stream) {
+  namoh_status s;
+  if ((s = check_shared_decode(B, Hs, d_head, cap, window, dtype, rope_mode, rope_base)) !=
+      NAMOH_OK)
+    return s;
+  REQUIRE(!std::isnan(softmax_scale) && !std::isinf(softmax_scale), "softmax_scale must be finite");
+  REQUIRE(out_dtype == NAMOH_F32 || out_dtype == NAMOH_BF16, "unknown out_dtype %d", out_dtype);
+  REQUIRE(accumulate == 0 || accumulate == 1, "accumulate must be 0 or 1 (got %d)", accumulate);
+  REQUIRE_PTR(q, 16);
+  REQUIRE_PTR(k, 16);
+  REQUIRE_PTR(v, 16);
+  REQUIRE_PTR(k_cache, 16);
+  REQUIRE_PTR(v_cache, 16);
+  REQUIRE_PTR(cache_len, 4);
+  REQUIRE_PTR(out, 16);
+  if (dev_status != nullptr) REQUIRE_PTR(dev_status, 4);
+  if ((s = check_workspace(workspace, workspace_bytes,
+                           namoh::shared_decode_workspace_bytes(B, Hs, d_head, cap))) != NAMOH_OK)
+    return s;
+  const float scale = softmax_scale > 0.f ? softmax_scale : 1.f / std::sqrt(static_cast<float>(d_head));
+  clear_hip_error();
+  return launched(stream, namoh::launch_shared_decode(
+                              q, k, v, dtype, k_cache, v_cache, cache_len, B, Hs, d_head, cap,
+                              window, rope_base, rope_mode == NAMOH_ROPE_NONE ? 2 : 1, scale, out,
+                              out_dtype, accumulate, dev_status, workspace,
+                              static_cast<hipStream_t>(stream)));
+}
+
+namoh_status namoh_shared_prefill_cache(const void* k, const void* v, int dtype, int B, int T,
+                                        int Hs, int d_head, int cap, int window, float rope_base,
+                                        int rope_mode, void* k_cache, void* v_cache,
+                                        int32_t* cache_len, void* stream) {
+  namoh_status s;
+  if ((s = check_shared_decode(B, Hs, d_head, cap, window, dtype, rope_mode, rope_base)) !=
+      NAMOH_OK)
+    return s;
+  REQUIRE(T >= 1, "T must be >= 1 (got %d)", T);
+  REQUIRE(static_cast<long long>(B) * Hs * T < (1ll << 31), "B*Hs*T must be < 2^31");
+  REQUIRE(window > 0 || cap >= T, "without a window cap (%d) must hold the prompt (T = %d)", cap,
+          T);
+  REQUIRE_PTR(k, 16);
+  REQUIRE_PTR(v, 16);
+  REQUIRE_PTR(k_cache, 16);
+  REQUIRE_PTR(v_cache, 16);
+  REQUIRE_PTR(cache_len, 4);
+  clear_hip_error();
+  return launched(stream, namoh::launch_shared_prefill_cache(
+                              k, v, dtype, B, T, Hs, d_head, cap, rope_base,
+                              rope_mode == NAMOH_ROPE_NONE ? 2 : 1, k_cache, v_cache, cache_len,
+                              static_cast<hipStream_t>(stream)));
+}
+
 size_t namoh_attn_fwd_grouped_workspace_size(int B, int T, int H_kv, int K_kv, int group_size,
                                              int d_head, int dtype) {
   if (check_sizes(B, T, H_kv, K_kv) != NAMOH_OK || group_size < 1 || group_size > 16 ||

@@ -157,12 +157,15 @@ __global__ __launch_bounds__(64 * kAppendWaves) void k_decode_route_append(
 // without groups): each row is read once and scored against all of them, with
 // one online softmax per query; the partial of query u of selected head bk is
 // (bk * GQ + u) * nchunk + chunk.
-template <int D, bool BF16, int GQ = 1>
+// RING (shared heads with a window): the caches are rings of cap rows and
+// history row r of bk is physical row (row0[bk] + r) mod cap.
+template <int D, bool BF16, int GQ = 1, bool RING = false>
 __global__ __launch_bounds__(256) void k_decode_attn(
     const void* __restrict__ k_cache, const void* __restrict__ v_cache,
     const int32_t* __restrict__ topk_idx, const int32_t* __restrict__ rows,
     const float* __restrict__ qrot, int H, int K, long cap, int nchunk,
-    float* __restrict__ part_acc, float* __restrict__ part_ml) {
+    float* __restrict__ part_acc, float* __restrict__ part_ml,
+    const int32_t* __restrict__ row0 = nullptr) {
   constexpr int EPG = BF16 ? 8 : 4;   // elements per 16-byte granule
   constexpr int G = D / EPG;          // lanes per row
   constexpr int RPW = 64 / G;         // rows per wave per step
@@ -181,6 +184,7 @@ __global__ __launch_bounds__(256) void k_decode_attn(
   const int b = bk / K;
   const int h = topk_idx[bk];
   const size_t rowbase = (static_cast<size_t>(b) * H + h) * cap;
+  const int ring0 = RING ? row0[bk] : 0;
   const int tid = thread_x();
   const int lane = tid % 64, wave = tid / 64;
   const int sub = lane % G;
@@ -209,7 +213,12 @@ __global__ __launch_bounds__(256) void k_decode_attn(
     for (int u = 0; u < U; ++u) {
       const int r = rb + u * RPB + grp;
       if (r < r1) {
-        const size_t gi = (rowbase + r) * G + sub;
+        long pr = r;
+        if constexpr (RING) {
+          pr += ring0;
+          if (pr >= cap) pr -= cap;
+        }
+        const size_t gi = (rowbase + pr) * G + sub;
         kx[u] = kc[gi];
         vx[u] = vc[gi];
       } else {
@@ -535,7 +544,7 @@ template <int D, bool OUT_BF16>
 __global__ __launch_bounds__(256) void k_decode_combine(
     const float* __restrict__ gates, const int32_t* __restrict__ rows,
     const float* __restrict__ part_acc, const float* __restrict__ part_ml,
-    int K, int nchunk, void* __restrict__ out, int G) {
+    int K, int nchunk, void* __restrict__ out, int G, int accumulate = 0) {
   constexpr int NWV = 4;
   constexpr int DPL = (D + 63) / 64;  // output columns per lane
   __shared__ float s_o[NWV][D];
@@ -582,11 +591,16 @@ __global__ __launch_bounds__(256) void k_decode_combine(
   }
   __syncthreads();
   if (thread_x() < D) {
+    const size_t oi = static_cast<size_t>(b) * D + thread_x();
     float r = 0.f;
+    if (accumulate) {   // added to what out holds (shared heads after the routed step)
+      if constexpr (OUT_BF16) r = bf16_to_f32(static_cast<const uint16_t*>(out)[oi]);
+      else r = static_cast<const float*>(out)[oi];
+    }
 #pragma unroll
     for (int w = 0; w < NWV; ++w) r += s_o[w][thread_x()];
-    if constexpr (OUT_BF16) static_cast<uint16_t*>(out)[static_cast<size_t>(b) * D + thread_x()] = f32_to_bf16(r);
-    else static_cast<float*>(out)[static_cast<size_t>(b) * D + thread_x()] = r;
+    if constexpr (OUT_BF16) static_cast<uint16_t*>(out)[oi] = f32_to_bf16(r);
+    else static_cast<float*>(out)[oi] = r;
   }
 }
 
@@ -830,7 +844,7 @@ static hipError_t run_decode(const float* logits, const float* bias, const void*
   else
     launch_k("decode_attn", k_decode_attn<D, BF16, GQ>, dim3(static_cast<unsigned>(grid)),
              dim3(256), st, k_cache, v_cache, topk_idx, w.rows, w.qrot, H, K, cap, nc,
-             w.part_acc, w.part_ml);
+             w.part_acc, w.part_ml, static_cast<const int32_t*>(nullptr));
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (out_dtype == 1)
     k_decode_combine<D, true><<<B, 256, 0, st>>>(gates, w.rows, w.part_acc, w.part_ml, K, nc, out,
@@ -838,6 +852,212 @@ static hipError_t run_decode(const float* logits, const float* bias, const void*
   else
     k_decode_combine<D, false><<<B, 256, 0, st>>>(gates, w.rows, w.part_acc, w.part_ml, K, nc,
                                                  out, GQ);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Shared heads in the decode step (Sec. 4.4, shared heads for local context):
+// the new token of sequence b, at global position p = cache_len[b], enters
+// every one of the Hs always-active heads.  Its key (rotated at p, or not at
+// all) and value go to row p mod cap of the head's caches, and its query
+// attends over the keys at positions max(0, p + 1 - window) .. p (window 0:
+// 0 .. p), itself included; the head outputs are summed without a gate.
+// With a window the caches are rings that keep the most recent cap >= window
+// tokens; without one row p must exist (p < cap), else the step skips the
+// sequence and reports it.
+//
+//   k_shared_decode_append  one workgroup per sequence: wave w takes heads
+//                           w, w + 4, ...: rotation (angles in double), the
+//                           cache rows, the scaled rotated query, and the
+//                           history each head reads (length, first ring row).
+//   k_decode_attn<…, RING>  the routed step's split-K attention over those
+//                           histories.
+//   k_decode_combine        the routed step's merge, gates 1, added to out.
+template <int D, bool BF16>
+__global__ __launch_bounds__(64 * kAppendWaves) void k_shared_decode_append(
+    const void* __restrict__ q, const void* __restrict__ k, const void* __restrict__ v,
+    void* __restrict__ k_cache, void* __restrict__ v_cache, int32_t* __restrict__ cache_len,
+    int Hs, long cap, int window, double log_base, int rope_mode, float qscale,
+    int32_t* __restrict__ dev_status, float* __restrict__ qrot, int32_t* __restrict__ rows,
+    int32_t* __restrict__ row0, int32_t* __restrict__ heads, float* __restrict__ gates) {
+  const int b = block_x();
+  const int lane = thread_x() % 64, wave = thread_x() / 64;
+  const int p = cache_len[b];
+  const bool over = p < 0 || (window == 0 && p >= cap);
+  const int m = over ? 0 : (window > 0 ? min(p + 1, window) : p + 1);
+  const long slot = over ? 0 : p % cap;
+  for (int s = wave; s < Hs; s += kAppendWaves) {
+    const size_t bs = static_cast<size_t>(b) * Hs + s;
+    if (lane == 0) {
+      rows[bs] = m;
+      row0[bs] = over ? 0 : static_cast<int>((static_cast<long>(p) + 1 - m) % cap);
+      heads[bs] = s;
+      gates[bs] = 1.f;
+    }
+    if (over) continue;
+    const size_t src = bs * D;
+    const size_t dst = (bs * cap + slot) * D;
+    for (int j = lane; j < D / 2; j += 64) {
+      float cs = 1.f, sn = 0.f;
+      if (rope_mode != 2) {
+        const float2 w = rope_cos_sin(static_cast<double>(p) * exp(-(2.0 * j / D) * log_base));
+        cs = w.x;
+        sn = w.y;
+      }
+      const float k1 = ld_elem<BF16>(k, src + j), k2 = ld_elem<BF16>(k, src + j + D / 2);
+      st_elem<BF16>(k_cache, dst + j, k1 * cs - k2 * sn);
+      st_elem<BF16>(k_cache, dst + j + D / 2, k2 * cs + k1 * sn);
+      st_elem<BF16>(v_cache, dst + j, ld_elem<BF16>(v, src + j));
+      st_elem<BF16>(v_cache, dst + j + D / 2, ld_elem<BF16>(v, src + j + D / 2));
+      const float q1 = ld_elem<BF16>(q, src + j), q2 = ld_elem<BF16>(q, src + j + D / 2);
+      qrot[src + j] = (q1 * cs - q2 * sn) * qscale;
+      qrot[src + j + D / 2] = (q2 * cs + q1 * sn) * qscale;
+    }
+  }
+  __syncthreads();   // every wave has read cache_len[b]
+  if (thread_x() == 0) {
+    if (over) {
+      if (dev_status) dev_status[0] = 1;
+    } else {
+      cache_len[b] = p + 1;
+    }
+  }
+}
+
+// Prefill -> decode hand-off of the shared heads: token t of the prompt
+// (rotated at t, or not at all) goes to row t mod cap of every shared head's
+// caches, for the last min(T, cap) tokens (with a window the earlier ones are
+// never read again); cache_len[b] = T.  One thread per (row, rotation pair).
+template <int D, bool BF16>
+__global__ __launch_bounds__(256) void k_shared_prefill_cache(
+    const void* __restrict__ k, const void* __restrict__ v, int T, int Hs, long cap,
+    long first, double log_base, int rope_mode, void* __restrict__ k_cache,
+    void* __restrict__ v_cache, int32_t* __restrict__ cache_len, long nrows) {
+  const long idx = static_cast<long>(block_x()) * 256 + thread_x();
+  const long row = idx / (D / 2);
+  const int j = static_cast<int>(idx - row * (D / 2));
+  if (row >= nrows) return;
+  const long keep = T - first;              // tokens first .. T - 1
+  const long bs = row / keep;               // b * Hs + s
+  const long t = first + (row - bs * keep);
+  if (j == 0 && t == T - 1 && bs % Hs == 0) cache_len[bs / Hs] = T;
+  float cs = 1.f, sn = 0.f;
+  if (rope_mode != 2) {
+    const float2 w = rope_cos_sin(static_cast<double>(t) * exp(-(2.0 * j / D) * log_base));
+    cs = w.x;
+    sn = w.y;
+  }
+  const size_t src = (static_cast<size_t>(bs) * T + t) * D;
+  const size_t dst = (static_cast<size_t>(bs) * cap + t % cap) * D;
+  const float k1 = ld_elem<BF16>(k, src + j), k2 = ld_elem<BF16>(k, src + j + D / 2);
+  st_elem<BF16>(k_cache, dst + j, k1 * cs - k2 * sn);
+  st_elem<BF16>(k_cache, dst + j + D / 2, k2 * cs + k1 * sn);
+  st_elem<BF16>(v_cache, dst + j, ld_elem<BF16>(v, src + j));
+  st_elem<BF16>(v_cache, dst + j + D / 2, ld_elem<BF16>(v, src + j + D / 2));
+}
+
+struct SharedDecWs {
+  float* qrot;
+  int32_t* rows;
+  int32_t* row0;
+  int32_t* heads;
+  float* gates;
+  float* part_acc;
+  float* part_ml;
+  size_t bytes;
+};
+
+static SharedDecWs carve_shared_dec(void* ws, int B, int Hs, int d, int cap) {
+  const size_t BS = static_cast<size_t>(B) * Hs;
+  const size_t nc = dec_nchunk(cap);
+  Carver cv(ws);
+  SharedDecWs w;
+  w.qrot = cv.take<float>(BS * d);
+  w.rows = cv.take<int32_t>(BS);
+  w.row0 = cv.take<int32_t>(BS);
+  w.heads = cv.take<int32_t>(BS);
+  w.gates = cv.take<float>(BS);
+  w.part_acc = cv.take<float>(BS * nc * d);
+  w.part_ml = cv.take<float>(BS * nc * 2);
+  w.bytes = cv.off;
+  return w;
+}
+
+size_t shared_decode_workspace_bytes(int B, int Hs, int d, int cap) {
+  return carve_shared_dec(nullptr, B, Hs, d, cap).bytes;
+}
+
+template <int D, bool BF16>
+static hipError_t run_shared_decode(const void* q, const void* k, const void* v, void* k_cache,
+                                    void* v_cache, int32_t* cache_len, int B, int Hs, int cap,
+                                    int window, float rope_base, int rope_mode, float scale,
+                                    void* out, int out_dtype, int accumulate,
+                                    int32_t* dev_status, void* ws, hipStream_t st) {
+  const SharedDecWs w = carve_shared_dec(ws, B, Hs, D, cap);
+  const int nc = dec_nchunk(cap);
+  const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
+  k_shared_decode_append<D, BF16><<<B, 64 * kAppendWaves, 0, st>>>(
+      q, k, v, k_cache, v_cache, cache_len, Hs, cap, window, log_base, rope_mode,
+      scale * 1.4426950408889634f, dev_status, w.qrot, w.rows, w.row0, w.heads, w.gates);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t grid = static_cast<size_t>(B) * Hs * nc;
+  launch_k("decode_attn", k_decode_attn<D, BF16, 1, true>, dim3(static_cast<unsigned>(grid)),
+           dim3(256), st, k_cache, v_cache, w.heads, w.rows, w.qrot, Hs, Hs, cap, nc, w.part_acc,
+           w.part_ml, w.row0);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (out_dtype == 1)
+    k_decode_combine<D, true><<<B, 256, 0, st>>>(w.gates, w.rows, w.part_acc, w.part_ml, Hs, nc,
+                                                out, 1, accumulate);
+  else
+    k_decode_combine<D, false><<<B, 256, 0, st>>>(w.gates, w.rows, w.part_acc, w.part_ml, Hs, nc,
+                                                 out, 1, accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_shared_decode(const void* q, const void* k, const void* v, int dtype,
+                                void* k_cache, void* v_cache, int32_t* cache_len, int B, int Hs,
+                                int d, int cap, int window, float rope_base, int rope_mode,
+                                float scale, void* out, int out_dtype, int accumulate,
+                                int32_t* dev_status, void* ws, hipStream_t st) {
+#define NAMOH_SDEC(DD, BF)                                                                    \
+  return run_shared_decode<DD, BF>(q, k, v, k_cache, v_cache, cache_len, B, Hs, cap, window, \
+                                   rope_base, rope_mode, scale, out, out_dtype, accumulate,  \
+                                   dev_status, ws, st)
+  if (dtype == 1) {
+    if (d == 32) NAMOH_SDEC(32, true);
+    if (d == 64) NAMOH_SDEC(64, true);
+    NAMOH_SDEC(128, true);
+  }
+  if (d == 32) NAMOH_SDEC(32, false);
+  if (d == 64) NAMOH_SDEC(64, false);
+  NAMOH_SDEC(128, false);
+#undef NAMOH_SDEC
+}
+
+hipError_t launch_shared_prefill_cache(const void* k, const void* v, int dtype, int B, int T,
+                                       int Hs, int d, int cap, float rope_base, int rope_mode,
+                                       void* k_cache, void* v_cache, int32_t* cache_len,
+                                       hipStream_t st) {
+  const long first = T > cap ? static_cast<long>(T) - cap : 0;
+  const long nrows = static_cast<long>(B) * Hs * (T - first);
+  const long threads = nrows * (d / 2);
+  const unsigned grid = static_cast<unsigned>((threads + 255) / 256);
+  const double log_base = rope_mode == 2 ? 0.0 : std::log(static_cast<double>(rope_base));
+#define NAMOH_SPC(DD, BF)                                                                       \
+  k_shared_prefill_cache<DD, BF><<<grid, 256, 0, st>>>(k, v, T, Hs, cap, first, log_base,       \
+                                                        rope_mode, k_cache, v_cache, cache_len, \
+                                                        nrows)
+  if (dtype == 1) {
+    if (d == 32) NAMOH_SPC(32, true);
+    else if (d == 64) NAMOH_SPC(64, true);
+    else NAMOH_SPC(128, true);
+  } else {
+    if (d == 32) NAMOH_SPC(32, false);
+    else if (d == 64) NAMOH_SPC(64, false);
+    else NAMOH_SPC(128, false);
+  }
+#undef NAMOH_SPC
   return hipGetLastError();
 }
 

@@ -123,6 +123,19 @@ hipError_t launch_decode_grouped(const float* logits, const void* q, const void*
                                  float rope_base, int rope_mode, int gate_mode, float scale,
                                  int32_t* topk_idx, float* gates, void* out, int out_dtype,
                                  int32_t* dev_status, void* ws, hipStream_t st);
+// Shared heads in the decode step: Hs always-active heads per sequence, caches
+// [B, Hs, cap, d] (rings of the most recent cap tokens when window > 0),
+// cache_len [B] = tokens so far; out (+)= the ungated sum of the heads.
+size_t shared_decode_workspace_bytes(int B, int Hs, int d, int cap);
+hipError_t launch_shared_decode(const void* q, const void* k, const void* v, int dtype,
+                                void* k_cache, void* v_cache, int32_t* cache_len, int B, int Hs,
+                                int d, int cap, int window, float rope_base, int rope_mode,
+                                float scale, void* out, int out_dtype, int accumulate,
+                                int32_t* dev_status, void* ws, hipStream_t st);
+hipError_t launch_shared_prefill_cache(const void* k, const void* v, int dtype, int B, int T,
+                                       int Hs, int d, int cap, float rope_base, int rope_mode,
+                                       void* k_cache, void* v_cache, int32_t* cache_len,
+                                       hipStream_t st);
 hipError_t launch_prefill_cache(const void* k, const void* v, int dtype, int B, int T, int H,
                                 int K, int d, float rope_base, int rope_mode,
                                 const int32_t* seg_offsets, const int32_t* perm_token,

@@ -348,6 +348,47 @@ def test_shared_attn_rejects(lib, kw, code):
     assert _shared(lib, **kw) == code
 
 
+def _sdec(lib, dtype=1, B=2, Hs=2, d=64, cap=256, window=128, base=1e4, rope=1, q=fake(0),
+          kc=fake(3), clen=fake(5), out=fake(6), odt=0, acc=1, st=None, wsb=1 << 30, ws=fake(8)):
+    return lib.namoh_shared_decode_step(q, fake(1), fake(2), dtype, B, Hs, d, cap, window, base,
+                                        rope, 0.0, kc, fake(4), clen, out, odt, acc, st, ws, wsb,
+                                        None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=2), 1), (dict(d=48), 2), (dict(B=0), 1), (dict(Hs=0), 1), (dict(Hs=1025), 1),
+    (dict(cap=0), 1), (dict(window=-1), 1), (dict(cap=100, window=128), 1), (dict(rope=3), 1),
+    (dict(base=-1.0), 1), (dict(q=None), 1), (dict(kc=P(A + 8)), 1), (dict(clen=None), 1),
+    (dict(out=None), 1), (dict(odt=2), 1), (dict(acc=2), 1), (dict(st=P(A + 2)), 1),
+    (dict(wsb=64), 3), (dict(ws=None), 3), (dict(B=1 << 20, Hs=1024, cap=1 << 20), 1),
+])
+def test_shared_decode_rejects(lib, kw, code):
+    assert _sdec(lib, **kw) == code
+
+
+def _spc(lib, dtype=1, B=2, T=300, Hs=2, d=64, cap=512, window=0, base=1e4, rope=1, k=fake(0),
+         clen=fake(4)):
+    return lib.namoh_shared_prefill_cache(k, fake(1), dtype, B, T, Hs, d, cap, window, base, rope,
+                                          fake(2), fake(3), clen, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(cap=200), 1), (dict(cap=100, window=128), 1), (dict(T=0), 1), (dict(d=16), 2),
+    (dict(k=None), 1), (dict(clen=None), 1), (dict(dtype=5), 1), (dict(B=1 << 20, T=1 << 12), 1),
+])
+def test_shared_prefill_cache_rejects(lib, kw, code):
+    assert _spc(lib, **kw) == code
+
+
+def test_shared_decode_sizes_and_calls_without_device(lib):
+    a = lib.namoh_shared_decode_workspace_size(4, 2, 128, 1000)
+    # rotated queries, four int/float words per head, two 512-row partials per head
+    assert a >= 4 * 2 * (128 * 4 + 16 + 2 * (128 * 4 + 8))
+    assert lib.namoh_shared_decode_workspace_size(4, 2, 96, 1000) == 0
+    assert _sdec(lib, wsb=a, B=4, d=128, cap=1000) == L.NAMOH_ERR_HIP
+    assert _spc(lib, cap=128, window=128) == L.NAMOH_ERR_HIP   # window: the last 128 tokens
+
+
 def _gdec(lib, dtype=1, B=2, H=8, K=2, g=4, d=64, cap=100, q=fake(1), wsb=1 << 30):
     return lib.namoh_decode_step_grouped(fake(0), q, fake(2), fake(3), dtype, fake(4), fake(5),
                                          fake(6), None, B, H, K, g, d, cap, 1e4, 0, 0, 0.0,
