@@ -157,6 +157,18 @@ NAMOH_DEV int serpentine(int rank, int total, int period) {
   return first + len - 1 - (rank - first);
 }
 
+// Dispatch position of rank `rank` among `total` items when `slots`
+// workgroups are resident at once.  Only the first round is placed by the
+// hardware's fixed unit order, so only ranks below `slots` are reversed in
+// alternate blocks; later workgroups start on whichever unit (of their XCD)
+// frees a slot first, in index order, so they keep the heaviest-first order
+// (a reversed block would start its heaviest item last).  slots <= 0: every
+// block alternates.
+NAMOH_DEV int resident_pos(int rank, int total, int slots, int period) {
+  if (slots <= 0 || total <= slots) return serpentine(rank, total, period);
+  return rank < slots ? serpentine(rank, slots, period) : rank;
+}
+
 NAMOH_DEV bool late_pairs_fit(int slots, int extra, int period) {
   return extra > 0 && period > 1 && period % kXcds == 0 && slots % period == 0 &&
          (slots / period) % 2 == 0 && extra <= slots / kPairMaxFrac && extra <= period;
@@ -398,7 +410,7 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
             const int r = rank + u;
             if (r >= placed) break;
             const int pos = extra > 0 ? late_pair_pos(r, split_slots, extra, period)
-                                      : serpentine(r, placed, period);
+                                      : resident_pos(r, placed, split_slots, period);
             WorkItem wi;
             wi.s = sg;
             wi.qb = qb;
