@@ -417,7 +417,8 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
             wi.seg0 = seg0;
             wi.n = n;
             wi.tile0 = seg_tile0(seg0, sg);
-            wi.qh = u | ((P > 1 ? base + u * P + p + 1 : 0) << kQhBits);
+            wi.qh = u | ((P > 1 ? base + u * P + p + 1 : 0) << kQhBits) |
+                    ((P > 1 ? P : 0) << kQhPartsShift);
             wi.kt_lo = lo;
             wi.kt_hi = hi;
             items[pos] = wi;
@@ -840,6 +841,27 @@ NAMOH_DEV void softmax_pv(f32x16 (&S)[2][NQT], f32x16 (&O)[D / 32][NQT],
         O[mt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[k2][mt], pB[qt][k2], O[mt][qt], 0, 0, 0);
 }
 
+// Part record: a 16-byte granule of a bf16 head-output row that the first
+// key-range part of a split block writes in place of the row's values, in
+// every granule of the row: element 0 is 0x7F81, a signalling NaN, which no
+// value row holds (the attention's rows are rounded from arithmetic results,
+// and arithmetic never yields a signalling NaN; the rounding of a quiet NaN
+// gives a quiet NaN or a zero); elements 1-2 hold 1 + the index of the row's
+// first partial row (the partial of part p is p * BM rows further on) and
+// element 3 the part count P.
+constexpr uint32_t kPartRecordTag = 0x7F81u;
+NAMOH_DEV uint4 part_record(int first, int P) {
+  const uint32_t code = static_cast<uint32_t>(first + 1);
+  return make_uint4(kPartRecordTag | (code << 16), (code >> 16) | (static_cast<uint32_t>(P) << 16),
+                    0u, 0u);
+}
+// The record's (first partial row, part count), or P = 0 for a value granule.
+NAMOH_DEV void read_part_record(const uint4 u, int& first, int& P) {
+  const bool rec = (u.x & 0xFFFFu) == kPartRecordTag;
+  first = static_cast<int>((u.x >> 16) | ((u.y & 0xFFFFu) << 16)) - 1;
+  P = rec ? static_cast<int>(u.y >> 16) : 0;
+}
+
 // ---------------------------------------------------------------------------
 // bf16 MFMA flash attention over one (segment, query block) work item.
 //
@@ -858,7 +880,7 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
     const int32_t* __restrict__ perm_token, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ meta, const float* __restrict__ knorm, int T, int H, int G,
     int rope_mode, float scale_log2, void* __restrict__ hout, float* __restrict__ lse_out,
-    int window, float* __restrict__ part_o, float* __restrict__ part_ml) {
+    int window, float* __restrict__ part_o, float* __restrict__ part_ml, int mark_parts) {
   constexpr int BM = 32 * NQT * NW;
   constexpr int KS = D / 16;  // reduction steps of S^T = K Q^T
   constexpr int MT = D / 32;  // 32-row tiles of O^T
@@ -884,7 +906,7 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
   // key tiles of the item: the causal range, or a key-range part of it
   // (kt_lo, kt_hi) whose unnormalised partial k_attn_merge combines
   const int kt_end = WIN ? min(ntiles, (q0 + BM + kBN - 1) / kBN) : it.kt_hi;
-  const int part = (it.qh >> kQhBits) - 1;   // partial slot, -1 for a whole item
+  const int part = ((it.qh >> kQhBits) & kQhSlotMask) - 1;   // partial slot, -1 for a whole item
   const int tid = thread_x();
   const int wave = tid / 64, lane = tid % 64;
   const int c = lane & 31, g = lane >> 5;
@@ -1090,6 +1112,15 @@ __global__ __launch_bounds__(NW * 64, MfmaShape<D>::MINB) void k_attn_mfma(
         if (g == 0)
           *reinterpret_cast<float2*>(part_ml + (static_cast<size_t>(part) * BM + ri) * 2) =
               make_float2(m_run[qt], lsum);
+        // bf16 head outputs merged by the combine: the first part writes the
+        // row as a record of where its P partials are (part_record)
+        if (HB && mark_parts && kb == 0) {
+          const uint4 rec = part_record(part * BM + ri, it.qh >> kQhPartsShift);
+          uint4* const hrow = reinterpret_cast<uint4*>(
+              static_cast<uint16_t*>(hout) + (static_cast<size_t>(seg0 + q0 + ri) * G + qh) * D);
+#pragma unroll
+          for (int j = 0; j < D / 16; ++j) hrow[2 * j + g] = rec;
+        }
       }
     }
     return;
@@ -1364,12 +1395,88 @@ __global__ __launch_bounds__(64) void k_attn_generic(
 // at a time (all loads of a batch issued before their products) and summed
 // in k order.  GC = 1 fixes G = 1 at compile time (no per-row division,
 // whose branch would split the batch of loads).
+//
+// PartRows (bf16 head outputs of the forward only): the key-range parts' rows
+// are merged here instead of by k_attn_merge.  The first part of a split
+// block writes each of the block's head-output rows as a part record
+// (part_record) instead of a value; such a row is formed from its P partials
+// as k_attn_merge forms it (same operations in the same order, rounded to
+// bf16) and added after the round's value rows.
+struct PartRows {
+  const float* part_o = nullptr;
+  const float* part_ml = nullptr;
+  int BM = 0;
+  int rows = 0;   // partial rows in part_o / part_ml (indices are checked against it)
+};
+
+// Row of a split block from its partials (the arithmetic of merge_row with
+// the part count at run time): x receives the 8 values of column group cc,
+// rounded to bf16 as the merge kernel stores them.  An entry that does not
+// name partial rows inside the buffers gives zeros.
+NAMOH_DEV void merge_part_row(const PartRows& pr, int first, int P, int D, int cc, float* x) {
+  if (P < 2 || P > kSplitMaxParts || first < 0 || first + (P - 1) * pr.BM >= pr.rows) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = 0.f;
+    return;
+  }
+  // the parts' (m, l) and the first two partial rows together (parts past P
+  // repeat the last one and are left out), then two partial rows at a time:
+  // few registers, so the combine keeps its occupancy
+  auto row_of = [&](int p) { return static_cast<size_t>(first + min(p, P - 1) * pr.BM); };
+  float2 ml[kSplitMaxParts];
+  float4 a[2][2];
+#pragma unroll
+  for (int p = 0; p < kSplitMaxParts; ++p)
+    ml[p] = *reinterpret_cast<const float2*>(pr.part_ml + row_of(p) * 2);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const float4* src = reinterpret_cast<const float4*>(pr.part_o + row_of(h) * D + 8 * cc);
+    a[h][0] = src[0];
+    a[h][1] = src[1];
+  }
+  float M = -INFINITY;
+#pragma unroll
+  for (int p = 0; p < kSplitMaxParts; ++p)
+    if (p < P && ml[p].y > 0.f) M = fmaxf(M, ml[p].x);
+  float acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  float den = 0.f;
+  auto add = [&](float2 m, const float4 (&v)[2]) {
+    const float wgt = m.y > 0.f ? __builtin_amdgcn_exp2f(m.x - M) : 0.f;
+    den = fmaf(wgt, m.y, den);
+    acc[0] = fmaf(wgt, v[0].x, acc[0]); acc[1] = fmaf(wgt, v[0].y, acc[1]);
+    acc[2] = fmaf(wgt, v[0].z, acc[2]); acc[3] = fmaf(wgt, v[0].w, acc[3]);
+    acc[4] = fmaf(wgt, v[1].x, acc[4]); acc[5] = fmaf(wgt, v[1].y, acc[5]);
+    acc[6] = fmaf(wgt, v[1].z, acc[6]); acc[7] = fmaf(wgt, v[1].w, acc[7]);
+  };
+  add(ml[0], a[0]);
+  add(ml[1], a[1]);   // (P >= 2)
+#pragma unroll 1
+  for (int p0 = 2; p0 < P; p0 += 2) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const float4* src = reinterpret_cast<const float4*>(pr.part_o + row_of(p0 + h) * D + 8 * cc);
+      a[h][0] = src[0];
+      a[h][1] = src[1];
+    }
+    const float2 m0 = *reinterpret_cast<const float2*>(pr.part_ml + row_of(p0) * 2);
+    const float2 m1 = *reinterpret_cast<const float2*>(pr.part_ml + row_of(p0 + 1) * 2);
+    add(m0, a[0]);
+    if (p0 + 1 < P) add(m1, a[1]);
+  }
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] *= inv;
+  unpack8(pack8(acc), x);
+}
+
 constexpr int kCombineThreads = 256;
-template <bool IN_BF16, bool OUT_BF16, int GC = 0>
+template <bool IN_BF16, bool OUT_BF16, int GC = 0, bool MERGE = false>
 __global__ __launch_bounds__(kCombineThreads) void k_combine(
     const void* __restrict__ hout, const float* __restrict__ gates,
     const int32_t* __restrict__ slot_pos, long BT, int K, int D, int Nr, int G,
-    void* __restrict__ out) {
+    void* __restrict__ out, PartRows pr) {
   const int C = D / 8;
   const long idx = static_cast<long>(block_x()) * kCombineThreads + thread_x();
   const long tok = idx / C;
@@ -1395,6 +1502,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
     bool ok[KC];
     float gk[KC];
     float x[KC][8];
+    bool rec[KC];
 #pragma unroll
     for (int i = 0; i < KC; ++i) {
       const int vr = k0 + i;
@@ -1409,8 +1517,10 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
     for (int i = 0; i < KC; ++i) {
       if constexpr (IN_BF16) {
         const uint4 u = reinterpret_cast<const uint4*>(hout)[static_cast<size_t>(p[i]) * C + cc];
+        rec[i] = (u.x & 0xFFFFu) == kPartRecordTag;
         unpack8(u, x[i]);
       } else {
+        rec[i] = false;
         const float4* src =
             reinterpret_cast<const float4*>(hout) + (static_cast<size_t>(p[i]) * C + cc) * 2;
         const float4 a = src[0], bb = src[1];
@@ -1420,11 +1530,34 @@ __global__ __launch_bounds__(kCombineThreads) void k_combine(
 #pragma unroll
       for (int e = 0; e < 8; ++e) x[i][e] = ok[i] ? x[i][e] : 0.f;
     }
+    // value rows in order (a part record counts as zero here) ...
 #pragma unroll
     for (int i = 0; i < KC; ++i)
       if (k0 + i < KV)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = fmaf(gk[i], x[i][e], acc[e]);
+        for (int e = 0; e < 8; ++e) acc[e] = fmaf(gk[i], rec[i] ? 0.f : x[i][e], acc[e]);
+    // ... then the rows of split blocks (rare), each formed from its
+    // partials; their slot, gate and record are read again here (a loop
+    // over a bit mask), so the common path keeps no registers for them
+    if constexpr (MERGE) {
+      unsigned mask = 0;
+#pragma unroll
+      for (int i = 0; i < KC; ++i) mask |= (ok[i] && rec[i] ? 1u : 0u) << i;
+#pragma unroll 1
+      for (; mask != 0; mask &= mask - 1) {
+        const int vr = k0 + __builtin_ctz(mask);
+        const int kk = min(GC == 1 ? vr : vr / G, K - 1);
+        const int pv = sp[kk] * G + (vr - kk * G);   // (ok: a packed row)
+        const float gv = gp[kk];
+        const uint4 u = reinterpret_cast<const uint4*>(hout)[static_cast<size_t>(pv) * C + cc];
+        int first, P;
+        read_part_record(u, first, P);
+        float xv[8];
+        merge_part_row(pr, first, P, D, cc, xv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = fmaf(gv, xv[e], acc[e]);
+      }
+    }
   }
   if constexpr (OUT_BF16) {
     reinterpret_cast<uint4*>(out)[idx] = pack8(acc);
@@ -1520,7 +1653,7 @@ static void launch_mfma(const AttnWs& w, const void* q, const void* k, const voi
                         int B, int T, int H, int G, int Nr, int rope_mode, double log_base,
                         float scale_log2, const int32_t* seg_offsets, const int32_t* perm_token,
                         void* hout, bool hout_bf16, float* lse, hipStream_t st, int window = 0,
-                        bool split = false) {
+                        bool split = false, bool merge_in_combine = false) {
   constexpr int NW = MfmaShape<D>::NW, NQT = MfmaShape<D>::NQT;
   constexpr int BM = 32 * NQT * NW;
   // key-range parts only for the whole-prefix forward (the window variant and
@@ -1534,23 +1667,26 @@ static void launch_mfma(const AttnWs& w, const void* q, const void* k, const voi
   const dim3 grid(static_cast<unsigned>(w.max_items)), block(NW * 64);
   const uint16_t* q16 = static_cast<const uint16_t*>(q);
   float* const nof = nullptr;
+  // bf16 head outputs read only by the layer's combine: the combine merges
+  // the parts' rows itself (one launch fewer)
+  const int fused = slots > 0 && hout_bf16 && merge_in_combine ? 1 : 0;
   if (window > 0 && hout_bf16)
     launch_k("attn", k_attn_mfma<D, NQT, NW, true, true>, grid, block, st, q16, w.Kp, w.Vt,
              w.freq, perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout,
-             nof, window, nof, nof);
+             nof, window, nof, nof, 0);
   else if (window > 0)
     launch_k("attn", k_attn_mfma<D, NQT, NW, false, true>, grid, block, st, q16, w.Kp, w.Vt,
              w.freq, perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout,
-             nof, window, nof, nof);
+             nof, window, nof, nof, 0);
   else if (hout_bf16)
     launch_k("attn", k_attn_mfma<D, NQT, NW, true>, grid, block, st, q16, w.Kp, w.Vt, w.freq,
              perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout, nof, 0,
-             w.part_o, w.part_ml);
+             w.part_o, w.part_ml, fused);
   else
     launch_k("attn", k_attn_mfma<D, NQT, NW, false>, grid, block, st, q16, w.Kp, w.Vt, w.freq,
              perm_token, w.items, w.meta, w.knorm, T, H, G, rope_mode, scale_log2, hout, lse, 0,
-             w.part_o, w.part_ml);
-  if (slots > 0) {
+             w.part_o, w.part_ml, 0);
+  if (slots > 0 && !fused) {
     constexpr int kMergeBlocks = 512;   // about one (item, row pass) unit each
     if (hout_bf16)
       launch_k("merge", k_attn_merge<D, true>, dim3(kMergeBlocks), dim3(kMergeThreads), st,
@@ -1597,12 +1733,13 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   if (e != hipSuccess) return e;
   if (use_mfma(d, dtype)) {
     const float sl2 = scale * 1.4426950408889634f;
+    const bool fuse = hb && out != nullptr;   // nobody but the combine reads the head outputs
     if (d == 64)
       launch_mfma<64>(w, q, k, v, B, T, H, G, Nr, rope_mode, log_base, sl2, seg_offsets,
-                      perm_token, hout, hb, nullptr, st, 0, true);
+                      perm_token, hout, hb, nullptr, st, 0, true, fuse);
     else
       launch_mfma<128>(w, q, k, v, B, T, H, G, Nr, rope_mode, log_base, sl2, seg_offsets,
-                       perm_token, hout, hb, nullptr, st, 0, true);
+                       perm_token, hout, hb, nullptr, st, 0, true, fuse);
   } else {
     if (G != 1) return hipErrorInvalidValue;   // key/value groups run on the MFMA path only
     k_attn_schedule<<<1, kPackThreads, 0, st>>>(seg_offsets, B * H, T, BM, Nr,
@@ -1624,18 +1761,25 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
   const long threads = BT * (d / 8);
   const unsigned grid = static_cast<unsigned>((threads + kCombineThreads - 1) / kCombineThreads);
   const dim3 cg(grid), cb(kCombineThreads);
+  PartRows pr;   // (hb: the forward's key-range parts, merged by the combine)
+  if (hb) {
+    pr.part_o = w.part_o;
+    pr.part_ml = w.part_ml;
+    pr.BM = BM;
+    pr.rows = 2 * w.split_slots * BM;
+  }
   if (hb && out_dtype == 1)
-    launch_k("combine", G == 1 ? k_combine<true, true, 1> : k_combine<true, true>, cg, cb, st,
-             hout, gates, slot_pos, BT, K, d, Nr, G, out);
+    launch_k("combine", G == 1 ? k_combine<true, true, 1, true> : k_combine<true, true, 0, true>,
+             cg, cb, st, hout, gates, slot_pos, BT, K, d, Nr, G, out, pr);
   else if (hb)
-    launch_k("combine", G == 1 ? k_combine<true, false, 1> : k_combine<true, false>, cg, cb, st,
-             hout, gates, slot_pos, BT, K, d, Nr, G, out);
+    launch_k("combine", G == 1 ? k_combine<true, false, 1, true> : k_combine<true, false, 0, true>,
+             cg, cb, st, hout, gates, slot_pos, BT, K, d, Nr, G, out, pr);
   else if (out_dtype == 1)
     launch_k("combine", G == 1 ? k_combine<false, true, 1> : k_combine<false, true>, cg, cb, st,
-             hout, gates, slot_pos, BT, K, d, Nr, G, out);
+             hout, gates, slot_pos, BT, K, d, Nr, G, out, pr);
   else
     launch_k("combine", G == 1 ? k_combine<false, false, 1> : k_combine<false, false>, cg, cb,
-             st, hout, gates, slot_pos, BT, K, d, Nr, G, out);
+             st, hout, gates, slot_pos, BT, K, d, Nr, G, out, pr);
   return hipGetLastError();
 }
 
@@ -1646,10 +1790,10 @@ hipError_t launch_combine_f32(const float* rows, const float* gates, const int32
   const unsigned grid = static_cast<unsigned>((threads + kCombineThreads - 1) / kCombineThreads);
   if (out_dtype == 1)
     launch_k("combine", k_combine<false, true, 1>, dim3(grid), dim3(kCombineThreads), st, rows,
-             gates, slot_pos, BT, K, D, Nr, 1, out);
+             gates, slot_pos, BT, K, D, Nr, 1, out, PartRows{});
   else
     launch_k("combine", k_combine<false, false, 1>, dim3(grid), dim3(kCombineThreads), st, rows,
-             gates, slot_pos, BT, K, D, Nr, 1, out);
+             gates, slot_pos, BT, K, D, Nr, 1, out, PartRows{});
   return hipGetLastError();
 }
 
@@ -1660,10 +1804,10 @@ hipError_t launch_combine_rows(const uint16_t* rows, const float* gates, const i
   const unsigned grid = static_cast<unsigned>((threads + kCombineThreads - 1) / kCombineThreads);
   if (out_dtype == 1)
     k_combine<true, true, 1><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D, Nr,
-                                                              1, out);
+                                                              1, out, PartRows{});
   else
     k_combine<true, false, 1><<<grid, kCombineThreads, 0, st>>>(rows, gates, slot_pos, BT, K, D,
-                                                               Nr, 1, out);
+                                                               Nr, 1, out, PartRows{});
   return hipGetLastError();
 }
 

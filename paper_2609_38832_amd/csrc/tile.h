@@ -34,11 +34,14 @@ struct __attribute__((aligned(32))) WorkItem {
   int s, qb, seg0, n;            // segment b*H + h, query block, first packed row, length
   int tile0;                     // first packed key tile of the segment
   int qh;                        // bits 0-2: query head of the item within its key/value
-                                 // group (0 without groups); bits 3-: 1 + partial slot of a
-                                 // key-range part, 0 for a whole item
+                                 // group (0 without groups); bits 3-19: 1 + partial slot of
+                                 // a key-range part, 0 for a whole item; bits 20-23: the
+                                 // part count of a split item (0 for a whole item)
   int kt_lo, kt_hi;              // key tiles [kt_lo, kt_hi) of the segment the item covers
 };
 constexpr int kQhBits = 3;
+constexpr int kQhSlotMask = (1 << 17) - 1;   // (qh >> kQhBits) & mask: 1 + partial slot
+constexpr int kQhPartsShift = 20;
 
 // Work item of this workgroup, or false if it has none.  The record is read
 // together with the item count (the grid has max_items workgroups, so the
