@@ -81,6 +81,36 @@ def test_grouped_attention_parity(name):
     check_out(from_dev(out), o_ref, "bf16", what=f"{name} out")
 
 
+@pytest.mark.parametrize("d,g,T", [(64, 2, 4500), (128, 4, 3000)])
+def test_grouped_long_segment_parts(d, g, T):
+    # Every token on the same group: one long segment whose heaviest query
+    # blocks run as key-range parts (g items per block, one per query head).
+    # The layer output from bf16 head rows inside the library (the combine
+    # merges each query head's parts) and from f32 head rows handed in (the
+    # merge kernel), both against the oracle.
+    Hkv, Kkv = 3, 1
+    say(f"grouped long segment d={d} g={g} T={T}")
+    wk, logits, q, k, v = _inputs(1, T, Hkv, Kkv, g, d, 1.0)
+    logits = logits.copy()
+    logits[:, :, :Kkv] += 100.0
+    r = L.route(torch.from_numpy(logits).to(DEV), Kkv)
+    qd, kd, vd = (to_dev(x, "bf16") for x in (q, k, v))
+    out_bf = L.attn_fwd_grouped(qd, kd, vd, r, Kkv, wk.rope_base, out_dtype=torch.float32)
+    ho = torch.empty(T * Kkv, g, d, dtype=torch.float32, device=DEV)
+    out_f32 = L.attn_fwd_grouped(qd, kd, vd, r, Kkv, wk.rope_base, out_dtype=torch.float32,
+                                 head_out=ho)
+    out_again = L.attn_fwd_grouped(qd, kd, vd, r, Kkv, wk.rope_base, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(out_bf, out_again)
+    topk = O.select_heads(logits, Kkv)
+    f64 = [W.as_float64(x, "bf16") for x in (q, k, v)]
+    h_ref = O.attention_kv_groups(f64[0], f64[1], f64[2], topk, g, wk.rope_base)
+    gates = r["gates"].cpu().numpy().astype(np.float64)
+    o_ref = O.combine_kv_groups(h_ref, topk, gates, g)
+    check_out(from_dev(out_bf), o_ref, "bf16", what="out (bf16 head rows, parts merged in the combine)")
+    check_out(from_dev(out_f32), o_ref, "bf16", what="out (f32 head rows)")
+
+
 def test_group_of_one_equals_the_routed_attention():
     # g = 1: the grouped entry point computes bit for bit what namoh_attn_fwd does
     w = W.WORKLOADS[2].with_(B=2, T=900, H=8, K=2)
