@@ -93,6 +93,11 @@ constexpr int kPackThreads = 256;
 constexpr int kSplitMinTiles = 32;
 constexpr int kSplitMaxParts = 8;
 
+// Dispatch positions: `resident_slots` workgroups of the attention kernel are
+// resident at once (256 units times the kernel's workgroups per unit); only
+// the first round of ranks is placed in alternating block order
+// (resident_pos), with or without key-range parts.
+//
 // Late pairs (split_slots > 0, S = split_slots resident slots, E = items - S
 // with 0 < E <= S / kPairMaxFrac).  The E items past the slots would start
 // only when a slot frees, late in the kernel, and end it.  The hardware puts
@@ -196,7 +201,7 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
                              int Nr, int max_items, int period, int G,
                              WorkItem* __restrict__ items, int32_t* __restrict__ meta,
                              SchedLds& L, int split_slots = 0,
-                             SplitItem* __restrict__ splits = nullptr) {
+                             SplitItem* __restrict__ splits = nullptr, int resident_slots = 0) {
   static_assert(NT % kWave == 0 && NT / kWave <= 16 && kSortBins % NT == 0, "block size");
   const int tid = thread_x();
   const int lane = tid % kWave, wave = tid / kWave;
@@ -410,7 +415,7 @@ NAMOH_DEV void attn_schedule(const int32_t* __restrict__ seg_offsets_g, int BH, 
             const int r = rank + u;
             if (r >= placed) break;
             const int pos = extra > 0 ? late_pair_pos(r, split_slots, extra, period)
-                                      : resident_pos(r, placed, split_slots, period);
+                                      : resident_pos(r, placed, resident_slots, period);
             WorkItem wi;
             wi.s = sg;
             wi.qb = qb;
@@ -506,7 +511,8 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
     const int32_t* __restrict__ perm_token, int BH, int T, int H, int Nr, int rope_mode,
     int BM, int max_items, int period, int G, WorkItem* __restrict__ items,
     int32_t* __restrict__ meta, uint16_t* __restrict__ Kp, uint16_t* __restrict__ Vt,
-    float* __restrict__ knorm, int split_slots, SplitItem* __restrict__ splits) {
+    float* __restrict__ knorm, int split_slots, SplitItem* __restrict__ splits,
+    int resident_slots) {
   __shared__ __attribute__((aligned(16))) union {
     SchedLds sched;
     PackLds<D> pack;
@@ -515,7 +521,7 @@ __global__ __launch_bounds__(kPackThreads) void k_pack_kv(
     // the rotation frequencies for the attention kernel, then the schedule
     if (thread_x() < D / 2) freq_out[thread_x()] = rope_freq_rev(thread_x(), D, log_base);
     attn_schedule<kPackThreads>(seg_offsets, BH, T, BM, Nr, max_items, period, G, items, meta,
-                                L.sched, split_slots, splits);
+                                L.sched, split_slots, splits, resident_slots);
     return;
   }
   const int gt = block_x() - 1;
@@ -1663,7 +1669,7 @@ static void launch_mfma(const AttnWs& w, const void* q, const void* k, const voi
            st, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), log_base, w.freq,
            seg_offsets, perm_token, B * H, T, H, Nr, rope_mode, BM,
            static_cast<int>(w.max_items), device_cu_count(), G, w.items, w.meta, w.Kp, w.Vt,
-           w.knorm, slots, w.splits);
+           w.knorm, slots, w.splits, w.split_slots);
   const dim3 grid(static_cast<unsigned>(w.max_items)), block(NW * 64);
   const uint16_t* q16 = static_cast<const uint16_t*>(q);
   float* const nof = nullptr;
