@@ -31,6 +31,7 @@
 
 #include "common.h"
 #include "internal.h"
+#include "sched.h"
 #include "tile.h"
 
 namespace namoh {
@@ -467,6 +468,15 @@ constexpr int kBwdMfmaThreads = 256;   // 4 waves of 32 rows: 128-row blocks
 constexpr int kBwdMfmaBlock = 128;
 constexpr float kLn2 = 0.6931471805599453f;
 
+// The key side's own work list (built by the packing kernel's workgroup 0):
+// where it goes, its capacity, and the placement (period: compute units;
+// resident: the key-side kernel's resident workgroups).
+struct KeyList {
+  WorkItem* items;
+  int32_t* meta;
+  int max_items, period, resident;
+};
+
 template <int D>
 struct BwdPackLds {
   uint16_t t[3][kBN][D + 8];   // q, dO, k tiles for the transposes
@@ -486,9 +496,21 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
     const float* __restrict__ lse, int BH, int H, int T, int K, int Nr, int rope_mode,
     float scale_log2, uint16_t* __restrict__ Qs, uint16_t* __restrict__ dO,
     uint16_t* __restrict__ Vp, uint16_t* __restrict__ Qt, uint16_t* __restrict__ dOt,
-    uint16_t* __restrict__ Kt, float2* __restrict__ LD, float* __restrict__ dgates) {
-  __shared__ __attribute__((aligned(16))) BwdPackLds<D> L;
-  const int gt = block_x();
+    uint16_t* __restrict__ Kt, float2* __restrict__ LD, float* __restrict__ dgates,
+    KeyList kl) {
+  __shared__ __attribute__((aligned(16))) union {
+    BwdPackLds<D> pack;
+    SchedLds sched;
+  } U;
+  BwdPackLds<D>& L = U.pack;
+  if (block_x() == 0) {
+    // the key side's work list: whole blocks, heaviest first, placed for the
+    // key-side kernel's resident workgroups (it runs alongside the packing)
+    attn_schedule<kBwdPackThreads>(seg_offsets, BH, T, kBwdMfmaBlock, Nr, kl.max_items, kl.period,
+                                   1, kl.items, kl.meta, U.sched, 0, nullptr, kl.resident);
+    return;
+  }
+  const int gt = block_x() - 1;   // the tile this workgroup packs
   const int tid = thread_x();
   const bool in_lds = BH <= kBwdSegLds;
   // (published by the barrier before the rows are packed)
@@ -817,10 +839,15 @@ template <int D> struct BwdMfmaShape {
 NAMOH_DEV bool bwd_item_ok(const WorkItem& it, int BH, int T, int Nr, int max_tiles) {
   if (it.s < 0 || it.s >= BH || it.n <= 0 || it.n > T || it.seg0 < 0 || it.seg0 > Nr - it.n)
     return false;
-  if ((it.qh >> kQhBits) != 0) return false;
   const int nt = (it.n + kBN - 1) / kBN;
   return it.qb >= 0 && it.qb < (it.n + kBwdMfmaBlock - 1) / kBwdMfmaBlock && it.tile0 >= 0 &&
-         it.tile0 <= max_tiles - nt;
+         it.tile0 <= max_tiles - nt && it.kt_lo >= 0 && it.kt_lo < it.kt_hi && it.kt_hi <= nt;
+}
+
+// The key side takes a split block once, whole, at the position of its part
+// 1 (parts 1 .. P - 1 are the longest and rank earliest), and no other part.
+NAMOH_DEV bool bwd_key_side_item(const WorkItem& it) {
+  return item_parts(it.qh) <= 1 || item_part(it.qh) == 1;
 }
 
 // Query side: dQ~ of one (segment, 128-query block) item.
@@ -832,7 +859,7 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
     const WorkItem* __restrict__ items, const int32_t* __restrict__ meta,
     const int32_t* __restrict__ perm_token, const double* __restrict__ freq, int T,
     int rope_mode, float scale, float* __restrict__ dq, int packed, int BH, int Nr,
-    int max_tiles) {
+    int max_tiles, float* __restrict__ part, int part_rows) {
   constexpr int NT = kBwdMfmaThreads, BM = kBwdMfmaBlock;
   constexpr int KS = D / 16, MT = D / 32;
   constexpr int KPT = kBN * D / 8 / NT;
@@ -846,10 +873,13 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
   __shared__ __attribute__((aligned(16))) uint16_t sKt[kBN * D];
   WorkItem it;
   if (!my_item(items, meta, it) || !bwd_item_ok(it, BH, T, Nr, max_tiles)) return;
+  // a key-range part of a split block adds its keys' share of dQ~ to the
+  // block's partial rows (summed by the key-side kernel's merge workgroups)
+  const int slot = item_slot(it.qh);
+  if (slot >= 0 && (part == nullptr || (slot + 1) * BM > part_rows)) return;
   const int q0 = it.qb * BM;
   const int seg0 = it.seg0, n = it.n, tile0 = it.tile0;
-  const int ntiles = (n + kBN - 1) / kBN;
-  const int kt_end = min(ntiles, (q0 + BM + kBN - 1) / kBN);
+  const int kt_lo = it.kt_lo, kt_end = it.kt_hi;
   const int tid = thread_x();
   const int wave = tid / 64, lane = tid % 64;
   const int c = lane & 31, g = lane >> 5;
@@ -892,8 +922,8 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
   const uint32_t lK = lds_address(&sK[0][0]) + wave_s * kWave * 16;
   const uint32_t lV = lds_address(&sV[0][0]) + wave_s * kWave * 16;
   const uint32_t lKt = lds_address(&sKt[0]) + wave_s * kWave * 16;
-  tile_dma<KPT, NT>(bK, nb, 0, lK, voffR);
-  tile_dma<KPT, NT>(bV, nb, 0, lV, voffR);
+  tile_dma<KPT, NT>(bK, nb, static_cast<uint32_t>(kt_lo) * TB, lK, voffR);
+  tile_dma<KPT, NT>(bV, nb, static_cast<uint32_t>(kt_lo) * TB, lV, voffR);
 
   f32x16 acc[MT];
 #pragma unroll
@@ -907,8 +937,8 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
   // wave's part of it visible.  (A partial wait, leaving the next tile's
   // loads in flight, gave wrong transposed tiles: LDS-DMA loads are not
   // known to complete in issue order.)
-  for (int kt = 0; kt < kt_end; ++kt) {
-    const int st = kt & 1;
+  for (int kt = kt_lo; kt < kt_end; ++kt) {
+    const int st = (kt - kt_lo) & 1;
     wait_vmcnt<0>();
     __syncthreads();
     tile_dma<KPT, NT>(bKt, nb, static_cast<uint32_t>(kt) * TB, lKt, voffT);
@@ -948,12 +978,85 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
     __syncthreads();
     if (act) tposed_x_c<D>(acc, sKt, dsB, c, g);
   }
-  if (valid) {   // dq~ = scale sum_j dS k~_j, back through the query's rotation
+  if (valid && slot >= 0) {   // the part's sum, unscaled and in the rotated frame
+    store_row_unrotated<D>(part + (static_cast<size_t>(slot) * BM + (r - q0)) * D, acc, 1.f,
+                           nullptr, 0.0, g);
+  } else if (valid) {   // dq~ = scale sum_j dS k~_j, back through the query's rotation
     const int t = min(static_cast<unsigned>(perm_token[seg0 + r]), static_cast<unsigned>(T - 1));
     const double* fq = rope_mode == 2 ? nullptr : freq;
     const double pos = rope_mode == 0 ? r : t;
     const size_t o = packed ? static_cast<size_t>(seg0 + r) * D : (static_cast<size_t>(it.s) * T + t) * D;
     store_row_unrotated<D>(dq + o, acc, scale, fq, pos, g);
+  }
+}
+
+// dQ rows of the split blocks: the sum of their parts' partial rows in part
+// order, scaled and back through the query's rotation as k_bwd_dq stores a
+// whole block's rows.  Run by the workgroups past the key-side kernel's work
+// items (k_bwd_dq has finished by then); units are (split block, pass of
+// NT / (D / 8) rows), each thread four rotation pairs (x, x + d/2) of a row.
+constexpr int kDqMergeGroups = 64;
+struct DqMerge {
+  const SplitItem* splits;
+  const int32_t* meta;
+  const float* part;
+  float* dq;
+  int part_rows, packed, rope_mode;
+  float scale;
+  int BH, Nr;
+};
+template <int D, int NT>
+NAMOH_DEV void dq_merge_units(const DqMerge& m, int unit0, int nunits_wg,
+                              const int32_t* __restrict__ perm_token,
+                              const double* __restrict__ freq, int T) {
+  constexpr int BM = kBwdMfmaBlock;
+  constexpr int TPR = D / 8;          // threads per row
+  constexpr int RPP = NT / TPR;       // rows per pass
+  constexpr int NPASS = (BM + RPP - 1) / RPP;
+  // (the records come from the caller's workspace: the count and every
+  // record are range-checked before use; at most part_rows / (2 BM) blocks)
+  const int nsplit = min(max(m.meta[kMetaSplit], 0), m.part_rows / (2 * BM));
+  const int tid = thread_x();
+  const int sub = tid % TPR, rw = tid / TPR;
+  const int x = 4 * sub;              // pairs x .. x + 3 with x + d/2 .. x + d/2 + 3
+  for (int u = unit0; u < nsplit * NPASS; u += nunits_wg) {
+    const int j = u / NPASS;
+    const int ri = (u - j * NPASS) * RPP + rw;
+    const SplitItem si = m.splits[j];
+    const int q0 = si.qb * BM;
+    const int r = q0 + ri;
+    if (ri >= BM || si.qb < 0 || r >= si.n || si.n > T || si.s < 0 || si.s >= m.BH ||
+        si.seg0 < 0 || si.seg0 > m.Nr - si.n || si.P < 2 || si.P > 8 || si.base < 0 ||
+        (si.base + si.P) * BM > m.part_rows)
+      continue;
+    float a[4] = {0.f, 0.f, 0.f, 0.f}, b[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int p = 0; p < si.P; ++p) {
+      const float* row = m.part + (static_cast<size_t>(si.base + p) * BM + ri) * D;
+      const float4 u1 = *reinterpret_cast<const float4*>(row + x);
+      const float4 u2 = *reinterpret_cast<const float4*>(row + x + D / 2);
+      a[0] += u1.x; a[1] += u1.y; a[2] += u1.z; a[3] += u1.w;
+      b[0] += u2.x; b[1] += u2.y; b[2] += u2.z; b[3] += u2.w;
+    }
+    const int t = min(static_cast<unsigned>(perm_token[si.seg0 + r]), static_cast<unsigned>(T - 1));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      a[i] *= m.scale;
+      b[i] *= m.scale;
+    }
+    if (m.rope_mode != 2) {
+      const double pos = m.rope_mode == 0 ? r : t;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float2 w = rope_cs_rev(pos, freq[x + i]);
+        const float d1 = a[i], d2 = b[i];
+        a[i] = d1 * w.x + d2 * w.y;
+        b[i] = d2 * w.x - d1 * w.y;
+      }
+    }
+    const size_t o = m.packed ? static_cast<size_t>(si.seg0 + r) * D
+                              : (static_cast<size_t>(si.s) * T + t) * D;
+    *reinterpret_cast<float4*>(m.dq + o + x) = make_float4(a[0], a[1], a[2], a[3]);
+    *reinterpret_cast<float4*>(m.dq + o + x + D / 2) = make_float4(b[0], b[1], b[2], b[3]);
   }
 }
 
@@ -966,7 +1069,7 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
     const uint16_t* __restrict__ Vp, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ meta, const int32_t* __restrict__ perm_token,
     const double* __restrict__ freq, int T, int rope_mode, float* __restrict__ dk,
-    float* __restrict__ dv, int packed, int BH, int Nr, int max_tiles) {
+    float* __restrict__ dv, int packed, int BH, int Nr, int max_tiles, int n_list, DqMerge dqm) {
   constexpr int NT = kBwdMfmaThreads, BM = kBwdMfmaBlock;
   constexpr int KS = D / 16, MT = D / 32;
   constexpr int KPT = kBN * D / 8 / NT;
@@ -979,7 +1082,14 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
   __shared__ __attribute__((aligned(16))) uint16_t sdOt[2][D * kBN];
   __shared__ __attribute__((aligned(16))) float2 sLD[2][kBN];
   WorkItem it;
-  if (!my_item(items, meta, it) || !bwd_item_ok(it, BH, T, Nr, max_tiles)) return;
+  if (block_x() >= n_list) {   // past the work list: the split blocks' dQ rows
+    dq_merge_units<D, NT>(dqm, block_x() - n_list, static_cast<int>(gridDim.x) - n_list,
+                          perm_token, freq, T);
+    return;
+  }
+  if (!my_item(items, meta, it) || !bwd_item_ok(it, BH, T, Nr, max_tiles) ||
+      !bwd_key_side_item(it))
+    return;
   const int seg0 = it.seg0, n = it.n, tile0 = it.tile0;
   const int nkb = (n + BM - 1) / BM;
   const int j0 = (nkb - 1 - it.qb) * BM;
@@ -1118,7 +1228,7 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
     const uint16_t* __restrict__ Vp, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ meta, const int32_t* __restrict__ perm_token,
     const double* __restrict__ freq, int T, int rope_mode, float* __restrict__ dk,
-    float* __restrict__ dv, int packed, int BH, int Nr, int max_tiles) {
+    float* __restrict__ dv, int packed, int BH, int Nr, int max_tiles, int n_list, DqMerge dqm) {
   constexpr int NT = 2 * kBwdMfmaThreads, BM = kBwdMfmaBlock;
   constexpr int KS = D / 16, MT = D / 32;
   constexpr int KPT = kBN * D / 8 / NT;
@@ -1135,7 +1245,14 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
   // group, in the tile stages once the loop is done
   static_assert(sizeof(sQ) >= 2 * MT * 16 * 64 * sizeof(float), "partial staging");
   WorkItem it;
-  if (!my_item(items, meta, it) || !bwd_item_ok(it, BH, T, Nr, max_tiles)) return;
+  if (block_x() >= n_list) {   // past the work list: the split blocks' dQ rows
+    dq_merge_units<D, NT>(dqm, block_x() - n_list, static_cast<int>(gridDim.x) - n_list,
+                          perm_token, freq, T);
+    return;
+  }
+  if (!my_item(items, meta, it) || !bwd_item_ok(it, BH, T, Nr, max_tiles) ||
+      !bwd_key_side_item(it))
+    return;
   const int seg0 = it.seg0, n = it.n, tile0 = it.tile0;
   const int nkb = (n + BM - 1) / BM;
   const int j0 = (nkb - 1 - it.qb) * BM;
@@ -1315,6 +1432,8 @@ struct BwdMfmaWs {
   float* lse;
   uint16_t *Qs, *dO, *Vp, *Qt, *dOt, *Kt;
   float2* LD;
+  WorkItem* kitems;   // the key side's work list (whole blocks)
+  int32_t* kmeta;
   size_t rows, bytes;
 };
 
@@ -1333,11 +1452,24 @@ static BwdMfmaWs carve_bwd_mfma(void* ws, int B, int T, int H, int K, int d) {
   w.dOt = cv.take<uint16_t>(w.rows * d);
   w.Kt = cv.take<uint16_t>(w.rows * d);
   w.LD = cv.take<float2>(w.rows);
+  AttnTiles tl;
+  attn_stats_tiles(nullptr, B, T, H, K, d, tl);
+  w.kitems = cv.take<WorkItem>(static_cast<size_t>(tl.max_items));
+  w.kmeta = cv.take<int32_t>(kMetaCount);
   w.bytes = cv.off;
   return w;
 }
 
 static bool bwd_uses_mfma(int dtype, int d) { return dtype == 1 && (d == 64 || d == 128); }
+
+// Compute units of the current device (the period of the hardware's
+// workgroup placement; 0 turns the alternating placement off).
+static int bwd_cu_count() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return n;
+}
 
 // Large enough for either path (the size query takes no dtype).
 size_t attn_bwd_workspace_bytes(int B, int T, int H, int K, int d) {
@@ -1376,27 +1508,37 @@ static hipError_t run_bwd_mfma(const void* q, const void* k, const void* v, int 
   }
   const double* freq = tl.freq;
   prof_mark("bwd_pack", true, st);
-  k_bwd_pack<D><<<static_cast<unsigned>(tl.max_tiles), kBwdPackThreads, 0, st>>>(
+  // the key side takes whole blocks: its own list, heaviest first, placed for
+  // its own resident workgroups (the query side runs the forward's list with
+  // its key-range parts)
+  const int cus = bwd_cu_count();
+  const KeyList kl{w.kitems, w.kmeta, tl.max_items, cus, cus * BwdMfmaShape<D>::MINB};
+  k_bwd_pack<D><<<static_cast<unsigned>(tl.max_tiles) + 1, kBwdPackThreads, 0, st>>>(
       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(v), dout, topk_idx, gates,
       seg_offsets, perm_token, freq, tl.Kp, tl.h, w.lse, BH, H, T, K, Nr, rope_mode,
-      scale * kLog2e, w.Qs, w.dO, w.Vp, w.Qt, w.dOt, w.Kt, w.LD, dgates);
+      scale * kLog2e, w.Qs, w.dO, w.Vp, w.Qt, w.dOt, w.Kt, w.LD, dgates, kl);
   prof_mark("bwd_pack", false, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_mark("bwd_dq", true, st);
   k_bwd_dq<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
       w.Qs, w.dO, w.LD, tl.Kp, w.Vp, w.Kt, tl.items, tl.meta, perm_token, freq, T, rope_mode,
-      scale, dq, packed ? 1 : 0, BH, Nr, tl.max_tiles);
+      scale, dq, packed ? 1 : 0, BH, Nr, tl.max_tiles, tl.part, tl.part_rows);
   prof_mark("bwd_dq", false, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_mark("bwd_dkdv", true, st);
+  // the key-side grid carries kDqMergeGroups more workgroups, which sum the
+  // split blocks' dQ partials (the query-side kernel has finished)
+  const DqMerge dqm{tl.splits, tl.meta, tl.part, dq, tl.part_rows, packed ? 1 : 0, rope_mode,
+                    scale, BH, Nr};
+  const unsigned kgrid = static_cast<unsigned>(tl.max_items) + kDqMergeGroups;
   if constexpr (D == 128)
-    k_bwd_dkdv8<D><<<static_cast<unsigned>(tl.max_items), 2 * kBwdMfmaThreads, 0, st>>>(
-        w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, freq, T,
-        rope_mode, dk, dv, packed ? 1 : 0, BH, Nr, tl.max_tiles);
+    k_bwd_dkdv8<D><<<kgrid, 2 * kBwdMfmaThreads, 0, st>>>(
+        w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, w.kitems, w.kmeta, perm_token, freq, T,
+        rope_mode, dk, dv, packed ? 1 : 0, BH, Nr, tl.max_tiles, tl.max_items, dqm);
   else
-    k_bwd_dkdv<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
-        w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, freq, T,
-        rope_mode, dk, dv, packed ? 1 : 0, BH, Nr, tl.max_tiles);
+    k_bwd_dkdv<D><<<kgrid, kBwdMfmaThreads, 0, st>>>(
+        w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, w.kitems, w.kmeta, perm_token, freq, T,
+        rope_mode, dk, dv, packed ? 1 : 0, BH, Nr, tl.max_tiles, tl.max_items, dqm);
   prof_mark("bwd_dkdv", false, st);
   return hipGetLastError();
 }

@@ -54,15 +54,19 @@ hipError_t launch_attn(const void* q, const void* k, const void* v, int dtype,
                        float* head_out, void* ws, hipStream_t st, int G = 1);
 
 struct WorkItem;
+struct SplitItem;
 // Where launch_attn_stats leaves the forward's pieces inside its workspace.
 struct AttnTiles {
   const uint16_t* Kp;      // rotated keys, bf16, 64-row tiles [max_tiles * 64, d]
   const uint16_t* Vt;      // values, bf16, per tile transposed [max_tiles, d, 64]
   const double* freq;      // RoPE theta_j / (2 pi), double [d / 2] (as the forward rotates)
-  const WorkItem* items;   // (segment, query block) work list, heaviest first
-  const int32_t* meta;     // item count, validity flag
+  const WorkItem* items;   // (segment, query block) work list, heaviest first, with
+                           // key-range parts for blocks heavier than a fair share
+  const int32_t* meta;     // item count, validity flag, split-item count
+  const SplitItem* splits; // the split blocks and their parts' partial slots
+  float* part;             // partial rows [part_rows, d] f32 (free once the forward merged)
   float* h;                // head outputs, f32 packed [Nr, d]
-  int max_items, max_tiles, BM;
+  int max_items, max_tiles, BM, part_rows;
 };
 hipError_t launch_attn_stats(const void* q, const void* k, const void* v, int B, int T, int H,
                              int K, int d, float rope_base, int rope_mode, float scale,

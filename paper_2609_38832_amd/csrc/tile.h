@@ -36,12 +36,23 @@ struct __attribute__((aligned(32))) WorkItem {
   int qh;                        // bits 0-2: query head of the item within its key/value
                                  // group (0 without groups); bits 3-19: 1 + partial slot of
                                  // a key-range part, 0 for a whole item; bits 20-23: the
-                                 // part count of a split item (0 for a whole item)
+                                 // part count of a split item (0 for a whole item); bits
+                                 // 24-26: the part's index
   int kt_lo, kt_hi;              // key tiles [kt_lo, kt_hi) of the segment the item covers
 };
 constexpr int kQhBits = 3;
 constexpr int kQhSlotMask = (1 << 17) - 1;   // (qh >> kQhBits) & mask: 1 + partial slot
-constexpr int kQhPartsShift = 20;
+constexpr int kQhPartsShift = 20;            // (qh >> shift) & 15: part count P (0: whole)
+constexpr int kQhPartShift = 24;             // (qh >> shift) & 7: part index p
+NAMOH_DEV int item_slot(int qh) { return ((qh >> kQhBits) & kQhSlotMask) - 1; }
+NAMOH_DEV int item_parts(int qh) { return (qh >> kQhPartsShift) & 15; }
+NAMOH_DEV int item_part(int qh) { return (qh >> kQhPartShift) & 7; }
+
+// A split item (a query block run as key-range parts): its parts' partial
+// slots are [base, base + P); qh is the query head.
+struct SplitItem {
+  int s, qb, seg0, n, qh, P, base, pad;
+};
 
 // Work item of this workgroup, or false if it has none.  The record is read
 // together with the item count (the grid has max_items workgroups, so the

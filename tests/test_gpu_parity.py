@@ -209,6 +209,11 @@ BWD = {
     # rows), and 16 heads of ~4096 rows at d = 128
     "balanced_b2": (W.WORKLOADS[2].with_(B=2), O.ROPE_HEAD_RELATIVE),
     "long_d128": (W.WORKLOADS[3].with_(T=8192, H=16), O.ROPE_HEAD_RELATIVE),
+    # long segments: query blocks far heavier than a workgroup's fair share
+    # run as key-range parts (up to eight), on the query side summed by the
+    # merge, on the key side taken once
+    "parts_d64": (W.WORKLOADS[2].with_(B=1, T=4500, H=4, K=2), O.ROPE_HEAD_RELATIVE),
+    "parts_d128_global": (W.WORKLOADS[3].with_(B=1, T=6000, H=2, K=1), O.ROPE_GLOBAL),
 }
 
 
@@ -240,7 +245,7 @@ def test_attn_bwd_parity(name):
 
 
 @pytest.mark.parametrize("name", ["bf16_d64_rel", "bf16_d128_global", "f32_d32_none",
-                                  "bf16_d32_rel", "balanced_b2", "long_d128"])
+                                  "bf16_d32_rel", "balanced_b2", "long_d128", "parts_d64"])
 def test_attn_bwd_packed(name):
     # namoh_attn_bwd_packed: the routed pairs' gradients in the routing's
     # packed order, against the oracle's gradients at those pairs, and bit
@@ -276,7 +281,8 @@ def test_attn_bwd_packed(name):
 
 
 @pytest.mark.parametrize("name", ["bf16_d64_rel", "bf16_d128_global", "bf16_d128_rel",
-                                  "bf16_d64_none", "balanced_b2", "long_d128"])
+                                  "bf16_d64_none", "balanced_b2", "long_d128", "parts_d64",
+                                  "parts_d128_global"])
 def test_attn_train_saved(name):
     # namoh_attn_fwd_train: the layer output against the oracle; then
     # namoh_attn_bwd_saved on its workspace: bit for bit the gradients of the
