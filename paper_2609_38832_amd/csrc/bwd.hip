@@ -452,15 +452,14 @@ __global__ __launch_bounds__(256) void k_bwd_scatter(
 // segment s at packed row 64 * seg_tile0 + r, rows past n zero):
 //   Qs  = bf16(q~ * scale * log2 e), exactly the forward's query operand;
 //   dO  = bf16(g * dout);  Vp = v;  (row-major, like Kp)
-//   Qt, dOt, Kt: Qs, dO, Kp transposed per tile with the 16-row permutation
-//   of tile.h (like Vt);
 //   LD  = (lse, D) per row, D = <dO, h>; (+inf, 0) past n, so padding rows
 //   get zero probabilities.
 // k_bwd_dq (one wave per 32 queries, key tiles streamed): S^T - lse and
 // dP^T - D start from the accumulators, dS^T = exp2(S^T - lse) (dP^T - D),
-// dQ^T += Kt dS^T.  k_bwd_dkdv (one wave per 32 keys, query tiles
-// streamed from the key block on): S - lse, dP - D, dV^T += dOt P,
-// dK^T += Qt dS.  Both take the forward's work list (heaviest first); the
+// dQ^T += K^T dS^T.  k_bwd_dkdv (one wave per 32 keys, query tiles
+// streamed from the key block on): S - lse, dP - D, dV^T += dO^T P,
+// dK^T += Q^T dS.  The transposed operands (K^T, dO^T, Q^T) are read from the
+// same row-major LDS tiles with gfx950's transposing LDS reads.  Both take the forward's work list (heaviest first); the
 // key side reads item (s, qb) as key block ceil(n / 128) - 1 - qb, whose work
 // (the later queries) is what the query block's was (the earlier keys).
 constexpr int kBwdPackThreads = 256;
@@ -479,7 +478,6 @@ struct KeyList {
 
 template <int D>
 struct BwdPackLds {
-  uint16_t t[3][kBN][D + 8];   // q, dO, k tiles for the transposes
   int off[kBwdSegLds + 1];
   int tok[kBN], ks[kBN];       // per tile row: token, k slot (-1: none)
   float g[kBN];                // per tile row: gate
@@ -492,12 +490,9 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
     const float* __restrict__ dout, const int32_t* __restrict__ topk_idx,
     const float* __restrict__ gates, const int32_t* __restrict__ seg_offsets,
     const int32_t* __restrict__ perm_token, const double* __restrict__ freq,
-    const uint16_t* __restrict__ Kp, const float* __restrict__ hpack,
-    const float* __restrict__ lse, int BH, int H, int T, int K, int Nr, int rope_mode,
-    float scale_log2, uint16_t* __restrict__ Qs, uint16_t* __restrict__ dO,
-    uint16_t* __restrict__ Vp, uint16_t* __restrict__ Qt, uint16_t* __restrict__ dOt,
-    uint16_t* __restrict__ Kt, float2* __restrict__ LD, float* __restrict__ dgates,
-    KeyList kl) {
+    const float* __restrict__ hpack, const float* __restrict__ lse, int BH, int H, int T, int K,
+    int Nr, int rope_mode, float scale_log2, uint16_t* __restrict__ Qs, uint16_t* __restrict__ dO,
+    uint16_t* __restrict__ Vp, float2* __restrict__ LD, float* __restrict__ dgates, KeyList kl) {
   __shared__ __attribute__((aligned(16))) union {
     BwdPackLds<D> pack;
     SchedLds sched;
@@ -604,16 +599,6 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
     *reinterpret_cast<uint4*>(dO + o + D / 2 + 8 * c) = o2;
     *reinterpret_cast<uint4*>(Vp + o + 8 * c) = v1;
     *reinterpret_cast<uint4*>(Vp + o + D / 2 + 8 * c) = v2;
-    *reinterpret_cast<uint4*>(&L.t[0][row][8 * c]) = q1;
-    *reinterpret_cast<uint4*>(&L.t[0][row][D / 2 + 8 * c]) = q2;
-    *reinterpret_cast<uint4*>(&L.t[1][row][8 * c]) = o1;
-    *reinterpret_cast<uint4*>(&L.t[1][row][D / 2 + 8 * c]) = o2;
-  }
-  constexpr int RG = D / 8;   // 16-byte granules per row
-  for (int u = tid; u < kBN * RG; u += kBwdPackThreads) {
-    const int row = u / RG, gr = u - (u / RG) * RG;
-    *reinterpret_cast<uint4*>(&L.t[2][row][8 * gr]) =
-        *reinterpret_cast<const uint4*>(Kp + (prow0 + row) * D + 8 * gr);
   }
   // per row: D = <dO, h> (dO as rounded for the products), the gate
   // gradient <dout, h>, the log-sum-exp; four lanes per row
@@ -647,24 +632,6 @@ __global__ __launch_bounds__(kBwdPackThreads) void k_bwd_pack(
       if (r < n && ks >= 0) dgates[(static_cast<size_t>(b) * T + t) * K + ks] = dg;
     }
   }
-  __syncthreads();
-  // transposed tiles: position p of each 16-row group holds row
-  // vt_key_of_pos(p), as in the forward's value tiles
-  uint16_t* const dst[3] = {Qt, dOt, Kt};
-#pragma unroll
-  for (int x = 0; x < 3; ++x)
-    for (int u = tid; u < D * (kBN / 8); u += kBwdPackThreads) {
-      const int m = u / (kBN / 8), pg = u - (u / (kBN / 8)) * (kBN / 8);
-      uint32_t w[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t a = L.t[x][vt_key_of_pos(8 * pg + 2 * e)][m];
-        const uint32_t c2 = L.t[x][vt_key_of_pos(8 * pg + 2 * e + 1)][m];
-        w[e] = a | (c2 << 16);
-      }
-      *reinterpret_cast<uint4*>(dst[x] + (static_cast<size_t>(gt) * D + m) * kBN + 8 * pg) =
-          make_uint4(w[0], w[1], w[2], w[3]);
-    }
 }
 
 // C[kk] = A[kk] B for the two 32-row halves kk of a 64-row row-major LDS
@@ -694,25 +661,67 @@ NAMOH_DEV void tile_rows_x_regs(f32x16 (&C)[2], const uint16_t* __restrict__ til
       C[kk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][kk], bop[ks], C[kk], 0, 0, 0);
 }
 
-// acc[mt] += Tt(rows 32 mt + c) X over the tile's 64 reduction slots, Tt a
-// transposed tile [D][64] in LDS, X given as four 16-slot B operands taken
-// from C-layout accumulators (slot order as tile.h describes).
+// A operand of the transposed view of a row-major 64-row LDS tile X [64][D]
+// (granules swizzled by swz<D/8>, as the tile loads store it): lane (c, g)
+// gets X[row(16 ks + 8 g + e)][32 mt + c], e = 0..7, with row(p) =
+// vt_key_of_pos(p), the slot order of the C-layout B operands below.  Two
+// transposing LDS reads (ds_read_b64_tr_b16): within each 16-lane group,
+// source lane a + 4k names 4 consecutive columns 4a .. 4a + 3 of the row of
+// slot k, and destination lane 4a + b receives column 4a + b of the four
+// rows k = 0..3, so lanes 0-15 / 16-31 cover columns 0-15 / 16-31 of the
+// 32-column block and lanes 32-63 the slots 8 .. 15.
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+// The lane's byte offsets inside a tile for slot step 0 (read hh, column
+// block mt); step ks adds 16 ks rows, a constant the read's offset field
+// carries (row & 15 and so the swizzle do not change with ks).
 template <int D>
-NAMOH_DEV void tposed_x_c(f32x16 (&acc)[D / 32], const uint16_t* __restrict__ tt,
-                          const bf16x8 (&x)[4], int c, int g) {
-  bf16x8 a[4][D / 32];
+struct TrOff {
+  uint32_t o[2][D / 32];
+};
+template <int D>
+NAMOH_DEV TrOff<D> tr_offsets(int lane) {
+  const int grp = lane >> 4, i = lane & 15;
+  TrOff<D> t;
 #pragma unroll
-  for (int k2 = 0; k2 < 4; ++k2)
+  for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
     for (int mt = 0; mt < D / 32; ++mt) {
-      const int row = 32 * mt + c;
-      a[k2][mt] = *reinterpret_cast<const bf16x8*>(&tt[row * kBN + swz<kBN / 8>(row, 2 * k2 + g) * 8]);
+      const int col = 32 * mt + 16 * (grp & 1) + 4 * (i & 3);
+      const int row = vt_key_of_pos(8 * (grp >> 1) + 4 * hh + (i >> 2));
+      t.o[hh][mt] = static_cast<uint32_t>((row * D + swz<D / 8>(row, col >> 3) * 8 + (col & 7)) * 2);
     }
+  return t;
+}
+template <int D>
+NAMOH_DEV bf16x8 tr_operand(uint32_t tile_lds, const TrOff<D>& t, int mt, int ks) {
+  union {
+    i16x4 h[2];
+    bf16x8 v;
+  } u;
 #pragma unroll
-  for (int k2 = 0; k2 < 4; ++k2)
+  for (int hh = 0; hh < 2; ++hh) {
+    const uint32_t a = tile_lds + t.o[hh][mt] + static_cast<uint32_t>(16 * ks * D * 2);
+    u.h[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(static_cast<size_t>(a)));
+  }
+  return u.v;
+}
+
+// acc[mt] += X^T(rows 32 mt + c) Y over the tile's 64 reduction slots: X the
+// row-major tile [64][D] in LDS read transposed, Y given as four 16-slot B
+// operands taken from C-layout accumulators (slot order as tile.h describes).
+template <int D>
+NAMOH_DEV void rows_tposed_x_c(f32x16 (&acc)[D / 32], uint32_t tile_lds, const TrOff<D>& t,
+                               const bf16x8 (&x)[4]) {
+#pragma unroll
+  for (int k2 = 0; k2 < 4; ++k2) {
+    bf16x8 a[D / 32];
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt) a[mt] = tr_operand<D>(tile_lds, t, mt, k2);
 #pragma unroll
     for (int mt = 0; mt < D / 32; ++mt)
-      acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[k2][mt], x[k2], acc[mt], 0, 0, 0);
+      acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], x[k2], acc[mt], 0, 0, 0);
+  }
 }
 
 // One 32-row half of tile_rows_x_regs: rows 32 kk .. 32 kk + 31 (kk wave
@@ -731,18 +740,16 @@ NAMOH_DEV void tile_half_x_regs(f32x16& C, const uint16_t* __restrict__ tile,
   }
 }
 
-// tposed_x_c over the 32 reduction slots 32 kk .. 32 kk + 31 (kk wave
-// uniform), X given as their two 16-slot B operands.
+// rows_tposed_x_c over the 32 reduction slots 32 kk .. 32 kk + 31 (kk wave
+// uniform), Y given as their two 16-slot B operands.
 template <int D>
-NAMOH_DEV void tposed_half_x_c(f32x16 (&acc)[D / 32], const uint16_t* __restrict__ tt,
-                               const bf16x8 (&x)[2], int kk, int c, int g) {
+NAMOH_DEV void rows_tposed_half_x_c(f32x16 (&acc)[D / 32], uint32_t tile_lds,
+                                    const TrOff<D>& t, const bf16x8 (&x)[2], int kk) {
 #pragma unroll
   for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
     for (int mt = 0; mt < D / 32; ++mt) {
-      const int row = 32 * mt + c;
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-          &tt[row * kBN + swz<kBN / 8>(row, 2 * (2 * kk + kh) + g) * 8]);
+      const bf16x8 a = tr_operand<D>(tile_lds, t, mt, 2 * kk + kh);
       acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, x[kh], acc[mt], 0, 0, 0);
     }
 }
@@ -855,8 +862,8 @@ template <int D>
 __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bwd_dq(
     const uint16_t* __restrict__ Qs, const uint16_t* __restrict__ dO,
     const float2* __restrict__ LD, const uint16_t* __restrict__ Kp,
-    const uint16_t* __restrict__ Vp, const uint16_t* __restrict__ Kt,
-    const WorkItem* __restrict__ items, const int32_t* __restrict__ meta,
+    const uint16_t* __restrict__ Vp, const WorkItem* __restrict__ items,
+    const int32_t* __restrict__ meta,
     const int32_t* __restrict__ perm_token, const double* __restrict__ freq, int T,
     int rope_mode, float scale, float* __restrict__ dq, int packed, int BH, int Nr,
     int max_tiles, float* __restrict__ part, int part_rows) {
@@ -865,12 +872,10 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
   constexpr int KPT = kBN * D / 8 / NT;
   constexpr size_t TS = static_cast<size_t>(kBN) * D;
   constexpr uint32_t TB = static_cast<uint32_t>(TS * 2);
-  // K and V tiles double-buffered; the transposed key tile (read last) has
-  // one stage, loaded behind the tile's first products (at d = 128 the
-  // workgroup then takes 80 KB, two per compute unit)
+  // K and V tiles double-buffered; the dQ products read the key tile
+  // transposed (64 KB per workgroup at d = 128)
   __shared__ __attribute__((aligned(16))) uint16_t sK[2][kBN * D];
   __shared__ __attribute__((aligned(16))) uint16_t sV[2][kBN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t sKt[kBN * D];
   WorkItem it;
   if (!my_item(items, meta, it) || !bwd_item_ok(it, BH, T, Nr, max_tiles)) return;
   // a key-range part of a split block adds its keys' share of dQ~ to the
@@ -914,14 +919,13 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
   const int kt_end_s = __builtin_amdgcn_readfirstlane(kt_end);
   const uint16_t* const bK = Kp + static_cast<size_t>(tile0_s) * TS;
   const uint16_t* const bV = Vp + static_cast<size_t>(tile0_s) * TS;
-  const uint16_t* const bKt = Kt + static_cast<size_t>(tile0_s) * TS;
   const uint32_t nb = static_cast<uint32_t>(kt_end_s) * TB;
   const uint32_t voffR = tile_voffset<D / 8, NT>(tid);
-  const uint32_t voffT = tile_voffset<kBN / 8, NT>(tid);
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  const uint32_t lK = lds_address(&sK[0][0]) + wave_s * kWave * 16;
+  const uint32_t lK0 = lds_address(&sK[0][0]);
+  const uint32_t lK = lK0 + wave_s * kWave * 16;
   const uint32_t lV = lds_address(&sV[0][0]) + wave_s * kWave * 16;
-  const uint32_t lKt = lds_address(&sKt[0]) + wave_s * kWave * 16;
+  const TrOff<D> tro = tr_offsets<D>(lane);
   tile_dma<KPT, NT>(bK, nb, static_cast<uint32_t>(kt_lo) * TB, lK, voffR);
   tile_dma<KPT, NT>(bV, nb, static_cast<uint32_t>(kt_lo) * TB, lV, voffR);
 
@@ -931,17 +935,12 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[mt][e] = 0.f;
   // Per tile: wait for K, V of tile kt; the barrier also ends every wave's
-  // reads of the previous transposed tile, so tile kt's goes in now,
-  // together with K, V of tile kt + 1, all behind the tile's first products;
-  // a full wait and a second barrier before the dQ products make every
-  // wave's part of it visible.  (A partial wait, leaving the next tile's
-  // loads in flight, gave wrong transposed tiles: LDS-DMA loads are not
-  // known to complete in issue order.)
+  // reads of the other stage (tile kt - 1), so K, V of tile kt + 1 go there
+  // now, behind the tile's products.
   for (int kt = kt_lo; kt < kt_end; ++kt) {
     const int st = (kt - kt_lo) & 1;
     wait_vmcnt<0>();
     __syncthreads();
-    tile_dma<KPT, NT>(bKt, nb, static_cast<uint32_t>(kt) * TB, lKt, voffT);
     const bool more = kt + 1 < kt_end;
     if (more) {
       const uint32_t tb = static_cast<uint32_t>(kt + 1) * TB;
@@ -949,9 +948,7 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
       tile_dma<KPT, NT>(bK, nb, tb, lK + ns * TB, voffR);
       tile_dma<KPT, NT>(bV, nb, tb, lV + ns * TB, voffR);
     }
-    const bool act = kt < wave_tiles;
-    bf16x8 dsB[4];
-    if (act) {
+    if (kt < wave_tiles) {
       f32x16 S[2], dP[2];
       tile_rows_x_regs<D>(S, sK[st], qB, init_l, init_l, c, g);    // S^T - lse (log2 units)
       tile_rows_x_regs<D>(dP, sV[st], doB, init_d, init_d, c, g);  // dP^T - D
@@ -966,6 +963,7 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
             for (int i = 0; i < 4; ++i)
               if (32 * kk + 8 * j + i > lim) S[kk][4 * j + i] = -INFINITY;
       }
+      bf16x8 dsB[4];
 #pragma unroll
       for (int k2 = 0; k2 < 4; ++k2)
 #pragma unroll
@@ -973,10 +971,8 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
           const int a = 8 * (k2 & 1) + e;
           dsB[k2][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(S[k2 >> 1][a]) * dP[k2 >> 1][a]);
         }
+      rows_tposed_x_c<D>(acc, lK0 + st * TB, tro, dsB);   // dQ^T += K^T dS^T
     }
-    wait_vmcnt<0>();
-    __syncthreads();
-    if (act) tposed_x_c<D>(acc, sKt, dsB, c, g);
   }
   if (valid && slot >= 0) {   // the part's sum, unscaled and in the rotated frame
     store_row_unrotated<D>(part + (static_cast<size_t>(slot) * BM + (r - q0)) * D, acc, 1.f,
@@ -1064,7 +1060,6 @@ NAMOH_DEV void dq_merge_units(const DqMerge& m, int unit0, int nunits_wg,
 template <int D>
 __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_dkdv(
     const uint16_t* __restrict__ Qs, const uint16_t* __restrict__ dO,
-    const uint16_t* __restrict__ Qt, const uint16_t* __restrict__ dOt,
     const float2* __restrict__ LD, const uint16_t* __restrict__ Kp,
     const uint16_t* __restrict__ Vp, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ meta, const int32_t* __restrict__ perm_token,
@@ -1076,10 +1071,10 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
   constexpr size_t TS = static_cast<size_t>(kBN) * D;
   constexpr uint32_t TB = static_cast<uint32_t>(TS * 2);
   constexpr uint32_t LB = kBN * sizeof(float2);
+  // query and output-gradient tiles, read row-major for S and dP and
+  // transposed for dV and dK
   __shared__ __attribute__((aligned(16))) uint16_t sQ[2][kBN * D];
   __shared__ __attribute__((aligned(16))) uint16_t sdO[2][kBN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t sQt[2][D * kBN];
-  __shared__ __attribute__((aligned(16))) uint16_t sdOt[2][D * kBN];
   __shared__ __attribute__((aligned(16))) float2 sLD[2][kBN];
   WorkItem it;
   if (block_x() >= n_list) {   // past the work list: the split blocks' dQ rows
@@ -1123,25 +1118,20 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
   const int qt0_s = __builtin_amdgcn_readfirstlane(qt0);
   const uint16_t* const bQ = Qs + static_cast<size_t>(tile0_s) * TS;
   const uint16_t* const bdO = dO + static_cast<size_t>(tile0_s) * TS;
-  const uint16_t* const bQt = Qt + static_cast<size_t>(tile0_s) * TS;
-  const uint16_t* const bdOt = dOt + static_cast<size_t>(tile0_s) * TS;
   const float2* const bLD = LD + static_cast<size_t>(tile0_s) * kBN;
   const uint32_t nb = static_cast<uint32_t>(nt_s) * TB;
   const uint32_t nbl = static_cast<uint32_t>(nt_s) * LB;
   const uint32_t voffR = tile_voffset<D / 8, NT>(tid);
-  const uint32_t voffT = tile_voffset<kBN / 8, NT>(tid);
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  const uint32_t lQ = lds_address(&sQ[0][0]) + wave_s * kWave * 16;
-  const uint32_t ldO = lds_address(&sdO[0][0]) + wave_s * kWave * 16;
-  const uint32_t lQt = lds_address(&sQt[0][0]) + wave_s * kWave * 16;
-  const uint32_t ldOt = lds_address(&sdOt[0][0]) + wave_s * kWave * 16;
+  const uint32_t lQ0 = lds_address(&sQ[0][0]), ldO0 = lds_address(&sdO[0][0]);
+  const uint32_t lQ = lQ0 + wave_s * kWave * 16;
+  const uint32_t ldO = ldO0 + wave_s * kWave * 16;
   const uint32_t lLD = lds_address(&sLD[0][0]);
+  const TrOff<D> tro = tr_offsets<D>(lane);
   auto issue = [&](int qt, int stage) {
     const uint32_t tb = static_cast<uint32_t>(qt) * TB;
     tile_dma<KPT, NT>(bQ, nb, tb, lQ + stage * TB, voffR);
     tile_dma<KPT, NT>(bdO, nb, tb, ldO + stage * TB, voffR);
-    tile_dma<KPT, NT>(bQt, nb, tb, lQt + stage * TB, voffT);
-    tile_dma<KPT, NT>(bdOt, nb, tb, ldOt + stage * TB, voffT);
     ld_tile_dma(bLD, nbl, static_cast<uint32_t>(qt) * LB, lLD + stage * LB, wave_s, lane);
   };
   issue(qt0_s, 0);
@@ -1198,8 +1188,8 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
           pB[k2][e] = static_cast<__bf16>(p);
           dsB[k2][e] = static_cast<__bf16>(p * dP[k2 >> 1][a]);
         }
-      tposed_x_c<D>(aV, sdOt[st], pB, c, g);
-      tposed_x_c<D>(aK, sQt[st], dsB, c, g);
+      rows_tposed_x_c<D>(aV, ldO0 + st * TB, tro, pB);   // dV^T += dO^T P
+      rows_tposed_x_c<D>(aK, lQ0 + st * TB, tro, dsB);   // dK^T += Q^T dS
     }
   }
   if (valid) {
@@ -1223,7 +1213,6 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
 template <int D>
 __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
     const uint16_t* __restrict__ Qs, const uint16_t* __restrict__ dO,
-    const uint16_t* __restrict__ Qt, const uint16_t* __restrict__ dOt,
     const float2* __restrict__ LD, const uint16_t* __restrict__ Kp,
     const uint16_t* __restrict__ Vp, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ meta, const int32_t* __restrict__ perm_token,
@@ -1236,13 +1225,15 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
   constexpr uint32_t TB = static_cast<uint32_t>(TS * 2);
   constexpr uint32_t LB = kBN * sizeof(float2);
   static_assert(KPT >= 1 && KPT * NT * 8 == kBN * D, "tile/thread mismatch");
+  // query and output-gradient tiles, read row-major for S and dP and
+  // transposed for dV and dK
   __shared__ __attribute__((aligned(16))) uint16_t sQ[2][kBN * D];
   __shared__ __attribute__((aligned(16))) uint16_t sdO[2][kBN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t sQt[2][D * kBN];
-  __shared__ __attribute__((aligned(16))) uint16_t sdOt[2][D * kBN];
   __shared__ __attribute__((aligned(16))) float2 sLD[2][kBN];
   // the partials of query half 1, one 2 * MT * 16 * 64-float block per key
-  // group, in the tile stages once the loop is done
+  // group: groups 0 and 1 in the tile stages once the loop is done, groups
+  // 2 and 3 here (one workgroup per compute unit: 129 KB at d = 128)
+  __shared__ __attribute__((aligned(16))) float sPart[2][2 * MT * 16 * 64];
   static_assert(sizeof(sQ) >= 2 * MT * 16 * 64 * sizeof(float), "partial staging");
   WorkItem it;
   if (block_x() >= n_list) {   // past the work list: the split blocks' dQ rows
@@ -1288,25 +1279,20 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
   const int qh_s = __builtin_amdgcn_readfirstlane(qh);
   const uint16_t* const bQ = Qs + static_cast<size_t>(tile0_s) * TS;
   const uint16_t* const bdO = dO + static_cast<size_t>(tile0_s) * TS;
-  const uint16_t* const bQt = Qt + static_cast<size_t>(tile0_s) * TS;
-  const uint16_t* const bdOt = dOt + static_cast<size_t>(tile0_s) * TS;
   const float2* const bLD = LD + static_cast<size_t>(tile0_s) * kBN;
   const uint32_t nb = static_cast<uint32_t>(nt_s) * TB;
   const uint32_t nbl = static_cast<uint32_t>(nt_s) * LB;
   const uint32_t voffR = tile_voffset<D / 8, NT>(tid);
-  const uint32_t voffT = tile_voffset<kBN / 8, NT>(tid);
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  const uint32_t lQ = lds_address(&sQ[0][0]) + wave_s * kWave * 16;
-  const uint32_t ldO = lds_address(&sdO[0][0]) + wave_s * kWave * 16;
-  const uint32_t lQt = lds_address(&sQt[0][0]) + wave_s * kWave * 16;
-  const uint32_t ldOt = lds_address(&sdOt[0][0]) + wave_s * kWave * 16;
+  const uint32_t lQ0 = lds_address(&sQ[0][0]), ldO0 = lds_address(&sdO[0][0]);
+  const uint32_t lQ = lQ0 + wave_s * kWave * 16;
+  const uint32_t ldO = ldO0 + wave_s * kWave * 16;
   const uint32_t lLD = lds_address(&sLD[0][0]);
+  const TrOff<D> tro = tr_offsets<D>(lane);
   auto issue = [&](int qt, int stage) {
     const uint32_t tb = static_cast<uint32_t>(qt) * TB;
     tile_dma<KPT, NT>(bQ, nb, tb, lQ + stage * TB, voffR);
     tile_dma<KPT, NT>(bdO, nb, tb, ldO + stage * TB, voffR);
-    tile_dma<KPT, NT>(bQt, nb, tb, lQt + stage * TB, voffT);
-    tile_dma<KPT, NT>(bdOt, nb, tb, ldOt + stage * TB, voffT);
     ld_tile_dma(bLD, nbl, static_cast<uint32_t>(qt) * LB, lLD + stage * LB, wave_s, lane);
   };
   issue(qt0_s, 0);
@@ -1359,8 +1345,8 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
           pB[kh][e] = static_cast<__bf16>(p);
           dsB[kh][e] = static_cast<__bf16>(p * dP[a]);
         }
-      tposed_half_x_c<D>(aV, sdOt[st], pB, qh_s, c, g);
-      tposed_half_x_c<D>(aK, sQt[st], dsB, qh_s, c, g);
+      rows_tposed_half_x_c<D>(aV, ldO0 + st * TB, tro, pB, qh_s);   // dV^T += dO^T P
+      rows_tposed_half_x_c<D>(aK, lQ0 + st * TB, tro, dsB, qh_s);   // dK^T += Q^T dS
     }
   }
   // the two query halves' partials of each key: half 1 stages them in LDS
@@ -1368,8 +1354,7 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
   __syncthreads();   // every wave is done with the tiles
   float* const stage = kgw == 0 ? reinterpret_cast<float*>(&sQ[0][0])
                      : kgw == 1 ? reinterpret_cast<float*>(&sdO[0][0])
-                     : kgw == 2 ? reinterpret_cast<float*>(&sQt[0][0])
-                                : reinterpret_cast<float*>(&sdOt[0][0]);
+                                : &sPart[kgw - 2][0];
   if (qh == 1) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -1430,7 +1415,7 @@ static BwdWs carve_bwd(void* ws, int B, int T, int K, int d) {
 struct BwdMfmaWs {
   void* attn;
   float* lse;
-  uint16_t *Qs, *dO, *Vp, *Qt, *dOt, *Kt;
+  uint16_t *Qs, *dO, *Vp;
   float2* LD;
   WorkItem* kitems;   // the key side's work list (whole blocks)
   int32_t* kmeta;
@@ -1448,9 +1433,6 @@ static BwdMfmaWs carve_bwd_mfma(void* ws, int B, int T, int H, int K, int d) {
   w.Qs = cv.take<uint16_t>(w.rows * d);
   w.dO = cv.take<uint16_t>(w.rows * d);
   w.Vp = cv.take<uint16_t>(w.rows * d);
-  w.Qt = cv.take<uint16_t>(w.rows * d);
-  w.dOt = cv.take<uint16_t>(w.rows * d);
-  w.Kt = cv.take<uint16_t>(w.rows * d);
   w.LD = cv.take<float2>(w.rows);
   AttnTiles tl;
   attn_stats_tiles(nullptr, B, T, H, K, d, tl);
@@ -1515,13 +1497,13 @@ static hipError_t run_bwd_mfma(const void* q, const void* k, const void* v, int 
   const KeyList kl{w.kitems, w.kmeta, tl.max_items, cus, cus * BwdMfmaShape<D>::MINB};
   k_bwd_pack<D><<<static_cast<unsigned>(tl.max_tiles) + 1, kBwdPackThreads, 0, st>>>(
       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(v), dout, topk_idx, gates,
-      seg_offsets, perm_token, freq, tl.Kp, tl.h, w.lse, BH, H, T, K, Nr, rope_mode,
-      scale * kLog2e, w.Qs, w.dO, w.Vp, w.Qt, w.dOt, w.Kt, w.LD, dgates, kl);
+      seg_offsets, perm_token, freq, tl.h, w.lse, BH, H, T, K, Nr, rope_mode, scale * kLog2e,
+      w.Qs, w.dO, w.Vp, w.LD, dgates, kl);
   prof_mark("bwd_pack", false, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_mark("bwd_dq", true, st);
   k_bwd_dq<D><<<static_cast<unsigned>(tl.max_items), kBwdMfmaThreads, 0, st>>>(
-      w.Qs, w.dO, w.LD, tl.Kp, w.Vp, w.Kt, tl.items, tl.meta, perm_token, freq, T, rope_mode,
+      w.Qs, w.dO, w.LD, tl.Kp, w.Vp, tl.items, tl.meta, perm_token, freq, T, rope_mode,
       scale, dq, packed ? 1 : 0, BH, Nr, tl.max_tiles, tl.part, tl.part_rows);
   prof_mark("bwd_dq", false, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1533,11 +1515,11 @@ static hipError_t run_bwd_mfma(const void* q, const void* k, const void* v, int 
   const unsigned kgrid = static_cast<unsigned>(tl.max_items) + kDqMergeGroups;
   if constexpr (D == 128)
     k_bwd_dkdv8<D><<<kgrid, 2 * kBwdMfmaThreads, 0, st>>>(
-        w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, w.kitems, w.kmeta, perm_token, freq, T,
+        w.Qs, w.dO, w.LD, tl.Kp, w.Vp, w.kitems, w.kmeta, perm_token, freq, T,
         rope_mode, dk, dv, packed ? 1 : 0, BH, Nr, tl.max_tiles, tl.max_items, dqm);
   else
     k_bwd_dkdv<D><<<kgrid, kBwdMfmaThreads, 0, st>>>(
-        w.Qs, w.dO, w.Qt, w.dOt, w.LD, tl.Kp, w.Vp, w.kitems, w.kmeta, perm_token, freq, T,
+        w.Qs, w.dO, w.LD, tl.Kp, w.Vp, w.kitems, w.kmeta, perm_token, freq, T,
         rope_mode, dk, dv, packed ? 1 : 0, BH, Nr, tl.max_tiles, tl.max_items, dqm);
   prof_mark("bwd_dkdv", false, st);
   return hipGetLastError();
