@@ -214,6 +214,10 @@ BWD = {
     # merge, on the key side taken once
     "parts_d64": (W.WORKLOADS[2].with_(B=1, T=4500, H=4, K=2), O.ROPE_HEAD_RELATIVE),
     "parts_d128_global": (W.WORKLOADS[3].with_(B=1, T=6000, H=2, K=1), O.ROPE_GLOBAL),
+    # more (batch, head) segments than the packing and the key-side work list
+    # stage in LDS (2112 > 2048): both search the offsets in global memory
+    "many_segments_d64": (W.WORKLOADS[2].with_(B=33, T=64, H=64, K=2), O.ROPE_HEAD_RELATIVE),
+    "many_segments_d128": (W.WORKLOADS[3].with_(B=33, T=96, H=64, K=4), O.ROPE_GLOBAL),
 }
 
 
@@ -245,7 +249,8 @@ def test_attn_bwd_parity(name):
 
 
 @pytest.mark.parametrize("name", ["bf16_d64_rel", "bf16_d128_global", "f32_d32_none",
-                                  "bf16_d32_rel", "balanced_b2", "long_d128", "parts_d64"])
+                                  "bf16_d32_rel", "balanced_b2", "long_d128", "parts_d64",
+                                  "many_segments_d128"])
 def test_attn_bwd_packed(name):
     # namoh_attn_bwd_packed: the routed pairs' gradients in the routing's
     # packed order, against the oracle's gradients at those pairs, and bit
@@ -282,7 +287,7 @@ def test_attn_bwd_packed(name):
 
 @pytest.mark.parametrize("name", ["bf16_d64_rel", "bf16_d128_global", "bf16_d128_rel",
                                   "bf16_d64_none", "balanced_b2", "long_d128", "parts_d64",
-                                  "parts_d128_global"])
+                                  "parts_d128_global", "many_segments_d64"])
 def test_attn_train_saved(name):
     # namoh_attn_fwd_train: the layer output against the oracle; then
     # namoh_attn_bwd_saved on its workspace: bit for bit the gradients of the
