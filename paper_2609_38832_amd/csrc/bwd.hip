@@ -893,6 +893,22 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
   const int wave_tiles = q0 + 32 * wave < n ? min(q0 + 32 * wave + 31, n - 1) / kBN + 1 : 0;
   const size_t prow = static_cast<size_t>(tile0) * kBN + (valid ? r : n - 1);
 
+  // the first key and value tiles go in first, so their latency overlaps
+  // the query operands' (one full wait covers both)
+  const int tile0_s = __builtin_amdgcn_readfirstlane(tile0);
+  const int kt_end_s = __builtin_amdgcn_readfirstlane(kt_end);
+  const uint16_t* const bK = Kp + static_cast<size_t>(tile0_s) * TS;
+  const uint16_t* const bV = Vp + static_cast<size_t>(tile0_s) * TS;
+  const uint32_t nb = static_cast<uint32_t>(kt_end_s) * TB;
+  const uint32_t voffR = tile_voffset<D / 8, NT>(tid);
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t lK0 = lds_address(&sK[0][0]);
+  const uint32_t lK = lK0 + wave_s * kWave * 16;
+  const uint32_t lV = lds_address(&sV[0][0]) + wave_s * kWave * 16;
+  const TrOff<D> tro = tr_offsets<D>(lane);
+  tile_dma<KPT, NT>(bK, nb, static_cast<uint32_t>(kt_lo) * TB, lK, voffR);
+  tile_dma<KPT, NT>(bV, nb, static_cast<uint32_t>(kt_lo) * TB, lV, voffR);
+
   // the query's operands and statistics (padding rows: zero operands,
   // lse = +inf, so their probabilities are 0)
   bf16x8 qB[KS], doB[KS];
@@ -914,20 +930,6 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB_Q) void k_bw
       init_d[e] = nd;
     }
   }
-
-  const int tile0_s = __builtin_amdgcn_readfirstlane(tile0);
-  const int kt_end_s = __builtin_amdgcn_readfirstlane(kt_end);
-  const uint16_t* const bK = Kp + static_cast<size_t>(tile0_s) * TS;
-  const uint16_t* const bV = Vp + static_cast<size_t>(tile0_s) * TS;
-  const uint32_t nb = static_cast<uint32_t>(kt_end_s) * TB;
-  const uint32_t voffR = tile_voffset<D / 8, NT>(tid);
-  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  const uint32_t lK0 = lds_address(&sK[0][0]);
-  const uint32_t lK = lK0 + wave_s * kWave * 16;
-  const uint32_t lV = lds_address(&sV[0][0]) + wave_s * kWave * 16;
-  const TrOff<D> tro = tr_offsets<D>(lane);
-  tile_dma<KPT, NT>(bK, nb, static_cast<uint32_t>(kt_lo) * TB, lK, voffR);
-  tile_dma<KPT, NT>(bV, nb, static_cast<uint32_t>(kt_lo) * TB, lV, voffR);
 
   f32x16 acc[MT];
 #pragma unroll
@@ -1099,20 +1101,8 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
   const bool wave_on = jw0 < n;
   const size_t prow = static_cast<size_t>(tile0) * kBN + (valid ? j : n - 1);
 
-  bf16x8 kB[KS], vB[KS];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    kB[ks] = *reinterpret_cast<const bf16x8*>(Kp + prow * D + 16 * ks + 8 * g);
-    vB[ks] = *reinterpret_cast<const bf16x8*>(Vp + prow * D + 16 * ks + 8 * g);
-  }
-  wait_vmcnt<0>();
-  if (!valid) {
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) kB[ks][e] = vB[ks][e] = static_cast<__bf16>(0.f);
-  }
-
+  // the first query tile goes in first, so its latency overlaps the key
+  // operands' (one full wait covers both)
   const int tile0_s = __builtin_amdgcn_readfirstlane(tile0);
   const int nt_s = __builtin_amdgcn_readfirstlane(ntiles);
   const int qt0_s = __builtin_amdgcn_readfirstlane(qt0);
@@ -1135,6 +1125,20 @@ __global__ __launch_bounds__(kBwdMfmaThreads, BwdMfmaShape<D>::MINB) void k_bwd_
     ld_tile_dma(bLD, nbl, static_cast<uint32_t>(qt) * LB, lLD + stage * LB, wave_s, lane);
   };
   issue(qt0_s, 0);
+
+  bf16x8 kB[KS], vB[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    kB[ks] = *reinterpret_cast<const bf16x8*>(Kp + prow * D + 16 * ks + 8 * g);
+    vB[ks] = *reinterpret_cast<const bf16x8*>(Vp + prow * D + 16 * ks + 8 * g);
+  }
+  wait_vmcnt<0>();
+  if (!valid) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kB[ks][e] = vB[ks][e] = static_cast<__bf16>(0.f);
+  }
 
   f32x16 aK[MT], aV[MT];
 #pragma unroll
@@ -1259,20 +1263,8 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
   const bool wave_on = jw0 < n;
   const size_t prow = static_cast<size_t>(tile0) * kBN + (valid ? j : n - 1);
 
-  bf16x8 kB[KS], vB[KS];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    kB[ks] = *reinterpret_cast<const bf16x8*>(Kp + prow * D + 16 * ks + 8 * g);
-    vB[ks] = *reinterpret_cast<const bf16x8*>(Vp + prow * D + 16 * ks + 8 * g);
-  }
-  wait_vmcnt<0>();
-  if (!valid) {
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) kB[ks][e] = vB[ks][e] = static_cast<__bf16>(0.f);
-  }
-
+  // the first query tile goes in first, so its latency overlaps the key
+  // operands' (one full wait covers both)
   const int tile0_s = __builtin_amdgcn_readfirstlane(tile0);
   const int nt_s = __builtin_amdgcn_readfirstlane(ntiles);
   const int qt0_s = __builtin_amdgcn_readfirstlane(qt0);
@@ -1296,6 +1288,20 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
     ld_tile_dma(bLD, nbl, static_cast<uint32_t>(qt) * LB, lLD + stage * LB, wave_s, lane);
   };
   issue(qt0_s, 0);
+
+  bf16x8 kB[KS], vB[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    kB[ks] = *reinterpret_cast<const bf16x8*>(Kp + prow * D + 16 * ks + 8 * g);
+    vB[ks] = *reinterpret_cast<const bf16x8*>(Vp + prow * D + 16 * ks + 8 * g);
+  }
+  wait_vmcnt<0>();
+  if (!valid) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kB[ks][e] = vB[ks][e] = static_cast<__bf16>(0.f);
+  }
 
   f32x16 aK[MT], aV[MT];
 #pragma unroll
