@@ -851,8 +851,10 @@ NAMOH_DEV bool bwd_item_ok(const WorkItem& it, int BH, int T, int Nr, int max_ti
          it.tile0 <= max_tiles - nt && it.kt_lo >= 0 && it.kt_lo < it.kt_hi && it.kt_hi <= nt;
 }
 
-// The key side takes a split block once, whole, at the position of its part
-// 1 (parts 1 .. P - 1 are the longest and rank earliest), and no other part.
+// The key side runs its own list of whole blocks, where every item passes
+// this test.  It guards that list: were the key side given a list with
+// key-range parts, it would take a split block once, whole, at its part 1
+// and skip the other parts, so no block's dK, dV would be written twice.
 NAMOH_DEV bool bwd_key_side_item(const WorkItem& it) {
   return item_parts(it.qh) <= 1 || item_part(it.qh) == 1;
 }
