@@ -153,11 +153,16 @@ NAMOH_DEV int vt_key_of_pos(int p) {
 // consecutive lanes read the same logical 16-byte granule of 16 consecutive
 // rows.  XOR-ing the granule index with row bits makes those 16 reads cover
 // all 64 banks: rows of 16 granules (256 B) use row & 15; rows of 8 granules
-// (128 B, two rows per bank sweep) use (row >> 1) & 7.
+// (128 B, two rows per bank sweep) use x = (row >> 1) & 7 with bit 2 flipped
+// for odd x (still one value per row pair).  The flip serves the transposing
+// reads of the backward, where a read covers four granules of eight
+// consecutive rows: the row pairs then alternate between the two halves of
+// the granule range and every bank is hit twice (the minimum for 512 bytes),
+// not four times.
 template <int GPR>
 NAMOH_DEV int swz(int row, int gr) {
   static_assert(GPR == 8 || GPR == 16, "granules per row");
-  return GPR == 16 ? (gr ^ (row & 15)) : (gr ^ ((row >> 1) & 7));
+  return GPR == 16 ? (gr ^ (row & 15)) : (gr ^ (((row >> 1) & 7) ^ ((row & 2) << 1)));
 }
 
 // Tile staging, direct HBM -> LDS (buffer_load_dwordx4 ... lds): KPT 16-byte
