@@ -661,15 +661,6 @@ NAMOH_DEV void tile_rows_x_regs(f32x16 (&C)[2], const uint16_t* __restrict__ til
       C[kk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][kk], bop[ks], C[kk], 0, 0, 0);
 }
 
-// A operand of the transposed view of a row-major 64-row LDS tile X [64][D]
-// (granules swizzled by swz<D/8>, as the tile loads store it): lane (c, g)
-// gets X[row(16 ks + 8 g + e)][32 mt + c], e = 0..7, with row(p) =
-// vt_key_of_pos(p), the slot order of the C-layout B operands below.  Two
-// transposing LDS reads (ds_read_b64_tr_b16): within each 16-lane group,
-// source lane a + 4k names 4 consecutive columns 4a .. 4a + 3 of the row of
-// slot k, and destination lane 4a + b receives column 4a + b of the four
-// rows k = 0..3, so lanes 0-15 / 16-31 cover columns 0-15 / 16-31 of the
-// 32-column block and lanes 32-63 the slots 8 .. 15.
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 // The lane's byte offsets inside a tile for slot step 0 (read hh, column
@@ -693,6 +684,15 @@ NAMOH_DEV TrOff<D> tr_offsets(int lane) {
     }
   return t;
 }
+// A operand of the transposed view of a row-major 64-row LDS tile X [64][D]
+// (granules swizzled by swz<D/8>, as the tile loads store it): lane (c, g)
+// gets X[row(16 ks + 8 g + e)][32 mt + c], e = 0..7, with row(p) =
+// vt_key_of_pos(p), the slot order of the C-layout B operands below.  Two
+// transposing LDS reads (ds_read_b64_tr_b16): within each 16-lane group,
+// source lane a + 4k names 4 consecutive columns 4a .. 4a + 3 of the row of
+// slot k, and destination lane 4a + b receives column 4a + b of the four
+// rows k = 0..3, so lanes 0-15 / 16-31 cover columns 0-15 / 16-31 of the
+// 32-column block and lanes 32-63 the slots 8 .. 15.
 template <int D>
 NAMOH_DEV bf16x8 tr_operand(uint32_t tile_lds, const TrOff<D>& t, int mt, int ks) {
   union {
