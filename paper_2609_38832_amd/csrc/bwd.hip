@@ -1357,39 +1357,38 @@ __global__ __launch_bounds__(2 * kBwdMfmaThreads, 1) void k_bwd_dkdv8(
       rows_tposed_half_x_c<D>(aK, lQ0 + st * TB, tro, dsB, qh_s);   // dK^T += Q^T dS
     }
   }
-  // the two query halves' partials of each key: half 1 stages them in LDS
-  // (the tile stages of its key group), half 0 adds them and stores
+  // the two query halves' partials of each key: half 1 hands its dK partial
+  // to half 0 and half 0 its dV partial to half 1 through LDS (the tile
+  // stages of the key group, idle by now, or sPart); half 0 then stores dK,
+  // half 1 dV, so all eight waves share the epilogue
   __syncthreads();   // every wave is done with the tiles
   float* const stage = kgw == 0 ? reinterpret_cast<float*>(&sQ[0][0])
                      : kgw == 1 ? reinterpret_cast<float*>(&sdO[0][0])
                                 : &sPart[kgw - 2][0];
-  if (qh == 1) {
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        stage[((0 * MT + mt) * 16 + e) * 64 + lane] = aK[mt][e];
-        stage[((1 * MT + mt) * 16 + e) * 64 + lane] = aV[mt][e];
-      }
-  }
-  __syncthreads();
-  if (qh == 1) return;
+  float* const give = stage + (qh == 1 ? 0 : MT * 16 * 64);   // dK from half 1, dV from half 0
+  float* const take = stage + (qh == 1 ? MT * 16 * 64 : 0);
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      aK[mt][e] += stage[((0 * MT + mt) * 16 + e) * 64 + lane];
-      aV[mt][e] += stage[((1 * MT + mt) * 16 + e) * 64 + lane];
-    }
+    for (int e = 0; e < 16; ++e) give[(mt * 16 + e) * 64 + lane] = qh == 1 ? aK[mt][e] : aV[mt][e];
+  __syncthreads();
+  f32x16 (&mine)[MT] = qh == 1 ? aV : aK;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) mine[mt][e] += take[(mt * 16 + e) * 64 + lane];
   if (valid) {
-    // the queries were scaled by scale * log2 e: dk~ = ln 2 * sum dS Qs,
-    // back through the key's rotation; dv as it is
     const int t = min(static_cast<unsigned>(perm_token[seg0 + j]), static_cast<unsigned>(T - 1));
     const size_t o = packed ? static_cast<size_t>(seg0 + j) * D : (static_cast<size_t>(it.s) * T + t) * D;
-    const double* fq = rope_mode == 2 ? nullptr : freq;
-    const double pos = rope_mode == 0 ? j : t;
-    store_row_unrotated<D>(dk + o, aK, kLn2, fq, pos, g);
-    store_row_unrotated<D>(dv + o, aV, 1.f, nullptr, 0.0, g);
+    if (qh == 0) {
+      // the queries were scaled by scale * log2 e: dk~ = ln 2 * sum dS Qs,
+      // back through the key's rotation
+      const double* fq = rope_mode == 2 ? nullptr : freq;
+      const double pos = rope_mode == 0 ? j : t;
+      store_row_unrotated<D>(dk + o, aK, kLn2, fq, pos, g);
+    } else {
+      store_row_unrotated<D>(dv + o, aV, 1.f, nullptr, 0.0, g);   // dv as it is
+    }
   }
 }
 
